@@ -1,0 +1,433 @@
+"""CPU oracle of one SMoES-routed MoE layer (test infrastructure only).
+
+This is the checker, not the product: only the tests, the smoke entry and the
+CPU-baseline leg of the benchmark may import it. It shares no code with the
+HIP path. Everything is plain NumPy in float64 on the exact stored input values
+(bf16 inputs are widened exactly), written step by step in the order and
+notation of the paper, "Soft Modality-Guided Expert Specialization in
+MoE-VLMs" (SMoES):
+
+  * Sec. 3.1   router gating g = softmax(W_gate x) and top-k selection
+  * Sec. 3.2.2 EMA variant of Welford's update (Eq. 5-7), per-modality
+               log-likelihood (Eq. 8), temperature softmax score (Eq. 9)
+  * Sec. 3.3   expert binning (bins of N_B = N_e / N_bins experts)
+  * Sec. 3.4   per-sample bin-by-modality gating mass (Eq. 12), joint (Eq. 13),
+               mutual information (Eq. 14), loss (Eq. 15, one layer)
+  * derived    gradient of the MI loss with respect to the router logits
+               (the paper does not print it; the closed form below follows from
+               Eq. 12-15 by the chain rule and is pinned by finite differences)
+  * MoE layer  expert-contiguous permutation, SwiGLU experts, shared experts,
+               weighted combine (the backbones of the supplementary backbone
+               table: DeepSeekMoE with 2 shared experts, gated-SiLU FFNs)
+
+Readings where the paper is silent (each also listed in the design notes):
+  R1  logarithms are natural (MI in nats);
+  R2  g inside the MI is the full softmax over all experts, not the top-k mask;
+  R3  combine weights are the raw top-k gate values unless renorm is asked for;
+  R4  top-k is decided on float32 logits, ordered by descending logit, ties to
+      the lower expert index;
+  R5  a per-expert logit bias, when given, is added before softmax and top-k;
+  R6  shared experts have weight 1 and are ungated; S shared experts of inner
+      size I are one SwiGLU of inner size S*I;
+  R7  SwiGLU is down(silu(gate x) * up x), silu(a) = a / (1 + exp(-a));
+  R8  samples are contiguous token ranges given by offsets;
+  R9  the modality score is treated as a constant in the MI gradient;
+  R10 statistics are updated with the current batch before scoring it;
+  R11 the 2*pi constant of the log-likelihood is dropped (it cancels in Eq. 9),
+      the variance is floored at var_floor, and a modality with N = 0 has
+      mu = 0, sigma^2 = 1;
+  R12 an MI term with P(m, B_k) = 0 contributes 0, and a modality with zero
+      total score mass in a sample has S-bar = 0 for every bin;
+  R13 column 0 of the modality score is vision, column 1 is text.
+
+Parity pins live in tests/test_oracle_pins.py; no part of this file is
+"parity unpinned" except the conventions R3-R5, R8, R11, R12 above, which fix
+choices the paper does not make (both sides implement the same stated choice).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+VISION, TEXT = 0, 1
+
+
+def _f64(a) -> np.ndarray:
+    """Exact float64 view of a stored array (uint16 = bf16 bit patterns)."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.1: router
+# ----------------------------------------------------------------------------
+
+def router_logits(x, w_gate, logit_bias=None) -> np.ndarray:
+    """z_j = W_gate x_j (+ b): the pre-softmax router scores, float64."""
+    z = _f64(x) @ _f64(w_gate).T
+    if logit_bias is not None:
+        z = z + _f64(logit_bias)[None, :]
+    return z
+
+
+def softmax_rows(z) -> np.ndarray:
+    """g_je = exp(z_je) / sum_e' exp(z_je') over all N_e experts (Sec. 3.1)."""
+    z = np.asarray(z, dtype=np.float64)
+    e = np.exp(z - z.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def topk_select(z, k: int) -> np.ndarray:
+    """Indices of the k highest scores per token (Sec. 3.1), decided on the
+    float32 value of the logits (R4); descending order, ties to lower index."""
+    z32 = np.asarray(z, dtype=np.float64).astype(np.float32)
+    order = np.argsort(-z32, axis=1, kind="stable")
+    return order[:, :k].astype(np.int32)
+
+
+def topk_gap(z, k: int) -> np.ndarray:
+    """z_(k) - z_(k+1) per token (inf when k = E): tokens with a small gap may
+    legitimately pick a different k-th expert under rounding."""
+    z = np.asarray(z, dtype=np.float64)
+    if k >= z.shape[1]:
+        return np.full(z.shape[0], np.inf)
+    s = -np.sort(-z, axis=1)
+    return s[:, k - 1] - s[:, k]
+
+
+def route(x, w_gate, k: int, logit_bias=None, renorm_topk: bool = False):
+    """Router step: logits, full softmax, top-k indices and combine weights."""
+    z = router_logits(x, w_gate, logit_bias)
+    g = softmax_rows(z)
+    idx = topk_select(z, k)
+    w = np.take_along_axis(g, idx.astype(np.int64), axis=1)
+    if renorm_topk:
+        w = w / w.sum(axis=1, keepdims=True)
+    return z, g, idx, w
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.2.2: Gaussian-statistics modality score
+# ----------------------------------------------------------------------------
+
+@dataclass
+class GaussState:
+    """Per-layer EMA-Welford state for the two modalities: N_m, S_mu,m, S_sigma2,m."""
+
+    n: np.ndarray  # [2]
+    s_mu: np.ndarray  # [2, D]
+    s_sig: np.ndarray  # [2, D]
+
+    @staticmethod
+    def zeros(d: int) -> "GaussState":
+        return GaussState(np.zeros(2), np.zeros((2, d)), np.zeros((2, d)))
+
+    @staticmethod
+    def of(n, s_mu, s_sig) -> "GaussState":
+        return GaussState(_f64(n).copy(), _f64(s_mu).copy(), _f64(s_sig).copy())
+
+
+def gauss_update(state: GaussState, x, modality_id, beta: float) -> GaussState:
+    """One EMA-Welford step (Eq. 5-7) for each modality m:
+
+        N_t      = beta N_{t-1} + |T_m|
+        S_mu,t   = beta S_mu,t-1 + |T_m| mu_T
+        S_sig,t  = beta S_sig,t-1 + sum_{x in T_m} (x - mu_T)^2
+                   + (mu_T - S_mu,t-1 / N_{t-1})^2 beta N_{t-1} |T_m| / (beta N_{t-1} + |T_m|)
+
+    with T_m the modality-m tokens of the batch and mu_T their mean. The last
+    term is taken as 0 when N_{t-1} = 0 or |T_m| = 0 (its factor vanishes)."""
+    X = _f64(x)
+    mid = np.asarray(modality_id)
+    n_new = state.n.copy()
+    s_mu_new = state.s_mu.copy()
+    s_sig_new = state.s_sig.copy()
+    for m in (VISION, TEXT):
+        sel = X[mid == m]
+        cnt = sel.shape[0]
+        n_prev = state.n[m]
+        if cnt > 0:
+            mu_T = sel.mean(axis=0)
+            sq = ((sel - mu_T) ** 2).sum(axis=0)
+        else:
+            mu_T = np.zeros(X.shape[1])
+            sq = np.zeros(X.shape[1])
+        if n_prev > 0 and cnt > 0:
+            prev_mean = state.s_mu[m] / n_prev
+            cross = (mu_T - prev_mean) ** 2 * (beta * n_prev * cnt) / (beta * n_prev + cnt)
+        else:
+            cross = np.zeros(X.shape[1])
+        n_new[m] = beta * n_prev + cnt
+        s_mu_new[m] = beta * state.s_mu[m] + cnt * mu_T
+        s_sig_new[m] = beta * state.s_sig[m] + sq + cross
+    return GaussState(n_new, s_mu_new, s_sig_new)
+
+
+def gauss_params(state: GaussState, var_floor: float) -> Tuple[np.ndarray, np.ndarray]:
+    """mu_m = S_mu / N and sigma^2_m = S_sigma2 / N (Sec. 3.2.2), floored (R11)."""
+    d = state.s_mu.shape[1]
+    mu = np.zeros((2, d))
+    var = np.ones((2, d))
+    for m in (VISION, TEXT):
+        if state.n[m] > 0:
+            mu[m] = state.s_mu[m] / state.n[m]
+            var[m] = np.maximum(state.s_sig[m] / state.n[m], var_floor)
+    return mu, var
+
+
+def log_likelihood(x, mu, var) -> np.ndarray:
+    """LL_jm = -1/2 sum_d (log sigma^2_md + (x_jd - mu_md)^2 / sigma^2_md)  (Eq. 8)."""
+    X = _f64(x)
+    ll = np.empty((X.shape[0], 2))
+    for m in (VISION, TEXT):
+        ll[:, m] = -0.5 * (np.log(var[m]).sum() + (((X - mu[m]) ** 2) / var[m]).sum(axis=1))
+    return ll
+
+
+def modality_score(x, mu, var, tau: float) -> np.ndarray:
+    """M_jm = exp(LL_jm / tau) / sum_m' exp(LL_jm' / tau)  (Eq. 9); [T, 2]."""
+    ll = log_likelihood(x, mu, var) / tau
+    ll = ll - ll.max(axis=1, keepdims=True)
+    e = np.exp(ll)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def default_tau(d: int, tau: float) -> float:
+    """tau <= 0 selects the paper's default tau = 0.5 D (Sec. 3.5)."""
+    return 0.5 * d if tau <= 0 else tau
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.3 - 3.4: expert bins and inter-bin mutual information
+# ----------------------------------------------------------------------------
+
+def bin_members(expert_to_bin, n_bins: int):
+    e2b = np.asarray(expert_to_bin)
+    return [np.nonzero(e2b == k)[0] for k in range(n_bins)]
+
+
+def mi_sample_terms(g, M, expert_to_bin, n_bins: int) -> Dict[str, np.ndarray]:
+    """The quantities of Eq. 12-14 for ONE sample (rows of g and M).
+
+    S_bar[m, k] = sum_{e in B_k} sum_j M_jm g_je / (N_B sum_j M_jm)   (Eq. 12)
+    P[m, k]     = S_bar[m, k] / sum_{m', k'} S_bar[m', k']             (Eq. 13)
+    I           = sum_{m, k} P log(P / (P(m) P(B_k)))                   (Eq. 14)
+    """
+    g = np.asarray(g, dtype=np.float64)
+    M = np.asarray(M, dtype=np.float64)
+    E = g.shape[1]
+    n_b = E // n_bins
+    members = bin_members(expert_to_bin, n_bins)
+    S = np.zeros((2, n_bins))
+    W = M.sum(axis=0)
+    for m in (VISION, TEXT):
+        if W[m] <= 0:
+            continue
+        for k in range(n_bins):
+            mass = (M[:, m][:, None] * g[:, members[k]]).sum()
+            S[m, k] = mass / (n_b * W[m])
+    Z = S.sum()
+    P = S / Z if Z > 0 else np.zeros_like(S)
+    Pm = P.sum(axis=1)
+    Pk = P.sum(axis=0)
+    I = 0.0
+    for m in (VISION, TEXT):
+        for k in range(n_bins):
+            if P[m, k] > 0:
+                I += P[m, k] * np.log(P[m, k] / (Pm[m] * Pk[k]))
+    return dict(S_bar=S, W=W, Z=Z, P=P, Pm=Pm, Pk=Pk, I=I)
+
+
+def mi_per_sample(g, M, sample_offsets, expert_to_bin, n_bins: int) -> np.ndarray:
+    """I_i(M; B) for every sample i (Eq. 14)."""
+    off = np.asarray(sample_offsets)
+    out = np.zeros(len(off) - 1)
+    for i in range(len(off) - 1):
+        a, b = int(off[i]), int(off[i + 1])
+        if b > a:
+            out[i] = mi_sample_terms(g[a:b], M[a:b], expert_to_bin, n_bins)["I"]
+    return out
+
+
+def mi_loss(g, M, sample_offsets, expert_to_bin, n_bins: int) -> float:
+    """L_MI = -(1 / N_batch) sum_i I_i for one layer (Eq. 15)."""
+    I = mi_per_sample(g, M, sample_offsets, expert_to_bin, n_bins)
+    return -float(I.sum()) / len(I)
+
+
+def mi_loss_grad_logits(g, M, sample_offsets, expert_to_bin, n_bins: int,
+                        grad_scale: float = 1.0) -> np.ndarray:
+    """grad_scale * dL_MI / dz for the router logits z (M held constant, R9).
+
+    Chain rule through Eq. 12-15 and the softmax of Sec. 3.1:
+      dI_i / dS_bar[m, k] = (log r_mk - I_i) / Z,  r_mk = P_mk / (P_m P_k)
+      dI_i / dG_jk        = h_jk = sum_m M_jm (log r_mk - I_i) / (N_B W_m Z)
+      dI_i / dz_je        = g_je (h_j,bin(e) - sum_k G_jk h_jk)
+    where G_jk = sum_{e in B_k} g_je and W_m = sum_j M_jm; terms with W_m = 0 or
+    P_mk = 0 are dropped (R12). L_MI = -(1/N_batch) sum_i I_i."""
+    g = np.asarray(g, dtype=np.float64)
+    M = np.asarray(M, dtype=np.float64)
+    off = np.asarray(sample_offsets)
+    n_batch = len(off) - 1
+    E = g.shape[1]
+    n_b = E // n_bins
+    e2b = np.asarray(expert_to_bin)
+    members = bin_members(e2b, n_bins)
+    out = np.zeros_like(g)
+    for i in range(n_batch):
+        a, b = int(off[i]), int(off[i + 1])
+        if b <= a:
+            continue
+        t = mi_sample_terms(g[a:b], M[a:b], e2b, n_bins)
+        coef = np.zeros((2, n_bins))
+        for m in (VISION, TEXT):
+            if t["W"][m] <= 0:
+                continue
+            for k in range(n_bins):
+                if t["P"][m, k] > 0:
+                    log_r = np.log(t["P"][m, k] / (t["Pm"][m] * t["Pk"][k]))
+                    coef[m, k] = (log_r - t["I"]) / (n_b * t["W"][m] * t["Z"])
+        gi = g[a:b]
+        G = np.stack([gi[:, members[k]].sum(axis=1) for k in range(n_bins)], axis=1)
+        h = M[a:b] @ coef  # [rows, n_bins]
+        hG = (h * G).sum(axis=1)
+        out[a:b] = gi * (h[:, e2b] - hG[:, None])
+    return (-grad_scale / n_batch) * out
+
+
+# ----------------------------------------------------------------------------
+# MoE experts: permutation, SwiGLU experts, shared experts, combine
+# ----------------------------------------------------------------------------
+
+def permutation(topk_idx, E: int):
+    """Expert-contiguous order of the (token, slot) pairs: a stable counting
+    sort by expert, tokens ascending inside each expert.
+
+    Returns counts[E], offsets[E+1] (exclusive scan), perm_token[R] (token of
+    each permuted row) and inv[T, k] (permuted row of each (token, slot))."""
+    idx = np.asarray(topk_idx, dtype=np.int64)
+    T, k = idx.shape
+    counts = np.zeros(E, dtype=np.int64)
+    for e in idx.reshape(-1):
+        counts[e] += 1
+    offsets = np.zeros(E + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    cursor = offsets[:-1].copy()
+    perm_token = np.zeros(T * k, dtype=np.int64)
+    inv = np.zeros((T, k), dtype=np.int64)
+    # tokens in ascending order; each token visits its k experts
+    for j in range(T):
+        for s in range(k):
+            e = idx[j, s]
+            r = cursor[e]
+            cursor[e] += 1
+            perm_token[r] = j
+            inv[j, s] = r
+    return counts, offsets, perm_token, inv
+
+
+def silu(a):
+    return a / (1.0 + np.exp(-a))
+
+
+def swiglu(x, w13, w2) -> np.ndarray:
+    """down(silu(gate x) * up x) with w13 = [gate rows; up rows] ([2I, d]) and
+    w2 = [d, I]  (R7)."""
+    X = _f64(x)
+    W13 = _f64(w13)
+    inter = W13.shape[0] // 2
+    a = X @ W13[:inter].T
+    u = X @ W13[inter:].T
+    return (silu(a) * u) @ _f64(w2).T
+
+
+def experts_grouped(x, topk_idx, topk_w, w13, w2, ws13=None, ws2=None, E=None):
+    """Routed experts over the expert-contiguous permutation, then the weighted
+    combine out_j = sum_s w_js Y[inv(j, s)] + shared(x_j)."""
+    X = _f64(x)
+    idx = np.asarray(topk_idx)
+    T, k = idx.shape
+    E = E if E is not None else w13.shape[0]
+    counts, offsets, perm_token, inv = permutation(idx, E)
+    Y = np.zeros((T * k, X.shape[1]))
+    for e in range(E):
+        a, b = offsets[e], offsets[e + 1]
+        if b > a:
+            Y[a:b] = swiglu(X[perm_token[a:b]], w13[e], w2[e])
+    w = np.asarray(topk_w, dtype=np.float64)
+    out = np.zeros_like(X)
+    for s in range(k):
+        out += w[:, s:s + 1] * Y[inv[:, s]]
+    shared = swiglu(X, ws13, ws2) if ws13 is not None else np.zeros_like(X)
+    return out + shared, out, shared
+
+
+def experts_naive(x, topk_idx, topk_w, w13, w2, ws13=None, ws2=None):
+    """The same layer output by a plain loop: every token through each of its
+    k experts, weighted, plus the shared experts."""
+    X = _f64(x)
+    idx = np.asarray(topk_idx)
+    w = np.asarray(topk_w, dtype=np.float64)
+    out = np.zeros_like(X)
+    for j in range(X.shape[0]):
+        for s in range(idx.shape[1]):
+            out[j] += w[j, s] * swiglu(X[j:j + 1], w13[idx[j, s]], w2[idx[j, s]])[0]
+        if ws13 is not None:
+            out[j] += swiglu(X[j:j + 1], ws13, ws2)[0]
+    return out
+
+
+# ----------------------------------------------------------------------------
+# The whole layer
+# ----------------------------------------------------------------------------
+
+def layer_forward(x, modality_id, sample_offsets, w_gate, logit_bias, expert_to_bin,
+                  n_bins, k, w13, w2, ws13, ws2, state: GaussState, *, update_stats: bool,
+                  beta: float = 0.99, tau: float = 0.0, var_floor: float = 1e-6,
+                  grad_scale: float = 1.0, renorm_topk: bool = False,
+                  rows: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
+    """One SMoES MoE layer forward: route, (update and) score modality, MI loss
+    and its logit gradient, permutation, experts, combine.
+
+    `rows`, when given, restricts the expert computation to those tokens (the
+    routing, modality score and MI always cover the whole batch)."""
+    d = _f64(w_gate).shape[1]
+    z, g, idx, w = route(x, w_gate, k, logit_bias, renorm_topk)
+    if update_stats:
+        state = gauss_update(state, x, modality_id, beta)
+    mu, var = gauss_params(state, var_floor)
+    M = modality_score(x, mu, var, default_tau(d, tau))
+    I = mi_per_sample(g, M, sample_offsets, expert_to_bin, n_bins)
+    loss = -float(I.sum()) / len(I)
+    dlogits = mi_loss_grad_logits(g, M, sample_offsets, expert_to_bin, n_bins, grad_scale)
+    E = _f64(w_gate).shape[0]
+    counts, offsets, perm_token, inv = permutation(idx, E)
+    out = {"logits": z, "probs": g, "topk_idx": idx, "topk_w": w, "gap": topk_gap(z, k),
+           "state": state, "M": M, "mi_per_sample": I, "loss": loss, "dlogits": dlogits,
+           "expert_counts": counts, "expert_offsets": offsets, "perm_token": perm_token, "inv": inv}
+    if w13 is not None:
+        if rows is None:
+            full, routed, shared = experts_grouped(x, idx, w, w13, w2, ws13, ws2, E)
+        else:
+            xs = np.asarray(x)[rows]
+            full, routed, shared = experts_grouped(xs, idx[rows], w[rows], w13, w2, ws13, ws2, E)
+        out.update(out=full, routed=routed, shared=shared)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Sec. 4.1 diagnostic: modality specialization index (test utility)
+# ----------------------------------------------------------------------------
+
+def msi(counts_text, counts_vision) -> float:
+    """MSI for one layer (Eq. 18-19) from per-expert token counts per modality."""
+    ct = np.asarray(counts_text, dtype=np.float64)
+    cv = np.asarray(counts_vision, dtype=np.float64)
+    nt = ct / ct.sum()
+    nv = cv / cv.sum()
+    c_text = nt / (nt + nv)
+    return float(np.mean(2.0 * np.abs(c_text - 0.5)))

@@ -1,0 +1,498 @@
+"""Pins of the CPU oracle against facts the paper and mathematics fix.
+
+None of these re-types the oracle's own formulas: each checks it against a
+library routine, a closed form, an invariant, finite differences, or brute
+force on tiny inputs, chosen so that a dropped term, a wrong sign or index, or
+a transposed operand in the oracle fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+import torch
+from scipy.spatial.distance import jensenshannon
+from sklearn.metrics import mutual_info_score
+
+import oracle as O
+from paper_2604_23996_amd import workloads as W
+
+RNG = np.random.default_rng(20240601)
+
+
+# ---------------------------------------------------------------- router (Sec. 3.1)
+
+def test_router_logits_brute_force_dot():
+    x = RNG.standard_normal((5, 7))
+    w = RNG.standard_normal((3, 7))
+    b = RNG.standard_normal(3)
+    z = O.router_logits(x, w, b)
+    for j in range(5):
+        for e in range(3):
+            ref = math.fsum(x[j, t] * w[e, t] for t in range(7)) + b[e]
+            assert abs(z[j, e] - ref) < 1e-12
+
+
+def test_router_logits_bf16_inputs_widened_exactly():
+    x32 = RNG.standard_normal((4, 16)).astype(np.float32)
+    bits = W.f32_to_bf16_bits(x32)
+    w = RNG.standard_normal((3, 16)).astype(np.float32)
+    z = O.router_logits(bits, w)
+    xw = W.bf16_bits_to_f32(bits).astype(np.float64)
+    assert np.array_equal(z, xw @ w.astype(np.float64).T)
+    # the bf16 value is the nearest one: |x - bf16(x)| <= half an ulp of 8 bits
+    assert np.all(np.abs(xw - x32) <= np.abs(x32) * 2.0 ** -8 + 1e-38)
+
+
+def test_softmax_matches_scipy_and_sums_to_one():
+    z = RNG.standard_normal((20, 11)) * 5
+    g = O.softmax_rows(z)
+    assert np.allclose(g, scipy.special.softmax(z, axis=1), rtol=1e-14, atol=0)
+    assert np.allclose(g.sum(axis=1), 1.0, atol=1e-15)
+    assert np.all(g > 0)
+
+
+def _topk_brute(z, k):
+    out = []
+    for row in np.asarray(z, dtype=np.float32):
+        taken = []
+        for _ in range(k):
+            best = None
+            for e, v in enumerate(row):
+                if e in taken:
+                    continue
+                if best is None or v > row[best]:
+                    best = e  # strict '>' keeps the lower index on ties
+            taken.append(best)
+        out.append(taken)
+    return np.array(out)
+
+
+def test_topk_brute_force_with_ties():
+    z = RNG.integers(-3, 4, size=(40, 9)).astype(np.float64)  # many exact ties
+    for k in (1, 2, 4, 9):
+        assert np.array_equal(O.topk_select(z, k), _topk_brute(z, k))
+
+
+def test_topk_decided_in_float32():
+    # two logits that differ only below float32 resolution tie in float32,
+    # so the lower index wins (reading R4)
+    z = np.array([[1.0, 1.0 + 1e-12, 0.0]])
+    assert O.topk_select(z, 1)[0, 0] == 0
+
+
+def test_route_weights_are_gate_values_and_renorm():
+    x = RNG.standard_normal((6, 5))
+    w = RNG.standard_normal((8, 5))
+    z, g, idx, wt = O.route(x, w, 3)
+    assert np.allclose(wt, scipy.special.softmax(z, axis=1)[np.arange(6)[:, None], idx])
+    _, _, idx2, wr = O.route(x, w, 3, renorm_topk=True)
+    assert np.array_equal(idx, idx2)
+    assert np.allclose(wr.sum(axis=1), 1.0)
+    assert np.allclose(wr, wt / wt.sum(axis=1, keepdims=True))
+
+
+def test_topk_gap():
+    z = np.array([[3.0, 1.0, 2.0, 0.5]])
+    assert O.topk_gap(z, 1)[0] == 1.0
+    assert O.topk_gap(z, 2)[0] == 1.0
+    assert O.topk_gap(z, 3)[0] == 0.5
+    assert np.isinf(O.topk_gap(z, 4)[0])
+
+
+# ---------------------------------------------------------------- Gaussian statistics (Sec. 3.2.2)
+
+def _batches(n_batches=6, d=5):
+    out = []
+    for b in range(n_batches):
+        T = int(RNG.integers(3, 12))
+        x = RNG.standard_normal((T, d)) * (1 + b) + b
+        mid = RNG.integers(0, 2, size=T).astype(np.uint8)
+        if b == 2:
+            mid[:] = 0  # a batch with no text tokens
+        out.append((x, mid))
+    return out
+
+
+@pytest.mark.parametrize("beta", [0.99, 0.7, 1.0])
+def test_ema_welford_equals_weighted_brute_force(beta):
+    """After batches 1..t, N = sum_b beta^(t-b) n_b, mu = weighted mean and
+    S_sigma2 = sum_b beta^(t-b) sum_{x in b} (x - mu)^2 (the weighted
+    population scatter): the closed form the EMA-Welford recursion realises."""
+    d = 5
+    st = O.GaussState.zeros(d)
+    seen = []
+    for x, mid in _batches(d=d):
+        st = O.gauss_update(st, x, mid, beta)
+        seen.append((x, mid))
+        t = len(seen)
+        for m in (0, 1):
+            wts, rows = [], []
+            for b, (xb, mb) in enumerate(seen):
+                sel = xb[mb == m]
+                rows.append(sel)
+                wts.append(np.full(len(sel), beta ** (t - 1 - b)))
+            X = np.concatenate(rows)
+            wv = np.concatenate(wts)
+            n = wv.sum()
+            assert abs(st.n[m] - n) < 1e-12 * max(1, n)
+            if n == 0:
+                continue
+            mu = (wv[:, None] * X).sum(axis=0) / n
+            sc = (wv[:, None] * (X - mu) ** 2).sum(axis=0)
+            assert np.allclose(st.s_mu[m] / st.n[m], mu, rtol=1e-12, atol=1e-12)
+            assert np.allclose(st.s_sig[m], sc, rtol=1e-11, atol=1e-11)
+
+
+def test_ema_welford_beta_one_is_pooled_population_variance():
+    d = 4
+    st = O.GaussState.zeros(d)
+    xs = []
+    for x, mid in _batches(d=d):
+        st = O.gauss_update(st, x, mid, 1.0)
+        xs.append(x[mid == 1])
+    X = np.concatenate(xs)
+    mu, var = O.gauss_params(st, 0.0)
+    assert np.allclose(mu[1], X.mean(axis=0), rtol=1e-12)
+    assert np.allclose(var[1], np.var(X, axis=0), rtol=1e-12)
+
+
+def test_gauss_params_floor_and_empty_modality():
+    st = O.GaussState(np.array([2.0, 0.0]), np.array([[2.0, 4.0], [0, 0]]), np.array([[0.0, 8.0], [0, 0]]))
+    mu, var = O.gauss_params(st, 1e-3)
+    assert np.array_equal(mu[0], [1.0, 2.0]) and np.array_equal(var[0], [1e-3, 4.0])
+    assert np.array_equal(mu[1], [0, 0]) and np.array_equal(var[1], [1, 1])
+
+
+def test_log_likelihood_matches_scipy_normal_logpdf():
+    d = 6
+    x = RNG.standard_normal((7, d))
+    mu = RNG.standard_normal((2, d))
+    var = RNG.uniform(0.3, 3.0, size=(2, d))
+    ll = O.log_likelihood(x, mu, var)
+    for m in (0, 1):
+        ref = scipy.stats.norm.logpdf(x, loc=mu[m], scale=np.sqrt(var[m])).sum(axis=1)
+        # Eq. 8 drops the constant -D/2 log(2 pi)
+        assert np.allclose(ll[:, m], ref + 0.5 * d * np.log(2 * np.pi), rtol=1e-13, atol=1e-12)
+
+
+def test_modality_score_is_logistic_of_ll_difference():
+    d = 8
+    x = RNG.standard_normal((30, d)) * 2
+    mu = RNG.standard_normal((2, d))
+    var = RNG.uniform(0.3, 3.0, size=(2, d))
+    for tau in (0.05 * d, 0.5 * d, 1.0 * d):
+        M = O.modality_score(x, mu, var, tau)
+        ll_v = scipy.stats.multivariate_normal(mu[0], np.diag(var[0])).logpdf(x)
+        ll_t = scipy.stats.multivariate_normal(mu[1], np.diag(var[1])).logpdf(x)
+        assert np.allclose(M[:, 0], scipy.special.expit((ll_v - ll_t) / tau), rtol=1e-12, atol=1e-15)
+        assert np.allclose(M.sum(axis=1), 1.0, atol=1e-15)
+        assert np.all((M >= 0) & (M <= 1))
+
+
+def test_modality_score_symmetries():
+    d = 5
+    x = RNG.standard_normal((10, d))
+    mu = RNG.standard_normal((2, d))
+    var = RNG.uniform(0.5, 2, size=(2, d))
+    M = O.modality_score(x, mu, var, 0.5 * d)
+    Ms = O.modality_score(x, mu[::-1], var[::-1], 0.5 * d)
+    assert np.allclose(M, Ms[:, ::-1], atol=1e-15)  # swapping statistics swaps columns
+    same = O.modality_score(x, np.stack([mu[0], mu[0]]), np.stack([var[0], var[0]]), 2.0)
+    assert np.allclose(same, 0.5)  # identical statistics give (1/2, 1/2)
+    # a token at the vision mean with equal variances leans to vision
+    near = O.modality_score(mu[:1], mu, np.ones((2, d)), 1.0)
+    assert near[0, 0] > 0.5
+
+
+def test_default_tau():
+    assert O.default_tau(2048, 0.0) == 1024.0
+    assert O.default_tau(2048, 3.0) == 3.0
+
+
+# ---------------------------------------------------------------- inter-bin MI (Sec. 3.3, 3.4)
+
+def _binary_entropy(p):
+    return -(p * math.log(p) + (1 - p) * math.log(1 - p))
+
+
+def _hard_sample(qv, qt, n_each=4, N_B=3):
+    """Hard-score sample whose per-bin gate mass is qv for every vision token
+    and qt for every text token (spread evenly over each bin's experts)."""
+    B = len(qv)
+    g = []
+    M = []
+    for q, m in ((qv, 0), (qt, 1)):
+        row = np.repeat(np.asarray(q, dtype=np.float64) / N_B, N_B)
+        for _ in range(n_each):
+            g.append(row)
+            M.append([1.0, 0.0] if m == 0 else [0.0, 1.0])
+    e2b = np.repeat(np.arange(B), N_B)
+    return np.array(g), np.array(M), e2b
+
+
+@pytest.mark.parametrize("qv,qt,expected", [
+    ((0.9, 0.1), (0.1, 0.9), 0.3680642071684971),
+    ((0.7, 0.3), (0.4, 0.6), 0.04620082918151347),
+])
+def test_mi_hard_two_bins_closed_form(qv, qt, expected):
+    """Hard scores, B = 2: I = H((a+b)/2) - (H(a) + H(b)) / 2 (a Jensen-Shannon
+    divergence in nats, since P(m) = 1/2 under the per-modality normalisation)."""
+    g, M, e2b = _hard_sample(qv, qt)
+    I = O.mi_per_sample(g, M, [0, len(g)], e2b, 2)[0]
+    a, b = qv[0], qt[0]
+    closed = _binary_entropy((a + b) / 2) - 0.5 * (_binary_entropy(a) + _binary_entropy(b))
+    assert abs(closed - expected) < 1e-15
+    assert abs(I - closed) < 1e-14
+    assert abs(I - jensenshannon(qv, qt) ** 2) < 1e-13
+
+
+def test_mi_hard_many_bins_equals_jsd():
+    for B in (3, 4, 8):
+        qv = RNG.dirichlet(np.ones(B))
+        qt = RNG.dirichlet(np.ones(B))
+        g, M, e2b = _hard_sample(qv, qt, N_B=2)
+        I = O.mi_per_sample(g, M, [0, len(g)], e2b, B)[0]
+        assert abs(I - jensenshannon(qv, qt) ** 2) < 1e-13
+
+
+def test_mi_one_hot_routing_equals_contingency_mi():
+    """Hard scores and one-hot gates: the joint is P(m, k) = count(m, k) / (2 n_m).
+    With equal token counts per modality this is the plain contingency MI."""
+    n = 12
+    B, N_B = 4, 2
+    E = B * N_B
+    rows, M = [], []
+    cont = np.zeros((2, B), dtype=np.int64)
+    for m in (0, 1):
+        for _ in range(n):
+            e = int(RNG.integers(0, E))
+            r = np.zeros(E)
+            r[e] = 1.0
+            rows.append(r)
+            M.append([1.0 - m, float(m)])
+            cont[m, e // N_B] += 1
+    I = O.mi_per_sample(np.array(rows), np.array(M), [0, 2 * n], np.arange(E) // N_B, B)[0]
+    assert abs(I - mutual_info_score(None, None, contingency=cont)) < 1e-13
+
+
+def test_mi_soft_scores_equal_duplicated_hard_tokens():
+    """Eq. 12 is linear in M: a token with M = (1/4, 3/4) counts as one hard
+    vision copy and three hard text copies of itself."""
+    E, B = 6, 3
+    e2b = np.arange(E) // 2
+    g = RNG.dirichlet(np.ones(E), size=5)
+    soft = np.array([[0.25, 0.75], [0.5, 0.5], [1.0, 0.0], [0.0, 1.0], [0.75, 0.25]])
+    I_soft = O.mi_per_sample(g, soft, [0, 5], e2b, B)[0]
+    rows, M = [], []
+    for j in range(5):
+        nv = int(round(4 * soft[j, 0]))
+        for c in range(4):
+            rows.append(g[j])
+            M.append([1.0, 0.0] if c < nv else [0.0, 1.0])
+    I_hard = O.mi_per_sample(np.array(rows), np.array(M), [0, len(rows)], e2b, B)[0]
+    assert abs(I_soft - I_hard) < 1e-14
+    # and the hard copy is the JSD of the two modality-conditional bin masses
+    Mh = np.array(M)
+    Gh = np.stack([np.array(rows)[:, e2b == k].sum(axis=1) for k in range(B)], axis=1)
+    qv = Gh[Mh[:, 0] == 1].mean(axis=0)
+    qt = Gh[Mh[:, 1] == 1].mean(axis=0)
+    assert abs(I_hard - jensenshannon(qv, qt) ** 2) < 1e-13
+
+
+def test_mi_bounds_and_zero_cases():
+    for _ in range(20):
+        B = int(RNG.choice([2, 4, 8]))
+        N_B = int(RNG.integers(1, 4))
+        E = B * N_B
+        T = int(RNG.integers(2, 40))
+        g = RNG.dirichlet(np.ones(E) * RNG.uniform(0.05, 2), size=T)
+        M = W.random_soft_scores(RNG, T).astype(np.float64)
+        e2b = RNG.permutation(np.arange(E) // N_B)
+        I = O.mi_per_sample(g, M, [0, T], e2b, B)[0]
+        assert -1e-15 <= I <= min(math.log(B), math.log(2)) + 1e-15
+        # constant modality score across the sample: bins carry no information
+        Mc = np.tile(M[:1], (T, 1))
+        assert abs(O.mi_per_sample(g, Mc, [0, T], e2b, B)[0]) < 1e-15
+        # every token with the same gate row: independence
+        gc = np.tile(g[:1], (T, 1))
+        assert abs(O.mi_per_sample(gc, M, [0, T], e2b, B)[0]) < 1e-15
+
+
+def test_mi_marginal_over_modalities_is_one_half():
+    """Under the full softmax every modality row of S-bar sums to 1/N_B, so
+    P(m) = 1/2 exactly (reading R2)."""
+    g = O.softmax_rows(RNG.standard_normal((30, 12)))
+    M = W.random_soft_scores(RNG, 30)
+    t = O.mi_sample_terms(g, M, np.arange(12) // 3, 4)
+    assert np.allclose(t["S_bar"].sum(axis=1), 1.0 / 3, rtol=1e-14)
+    assert np.allclose(t["Pm"], 0.5, rtol=1e-14)
+
+
+def test_mi_invariances():
+    E, B = 8, 4
+    e2b = np.arange(E) // 2
+    g = RNG.dirichlet(np.ones(E), size=25)
+    M = W.random_soft_scores(RNG, 25)
+    I0 = O.mi_per_sample(g, M, [0, 25], e2b, B)[0]
+    # relabel bins
+    relabel = np.array([2, 0, 3, 1])
+    assert abs(O.mi_per_sample(g, M, [0, 25], relabel[e2b], B)[0] - I0) < 1e-15
+    # reorder experts (columns) together with their bin labels
+    p = RNG.permutation(E)
+    assert abs(O.mi_per_sample(g[:, p], M, [0, 25], e2b[p], B)[0] - I0) < 1e-15
+    # swap modalities
+    assert abs(O.mi_per_sample(g, M[:, ::-1], [0, 25], e2b, B)[0] - I0) < 1e-15
+    # reorder tokens
+    q = RNG.permutation(25)
+    assert abs(O.mi_per_sample(g[q], M[q], [0, 25], e2b, B)[0] - I0) < 1e-15
+
+
+def test_mi_separates_samples():
+    E, B = 6, 2
+    e2b = np.arange(E) // 3
+    g = RNG.dirichlet(np.ones(E), size=30)
+    M = W.random_soft_scores(RNG, 30)
+    off = [0, 7, 7, 30]  # the middle sample is empty
+    I = O.mi_per_sample(g, M, off, e2b, B)
+    assert I[1] == 0.0
+    assert abs(I[0] - O.mi_per_sample(g[:7], M[:7], [0, 7], e2b, B)[0]) == 0.0
+    assert abs(I[2] - O.mi_per_sample(g[7:], M[7:], [0, 23], e2b, B)[0]) == 0.0
+    assert O.mi_loss(g, M, off, e2b, B) == pytest.approx(-I.sum() / 3, rel=1e-15)
+
+
+def test_mi_approaches_ln2_for_separated_sharp_routing():
+    # hard scores, vision tokens all in bin 0 and text all in bin 1 with huge logit gaps
+    E, B = 4, 2
+    z = np.zeros((8, E))
+    z[:4, :2] = 60.0
+    z[4:, 2:] = 60.0
+    g = O.softmax_rows(z)
+    M = np.array([[1.0, 0.0]] * 4 + [[0.0, 1.0]] * 4)
+    I = O.mi_per_sample(g, M, [0, 8], np.arange(E) // 2, B)[0]
+    assert abs(I - math.log(2)) < 1e-12
+
+
+# ---------------------------------------------------------------- MI gradient
+
+def _loss_of_logits(z, M, off, e2b, B):
+    return O.mi_loss(O.softmax_rows(z), M, off, e2b, B)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_mi_grad_matches_central_differences(seed):
+    rng = np.random.default_rng(seed)
+    E, B, T = 6, 3, 9
+    e2b = rng.permutation(np.arange(E) // 2)
+    z = rng.standard_normal((T, E)) * 1.5
+    M = W.random_soft_scores(rng, T).astype(np.float64)
+    off = [0, 4, 9]
+    gs = 0.37
+    grad = O.mi_loss_grad_logits(O.softmax_rows(z), M, off, e2b, B, gs)
+    h = 1e-5
+    fd = np.zeros_like(z)
+    for j in range(T):
+        for e in range(E):
+            zp = z.copy(); zp[j, e] += h
+            zm = z.copy(); zm[j, e] -= h
+            fd[j, e] = gs * (_loss_of_logits(zp, M, off, e2b, B) - _loss_of_logits(zm, M, off, e2b, B)) / (2 * h)
+    assert np.max(np.abs(grad - fd)) < 1e-9 * max(1.0, np.max(np.abs(fd)))
+    assert np.max(np.abs(fd)) > 1e-4  # the check is not vacuous
+
+
+def test_mi_grad_rows_sum_to_zero_and_vanish_at_independence():
+    E, B, T = 8, 4, 12
+    e2b = np.arange(E) // 2
+    g = O.softmax_rows(RNG.standard_normal((T, E)))
+    M = W.random_soft_scores(RNG, T)
+    grad = O.mi_loss_grad_logits(g, M, [0, T], e2b, B)
+    assert np.max(np.abs(grad.sum(axis=1))) < 1e-17 + 1e-12 * np.max(np.abs(grad))
+    Mc = np.tile(M[:1], (T, 1))
+    assert np.max(np.abs(O.mi_loss_grad_logits(g, Mc, [0, T], e2b, B))) < 1e-15
+
+
+# ---------------------------------------------------------------- permutation
+
+@pytest.mark.parametrize("T,E,k", [(1, 4, 1), (17, 8, 2), (64, 5, 5), (40, 32, 6)])
+def test_permutation_matches_stable_argsort(T, E, k):
+    idx = W.random_topk(RNG, T, E, k, skew=2.0)
+    counts, offsets, perm_token, inv = O.permutation(idx, E)
+    flat = idx.reshape(-1)
+    order = np.argsort(flat, kind="stable")  # library stable sort of the (token, slot) pairs
+    assert np.array_equal(counts, np.bincount(flat, minlength=E))
+    assert offsets[0] == 0 and offsets[-1] == T * k
+    assert np.array_equal(perm_token, order // k)
+    ref_inv = np.empty(T * k, dtype=np.int64)
+    ref_inv[order] = np.arange(T * k)
+    assert np.array_equal(inv.reshape(-1), ref_inv)
+    # perm o inv = identity on tokens
+    assert np.array_equal(perm_token[inv], np.repeat(np.arange(T)[:, None], k, axis=1))
+
+
+# ---------------------------------------------------------------- experts
+
+def _torch_swiglu(x, w13, w2):
+    X = torch.from_numpy(np.asarray(x, dtype=np.float64))
+    W13 = torch.from_numpy(np.asarray(w13, dtype=np.float64))
+    I = W13.shape[0] // 2
+    h = torch.nn.functional.silu(X @ W13[:I].T) * (X @ W13[I:].T)
+    return (h @ torch.from_numpy(np.asarray(w2, dtype=np.float64)).T).numpy()
+
+
+def test_swiglu_matches_torch():
+    x = RNG.standard_normal((5, 12))
+    w13 = RNG.standard_normal((2 * 7, 12))
+    w2 = RNG.standard_normal((12, 7))
+    assert np.allclose(O.swiglu(x, w13, w2), _torch_swiglu(x, w13, w2), rtol=1e-13, atol=1e-13)
+
+
+def test_merged_shared_experts_equal_sum_of_two():
+    d, I = 10, 6
+    x = RNG.standard_normal((7, d))
+    a13, b13 = RNG.standard_normal((2 * I, d)), RNG.standard_normal((2 * I, d))
+    a2, b2 = RNG.standard_normal((d, I)), RNG.standard_normal((d, I))
+    merged13 = np.concatenate([a13[:I], b13[:I], a13[I:], b13[I:]])
+    merged2 = np.concatenate([a2, b2], axis=1)
+    two = _torch_swiglu(x, a13, a2) + _torch_swiglu(x, b13, b2)
+    assert np.allclose(O.swiglu(x, merged13, merged2), two, rtol=1e-12, atol=1e-12)
+
+
+def test_grouped_experts_equal_naive_loop_and_torch():
+    cfg = W.small_config(d=16, E=6, k=3, inter=8, n_shared=1, n_bins=3, samples=((9, 4),))
+    inp = W.make_layer_inputs(cfg)
+    z, g, idx, w = O.route(inp.x, inp.w_gate, cfg.k)
+    full, routed, shared = O.experts_grouped(inp.x, idx, w, inp.w13, inp.w2, inp.ws13, inp.ws2)
+    naive = O.experts_naive(inp.x, idx, w, inp.w13, inp.w2, inp.ws13, inp.ws2)
+    assert np.max(np.abs(full - naive)) < 1e-12
+    ref = np.zeros_like(full)
+    for j in range(cfg.T):
+        for s in range(cfg.k):
+            ref[j] += w[j, s] * _torch_swiglu(inp.x[j:j + 1], inp.w13[idx[j, s]], inp.w2[idx[j, s]])[0]
+    ref += _torch_swiglu(inp.x, inp.ws13, inp.ws2)
+    assert np.max(np.abs(full - ref)) < 1e-12
+
+
+# ---------------------------------------------------------------- whole layer and diagnostics
+
+def test_layer_forward_consistency_small():
+    cfg = W.small_config()
+    inp = W.make_layer_inputs(cfg)
+    st = O.GaussState.zeros(cfg.d)
+    r = O.layer_forward(inp.x, inp.modality_id, inp.sample_offsets, inp.w_gate, inp.logit_bias,
+                        inp.expert_to_bin, cfg.n_bins, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
+                        st, update_stats=True)
+    # update from the zero state gives the batch population mean / variance per modality
+    X = inp.x.astype(np.float64)
+    for m in (0, 1):
+        sel = X[inp.modality_id == m]
+        assert np.allclose(r["state"].s_mu[m] / r["state"].n[m], sel.mean(axis=0), rtol=1e-12)
+        assert np.allclose(r["state"].s_sig[m] / r["state"].n[m], np.var(sel, axis=0), rtol=1e-12)
+    assert np.allclose(r["M"].sum(axis=1), 1)
+    assert r["loss"] == pytest.approx(-r["mi_per_sample"].mean())
+    assert np.array_equal(r["expert_counts"], np.bincount(r["topk_idx"].reshape(-1), minlength=cfg.E))
+
+
+def test_msi_extremes():
+    assert O.msi([5, 0, 3], [0, 7, 0]) == 1.0
+    assert O.msi([2, 4, 6], [1, 2, 3]) == pytest.approx(0.0, abs=1e-15)
