@@ -1,0 +1,277 @@
+/*
+ * smoes.h - C ABI of the SMoES MoE-layer hot path for AMD Instinct MI355X (gfx950).
+ *
+ * SMoES ("Soft Modality-Guided Expert Specialization in MoE-VLMs") routes the
+ * tokens of a mixed vision + text batch through a Mixture-of-Experts layer and
+ * regularises the router with the mutual information between a soft modality
+ * score and groups ("bins") of experts. This library computes one layer:
+ *
+ *   smoes_route            router logits, softmax gate, top-k        (Sec. 3.1)
+ *   smoes_modality_score   EMA-Welford statistics + Gaussian score   (Sec. 3.2.2, Eq. 5-9)
+ *   smoes_mi_loss          inter-bin MI, its loss and d loss / d logits (Sec. 3.3-3.4, Eq. 12-15)
+ *   smoes_permute          expert-contiguous token order (+ optional row gather)
+ *   smoes_moe_forward      all of the above + grouped SwiGLU experts, shared
+ *                          experts and the weighted combine
+ *
+ * Conventions shared by every entry point
+ *   - Every array pointer is a DEVICE pointer owned by the caller; arrays are
+ *     dense and row-major. The library allocates no device memory: scratch
+ *     comes from a caller-provided workspace whose size the matching
+ *     *_workspace_size query returns (any alignment; the library aligns
+ *     inside it). Workspace contents need not be initialised and are
+ *     clobbered.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
+ *     asynchronously; no call synchronises the host. The library keeps no
+ *     global state, so distinct calls with distinct buffers may run from
+ *     different threads.
+ *   - Return value: SMOES_OK (0) or a negative smoes_status. Argument checks
+ *     happen on the host before anything is enqueued; on an error nothing is
+ *     launched and no output is written. T = 0 is a successful no-op.
+ *   - Values that live on the device are NOT checked (that would need a
+ *     synchronisation); the caller guarantees them: modality ids in {0, 1},
+ *     sample offsets non-decreasing with offsets[0] = 0 and offsets[n_batch] = T,
+ *     expert_to_bin entries in [0, n_bins) with exactly E / n_bins experts per
+ *     bin, top-k indices in [0, E) and distinct within a token.
+ *   - Activation dtype codes: SMOES_F32 (float) or SMOES_BF16 (bfloat16 bits,
+ *     uint16 storage). Router weights, logits, gate probabilities, modality
+ *     scores and losses are always float32.
+ */
+#ifndef SMOES_H
+#define SMOES_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum smoes_status {
+    SMOES_OK = 0,
+    SMOES_ERR_ARG = -1,       /* a required pointer is NULL, or a scalar/dtype is out of range */
+    SMOES_ERR_SHAPE = -2,     /* inconsistent sizes (see each entry point) */
+    SMOES_ERR_WORKSPACE = -3, /* workspace_bytes smaller than the query's answer */
+    SMOES_ERR_HIP = -4        /* a HIP launch or runtime call failed */
+};
+
+/* Activation storage types. */
+enum smoes_dtype { SMOES_F32 = 0, SMOES_BF16 = 1 };
+
+/* Limits checked by every entry point (SMOES_ERR_SHAPE beyond them). */
+#define SMOES_E_MAX 256   /* routed experts */
+#define SMOES_K_MAX 16    /* top-k */
+#define SMOES_BINS_MAX 64 /* expert bins */
+#define SMOES_D_MAX 16384 /* hidden size */
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char* smoes_status_string(int status);
+
+/* Library version string (static storage). */
+const char* smoes_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Router (Sec. 3.1: g = softmax(W_gate x); the k highest-scoring experts).  */
+/* ------------------------------------------------------------------------ */
+
+size_t smoes_route_workspace_size(int64_t T, int d, int E, int x_dtype);
+
+/*
+ * x          [T, d] activations (x_dtype). For SMOES_BF16 the logits are
+ *            computed fp32-faithfully (the fp32 weights are split into three
+ *            bf16 terms whose products with the exact bf16 inputs are exact).
+ * w_gate     [E, d] float32 router weights.
+ * logit_bias [E] float32 added to every token's logits before softmax and
+ *            top-k, or NULL.
+ * renorm_topk  0: topk_w are the gate probabilities of the chosen experts;
+ *              1: they are renormalised to sum to 1 per token.
+ * logits     [T, E] float32 output, or NULL (not stored).
+ * probs      [T, E] float32 output: the full softmax over all E experts.
+ * topk_idx   [T, k] int32 output: experts by descending logit, ties to the
+ *            lower index (decided on the float32 logits).
+ * topk_w     [T, k] float32 output: combine weights.
+ * Shapes: 1 <= d <= SMOES_D_MAX, d % 8 == 0; 1 <= E <= SMOES_E_MAX;
+ *         1 <= k <= min(E, SMOES_K_MAX).
+ */
+int smoes_route(const void* x, int x_dtype, int64_t T, int d,
+                const float* w_gate, const float* logit_bias, int E, int k, int renorm_topk,
+                float* logits, float* probs, int32_t* topk_idx, float* topk_w,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Gaussian-statistics modality score (Sec. 3.2.2, Eq. 5-9).                 */
+/* ------------------------------------------------------------------------ */
+
+size_t smoes_modality_workspace_size(int64_t T, int d);
+
+/*
+ * x            [T, d] activations (x_dtype): the MoE layer input.
+ * modality_id  [T] uint8, 0 = vision, 1 = text. Required iff update != 0.
+ * gauss_n      [2] float32 EMA token counts N_m (in/out when update != 0).
+ * gauss_smu    [2, d] float32 S_mu,m (in/out when update != 0).
+ * gauss_ssig   [2, d] float32 S_sigma2,m (in/out when update != 0).
+ *              Row/entry 0 is vision, 1 is text. The caller owns (and
+ *              checkpoints) this state; a fresh layer starts from zeros.
+ * update       1: first fold the batch into the state with the EMA-Welford
+ *              step of Eq. 5-7 (decay beta), then score; 0: score only.
+ * beta         EMA decay in [0, 1] (paper: 0.99).
+ * tau          temperature of Eq. 9; tau <= 0 selects 0.5 * d (paper default).
+ * var_floor    lower bound applied to sigma^2 = S_sigma2 / N (>= 0).
+ * M            [T, 2] float32 output: column 0 vision score, column 1 text
+ *              score; each row sums to 1.
+ * A modality with N = 0 scores with mu = 0, sigma^2 = 1.
+ * Shapes: 1 <= d <= SMOES_D_MAX, d % 8 == 0.
+ */
+int smoes_modality_score(const void* x, int x_dtype, int64_t T, int d,
+                         const uint8_t* modality_id,
+                         float* gauss_n, float* gauss_smu, float* gauss_ssig,
+                         int update, float beta, float tau, float var_floor,
+                         float* M, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Inter-bin mutual information (Sec. 3.3-3.4, Eq. 12-15) and its gradient. */
+/* ------------------------------------------------------------------------ */
+
+size_t smoes_mi_workspace_size(int64_t T, int E, int n_batch, int n_bins);
+
+/*
+ * probs          [T, E] float32 full-softmax gate g.
+ * M              [T, 2] float32 soft modality scores (column 0 vision).
+ * sample_offsets [n_batch + 1] int32 token offsets of the samples, or NULL
+ *                for one sample covering all T tokens (then n_batch must be 1).
+ * expert_to_bin  [E] int32 bin of every expert (bins hold E / n_bins experts).
+ * grad_scale     multiplies the gradient (e.g. the loss weight alpha_MI).
+ * mi_per_sample  [n_batch] float32 output: I_i(M; B) in nats (Eq. 14).
+ * loss           [1] float32 output: L_MI = -(1/n_batch) sum_i I_i (Eq. 15).
+ * dlogits        [T, E] float32 output grad_scale * dL_MI / d logits with the
+ *                modality scores held constant, or NULL to skip it.
+ * Sums are accumulated in float64 in a fixed order: results are bit-for-bit
+ * reproducible. Shapes: 1 <= E <= SMOES_E_MAX, 1 <= n_bins <= SMOES_BINS_MAX,
+ * E % n_bins == 0, n_batch >= 1.
+ */
+int smoes_mi_loss(const float* probs, const float* M, int64_t T, int E,
+                  const int32_t* sample_offsets, int n_batch,
+                  const int32_t* expert_to_bin, int n_bins, float grad_scale,
+                  float* mi_per_sample, float* loss, float* dlogits,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Expert-contiguous permutation of the routed (token, slot) pairs.          */
+/* ------------------------------------------------------------------------ */
+
+size_t smoes_permute_workspace_size(int64_t T, int E, int k);
+
+/*
+ * topk_idx       [T, k] int32 experts of every token (distinct per token).
+ * expert_offsets [E + 1] int32 output: exclusive prefix sum of the per-expert
+ *                row counts (expert e owns rows [off[e], off[e+1])).
+ * perm_token     [T * k] int32 output: token of every permuted row; rows of
+ *                one expert are in ascending token order.
+ * perm_inv       [T, k] int32 output: permuted row of every (token, slot).
+ * x, x_perm      optional: when x_perm is non-NULL, x_perm[r] = x[perm_token[r]]
+ *                ([T * k, d], same dtype as x) is also written.
+ * The order is a deterministic stable counting sort (no atomics decide it).
+ * Shapes: 1 <= E <= SMOES_E_MAX, 1 <= k <= min(E, SMOES_K_MAX); d % 8 == 0
+ * when x_perm is given.
+ */
+int smoes_permute(const int32_t* topk_idx, int64_t T, int E, int k,
+                  int32_t* expert_offsets, int32_t* perm_token, int32_t* perm_inv,
+                  const void* x, int x_dtype, int d, void* x_perm,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* The whole SMoES MoE layer forward.                                        */
+/* ------------------------------------------------------------------------ */
+
+typedef struct smoes_layer {
+    int64_t T;        /* tokens */
+    int d;            /* hidden size, d % 8 == 0 */
+    int E;            /* routed experts */
+    int k;            /* top-k */
+    int inter;        /* routed expert FFN inner size, inter % 16 == 0 */
+    int shared_inter; /* merged inner size of the shared experts (0 = none), % 16 == 0 */
+    int n_bins;       /* expert bins, E % n_bins == 0 */
+    int n_batch;      /* samples (>= 1) */
+    int act_dtype;    /* SMOES_F32 or SMOES_BF16: x, expert weights and out */
+    float tau;        /* Eq. 9 temperature; <= 0 selects 0.5 * d */
+    float beta;       /* EMA decay of Eq. 5-7 */
+    float var_floor;  /* floor on sigma^2 */
+    float grad_scale; /* scale of dlogits */
+    int renorm_topk;  /* renormalise the combine weights */
+    int update_stats; /* fold the batch into the Gaussian state before scoring */
+} smoes_layer;
+
+typedef struct smoes_layer_io {
+    /* inputs */
+    const void* x;                 /* [T, d] act_dtype */
+    const uint8_t* modality_id;    /* [T]; required iff update_stats */
+    const int32_t* sample_offsets; /* [n_batch + 1] or NULL (one sample) */
+    const float* w_gate;           /* [E, d] */
+    const float* logit_bias;       /* [E] or NULL */
+    const int32_t* expert_to_bin;  /* [E] */
+    const void* w13;               /* [E, 2*inter, d]: rows [0, inter) gate, [inter, 2*inter) up */
+    const void* w2;                /* [E, d, inter] down projection */
+    const void* ws13;              /* [2*shared_inter, d] or NULL when shared_inter == 0 */
+    const void* ws2;               /* [d, shared_inter] or NULL when shared_inter == 0 */
+    /* caller-owned Gaussian state (in/out when update_stats) */
+    float* gauss_n;   /* [2] */
+    float* gauss_smu; /* [2, d] */
+    float* gauss_ssig;/* [2, d] */
+    /* outputs (NULL allowed where marked) */
+    float* logits;          /* [T, E] or NULL */
+    float* probs;           /* [T, E] */
+    int32_t* topk_idx;      /* [T, k] */
+    float* topk_w;          /* [T, k] */
+    float* M;               /* [T, 2] */
+    float* mi_per_sample;   /* [n_batch] */
+    float* loss;            /* [1] */
+    float* dlogits;         /* [T, E] or NULL */
+    int32_t* expert_offsets;/* [E + 1] or NULL */
+    int32_t* perm_token;    /* [T * k] or NULL */
+    int32_t* perm_inv;      /* [T, k] or NULL */
+    void* out;              /* [T, d] act_dtype: routed experts + shared experts */
+    /* optional stage timing: NULL, or SMOES_N_STAGES + 1 events made by
+     * smoes_events_create; event s is recorded on `stream` before stage s and
+     * the last one after the final stage. */
+    void* const* stage_events;
+} smoes_layer_io;
+
+/* Stages of smoes_moe_forward, in launch order. */
+enum smoes_stage {
+    SMOES_STAGE_ROUTE = 0,    /* router GEMM + softmax + top-k */
+    SMOES_STAGE_MODALITY = 1, /* statistics update (optional) + modality score */
+    SMOES_STAGE_MI = 2,       /* MI partials, loss, gradient */
+    SMOES_STAGE_PERMUTE = 3,  /* expert-contiguous order + work list */
+    SMOES_STAGE_GEMM1 = 4,    /* grouped gate/up GEMM + SwiGLU (routed + shared) */
+    SMOES_STAGE_GEMM2 = 5,    /* grouped down GEMM (routed + shared) */
+    SMOES_STAGE_COMBINE = 6,  /* weighted combine */
+    SMOES_N_STAGES = 7
+};
+
+size_t smoes_workspace_bytes(const smoes_layer* desc);
+
+/*
+ * One SMoES MoE layer forward. Shapes as in the entry points above, plus
+ * inter >= 16, inter % 16 == 0 and shared_inter % 16 == 0. The expert FFN is
+ * SwiGLU: down(silu(gate x) * up x), silu(a) = a / (1 + exp(-a)); the shared
+ * experts (ungated, weight 1) are one SwiGLU of inner size shared_inter.
+ * With SMOES_BF16 the expert GEMMs take bf16 operands with float32
+ * accumulation and the intermediate activations are stored in bf16.
+ */
+int smoes_moe_forward(const smoes_layer* desc, const smoes_layer_io* io,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Timing helpers for stage_events (hipEvent_t handles behind void*).        */
+/* ------------------------------------------------------------------------ */
+
+int smoes_events_create(int n, void** events);
+int smoes_events_destroy(int n, void** events);
+/* Milliseconds between two recorded events (synchronises on `end`). */
+int smoes_event_elapsed_ms(void* start, void* end, float* ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SMOES_H */

@@ -1,0 +1,332 @@
+// C ABI of the SMoES layer: argument validation, workspace layout and the
+// launch sequence on the caller's stream. No call allocates device memory or
+// synchronises the host.
+#include <stdio.h>
+
+#include "../../include/smoes.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace smoes;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+// Carves aligned sub-buffers out of the caller's workspace.
+struct Carver {
+    char* base;
+    size_t used = 0;
+    explicit Carver(void* p) : base(static_cast<char*>(p)) {
+        // align the start inside the workspace
+        const uintptr_t a = reinterpret_cast<uintptr_t>(base);
+        used = (kAlign - (a % kAlign)) % kAlign;
+    }
+    void* take(size_t bytes) {
+        void* p = base + used;
+        used += align_up(bytes, kAlign);
+        return p;
+    }
+};
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? SMOES_OK : SMOES_ERR_HIP; }
+
+bool dtype_ok(int dt) { return dt == SMOES_F32 || dt == SMOES_BF16; }
+
+int check_router_shape(int64_t T, int d, int E, int k) {
+    if (T < 0 || d < 1 || d > SMOES_D_MAX || (d % 8) != 0) return SMOES_ERR_SHAPE;
+    if (E < 1 || E > SMOES_E_MAX) return SMOES_ERR_SHAPE;
+    if (k < 1 || k > E || k > SMOES_K_MAX) return SMOES_ERR_SHAPE;
+    return SMOES_OK;
+}
+
+int check_mi_shape(int64_t T, int E, int n_batch, int n_bins) {
+    if (T < 0 || E < 1 || E > SMOES_E_MAX) return SMOES_ERR_SHAPE;
+    if (n_bins < 1 || n_bins > SMOES_BINS_MAX || (E % n_bins) != 0) return SMOES_ERR_SHAPE;
+    if (n_batch < 1) return SMOES_ERR_SHAPE;
+    return SMOES_OK;
+}
+
+// Total workspace of the standalone entry points (max alignment slack included).
+size_t route_ws(int64_t T, int d, int E, int x_dtype) {
+    (void)T;
+    return router_workspace_bytes(d, E, x_dtype) + 2 * kAlign;
+}
+size_t modality_ws(int64_t T, int d) { return modality_workspace_bytes(T, d) + 2 * kAlign; }
+size_t mi_ws(int64_t T, int E, int n_batch, int n_bins) {
+    return mi_workspace_bytes(T, E, n_batch, n_bins) + 2 * kAlign;
+}
+size_t permute_ws(int64_t T, int E, int k) { return permute_workspace_bytes(T, E, k) + 2 * kAlign; }
+
+hipError_t record(void* const* ev, int s, hipStream_t st) {
+    if (ev == nullptr) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(ev[s]), st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* smoes_status_string(int status) {
+    switch (status) {
+        case SMOES_OK: return "SMOES_OK: success";
+        case SMOES_ERR_ARG: return "SMOES_ERR_ARG: a required pointer is NULL or a scalar/dtype is invalid";
+        case SMOES_ERR_SHAPE: return "SMOES_ERR_SHAPE: inconsistent or unsupported sizes";
+        case SMOES_ERR_WORKSPACE: return "SMOES_ERR_WORKSPACE: workspace smaller than the size query";
+        case SMOES_ERR_HIP: return "SMOES_ERR_HIP: a HIP launch or runtime call failed";
+        default: return "SMOES: unknown status code";
+    }
+}
+
+const char* smoes_version(void) { return "smoes-gfx950 0.1.0"; }
+
+size_t smoes_route_workspace_size(int64_t T, int d, int E, int x_dtype) {
+    return route_ws(T, d, E, x_dtype);
+}
+
+int smoes_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gate,
+                const float* logit_bias, int E, int k, int renorm_topk, float* logits, float* probs,
+                int32_t* topk_idx, float* topk_w, void* workspace, size_t workspace_bytes,
+                void* stream) {
+    if (!dtype_ok(x_dtype)) return SMOES_ERR_ARG;
+    int st = check_router_shape(T, d, E, k);
+    if (st != SMOES_OK) return st;
+    if (T == 0) return SMOES_OK;
+    if (x == nullptr || w_gate == nullptr || probs == nullptr || topk_idx == nullptr || topk_w == nullptr)
+        return SMOES_ERR_ARG;
+    const size_t need = route_ws(T, d, E, x_dtype);
+    if (x_dtype == SMOES_BF16 && (workspace == nullptr || workspace_bytes < need)) return SMOES_ERR_WORKSPACE;
+    Carver c(workspace);
+    void* ws = x_dtype == SMOES_BF16 ? c.take(router_workspace_bytes(d, E, x_dtype)) : nullptr;
+    return hip_status(launch_route(x, x_dtype, T, d, w_gate, logit_bias, E, k, renorm_topk ? 1 : 0,
+                                   logits, probs, topk_idx, topk_w, ws, as_stream(stream)));
+}
+
+size_t smoes_modality_workspace_size(int64_t T, int d) { return modality_ws(T, d); }
+
+int smoes_modality_score(const void* x, int x_dtype, int64_t T, int d, const uint8_t* modality_id,
+                         float* gauss_n, float* gauss_smu, float* gauss_ssig, int update, float beta,
+                         float tau, float var_floor, float* M, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+    if (!dtype_ok(x_dtype)) return SMOES_ERR_ARG;
+    if (T < 0 || d < 1 || d > SMOES_D_MAX || (d % 8) != 0) return SMOES_ERR_SHAPE;
+    if (!(beta >= 0.0f && beta <= 1.0f) || !(var_floor >= 0.0f) || tau != tau) return SMOES_ERR_ARG;
+    if (T == 0) return SMOES_OK;
+    if (x == nullptr || gauss_n == nullptr || gauss_smu == nullptr || gauss_ssig == nullptr || M == nullptr)
+        return SMOES_ERR_ARG;
+    if (update && modality_id == nullptr) return SMOES_ERR_ARG;
+    if (workspace == nullptr || workspace_bytes < modality_ws(T, d)) return SMOES_ERR_WORKSPACE;
+    Carver c(workspace);
+    void* ws = c.take(modality_workspace_bytes(T, d));
+    return hip_status(launch_modality(x, x_dtype, T, d, modality_id, gauss_n, gauss_smu, gauss_ssig,
+                                      update ? 1 : 0, beta, tau, var_floor, M, ws, as_stream(stream)));
+}
+
+size_t smoes_mi_workspace_size(int64_t T, int E, int n_batch, int n_bins) {
+    return mi_ws(T, E, n_batch, n_bins);
+}
+
+int smoes_mi_loss(const float* probs, const float* M, int64_t T, int E, const int32_t* sample_offsets,
+                  int n_batch, const int32_t* expert_to_bin, int n_bins, float grad_scale,
+                  float* mi_per_sample, float* loss, float* dlogits, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+    int st = check_mi_shape(T, E, n_batch, n_bins);
+    if (st != SMOES_OK) return st;
+    if (sample_offsets == nullptr && n_batch != 1) return SMOES_ERR_SHAPE;
+    if (grad_scale != grad_scale) return SMOES_ERR_ARG;
+    if (probs == nullptr || M == nullptr || expert_to_bin == nullptr || mi_per_sample == nullptr ||
+        loss == nullptr)
+        return SMOES_ERR_ARG;
+    if (workspace == nullptr || workspace_bytes < mi_ws(T, E, n_batch, n_bins)) return SMOES_ERR_WORKSPACE;
+    Carver c(workspace);
+    void* ws = c.take(mi_workspace_bytes(T, E, n_batch, n_bins));
+    // T == 0 still defines the outputs (every I_i = 0, loss = 0)
+    return hip_status(launch_mi(probs, M, T, E, sample_offsets, n_batch, expert_to_bin, n_bins,
+                                grad_scale, mi_per_sample, loss, T > 0 ? dlogits : nullptr, ws,
+                                as_stream(stream)));
+}
+
+size_t smoes_permute_workspace_size(int64_t T, int E, int k) { return permute_ws(T, E, k); }
+
+int smoes_permute(const int32_t* topk_idx, int64_t T, int E, int k, int32_t* expert_offsets,
+                  int32_t* perm_token, int32_t* perm_inv, const void* x, int x_dtype, int d,
+                  void* x_perm, void* workspace, size_t workspace_bytes, void* stream) {
+    if (T < 0 || E < 1 || E > SMOES_E_MAX || k < 1 || k > E || k > SMOES_K_MAX) return SMOES_ERR_SHAPE;
+    if (x_perm != nullptr) {
+        if (!dtype_ok(x_dtype)) return SMOES_ERR_ARG;
+        if (d < 1 || d > SMOES_D_MAX || (d % 8) != 0) return SMOES_ERR_SHAPE;
+        if (x == nullptr) return SMOES_ERR_ARG;
+    }
+    if (T * k > INT32_MAX) return SMOES_ERR_SHAPE;
+    if (topk_idx == nullptr || expert_offsets == nullptr || perm_token == nullptr || perm_inv == nullptr)
+        return SMOES_ERR_ARG;
+    if (workspace == nullptr || workspace_bytes < permute_ws(T, E, k)) return SMOES_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    if (T == 0) return hip_status(hipMemsetAsync(expert_offsets, 0, sizeof(int32_t) * (E + 1), s));
+    Carver c(workspace);
+    void* ws = c.take(permute_workspace_bytes(T, E, k));
+    hipError_t err = launch_permute(topk_idx, T, E, k, expert_offsets, perm_token, perm_inv, ws, s);
+    if (err != hipSuccess) return SMOES_ERR_HIP;
+    if (x_perm != nullptr) err = launch_gather_rows(x, x_dtype, d, perm_token, T * k, x_perm, s);
+    return hip_status(err);
+}
+
+// ------------------------------------------------------------------ layer
+
+namespace {
+
+struct LayerWs {
+    float* logits;
+    float* probs_unused;
+    int32_t* offsets;
+    int32_t* perm_token;
+    int32_t* perm_inv;
+    void* route;
+    void* modality;
+    void* mi;
+    void* permute;
+    void* experts;
+};
+
+int check_layer(const smoes_layer* L) {
+    if (L == nullptr) return SMOES_ERR_ARG;
+    if (!dtype_ok(L->act_dtype)) return SMOES_ERR_ARG;
+    int st = check_router_shape(L->T, L->d, L->E, L->k);
+    if (st != SMOES_OK) return st;
+    st = check_mi_shape(L->T, L->E, L->n_batch, L->n_bins);
+    if (st != SMOES_OK) return st;
+    if (L->inter < 16 || (L->inter % 16) != 0) return SMOES_ERR_SHAPE;
+    if (L->shared_inter < 0 || (L->shared_inter % 16) != 0) return SMOES_ERR_SHAPE;
+    if (L->T * L->k > INT32_MAX) return SMOES_ERR_SHAPE;
+    if (!(L->beta >= 0.0f && L->beta <= 1.0f) || !(L->var_floor >= 0.0f) || L->tau != L->tau ||
+        L->grad_scale != L->grad_scale)
+        return SMOES_ERR_ARG;
+    return SMOES_OK;
+}
+
+size_t layer_ws_parts(const smoes_layer* L, LayerWs* out, void* base) {
+    Carver c(base);
+    const int64_t T = L->T;
+    LayerWs w;
+    w.logits = static_cast<float*>(c.take(sizeof(float) * T * L->E));
+    w.probs_unused = nullptr;
+    w.offsets = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 1)));
+    w.perm_token = static_cast<int32_t*>(c.take(sizeof(int32_t) * T * L->k));
+    w.perm_inv = static_cast<int32_t*>(c.take(sizeof(int32_t) * T * L->k));
+    w.route = c.take(router_workspace_bytes(L->d, L->E, L->act_dtype));
+    w.modality = c.take(modality_workspace_bytes(T, L->d));
+    w.mi = c.take(mi_workspace_bytes(T, L->E, L->n_batch, L->n_bins));
+    w.permute = c.take(permute_workspace_bytes(T, L->E, L->k));
+    w.experts = c.take(experts_workspace_bytes(T, L->d, L->E, L->k, L->inter, L->shared_inter, L->act_dtype));
+    if (out != nullptr) *out = w;
+    return c.used + kAlign;
+}
+
+}  // namespace
+
+size_t smoes_workspace_bytes(const smoes_layer* desc) {
+    if (check_layer(desc) != SMOES_OK) return 0;
+    // sizes only: carve from a fake aligned base
+    return layer_ws_parts(desc, nullptr, reinterpret_cast<void*>(static_cast<uintptr_t>(kAlign)));
+}
+
+int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+    int st = check_layer(L);
+    if (st != SMOES_OK) return st;
+    if (io == nullptr) return SMOES_ERR_ARG;
+    if (L->T == 0) return SMOES_OK;
+    if (io->x == nullptr || io->w_gate == nullptr || io->expert_to_bin == nullptr || io->w13 == nullptr ||
+        io->w2 == nullptr || io->gauss_n == nullptr || io->gauss_smu == nullptr ||
+        io->gauss_ssig == nullptr || io->probs == nullptr || io->topk_idx == nullptr ||
+        io->topk_w == nullptr || io->M == nullptr || io->mi_per_sample == nullptr ||
+        io->loss == nullptr || io->out == nullptr)
+        return SMOES_ERR_ARG;
+    if (L->update_stats && io->modality_id == nullptr) return SMOES_ERR_ARG;
+    if (L->shared_inter > 0 && (io->ws13 == nullptr || io->ws2 == nullptr)) return SMOES_ERR_ARG;
+    if (io->sample_offsets == nullptr && L->n_batch != 1) return SMOES_ERR_SHAPE;
+    if (workspace == nullptr || workspace_bytes < smoes_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
+
+    hipStream_t s = as_stream(stream);
+    LayerWs w;
+    layer_ws_parts(L, &w, workspace);
+    const int64_t T = L->T;
+    float* logits = io->logits != nullptr ? io->logits : w.logits;
+    int32_t* offsets = io->expert_offsets != nullptr ? io->expert_offsets : w.offsets;
+    int32_t* perm_token = io->perm_token != nullptr ? io->perm_token : w.perm_token;
+    int32_t* perm_inv = io->perm_inv != nullptr ? io->perm_inv : w.perm_inv;
+    void* const* ev = io->stage_events;
+    hipError_t err;
+#define SMOES_TRY(expr)                          \
+    do {                                         \
+        if ((err = (expr)) != hipSuccess) return SMOES_ERR_HIP; \
+    } while (0)
+
+    SMOES_TRY(record(ev, SMOES_STAGE_ROUTE, s));
+    SMOES_TRY(launch_route(io->x, L->act_dtype, T, L->d, io->w_gate, io->logit_bias, L->E, L->k,
+                           L->renorm_topk ? 1 : 0, logits, io->probs, io->topk_idx, io->topk_w, w.route, s));
+    SMOES_TRY(record(ev, SMOES_STAGE_MODALITY, s));
+    SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
+                              io->gauss_ssig, L->update_stats ? 1 : 0, L->beta, L->tau, L->var_floor,
+                              io->M, w.modality, s));
+    SMOES_TRY(record(ev, SMOES_STAGE_MI, s));
+    SMOES_TRY(launch_mi(io->probs, io->M, T, L->E, io->sample_offsets, L->n_batch, io->expert_to_bin,
+                        L->n_bins, L->grad_scale, io->mi_per_sample, io->loss, io->dlogits, w.mi, s));
+    SMOES_TRY(record(ev, SMOES_STAGE_PERMUTE, s));
+    SMOES_TRY(launch_permute(io->topk_idx, T, L->E, L->k, offsets, perm_token, perm_inv, w.permute, s));
+    ExpertArgs a;
+    a.T = T;
+    a.d = L->d;
+    a.E = L->E;
+    a.k = L->k;
+    a.inter = L->inter;
+    a.shared_inter = L->shared_inter;
+    a.act_dtype = L->act_dtype;
+    a.x = io->x;
+    a.w13 = io->w13;
+    a.w2 = io->w2;
+    a.ws13 = io->ws13;
+    a.ws2 = io->ws2;
+    a.expert_offsets = offsets;
+    a.perm_token = perm_token;
+    a.perm_inv = perm_inv;
+    a.topk_w = io->topk_w;
+    a.out = io->out;
+    SMOES_TRY(record(ev, SMOES_STAGE_GEMM1, s));
+    SMOES_TRY(launch_experts_gemm1(a, w.experts, s));
+    SMOES_TRY(record(ev, SMOES_STAGE_GEMM2, s));
+    SMOES_TRY(launch_experts_gemm2(a, w.experts, s));
+    SMOES_TRY(record(ev, SMOES_STAGE_COMBINE, s));
+    SMOES_TRY(launch_experts_combine(a, w.experts, s));
+    SMOES_TRY(record(ev, SMOES_N_STAGES, s));
+#undef SMOES_TRY
+    return SMOES_OK;
+}
+
+int smoes_events_create(int n, void** events) {
+    if (n < 0 || (n > 0 && events == nullptr)) return SMOES_ERR_ARG;
+    for (int i = 0; i < n; ++i) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return SMOES_ERR_HIP;
+        events[i] = e;
+    }
+    return SMOES_OK;
+}
+
+int smoes_events_destroy(int n, void** events) {
+    if (n < 0 || (n > 0 && events == nullptr)) return SMOES_ERR_ARG;
+    for (int i = 0; i < n; ++i)
+        if (events[i] != nullptr && hipEventDestroy(static_cast<hipEvent_t>(events[i])) != hipSuccess)
+            return SMOES_ERR_HIP;
+    return SMOES_OK;
+}
+
+int smoes_event_elapsed_ms(void* start, void* end, float* ms) {
+    if (start == nullptr || end == nullptr || ms == nullptr) return SMOES_ERR_ARG;
+    if (hipEventSynchronize(static_cast<hipEvent_t>(end)) != hipSuccess) return SMOES_ERR_HIP;
+    return hip_status(hipEventElapsedTime(ms, static_cast<hipEvent_t>(start), static_cast<hipEvent_t>(end)));
+}
+
+}  // extern "C"

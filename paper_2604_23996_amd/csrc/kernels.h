@@ -1,0 +1,62 @@
+// Internal launchers of the SMoES kernels (host side). Every launcher enqueues
+// on `stream` and returns the launch status; sizes are validated by the C ABI
+// layer before any launcher runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace smoes {
+
+// ---------------------------------------------------------------- router
+size_t router_workspace_bytes(int d, int E, int x_dtype);
+size_t router_lds_bytes(int E, int x_dtype);
+hipError_t launch_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gate,
+                        const float* bias, int E, int k, int renorm, float* logits, float* probs,
+                        int32_t* topk_idx, float* topk_w, void* ws, hipStream_t stream);
+
+// ---------------------------------------------------------------- modality score
+size_t modality_workspace_bytes(int64_t T, int d);
+hipError_t launch_modality(const void* x, int x_dtype, int64_t T, int d, const uint8_t* modality_id,
+                           float* gauss_n, float* gauss_smu, float* gauss_ssig, int update,
+                           float beta, float tau, float var_floor, float* M, void* ws,
+                           hipStream_t stream);
+
+// ---------------------------------------------------------------- MI loss
+size_t mi_workspace_bytes(int64_t T, int E, int n_batch, int n_bins);
+hipError_t launch_mi(const float* probs, const float* M, int64_t T, int E,
+                     const int32_t* sample_offsets, int n_batch, const int32_t* expert_to_bin,
+                     int n_bins, float grad_scale, float* mi_per_sample, float* loss,
+                     float* dlogits, void* ws, hipStream_t stream);
+
+// ---------------------------------------------------------------- permutation
+size_t permute_workspace_bytes(int64_t T, int E, int k);
+hipError_t launch_permute(const int32_t* topk_idx, int64_t T, int E, int k,
+                          int32_t* expert_offsets, int32_t* perm_token, int32_t* perm_inv,
+                          void* ws, hipStream_t stream);
+hipError_t launch_gather_rows(const void* x, int x_dtype, int d, const int32_t* perm_token,
+                              int64_t R, void* x_perm, hipStream_t stream);
+
+// ---------------------------------------------------------------- experts
+struct ExpertArgs {
+    int64_t T;
+    int d, E, k, inter, shared_inter, act_dtype;
+    const void* x;
+    const void* w13;
+    const void* w2;
+    const void* ws13;
+    const void* ws2;
+    const int32_t* expert_offsets;  // [E + 1]
+    const int32_t* perm_token;      // [T * k]
+    const int32_t* perm_inv;        // [T, k]
+    const float* topk_w;            // [T, k]
+    void* out;                      // [T, d]
+};
+size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int shared_inter,
+                               int act_dtype);
+hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream);
+hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream);
+hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t stream);
+
+}  // namespace smoes

@@ -1,0 +1,334 @@
+// Inter-bin mutual information between the soft modality score and expert
+// bins (Sec. 3.3-3.4, Eq. 12-15) and its gradient with respect to the router
+// logits.
+//
+// Eq. 12 is linear in the gate, so the per-sample work reduces to the
+// per-expert, per-modality masses A[m][e] = sum_j M_jm g_je and the score
+// totals W[m] = sum_j M_jm; bins only enter in the small finalize step.
+//   mi_partial : (sample, chunk) blocks; threads own expert columns, rows are
+//                split over row groups; fp64 sums, fixed-order LDS reduction.
+//   mi_finalize: one block; chunk partials in chunk order, bin sums in
+//                ascending expert order, then S-bar (Eq. 12), the joint (Eq. 13),
+//                I_i (Eq. 14), the loss (Eq. 15) and the gradient
+//                coefficients c[m][k] = (log r_mk - I_i) / (N_B W_m Z).
+//   mi_grad    : one wave per token; G_k = bin masses of the token,
+//                h_k = sum_m M_jm c[m][k], dlogit_e = s g_e (h_bin(e) - sum_k G_k h_k)
+//                with s = -grad_scale / N_batch.
+// No atomics: every result is reproducible bit for bit.
+#include "common.h"
+#include "kernels.h"
+
+namespace smoes {
+
+namespace {
+
+constexpr int kMiThreads = 256;
+constexpr int kRowsPerChunk = 32;
+
+struct MiWs {
+    double* part;     // [n_batch * C][2E + 2]
+    double* coef;     // [n_batch][2][B]
+    double* mi;       // [n_batch]
+    int32_t* members; // [B][N_B]
+    int C;
+};
+
+int mi_chunks(int64_t T, int n_batch) {
+    int64_t c = ceil_div(T, static_cast<int64_t>(n_batch) * kRowsPerChunk);
+    if (c < 1) c = 1;
+    if (c > 1024) c = 1024;
+    return static_cast<int>(c);
+}
+
+MiWs carve(void* ws, int64_t T, int E, int n_batch, int n_bins) {
+    MiWs w;
+    w.C = mi_chunks(T, n_batch);
+    char* p = static_cast<char*>(ws);
+    w.part = reinterpret_cast<double*>(p);
+    p += align_up(sizeof(double) * static_cast<size_t>(n_batch) * w.C * (2 * E + 2), 256);
+    w.coef = reinterpret_cast<double*>(p);
+    p += align_up(sizeof(double) * static_cast<size_t>(n_batch) * 2 * n_bins, 256);
+    w.mi = reinterpret_cast<double*>(p);
+    p += align_up(sizeof(double) * static_cast<size_t>(n_batch), 256);
+    w.members = reinterpret_cast<int32_t*>(p);
+    return w;
+}
+
+__device__ __forceinline__ void sample_range(const int32_t* off, int64_t T, int i, int64_t& a, int64_t& b) {
+    if (off == nullptr) {
+        a = 0;
+        b = T;
+    } else {
+        a = off[i];
+        b = off[i + 1];
+    }
+}
+
+__global__ void __launch_bounds__(kMiThreads)
+mi_partial_kernel(const float* __restrict__ probs, const float* __restrict__ M, int64_t T, int E,
+                  const int32_t* __restrict__ off, int C, double* __restrict__ part) {
+    __shared__ double red[kMiThreads][2];
+    __shared__ double wred[kMiThreads][2];
+    const int i = blockIdx.y;
+    const int c = blockIdx.x;
+    const int EP = static_cast<int>(ceil_div(E, kWave) * kWave);
+    const int RG = kMiThreads / EP;  // row groups (>= 1 since E <= 256)
+    const int rg = threadIdx.x / EP;
+    const int e = threadIdx.x % EP;
+    int64_t a, b;
+    sample_range(off, T, i, a, b);
+    const int64_t len = b - a;
+    const int64_t L = ceil_div(len, C);
+    const int64_t s0 = a + c * L;
+    const int64_t s1 = s0 + L < b ? s0 + L : b;
+    double a0 = 0.0, a1 = 0.0, w0 = 0.0, w1 = 0.0;
+    if (rg < RG) {
+        for (int64_t j = s0 + rg; j < s1; j += RG) {
+            const float2 mj = *reinterpret_cast<const float2*>(M + 2 * j);
+            const double m0 = mj.x, m1 = mj.y;
+            if (e < E) {
+                const double g = probs[j * E + e];
+                a0 = fma(m0, g, a0);
+                a1 = fma(m1, g, a1);
+            }
+            w0 += m0;
+            w1 += m1;
+        }
+    }
+    red[threadIdx.x][0] = a0;
+    red[threadIdx.x][1] = a1;
+    wred[threadIdx.x][0] = w0;
+    wred[threadIdx.x][1] = w1;
+    __syncthreads();
+    double* out = part + (static_cast<int64_t>(i) * C + c) * (2 * E + 2);
+    if (rg == 0) {
+        double s_0 = 0.0, s_1 = 0.0;
+        for (int r = 0; r < RG; ++r) {
+            s_0 += red[r * EP + e][0];
+            s_1 += red[r * EP + e][1];
+        }
+        if (e < E) {
+            out[e] = s_0;
+            out[E + e] = s_1;
+        }
+        if (e == 0) {
+            double t0 = 0.0, t1 = 0.0;
+            for (int r = 0; r < RG; ++r) {
+                t0 += wred[r * EP][0];
+                t1 += wred[r * EP][1];
+            }
+            out[2 * E] = t0;
+            out[2 * E + 1] = t1;
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kMiThreads)
+mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batch, int C,
+                   const int32_t* __restrict__ e2b, int n_bins, const double* __restrict__ part,
+                   double* __restrict__ coef, double* __restrict__ mi64, int32_t* __restrict__ members,
+                   float* __restrict__ mi_per_sample, float* __restrict__ loss) {
+    __shared__ double A[2][256];
+    __shared__ double Abin[2][64];
+    __shared__ double Wm[2];
+    __shared__ int32_t mem[256];
+    const int NB = E / n_bins;
+    // bin member lists in ascending expert order
+    if (threadIdx.x < n_bins) {
+        const int k = threadIdx.x;
+        int n = 0;
+        for (int e = 0; e < E; ++e)
+            if (e2b[e] == k && n < NB) {
+                mem[k * NB + n] = e;
+                members[k * NB + n] = e;
+                ++n;
+            }
+        for (; n < NB; ++n) {  // violated precondition: pad with expert 0 of the bin list
+            mem[k * NB + n] = -1;
+            members[k * NB + n] = -1;
+        }
+    }
+    __syncthreads();
+    for (int i = 0; i < n_batch; ++i) {
+        int64_t a, b;
+        sample_range(off, T, i, a, b);
+        const double* pi = part + static_cast<int64_t>(i) * C * (2 * E + 2);
+        for (int e = threadIdx.x; e < E; e += blockDim.x) {
+            double s0 = 0.0, s1 = 0.0;
+            for (int c = 0; c < C; ++c) {
+                s0 += pi[c * (2 * E + 2) + e];
+                s1 += pi[c * (2 * E + 2) + E + e];
+            }
+            A[0][e] = s0;
+            A[1][e] = s1;
+        }
+        if (threadIdx.x == 0) {
+            double t0 = 0.0, t1 = 0.0;
+            for (int c = 0; c < C; ++c) {
+                t0 += pi[c * (2 * E + 2) + 2 * E];
+                t1 += pi[c * (2 * E + 2) + 2 * E + 1];
+            }
+            Wm[0] = t0;
+            Wm[1] = t1;
+        }
+        __syncthreads();
+        if (threadIdx.x < 2 * n_bins) {
+            const int m = threadIdx.x / n_bins, k = threadIdx.x % n_bins;
+            double s = 0.0;
+            for (int n = 0; n < NB; ++n) {
+                const int e = mem[k * NB + n];
+                if (e >= 0) s += A[m][e];
+            }
+            Abin[m][k] = s;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            double S[2][64];
+            double Z = 0.0;
+            for (int m = 0; m < 2; ++m)
+                for (int k = 0; k < n_bins; ++k) {
+                    S[m][k] = (b > a && Wm[m] > 0.0) ? Abin[m][k] / (static_cast<double>(NB) * Wm[m]) : 0.0;
+                    Z += S[m][k];
+                }
+            double Pm[2] = {0.0, 0.0};
+            double Pk[64];
+            for (int k = 0; k < n_bins; ++k) Pk[k] = 0.0;
+            for (int m = 0; m < 2; ++m)
+                for (int k = 0; k < n_bins; ++k) {
+                    S[m][k] = Z > 0.0 ? S[m][k] / Z : 0.0;  // now P(m, k)
+                    Pm[m] += S[m][k];
+                    Pk[k] += S[m][k];
+                }
+            double I = 0.0;
+            for (int m = 0; m < 2; ++m)
+                for (int k = 0; k < n_bins; ++k)
+                    if (S[m][k] > 0.0) I += S[m][k] * log(S[m][k] / (Pm[m] * Pk[k]));
+            for (int m = 0; m < 2; ++m)
+                for (int k = 0; k < n_bins; ++k) {
+                    double cv = 0.0;
+                    if (Wm[m] > 0.0 && S[m][k] > 0.0)
+                        cv = (log(S[m][k] / (Pm[m] * Pk[k])) - I) / (static_cast<double>(NB) * Wm[m] * Z);
+                    coef[(static_cast<int64_t>(i) * 2 + m) * n_bins + k] = cv;
+                }
+            mi64[i] = I;
+            mi_per_sample[i] = static_cast<float>(I);
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        double s = 0.0;
+        for (int i = 0; i < n_batch; ++i) s += mi64[i];
+        loss[0] = static_cast<float>(-s / n_batch);
+    }
+}
+
+__global__ void __launch_bounds__(kMiThreads)
+mi_grad_kernel(const float* __restrict__ probs, const float* __restrict__ M, int64_t T, int E,
+               const int32_t* __restrict__ off, int n_batch, const int32_t* __restrict__ e2b,
+               int n_bins, const int32_t* __restrict__ members, const double* __restrict__ coef,
+               double scale, float* __restrict__ dlogits) {
+    constexpr int kWaves = kMiThreads / kWave;
+    __shared__ float gl[kWaves][256];
+    __shared__ double hl[kWaves][64];
+    __shared__ int32_t mem[256];
+    __shared__ int32_t bin[256];
+    const int wave = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int NB = E / n_bins;
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        mem[e] = members[e];
+        bin[e] = e2b[e];
+    }
+    const int QE = static_cast<int>(ceil_div(E, kWave));
+    const int64_t per_iter = static_cast<int64_t>(gridDim.x) * kWaves;
+    const int64_t iters = ceil_div(T, per_iter);
+    __syncthreads();
+    for (int64_t it = 0; it < iters; ++it) {
+        const int64_t j = it * per_iter + static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+        const bool live = j < T;
+        float g[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        int si = 0;
+        if (live) {
+            if (off != nullptr) {  // sample of token j: last i with off[i] <= j
+                int lo = 0, hi = n_batch - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (off[mid] <= j) lo = mid; else hi = mid - 1;
+                }
+                si = lo;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e = lane + q * kWave;
+                if (q < QE && e < E) {
+                    g[q] = probs[j * E + e];
+                    gl[wave][e] = g[q];
+                }
+            }
+        }
+        __syncthreads();
+        double gh = 0.0;
+        if (live && lane < n_bins) {
+            double G = 0.0;
+            for (int n = 0; n < NB; ++n) {
+                const int e = mem[lane * NB + n];
+                if (e >= 0) G += static_cast<double>(gl[wave][e]);
+            }
+            const float2 mj = *reinterpret_cast<const float2*>(M + 2 * j);
+            const double* cf = coef + static_cast<int64_t>(si) * 2 * n_bins;
+            const double h = static_cast<double>(mj.x) * cf[lane] + static_cast<double>(mj.y) * cf[n_bins + lane];
+            hl[wave][lane] = h;
+            gh = G * h;
+        }
+        gh = wave_sum(gh);
+        __syncthreads();
+        if (live) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e = lane + q * kWave;
+                if (q < QE && e < E) {
+                    const double dv = scale * static_cast<double>(g[q]) * (hl[wave][bin[e]] - gh);
+                    dlogits[j * E + e] = static_cast<float>(dv);
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+size_t mi_workspace_bytes(int64_t T, int E, int n_batch, int n_bins) {
+    const int C = mi_chunks(T, n_batch);
+    return align_up(sizeof(double) * static_cast<size_t>(n_batch) * C * (2 * E + 2), 256) +
+           align_up(sizeof(double) * static_cast<size_t>(n_batch) * 2 * n_bins, 256) +
+           align_up(sizeof(double) * static_cast<size_t>(n_batch), 256) +
+           align_up(sizeof(int32_t) * static_cast<size_t>(E), 256);
+}
+
+hipError_t launch_mi(const float* probs, const float* M, int64_t T, int E,
+                     const int32_t* sample_offsets, int n_batch, const int32_t* expert_to_bin,
+                     int n_bins, float grad_scale, float* mi_per_sample, float* loss,
+                     float* dlogits, void* ws, hipStream_t stream) {
+    MiWs w = carve(ws, T, E, n_batch, n_bins);
+    hipError_t err;
+    hipLaunchKernelGGL(mi_partial_kernel, dim3(w.C, n_batch), dim3(kMiThreads), 0, stream, probs, M,
+                       T, E, sample_offsets, w.C, w.part);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    hipLaunchKernelGGL(mi_finalize_kernel, dim3(1), dim3(kMiThreads), 0, stream, T, E,
+                       sample_offsets, n_batch, w.C, expert_to_bin, n_bins, w.part, w.coef, w.mi,
+                       w.members, mi_per_sample, loss);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if (dlogits != nullptr) {
+        int64_t blocks = ceil_div(T, kMiThreads / kWave);
+        if (blocks > 2048) blocks = 2048;
+        const double scale = -static_cast<double>(grad_scale) / n_batch;
+        hipLaunchKernelGGL(mi_grad_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kMiThreads), 0,
+                           stream, probs, M, T, E, sample_offsets, n_batch, expert_to_bin, n_bins,
+                           w.members, w.coef, scale, dlogits);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    return hipSuccess;
+}
+
+}  // namespace smoes

@@ -1,0 +1,311 @@
+"""Python binding of libsmoes.so (ctypes; argument marshalling only).
+
+Every function takes and returns torch tensors on the current HIP device and
+enqueues on torch's current stream; all arithmetic runs in the HIP kernels of
+libsmoes.so. There is no fallback: if the library is missing this module
+raises when it is used.
+
+Names follow the C ABI in include/smoes.h: route, modality_score, mi_loss,
+permute, moe_forward (+ workspace helpers and the layer descriptor).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from dataclasses import dataclass
+from typing import Dict, Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsmoes.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "smoes.h")
+
+SMOES_OK, SMOES_ERR_ARG, SMOES_ERR_SHAPE, SMOES_ERR_WORKSPACE, SMOES_ERR_HIP = 0, -1, -2, -3, -4
+SMOES_F32, SMOES_BF16 = 0, 1
+N_STAGES = 7
+STAGES = ("route", "modality", "mi", "permute", "gemm1", "gemm2", "combine")
+
+_lib = None
+
+
+class SmoesError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+c_i64, c_int, c_float, c_size, c_void = ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_void_p
+
+
+class SmoesLayer(ctypes.Structure):
+    _fields_ = [("T", c_i64), ("d", c_int), ("E", c_int), ("k", c_int), ("inter", c_int),
+                ("shared_inter", c_int), ("n_bins", c_int), ("n_batch", c_int), ("act_dtype", c_int),
+                ("tau", c_float), ("beta", c_float), ("var_floor", c_float), ("grad_scale", c_float),
+                ("renorm_topk", c_int), ("update_stats", c_int)]
+
+
+_IO_FIELDS = ["x", "modality_id", "sample_offsets", "w_gate", "logit_bias", "expert_to_bin", "w13",
+              "w2", "ws13", "ws2", "gauss_n", "gauss_smu", "gauss_ssig", "logits", "probs", "topk_idx",
+              "topk_w", "M", "mi_per_sample", "loss", "dlogits", "expert_offsets", "perm_token",
+              "perm_inv", "out", "stage_events"]
+
+
+class SmoesLayerIO(ctypes.Structure):
+    _fields_ = [(n, c_void) for n in _IO_FIELDS]
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsmoes.so (built by paper_2604_23996_amd.build); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2604_23996_amd.build` "
+                              "(there is no fallback path)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.smoes_status_string.restype = ctypes.c_char_p
+        L.smoes_status_string.argtypes = [c_int]
+        L.smoes_version.restype = ctypes.c_char_p
+        L.smoes_route_workspace_size.restype = c_size
+        L.smoes_route_workspace_size.argtypes = [c_i64, c_int, c_int, c_int]
+        L.smoes_route.restype = c_int
+        L.smoes_route.argtypes = [c_void, c_int, c_i64, c_int, c_void, c_void, c_int, c_int, c_int,
+                                  c_void, c_void, c_void, c_void, c_void, c_size, c_void]
+        L.smoes_modality_workspace_size.restype = c_size
+        L.smoes_modality_workspace_size.argtypes = [c_i64, c_int]
+        L.smoes_modality_score.restype = c_int
+        L.smoes_modality_score.argtypes = [c_void, c_int, c_i64, c_int, c_void, c_void, c_void, c_void,
+                                           c_int, c_float, c_float, c_float, c_void, c_void, c_size, c_void]
+        L.smoes_mi_workspace_size.restype = c_size
+        L.smoes_mi_workspace_size.argtypes = [c_i64, c_int, c_int, c_int]
+        L.smoes_mi_loss.restype = c_int
+        L.smoes_mi_loss.argtypes = [c_void, c_void, c_i64, c_int, c_void, c_int, c_void, c_int, c_float,
+                                    c_void, c_void, c_void, c_void, c_size, c_void]
+        L.smoes_permute_workspace_size.restype = c_size
+        L.smoes_permute_workspace_size.argtypes = [c_i64, c_int, c_int]
+        L.smoes_permute.restype = c_int
+        L.smoes_permute.argtypes = [c_void, c_i64, c_int, c_int, c_void, c_void, c_void, c_void, c_int,
+                                    c_int, c_void, c_void, c_size, c_void]
+        L.smoes_workspace_bytes.restype = c_size
+        L.smoes_workspace_bytes.argtypes = [ctypes.POINTER(SmoesLayer)]
+        L.smoes_moe_forward.restype = c_int
+        L.smoes_moe_forward.argtypes = [ctypes.POINTER(SmoesLayer), ctypes.POINTER(SmoesLayerIO),
+                                        c_void, c_size, c_void]
+        L.smoes_events_create.restype = c_int
+        L.smoes_events_create.argtypes = [c_int, ctypes.POINTER(c_void)]
+        L.smoes_events_destroy.restype = c_int
+        L.smoes_events_destroy.argtypes = [c_int, ctypes.POINTER(c_void)]
+        L.smoes_event_elapsed_ms.restype = c_int
+        L.smoes_event_elapsed_ms.argtypes = [c_void, c_void, ctypes.POINTER(c_float)]
+        _lib = L
+    return _lib
+
+
+def header_functions() -> Sequence[str]:
+    """Names of the functions include/smoes.h declares."""
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(smoes_[a-z_0-9]+)\s*\(", text)))
+
+
+def status_string(status: int) -> str:
+    return lib().smoes_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != SMOES_OK:
+        raise SmoesError(status, where)
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libsmoes must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SMOES_BF16
+    if t.dtype == torch.float32:
+        return SMOES_F32
+    raise TypeError(f"unsupported activation dtype {t.dtype}")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------- entry points
+
+def route(x: torch.Tensor, w_gate: torch.Tensor, k: int, logit_bias: Optional[torch.Tensor] = None,
+          renorm_topk: bool = False, want_logits: bool = True) -> Dict[str, torch.Tensor]:
+    T, d = x.shape
+    E = w_gate.shape[0]
+    dev = x.device
+    logits = torch.empty((T, E), dtype=torch.float32, device=dev) if want_logits else None
+    probs = torch.empty((T, E), dtype=torch.float32, device=dev)
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = torch.empty((T, k), dtype=torch.float32, device=dev)
+    dt = _dtype_code(x)
+    nbytes = lib().smoes_route_workspace_size(T, d, E, dt)
+    ws = _workspace(nbytes, dev)
+    _check(lib().smoes_route(_p(x), dt, T, d, _p(w_gate), _p(logit_bias), E, k, int(renorm_topk),
+                             _p(logits), _p(probs), _p(idx), _p(w), _p(ws), nbytes, _stream()),
+           "smoes_route")
+    return {"logits": logits, "probs": probs, "topk_idx": idx, "topk_w": w}
+
+
+def modality_score(x: torch.Tensor, gauss_n: torch.Tensor, gauss_smu: torch.Tensor,
+                   gauss_ssig: torch.Tensor, modality_id: Optional[torch.Tensor] = None,
+                   update: bool = False, beta: float = 0.99, tau: float = 0.0,
+                   var_floor: float = 1e-6) -> torch.Tensor:
+    """Soft modality scores [T, 2]; with update=True the state tensors are updated in place."""
+    T, d = x.shape
+    M = torch.empty((T, 2), dtype=torch.float32, device=x.device)
+    nbytes = lib().smoes_modality_workspace_size(T, d)
+    ws = _workspace(nbytes, x.device)
+    _check(lib().smoes_modality_score(_p(x), _dtype_code(x), T, d, _p(modality_id), _p(gauss_n),
+                                      _p(gauss_smu), _p(gauss_ssig), int(update), beta, tau, var_floor,
+                                      _p(M), _p(ws), nbytes, _stream()), "smoes_modality_score")
+    return M
+
+
+def mi_loss(probs: torch.Tensor, M: torch.Tensor, sample_offsets: Optional[torch.Tensor],
+            expert_to_bin: torch.Tensor, n_bins: int, grad_scale: float = 1.0,
+            want_grad: bool = True):
+    """Returns (mi_per_sample [n_batch], loss [1], dlogits [T, E] or None)."""
+    T, E = probs.shape
+    n_batch = 1 if sample_offsets is None else sample_offsets.numel() - 1
+    dev = probs.device
+    mi = torch.empty(n_batch, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    dl = torch.empty((T, E), dtype=torch.float32, device=dev) if want_grad else None
+    nbytes = lib().smoes_mi_workspace_size(T, E, n_batch, n_bins)
+    ws = _workspace(nbytes, dev)
+    _check(lib().smoes_mi_loss(_p(probs), _p(M), T, E, _p(sample_offsets), n_batch, _p(expert_to_bin),
+                               n_bins, grad_scale, _p(mi), _p(loss), _p(dl), _p(ws), nbytes, _stream()),
+           "smoes_mi_loss")
+    return mi, loss, dl
+
+
+def permute(topk_idx: torch.Tensor, E: int, x: Optional[torch.Tensor] = None):
+    """Returns (expert_offsets [E+1], perm_token [T*k], perm_inv [T, k], x_perm or None)."""
+    T, k = topk_idx.shape
+    dev = topk_idx.device
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    perm = torch.empty(T * k, dtype=torch.int32, device=dev)
+    inv = torch.empty((T, k), dtype=torch.int32, device=dev)
+    xp = None
+    dt, d = SMOES_F32, 8
+    if x is not None:
+        d = x.shape[1]
+        dt = _dtype_code(x)
+        xp = torch.empty((T * k, d), dtype=x.dtype, device=dev)
+    nbytes = lib().smoes_permute_workspace_size(T, E, k)
+    ws = _workspace(nbytes, dev)
+    _check(lib().smoes_permute(_p(topk_idx), T, E, k, _p(off), _p(perm), _p(inv), _p(x), dt, d, _p(xp),
+                               _p(ws), nbytes, _stream()), "smoes_permute")
+    return off, perm, inv, xp
+
+
+# ---------------------------------------------------------------- whole layer
+
+@dataclass
+class LayerSpec:
+    T: int
+    d: int
+    E: int
+    k: int
+    inter: int
+    shared_inter: int
+    n_bins: int
+    n_batch: int
+    act_dtype: int
+    tau: float = 0.0
+    beta: float = 0.99
+    var_floor: float = 1e-6
+    grad_scale: float = 1.0
+    renorm_topk: bool = False
+    update_stats: bool = False
+
+    def c(self) -> SmoesLayer:
+        return SmoesLayer(self.T, self.d, self.E, self.k, self.inter, self.shared_inter, self.n_bins,
+                          self.n_batch, self.act_dtype, self.tau, self.beta, self.var_floor,
+                          self.grad_scale, int(self.renorm_topk), int(self.update_stats))
+
+
+def workspace_bytes(spec: LayerSpec) -> int:
+    desc = spec.c()
+    return int(lib().smoes_workspace_bytes(ctypes.byref(desc)))
+
+
+class Events:
+    """SMOES_N_STAGES + 1 HIP events for the forward's stage timing."""
+
+    def __init__(self, n: int = N_STAGES + 1):
+        self.n = n
+        self.arr = (c_void * n)()
+        _check(lib().smoes_events_create(n, self.arr), "smoes_events_create")
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = c_float()
+        _check(lib().smoes_event_elapsed_ms(self.arr[a], self.arr[b], ctypes.byref(ms)), "smoes_event_elapsed_ms")
+        return float(ms.value)
+
+    def close(self):
+        if self.arr is not None:
+            lib().smoes_events_destroy(self.n, self.arr)
+            self.arr = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def alloc_outputs(spec: LayerSpec, device, act_torch_dtype, want_logits=True, want_dlogits=True,
+                  want_perm=True) -> Dict[str, torch.Tensor]:
+    T, E, k = spec.T, spec.E, spec.k
+    f = dict(dtype=torch.float32, device=device)
+    i = dict(dtype=torch.int32, device=device)
+    return {
+        "logits": torch.empty((T, E), **f) if want_logits else None,
+        "probs": torch.empty((T, E), **f),
+        "topk_idx": torch.empty((T, k), **i),
+        "topk_w": torch.empty((T, k), **f),
+        "M": torch.empty((T, 2), **f),
+        "mi_per_sample": torch.empty(spec.n_batch, **f),
+        "loss": torch.empty(1, **f),
+        "dlogits": torch.empty((T, E), **f) if want_dlogits else None,
+        "expert_offsets": torch.empty(E + 1, **i) if want_perm else None,
+        "perm_token": torch.empty(T * k, **i) if want_perm else None,
+        "perm_inv": torch.empty((T, k), **i) if want_perm else None,
+        "out": torch.empty((T, spec.d), dtype=act_torch_dtype, device=device),
+    }
+
+
+def moe_forward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
+                outputs: Dict[str, Optional[torch.Tensor]], workspace: torch.Tensor,
+                events: Optional[Events] = None) -> Dict[str, Optional[torch.Tensor]]:
+    """One layer forward. `inputs` holds x, modality_id, sample_offsets, w_gate,
+    logit_bias, expert_to_bin, w13, w2, ws13, ws2, gauss_n, gauss_smu, gauss_ssig
+    (the Gaussian state is updated in place when spec.update_stats)."""
+    desc = spec.c()
+    io = SmoesLayerIO()
+    for name in _IO_FIELDS:
+        if name == "stage_events":
+            continue
+        t = inputs.get(name) if name in inputs else outputs.get(name)
+        setattr(io, name, None if t is None else _p(t).value)
+    io.stage_events = ctypes.cast(events.arr, c_void).value if events is not None else None
+    _check(lib().smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), _p(workspace),
+                                   workspace.numel(), _stream()), "smoes_moe_forward")
+    return outputs

@@ -1,0 +1,114 @@
+"""Shared helpers of the GPU parity tests: moving the seeded inputs to the
+device, running the oracle on the same arrays, and the tolerance checks."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle as O
+from paper_2604_23996_amd import smoes as S
+from paper_2604_23996_amd import workloads as W
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    """Name the case before a GPU step (flushed, so a crash still shows it)."""
+    print("[gpu]", *a, file=sys.stderr, flush=True)
+
+
+def t(a: np.ndarray, dtype=None) -> torch.Tensor:
+    """numpy -> device tensor; uint16 arrays are bf16 bit patterns."""
+    if a is None:
+        return None
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
+    x = torch.from_numpy(a)
+    if dtype is not None:
+        x = x.to(dtype)
+    return x.to(DEV)
+
+
+def host(x: torch.Tensor) -> np.ndarray:
+    if x.dtype == torch.bfloat16:
+        return W.bf16_bits_to_f32(x.view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+    return x.cpu().numpy()
+
+
+def rel_err(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = np.linalg.norm(b.ravel())
+    return np.linalg.norm((a - b).ravel()) / (den if den > 0 else 1.0)
+
+
+def check_topk(idx_gpu, idx_ref, z_ref, k, gap_tol=1e-4):
+    """Bit-exact top-k wherever the oracle's k-th vs (k+1)-th logit gap exceeds
+    gap_tol; elsewhere every chosen expert must be a valid choice (its logit
+    within gap_tol of the k-th largest). Returns the mask of clear tokens."""
+    gap = O.topk_gap(z_ref, k)
+    clear = gap > gap_tol
+    assert np.array_equal(idx_gpu[clear], idx_ref[clear]), \
+        f"top-k mismatch on {np.sum(np.any(idx_gpu[clear] != idx_ref[clear], axis=1))} clear tokens"
+    if (~clear).any():
+        zs = -np.sort(-z_ref[~clear], axis=1)
+        kth = zs[:, k - 1]
+        chosen = np.take_along_axis(z_ref[~clear], idx_gpu[~clear].astype(np.int64), axis=1)
+        assert np.all(chosen >= kth[:, None] - gap_tol)
+        for row in idx_gpu[~clear]:
+            assert len(set(row.tolist())) == k
+    return clear
+
+
+def gauss_state_dev(d):
+    return (torch.zeros(2, dtype=torch.float32, device=DEV),
+            torch.zeros((2, d), dtype=torch.float32, device=DEV),
+            torch.zeros((2, d), dtype=torch.float32, device=DEV))
+
+
+def layer_spec(cfg: W.LayerConfig, T=None, **kw) -> S.LayerSpec:
+    return S.LayerSpec(T=cfg.T if T is None else T, d=cfg.d, E=cfg.E, k=cfg.k, inter=cfg.inter,
+                       shared_inter=cfg.shared_inter, n_bins=cfg.n_bins, n_batch=cfg.n_batch,
+                       act_dtype=S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32,
+                       tau=cfg.tau, beta=cfg.beta, **kw)
+
+
+def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None):
+    """The full layer through smoes_moe_forward. For layers that do not update
+    their statistics in the call, the Gaussian state is first estimated from
+    the batch by smoes_modality_score(update=1) from the zero state."""
+    cfg = inp.cfg
+    upd = cfg.update_stats if update_stats is None else update_stats
+    spec = layer_spec(cfg, update_stats=upd)
+    dev_in = {
+        "x": t(inp.x), "modality_id": t(inp.modality_id), "sample_offsets": t(inp.sample_offsets),
+        "w_gate": t(inp.w_gate if w_gate is None else w_gate), "logit_bias": t(inp.logit_bias),
+        "expert_to_bin": t(inp.expert_to_bin), "w13": t(inp.w13), "w2": t(inp.w2),
+        "ws13": t(inp.ws13), "ws2": t(inp.ws2),
+    }
+    n, smu, ssig = gauss_state_dev(cfg.d)
+    if not upd:
+        S.modality_score(dev_in["x"], n, smu, ssig, dev_in["modality_id"], update=True, beta=cfg.beta,
+                         tau=cfg.tau)
+    dev_in.update(gauss_n=n, gauss_smu=smu, gauss_ssig=ssig)
+    act = torch.bfloat16 if cfg.dtype == W.BF16 else torch.float32
+    outs = S.alloc_outputs(spec, DEV, act)
+    ws = torch.empty(S.workspace_bytes(spec), dtype=torch.uint8, device=DEV)
+    S.moe_forward(spec, dev_in, outs, ws, events=events)
+    torch.cuda.synchronize()
+    return spec, dev_in, outs
+
+
+def run_oracle_layer(inp: W.LayerInputs, w_gate=None, rows=None, update_stats=None):
+    cfg = inp.cfg
+    upd = cfg.update_stats if update_stats is None else update_stats
+    st = O.GaussState.zeros(cfg.d)
+    if not upd:
+        st = O.gauss_update(st, inp.x, inp.modality_id, cfg.beta)
+    return O.layer_forward(inp.x, inp.modality_id, inp.sample_offsets,
+                           inp.w_gate if w_gate is None else w_gate, inp.logit_bias,
+                           inp.expert_to_bin, cfg.n_bins, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
+                           st, update_stats=upd, beta=cfg.beta, tau=cfg.tau, rows=rows)

@@ -1,0 +1,131 @@
+"""The C ABI library: it loads, exports every function include/smoes.h
+declares, and rejects bad arguments on the host before touching the GPU.
+None of these calls launches a kernel, so they run without a GPU."""
+import ctypes
+import os
+
+import pytest
+
+from paper_2604_23996_amd import smoes as S
+
+pytestmark = pytest.mark.skipif(not os.path.exists(S.LIB_PATH), reason="libsmoes.so not built")
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+
+
+def test_exports_every_declared_function():
+    names = S.header_functions()
+    assert {"smoes_route", "smoes_modality_score", "smoes_mi_loss", "smoes_permute",
+            "smoes_moe_forward", "smoes_workspace_bytes"} <= set(names)
+    L = S.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4):
+        s = S.status_string(code)
+        assert s.startswith("SMOES_")
+    assert "unknown" in S.status_string(-99)
+
+
+def test_route_argument_checks():
+    L = S.lib()
+    # null x
+    assert L.smoes_route(None, 1, 10, 64, FAKE, None, 8, 2, 0, None, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == S.SMOES_ERR_ARG
+    # bad dtype
+    assert L.smoes_route(FAKE, 7, 10, 64, FAKE, None, 8, 2, 0, None, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == S.SMOES_ERR_ARG
+    # d not a multiple of 8, k > E, k > K_MAX, E > E_MAX
+    for (d, E, k) in ((63, 8, 2), (64, 8, 9), (64, 64, 17), (64, 257, 2), (0, 8, 2)):
+        assert L.smoes_route(FAKE, 1, 10, d, FAKE, None, E, k, 0, None, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == S.SMOES_ERR_SHAPE
+    # workspace too small (bf16 needs the split router weights)
+    need = L.smoes_route_workspace_size(10, 64, 8, 1)
+    assert need > 0
+    assert L.smoes_route(FAKE, 1, 10, 64, FAKE, None, 8, 2, 0, None, FAKE, FAKE, FAKE, FAKE, need - 1, None) == S.SMOES_ERR_WORKSPACE
+    # T = 0 is a no-op success, even with null buffers
+    assert L.smoes_route(None, 1, 0, 64, None, None, 8, 2, 0, None, None, None, None, None, 0, None) == S.SMOES_OK
+
+
+def test_modality_argument_checks():
+    L = S.lib()
+    ws = L.smoes_modality_workspace_size(10, 64)
+    args = lambda **kw: dict(dict(x=FAKE, dt=1, T=10, d=64, mid=FAKE, n=FAKE, smu=FAKE, ssig=FAKE,
+                                   upd=1, beta=0.99, tau=0.0, vf=1e-6, M=FAKE, ws=FAKE, wsb=ws), **kw)
+    call = lambda a: L.smoes_modality_score(a["x"], a["dt"], a["T"], a["d"], a["mid"], a["n"], a["smu"],
+                                            a["ssig"], a["upd"], a["beta"], a["tau"], a["vf"], a["M"],
+                                            a["ws"], a["wsb"], None)
+    assert call(args(mid=None)) == S.SMOES_ERR_ARG  # update needs modality ids
+    assert call(args(beta=1.5)) == S.SMOES_ERR_ARG
+    assert call(args(vf=-1.0)) == S.SMOES_ERR_ARG
+    assert call(args(d=20)) == S.SMOES_ERR_SHAPE
+    assert call(args(wsb=ws - 1)) == S.SMOES_ERR_WORKSPACE
+    assert call(args(M=None)) == S.SMOES_ERR_ARG
+    assert call(args(T=0, x=None)) == S.SMOES_OK
+
+
+def test_mi_argument_checks():
+    L = S.lib()
+    ws = L.smoes_mi_workspace_size(10, 8, 2, 2)
+    call = lambda E=8, nb=2, bins=2, off=FAKE, wsb=ws, probs=FAKE: L.smoes_mi_loss(
+        probs, FAKE, 10, E, off, nb, FAKE, bins, 1.0, FAKE, FAKE, None, FAKE, wsb, None)
+    assert call(bins=3) == S.SMOES_ERR_SHAPE  # E % n_bins
+    assert call(bins=65, E=130) == S.SMOES_ERR_SHAPE
+    assert call(nb=0) == S.SMOES_ERR_SHAPE
+    assert call(off=None) == S.SMOES_ERR_SHAPE  # several samples need offsets
+    assert call(probs=None) == S.SMOES_ERR_ARG
+    assert call(wsb=ws - 1) == S.SMOES_ERR_WORKSPACE
+
+
+def test_permute_argument_checks():
+    L = S.lib()
+    ws = L.smoes_permute_workspace_size(10, 8, 2)
+    call = lambda E=8, k=2, idx=FAKE, xp=None, x=FAKE, d=64, wsb=ws: L.smoes_permute(
+        idx, 10, E, k, FAKE, FAKE, FAKE, x, 1, d, xp, FAKE, wsb, None)
+    assert call(k=9) == S.SMOES_ERR_SHAPE
+    assert call(idx=None) == S.SMOES_ERR_ARG
+    assert call(xp=FAKE, x=None) == S.SMOES_ERR_ARG
+    assert call(xp=FAKE, d=12) == S.SMOES_ERR_SHAPE
+    assert call(wsb=ws - 1) == S.SMOES_ERR_WORKSPACE
+
+
+def _spec(**kw):
+    base = dict(T=300, d=128, E=16, k=4, inter=96, shared_inter=96, n_bins=4, n_batch=2, act_dtype=1)
+    base.update(kw)
+    return S.LayerSpec(**base)
+
+
+def test_layer_workspace_and_checks():
+    L = S.lib()
+    assert S.workspace_bytes(_spec()) > 0
+    for bad in (dict(inter=100), dict(inter=0), dict(shared_inter=24), dict(n_bins=3), dict(k=17),
+                dict(d=100), dict(act_dtype=5), dict(beta=2.0)):
+        assert S.workspace_bytes(_spec(**bad)) == 0, bad
+    desc = _spec().c()
+    io = S.SmoesLayerIO()
+    assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, 1 << 30, None) == S.SMOES_ERR_ARG
+    assert L.smoes_moe_forward(None, ctypes.byref(io), FAKE, 1 << 30, None) == S.SMOES_ERR_ARG
+    # every required pointer present but the workspace too small
+    for name in ("x", "w_gate", "expert_to_bin", "w13", "w2", "ws13", "ws2", "gauss_n", "gauss_smu",
+                 "gauss_ssig", "probs", "topk_idx", "topk_w", "M", "mi_per_sample", "loss", "out",
+                 "sample_offsets"):
+        setattr(io, name, 0x1000)
+    need = S.workspace_bytes(_spec())
+    assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, need - 1, None) == S.SMOES_ERR_WORKSPACE
+    # shared experts declared but weights missing
+    io.ws13 = None
+    assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, need, None) == S.SMOES_ERR_ARG
+    # T = 0 is a no-op
+    d0 = _spec(T=0).c()
+    assert L.smoes_moe_forward(ctypes.byref(d0), ctypes.byref(S.SmoesLayerIO()), None, 0, None) == S.SMOES_OK
+
+
+def test_struct_layout_matches_header():
+    # smoes_layer: int64 + 8 int + 4 float + 2 int = 64 bytes; io: 26 pointers
+    assert ctypes.sizeof(S.SmoesLayer) == 64
+    assert ctypes.sizeof(S.SmoesLayerIO) == 26 * 8
+    text = open(S.HEADER_PATH).read()
+    import re
+    io_block = text[text.index("typedef struct smoes_layer_io"):text.index("} smoes_layer_io;")]
+    io_block = re.sub(r"/\*.*?\*/", "", io_block, flags=re.S)
+    fields = re.findall(r"\*\s*(?:const\s*\*\s*)?([A-Za-z_0-9]+);", io_block)
+    assert fields == S._IO_FIELDS

@@ -1,0 +1,341 @@
+"""GPU parity: every entry point of the C ABI against the CPU oracle on the
+same seeded inputs, element by element.
+
+Tolerances (from the layer's stated targets):
+  * top-k indices and the permutation: bit-exact (top-k where the oracle's
+    k-th vs (k+1)-th logit gap exceeds 1e-4; the permutation is fed the same
+    index array on both sides);
+  * modality scores and MI: relative error <= 1e-5 (fp32 outputs of fp64
+    accumulations); dlogits: normwise relative error <= 1e-5;
+  * layer outputs: |gpu - ref| <= 1e-2 + 2e-2 |ref| elementwise, plus a
+    normwise relative error of the routed part <= 2e-2 (bf16 operands, fp32
+    accumulation) or <= 1e-5 (fp32 layers), because the absolute bound alone
+    is loose for outputs of magnitude ~1e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2604_23996_amd import smoes as S
+from paper_2604_23996_amd import workloads as W
+from tests.gpu_util import (DEV, check_topk, gauss_state_dev, host, rel_err, run_gpu_layer,
+                            run_oracle_layer, say, t)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _name_case(request):
+    say("case", request.node.nodeid)
+    yield
+
+
+# ---------------------------------------------------------------- router
+
+ROUTE_CASES = [
+    # (T, d, E, k, dtype, bias)
+    (100, 136, 40, 5, W.BF16, False),   # ragged T, d % 16 == 8, E not a multiple of 32
+    (257, 256, 64, 6, W.BF16, False),
+    (64, 64, 160, 6, W.BF16, True),
+    (33, 512, 256, 16, W.BF16, False),  # maximum E and k
+    (31, 2048, 8, 2, W.BF16, False),
+    (1, 8, 1, 1, W.BF16, False),        # degenerate: one token, one expert
+    (100, 72, 8, 2, W.F32, False),
+    (70, 256, 20, 3, W.F32, True),
+]
+
+
+@pytest.mark.parametrize("T,d,E,k,dt,bias", ROUTE_CASES)
+@pytest.mark.parametrize("renorm", [False, True])
+def test_route(T, d, E, k, dt, bias, renorm):
+    rng = np.random.default_rng(T * 7 + d + E)
+    x32 = rng.standard_normal((T, d)).astype(np.float32)
+    x = W.f32_to_bf16_bits(x32) if dt == W.BF16 else x32
+    w = (0.05 * rng.standard_normal((E, d))).astype(np.float32)
+    b = rng.standard_normal(E).astype(np.float32) if bias else None
+    z, g, idx, wt = O.route(x, w, k, b, renorm)
+    r = S.route(t(x), t(w), k, t(b), renorm_topk=renorm)
+    zg, gg, ig, wg = (host(r["logits"]), host(r["probs"]), host(r["topk_idx"]), host(r["topk_w"]))
+    # fp32-faithful logits: error within a few fp32 ulps of sum |x w|
+    scale = np.abs(O._f64(x)) @ np.abs(w.astype(np.float64)).T + (np.abs(b) if bias else 0)
+    assert np.all(np.abs(zg - z) <= 4e-7 * scale + 1e-30), np.max(np.abs(zg - z) / scale)
+    assert np.all(np.abs(gg - g) <= 1e-5 * g + 1e-12)
+    assert np.allclose(gg.sum(axis=1), 1.0, atol=1e-5)
+    clear = check_topk(ig, idx, z, k)
+    assert np.all(np.abs(wg[clear] - wt[clear]) <= 1e-5 * wt[clear] + 1e-12)
+
+
+# ---------------------------------------------------------------- modality score
+
+MOD_CASES = [
+    # (T, d, dtype, update, tau_scale, beta, state)
+    (333, 200, W.BF16, False, 0.5, 0.99, "random"),
+    (600, 1024, W.BF16, True, 0.5, 0.99, "zero"),
+    (600, 1024, W.BF16, True, 0.05, 0.9, "random"),
+    (257, 64, W.F32, True, 1.0, 0.99, "random"),
+    (300, 256, W.BF16, True, 0.1, 0.99, "one-modality"),
+    (1, 8, W.F32, True, 0.3, 0.5, "zero"),
+]
+
+
+@pytest.mark.parametrize("T,d,dt,update,tau_scale,beta,state", MOD_CASES)
+def test_modality_score(T, d, dt, update, tau_scale, beta, state):
+    rng = np.random.default_rng(T + d)
+    mu = rng.standard_normal((2, d)).astype(np.float32) * 0.5
+    mid = rng.integers(0, 2, size=T).astype(np.uint8)
+    if state == "one-modality":
+        mid[:] = 0
+    x32 = (mu[mid] + rng.standard_normal((T, d)) * np.where(mid == 0, 1.0, 1.5)[:, None]).astype(np.float32)
+    x = W.f32_to_bf16_bits(x32) if dt == W.BF16 else x32
+    if state == "zero" or state == "one-modality":
+        n0 = np.zeros(2, np.float32); smu0 = np.zeros((2, d), np.float32); ssig0 = np.zeros((2, d), np.float32)
+        if state == "one-modality":
+            n0, smu0, ssig0 = W.random_gauss_state(rng, d, count=50.0)
+    else:
+        n0, smu0, ssig0 = W.random_gauss_state(rng, d)
+    tau = tau_scale * d
+    st = O.GaussState.of(n0, smu0, ssig0)
+    if update:
+        st = O.gauss_update(st, x, mid, beta)
+    mu_o, var_o = O.gauss_params(st, 1e-6)
+    M_ref = O.modality_score(x, mu_o, var_o, tau)
+    n, smu, ssig = t(n0), t(smu0), t(ssig0)
+    M = host(S.modality_score(t(x), n, smu, ssig, t(mid), update=update, beta=beta, tau=tau, var_floor=1e-6))
+    assert np.all(np.abs(M - M_ref) <= 1e-5 * M_ref + 1e-30), np.max(np.abs(M - M_ref) / M_ref)
+    assert np.allclose(M.sum(axis=1), 1.0, atol=1e-6)
+    if update:
+        assert np.allclose(host(n), st.n, rtol=1e-6)
+        assert np.allclose(host(smu), st.s_mu, rtol=2e-6, atol=1e-6 * np.abs(st.s_mu).max())
+        assert np.allclose(host(ssig), st.s_sig, rtol=2e-6, atol=1e-6 * np.abs(st.s_sig).max())
+
+
+def test_modality_tau_default_is_half_d():
+    rng = np.random.default_rng(5)
+    d, T = 128, 64
+    x = rng.standard_normal((T, d)).astype(np.float32)
+    n0, smu0, ssig0 = W.random_gauss_state(rng, d)
+    a = host(S.modality_score(t(x), t(n0), t(smu0), t(ssig0), tau=0.0))
+    b = host(S.modality_score(t(x), t(n0), t(smu0), t(ssig0), tau=0.5 * d))
+    assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------- MI loss + gradient
+
+MI_CASES = [
+    # (T, E, B, offsets kind, bin map, score kind, concentration)
+    (500, 64, 8, "with-empty", "random", "soft", 1.0),
+    (2000, 160, 8, "16", "contiguous", "soft", 0.3),
+    (1, 8, 2, "none", "contiguous", "soft", 1.0),
+    (100, 256, 64, "3", "random", "hard", 0.1),
+    (3000, 128, 16, "none", "contiguous", "soft", 2.0),
+    (4096, 64, 8, "4", "contiguous", "aligned", 0.5),
+]
+
+
+def _mi_inputs(T, E, B, offk, binmap, scores, conc, seed=11):
+    rng = np.random.default_rng(seed + T + E)
+    probs = W.random_probs(rng, T, E, conc)
+    if scores == "hard":
+        mid = rng.integers(0, 2, size=T)
+        M = np.stack([1.0 - mid, mid], axis=1).astype(np.float32)
+    else:
+        M = W.random_soft_scores(rng, T)
+    e2b = W.random_bin_map(rng, E, B, contiguous=(binmap == "contiguous"))
+    if scores == "aligned":  # gate mass leaning to the bins that match the score
+        tilt = np.where(e2b < B // 2, 1.0, -1.0)[None, :] * (M[:, :1] - 0.5)
+        probs = probs * np.exp(2.0 * tilt)
+        probs = (probs / probs.sum(axis=1, keepdims=True)).astype(np.float32)
+    if offk == "none":
+        off = None
+    elif offk == "with-empty":
+        off = np.array([0, 120, 120, 371, 500], dtype=np.int32)
+    else:
+        off = W.random_offsets(rng, T, int(offk))
+    return probs, M, off, e2b
+
+
+@pytest.mark.parametrize("T,E,B,offk,binmap,scores,conc", MI_CASES)
+def test_mi_loss(T, E, B, offk, binmap, scores, conc):
+    probs, M, off, e2b = _mi_inputs(T, E, B, offk, binmap, scores, conc)
+    off_ref = off if off is not None else np.array([0, T])
+    I_ref = O.mi_per_sample(probs, M, off_ref, e2b, B)
+    L_ref = -I_ref.mean()
+    G_ref = O.mi_loss_grad_logits(probs, M, off_ref, e2b, B, grad_scale=0.37)
+    mi, loss, dl = S.mi_loss(t(probs), t(M), t(off), t(e2b), B, grad_scale=0.37)
+    mi, loss, dl = host(mi), host(loss), host(dl)
+    assert np.all(np.abs(mi - I_ref) <= 1e-5 * np.abs(I_ref) + 1e-14), (mi, I_ref)
+    assert abs(loss[0] - L_ref) <= 1e-5 * abs(L_ref) + 1e-14
+    assert rel_err(dl, G_ref) <= 1e-5, rel_err(dl, G_ref)
+    assert np.max(np.abs(dl.sum(axis=1))) <= 1e-6 * np.max(np.abs(G_ref)) + 1e-30
+
+
+def test_mi_loss_without_gradient_and_determinism():
+    probs, M, off, e2b = _mi_inputs(1000, 64, 8, "4", "contiguous", "soft", 1.0)
+    a = S.mi_loss(t(probs), t(M), t(off), t(e2b), 8, want_grad=False)
+    b = S.mi_loss(t(probs), t(M), t(off), t(e2b), 8)
+    c = S.mi_loss(t(probs), t(M), t(off), t(e2b), 8)
+    assert a[2] is None
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert torch.equal(b[2], c[2])  # bit-for-bit reproducible
+
+
+# ---------------------------------------------------------------- permutation
+
+PERM_CASES = [
+    # (T, E, k, skew, with_x)
+    (1000, 64, 6, 0.0, True),
+    (1, 4, 1, 0.0, True),
+    (257, 160, 6, 6.0, False),  # skewed: many empty experts
+    (300, 256, 16, 0.0, True),
+    (4096, 128, 8, 1.0, False),
+]
+
+
+@pytest.mark.parametrize("T,E,k,skew,with_x", PERM_CASES)
+@pytest.mark.parametrize("dt", [W.BF16, W.F32])
+def test_permute(T, E, k, skew, with_x, dt):
+    rng = np.random.default_rng(T + E + k)
+    idx = W.random_topk(rng, T, E, k, skew)
+    counts, off_ref, perm_ref, inv_ref = O.permutation(idx, E)
+    x = None
+    if with_x:
+        x32 = rng.standard_normal((T, 64)).astype(np.float32)
+        x = W.f32_to_bf16_bits(x32) if dt == W.BF16 else x32
+    off, perm, inv, xp = S.permute(t(idx), E, t(x) if with_x else None)
+    assert np.array_equal(host(off), off_ref)
+    assert np.array_equal(host(perm), perm_ref)
+    assert np.array_equal(host(inv), inv_ref)
+    if with_x:
+        xs = O._f64(x)
+        assert np.array_equal(host(xp), xs[perm_ref])
+
+
+# ---------------------------------------------------------------- whole layer
+
+def _check_layer(inp, spec, outs, ref, rows=None, fp32=False):
+    cfg = inp.cfg
+    z = ref["logits"]
+    clear = check_topk(host(outs["topk_idx"]), ref["topk_idx"], z, cfg.k)
+    g = host(outs["probs"])
+    assert np.all(np.abs(g - ref["probs"]) <= 1e-5 * ref["probs"] + 1e-12)
+    M = host(outs["M"])
+    assert np.all(np.abs(M - ref["M"]) <= 1e-5 * ref["M"] + 1e-30), np.max(np.abs(M - ref["M"]) / ref["M"])
+    # permutation: the GPU's rows follow its own routing; check it is the
+    # stable counting sort wherever the routing is the oracle's
+    off = host(outs["expert_offsets"])
+    perm = host(outs["perm_token"])
+    inv = host(outs["perm_inv"])
+    idx_g = host(outs["topk_idx"])
+    assert np.array_equal(off, np.concatenate([[0], np.cumsum(np.bincount(idx_g.ravel(), minlength=cfg.E))]))
+    assert np.array_equal(perm[inv], np.repeat(np.arange(cfg.T)[:, None], cfg.k, axis=1))
+    if clear.all():
+        assert np.array_equal(off, ref["expert_offsets"])
+        assert np.array_equal(perm, ref["perm_token"])
+        assert np.array_equal(inv, ref["inv"])
+    for e in range(cfg.E):  # tokens ascending inside every expert
+        seg = perm[off[e]:off[e + 1]]
+        assert np.all(np.diff(seg) > 0)
+    # layer output on the checked rows
+    out = host(outs["out"])
+    sel = np.arange(cfg.T) if rows is None else rows
+    ok = clear[sel]
+    o = out[sel][ok]
+    r_full = ref["out"][ok]
+    assert np.all(np.abs(o - r_full) <= 1e-2 + 2e-2 * np.abs(r_full)), np.max(np.abs(o - r_full))
+    routed_err = np.linalg.norm(o - r_full) / max(np.linalg.norm(ref["routed"][ok]), 1e-30)
+    assert routed_err <= (1e-5 if fp32 else 2e-2), routed_err
+    return clear
+
+
+def _check_mi(outs, ref, inp, strict):
+    mi = host(outs["mi_per_sample"])
+    I = ref["mi_per_sample"]
+    if strict:
+        assert np.all(np.abs(mi - I) <= 1e-5 * np.abs(I) + 1e-14), (mi, I)
+    else:
+        # conditioning: MI from fp32-rounded oracle gates / scores vs exact
+        off = inp.sample_offsets
+        I32 = O.mi_per_sample(ref["probs"].astype(np.float32), ref["M"].astype(np.float32), off,
+                              inp.expert_to_bin, inp.cfg.n_bins)
+        tol = 1e-5 * np.abs(I) + 10 * np.abs(I32 - I) + 1e-13
+        assert np.all(np.abs(mi - I) <= tol), (mi, I, tol)
+    dl = host(outs["dlogits"])
+    return rel_err(dl, ref["dlogits"])
+
+
+SMALL_LAYERS = [
+    dict(d=128, E=16, k=4, inter=96, n_shared=1, n_bins=4, samples=((200, 100), (40, 60)), dtype=W.BF16),
+    dict(d=256, E=12, k=3, inter=64, n_shared=0, n_bins=3, samples=((500, 200),), dtype=W.BF16),
+    dict(d=64, E=8, k=2, inter=48, n_shared=2, n_bins=2, samples=((90, 40), (10, 3), (60, 60)), dtype=W.F32),
+    dict(d=512, E=64, k=6, inter=128, n_shared=2, n_bins=8, samples=((700, 300),), dtype=W.BF16,
+         logit_bias=True),
+]
+
+
+@pytest.mark.parametrize("layer", range(len(SMALL_LAYERS)))
+@pytest.mark.parametrize("update", [False, True])
+def test_layer_small(layer, update):
+    kw = dict(SMALL_LAYERS[layer])
+    cfg = W.small_config(seed=100 + layer, **kw)
+    inp = W.make_layer_inputs(cfg)
+    wg = W.aligned_router(inp, 0.5)  # well-conditioned MI
+    spec, _, outs = run_gpu_layer(inp, w_gate=wg, update_stats=update)
+    ref = run_oracle_layer(inp, w_gate=wg, update_stats=update)
+    _check_layer(inp, spec, outs, ref, fp32=cfg.dtype == W.F32)
+    assert _check_mi(outs, ref, inp, strict=True) <= 1e-5
+
+
+def test_layer_config0_full():
+    inp = W.make_layer_inputs(W.CONFIGS[0])
+    spec, _, outs = run_gpu_layer(inp)
+    ref = run_oracle_layer(inp)
+    _check_layer(inp, spec, outs, ref, fp32=True)
+    assert _check_mi(outs, ref, inp, strict=False) <= 1e-3
+
+
+@pytest.mark.parametrize("ci", [1, 2, 3, 4])
+def test_layer_config_full(ci):
+    """The full-size workloads in the launch configuration the benchmark times;
+    routing, scores and MI on every token, the output on a seeded sample."""
+    cfg = W.CONFIGS[ci]
+    inp = W.make_layer_inputs(cfg)
+    spec, _, outs = run_gpu_layer(inp)
+    rows = np.sort(np.random.default_rng(ci).choice(cfg.T, size=192, replace=False))
+    ref = run_oracle_layer(inp, rows=rows)
+    _check_layer(inp, spec, outs, ref, rows=rows)
+    err = _check_mi(outs, ref, inp, strict=False)
+    assert err <= 1e-3, err
+
+
+def test_layer_aligned_router_config1_strict_mi():
+    """Config-1 shapes with a modality-aligned router: MI ~1e-3, so the
+    end-to-end MI and gradient meet the 1e-5 bound directly."""
+    cfg = W.CONFIGS[1]
+    inp = W.make_layer_inputs(cfg)
+    wg = W.aligned_router(inp, 0.5)
+    spec, _, outs = run_gpu_layer(inp, w_gate=wg)
+    ref = run_oracle_layer(inp, w_gate=wg, rows=np.arange(64))
+    err = _check_mi(outs, ref, inp, strict=True)
+    assert err <= 1e-5, err
+
+
+def test_layer_deterministic():
+    cfg = W.small_config(seed=7, d=128, E=16, k=4, inter=96, n_shared=1, n_bins=4,
+                         samples=((200, 100),), dtype=W.BF16)
+    inp = W.make_layer_inputs(cfg)
+    _, _, a = run_gpu_layer(inp)
+    _, _, b = run_gpu_layer(inp)
+    for key in ("probs", "topk_idx", "M", "mi_per_sample", "loss", "dlogits", "perm_token", "out"):
+        assert torch.equal(a[key], b[key]), key
+
+
+def test_stage_events():
+    cfg = W.small_config(seed=8, d=128, E=16, k=4, inter=96, n_shared=1, n_bins=4,
+                         samples=((200, 100),), dtype=W.BF16)
+    inp = W.make_layer_inputs(cfg)
+    ev = S.Events()
+    run_gpu_layer(inp, events=ev)
+    times = [ev.elapsed_ms(s, s + 1) for s in range(S.N_STAGES)]
+    assert all(x >= 0 for x in times)
+    ev.close()
