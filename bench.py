@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Throughput of one SMoES MoE layer forward on one MI355X.
+
+One step = one smoes_moe_forward call over one synthetic batch: router GEMM,
+softmax and top-k; Gaussian modality score (with the statistics update when
+the workload re-estimates them); inter-bin MI loss and its logit gradient;
+expert-contiguous permutation; grouped SwiGLU expert GEMMs with shared
+experts; weighted combine. Inputs are resident in HBM before timing starts.
+
+    python bench.py [--steps K] [--warmup W] [--config I] [--no-cpu-baseline]
+
+Prints one JSON line (the last line on stdout). `value` is tokens/s; the
+`roofline` object covers the stage that takes the most time, with its
+algorithmic work divided by its mean duration measured with HIP events on the
+launch stream inside the timed loop; `cpu_baseline` times the float64 CPU
+oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tokens/sec through SMoES MoE layer fwd (+MI loss); % bf16 MFMA peak, % HBM BW"
+PEAK_BF16_TFLOPS = 2500.0   # dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # fp32 vector
+PEAK_HBM_GBS = 8000.0       # HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def stage_work(cfg, T):
+    """Algorithmic flops and HBM bytes of every stage for T tokens."""
+    s = 2 if cfg.dtype == "bf16" else 4
+    d, E, k, I, SI = cfg.d, cfg.E, cfg.k, cfg.inter, cfg.shared_inter
+    R = T * k
+    upd = 2 if cfg.update_stats else 1
+    w = {
+        "route": dict(flops=2 * T * d * E, bytes=T * d * s + E * d * 4 + T * E * 8 + T * k * 8),
+        "modality": dict(flops=6 * T * d * upd, bytes=upd * T * d * s + T * 8 + T * (1 if upd > 1 else 0)),
+        "mi": dict(flops=4 * T * E, bytes=T * (12 * E + 16)),
+        "permute": dict(flops=0, bytes=2 * R * 4 + 2 * R * 4),
+        "gemm1": dict(flops=4 * R * d * I + 4 * T * d * SI,
+                      bytes=(E * 2 * I * d + 2 * SI * d + R * d + T * d + R * I + T * SI) * s),
+        "gemm2": dict(flops=2 * R * I * d + 2 * T * SI * d,
+                      bytes=(E * d * I + d * SI + R * I + T * SI + R * d + T * d) * s),
+        "combine": dict(flops=2 * R * d, bytes=(R + (T if SI else 0) + T) * d * s + R * 8),
+    }
+    return w
+
+
+def source_digest(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel_stage):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when it is missing or the kernel source changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(kernel_stage)
+    if not ent:
+        return None
+    src = os.path.join(ROOT, ent["source"])
+    if not os.path.exists(src) or source_digest(src) != ent["source_sha256"]:
+        return None
+    return ent["bytes_per_launch"]
+
+
+def cpu_baseline(cfg, inp, n_samples):
+    """The float64 oracle, as it stands, on the first n_samples samples."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    Ts = int(inp.sample_offsets[n_samples])
+    off = inp.sample_offsets[:n_samples + 1]
+    x = inp.x[:Ts]
+    mid = inp.modality_id[:Ts]
+    t0 = time.perf_counter()
+    st = O.GaussState.zeros(cfg.d)
+    st = O.gauss_update(st, x, mid, cfg.beta)
+    O.layer_forward(x, mid, off, inp.w_gate, inp.logit_bias, inp.expert_to_bin, cfg.n_bins, cfg.k,
+                    inp.w13, inp.w2, inp.ws13, inp.ws2, st, update_stats=cfg.update_stats,
+                    beta=cfg.beta, tau=cfg.tau)
+    dt = time.perf_counter() - t0
+    cores = min(threads, len(os.sched_getaffinity(0)))
+    return {"value": Ts / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n_samples} samples ({Ts} tokens) of the workload: full layer forward "
+                      f"(statistics, routing, MI + gradient, permutation, experts) in float64 NumPy, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-samples", type=int, default=2)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the single-GPU layer only: this build runs on one MI355X, with no "
+              "expert parallelism or collectives; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2604_23996_amd import smoes as S
+    from paper_2604_23996_amd import workloads as W
+
+    S.lib()  # fail loudly if the HIP library is missing
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda:0"
+    cfg = W.CONFIGS[args.config]
+    log(f"[bench] generating workload {cfg.name} (seed {cfg.seed})")
+    inp = W.make_layer_inputs(cfg)
+
+    def t(a):
+        if a is None:
+            return None
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(a).to(dev)
+
+    act = torch.bfloat16 if cfg.dtype == W.BF16 else torch.float32
+    spec = S.LayerSpec(T=cfg.T, d=cfg.d, E=cfg.E, k=cfg.k, inter=cfg.inter,
+                       shared_inter=cfg.shared_inter, n_bins=cfg.n_bins, n_batch=cfg.n_batch,
+                       act_dtype=S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32,
+                       tau=cfg.tau, beta=cfg.beta, update_stats=cfg.update_stats)
+    dev_in = dict(x=t(inp.x), modality_id=t(inp.modality_id), sample_offsets=t(inp.sample_offsets),
+                  w_gate=t(inp.w_gate), logit_bias=t(inp.logit_bias), expert_to_bin=t(inp.expert_to_bin),
+                  w13=t(inp.w13), w2=t(inp.w2), ws13=t(inp.ws13), ws2=t(inp.ws2),
+                  gauss_n=torch.zeros(2, device=dev), gauss_smu=torch.zeros((2, cfg.d), device=dev),
+                  gauss_ssig=torch.zeros((2, cfg.d), device=dev))
+    if not cfg.update_stats:  # statistics estimated once from the batch, outside the timed call
+        S.modality_score(dev_in["x"], dev_in["gauss_n"], dev_in["gauss_smu"], dev_in["gauss_ssig"],
+                         dev_in["modality_id"], update=True, beta=cfg.beta, tau=cfg.tau)
+    outs = S.alloc_outputs(spec, dev, act)
+    ws = torch.empty(S.workspace_bytes(spec), dtype=torch.uint8, device=dev)
+    events = [S.Events() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        S.moe_forward(spec, dev_in, outs, ws)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        S.moe_forward(spec, dev_in, outs, ws, events=events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    value = cfg.T / (ms * 1e-3)
+
+    stage_ms = {}
+    for si, name in enumerate(S.STAGES):
+        stage_ms[name] = float(np.mean([ev.elapsed_ms(si, si + 1) for ev in events]))
+    for ev in events:
+        ev.close()
+    work = stage_work(cfg, cfg.T)
+    stages = {}
+    for name in S.STAGES:
+        sec = stage_ms[name] * 1e-3
+        wk = work[name]
+        stages[name] = {"ms": round(stage_ms[name], 5),
+                        "tflops": round(wk["flops"] / sec / 1e12, 3) if wk["flops"] else 0.0,
+                        "gbs": round(wk["bytes"] / sec / 1e9, 1)}
+    dom = max(S.STAGES, key=lambda n: stage_ms[n])
+    sec = stage_ms[dom] * 1e-3
+    if dom in ("gemm1", "gemm2", "route") and cfg.dtype == W.BF16:
+        achieved = work[dom]["flops"] / sec / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    elif dom in ("gemm1", "gemm2"):
+        achieved = work[dom]["flops"] / sec / 1e12
+        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
+    else:
+        achieved = work[dom]["bytes"] / sec / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = dom
+    roof["traffic"] = measured_traffic(dom)
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == W.BF16 else "f32", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: SMoES MoE layer, T={cfg.T} tokens "
+                               f"({cfg.n_batch} samples of vision+text), d={cfg.d}, E={cfg.E} routed"
+                               f" + {cfg.n_shared} shared experts, top-{cfg.k}, inter={cfg.inter}, "
+                               f"{cfg.n_bins} bins",
+                   "T": cfg.T, "d": cfg.d, "E": cfg.E, "k": cfg.k, "inter": cfg.inter,
+                   "n_shared": cfg.n_shared, "n_bins": cfg.n_bins, "update_stats": cfg.update_stats,
+                   "parallelism": "none (1 GPU)"},
+        "roofline": roof,
+        "stages": stages,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle on {args.cpu_samples} samples")
+        line["cpu_baseline"] = cpu_baseline(cfg, inp, min(args.cpu_samples, cfg.n_batch))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -54,7 +54,7 @@ import numpy as np
 VISION, TEXT = 0, 1
 
 
-def _f64(a) -> np.ndarray:
+def widen(a) -> np.ndarray:
     """Exact float64 view of a stored array (uint16 = bf16 bit patterns)."""
     a = np.asarray(a)
     if a.dtype == np.uint16:
@@ -68,9 +68,9 @@ def _f64(a) -> np.ndarray:
 
 def router_logits(x, w_gate, logit_bias=None) -> np.ndarray:
     """z_j = W_gate x_j (+ b): the pre-softmax router scores, float64."""
-    z = _f64(x) @ _f64(w_gate).T
+    z = widen(x) @ widen(w_gate).T
     if logit_bias is not None:
-        z = z + _f64(logit_bias)[None, :]
+        z = z + widen(logit_bias)[None, :]
     return z
 
 
@@ -128,7 +128,7 @@ class GaussState:
 
     @staticmethod
     def of(n, s_mu, s_sig) -> "GaussState":
-        return GaussState(_f64(n).copy(), _f64(s_mu).copy(), _f64(s_sig).copy())
+        return GaussState(widen(n).copy(), widen(s_mu).copy(), widen(s_sig).copy())
 
 
 def gauss_update(state: GaussState, x, modality_id, beta: float) -> GaussState:
@@ -141,7 +141,7 @@ def gauss_update(state: GaussState, x, modality_id, beta: float) -> GaussState:
 
     with T_m the modality-m tokens of the batch and mu_T their mean. The last
     term is taken as 0 when N_{t-1} = 0 or |T_m| = 0 (its factor vanishes)."""
-    X = _f64(x)
+    X = widen(x)
     mid = np.asarray(modality_id)
     n_new = state.n.copy()
     s_mu_new = state.s_mu.copy()
@@ -181,7 +181,7 @@ def gauss_params(state: GaussState, var_floor: float) -> Tuple[np.ndarray, np.nd
 
 def log_likelihood(x, mu, var) -> np.ndarray:
     """LL_jm = -1/2 sum_d (log sigma^2_md + (x_jd - mu_md)^2 / sigma^2_md)  (Eq. 8)."""
-    X = _f64(x)
+    X = widen(x)
     ll = np.empty((X.shape[0], 2))
     for m in (VISION, TEXT):
         ll[:, m] = -0.5 * (np.log(var[m]).sum() + (((X - mu[m]) ** 2) / var[m]).sum(axis=1))
@@ -337,18 +337,18 @@ def silu(a):
 def swiglu(x, w13, w2) -> np.ndarray:
     """down(silu(gate x) * up x) with w13 = [gate rows; up rows] ([2I, d]) and
     w2 = [d, I]  (R7)."""
-    X = _f64(x)
-    W13 = _f64(w13)
+    X = widen(x)
+    W13 = widen(w13)
     inter = W13.shape[0] // 2
     a = X @ W13[:inter].T
     u = X @ W13[inter:].T
-    return (silu(a) * u) @ _f64(w2).T
+    return (silu(a) * u) @ widen(w2).T
 
 
 def experts_grouped(x, topk_idx, topk_w, w13, w2, ws13=None, ws2=None, E=None):
     """Routed experts over the expert-contiguous permutation, then the weighted
     combine out_j = sum_s w_js Y[inv(j, s)] + shared(x_j)."""
-    X = _f64(x)
+    X = widen(x)
     idx = np.asarray(topk_idx)
     T, k = idx.shape
     E = E if E is not None else w13.shape[0]
@@ -369,7 +369,7 @@ def experts_grouped(x, topk_idx, topk_w, w13, w2, ws13=None, ws2=None, E=None):
 def experts_naive(x, topk_idx, topk_w, w13, w2, ws13=None, ws2=None):
     """The same layer output by a plain loop: every token through each of its
     k experts, weighted, plus the shared experts."""
-    X = _f64(x)
+    X = widen(x)
     idx = np.asarray(topk_idx)
     w = np.asarray(topk_w, dtype=np.float64)
     out = np.zeros_like(X)
@@ -395,7 +395,7 @@ def layer_forward(x, modality_id, sample_offsets, w_gate, logit_bias, expert_to_
 
     `rows`, when given, restricts the expert computation to those tokens (the
     routing, modality score and MI always cover the whole batch)."""
-    d = _f64(w_gate).shape[1]
+    d = widen(w_gate).shape[1]
     z, g, idx, w = route(x, w_gate, k, logit_bias, renorm_topk)
     if update_stats:
         state = gauss_update(state, x, modality_id, beta)
@@ -404,7 +404,7 @@ def layer_forward(x, modality_id, sample_offsets, w_gate, logit_bias, expert_to_
     I = mi_per_sample(g, M, sample_offsets, expert_to_bin, n_bins)
     loss = -float(I.sum()) / len(I)
     dlogits = mi_loss_grad_logits(g, M, sample_offsets, expert_to_bin, n_bins, grad_scale)
-    E = _f64(w_gate).shape[0]
+    E = widen(w_gate).shape[0]
     counts, offsets, perm_token, inv = permutation(idx, E)
     out = {"logits": z, "probs": g, "topk_idx": idx, "topk_w": w, "gap": topk_gap(z, k),
            "state": state, "M": M, "mi_per_sample": I, "loss": loss, "dlogits": dlogits,

@@ -294,6 +294,7 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     a.perm_inv = perm_inv;
     a.topk_w = io->topk_w;
     a.out = io->out;
+    SMOES_TRY(launch_experts_plan(a, w.experts, s));
     SMOES_TRY(record(ev, SMOES_STAGE_GEMM1, s));
     SMOES_TRY(launch_experts_gemm1(a, w.experts, s));
     SMOES_TRY(record(ev, SMOES_STAGE_GEMM2, s));

@@ -470,6 +470,24 @@ int64_t work_bound(int64_t T, int k, int E, int bm, int nt_r, int nt_s, bool has
     return ceil_div(b, 8) * 8;
 }
 
+struct Plan {
+    int bm, nt1_r, nt1_s, nt2;
+    bool has_shared;
+};
+
+Plan plan_of(const ExpertArgs& a) {
+    Plan p;
+    const bool bf16 = a.act_dtype == 1;
+    p.bm = bf16 ? BM : FBM;
+    const int tn1 = bf16 ? 64 : 32;   // H columns per GEMM1 tile
+    const int tn2 = bf16 ? 128 : 64;  // output columns per GEMM2 tile
+    p.nt1_r = static_cast<int>(ceil_div(a.inter, tn1));
+    p.nt1_s = static_cast<int>(ceil_div(a.shared_inter, tn1));
+    p.nt2 = static_cast<int>(ceil_div(a.d, tn2));
+    p.has_shared = a.shared_inter > 0;
+    return p;
+}
+
 }  // namespace
 
 size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int shared_inter,
@@ -481,21 +499,24 @@ size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int sh
            2 * align_up(sizeof(int32_t) * (E + 2), 256);
 }
 
-hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream) {
+hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream) {
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
-    const bool bf16 = a.act_dtype == 1;
-    const int bm = bf16 ? BM : FBM;
-    const int tn = bf16 ? 64 : 32;  // H columns per tile
-    const int nt_r = static_cast<int>(ceil_div(a.inter, tn));
-    const int nt_s = static_cast<int>(ceil_div(a.shared_inter, tn));
-    const bool has_shared = a.shared_inter > 0;
+    const Plan p = plan_of(a);
     hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T,
-                       has_shared ? 1 : 0, bm, nt_r, nt_s, w.work1);
+                       p.has_shared ? 1 : 0, p.bm, p.nt1_r, p.nt1_s, w.work1);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T,
+                       p.has_shared ? 1 : 0, p.bm, p.nt2, p.nt2, w.work2);
+    return hipGetLastError();
+}
+
+hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream) {
+    ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
+    const Plan p = plan_of(a);
     const GemmArgs g = make_args(a, w, w.work1);
-    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, bm, nt_r, nt_s, has_shared)));
-    if (bf16)
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared)));
+    if (a.act_dtype == 1)
         hipLaunchKernelGGL(gemm_bf16_kernel<1>, grid, dim3(kThreads), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<1>, grid, dim3(kThreads), 0, stream, g);
@@ -504,18 +525,10 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t strea
 
 hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream) {
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
-    const bool bf16 = a.act_dtype == 1;
-    const int bm = bf16 ? BM : FBM;
-    const int tn = bf16 ? 128 : 64;
-    const int nt = static_cast<int>(ceil_div(a.d, tn));
-    const bool has_shared = a.shared_inter > 0;
-    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T,
-                       has_shared ? 1 : 0, bm, nt, nt, w.work2);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
+    const Plan p = plan_of(a);
     const GemmArgs g = make_args(a, w, w.work2);
-    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, bm, nt, nt, has_shared)));
-    if (bf16)
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt2, p.nt2, p.has_shared)));
+    if (a.act_dtype == 1)
         hipLaunchKernelGGL(gemm_bf16_kernel<2>, grid, dim3(kThreads), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<2>, grid, dim3(kThreads), 0, stream, g);

@@ -55,6 +55,8 @@ struct ExpertArgs {
 };
 size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int shared_inter,
                                int act_dtype);
+// work tables of both grouped GEMMs (reads expert_offsets on the device)
+hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t stream);

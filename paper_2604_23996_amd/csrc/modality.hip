@@ -7,12 +7,15 @@
 //       the shift is the previous mean, then a fixed-order LDS tree.
 //     gauss_merge: one thread per (modality, column) adds the chunk partials
 //       in chunk order and applies the EMA update.
-//  score: gauss_prep turns the state into per-column coefficients, and
+//  score: gauss_prep turns the state into per-column mu_m and 1 / sigma^2_m
+//     (fp64 division, stored fp32) and the fp64 constant sum_d log(s2_v / s2_t);
 //     modality_score evaluates, per token,
 //       Delta = sum_d [log s2_v - log s2_t + (x - mu_v)^2 / s2_v - (x - mu_t)^2 / s2_t]
-//     with fp64 accumulation; M_vision = sigmoid(-Delta / (2 tau)) (Eq. 8-9).
-//     Centring at the midpoint m = (mu_v + mu_t) / 2 with delta = (mu_v - mu_t) / 2
-//     turns each term into a y^2 + b y + const with y = x - m.
+//     (each column's two squared terms in fp32, accumulated in fp64);
+//     M_vision = sigmoid(-Delta / (2 tau)), M_text = 1 - M_vision (Eq. 8-9).
+//     The two squared terms are kept apart rather than expanded around a
+//     common centre: with very different variances the expansion cancels
+//     terms ~1/sigma^2 times larger than the result.
 #include "common.h"
 #include "kernels.h"
 
@@ -26,8 +29,8 @@ constexpr int kScoreTokPerWave = 8;
 constexpr int kScoreThreads = 256;
 
 struct ModalityWs {
-    float* coef;       // [3][d]: midpoint, a, b
-    double* cst;       // [1]: sum_d (log s2_v - log s2_t + delta^2 (1/s2_v - 1/s2_t))
+    float* coef;       // [4][d]: mu_v, 1/s2_v, mu_t, 1/s2_t
+    double* cst;       // [1]: sum_d (log s2_v - log s2_t)
     double* n_old;     // [2]: state counts before the update
     int32_t* counts;   // [nchunk][2]
     double* s1;        // [nchunk][2][d]
@@ -39,7 +42,7 @@ ModalityWs carve(void* ws, int64_t T, int d) {
     ModalityWs w;
     const int64_t nchunk = ceil_div(T, kChunkRows);
     w.coef = reinterpret_cast<float*>(p);
-    p += align_up(sizeof(float) * 3 * d, 256);
+    p += align_up(sizeof(float) * 4 * d, 256);
     w.cst = reinterpret_cast<double*>(p);
     p += 256;
     w.n_old = reinterpret_cast<double*>(p);
@@ -210,12 +213,11 @@ gauss_prep_kernel(int d, const float* __restrict__ gauss_n, const float* __restr
             mt = gauss_smu[d + c] / nt;
             vt = fmax(static_cast<double>(gauss_ssig[d + c]) / nt, static_cast<double>(var_floor));
         }
-        const double iv = 1.0 / vv, it = 1.0 / vt;
-        const double mid = 0.5 * (mv + mt), del = 0.5 * (mv - mt);
-        coef[c] = static_cast<float>(mid);
-        coef[d + c] = static_cast<float>(iv - it);
-        coef[2 * d + c] = static_cast<float>(-2.0 * del * (iv + it));
-        acc += (log(vv) - log(vt)) + del * del * (iv - it);
+        coef[c] = static_cast<float>(mv);
+        coef[d + c] = static_cast<float>(1.0 / vv);
+        coef[2 * d + c] = static_cast<float>(mt);
+        coef[3 * d + c] = static_cast<float>(1.0 / vt);
+        acc += log(vv) - log(vt);
     }
     part[threadIdx.x] = acc;
     __syncthreads();
@@ -241,16 +243,19 @@ modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float*
 #pragma unroll
     for (int t = 0; t < kScoreTokPerWave; ++t) acc[t] = 0.0;
     for (int c0 = lane * 8; c0 < d; c0 += kWave * 8) {
-        float mid[8], a[8], b[8];
-        const float4* cp = reinterpret_cast<const float4*>(coef + c0);
-        const float4* ap = reinterpret_cast<const float4*>(coef + d + c0);
-        const float4* bp = reinterpret_cast<const float4*>(coef + 2 * d + c0);
-        *reinterpret_cast<float4*>(&mid[0]) = cp[0];
-        *reinterpret_cast<float4*>(&mid[4]) = cp[1];
-        *reinterpret_cast<float4*>(&a[0]) = ap[0];
-        *reinterpret_cast<float4*>(&a[4]) = ap[1];
-        *reinterpret_cast<float4*>(&b[0]) = bp[0];
-        *reinterpret_cast<float4*>(&b[4]) = bp[1];
+        float mv[8], iv[8], mt[8], it[8];
+        const float4* p0 = reinterpret_cast<const float4*>(coef + c0);
+        const float4* p1 = reinterpret_cast<const float4*>(coef + d + c0);
+        const float4* p2 = reinterpret_cast<const float4*>(coef + 2 * d + c0);
+        const float4* p3 = reinterpret_cast<const float4*>(coef + 3 * d + c0);
+        *reinterpret_cast<float4*>(&mv[0]) = p0[0];
+        *reinterpret_cast<float4*>(&mv[4]) = p0[1];
+        *reinterpret_cast<float4*>(&iv[0]) = p1[0];
+        *reinterpret_cast<float4*>(&iv[4]) = p1[1];
+        *reinterpret_cast<float4*>(&mt[0]) = p2[0];
+        *reinterpret_cast<float4*>(&mt[4]) = p2[1];
+        *reinterpret_cast<float4*>(&it[0]) = p3[0];
+        *reinterpret_cast<float4*>(&it[4]) = p3[1];
 #pragma unroll
         for (int t = 0; t < kScoreTokPerWave; ++t) {
             float v[8];
@@ -258,8 +263,9 @@ modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float*
             float part = 0.0f;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const float y = v[i] - mid[i];
-                part += y * fmaf(a[i], y, b[i]);
+                const float dv = v[i] - mv[i];
+                const float dt = v[i] - mt[i];
+                part += dv * dv * iv[i] - dt * dt * it[i];
             }
             acc[t] += static_cast<double>(part);
         }
@@ -290,7 +296,7 @@ modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float*
 
 size_t modality_workspace_bytes(int64_t T, int d) {
     const int64_t nchunk = ceil_div(T, kChunkRows);
-    return align_up(sizeof(float) * 3 * d, 256) + 256 + 256 +
+    return align_up(sizeof(float) * 4 * d, 256) + 256 + 256 +
            align_up(sizeof(int32_t) * 2 * nchunk, 256) +
            2 * align_up(sizeof(double) * 2 * nchunk * d, 256);
 }

@@ -17,6 +17,8 @@ The paper's datasets are not used; these draws stand in for them.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
+import os
 from dataclasses import dataclass, field
 from typing import List, Optional, Tuple
 
@@ -105,9 +107,10 @@ def small_config(d=64, E=8, k=2, inter=64, n_shared=1, n_bins=2, samples=((24, 8
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round float32 to bf16 with round-to-nearest-even; returns uint16 bits."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    rounding = ((u >> 16) & 1) + 0x7FFF
-    out = ((u + rounding) >> 16).astype(np.uint16)
+    u = a.view(np.uint32)
+    # finite values never overflow 32 bits here; NaNs are fixed up below
+    rounding = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    out = ((u + rounding) >> np.uint32(16)).astype(np.uint16)
     nan = np.isnan(a)
     if nan.any():
         out[nan] = 0x7FC0
@@ -202,19 +205,32 @@ def make_layer_inputs(cfg: LayerConfig, with_weights: bool = True) -> LayerInput
     w_gate = (np.float32(0.02) * rng.standard_normal((cfg.E, d), dtype=np.float32))
     # 8. per-expert logit bias
     bias = rng.standard_normal(cfg.E, dtype=np.float32) if cfg.logit_bias else None
-    # 9. expert weights, drawn per expert
+    # 9. expert weights: every matrix from its own child stream of the seed, so
+    #    the matrices can be drawn in parallel and still be reproducible
     w13 = w2 = ws13 = ws2 = None
     if with_weights:
-        w13 = np.empty((cfg.E, 2 * cfg.inter, d), dtype=np.uint16 if cfg.dtype == BF16 else np.float32)
-        w2 = np.empty((cfg.E, d, cfg.inter), dtype=w13.dtype)
-        for e in range(cfg.E):
-            w13[e] = _store(np.float32(0.02) * rng.standard_normal((2 * cfg.inter, d), dtype=np.float32), cfg.dtype)
-        for e in range(cfg.E):
-            w2[e] = _store(np.float32(0.02) * rng.standard_normal((d, cfg.inter), dtype=np.float32), cfg.dtype)
+        wdt = np.uint16 if cfg.dtype == BF16 else np.float32
+        w13 = np.empty((cfg.E, 2 * cfg.inter, d), dtype=wdt)
+        w2 = np.empty((cfg.E, d, cfg.inter), dtype=wdt)
+        si = cfg.shared_inter
         if cfg.n_shared > 0:
-            si = cfg.shared_inter
-            ws13 = _store(np.float32(0.02) * rng.standard_normal((2 * si, d), dtype=np.float32), cfg.dtype)
-            ws2 = _store(np.float32(0.02) * rng.standard_normal((d, si), dtype=np.float32), cfg.dtype)
+            ws13 = np.empty((2 * si, d), dtype=wdt)
+            ws2 = np.empty((d, si), dtype=wdt)
+        jobs = [(w13, e) for e in range(cfg.E)] + [(w2, e) for e in range(cfg.E)]
+        if cfg.n_shared > 0:
+            jobs += [(ws13, None), (ws2, None)]
+        children = np.random.SeedSequence([cfg.seed, 0x5EED]).spawn(len(jobs))
+
+        def draw(i):
+            arr, e = jobs[i]
+            dst = arr if e is None else arr[e]
+            buf = np.random.default_rng(children[i]).standard_normal(dst.shape, dtype=np.float32)
+            buf *= np.float32(0.02)
+            dst[...] = _store(buf, cfg.dtype)
+
+        workers = max(1, min(16, os.cpu_count() or 1))
+        with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(draw, range(len(jobs))))
     # 10. activation storage type
     x_store = _store(x, cfg.dtype)
     # 12. fixed contiguous bins

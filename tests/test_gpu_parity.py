@@ -58,7 +58,7 @@ def test_route(T, d, E, k, dt, bias, renorm):
     r = S.route(t(x), t(w), k, t(b), renorm_topk=renorm)
     zg, gg, ig, wg = (host(r["logits"]), host(r["probs"]), host(r["topk_idx"]), host(r["topk_w"]))
     # fp32-faithful logits: error within a few fp32 ulps of sum |x w|
-    scale = np.abs(O._f64(x)) @ np.abs(w.astype(np.float64)).T + (np.abs(b) if bias else 0)
+    scale = np.abs(O.widen(x)) @ np.abs(w.astype(np.float64)).T + (np.abs(b) if bias else 0)
     assert np.all(np.abs(zg - z) <= 4e-7 * scale + 1e-30), np.max(np.abs(zg - z) / scale)
     assert np.all(np.abs(gg - g) <= 1e-5 * g + 1e-12)
     assert np.allclose(gg.sum(axis=1), 1.0, atol=1e-5)
@@ -207,7 +207,7 @@ def test_permute(T, E, k, skew, with_x, dt):
     assert np.array_equal(host(perm), perm_ref)
     assert np.array_equal(host(inv), inv_ref)
     if with_x:
-        xs = O._f64(x)
+        xs = O.widen(x)
         assert np.array_equal(host(xp), xs[perm_ref])
 
 
