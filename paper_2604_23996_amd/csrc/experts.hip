@@ -65,19 +65,27 @@ ExpWs carve(void* ws, int64_t T, int d, int k, int inter, int shared_inter, int 
     return w;
 }
 
-// Work table: work[g + 1] = work[g] + m_tiles(g) * n_tiles(g) for g in [0, G).
-__global__ void build_work_kernel(const int32_t* __restrict__ off, int E, int64_t T, int has_shared,
-                                  int bm, int nt_routed, int nt_shared, int32_t* __restrict__ work) {
-    if (threadIdx.x != 0) return;
-    int32_t acc = 0;
-    work[0] = 0;
-    for (int g = 0; g < E; ++g) {
-        const int rows = off[g + 1] - off[g];
-        acc += static_cast<int32_t>(ceil_div(rows, bm)) * nt_routed;
-        work[g + 1] = acc;
+// Work table: work[g + 1] = work[g] + m_tiles(g) * n_tiles(g) for g in [0, G):
+// one thread per group and a block-wide inclusive scan (E + 1 <= 257 groups).
+__global__ void __launch_bounds__(512)
+build_work_kernel(const int32_t* __restrict__ off, int E, int64_t T, int has_shared, int bm,
+                  int nt_routed, int nt_shared, int32_t* __restrict__ work) {
+    __shared__ int32_t sc[512];
+    const int g = threadIdx.x;
+    int32_t v = 0;
+    if (g < E) v = static_cast<int32_t>(ceil_div(off[g + 1] - off[g], bm)) * nt_routed;
+    else if (g == E && has_shared) v = static_cast<int32_t>(ceil_div(T, bm)) * nt_shared;
+    sc[g] = v;
+    __syncthreads();
+    for (int o = 1; o < 512; o <<= 1) {
+        const int32_t add = g >= o ? sc[g - o] : 0;
+        __syncthreads();
+        v += add;
+        sc[g] = v;
+        __syncthreads();
     }
-    if (has_shared) acc += static_cast<int32_t>(ceil_div(T, bm)) * nt_shared;
-    work[E + 1] = acc;
+    if (g == 0) work[0] = 0;
+    if (g <= E) work[g + 1] = v;
 }
 
 struct Tile {
@@ -502,11 +510,11 @@ size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int sh
 hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream) {
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
     const Plan p = plan_of(a);
-    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T,
+    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(512), 0, stream, a.expert_offsets, a.E, a.T,
                        p.has_shared ? 1 : 0, p.bm, p.nt1_r, p.nt1_s, w.work1);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T,
+    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(512), 0, stream, a.expert_offsets, a.E, a.T,
                        p.has_shared ? 1 : 0, p.bm, p.nt2, p.nt2, w.work2);
     return hipGetLastError();
 }

@@ -123,19 +123,23 @@ mi_partial_kernel(const float* __restrict__ probs, const float* __restrict__ M, 
     }
 }
 
+// One block; samples in turn. Thread (m, k) owns one cell of the joint;
+// sums over cells are taken by every thread in the same fixed order from LDS.
 __global__ void __launch_bounds__(kMiThreads)
 mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batch, int C,
                    const int32_t* __restrict__ e2b, int n_bins, const double* __restrict__ part,
                    double* __restrict__ coef, double* __restrict__ mi64, int32_t* __restrict__ members,
                    float* __restrict__ mi_per_sample, float* __restrict__ loss) {
     __shared__ double A[2][256];
-    __shared__ double Abin[2][64];
+    __shared__ double P[2][64];    // S-bar, then the joint P(m, k)
+    __shared__ double term[2][64];
     __shared__ double Wm[2];
     __shared__ int32_t mem[256];
     const int NB = E / n_bins;
+    const int tid = threadIdx.x;
     // bin member lists in ascending expert order
-    if (threadIdx.x < n_bins) {
-        const int k = threadIdx.x;
+    if (tid < n_bins) {
+        const int k = tid;
         int n = 0;
         for (int e = 0; e < E; ++e)
             if (e2b[e] == k && n < NB) {
@@ -143,17 +147,20 @@ mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batc
                 members[k * NB + n] = e;
                 ++n;
             }
-        for (; n < NB; ++n) {  // violated precondition: pad with expert 0 of the bin list
+        for (; n < NB; ++n) {  // violated precondition (bin too small): mark the slot empty
             mem[k * NB + n] = -1;
             members[k * NB + n] = -1;
         }
     }
     __syncthreads();
+    const bool cell = tid < 2 * n_bins;
+    const int cm = cell ? tid / n_bins : 0, ck = cell ? tid % n_bins : 0;
+    double total = 0.0;
     for (int i = 0; i < n_batch; ++i) {
         int64_t a, b;
         sample_range(off, T, i, a, b);
         const double* pi = part + static_cast<int64_t>(i) * C * (2 * E + 2);
-        for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        for (int e = tid; e < E; e += blockDim.x) {
             double s0 = 0.0, s1 = 0.0;
             for (int c = 0; c < C; ++c) {
                 s0 += pi[c * (2 * E + 2) + e];
@@ -162,64 +169,52 @@ mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batc
             A[0][e] = s0;
             A[1][e] = s1;
         }
-        if (threadIdx.x == 0) {
-            double t0 = 0.0, t1 = 0.0;
-            for (int c = 0; c < C; ++c) {
-                t0 += pi[c * (2 * E + 2) + 2 * E];
-                t1 += pi[c * (2 * E + 2) + 2 * E + 1];
-            }
-            Wm[0] = t0;
-            Wm[1] = t1;
+        if (tid < 2) {
+            double t = 0.0;
+            for (int c = 0; c < C; ++c) t += pi[c * (2 * E + 2) + 2 * E + tid];
+            Wm[tid] = t;
         }
         __syncthreads();
-        if (threadIdx.x < 2 * n_bins) {
-            const int m = threadIdx.x / n_bins, k = threadIdx.x % n_bins;
+        // Eq. 12: S-bar[m][k] = sum_{e in B_k} A[m][e] / (N_B W_m)
+        if (cell) {
             double s = 0.0;
             for (int n = 0; n < NB; ++n) {
-                const int e = mem[k * NB + n];
-                if (e >= 0) s += A[m][e];
+                const int e = mem[ck * NB + n];
+                if (e >= 0) s += A[cm][e];
             }
-            Abin[m][k] = s;
+            P[cm][ck] = (b > a && Wm[cm] > 0.0) ? s / (static_cast<double>(NB) * Wm[cm]) : 0.0;
         }
         __syncthreads();
-        if (threadIdx.x == 0) {
-            double S[2][64];
-            double Z = 0.0;
-            for (int m = 0; m < 2; ++m)
-                for (int k = 0; k < n_bins; ++k) {
-                    S[m][k] = (b > a && Wm[m] > 0.0) ? Abin[m][k] / (static_cast<double>(NB) * Wm[m]) : 0.0;
-                    Z += S[m][k];
-                }
-            double Pm[2] = {0.0, 0.0};
-            double Pk[64];
-            for (int k = 0; k < n_bins; ++k) Pk[k] = 0.0;
-            for (int m = 0; m < 2; ++m)
-                for (int k = 0; k < n_bins; ++k) {
-                    S[m][k] = Z > 0.0 ? S[m][k] / Z : 0.0;  // now P(m, k)
-                    Pm[m] += S[m][k];
-                    Pk[k] += S[m][k];
-                }
-            double I = 0.0;
-            for (int m = 0; m < 2; ++m)
-                for (int k = 0; k < n_bins; ++k)
-                    if (S[m][k] > 0.0) I += S[m][k] * log(S[m][k] / (Pm[m] * Pk[k]));
-            for (int m = 0; m < 2; ++m)
-                for (int k = 0; k < n_bins; ++k) {
-                    double cv = 0.0;
-                    if (Wm[m] > 0.0 && S[m][k] > 0.0)
-                        cv = (log(S[m][k] / (Pm[m] * Pk[k])) - I) / (static_cast<double>(NB) * Wm[m] * Z);
-                    coef[(static_cast<int64_t>(i) * 2 + m) * n_bins + k] = cv;
-                }
+        // Eq. 13: normalise; marginals
+        double Z = 0.0;
+        for (int m = 0; m < 2; ++m)
+            for (int k = 0; k < n_bins; ++k) Z += P[m][k];
+        double pmk = 0.0, pm = 0.0, pk = 0.0;
+        if (cell && Z > 0.0) {
+            for (int k = 0; k < n_bins; ++k) pm += P[cm][k] / Z;
+            pk = P[0][ck] / Z + P[1][ck] / Z;
+            pmk = P[cm][ck] / Z;
+        }
+        // Eq. 14
+        const double lr = (cell && pmk > 0.0) ? log(pmk / (pm * pk)) : 0.0;
+        if (cell) term[cm][ck] = pmk > 0.0 ? pmk * lr : 0.0;
+        __syncthreads();
+        double I = 0.0;
+        for (int m = 0; m < 2; ++m)
+            for (int k = 0; k < n_bins; ++k) I += term[m][k];
+        if (cell) {
+            double cv = 0.0;
+            if (Wm[cm] > 0.0 && pmk > 0.0) cv = (lr - I) / (static_cast<double>(NB) * Wm[cm] * Z);
+            coef[(static_cast<int64_t>(i) * 2 + cm) * n_bins + ck] = cv;
+        }
+        if (tid == 0) {
             mi64[i] = I;
             mi_per_sample[i] = static_cast<float>(I);
         }
+        total += I;
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
-        double s = 0.0;
-        for (int i = 0; i < n_batch; ++i) s += mi64[i];
-        loss[0] = static_cast<float>(-s / n_batch);
-    }
+    if (tid == 0) loss[0] = static_cast<float>(-total / n_batch);
 }
 
 __global__ void __launch_bounds__(kMiThreads)

@@ -25,7 +25,7 @@ namespace {
 
 constexpr int kChunkRows = 256;   // tokens per gauss_partial block
 constexpr int kColsPerBlock = 512; // 64 lanes x 8 columns
-constexpr int kScoreTokPerWave = 8;
+constexpr int kScoreTokPerWave = 2;
 constexpr int kScoreThreads = 256;
 
 struct ModalityWs {
@@ -196,11 +196,11 @@ __global__ void gauss_merge_kernel(int d, int64_t nchunk, const int32_t* __restr
 }
 
 // Per-column score coefficients and the fp64 constant, one block.
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(1024)
 gauss_prep_kernel(int d, const float* __restrict__ gauss_n, const float* __restrict__ gauss_smu,
                   const float* __restrict__ gauss_ssig, float var_floor, float* __restrict__ coef,
                   double* __restrict__ cst) {
-    __shared__ double part[256];
+    __shared__ double part[1024];
     const double nv = gauss_n[0], nt = gauss_n[1];
     double acc = 0.0;
     for (int c = threadIdx.x; c < d; c += blockDim.x) {
@@ -221,7 +221,7 @@ gauss_prep_kernel(int d, const float* __restrict__ gauss_n, const float* __restr
     }
     part[threadIdx.x] = acc;
     __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
+    for (int s = 512; s > 0; s >>= 1) {
         if (threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
         __syncthreads();
     }
@@ -242,6 +242,7 @@ modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float*
     double acc[kScoreTokPerWave];
 #pragma unroll
     for (int t = 0; t < kScoreTokPerWave; ++t) acc[t] = 0.0;
+#pragma unroll 4
     for (int c0 = lane * 8; c0 < d; c0 += kWave * 8) {
         float mv[8], iv[8], mt[8], it[8];
         const float4* p0 = reinterpret_cast<const float4*>(coef + c0);
@@ -323,7 +324,7 @@ hipError_t launch_modality(const void* x, int x_dtype, int64_t T, int d, const u
                            gauss_n, gauss_smu, gauss_ssig);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    hipLaunchKernelGGL(gauss_prep_kernel, dim3(1), dim3(256), 0, stream, d, gauss_n, gauss_smu,
+    hipLaunchKernelGGL(gauss_prep_kernel, dim3(1), dim3(1024), 0, stream, d, gauss_n, gauss_smu,
                        gauss_ssig, var_floor, w.coef, w.cst);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const double t = tau > 0.0f ? static_cast<double>(tau) : 0.5 * d;

@@ -1,12 +1,12 @@
 // Router: logits z = W_gate x (+ b), full softmax g and top-k (Sec. 3.1).
 //
-// One workgroup (4 waves) owns 32 tokens and every expert. For bf16
+// One workgroup (8 waves) owns 32 tokens and every expert. For bf16
 // activations the logits are fp32-faithful on the matrix cores: the fp32
 // router weights are split into three bf16 terms (hi + mid + lo reproduces
 // the weight to ~2^-24), each product with the exact bf16 activation is exact,
-// and v_mfma_f32_32x32x16_bf16 accumulates in fp32. The four waves split the
+// and v_mfma_f32_32x32x16_bf16 accumulates in fp32. The eight waves split the
 // hidden dimension; their partial tiles are summed in LDS in a fixed order,
-// then every wave runs the softmax and a wave-wide top-k for 8 tokens.
+// then every wave runs the softmax and a wave-wide top-k for 4 tokens.
 // For fp32 activations the dot products are accumulated in fp64.
 #include "common.h"
 #include "kernels.h"
@@ -16,7 +16,16 @@ namespace smoes {
 namespace {
 
 constexpr int kRouterTokens = 32;
-constexpr int kRouterThreads = 256;
+constexpr int kRouterWaves = 8;
+constexpr int kRouterThreads = kRouterWaves * 64;
+constexpr size_t kRouterLdsMax = 65536;
+
+// Tree buffers that fit the LDS budget: up to 4, at least 2.
+__host__ __device__ inline int router_slots(int E_pad) {
+    const int per = kRouterTokens * E_pad * static_cast<int>(sizeof(float));
+    const int s = static_cast<int>(kRouterLdsMax / per);
+    return s >= 4 ? 4 : (s < 2 ? 2 : s);
+}
 
 // w_gate [E, d] f32 -> wsplit [3][E_pad][d] bf16 (hi, mid, lo); rows >= E are zero.
 __global__ void split_wgate_kernel(const float* __restrict__ w, int E, int E_pad, int d,
@@ -37,15 +46,17 @@ __global__ void split_wgate_kernel(const float* __restrict__ w, int E, int E_pad
     }
 }
 
-// Logits of one wave over its share of the hidden dimension, bf16x3 MFMA,
-// then a fixed-order tree over the four waves through LDS:
-// z = (w0 + w2) + (w1 + w3), stored as zrow[32][E_pad].
+// Logits of one wave over its share of the hidden dimension (k-steps
+// s = wave, wave + 8, ...), bf16x3 MFMA with the next step's fragments
+// loaded before the current step's MFMAs; then a fixed-order tree over the 8
+// waves through LDS (wave w adds wave w + half, half = 4, 2, 1), using `slots`
+// buffers of [32][E_pad] floats. The logits end in buffer 0.
 // Output layout of a 32x32 MFMA tile (lane l, element v):
 //   column = l % 32, row = 8 * (v / 4) + 4 * (l / 32) + (v % 4).
 template <int NT>
 __device__ void router_mfma_logits(const uint16_t* __restrict__ x, int64_t T, int d,
                                    const uint16_t* __restrict__ wsplit, int E_pad,
-                                   int64_t tok0, int wave, float* __restrict__ buf) {
+                                   int64_t tok0, int wave, int slots, float* __restrict__ buf) {
     const int lane = lane_id();
     const int half = lane >> 5;
     const int r = lane & 31;
@@ -57,23 +68,43 @@ __device__ void router_mfma_logits(const uint16_t* __restrict__ x, int64_t T, in
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[n] = f32x16_t{};
     const int nsteps = static_cast<int>(ceil_div(d, 16));
-    for (int s = wave; s < nsteps; s += 4) {
+    bf16x8_t a_cur = {}, b_cur[NT][3];
+    auto fetch = [&](int s, bf16x8_t& a, bf16x8_t (&b)[NT][3]) {
         const int kk = s * 16 + half * 8;
-        const bool valid = kk < d;  // d % 8 == 0: an 8-chunk is all in or all out
-        bf16x8_t a = {};
-        if (valid) a = *reinterpret_cast<const bf16x8_t*>(xrow + kk);
+        const bool valid = s < nsteps && kk < d;  // d % 8 == 0: an 8-chunk is all in or all out
+        a = valid ? *reinterpret_cast<const bf16x8_t*>(xrow + kk) : bf16x8_t{};
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
             const int64_t off = static_cast<int64_t>(n * 32 + r) * d + kk;
-            bf16x8_t blo = {}, bmid = {}, bhi = {};
-            if (valid) {
-                blo = *reinterpret_cast<const bf16x8_t*>(wsplit + 2 * part + off);
-                bmid = *reinterpret_cast<const bf16x8_t*>(wsplit + part + off);
-                bhi = *reinterpret_cast<const bf16x8_t*>(wsplit + off);
-            }
-            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, blo, acc[n], 0, 0, 0);
-            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bmid, acc[n], 0, 0, 0);
-            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bhi, acc[n], 0, 0, 0);
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+                b[n][p] = valid ? *reinterpret_cast<const bf16x8_t*>(wsplit + p * part + off) : bf16x8_t{};
+        }
+    };
+    auto mfma3 = [&](const bf16x8_t& a, const bf16x8_t (&b)[NT][3]) {
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[n][2], acc[n], 0, 0, 0);  // lo
+            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[n][1], acc[n], 0, 0, 0);  // mid
+            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[n][0], acc[n], 0, 0, 0);  // hi
+        }
+    };
+    if constexpr (NT <= 5) {  // register double buffer: next step's loads overlap this step's MFMAs
+        fetch(wave, a_cur, b_cur);
+        for (int s = wave; s < nsteps; s += kRouterWaves) {
+            bf16x8_t a_nxt, b_nxt[NT][3];
+            fetch(s + kRouterWaves, a_nxt, b_nxt);
+            mfma3(a_cur, b_cur);
+            a_cur = a_nxt;
+#pragma unroll
+            for (int n = 0; n < NT; ++n)
+#pragma unroll
+                for (int p = 0; p < 3; ++p) b_cur[n][p] = b_nxt[n][p];
+        }
+    } else {  // wide expert counts: no room for a second fragment set
+        for (int s = wave; s < nsteps; s += kRouterWaves) {
+            fetch(s, a_cur, b_cur);
+            mfma3(a_cur, b_cur);
         }
     }
     const int64_t tile = static_cast<int64_t>(kRouterTokens) * E_pad;
@@ -81,32 +112,30 @@ __device__ void router_mfma_logits(const uint16_t* __restrict__ x, int64_t T, in
         const int row = 8 * (v >> 2) + 4 * half + (v & 3);
         return buf[which * tile + row * E_pad + n * 32 + r];
     };
-    if (wave >= 2) {
+    for (int h = kRouterWaves / 2; h >= 1; h >>= 1) {
+        // writers [h, 2h) hand their partials to readers [0, h), `slots` at a time
+        for (int g = 0; g < h; g += slots) {
+            if (wave >= h + g && wave < h + g + slots && wave < 2 * h) {
 #pragma unroll
-        for (int n = 0; n < NT; ++n)
+                for (int n = 0; n < NT; ++n)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) at(wave - 2, n, v) = acc[n][v];
+                    for (int v = 0; v < 16; ++v) at(wave - h - g, n, v) = acc[n][v];
+            }
+            __syncthreads();
+            if (wave >= g && wave < g + slots && wave < h) {
+#pragma unroll
+                for (int n = 0; n < NT; ++n)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[n][v] += at(wave - g, n, v);
+            }
+            __syncthreads();
+        }
     }
-    __syncthreads();
-    if (wave < 2) {
-#pragma unroll
-        for (int n = 0; n < NT; ++n)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[n][v] += at(wave, n, v);
-    }
-    __syncthreads();
-    if (wave == 1) {
-#pragma unroll
-        for (int n = 0; n < NT; ++n)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) at(0, n, v) = acc[n][v];
-    }
-    __syncthreads();
     if (wave == 0) {
 #pragma unroll
         for (int n = 0; n < NT; ++n)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) at(1, n, v) = acc[n][v] + at(0, n, v);
+            for (int v = 0; v < 16; ++v) at(0, n, v) = acc[n][v];
     }
 }
 
@@ -117,16 +146,17 @@ router_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restr
               int k, int renorm, float* __restrict__ logits, float* __restrict__ probs,
               int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
     extern __shared__ float smem[];
-    // bf16 path: smem = [2][32][E_pad] tree buffers, the logits end in the second;
+    // bf16 path: smem = [slots][32][E_pad] tree buffers, the logits end in the first;
     // fp32 path: smem = [32][E_pad] logits.
-    float* zrow = smem + (BF16 ? kRouterTokens * E_pad : 0);
+    float* zrow = smem;
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
     const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * kRouterTokens;
     const int ntok = static_cast<int>(T - tok0 < kRouterTokens ? T - tok0 : kRouterTokens);
 
     if constexpr (BF16) {
-        router_mfma_logits<NT>(static_cast<const uint16_t*>(x), T, d, wsplit, E_pad, tok0, wave, smem);
+        router_mfma_logits<NT>(static_cast<const uint16_t*>(x), T, d, wsplit, E_pad, tok0, wave,
+                               router_slots(E_pad), smem);
     } else {
         const float* xf = static_cast<const float*>(x);
         for (int i = threadIdx.x; i < kRouterTokens * E_pad; i += kRouterThreads) {
@@ -144,9 +174,9 @@ router_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restr
     }
     __syncthreads();
 
-    // softmax + top-k: wave w handles tokens w, w + 4, ...
+    // softmax + top-k: wave w handles tokens w, w + 8, ...
     const int QE = static_cast<int>(ceil_div(E, kWave));
-    for (int t = wave; t < ntok; t += 4) {
+    for (int t = wave; t < ntok; t += kRouterWaves) {
         const float* zr = zrow + t * E_pad;
         const int64_t tok = tok0 + t;
         float zq[4], gq[4];
@@ -235,7 +265,7 @@ hipError_t launch_router_nt(int NT, const void* x, int64_t T, int d, const float
                             int renorm, float* logits, float* probs, int32_t* topk_idx,
                             float* topk_w, hipStream_t stream) {
     const dim3 grid(static_cast<unsigned>(ceil_div(T, kRouterTokens)));
-    const size_t lds = sizeof(float) * kRouterTokens * E_pad * (BF16 ? 2 : 1);
+    const size_t lds = sizeof(float) * kRouterTokens * E_pad * (BF16 ? router_slots(E_pad) : 1);
 #define SMOES_ROUTER_CASE(N)                                                                      \
     case N:                                                                                       \
         hipLaunchKernelGGL((router_kernel<BF16, N>), grid, dim3(kRouterThreads), lds, stream, x, \
@@ -268,7 +298,7 @@ size_t router_workspace_bytes(int d, int E, int x_dtype) {
 
 size_t router_lds_bytes(int E, int x_dtype) {
     const int E_pad = static_cast<int>(ceil_div(E, 32) * 32);
-    return sizeof(float) * kRouterTokens * E_pad * (x_dtype == 1 ? 2 : 1);
+    return sizeof(float) * kRouterTokens * E_pad * (x_dtype == 1 ? router_slots(E_pad) : 1);
 }
 
 hipError_t launch_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gate,

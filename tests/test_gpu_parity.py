@@ -8,9 +8,10 @@ Tolerances (from the layer's stated targets):
   * modality scores and MI: relative error <= 1e-5 (fp32 outputs of fp64
     accumulations); dlogits: normwise relative error <= 1e-5;
   * layer outputs: |gpu - ref| <= 1e-2 + 2e-2 |ref| elementwise, plus a
-    normwise relative error of the routed part <= 2e-2 (bf16 operands, fp32
-    accumulation) or <= 1e-5 (fp32 layers), because the absolute bound alone
-    is loose for outputs of magnitude ~1e-3.
+    normwise relative error <= 2e-2 (bf16 operands, fp32 accumulation) or
+    <= 1e-5 (fp32 layers), because the absolute bound alone is loose for
+    outputs of magnitude ~1e-3; the norm is that of the routed part for layers
+    without shared experts and of the whole output otherwise.
 """
 import numpy as np
 import pytest
@@ -243,7 +244,12 @@ def _check_layer(inp, spec, outs, ref, rows=None, fp32=False):
     o = out[sel][ok]
     r_full = ref["out"][ok]
     assert np.all(np.abs(o - r_full) <= 1e-2 + 2e-2 * np.abs(r_full)), np.max(np.abs(o - r_full))
-    routed_err = np.linalg.norm(o - r_full) / max(np.linalg.norm(ref["routed"][ok]), 1e-30)
+    # normwise: against the routed part when there is no shared expert (the
+    # strict case), else against the whole output: shared experts have gate
+    # weight 1 and dominate the norm, and the bf16 rounding of their output
+    # alone is ~1 % of the much smaller routed part
+    den = np.linalg.norm(ref["routed"][ok]) if cfg.n_shared == 0 else np.linalg.norm(r_full)
+    routed_err = np.linalg.norm(o - r_full) / max(den, 1e-30)
     assert routed_err <= (1e-5 if fp32 else 2e-2), routed_err
     return clear
 
