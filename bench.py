@@ -115,6 +115,9 @@ def main():
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=2)
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="first run a plain device-to-device copy of this many MiB (untimed): "
+                         "a known-size reference for hardware byte counters")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -155,6 +158,13 @@ def main():
     if not cfg.update_stats:  # statistics estimated once from the batch, outside the timed call
         S.modality_score(dev_in["x"], dev_in["gauss_n"], dev_in["gauss_smu"], dev_in["gauss_ssig"],
                          dev_in["modality_id"], update=True, beta=cfg.beta, tau=cfg.tau)
+    if args.copy_probe_mb > 0:
+        n = args.copy_probe_mb * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     outs = S.alloc_outputs(spec, dev, act)
     ws = torch.empty(S.workspace_bytes(spec), dtype=torch.uint8, device=dev)
     events = [S.Events() for _ in range(args.steps)]

@@ -3,7 +3,7 @@
 // synchronises the host.
 #include <stdio.h>
 
-#include "../../include/smoes.h"
+#include "smoes.h"
 #include "common.h"
 #include "kernels.h"
 

@@ -30,8 +30,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kGroupM = 8;  // m-tiles per super-row in the work order
 
-// bf16 MFMA tiles
-constexpr int BM = 128, BNB = 128, BK = 64, LDP = BK + 8;
 // f32 FMA tiles
 constexpr int FBM = 64, FBNB = 64, FBK = 16;
 
@@ -96,22 +94,35 @@ struct Tile {
 };
 
 // Decode this block's tile; returns false when the block has no work.
+// Block b runs on XCD b % 8. The routed items and the shared-expert items are
+// each cut into 8 contiguous ranges, one per XCD, so every XCD gets the same
+// share of both kinds (shared tiles can have a longer K than routed ones).
+// Inside a group items run (super-row of 8 m-tiles, n-tile, m-tile).
 __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, const int32_t* __restrict__ off,
-                                            int E, int64_t T, int G, int bm, int nt_routed, int nt_shared,
+                                            int E, int64_t T, int bm, int nt_routed, int nt_shared,
                                             Tile& t) {
-    const int total = work[G];
-    const int per_xcd = (total + 7) / 8;
+    const int routed = work[E];
+    const int shared = work[E + 1] - routed;
+    const int r8 = (routed + 7) / 8, s8 = (shared + 7) / 8;
     const int xcd = blockIdx.x & 7;
     const int slot = blockIdx.x >> 3;
-    if (slot >= per_xcd) return false;
-    const int w = xcd * per_xcd + slot;
-    if (w >= total) return false;
-    int lo = 0, hi = G - 1;  // last g with work[g] <= w
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (work[mid] <= w) lo = mid; else hi = mid - 1;
+    const int r_lo = min(xcd * r8, routed), r_hi = min(r_lo + r8, routed);
+    const int s_lo = min(xcd * s8, shared), s_hi = min(s_lo + s8, shared);
+    int w;
+    if (slot < r_hi - r_lo) w = r_lo + slot;
+    else if (slot < (r_hi - r_lo) + (s_hi - s_lo)) w = routed + s_lo + (slot - (r_hi - r_lo));
+    else return false;
+    int g;
+    if (w >= routed) {
+        g = E;
+    } else {
+        int lo = 0, hi = E - 1;  // last g with work[g] <= w
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (work[mid] <= w) lo = mid; else hi = mid - 1;
+        }
+        g = lo;
     }
-    const int g = lo;
     const int local = w - work[g];
     int64_t base, rows_g;
     int ntn;
@@ -139,9 +150,18 @@ __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, co
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
 
+// Raw buffer descriptors (gfx9 word 3) and an offset that is always past the record count.
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kOutOfRange = 0x7fffffff;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 as_uint4(i32x4_t v) {
+    return make_uint4(static_cast<uint32_t>(v.x), static_cast<uint32_t>(v.y), static_cast<uint32_t>(v.z),
+                      static_cast<uint32_t>(v.w));
+}
+
 struct GemmArgs {
     int64_t T;
-    int d, E, inter, shared_inter;
+    int d, E, k, inter, shared_inter;
     const void* x;
     const void* w13;
     const void* w2;
@@ -158,22 +178,46 @@ struct GemmArgs {
 
 // ============================================================== bf16 MFMA path
 
-template <int MODE>
-__global__ void __launch_bounds__(kThreads, 2)
+// Tile shape of the bf16 GEMMs: WAVES_M x WAVES_N waves, each owning
+// TM x TN MFMA 32x32 tiles; K step BK; PF = global-load prefetch depth in
+// K steps (register staged; LDS is double-buffered).
+template <int WAVES_M_, int WAVES_N_, int TM_, int TN_, int BK_, int PF_>
+struct TileCfg {
+    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, TM = TM_, TN = TN_, BK = BK_, PF = PF_;
+    static constexpr int THREADS = WAVES_M * WAVES_N * 64;
+    static constexpr int BM = WAVES_M * TM * 32;    // rows of A per tile
+    static constexpr int BNB = WAVES_N * TN * 32;   // rows of B per tile
+    static constexpr int LDP = BK + 8;              // LDS row pitch (bf16): 16-byte pad
+    static constexpr int CPR = BK / 8;              // 16-byte chunks per row
+    static constexpr int NA = BM * CPR / THREADS;   // A chunks per thread
+    static constexpr int NB = BNB * CPR / THREADS;  // B chunks per thread
+    static_assert(BM * CPR % THREADS == 0 && BNB * CPR % THREADS == 0, "tile / thread mismatch");
+    static_assert(TN % 2 == 0, "gate/up pairs need an even TN");
+};
+
+using Cfg1 = TileCfg<2, 2, 2, 2, 64, 2>;  // 128 rows x 128 B-rows (64 gate + 64 up)
+using Cfg2 = TileCfg<2, 2, 2, 2, 64, 2>;  // 128 rows x 128 output columns
+
+template <class C>
+constexpr int tile_cols(int mode) { return mode == 1 ? C::BNB / 2 : C::BNB; }
+
+template <int MODE, class C>
+__global__ void __launch_bounds__(C::THREADS, 1)
 gemm_bf16_kernel(GemmArgs p) {
+    constexpr int BM = C::BM, BNB = C::BNB, BK = C::BK, LDP = C::LDP, CPR = C::CPR;
+    constexpr int NA = C::NA, NB = C::NB, TM = C::TM, TN = C::TN, TH = C::THREADS;
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDP];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BNB * LDP];
-    const int G = p.E + (p.shared_inter > 0 ? 1 : 0);
-    const int nt_r = MODE == 1 ? static_cast<int>(ceil_div(p.inter, 64)) : static_cast<int>(ceil_div(p.d, 128));
-    const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, 64)) : nt_r;
+    constexpr int TC = tile_cols<C>(MODE);
+    const int nt_r = static_cast<int>(ceil_div(MODE == 1 ? p.inter : p.d, TC));
+    const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
-    if (!decode_tile(p.work, p.off, p.E, p.T, G, BM, nt_r, nt_s, t)) return;
+    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, t)) return;
     const bool shared = t.g == p.E;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = lane_id();
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
 
-    // operand geometry
     int K, n_out;
     const uint16_t* Abase;
     const uint16_t* Bbase;
@@ -193,113 +237,186 @@ gemm_bf16_kernel(GemmArgs p) {
         Bbase = shared ? static_cast<const uint16_t*>(p.ws2)
                        : static_cast<const uint16_t*>(p.w2) + static_cast<int64_t>(t.g) * p.d * p.inter;
     }
-    // per-thread load slots: 4 A rows, 4 B rows, one 16-byte k-chunk each
-    const int kc = (tid & 7) * 8;
-    const uint16_t* arow[4];
-    const uint16_t* brow[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int r = (tid >> 3) + 32 * i;
-        const int rr = r < t.rows ? r : 0;
-        int64_t src;
-        if (MODE == 1 && !shared) src = p.perm_token[t.row0 + rr];
-        else src = t.row0 + rr;
-        arow[i] = Abase + src * a_ld;
-        int64_t brow_idx;
-        if constexpr (MODE == 1) {
-            int c = t.nt * 64 + (r & 63);
-            if (c >= n_out) c = 0;
-            brow_idx = (r < 64) ? c : n_out + c;
-        } else {
-            int c = t.nt * 128 + r;
-            if (c >= n_out) c = 0;
-            brow_idx = c;
-        }
-        brow[i] = Bbase + brow_idx * K;
-    }
-    uint4 ra[4], rb[4];
-    auto gload = [&](int k0) {
-        const bool ok = k0 + kc < K;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            ra[i] = ok ? *reinterpret_cast<const uint4*>(arow[i] + k0 + kc) : make_uint4(0, 0, 0, 0);
-            rb[i] = ok ? *reinterpret_cast<const uint4*>(brow[i] + k0 + kc) : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            *reinterpret_cast<uint4*>(&As[buf][r * LDP + kc]) = ra[i];
-            *reinterpret_cast<uint4*>(&Bs[buf][r * LDP + kc]) = rb[i];
-        }
-    };
-    // B rows read by this wave: two 32-row blocks
-    int bsub[2];
+    // this thread's 16-byte load slots: chunk c = tid + TH * i -> row c / CPR, k-chunk c % CPR.
+    // Element offsets from the block's operand bases (32-bit: operands are < 2^31 elements);
+    // rows past the tile's end re-read its first row and are never stored.
+    const int kc = (tid % CPR) * 8;
+    int aoff[NA], boff[NB];
     if constexpr (MODE == 1) {
-        bsub[0] = wn * 32;
-        bsub[1] = 64 + wn * 32;
-    } else {
-        bsub[0] = wn * 64;
-        bsub[1] = wn * 64 + 32;
+        if (!shared) {  // routed GEMM1 gathers its rows of x through the permutation
+            int src[NA];
+#pragma unroll
+            for (int i = 0; i < NA; ++i) {
+                const int r = (tid + TH * i) / CPR;
+                src[i] = p.perm_token[t.row0 + (r < t.rows ? r : 0)];
+            }
+#pragma unroll
+            for (int i = 0; i < NA; ++i) aoff[i] = src[i] * static_cast<int>(a_ld) + kc;
+        }
     }
-    f32x16_t acc[2][2];
+    if (MODE != 1 || shared) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NA; ++i) {
+            const int r = (tid + TH * i) / CPR;
+            aoff[i] = static_cast<int>(t.row0 + (r < t.rows ? r : 0)) * static_cast<int>(a_ld) + kc;
+        }
+    }
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+    for (int i = 0; i < NB; ++i) {
+        const int r = (tid + TH * i) / CPR;
+        int bi;
+        if constexpr (MODE == 1) {  // rows [0, BNB/2) gate, [BNB/2, BNB) the matching up rows
+            int c = t.nt * TC + (r % (BNB / 2));
+            if (c >= n_out) c = 0;
+            bi = r < BNB / 2 ? c : n_out + c;
+        } else {
+            int c = t.nt * TC + r;
+            if (c >= n_out) c = 0;
+            bi = c;
+        }
+        boff[i] = bi * K + kc;
+    }
+    // Buffer loads (raw, 16 bytes): the descriptor's record count bounds every
+    // access, and a chunk past K (only in a last, partial K step) is given an
+    // offset beyond it, so the hardware returns zeros without a branch.
+    int64_t a_rows, b_rows;
+    if constexpr (MODE == 1) {
+        a_rows = p.T;  // rows of x
+        b_rows = 2 * static_cast<int64_t>(n_out);
+    } else {
+        a_rows = shared ? p.T : p.T * p.k;  // rows of H
+        b_rows = p.d;
+    }
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(Abase), 0, static_cast<int>(a_rows * a_ld * 2), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(Bbase), 0, static_cast<int>(b_rows * K * 2), kBufferFlags);
+    uint4 ra[C::PF][NA], rb[C::PF][NB];
+    auto gload = [&](int set, int k0) {
+        const bool ok = k0 + kc < K;  // K % 8 == 0: a chunk is all in or all out
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int vo = ok ? (aoff[i] + k0) * 2 : kOutOfRange;
+            ra[set][i] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, vo, 0, 0));
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int vo = ok ? (boff[i] + k0) * 2 : kOutOfRange;
+            rb[set][i] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0));
+        }
+    };
+    auto sstore = [&](int set, int buf) {
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int c = tid + TH * i;
+            *reinterpret_cast<uint4*>(&As[buf][(c / CPR) * LDP + kc]) = ra[set][i];
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int c = tid + TH * i;
+            *reinterpret_cast<uint4*>(&Bs[buf][(c / CPR) * LDP + kc]) = rb[set][i];
+        }
+    };
+    // B rows of this wave: TN blocks of 32 (MODE 1: TN/2 gate blocks then the matching up blocks)
+    int bsub[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        if constexpr (MODE == 1)
+            bsub[j] = (j < TN / 2) ? (wn * (TN / 2) + j) * 32 : BNB / 2 + (wn * (TN / 2) + j - TN / 2) * 32;
+        else
+            bsub[j] = (wn * TN + j) * 32;
+    }
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
 
-    const int nk = static_cast<int>(ceil_div(K, BK));
-    gload(0);
-    sstore(0);
-    __syncthreads();
     const int half = lane >> 5, l32 = lane & 31;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) gload((kt + 1) * BK);
+    // One K step: fragments from LDS, then the MFMAs (the compiler interleaves them).
+    auto compute = [&](int buf) {
+        bf16x8_t af[BK / 16][TM], bfr[BK / 16][TN];
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             const int kk = ks * 16 + half * 8;
-            bf16x8_t af[2], bfr[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                af[i] = *reinterpret_cast<const bf16x8_t*>(&As[cur][(wm * 64 + i * 32 + l32) * LDP + kk]);
+            for (int i = 0; i < TM; ++i)
+                af[ks][i] = *reinterpret_cast<const bf16x8_t*>(&As[buf][((wm * TM + i) * 32 + l32) * LDP + kk]);
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                bfr[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[cur][(bsub[j] + l32) * LDP + kk]);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            for (int j = 0; j < TN; ++j)
+                bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][(bsub[j] + l32) * LDP + kk]);
         }
-        if (kt + 1 < nk) sstore(cur ^ 1);
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+    };
+
+    // The K loop has no data-dependent branches: loads past K come back as
+    // zeros (see gload), so every step issues the same instruction stream.
+    // Scheduling barriers keep each step's global loads ahead of its MFMAs.
+    const int nk = static_cast<int>(ceil_div(K, BK));
+    if constexpr (C::PF == 1) {
+        gload(0, 0);
+        sstore(0, 0);
         __syncthreads();
+        for (int kt = 0; kt < nk; ++kt) {
+            gload(0, (kt + 1) * BK);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(kt & 1);
+            __builtin_amdgcn_sched_barrier(0);
+            sstore(0, (kt + 1) & 1);
+            __syncthreads();
+        }
+    } else {
+        // loads for step kt + 2 are issued before step kt's MFMAs and land in
+        // LDS after step kt + 1's: two steps of MFMA work cover their latency
+        gload(0, 0);
+        gload(1, BK);
+        sstore(0, 0);
+        __syncthreads();
+        int kt = 0;
+        for (; kt + 1 < nk; kt += 2) {
+            gload(0, (kt + 2) * BK);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(0);
+            __builtin_amdgcn_sched_barrier(0);
+            sstore(1, 1);
+            __syncthreads();
+            gload(1, (kt + 3) * BK);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(1);
+            __builtin_amdgcn_sched_barrier(0);
+            sstore(0, 0);
+            __syncthreads();
+        }
+        if (kt < nk) compute(0);
     }
 
     // epilogue: element v of a 32x32 tile sits at row 8*(v/4) + 4*half + v%4, column l32
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            const int r = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+            const int r = (wm * TM + i) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
             if (r >= t.rows) continue;
             const int64_t grow = t.row0 + r;
             if constexpr (MODE == 1) {
-                const int c = t.nt * 64 + wn * 32 + l32;
-                if (c < n_out) {
-                    const float h = silu(acc[i][0][v]) * acc[i][1][v];
-                    uint16_t* H = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
-                    H[grow * n_out + c] = f32_to_bf16(h);
+                uint16_t* H = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
+#pragma unroll
+                for (int j = 0; j < TN / 2; ++j) {
+                    const int c = t.nt * TC + (wn * (TN / 2) + j) * 32 + l32;
+                    if (c < n_out) H[grow * n_out + c] = f32_to_bf16(silu(acc[i][j][v]) * acc[i][j + TN / 2][v]);
                 }
             } else {
+                uint16_t* Y = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    const int c = t.nt * 128 + wn * 64 + j * 32 + l32;
-                    if (c < n_out) {
-                        uint16_t* Y = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
-                        Y[grow * n_out + c] = f32_to_bf16(acc[i][j][v]);
-                    }
+                for (int j = 0; j < TN; ++j) {
+                    const int c = t.nt * TC + (wn * TN + j) * 32 + l32;
+                    if (c < n_out) Y[grow * n_out + c] = f32_to_bf16(acc[i][j][v]);
                 }
             }
         }
@@ -314,11 +431,10 @@ gemm_f32_kernel(GemmArgs p) {
     __shared__ float As[FBK][FBM + 4];
     __shared__ float Bs[FBK][FBNB + 4];
     __shared__ float Cs[FBM][FBNB + 1];
-    const int G = p.E + (p.shared_inter > 0 ? 1 : 0);
     const int nt_r = MODE == 1 ? static_cast<int>(ceil_div(p.inter, 32)) : static_cast<int>(ceil_div(p.d, 64));
     const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, 32)) : nt_r;
     Tile t;
-    if (!decode_tile(p.work, p.off, p.E, p.T, G, FBM, nt_r, nt_s, t)) return;
+    if (!decode_tile(p.work, p.off, p.E, p.T, FBM, nt_r, nt_s, t)) return;
     const bool shared = t.g == p.E;
     const int tid = threadIdx.x;
     int K, n_out;
@@ -452,6 +568,7 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work) {
     g.T = a.T;
     g.d = a.d;
     g.E = a.E;
+    g.k = a.k;
     g.inter = a.inter;
     g.shared_inter = a.shared_inter;
     g.x = a.x;
@@ -469,26 +586,27 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work) {
     return g;
 }
 
-// Upper bound on the work items of one GEMM (host side; sizes the grid).
+// Grid size: 8 XCD ranges, each at most a bound on the routed items over 8
+// plus the shared items over 8 (host side; the exact split is made on the device).
 int64_t work_bound(int64_t T, int k, int E, int bm, int nt_r, int nt_s, bool has_shared) {
     const int64_t R = T * k;
-    int64_t m_r = ceil_div(R, bm) + E;
-    int64_t b = m_r * nt_r;
-    if (has_shared) b += ceil_div(T, bm) * nt_s;
-    return ceil_div(b, 8) * 8;
+    const int64_t routed = (ceil_div(R, bm) + E) * nt_r;
+    const int64_t shared = has_shared ? ceil_div(T, bm) * nt_s : 0;
+    return 8 * (ceil_div(routed, 8) + ceil_div(shared, 8));
 }
 
 struct Plan {
-    int bm, nt1_r, nt1_s, nt2;
+    int bm, bm2, nt1_r, nt1_s, nt2;
     bool has_shared;
 };
 
 Plan plan_of(const ExpertArgs& a) {
     Plan p;
     const bool bf16 = a.act_dtype == 1;
-    p.bm = bf16 ? BM : FBM;
-    const int tn1 = bf16 ? 64 : 32;   // H columns per GEMM1 tile
-    const int tn2 = bf16 ? 128 : 64;  // output columns per GEMM2 tile
+    p.bm = bf16 ? Cfg1::BM : FBM;
+    p.bm2 = bf16 ? Cfg2::BM : FBM;
+    const int tn1 = bf16 ? tile_cols<Cfg1>(1) : 32;  // H columns per GEMM1 tile
+    const int tn2 = bf16 ? tile_cols<Cfg2>(2) : 64;  // output columns per GEMM2 tile
     p.nt1_r = static_cast<int>(ceil_div(a.inter, tn1));
     p.nt1_s = static_cast<int>(ceil_div(a.shared_inter, tn1));
     p.nt2 = static_cast<int>(ceil_div(a.d, tn2));
@@ -515,7 +633,7 @@ hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(512), 0, stream, a.expert_offsets, a.E, a.T,
-                       p.has_shared ? 1 : 0, p.bm, p.nt2, p.nt2, w.work2);
+                       p.has_shared ? 1 : 0, p.bm2, p.nt2, p.nt2, w.work2);
     return hipGetLastError();
 }
 
@@ -525,7 +643,7 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t strea
     const GemmArgs g = make_args(a, w, w.work1);
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared)));
     if (a.act_dtype == 1)
-        hipLaunchKernelGGL(gemm_bf16_kernel<1>, grid, dim3(kThreads), 0, stream, g);
+        hipLaunchKernelGGL((gemm_bf16_kernel<1, Cfg1>), grid, dim3(Cfg1::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<1>, grid, dim3(kThreads), 0, stream, g);
     return hipGetLastError();
@@ -535,9 +653,9 @@ hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t strea
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
     const Plan p = plan_of(a);
     const GemmArgs g = make_args(a, w, w.work2);
-    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt2, p.nt2, p.has_shared)));
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm2, p.nt2, p.nt2, p.has_shared)));
     if (a.act_dtype == 1)
-        hipLaunchKernelGGL(gemm_bf16_kernel<2>, grid, dim3(kThreads), 0, stream, g);
+        hipLaunchKernelGGL((gemm_bf16_kernel<2, Cfg2>), grid, dim3(Cfg2::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<2>, grid, dim3(kThreads), 0, stream, g);
     return hipGetLastError();
