@@ -7,10 +7,11 @@
 // totals W[m] = sum_j M_jm; bins only enter in the small finalize step.
 //   mi_partial : (sample, chunk) blocks; threads own expert columns, rows are
 //                split over row groups; fp64 sums, fixed-order LDS reduction.
-//   mi_finalize: one block; chunk partials in chunk order, bin sums in
-//                ascending expert order, then S-bar (Eq. 12), the joint (Eq. 13),
-//                I_i (Eq. 14), the loss (Eq. 15) and the gradient
-//                coefficients c[m][k] = (log r_mk - I_i) / (N_B W_m Z).
+//   mi_finalize: one block per sample; chunk partials in chunk order, bin
+//                sums in ascending expert order, then S-bar (Eq. 12), the joint
+//                (Eq. 13), I_i (Eq. 14) and the gradient coefficients
+//                c[m][k] = (log r_mk - I_i) / (N_B W_m Z); the loss (Eq. 15)
+//                is summed in sample order by the next kernel.
 //   mi_grad    : one wave per token; G_k = bin masses of the token,
 //                h_k = sum_m M_jm c[m][k], dlogit_e = s g_e (h_bin(e) - sum_k G_k h_k)
 //                with s = -grad_scale / N_batch.
@@ -123,13 +124,17 @@ mi_partial_kernel(const float* __restrict__ probs, const float* __restrict__ M, 
     }
 }
 
-// One block; samples in turn. Thread (m, k) owns one cell of the joint;
-// sums over cells are taken by every thread in the same fixed order from LDS.
+// One block per sample. The chunk partials are summed by (expert, chunk
+// group) threads in chunk order, the groups combined in a fixed order; then
+// thread (m, k) owns one cell of the joint, and sums over cells are taken by
+// every thread in the same fixed order from LDS.
 __global__ void __launch_bounds__(kMiThreads)
 mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batch, int C,
                    const int32_t* __restrict__ e2b, int n_bins, const double* __restrict__ part,
                    double* __restrict__ coef, double* __restrict__ mi64, int32_t* __restrict__ members,
-                   float* __restrict__ mi_per_sample, float* __restrict__ loss) {
+                   float* __restrict__ mi_per_sample) {
+    __shared__ double red[kMiThreads][2];
+    __shared__ double wred[kMiThreads][2];
     __shared__ double A[2][256];
     __shared__ double P[2][64];    // S-bar, then the joint P(m, k)
     __shared__ double term[2][64];
@@ -137,91 +142,123 @@ mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batc
     __shared__ int32_t mem[256];
     const int NB = E / n_bins;
     const int tid = threadIdx.x;
+    const int i = blockIdx.x;
     // bin member lists in ascending expert order
     if (tid < n_bins) {
         const int k = tid;
         int n = 0;
         for (int e = 0; e < E; ++e)
-            if (e2b[e] == k && n < NB) {
-                mem[k * NB + n] = e;
-                members[k * NB + n] = e;
-                ++n;
+            if (e2b[e] == k && n < NB) mem[k * NB + n++] = e;
+        for (; n < NB; ++n) mem[k * NB + n] = -1;  // violated precondition (bin too small): empty slot
+    }
+    // chunk partials: thread (cg, e) sums chunks cg, cg + RG, ... in order
+    const int EP = static_cast<int>(ceil_div(E, kWave) * kWave);
+    const int RG = kMiThreads / EP;
+    const int cg = tid / EP, e = tid % EP;
+    const double* pi = part + static_cast<int64_t>(i) * C * (2 * E + 2);
+    double s0 = 0.0, s1 = 0.0, w0 = 0.0, w1 = 0.0;
+    if (cg < RG) {
+#pragma unroll 4
+        for (int c = cg; c < C; c += RG) {
+            const double* pc = pi + static_cast<int64_t>(c) * (2 * E + 2);
+            if (e < E) {
+                s0 += pc[e];
+                s1 += pc[E + e];
             }
-        for (; n < NB; ++n) {  // violated precondition (bin too small): mark the slot empty
-            mem[k * NB + n] = -1;
-            members[k * NB + n] = -1;
+            if (e == 0) {
+                w0 += pc[2 * E];
+                w1 += pc[2 * E + 1];
+            }
+        }
+    }
+    red[tid][0] = s0;
+    red[tid][1] = s1;
+    wred[tid][0] = w0;
+    wred[tid][1] = w1;
+    __syncthreads();
+    if (cg == 0) {
+        double a0 = 0.0, a1 = 0.0;
+        for (int g = 0; g < RG; ++g) {
+            a0 += red[g * EP + e][0];
+            a1 += red[g * EP + e][1];
+        }
+        if (e < E) {
+            A[0][e] = a0;
+            A[1][e] = a1;
+        }
+        if (e == 0) {
+            double t0 = 0.0, t1 = 0.0;
+            for (int g = 0; g < RG; ++g) {
+                t0 += wred[g * EP][0];
+                t1 += wred[g * EP][1];
+            }
+            Wm[0] = t0;
+            Wm[1] = t1;
         }
     }
     __syncthreads();
+    if (i == 0)
+        for (int q = tid; q < E; q += blockDim.x) members[q] = mem[q];
+    int64_t a, b;
+    sample_range(off, T, i, a, b);
     const bool cell = tid < 2 * n_bins;
     const int cm = cell ? tid / n_bins : 0, ck = cell ? tid % n_bins : 0;
-    double total = 0.0;
-    for (int i = 0; i < n_batch; ++i) {
-        int64_t a, b;
-        sample_range(off, T, i, a, b);
-        const double* pi = part + static_cast<int64_t>(i) * C * (2 * E + 2);
-        for (int e = tid; e < E; e += blockDim.x) {
-            double s0 = 0.0, s1 = 0.0;
-            for (int c = 0; c < C; ++c) {
-                s0 += pi[c * (2 * E + 2) + e];
-                s1 += pi[c * (2 * E + 2) + E + e];
-            }
-            A[0][e] = s0;
-            A[1][e] = s1;
+    // Eq. 12: S-bar[m][k] = sum_{e in B_k} A[m][e] / (N_B W_m)
+    if (cell) {
+        double s = 0.0;
+        for (int n = 0; n < NB; ++n) {
+            const int ee = mem[ck * NB + n];
+            if (ee >= 0) s += A[cm][ee];
         }
-        if (tid < 2) {
-            double t = 0.0;
-            for (int c = 0; c < C; ++c) t += pi[c * (2 * E + 2) + 2 * E + tid];
-            Wm[tid] = t;
-        }
-        __syncthreads();
-        // Eq. 12: S-bar[m][k] = sum_{e in B_k} A[m][e] / (N_B W_m)
-        if (cell) {
-            double s = 0.0;
-            for (int n = 0; n < NB; ++n) {
-                const int e = mem[ck * NB + n];
-                if (e >= 0) s += A[cm][e];
-            }
-            P[cm][ck] = (b > a && Wm[cm] > 0.0) ? s / (static_cast<double>(NB) * Wm[cm]) : 0.0;
-        }
-        __syncthreads();
-        // Eq. 13: normalise; marginals
-        double Z = 0.0;
-        for (int m = 0; m < 2; ++m)
-            for (int k = 0; k < n_bins; ++k) Z += P[m][k];
-        double pmk = 0.0, pm = 0.0, pk = 0.0;
-        if (cell && Z > 0.0) {
-            for (int k = 0; k < n_bins; ++k) pm += P[cm][k] / Z;
-            pk = P[0][ck] / Z + P[1][ck] / Z;
-            pmk = P[cm][ck] / Z;
-        }
-        // Eq. 14
-        const double lr = (cell && pmk > 0.0) ? log(pmk / (pm * pk)) : 0.0;
-        if (cell) term[cm][ck] = pmk > 0.0 ? pmk * lr : 0.0;
-        __syncthreads();
-        double I = 0.0;
-        for (int m = 0; m < 2; ++m)
-            for (int k = 0; k < n_bins; ++k) I += term[m][k];
-        if (cell) {
-            double cv = 0.0;
-            if (Wm[cm] > 0.0 && pmk > 0.0) cv = (lr - I) / (static_cast<double>(NB) * Wm[cm] * Z);
-            coef[(static_cast<int64_t>(i) * 2 + cm) * n_bins + ck] = cv;
-        }
-        if (tid == 0) {
-            mi64[i] = I;
-            mi_per_sample[i] = static_cast<float>(I);
-        }
-        total += I;
-        __syncthreads();
+        P[cm][ck] = (b > a && Wm[cm] > 0.0) ? s / (static_cast<double>(NB) * Wm[cm]) : 0.0;
     }
-    if (tid == 0) loss[0] = static_cast<float>(-total / n_batch);
+    __syncthreads();
+    // Eq. 13: normalise; marginals
+    double Z = 0.0;
+    for (int m = 0; m < 2; ++m)
+        for (int k = 0; k < n_bins; ++k) Z += P[m][k];
+    double pmk = 0.0, pm = 0.0, pk = 0.0;
+    if (cell && Z > 0.0) {
+        for (int k = 0; k < n_bins; ++k) pm += P[cm][k] / Z;
+        pk = P[0][ck] / Z + P[1][ck] / Z;
+        pmk = P[cm][ck] / Z;
+    }
+    // Eq. 14
+    const double lr = (cell && pmk > 0.0) ? log(pmk / (pm * pk)) : 0.0;
+    if (cell) term[cm][ck] = pmk > 0.0 ? pmk * lr : 0.0;
+    __syncthreads();
+    double I = 0.0;
+    for (int m = 0; m < 2; ++m)
+        for (int k = 0; k < n_bins; ++k) I += term[m][k];
+    if (cell) {
+        double cv = 0.0;
+        if (Wm[cm] > 0.0 && pmk > 0.0) cv = (lr - I) / (static_cast<double>(NB) * Wm[cm] * Z);
+        coef[(static_cast<int64_t>(i) * 2 + cm) * n_bins + ck] = cv;
+    }
+    if (tid == 0) {
+        mi64[i] = I;
+        mi_per_sample[i] = static_cast<float>(I);
+    }
+}
+
+// Eq. 15 for one layer: loss = -(1 / N_batch) sum_i I_i, summed in sample order.
+__device__ __forceinline__ void write_loss(const double* mi64, int n_batch, float* loss) {
+    double s = 0.0;
+    for (int i = 0; i < n_batch; ++i) s += mi64[i];
+    loss[0] = static_cast<float>(-s / n_batch);
+}
+
+__global__ void mi_loss_kernel(const double* __restrict__ mi64, int n_batch, float* __restrict__ loss) {
+    if (threadIdx.x == 0) write_loss(mi64, n_batch, loss);
 }
 
 __global__ void __launch_bounds__(kMiThreads)
 mi_grad_kernel(const float* __restrict__ probs, const float* __restrict__ M, int64_t T, int E,
                const int32_t* __restrict__ off, int n_batch, const int32_t* __restrict__ e2b,
                int n_bins, const int32_t* __restrict__ members, const double* __restrict__ coef,
-               double scale, float* __restrict__ dlogits) {
+               double scale, float* __restrict__ dlogits, const double* __restrict__ mi64,
+               float* __restrict__ loss) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) write_loss(mi64, n_batch, loss);
     constexpr int kWaves = kMiThreads / kWave;
     __shared__ float gl[kWaves][256];
     __shared__ double hl[kWaves][64];
@@ -310,9 +347,9 @@ hipError_t launch_mi(const float* probs, const float* M, int64_t T, int E,
     hipLaunchKernelGGL(mi_partial_kernel, dim3(w.C, n_batch), dim3(kMiThreads), 0, stream, probs, M,
                        T, E, sample_offsets, w.C, w.part);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    hipLaunchKernelGGL(mi_finalize_kernel, dim3(1), dim3(kMiThreads), 0, stream, T, E,
+    hipLaunchKernelGGL(mi_finalize_kernel, dim3(n_batch), dim3(kMiThreads), 0, stream, T, E,
                        sample_offsets, n_batch, w.C, expert_to_bin, n_bins, w.part, w.coef, w.mi,
-                       w.members, mi_per_sample, loss);
+                       w.members, mi_per_sample);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if (dlogits != nullptr) {
         int64_t blocks = ceil_div(T, kMiThreads / kWave);
@@ -320,9 +357,11 @@ hipError_t launch_mi(const float* probs, const float* M, int64_t T, int E,
         const double scale = -static_cast<double>(grad_scale) / n_batch;
         hipLaunchKernelGGL(mi_grad_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kMiThreads), 0,
                            stream, probs, M, T, E, sample_offsets, n_batch, expert_to_bin, n_bins,
-                           w.members, w.coef, scale, dlogits);
-        if ((err = hipGetLastError()) != hipSuccess) return err;
+                           w.members, w.coef, scale, dlogits, w.mi, loss);
+    } else {
+        hipLaunchKernelGGL(mi_loss_kernel, dim3(1), dim3(64), 0, stream, w.mi, n_batch, loss);
     }
+    if ((err = hipGetLastError()) != hipSuccess) return err;
     return hipSuccess;
 }
 

@@ -1,12 +1,13 @@
 // Router: logits z = W_gate x (+ b), full softmax g and top-k (Sec. 3.1).
 //
-// One workgroup (8 waves) owns 32 tokens and every expert. For bf16
-// activations the logits are fp32-faithful on the matrix cores: the fp32
-// router weights are split into three bf16 terms (hi + mid + lo reproduces
-// the weight to ~2^-24), each product with the exact bf16 activation is exact,
-// and v_mfma_f32_32x32x16_bf16 accumulates in fp32. The eight waves split the
+// One workgroup (8 waves) owns 16 tokens and every expert, so a 4096-token
+// batch already spreads over 256 workgroups. For bf16 activations the logits
+// are fp32-faithful on the matrix cores: the fp32 router weights are split
+// into three bf16 terms (hi + mid + lo reproduces the weight to ~2^-24), each
+// product with the exact bf16 activation is exact, and
+// v_mfma_f32_16x16x32_bf16 accumulates in fp32. The eight waves split the
 // hidden dimension; their partial tiles are summed in LDS in a fixed order,
-// then every wave runs the softmax and a wave-wide top-k for 4 tokens.
+// then every wave runs the softmax and a wave-wide top-k for 2 tokens.
 // For fp32 activations the dot products are accumulated in fp64.
 #include "common.h"
 #include "kernels.h"
@@ -15,17 +16,12 @@ namespace smoes {
 
 namespace {
 
-constexpr int kRouterTokens = 32;
+constexpr int kRouterTokens = 16;
 constexpr int kRouterWaves = 8;
 constexpr int kRouterThreads = kRouterWaves * 64;
-constexpr size_t kRouterLdsMax = 65536;
+constexpr int kRouterSlots = 4;  // LDS tree buffers of [16][E_pad] floats (<= 64 KB)
 
-// Tree buffers that fit the LDS budget: up to 4, at least 2.
-__host__ __device__ inline int router_slots(int E_pad) {
-    const int per = kRouterTokens * E_pad * static_cast<int>(sizeof(float));
-    const int s = static_cast<int>(kRouterLdsMax / per);
-    return s >= 4 ? 4 : (s < 2 ? 2 : s);
-}
+__host__ __device__ inline int router_epad(int E) { return static_cast<int>(ceil_div(E, 16) * 16); }
 
 // w_gate [E, d] f32 -> wsplit [3][E_pad][d] bf16 (hi, mid, lo); rows >= E are zero.
 __global__ void split_wgate_kernel(const float* __restrict__ w, int E, int E_pad, int d,
@@ -46,50 +42,54 @@ __global__ void split_wgate_kernel(const float* __restrict__ w, int E, int E_pad
     }
 }
 
-// Logits of one wave over its share of the hidden dimension (k-steps
-// s = wave, wave + 8, ...), bf16x3 MFMA with the next step's fragments
-// loaded before the current step's MFMAs; then a fixed-order tree over the 8
-// waves through LDS (wave w adds wave w + half, half = 4, 2, 1), using `slots`
-// buffers of [32][E_pad] floats. The logits end in buffer 0.
-// Output layout of a 32x32 MFMA tile (lane l, element v):
-//   column = l % 32, row = 8 * (v / 4) + 4 * (l / 32) + (v % 4).
+// Logits of one wave over its share of the hidden dimension (k-steps of 32,
+// s = wave, wave + 8, ...), bf16x3 MFMA; for up to 6 expert tiles the next
+// step's fragments are loaded before the current step's MFMAs. Then a
+// fixed-order tree over the 8 waves through LDS (wave w adds wave w + h,
+// h = 4, 2, 1). The logits end in buffer 0.
+// 16x16x32 operands: lane l holds row (A) / column (B) l % 16 at k = 8 (l / 16) + 0..7;
+// result element i of lane l sits at row 4 (l / 16) + i, column l % 16.
 template <int NT>
 __device__ void router_mfma_logits(const uint16_t* __restrict__ x, int64_t T, int d,
                                    const uint16_t* __restrict__ wsplit, int E_pad,
-                                   int64_t tok0, int wave, int slots, float* __restrict__ buf) {
+                                   int64_t tok0, int wave, float* __restrict__ buf) {
     const int lane = lane_id();
-    const int half = lane >> 5;
-    const int r = lane & 31;
+    const int quad = lane >> 4;
+    const int r = lane & 15;
     int64_t tok = tok0 + r;
     if (tok >= T) tok = T - 1;
     const uint16_t* xrow = x + tok * d;
     const int64_t part = static_cast<int64_t>(E_pad) * d;
-    f32x16_t acc[NT];
+    f32x4_t acc[NT];
 #pragma unroll
-    for (int n = 0; n < NT; ++n) acc[n] = f32x16_t{};
-    const int nsteps = static_cast<int>(ceil_div(d, 16));
-    bf16x8_t a_cur = {}, b_cur[NT][3];
+    for (int n = 0; n < NT; ++n) acc[n] = f32x4_t{};
+    const int nsteps = static_cast<int>(ceil_div(d, 32));
     auto fetch = [&](int s, bf16x8_t& a, bf16x8_t (&b)[NT][3]) {
-        const int kk = s * 16 + half * 8;
+        const int kk = s * 32 + quad * 8;
         const bool valid = s < nsteps && kk < d;  // d % 8 == 0: an 8-chunk is all in or all out
-        a = valid ? *reinterpret_cast<const bf16x8_t*>(xrow + kk) : bf16x8_t{};
+        const int kc = valid ? kk : 0;
+        a = *reinterpret_cast<const bf16x8_t*>(xrow + kc);
+        if (!valid) a = bf16x8_t{};
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-            const int64_t off = static_cast<int64_t>(n * 32 + r) * d + kk;
+            const int64_t off = static_cast<int64_t>(n * 16 + r) * d + kc;
 #pragma unroll
-            for (int p = 0; p < 3; ++p)
-                b[n][p] = valid ? *reinterpret_cast<const bf16x8_t*>(wsplit + p * part + off) : bf16x8_t{};
+            for (int p = 0; p < 3; ++p) {
+                b[n][p] = *reinterpret_cast<const bf16x8_t*>(wsplit + p * part + off);
+                if (!valid) b[n][p] = bf16x8_t{};
+            }
         }
     };
     auto mfma3 = [&](const bf16x8_t& a, const bf16x8_t (&b)[NT][3]) {
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[n][2], acc[n], 0, 0, 0);  // lo
-            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[n][1], acc[n], 0, 0, 0);  // mid
-            acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[n][0], acc[n], 0, 0, 0);  // hi
+            acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[n][2], acc[n], 0, 0, 0);  // lo
+            acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[n][1], acc[n], 0, 0, 0);  // mid
+            acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[n][0], acc[n], 0, 0, 0);  // hi
         }
     };
-    if constexpr (NT <= 5) {  // register double buffer: next step's loads overlap this step's MFMAs
+    bf16x8_t a_cur, b_cur[NT][3];
+    if constexpr (NT <= 6) {  // register double buffer
         fetch(wave, a_cur, b_cur);
         for (int s = wave; s < nsteps; s += kRouterWaves) {
             bf16x8_t a_nxt, b_nxt[NT][3];
@@ -108,34 +108,31 @@ __device__ void router_mfma_logits(const uint16_t* __restrict__ x, int64_t T, in
         }
     }
     const int64_t tile = static_cast<int64_t>(kRouterTokens) * E_pad;
-    auto at = [&](int which, int n, int v) -> float& {
-        const int row = 8 * (v >> 2) + 4 * half + (v & 3);
-        return buf[which * tile + row * E_pad + n * 32 + r];
+    auto at = [&](int which, int n, int i) -> float& {
+        return buf[which * tile + (quad * 4 + i) * E_pad + n * 16 + r];
     };
     for (int h = kRouterWaves / 2; h >= 1; h >>= 1) {
-        // writers [h, 2h) hand their partials to readers [0, h), `slots` at a time
-        for (int g = 0; g < h; g += slots) {
-            if (wave >= h + g && wave < h + g + slots && wave < 2 * h) {
+        // writers [h, 2h) hand their partials to readers [0, h)
+        if (wave >= h && wave < 2 * h) {
 #pragma unroll
-                for (int n = 0; n < NT; ++n)
+            for (int n = 0; n < NT; ++n)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) at(wave - h - g, n, v) = acc[n][v];
-            }
-            __syncthreads();
-            if (wave >= g && wave < g + slots && wave < h) {
-#pragma unroll
-                for (int n = 0; n < NT; ++n)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) acc[n][v] += at(wave - g, n, v);
-            }
-            __syncthreads();
+                for (int i = 0; i < 4; ++i) at(wave - h, n, i) = acc[n][i];
         }
+        __syncthreads();
+        if (wave < h) {
+#pragma unroll
+            for (int n = 0; n < NT; ++n)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[n][i] += at(wave, n, i);
+        }
+        __syncthreads();
     }
     if (wave == 0) {
 #pragma unroll
         for (int n = 0; n < NT; ++n)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) at(0, n, v) = acc[n][v];
+            for (int i = 0; i < 4; ++i) at(0, n, i) = acc[n][i];
     }
 }
 
@@ -146,8 +143,8 @@ router_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restr
               int k, int renorm, float* __restrict__ logits, float* __restrict__ probs,
               int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
     extern __shared__ float smem[];
-    // bf16 path: smem = [slots][32][E_pad] tree buffers, the logits end in the first;
-    // fp32 path: smem = [32][E_pad] logits.
+    // bf16 path: smem = [4][16][E_pad] tree buffers, the logits end in the first;
+    // fp32 path: smem = [16][E_pad] logits.
     float* zrow = smem;
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -155,8 +152,7 @@ router_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restr
     const int ntok = static_cast<int>(T - tok0 < kRouterTokens ? T - tok0 : kRouterTokens);
 
     if constexpr (BF16) {
-        router_mfma_logits<NT>(static_cast<const uint16_t*>(x), T, d, wsplit, E_pad, tok0, wave,
-                               router_slots(E_pad), smem);
+        router_mfma_logits<NT>(static_cast<const uint16_t*>(x), T, d, wsplit, E_pad, tok0, wave, smem);
     } else {
         const float* xf = static_cast<const float*>(x);
         for (int i = threadIdx.x; i < kRouterTokens * E_pad; i += kRouterThreads) {
@@ -174,7 +170,7 @@ router_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restr
     }
     __syncthreads();
 
-    // softmax + top-k: wave w handles tokens w, w + 8, ...
+    // softmax + top-k: wave w handles tokens w and w + 8
     const int QE = static_cast<int>(ceil_div(E, kWave));
     for (int t = wave; t < ntok; t += kRouterWaves) {
         const float* zr = zrow + t * E_pad;
@@ -265,24 +261,36 @@ hipError_t launch_router_nt(int NT, const void* x, int64_t T, int d, const float
                             int renorm, float* logits, float* probs, int32_t* topk_idx,
                             float* topk_w, hipStream_t stream) {
     const dim3 grid(static_cast<unsigned>(ceil_div(T, kRouterTokens)));
-    const size_t lds = sizeof(float) * kRouterTokens * E_pad * (BF16 ? router_slots(E_pad) : 1);
+    const size_t lds = sizeof(float) * kRouterTokens * E_pad * (BF16 ? kRouterSlots : 1);
 #define SMOES_ROUTER_CASE(N)                                                                      \
     case N:                                                                                       \
         hipLaunchKernelGGL((router_kernel<BF16, N>), grid, dim3(kRouterThreads), lds, stream, x, \
                            T, d, w_gate, wsplit, bias, E, E_pad, k, renorm, logits, probs,       \
                            topk_idx, topk_w);                                                    \
         break;
-    switch (NT) {
-        SMOES_ROUTER_CASE(1)
-        SMOES_ROUTER_CASE(2)
-        SMOES_ROUTER_CASE(3)
-        SMOES_ROUTER_CASE(4)
-        SMOES_ROUTER_CASE(5)
-        SMOES_ROUTER_CASE(6)
-        SMOES_ROUTER_CASE(7)
-        SMOES_ROUTER_CASE(8)
-        default:
-            return hipErrorInvalidValue;
+    if constexpr (BF16) {
+        switch (NT) {
+            SMOES_ROUTER_CASE(1)
+            SMOES_ROUTER_CASE(2)
+            SMOES_ROUTER_CASE(3)
+            SMOES_ROUTER_CASE(4)
+            SMOES_ROUTER_CASE(5)
+            SMOES_ROUTER_CASE(6)
+            SMOES_ROUTER_CASE(7)
+            SMOES_ROUTER_CASE(8)
+            SMOES_ROUTER_CASE(9)
+            SMOES_ROUTER_CASE(10)
+            SMOES_ROUTER_CASE(11)
+            SMOES_ROUTER_CASE(12)
+            SMOES_ROUTER_CASE(13)
+            SMOES_ROUTER_CASE(14)
+            SMOES_ROUTER_CASE(15)
+            SMOES_ROUTER_CASE(16)
+            default:
+                return hipErrorInvalidValue;
+        }
+    } else {
+        switch (1) { SMOES_ROUTER_CASE(1) }
     }
 #undef SMOES_ROUTER_CASE
     return hipGetLastError();
@@ -292,20 +300,19 @@ hipError_t launch_router_nt(int NT, const void* x, int64_t T, int d, const float
 
 size_t router_workspace_bytes(int d, int E, int x_dtype) {
     if (x_dtype != 1) return 0;
-    const int E_pad = static_cast<int>(ceil_div(E, 32) * 32);
+    const int E_pad = router_epad(E);
     return align_up(sizeof(uint16_t) * 3 * static_cast<size_t>(E_pad) * d, 256);
 }
 
 size_t router_lds_bytes(int E, int x_dtype) {
-    const int E_pad = static_cast<int>(ceil_div(E, 32) * 32);
-    return sizeof(float) * kRouterTokens * E_pad * (x_dtype == 1 ? router_slots(E_pad) : 1);
+    return sizeof(float) * kRouterTokens * router_epad(E) * (x_dtype == 1 ? kRouterSlots : 1);
 }
 
 hipError_t launch_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gate,
                         const float* bias, int E, int k, int renorm, float* logits, float* probs,
                         int32_t* topk_idx, float* topk_w, void* ws, hipStream_t stream) {
-    const int E_pad = static_cast<int>(ceil_div(E, 32) * 32);
-    const int NT = E_pad / 32;
+    const int E_pad = router_epad(E);
+    const int NT = E_pad / 16;
     if (x_dtype == 1) {
         uint16_t* wsplit = static_cast<uint16_t*>(ws);
         const int64_t n = static_cast<int64_t>(E_pad) * d;
