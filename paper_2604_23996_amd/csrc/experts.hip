@@ -12,9 +12,12 @@
 // ordered (group, super-row of 8 m-tiles, n-tile, m-tile): the tiles that
 // share a weight slice run back to back on one XCD and hit its L2.
 //
-// bf16: 128 x 128 tiles, BK = 64, 4 waves of 64 x 64 (2 x 2 MFMA
-// 32x32x16 bf16 tiles), LDS double-buffered (row pitch 72 bf16 = 144 B keeps
-// the 16-byte fragment reads conflict-free), fp32 accumulation.
+// bf16: 128 x 128 tiles, 4 waves of 64 x 64 (2 x 2 MFMA 32x32x16 bf16
+// tiles), fp32 accumulation. Operand tiles are copied HBM -> LDS by buffer
+// loads with an LDS destination (no register staging) through a three-stage
+// ring of K = 32 slices; the MFMA fragments are read back with 16-byte LDS
+// reads from XOR-swizzled rows. The results leave through LDS as 16-byte
+// row chunks.
 //   GEMM1: B rows 0..63 are gate rows, 64..127 the matching up rows, so a
 //          wave holds gate and up outputs of the same (row, column) in the
 //          same lane: the SwiGLU epilogue is register-local. H is bf16.
@@ -178,55 +181,73 @@ struct GemmArgs {
 
 // ============================================================== bf16 MFMA path
 
-// Tile shape of the bf16 GEMMs: WAVES_M x WAVES_N waves, each owning
-// TM x TN MFMA 32x32 tiles; K step BK; PF = global-load prefetch depth in
-// K steps (register staged; LDS is double-buffered).
-template <int WAVES_M_, int WAVES_N_, int TM_, int TN_, int BK_, int PF_>
-struct TileCfg {
-    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, TM = TM_, TN = TN_, BK = BK_, PF = PF_;
+// The operand tiles go straight from HBM to LDS (buffer_load ... lds: each wave instruction writes
+// 64 x 16 bytes contiguously), through a ring of STAGES buffers, with one
+// barrier per K step and no VGPR staging. Rows are unpadded (BK bf16) and the
+// 16-byte chunks of a row are XOR-swizzled with (row / SWZ_DIV) % CPR so that
+// the MFMA fragment reads of consecutive rows fall in different banks.
+template <int WAVES_M_, int WAVES_N_, int TM_, int TN_, int BK_, int STAGES_, int SWZ_DIV_>
+struct DmaCfg {
+    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, TM = TM_, TN = TN_, BK = BK_;
+    static constexpr int STAGES = STAGES_, SWZ_DIV = SWZ_DIV_;
     static constexpr int THREADS = WAVES_M * WAVES_N * 64;
-    static constexpr int BM = WAVES_M * TM * 32;    // rows of A per tile
-    static constexpr int BNB = WAVES_N * TN * 32;   // rows of B per tile
-    static constexpr int LDP = BK + 8;              // LDS row pitch (bf16): 16-byte pad
-    static constexpr int CPR = BK / 8;              // 16-byte chunks per row
-    static constexpr int NA = BM * CPR / THREADS;   // A chunks per thread
-    static constexpr int NB = BNB * CPR / THREADS;  // B chunks per thread
-    static_assert(BM * CPR % THREADS == 0 && BNB * CPR % THREADS == 0, "tile / thread mismatch");
+    static constexpr int BM = WAVES_M * TM * 32;
+    static constexpr int BNB = WAVES_N * TN * 32;
+    static constexpr int CPR = BK / 8;                 // 16-byte chunks per row
+    static constexpr int RPI = 64 / CPR;               // rows per DMA instruction (1 KB)
+    static constexpr int IA = BM / RPI / (THREADS / 64);   // A instructions per wave per stage
+    static constexpr int IB = BNB / RPI / (THREADS / 64);  // B instructions per wave per stage
+    static_assert(IA * RPI * (THREADS / 64) == BM && IB * RPI * (THREADS / 64) == BNB, "tile / wave mismatch");
     static_assert(TN % 2 == 0, "gate/up pairs need an even TN");
 };
 
-using Cfg1 = TileCfg<2, 2, 2, 2, 64, 2>;  // 128 rows x 128 B-rows (64 gate + 64 up)
-using Cfg2 = TileCfg<2, 2, 2, 2, 64, 2>;  // 128 rows x 128 output columns
+// 128 rows x 128 B-rows (GEMM1: 64 gate + 64 up rows; GEMM2: 128 output columns),
+// 4 waves of 64 x 64, K step 32, three-stage ring (48 KB of LDS: 3 blocks per CU)
+using DCfg = DmaCfg<2, 2, 2, 2, 32, 3, 2>;
 
 template <class C>
 constexpr int tile_cols(int mode) { return mode == 1 ? C::BNB / 2 : C::BNB; }
 
+template <class C>
+__device__ __forceinline__ int dma_slot(int row, int chunk) {
+    return chunk ^ ((row / C::SWZ_DIV) % C::CPR);
+}
+
+// s_waitcnt with vmcnt(N) and lgkmcnt(0) (gfx9 encoding; expcnt left free)
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | 0x70);
+}
+
 template <int MODE, class C>
 __global__ void __launch_bounds__(C::THREADS, 1)
-gemm_bf16_kernel(GemmArgs p) {
-    constexpr int BM = C::BM, BNB = C::BNB, BK = C::BK, LDP = C::LDP, CPR = C::CPR;
-    constexpr int NA = C::NA, NB = C::NB, TM = C::TM, TN = C::TN, TH = C::THREADS;
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDP];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BNB * LDP];
+gemm_bf16_dma_kernel(GemmArgs p) {
+    constexpr int BM = C::BM, BNB = C::BNB, BK = C::BK, CPR = C::CPR, RPI = C::RPI;
+    constexpr int TM = C::TM, TN = C::TN, IA = C::IA, IB = C::IB, ST = C::STAGES;
+    constexpr int A_BYTES = BM * BK * 2, B_BYTES = BNB * BK * 2;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[ST][A_BYTES + B_BYTES];
     constexpr int TC = tile_cols<C>(MODE);
     const int nt_r = static_cast<int>(ceil_div(MODE == 1 ? p.inter : p.d, TC));
     const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
     if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, t)) return;
     const bool shared = t.g == p.E;
-    const int tid = threadIdx.x;
-    const int wave = tid / kWave, lane = lane_id();
+    const int wave = threadIdx.x / kWave, lane = lane_id();
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
 
     int K, n_out;
     const uint16_t* Abase;
     const uint16_t* Bbase;
-    int64_t a_ld;
+    int a_ld;
+    int64_t a_rows, b_rows;
     if constexpr (MODE == 1) {
         K = p.d;
         n_out = shared ? p.shared_inter : p.inter;
         Abase = static_cast<const uint16_t*>(p.x);
         a_ld = p.d;
+        a_rows = p.T;
+        b_rows = 2 * static_cast<int64_t>(n_out);
         Bbase = shared ? static_cast<const uint16_t*>(p.ws13)
                        : static_cast<const uint16_t*>(p.w13) + static_cast<int64_t>(t.g) * 2 * p.inter * p.d;
     } else {
@@ -234,90 +255,65 @@ gemm_bf16_kernel(GemmArgs p) {
         n_out = p.d;
         Abase = shared ? static_cast<const uint16_t*>(p.h_s) : static_cast<const uint16_t*>(p.h_r);
         a_ld = K;
+        a_rows = shared ? p.T : p.T * p.k;
+        b_rows = p.d;
         Bbase = shared ? static_cast<const uint16_t*>(p.ws2)
                        : static_cast<const uint16_t*>(p.w2) + static_cast<int64_t>(t.g) * p.d * p.inter;
-    }
-    // this thread's 16-byte load slots: chunk c = tid + TH * i -> row c / CPR, k-chunk c % CPR.
-    // Element offsets from the block's operand bases (32-bit: operands are < 2^31 elements);
-    // rows past the tile's end re-read its first row and are never stored.
-    const int kc = (tid % CPR) * 8;
-    int aoff[NA], boff[NB];
-    if constexpr (MODE == 1) {
-        if (!shared) {  // routed GEMM1 gathers its rows of x through the permutation
-            int src[NA];
-#pragma unroll
-            for (int i = 0; i < NA; ++i) {
-                const int r = (tid + TH * i) / CPR;
-                src[i] = p.perm_token[t.row0 + (r < t.rows ? r : 0)];
-            }
-#pragma unroll
-            for (int i = 0; i < NA; ++i) aoff[i] = src[i] * static_cast<int>(a_ld) + kc;
-        }
-    }
-    if (MODE != 1 || shared) {
-#pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int r = (tid + TH * i) / CPR;
-            aoff[i] = static_cast<int>(t.row0 + (r < t.rows ? r : 0)) * static_cast<int>(a_ld) + kc;
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-        const int r = (tid + TH * i) / CPR;
-        int bi;
-        if constexpr (MODE == 1) {  // rows [0, BNB/2) gate, [BNB/2, BNB) the matching up rows
-            int c = t.nt * TC + (r % (BNB / 2));
-            if (c >= n_out) c = 0;
-            bi = r < BNB / 2 ? c : n_out + c;
-        } else {
-            int c = t.nt * TC + r;
-            if (c >= n_out) c = 0;
-            bi = c;
-        }
-        boff[i] = bi * K + kc;
-    }
-    // Buffer loads (raw, 16 bytes): the descriptor's record count bounds every
-    // access, and a chunk past K (only in a last, partial K step) is given an
-    // offset beyond it, so the hardware returns zeros without a branch.
-    int64_t a_rows, b_rows;
-    if constexpr (MODE == 1) {
-        a_rows = p.T;  // rows of x
-        b_rows = 2 * static_cast<int64_t>(n_out);
-    } else {
-        a_rows = shared ? p.T : p.T * p.k;  // rows of H
-        b_rows = p.d;
     }
     const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(Abase), 0, static_cast<int>(a_rows * a_ld * 2), kBufferFlags);
     const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(Bbase), 0, static_cast<int>(b_rows * K * 2), kBufferFlags);
-    uint4 ra[C::PF][NA], rb[C::PF][NB];
-    auto gload = [&](int set, int k0) {
-        const bool ok = k0 + kc < K;  // K % 8 == 0: a chunk is all in or all out
+
+    // Lane `lane` of this wave's q-th instruction fills LDS row R = (wave * I + q) * RPI + lane / CPR,
+    // slot lane % CPR, with the row's chunk slot ^ swizzle(R).
+    const int lrow = lane / CPR, lslot = lane % CPR;
+    int aoff[IA], boff[IB];  // element offset of the row start
+    int achk[IA], bchk[IB];  // k offset of the chunk this lane moves (after the swizzle)
 #pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int vo = ok ? (aoff[i] + k0) * 2 : kOutOfRange;
-            ra[set][i] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, vo, 0, 0));
+    for (int q = 0; q < IA; ++q) {
+        const int R = (wave * IA + q) * RPI + lrow;
+        const int rr = R < t.rows ? R : 0;
+        int src;
+        if (MODE == 1 && !shared) src = p.perm_token[t.row0 + rr];
+        else src = static_cast<int>(t.row0 + rr);
+        aoff[q] = src * a_ld;
+        achk[q] = (lslot ^ ((R / C::SWZ_DIV) % CPR)) * 8;
+    }
+#pragma unroll
+    for (int q = 0; q < IB; ++q) {
+        const int R = (wave * IB + q) * RPI + lrow;
+        int bi;
+        if constexpr (MODE == 1) {
+            int cc = t.nt * TC + (R % (BNB / 2));
+            if (cc >= n_out) cc = 0;
+            bi = R < BNB / 2 ? cc : n_out + cc;
+        } else {
+            int cc = t.nt * TC + R;
+            if (cc >= n_out) cc = 0;
+            bi = cc;
+        }
+        boff[q] = bi * K;
+        bchk[q] = (lslot ^ ((R / C::SWZ_DIV) % CPR)) * 8;
+    }
+    // a chunk past K (K % 8 == 0) gets an offset beyond the record count: the DMA writes zeros
+    auto issue = [&](int stage, int k0) {
+        uint8_t* base = lds[stage];
+#pragma unroll
+        for (int q = 0; q < IA; ++q) {
+            const int k = k0 + achk[q];
+            const int vo = k < K ? (aoff[q] + k) * 2 : kOutOfRange;
+            auto* dst = (__attribute__((address_space(3))) void*)(base + (wave * IA + q) * 1024);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < NB; ++i) {
-            const int vo = ok ? (boff[i] + k0) * 2 : kOutOfRange;
-            rb[set][i] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0));
+        for (int q = 0; q < IB; ++q) {
+            const int k = k0 + bchk[q];
+            const int vo = k < K ? (boff[q] + k) * 2 : kOutOfRange;
+            auto* dst = (__attribute__((address_space(3))) void*)(base + A_BYTES + (wave * IB + q) * 1024);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, dst, 16, vo, 0, 0, 0);
         }
     };
-    auto sstore = [&](int set, int buf) {
-#pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int c = tid + TH * i;
-            *reinterpret_cast<uint4*>(&As[buf][(c / CPR) * LDP + kc]) = ra[set][i];
-        }
-#pragma unroll
-        for (int i = 0; i < NB; ++i) {
-            const int c = tid + TH * i;
-            *reinterpret_cast<uint4*>(&Bs[buf][(c / CPR) * LDP + kc]) = rb[set][i];
-        }
-    };
-    // B rows of this wave: TN blocks of 32 (MODE 1: TN/2 gate blocks then the matching up blocks)
     int bsub[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -331,95 +327,108 @@ gemm_bf16_kernel(GemmArgs p) {
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
-
     const int half = lane >> 5, l32 = lane & 31;
-    // One K step: fragments from LDS, then the MFMAs (the compiler interleaves them).
-    auto compute = [&](int buf) {
-        bf16x8_t af[BK / 16][TM], bfr[BK / 16][TN];
+    auto compute = [&](int stage) {
+        const uint8_t* base = lds[stage];
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            const int kk = ks * 16 + half * 8;
+            const int c = ks * 2 + half;
+            bf16x8_t af[TM], bfr[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                af[ks][i] = *reinterpret_cast<const bf16x8_t*>(&As[buf][((wm * TM + i) * 32 + l32) * LDP + kk]);
+            for (int i = 0; i < TM; ++i) {
+                const int R = (wm * TM + i) * 32 + l32;
+                af[i] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + dma_slot<C>(R, c) * 16);
+            }
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][(bsub[j] + l32) * LDP + kk]);
-        }
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks)
+            for (int j = 0; j < TN; ++j) {
+                const int R = bsub[j] + l32;
+                bfr[j] = *reinterpret_cast<const bf16x8_t*>(base + A_BYTES + R * (BK * 2) + dma_slot<C>(R, c) * 16);
+            }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
     };
 
-    // The K loop has no data-dependent branches: loads past K come back as
-    // zeros (see gload), so every step issues the same instruction stream.
-    // Scheduling barriers keep each step's global loads ahead of its MFMAs.
+    // K loop: ST-stage ring. Before reading stage kt, this wave waits until at
+    // most (ST - 2) newer stages of its own loads are in flight and its LDS
+    // reads are done, then a barrier makes every wave's loads visible and
+    // frees the stage that the next loads overwrite.
+    static_assert(ST == 3, "the loop below is written for three stages");
+    constexpr int PER_STAGE = IA + IB;
     const int nk = static_cast<int>(ceil_div(K, BK));
-    if constexpr (C::PF == 1) {
-        gload(0, 0);
-        sstore(0, 0);
-        __syncthreads();
-        for (int kt = 0; kt < nk; ++kt) {
-            gload(0, (kt + 1) * BK);
-            __builtin_amdgcn_sched_barrier(0);
-            compute(kt & 1);
-            __builtin_amdgcn_sched_barrier(0);
-            sstore(0, (kt + 1) & 1);
-            __syncthreads();
-        }
-    } else {
-        // loads for step kt + 2 are issued before step kt's MFMAs and land in
-        // LDS after step kt + 1's: two steps of MFMA work cover their latency
-        gload(0, 0);
-        gload(1, BK);
-        sstore(0, 0);
-        __syncthreads();
-        int kt = 0;
-        for (; kt + 1 < nk; kt += 2) {
-            gload(0, (kt + 2) * BK);
-            __builtin_amdgcn_sched_barrier(0);
-            compute(0);
-            __builtin_amdgcn_sched_barrier(0);
-            sstore(1, 1);
-            __syncthreads();
-            gload(1, (kt + 3) * BK);
-            __builtin_amdgcn_sched_barrier(0);
-            compute(1);
-            __builtin_amdgcn_sched_barrier(0);
-            sstore(0, 0);
-            __syncthreads();
-        }
-        if (kt < nk) compute(0);
+    issue(0, 0);
+    issue(1, BK);
+    int kt = 0;
+    for (; kt + 3 <= nk; kt += 3) {
+        wait_vm_lgkm0<PER_STAGE>();
+        __builtin_amdgcn_s_barrier();
+        issue(2, (kt + 2) * BK);
+        compute(0);
+        wait_vm_lgkm0<PER_STAGE>();
+        __builtin_amdgcn_s_barrier();
+        issue(0, (kt + 3) * BK);
+        compute(1);
+        wait_vm_lgkm0<PER_STAGE>();
+        __builtin_amdgcn_s_barrier();
+        issue(1, (kt + 4) * BK);
+        compute(2);
     }
+    if (kt < nk) {
+        wait_vm_lgkm0<PER_STAGE>();
+        __builtin_amdgcn_s_barrier();
+        issue(2, (kt + 2) * BK);
+        compute(0);
+    }
+    if (kt + 1 < nk) {
+        wait_vm_lgkm0<PER_STAGE>();
+        __builtin_amdgcn_s_barrier();
+        compute(1);
+    }
+    wait_vm_lgkm0<0>();  // drain the ring: the epilogue reuses its LDS
+    __builtin_amdgcn_s_barrier();
 
-    // epilogue: element v of a 32x32 tile sits at row 8*(v/4) + 4*half + v%4, column l32
+    // Epilogue through LDS: each wave writes its bf16 results (GEMM1: the
+    // SwiGLU output) into a [BM][TC + 8] tile, then every thread stores whole
+    // 16-byte row chunks. Element v of a 32x32 MFMA tile sits at row
+    // 8*(v/4) + 4*half + v%4, column l32.
+    constexpr int OP = TC + 8;  // row pitch (bf16) of the output tile
+    static_assert(BM * OP * 2 <= ST * (A_BYTES + B_BYTES), "output tile must fit the ring");
+    uint16_t* otile = reinterpret_cast<uint16_t*>(&lds[0][0]);
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int r = (wm * TM + i) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-            if (r >= t.rows) continue;
-            const int64_t grow = t.row0 + r;
             if constexpr (MODE == 1) {
-                uint16_t* H = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
 #pragma unroll
                 for (int j = 0; j < TN / 2; ++j) {
-                    const int c = t.nt * TC + (wn * (TN / 2) + j) * 32 + l32;
-                    if (c < n_out) H[grow * n_out + c] = f32_to_bf16(silu(acc[i][j][v]) * acc[i][j + TN / 2][v]);
+                    const int c = (wn * (TN / 2) + j) * 32 + l32;
+                    otile[r * OP + c] = f32_to_bf16(silu(acc[i][j][v]) * acc[i][j + TN / 2][v]);
                 }
             } else {
-                uint16_t* Y = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
-                    const int c = t.nt * TC + (wn * TN + j) * 32 + l32;
-                    if (c < n_out) Y[grow * n_out + c] = f32_to_bf16(acc[i][j][v]);
+                    const int c = (wn * TN + j) * 32 + l32;
+                    otile[r * OP + c] = f32_to_bf16(acc[i][j][v]);
                 }
             }
         }
+    }
+    __syncthreads();
+    uint16_t* O;
+    if constexpr (MODE == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
+    else O = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
+    constexpr int CH = TC / 8;  // 16-byte chunks per output row
+    const int col0 = t.nt * TC;
+    for (int q = threadIdx.x; q < BM * CH; q += C::THREADS) {
+        const int r = q / CH, ch = q % CH;
+        const int c = col0 + ch * 8;
+        if (r < t.rows && c < n_out)  // n_out % 8 == 0: a chunk is all in or all out
+            *reinterpret_cast<uint4*>(O + (t.row0 + r) * n_out + c) =
+                *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
     }
 }
 
@@ -603,10 +612,10 @@ struct Plan {
 Plan plan_of(const ExpertArgs& a) {
     Plan p;
     const bool bf16 = a.act_dtype == 1;
-    p.bm = bf16 ? Cfg1::BM : FBM;
-    p.bm2 = bf16 ? Cfg2::BM : FBM;
-    const int tn1 = bf16 ? tile_cols<Cfg1>(1) : 32;  // H columns per GEMM1 tile
-    const int tn2 = bf16 ? tile_cols<Cfg2>(2) : 64;  // output columns per GEMM2 tile
+    p.bm = bf16 ? DCfg::BM : FBM;
+    p.bm2 = bf16 ? DCfg::BM : FBM;
+    const int tn1 = bf16 ? tile_cols<DCfg>(1) : 32;  // H columns per GEMM1 tile
+    const int tn2 = bf16 ? tile_cols<DCfg>(2) : 64;  // output columns per GEMM2 tile
     p.nt1_r = static_cast<int>(ceil_div(a.inter, tn1));
     p.nt1_s = static_cast<int>(ceil_div(a.shared_inter, tn1));
     p.nt2 = static_cast<int>(ceil_div(a.d, tn2));
@@ -643,7 +652,7 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t strea
     const GemmArgs g = make_args(a, w, w.work1);
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared)));
     if (a.act_dtype == 1)
-        hipLaunchKernelGGL((gemm_bf16_kernel<1, Cfg1>), grid, dim3(Cfg1::THREADS), 0, stream, g);
+        hipLaunchKernelGGL((gemm_bf16_dma_kernel<1, DCfg>), grid, dim3(DCfg::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<1>, grid, dim3(kThreads), 0, stream, g);
     return hipGetLastError();
@@ -655,7 +664,7 @@ hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t strea
     const GemmArgs g = make_args(a, w, w.work2);
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm2, p.nt2, p.nt2, p.has_shared)));
     if (a.act_dtype == 1)
-        hipLaunchKernelGGL((gemm_bf16_kernel<2, Cfg2>), grid, dim3(Cfg2::THREADS), 0, stream, g);
+        hipLaunchKernelGGL((gemm_bf16_dma_kernel<2, DCfg>), grid, dim3(DCfg::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<2>, grid, dim3(kThreads), 0, stream, g);
     return hipGetLastError();
