@@ -257,6 +257,10 @@ size_t smoes_workspace_bytes(const smoes_layer* desc);
  * experts (ungated, weight 1) are one SwiGLU of inner size shared_inter.
  * With SMOES_BF16 the expert GEMMs take bf16 operands with float32
  * accumulation and the intermediate activations are stored in bf16.
+ * Size limit (SMOES_ERR_SHAPE beyond it): with s the activation element size
+ * (2 for bf16, 4 for f32), each of T*d*s, T*k*max(inter, d)*s,
+ * T*shared_inter*s and 2*max(inter, shared_inter)*d*s must be below 2^31
+ * bytes (the expert GEMMs address operands with 32-bit byte offsets).
  */
 int smoes_moe_forward(const smoes_layer* desc, const smoes_layer_io* io,
                       void* workspace, size_t workspace_bytes, void* stream);

@@ -200,6 +200,16 @@ int check_layer(const smoes_layer* L) {
     if (L->inter < 16 || (L->inter % 16) != 0) return SMOES_ERR_SHAPE;
     if (L->shared_inter < 0 || (L->shared_inter % 16) != 0) return SMOES_ERR_SHAPE;
     if (L->T * L->k > INT32_MAX) return SMOES_ERR_SHAPE;
+    {
+        // The GEMMs address each operand through a buffer descriptor with 32-bit byte offsets.
+        const int64_t es = L->act_dtype == SMOES_BF16 ? 2 : 4;
+        const int64_t lim = INT32_MAX;
+        const int64_t wide = L->inter > L->d ? L->inter : L->d;
+        if (L->T * L->d * es > lim || L->T * L->k * wide * es > lim ||
+            L->T * static_cast<int64_t>(L->shared_inter) * es > lim ||
+            2 * static_cast<int64_t>(L->inter > L->shared_inter ? L->inter : L->shared_inter) * L->d * es > lim)
+            return SMOES_ERR_SHAPE;
+    }
     if (!(L->beta >= 0.0f && L->beta <= 1.0f) || !(L->var_floor >= 0.0f) || L->tau != L->tau ||
         L->grad_scale != L->grad_scale)
         return SMOES_ERR_ARG;

@@ -100,6 +100,11 @@ def test_layer_workspace_and_checks():
     for bad in (dict(inter=100), dict(inter=0), dict(shared_inter=24), dict(n_bins=3), dict(k=17),
                 dict(d=100), dict(act_dtype=5), dict(beta=2.0)):
         assert S.workspace_bytes(_spec(**bad)) == 0, bad
+    # operands past 32-bit byte offsets are refused: routed activations, x, and the shared block
+    assert S.workspace_bytes(_spec(T=1 << 17, d=2048, k=8, inter=1408)) == 0
+    assert S.workspace_bytes(_spec(T=1 << 18, d=4096, k=1, inter=512, shared_inter=0)) == 0
+    assert S.workspace_bytes(_spec(T=1 << 16, d=2048, k=2, inter=512, shared_inter=16384)) == 0
+    assert S.workspace_bytes(_spec(T=1 << 16, d=2048, k=2, inter=512, shared_inter=2816)) > 0
     desc = _spec().c()
     io = S.SmoesLayerIO()
     assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, 1 << 30, None) == S.SMOES_ERR_ARG
