@@ -115,6 +115,8 @@ def main():
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=2)
+    ap.add_argument("--rowmajor-weights", action="store_true",
+                    help="bf16 expert weights row-major instead of the packed fragment order")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB (untimed): "
                          "a known-size reference for hardware byte counters")
@@ -149,12 +151,18 @@ def main():
     spec = S.LayerSpec(T=cfg.T, d=cfg.d, E=cfg.E, k=cfg.k, inter=cfg.inter,
                        shared_inter=cfg.shared_inter, n_bins=cfg.n_bins, n_batch=cfg.n_batch,
                        act_dtype=S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32,
-                       tau=cfg.tau, beta=cfg.beta, update_stats=cfg.update_stats)
+                       tau=cfg.tau, beta=cfg.beta, update_stats=cfg.update_stats,
+                       weights_packed=cfg.dtype == W.BF16 and not args.rowmajor_weights)
     dev_in = dict(x=t(inp.x), modality_id=t(inp.modality_id), sample_offsets=t(inp.sample_offsets),
                   w_gate=t(inp.w_gate), logit_bias=t(inp.logit_bias), expert_to_bin=t(inp.expert_to_bin),
                   w13=t(inp.w13), w2=t(inp.w2), ws13=t(inp.ws13), ws2=t(inp.ws2),
                   gauss_n=torch.zeros(2, device=dev), gauss_smu=torch.zeros((2, cfg.d), device=dev),
                   gauss_ssig=torch.zeros((2, cfg.d), device=dev))
+    if spec.weights_packed:  # weights are stored packed (converted once, when they are loaded)
+        for name, which in S.WEIGHT_NAMES.items():
+            if dev_in[name] is not None:
+                dev_in[name] = S.pack_weights(spec, which, dev_in[name])
+        torch.cuda.synchronize()
     if not cfg.update_stats:  # statistics estimated once from the batch, outside the timed call
         S.modality_score(dev_in["x"], dev_in["gauss_n"], dev_in["gauss_smu"], dev_in["gauss_ssig"],
                          dev_in["modality_id"], update=True, beta=cfg.beta, tau=cfg.tau)
@@ -223,6 +231,7 @@ def main():
                                f"{cfg.n_bins} bins",
                    "T": cfg.T, "d": cfg.d, "E": cfg.E, "k": cfg.k, "inter": cfg.inter,
                    "n_shared": cfg.n_shared, "n_bins": cfg.n_bins, "update_stats": cfg.update_stats,
+                   "expert_weights": "packed" if spec.weights_packed else "row-major",
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "stages": stages,

@@ -199,6 +199,9 @@ typedef struct smoes_layer {
     float grad_scale; /* scale of dlogits */
     int renorm_topk;  /* renormalise the combine weights */
     int update_stats; /* fold the batch into the Gaussian state before scoring */
+    int weights_packed; /* 1: w13, w2, ws13, ws2 are in the packed order of smoes_pack_weights
+                           (SMOES_BF16 only); 0: row-major as in smoes_layer_io */
+    int reserved;       /* must be 0 */
 } smoes_layer;
 
 typedef struct smoes_layer_io {
@@ -264,6 +267,37 @@ size_t smoes_workspace_bytes(const smoes_layer* desc);
  */
 int smoes_moe_forward(const smoes_layer* desc, const smoes_layer_io* io,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Packed expert weights (bf16). Same products and sums as the row-major    */
+/* weights of smoes_layer_io, stored in the order the matrix cores read     */
+/* them, so each GEMM streams its weights straight into registers.          */
+/* ------------------------------------------------------------------------ */
+
+/* Which expert weight tensor (shapes as in smoes_layer_io). */
+enum smoes_weight { SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3 };
+
+/*
+ * Layout: a matrix W[N][K] (N output rows, K the contraction) becomes
+ * ceil(N/32) groups of ceil(K/16) slices of 64 x 8 bf16:
+ *   P[g][c][l][e] = W[32g + l%32][16c + 8(l/32) + e], zero outside W.
+ * w13/ws13: W = the gate and up rows interleaved by 32-row groups (group 2q =
+ * gate rows 32q..32q+31, group 2q+1 = the up rows of the same columns),
+ * N = 2*32*ceil(inter/32), K = d; one matrix per expert, experts back to
+ * back. w2/ws2: W = w2[e] ([d][inter]), N = d, K = inter.
+ * Returns the byte size of the packed tensor, 0 for an invalid desc or
+ * `which` (ws13/ws2 need shared_inter > 0).
+ */
+size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which);
+
+/*
+ * Pack one row-major bf16 weight tensor `src` (device, shape of `which` in
+ * smoes_layer_io) into `dst` (device, smoes_packed_weight_bytes bytes, not
+ * overlapping src). Asynchronous on `stream`. SMOES_ERR_ARG for a NULL
+ * pointer, act_dtype != SMOES_BF16 or an invalid `which`; other desc errors
+ * as smoes_workspace_bytes.
+ */
+int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void* dst, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Timing helpers for stage_events (hipEvent_t handles behind void*).        */

@@ -210,6 +210,8 @@ int check_layer(const smoes_layer* L) {
             2 * static_cast<int64_t>(L->inter > L->shared_inter ? L->inter : L->shared_inter) * L->d * es > lim)
             return SMOES_ERR_SHAPE;
     }
+    if ((L->weights_packed != 0 && L->weights_packed != 1) || L->reserved != 0) return SMOES_ERR_ARG;
+    if (L->weights_packed && L->act_dtype != SMOES_BF16) return SMOES_ERR_ARG;
     if (!(L->beta >= 0.0f && L->beta <= 1.0f) || !(L->var_floor >= 0.0f) || L->tau != L->tau ||
         L->grad_scale != L->grad_scale)
         return SMOES_ERR_ARG;
@@ -294,6 +296,7 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     a.inter = L->inter;
     a.shared_inter = L->shared_inter;
     a.act_dtype = L->act_dtype;
+    a.packed = L->weights_packed;
     a.x = io->x;
     a.w13 = io->w13;
     a.w2 = io->w2;
@@ -314,6 +317,37 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     SMOES_TRY(record(ev, SMOES_N_STAGES, s));
 #undef SMOES_TRY
     return SMOES_OK;
+}
+
+namespace {
+// batch, rows n, contraction k and gate/up interleave of each packed tensor; false if invalid
+bool weight_dims(const smoes_layer* L, int which, int* batch, int* n, int* k, int* interleave) {
+    switch (which) {
+        case SMOES_W13: *batch = L->E; *n = L->inter; *k = L->d; *interleave = 1; return true;
+        case SMOES_W2: *batch = L->E; *n = L->d; *k = L->inter; *interleave = 0; return true;
+        case SMOES_WS13: *batch = 1; *n = L->shared_inter; *k = L->d; *interleave = 1; return L->shared_inter > 0;
+        case SMOES_WS2: *batch = 1; *n = L->d; *k = L->shared_inter; *interleave = 0; return L->shared_inter > 0;
+        default: return false;
+    }
+}
+}  // namespace
+
+size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which) {
+    if (check_layer(desc) != SMOES_OK) return 0;
+    int batch, n, k, il;
+    if (!weight_dims(desc, which, &batch, &n, &k, &il)) return 0;
+    return static_cast<size_t>(packed_weight_elems(batch, n, k, il)) * 2;
+}
+
+int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void* dst, void* stream) {
+    const int st = check_layer(desc);
+    if (st != SMOES_OK) return st;
+    int batch, n, k, il;
+    if (desc->act_dtype != SMOES_BF16 || !weight_dims(desc, which, &batch, &n, &k, &il) || src == nullptr ||
+        dst == nullptr)
+        return SMOES_ERR_ARG;
+    return launch_pack_weights(src, batch, n, k, il, dst, as_stream(stream)) == hipSuccess ? SMOES_OK
+                                                                                           : SMOES_ERR_HIP;
 }
 
 int smoes_events_create(int n, void** events) {

@@ -165,6 +165,7 @@ __device__ __forceinline__ uint4 as_uint4(i32x4_t v) {
 struct GemmArgs {
     int64_t T;
     int d, E, k, inter, shared_inter;
+    int packed;  // expert weights in the fragment order of pack_weights_kernel
     const void* x;
     const void* w13;
     const void* w2;
@@ -432,6 +433,264 @@ gemm_bf16_dma_kernel(GemmArgs p) {
     }
 }
 
+// ============================================================== bf16 MFMA path, packed weights
+//
+// Packed weights: a matrix W[N][K] (N output rows, K contraction) is stored as
+// 16-byte fragments P[N/32][ceil(K/16)][64][8] with
+//   P[g][c][l][e] = W[32 g + l % 32][16 c + 8 (l / 32) + e]   (zero outside W),
+// which is exactly the B operand of v_mfma_f32_32x32x16_bf16 for output
+// columns 32 g .. 32 g + 31 and contraction slice 16 c .. 16 c + 15: one wave
+// loads it with one fully coalesced 1 KB buffer load, straight into VGPRs.
+// GEMM1 packs the gate and up rows interleaved by 32-row groups (group 2q =
+// gate rows 32q.., group 2q + 1 = the matching up rows), so one wave holds
+// gate and up outputs of the same (row, column) in the same lane.
+//
+// Tiles: 128 rows x 4 waves; each wave owns all 128 rows and 64 B-rows (two
+// 32-row groups: 4 x 2 MFMA tiles of 32 x 32). The weights never pass through
+// LDS and no two waves read the same weight bytes; only the token rows (x
+// gathered through perm_token for GEMM1, H for GEMM2) are staged HBM -> LDS by
+// buffer_load ... lds through a three-stage ring of K = 64 slices.
+//   GEMM1: 128 H columns per tile (32 per wave), SwiGLU in registers.
+//   GEMM2: 256 output columns per tile (64 per wave).
+constexpr int PK_BM = 128, PK_BK = 64, PK_WAVES = 4, PK_THREADS = PK_WAVES * 64, PK_ST = 3;
+constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instructions per wave per stage
+constexpr int pk_tile_cols(int mode) { return mode == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
+constexpr int pk_lds_bytes(int mode) {
+    return PK_ST * PK_BM * PK_BK * 2 > PK_BM * (pk_tile_cols(mode) + 8) * 2 ? PK_ST * PK_BM * PK_BK * 2
+                                                                             : PK_BM * (pk_tile_cols(mode) + 8) * 2;
+}
+
+// Elements of one packed matrix with n rows (n_groups = ceil(n / 32) groups) and contraction k.
+__host__ __device__ inline int64_t packed_elems(int64_t n_groups, int k) {
+    return n_groups * ((k + 15) / 16) * 512;
+}
+
+// Values that are the same in every lane but that the compiler cannot prove
+// uniform (they derive from loads): pin them to SGPRs so buffer descriptors
+// built from them stay scalar.
+__device__ __forceinline__ int uniform_int(int v) { return __builtin_amdgcn_readfirstlane(v); }
+template <class T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return reinterpret_cast<T*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+template <int MODE>
+__global__ void __launch_bounds__(PK_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+gemm_bf16_pk_kernel(GemmArgs p) {
+    constexpr int BM = PK_BM, BK = PK_BK, IA = PK_IA;
+    constexpr int A_BYTES = BM * BK * 2;
+    constexpr int TC = pk_tile_cols(MODE);
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[pk_lds_bytes(MODE)];
+    const int nt_r = static_cast<int>(ceil_div(MODE == 1 ? p.inter : p.d, TC));
+    const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
+    Tile t;
+    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, t)) return;
+    const bool shared = t.g == p.E;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
+
+    int K, n_out;
+    const uint16_t* Abase;
+    int64_t a_rows;
+    const uint16_t* Bw;  // this wave's first packed group
+    int b_groups;        // packed groups of this wave that hold weights (0..2)
+    if constexpr (MODE == 1) {
+        K = p.d;
+        n_out = shared ? p.shared_inter : p.inter;
+        Abase = static_cast<const uint16_t*>(p.x);
+        a_rows = p.T;
+        const int ng = 2 * static_cast<int>(ceil_div(n_out, 32));  // gate + up groups
+        const uint16_t* W = shared ? static_cast<const uint16_t*>(p.ws13)
+                                   : static_cast<const uint16_t*>(p.w13) + t.g * packed_elems(ng, K);
+        const int q = t.nt * PK_WAVES + wave;  // output group of this wave
+        b_groups = 2 * q < ng ? 2 : 0;
+        Bw = W + packed_elems(b_groups ? 2 * q : 0, K);
+    } else {
+        K = shared ? p.shared_inter : p.inter;
+        n_out = p.d;
+        Abase = shared ? static_cast<const uint16_t*>(p.h_s) : static_cast<const uint16_t*>(p.h_r);
+        a_rows = shared ? p.T : p.T * p.k;
+        const int ng = static_cast<int>(ceil_div(p.d, 32));
+        const uint16_t* W = shared ? static_cast<const uint16_t*>(p.ws2)
+                                   : static_cast<const uint16_t*>(p.w2) + t.g * packed_elems(ng, K);
+        const int g0 = t.nt * (2 * PK_WAVES) + 2 * wave;
+        b_groups = ng - g0 >= 2 ? 2 : (ng - g0 > 0 ? ng - g0 : 0);
+        Bw = W + packed_elems(b_groups ? g0 : 0, K);
+    }
+    K = uniform_int(K);
+    const int kc_n = (K + 15) / 16;  // packed 16-wide contraction slices per group
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(uniform_ptr(Abase)), 0, uniform_int(static_cast<int>(a_rows * K * 2)), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(uniform_ptr(Bw)), 0, uniform_int(b_groups * kc_n * 1024), kBufferFlags);
+
+    // A DMA: instruction q of this wave fills LDS rows (wave * IA + q) * 8 .. + 7 of the stage;
+    // lane moves the 16-byte chunk (lane % 8) ^ swizzle(row) of its row into slot lane % 8.
+    int aoff[IA], achk[IA];
+#pragma unroll
+    for (int q = 0; q < IA; ++q) {
+        const int R = (wave * IA + q) * 8 + lane / 8;
+        const int rr = R < t.rows ? R : 0;
+        int src;
+        if (MODE == 1 && !shared) src = p.perm_token[t.row0 + rr];
+        else src = static_cast<int>(t.row0 + rr);
+        aoff[q] = src * K;
+        achk[q] = ((lane % 8) ^ ((R / 2) % 8)) * 8;
+    }
+    auto issue_a = [&](int stage, int s) {
+#pragma unroll
+        for (int q = 0; q < IA; ++q) {
+            const int k = s * BK + achk[q];
+            const int vo = ((aoff[q] + k) * 2) | (k < K ? 0 : kOutOfRange);
+            auto* dst = (__attribute__((address_space(3))) void*)(lds + stage * A_BYTES + (wave * IA + q) * 1024);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
+        }
+    };
+    i32x4_t b0[4][2], b1[4][2];
+    auto issue_b = [&](i32x4_t (&b)[4][2], int s) {
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int kc = s * 4 + j;
+                const int vo = (((g * kc_n + kc) * 64 + lane) * 16) | (kc < kc_n ? 0 : kOutOfRange);
+                b[j][g] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0);
+            }
+    };
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int g = 0; g < 2; ++g) acc[i][g] = f32x16_t{};
+    const int half = lane >> 5, l32 = lane & 31;
+    auto compute = [&](int stage, const i32x4_t (&b)[4][2]) {
+        const uint8_t* base = lds + stage * A_BYTES;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            bf16x8_t af[4];
+            const int c = j * 2 + half;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int R = i * 32 + l32;
+                af[i] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + ((c ^ ((R / 2) % 8)) * 16));
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int g = 0; g < 2; ++g)
+                    acc[i][g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], __builtin_bit_cast(bf16x8_t, b[j][g]),
+                                                                         acc[i][g], 0, 0, 0);
+        }
+    };
+
+    // K loop. Iteration s: wait until A(s) and B(s) have landed (only A(s + 1),
+    // IA loads, may still fly; loads retire in order), barrier (every wave's
+    // DMA of A(s) is visible and every wave is done with the ring slot that
+    // A(s + 2) overwrites), issue B(s + 1) and A(s + 2), then run the MFMAs of
+    // stage s. Unrolled by two so the two B register sets stay static.
+    const int nk = static_cast<int>(ceil_div(K, BK));
+    issue_b(b0, 0);
+    issue_a(0, 0);
+    issue_a(1, 1);
+    int s = 0, slot = 0;
+    for (; s + 2 <= nk; s += 2) {
+        wait_vm_lgkm0<IA>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue_b(b1, s + 1);
+        issue_a(slot == 0 ? 2 : slot - 1, s + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(slot, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        slot = slot == 2 ? 0 : slot + 1;
+        wait_vm_lgkm0<IA>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue_b(b0, s + 2);
+        issue_a(slot == 0 ? 2 : slot - 1, s + 3);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(slot, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        slot = slot == 2 ? 0 : slot + 1;
+    }
+    if (s < nk) {
+        wait_vm_lgkm0<IA>();
+        __builtin_amdgcn_s_barrier();
+        compute(slot, b0);
+    }
+    wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
+    __builtin_amdgcn_s_barrier();
+
+    // Epilogue through LDS: [BM][TC + 8] bf16 tile, then 16-byte row chunks.
+    // Element v of a 32x32 MFMA tile sits at row 8*(v/4) + 4*half + v%4, column l32.
+    constexpr int OP = TC + 8;
+    uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int r = i * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+            if constexpr (MODE == 1) {
+                otile[r * OP + wave * 32 + l32] = f32_to_bf16(silu(acc[i][0][v]) * acc[i][1][v]);
+            } else {
+#pragma unroll
+                for (int g = 0; g < 2; ++g) otile[r * OP + wave * 64 + g * 32 + l32] = f32_to_bf16(acc[i][g][v]);
+            }
+        }
+    __syncthreads();
+    uint16_t* O;
+    if constexpr (MODE == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
+    else O = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
+    constexpr int CH = TC / 8;
+    const int col0 = t.nt * TC;
+    for (int q = threadIdx.x; q < BM * CH; q += PK_THREADS) {
+        const int r = q / CH, ch = q % CH;
+        const int c = col0 + ch * 8;
+        if (r < t.rows && c < n_out)  // n_out % 8 == 0: a chunk is all in or all out
+            *reinterpret_cast<uint4*>(O + (t.row0 + r) * n_out + c) =
+                *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+    }
+}
+
+// Pack `batch` row-major matrices into the fragment order above. interleave:
+// the source has 2 * n rows (gate rows then up rows) and packed group 2q + h
+// takes rows 32q.. of half h; otherwise the source has n rows. One thread per
+// 16-byte fragment; k % 8 == 0.
+__global__ void pack_weights_kernel(const uint16_t* __restrict__ src, int batch, int n, int k, int interleave,
+                                    uint16_t* __restrict__ dst) {
+    const int ng = interleave ? 2 * static_cast<int>(ceil_div(n, 32)) : static_cast<int>(ceil_div(n, 32));
+    const int kc_n = (k + 15) / 16;
+    const int64_t per = static_cast<int64_t>(ng) * kc_n * 64;  // fragments per matrix
+    const int64_t total = per * batch;
+    const int64_t src_rows = interleave ? 2 * static_cast<int64_t>(n) : n;
+    for (int64_t f = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; f < total;
+         f += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t b = f / per;
+        const int64_t r = f % per;
+        const int l = static_cast<int>(r % 64);
+        const int c = static_cast<int>((r / 64) % kc_n);
+        const int g = static_cast<int>(r / (64 * kc_n));
+        int row;
+        bool ok;
+        if (interleave) {
+            const int q = g / 2, h = g % 2;
+            const int rr = q * 32 + l % 32;
+            ok = rr < n;
+            row = h * n + rr;
+        } else {
+            row = g * 32 + l % 32;
+            ok = row < n;
+        }
+        const int kk = c * 16 + 8 * (l / 32);
+        ok = ok && kk < k;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (ok) v = *reinterpret_cast<const uint4*>(src + (b * src_rows + row) * k + kk);
+        *reinterpret_cast<uint4*>(dst + f * 8) = v;
+    }
+}
+
 // ============================================================== f32 FMA path
 
 template <int MODE>
@@ -580,6 +839,7 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work) {
     g.k = a.k;
     g.inter = a.inter;
     g.shared_inter = a.shared_inter;
+    g.packed = a.packed;
     g.x = a.x;
     g.w13 = a.w13;
     g.w2 = a.w2;
@@ -612,10 +872,11 @@ struct Plan {
 Plan plan_of(const ExpertArgs& a) {
     Plan p;
     const bool bf16 = a.act_dtype == 1;
-    p.bm = bf16 ? DCfg::BM : FBM;
-    p.bm2 = bf16 ? DCfg::BM : FBM;
-    const int tn1 = bf16 ? tile_cols<DCfg>(1) : 32;  // H columns per GEMM1 tile
-    const int tn2 = bf16 ? tile_cols<DCfg>(2) : 64;  // output columns per GEMM2 tile
+    const bool pk = bf16 && a.packed;
+    p.bm = pk ? PK_BM : bf16 ? DCfg::BM : FBM;
+    p.bm2 = p.bm;
+    const int tn1 = pk ? pk_tile_cols(1) : bf16 ? tile_cols<DCfg>(1) : 32;  // H columns per GEMM1 tile
+    const int tn2 = pk ? pk_tile_cols(2) : bf16 ? tile_cols<DCfg>(2) : 64;  // output columns per GEMM2 tile
     p.nt1_r = static_cast<int>(ceil_div(a.inter, tn1));
     p.nt1_s = static_cast<int>(ceil_div(a.shared_inter, tn1));
     p.nt2 = static_cast<int>(ceil_div(a.d, tn2));
@@ -651,7 +912,9 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t strea
     const Plan p = plan_of(a);
     const GemmArgs g = make_args(a, w, w.work1);
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared)));
-    if (a.act_dtype == 1)
+    if (a.act_dtype == 1 && a.packed)
+        hipLaunchKernelGGL(gemm_bf16_pk_kernel<1>, grid, dim3(PK_THREADS), 0, stream, g);
+    else if (a.act_dtype == 1)
         hipLaunchKernelGGL((gemm_bf16_dma_kernel<1, DCfg>), grid, dim3(DCfg::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<1>, grid, dim3(kThreads), 0, stream, g);
@@ -663,10 +926,27 @@ hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t strea
     const Plan p = plan_of(a);
     const GemmArgs g = make_args(a, w, w.work2);
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm2, p.nt2, p.nt2, p.has_shared)));
-    if (a.act_dtype == 1)
+    if (a.act_dtype == 1 && a.packed)
+        hipLaunchKernelGGL(gemm_bf16_pk_kernel<2>, grid, dim3(PK_THREADS), 0, stream, g);
+    else if (a.act_dtype == 1)
         hipLaunchKernelGGL((gemm_bf16_dma_kernel<2, DCfg>), grid, dim3(DCfg::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<2>, grid, dim3(kThreads), 0, stream, g);
+    return hipGetLastError();
+}
+
+int64_t packed_weight_elems(int batch, int n, int k, int interleave) {
+    const int64_t ng = interleave ? 2 * ceil_div(n, 32) : ceil_div(n, 32);
+    return batch * packed_elems(ng, k);
+}
+
+hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, void* dst,
+                               hipStream_t stream) {
+    const int64_t frags = packed_weight_elems(batch, n, k, interleave) / 8;
+    if (frags == 0) return hipSuccess;
+    const unsigned blocks = static_cast<unsigned>(ceil_div(frags, 256) < 65536 ? ceil_div(frags, 256) : 65536);
+    hipLaunchKernelGGL(pack_weights_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<const uint16_t*>(src),
+                       batch, n, k, interleave, static_cast<uint16_t*>(dst));
     return hipGetLastError();
 }
 

@@ -42,6 +42,7 @@ hipError_t launch_gather_rows(const void* x, int x_dtype, int d, const int32_t* 
 struct ExpertArgs {
     int64_t T;
     int d, E, k, inter, shared_inter, act_dtype;
+    int packed;  // bf16 expert weights in the fragment order of launch_pack_weights
     const void* x;
     const void* w13;
     const void* w2;
@@ -60,5 +61,10 @@ hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream
 hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t stream);
+// packed bf16 expert weights: elements of `batch` packed n x k matrices
+// (interleave: gate and up halves of a 2n-row source)
+int64_t packed_weight_elems(int batch, int n, int k, int interleave);
+hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, void* dst,
+                               hipStream_t stream);
 
 }  // namespace smoes

@@ -43,7 +43,8 @@ class SmoesLayer(ctypes.Structure):
     _fields_ = [("T", c_i64), ("d", c_int), ("E", c_int), ("k", c_int), ("inter", c_int),
                 ("shared_inter", c_int), ("n_bins", c_int), ("n_batch", c_int), ("act_dtype", c_int),
                 ("tau", c_float), ("beta", c_float), ("var_floor", c_float), ("grad_scale", c_float),
-                ("renorm_topk", c_int), ("update_stats", c_int)]
+                ("renorm_topk", c_int), ("update_stats", c_int), ("weights_packed", c_int),
+                ("reserved", c_int)]
 
 
 _IO_FIELDS = ["x", "modality_id", "sample_offsets", "w_gate", "logit_bias", "expert_to_bin", "w13",
@@ -92,6 +93,10 @@ def lib() -> ctypes.CDLL:
         L.smoes_moe_forward.restype = c_int
         L.smoes_moe_forward.argtypes = [ctypes.POINTER(SmoesLayer), ctypes.POINTER(SmoesLayerIO),
                                         c_void, c_size, c_void]
+        L.smoes_packed_weight_bytes.restype = c_size
+        L.smoes_packed_weight_bytes.argtypes = [ctypes.POINTER(SmoesLayer), c_int]
+        L.smoes_pack_weights.restype = c_int
+        L.smoes_pack_weights.argtypes = [ctypes.POINTER(SmoesLayer), c_int, c_void, c_void, c_void]
         L.smoes_events_create.restype = c_int
         L.smoes_events_create.argtypes = [c_int, ctypes.POINTER(c_void)]
         L.smoes_events_destroy.restype = c_int
@@ -234,16 +239,40 @@ class LayerSpec:
     grad_scale: float = 1.0
     renorm_topk: bool = False
     update_stats: bool = False
+    weights_packed: bool = False
 
     def c(self) -> SmoesLayer:
         return SmoesLayer(self.T, self.d, self.E, self.k, self.inter, self.shared_inter, self.n_bins,
                           self.n_batch, self.act_dtype, self.tau, self.beta, self.var_floor,
-                          self.grad_scale, int(self.renorm_topk), int(self.update_stats))
+                          self.grad_scale, int(self.renorm_topk), int(self.update_stats),
+                          int(self.weights_packed), 0)
 
 
 def workspace_bytes(spec: LayerSpec) -> int:
     desc = spec.c()
     return int(lib().smoes_workspace_bytes(ctypes.byref(desc)))
+
+
+SMOES_W13, SMOES_W2, SMOES_WS13, SMOES_WS2 = 0, 1, 2, 3
+WEIGHT_NAMES = {"w13": SMOES_W13, "w2": SMOES_W2, "ws13": SMOES_WS13, "ws2": SMOES_WS2}
+
+
+def packed_weight_bytes(spec: LayerSpec, which: int) -> int:
+    desc = spec.c()
+    return int(lib().smoes_packed_weight_bytes(ctypes.byref(desc), which))
+
+
+def pack_weights(spec: LayerSpec, which: int, src: torch.Tensor) -> torch.Tensor:
+    """Pack one row-major bf16 expert weight tensor (device) into the
+    fragment order read by the packed GEMMs; returns a new uint8 tensor."""
+    n = packed_weight_bytes(spec, which)
+    if n == 0:
+        raise SmoesError(SMOES_ERR_ARG, "smoes_packed_weight_bytes")
+    dst = torch.empty(n, dtype=torch.uint8, device=src.device)
+    desc = spec.c()
+    _check(lib().smoes_pack_weights(ctypes.byref(desc), which, _p(src), _p(dst), _stream()),
+           "smoes_pack_weights")
+    return dst
 
 
 class Events:

@@ -76,19 +76,33 @@ def layer_spec(cfg: W.LayerConfig, T=None, **kw) -> S.LayerSpec:
                        tau=cfg.tau, beta=cfg.beta, **kw)
 
 
-def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None):
+def pack_layer_weights(spec: S.LayerSpec, dev_in) -> None:
+    """Replace the row-major bf16 expert weights in dev_in by their packed
+    form (smoes_pack_weights); spec must have weights_packed set."""
+    for name, which in S.WEIGHT_NAMES.items():
+        if dev_in.get(name) is not None:
+            dev_in[name] = S.pack_weights(spec, which, dev_in[name])
+    torch.cuda.synchronize()
+
+
+def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None, packed=None):
     """The full layer through smoes_moe_forward. For layers that do not update
     their statistics in the call, the Gaussian state is first estimated from
-    the batch by smoes_modality_score(update=1) from the zero state."""
+    the batch by smoes_modality_score(update=1) from the zero state. bf16
+    layers use packed expert weights unless packed=False."""
     cfg = inp.cfg
     upd = cfg.update_stats if update_stats is None else update_stats
-    spec = layer_spec(cfg, update_stats=upd)
+    if packed is None:
+        packed = cfg.dtype == W.BF16
+    spec = layer_spec(cfg, update_stats=upd, weights_packed=packed)
     dev_in = {
         "x": t(inp.x), "modality_id": t(inp.modality_id), "sample_offsets": t(inp.sample_offsets),
         "w_gate": t(inp.w_gate if w_gate is None else w_gate), "logit_bias": t(inp.logit_bias),
         "expert_to_bin": t(inp.expert_to_bin), "w13": t(inp.w13), "w2": t(inp.w2),
         "ws13": t(inp.ws13), "ws2": t(inp.ws2),
     }
+    if packed:
+        pack_layer_weights(spec, dev_in)
     n, smu, ssig = gauss_state_dev(cfg.d)
     if not upd:
         S.modality_score(dev_in["x"], n, smu, ssig, dev_in["modality_id"], update=True, beta=cfg.beta,

@@ -125,12 +125,38 @@ def test_layer_workspace_and_checks():
 
 
 def test_struct_layout_matches_header():
-    # smoes_layer: int64 + 8 int + 4 float + 2 int = 64 bytes; io: 26 pointers
-    assert ctypes.sizeof(S.SmoesLayer) == 64
+    # smoes_layer: int64 + 8 int + 4 float + 4 int = 72 bytes; io: 26 pointers
+    assert ctypes.sizeof(S.SmoesLayer) == 72
     assert ctypes.sizeof(S.SmoesLayerIO) == 26 * 8
     text = open(S.HEADER_PATH).read()
     import re
+    lay = text[text.index("typedef struct smoes_layer {"):text.index("} smoes_layer;")]
+    lay = re.sub(r"/\*.*?\*/", "", lay, flags=re.S)
+    names = re.findall(r"(?:int64_t|int|float)\s+([A-Za-z_0-9]+);", lay)
+    assert names == [f[0] for f in S.SmoesLayer._fields_]
     io_block = text[text.index("typedef struct smoes_layer_io"):text.index("} smoes_layer_io;")]
     io_block = re.sub(r"/\*.*?\*/", "", io_block, flags=re.S)
     fields = re.findall(r"\*\s*(?:const\s*\*\s*)?([A-Za-z_0-9]+);", io_block)
     assert fields == S._IO_FIELDS
+
+
+def test_packed_weight_sizes_and_checks():
+    L = S.lib()
+    spec = _spec(d=128, inter=96, shared_inter=48)
+    # w13: E experts of 2*32*ceil(inter/32) rows x ceil(d/16) slices x 128 bf16 per slice-group
+    assert S.packed_weight_bytes(spec, S.SMOES_W13) == 16 * (2 * 3) * (128 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_W2) == 16 * (128 // 32) * (96 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS13) == (2 * 2) * (128 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS2) == (128 // 32) * (48 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, 4) == 0
+    assert S.packed_weight_bytes(_spec(shared_inter=0), S.SMOES_WS13) == 0
+    desc = spec.c()
+    assert L.smoes_pack_weights(ctypes.byref(desc), S.SMOES_W13, None, FAKE, None) == S.SMOES_ERR_ARG
+    assert L.smoes_pack_weights(ctypes.byref(desc), 7, FAKE, FAKE, None) == S.SMOES_ERR_ARG
+    f32 = _spec(act_dtype=0).c()
+    assert L.smoes_pack_weights(ctypes.byref(f32), S.SMOES_W13, FAKE, FAKE, None) == S.SMOES_ERR_ARG
+    # packed weights are a bf16 layout; reserved must stay 0
+    assert S.workspace_bytes(_spec(act_dtype=0, weights_packed=True)) == 0
+    bad = _spec().c()
+    bad.reserved = 1
+    assert L.smoes_workspace_bytes(ctypes.byref(bad)) == 0

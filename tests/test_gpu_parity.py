@@ -276,6 +276,10 @@ SMALL_LAYERS = [
     dict(d=64, E=8, k=2, inter=48, n_shared=2, n_bins=2, samples=((90, 40), (10, 3), (60, 60)), dtype=W.F32),
     dict(d=512, E=64, k=6, inter=128, n_shared=2, n_bins=8, samples=((700, 300),), dtype=W.BF16,
          logit_bias=True),
+    # ragged for the packed weights: inter % 32 == 16, d % 32 == 8 (partial GEMM2 groups, padded K)
+    dict(d=136, E=10, k=3, inter=48, n_shared=2, n_bins=5, samples=((150, 70), (33, 17)), dtype=W.BF16),
+    # three tokens
+    dict(d=64, E=4, k=2, inter=32, n_shared=0, n_bins=2, samples=((2, 1),), dtype=W.BF16),
 ]
 
 
@@ -290,6 +294,72 @@ def test_layer_small(layer, update):
     ref = run_oracle_layer(inp, w_gate=wg, update_stats=update)
     _check_layer(inp, spec, outs, ref, fp32=cfg.dtype == W.F32)
     assert _check_mi(outs, ref, inp, strict=True) <= 1e-5
+
+
+@pytest.mark.parametrize("layer", [i for i, L in enumerate(SMALL_LAYERS) if L["dtype"] == W.BF16])
+def test_layer_small_rowmajor_weights(layer):
+    """bf16 layers with row-major expert weights (the path for weights that
+    are not kept packed)."""
+    kw = dict(SMALL_LAYERS[layer])
+    cfg = W.small_config(seed=100 + layer, **kw)
+    inp = W.make_layer_inputs(cfg)
+    wg = W.aligned_router(inp, 0.5)
+    spec, _, outs = run_gpu_layer(inp, w_gate=wg, packed=False)
+    ref = run_oracle_layer(inp, w_gate=wg)
+    _check_layer(inp, spec, outs, ref, fp32=False)
+
+
+@pytest.mark.parametrize("layer", [i for i, L in enumerate(SMALL_LAYERS) if L["dtype"] == W.BF16])
+def test_packed_weights_match_rowmajor(layer):
+    """Both bf16 GEMM paths feed the matrix cores the same operands in the
+    same K order, so the outputs agree bit for bit."""
+    cfg = W.small_config(seed=100 + layer, **dict(SMALL_LAYERS[layer]))
+    inp = W.make_layer_inputs(cfg)
+    _, _, a = run_gpu_layer(inp, packed=True)
+    _, _, b = run_gpu_layer(inp, packed=False)
+    assert torch.equal(a["out"], b["out"])
+
+
+def _pack_reference(w, n, k, interleave):
+    """The packed layout written out with numpy: P[g][c][l][e] =
+    W[32g + l%32][16c + 8(l/32) + e], gate/up interleaved by 32-row groups."""
+    batch = w.shape[0]
+    rows = w.reshape(batch, -1, k)
+    if interleave:
+        ip = -(-n // 32) * 32
+        gate = np.zeros((batch, ip, k), w.dtype)
+        up = np.zeros((batch, ip, k), w.dtype)
+        gate[:, :n] = rows[:, :n]
+        up[:, :n] = rows[:, n:]
+        src = np.stack([gate.reshape(batch, ip // 32, 32, k), up.reshape(batch, ip // 32, 32, k)], axis=2)
+        src = src.reshape(batch, 2 * ip, k)
+    else:
+        np_ = -(-n // 32) * 32
+        src = np.zeros((batch, np_, k), w.dtype)
+        src[:, :n] = rows
+    kp = -(-k // 16) * 16
+    full = np.zeros((batch, src.shape[1], kp), w.dtype)
+    full[:, :, :k] = src
+    g = full.shape[1] // 32
+    # [b][g][32 rows][kc][2 halves][8] -> [b][g][kc][half][32 rows][8]
+    v = full.reshape(batch, g, 32, kp // 16, 2, 8).transpose(0, 1, 3, 4, 2, 5)
+    return v.reshape(-1)
+
+
+@pytest.mark.parametrize("d,E,inter,shared", [(128, 3, 96, 96), (136, 2, 48, 64), (64, 1, 32, 0)])
+def test_pack_weights_layout(d, E, inter, shared):
+    rng = np.random.default_rng(5)
+    spec = S.LayerSpec(T=16, d=d, E=E, k=1, inter=inter, shared_inter=shared, n_bins=1, n_batch=1,
+                       act_dtype=S.SMOES_BF16, weights_packed=True)
+    mats = {"w13": (E, 2 * inter, d, inter, 1), "w2": (E, d, inter, d, 0)}
+    if shared:
+        mats.update(ws13=(1, 2 * shared, d, shared, 1), ws2=(1, d, shared, d, 0))
+    for name, (b, r, c, n, il) in mats.items():
+        w = rng.integers(1, 1 << 15, size=(b, r, c), dtype=np.uint16)
+        got = S.pack_weights(spec, S.WEIGHT_NAMES[name], t(w if b > 1 or name in ("w13", "w2") else w[0]))
+        torch.cuda.synchronize()
+        exp = _pack_reference(w, n, c, il)
+        assert np.array_equal(got.cpu().numpy().view(np.uint16), exp), name
 
 
 def test_layer_config0_full():
@@ -312,6 +382,16 @@ def test_layer_config_full(ci):
     _check_layer(inp, spec, outs, ref, rows=rows)
     err = _check_mi(outs, ref, inp, strict=False)
     assert err <= 1e-3, err
+
+
+def test_layer_config1_full_rowmajor_weights():
+    """The benchmark workload through the row-major bf16 weight path."""
+    cfg = W.CONFIGS[1]
+    inp = W.make_layer_inputs(cfg)
+    spec, _, outs = run_gpu_layer(inp, packed=False)
+    rows = np.sort(np.random.default_rng(11).choice(cfg.T, size=128, replace=False))
+    ref = run_oracle_layer(inp, rows=rows)
+    _check_layer(inp, spec, outs, ref, rows=rows)
 
 
 def test_layer_aligned_router_config1_strict_mi():
