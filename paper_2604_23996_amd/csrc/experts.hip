@@ -449,7 +449,9 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 // 32-row groups: 4 x 2 MFMA tiles of 32 x 32). The weights never pass through
 // LDS and no two waves read the same weight bytes; only the token rows (x
 // gathered through perm_token for GEMM1, H for GEMM2) are staged HBM -> LDS by
-// buffer_load ... lds through a three-stage ring of K = 64 slices.
+// buffer_load ... lds through a three-stage ring of K = 64 slices. The
+// weight loads of the next slice and the token-row DMA of the slice after
+// are spread between the MFMAs of the current one.
 //   GEMM1: 128 H columns per tile (32 per wave), SwiGLU in registers.
 //   GEMM2: 256 output columns per tile (64 per wave).
 constexpr int PK_BM = 128, PK_BK = 64, PK_WAVES = 4, PK_THREADS = PK_WAVES * 64, PK_ST = 3;
@@ -539,25 +541,21 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         aoff[q] = src * K;
         achk[q] = ((lane % 8) ^ ((R / 2) % 8)) * 8;
     }
-    auto issue_a = [&](int stage, int s) {
-#pragma unroll
-        for (int q = 0; q < IA; ++q) {
-            const int k = s * BK + achk[q];
-            const int vo = ((aoff[q] + k) * 2) | (k < K ? 0 : kOutOfRange);
-            auto* dst = (__attribute__((address_space(3))) void*)(lds + stage * A_BYTES + (wave * IA + q) * 1024);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
-        }
+    // One A DMA instruction (rows (wave * IA + q) * 8 ..) of stage s into ring slot `slot`.
+    auto issue_aq = [&](int slot, int s, int q) {
+        const int k = s * BK + achk[q];
+        const int vo = ((aoff[q] + k) * 2) | (k < K ? 0 : kOutOfRange);
+        auto* dst = (__attribute__((address_space(3))) void*)(lds + slot * A_BYTES + (wave * IA + q) * 1024);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
     };
-    i32x4_t b0[4][2], b1[4][2];
-    auto issue_b = [&](i32x4_t (&b)[4][2], int s) {
+    // The two B fragments (gate/up or two column groups) of K slice 16 * (4 s + j).
+    auto issue_bj = [&](i32x4_t (&b)[4][2], int s, int j) {
+        const int kc = s * 4 + j;
 #pragma unroll
-        for (int g = 0; g < 2; ++g)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int kc = s * 4 + j;
-                const int vo = (((g * kc_n + kc) * 64 + lane) * 16) | (kc < kc_n ? 0 : kOutOfRange);
-                b[j][g] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0);
-            }
+        for (int g = 0; g < 2; ++g) {
+            const int vo = (((g * kc_n + kc) * 64 + lane) * 16) | (kc < kc_n ? 0 : kOutOfRange);
+            b[j][g] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0);
+        }
     };
     f32x16_t acc[4][2];
 #pragma unroll
@@ -565,60 +563,88 @@ gemm_bf16_pk_kernel(GemmArgs p) {
 #pragma unroll
         for (int g = 0; g < 2; ++g) acc[i][g] = f32x16_t{};
     const int half = lane >> 5, l32 = lane & 31;
-    auto compute = [&](int stage, const i32x4_t (&b)[4][2]) {
-        const uint8_t* base = lds + stage * A_BYTES;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            bf16x8_t af[4];
+
+    // Stage s from ring slot `slot` with B registers bc, while the loads of
+    // the next stages go out between the MFMAs: substep j (K = 16) issues
+    // B(s + 1) slice j (2 loads) and the A DMA q = j of stage s + 2, reads the
+    // A fragments of substep j + 1 and runs 8 MFMAs. A wave issues in order,
+    // so spreading the memory instructions over the MFMAs keeps the matrix
+    // pipe fed while the address unit drains them.
+    static_assert(IA == 4, "one A DMA per K = 16 substep");
+    auto stage_run = [&](int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
+        const uint8_t* base = lds + slot * A_BYTES;
+        const int nslot = slot == 0 ? 2 : slot - 1;  // (slot + 2) % 3
+        bf16x8_t af[2][4];
+        auto rd = [&](int j, bf16x8_t (&a)[4]) {
             const int c = j * 2 + half;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int R = i * 32 + l32;
-                af[i] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + ((c ^ ((R / 2) % 8)) * 16));
+                a[i] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + ((c ^ ((R / 2) % 8)) * 16));
             }
+        };
+        rd(0, af[0]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            __builtin_amdgcn_sched_barrier(0);
+            issue_bj(bn, s + 1, j);
+            issue_aq(nslot, s + 2, j);
+            if (j < 3) rd(j + 1, af[(j + 1) & 1]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int g = 0; g < 2; ++g)
-                    acc[i][g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], __builtin_bit_cast(bf16x8_t, b[j][g]),
-                                                                         acc[i][g], 0, 0, 0);
+                    acc[i][g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        af[j & 1][i], __builtin_bit_cast(bf16x8_t, bc[j][g]), acc[i][g], 0, 0, 0);
+            // order: MFMA, VMEM x3 (one after each of the first three MFMAs), then one LDS read
+            // after each of the next four MFMAs, then the last MFMA
+#pragma unroll
+            for (int q = 0; q < 3; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
     };
 
-    // K loop. Iteration s: wait until A(s) and B(s) have landed (only A(s + 1),
-    // IA loads, may still fly; loads retire in order), barrier (every wave's
-    // DMA of A(s) is visible and every wave is done with the ring slot that
-    // A(s + 2) overwrites), issue B(s + 1) and A(s + 2), then run the MFMAs of
-    // stage s. Unrolled by two so the two B register sets stay static.
+    // Loads retire in order. Issue order: A(0), then per substep j of stage
+    // s - 1: B(s)[j] (2), A(s + 1)[j] (1). Before stage s reads LDS slot s % 3,
+    // at most the 12 loads issued after A(s)'s last DMA may still fly (B(s)
+    // and A(s + 1)); the compiler waits for B(s)'s registers by itself. The
+    // barrier makes every wave's DMA of A(s) visible and frees the slot that
+    // A(s + 2) overwrites. Unrolled by two so the B register sets stay static.
+    // Past the end of K the loads go out of range and return zeros, so every
+    // stage issues the same count and the waits stay exact.
     const int nk = static_cast<int>(ceil_div(K, BK));
-    issue_b(b0, 0);
-    issue_a(0, 0);
-    issue_a(1, 1);
+    i32x4_t b0[4][2], b1[4][2];
+#pragma unroll
+    for (int q = 0; q < IA; ++q) issue_aq(0, 0, q);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        issue_bj(b0, 0, j);
+        issue_aq(1, 1, j);
+    }
     int s = 0, slot = 0;
     for (; s + 2 <= nk; s += 2) {
-        wait_vm_lgkm0<IA>();
+        wait_vm_lgkm0<12>();
         __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        issue_b(b1, s + 1);
-        issue_a(slot == 0 ? 2 : slot - 1, s + 2);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(slot, b0);
-        __builtin_amdgcn_sched_barrier(0);
+        stage_run(slot, s, b0, b1);
         slot = slot == 2 ? 0 : slot + 1;
-        wait_vm_lgkm0<IA>();
+        wait_vm_lgkm0<12>();
         __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        issue_b(b0, s + 2);
-        issue_a(slot == 0 ? 2 : slot - 1, s + 3);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(slot, b1);
-        __builtin_amdgcn_sched_barrier(0);
+        stage_run(slot, s + 1, b1, b0);
         slot = slot == 2 ? 0 : slot + 1;
     }
     if (s < nk) {
-        wait_vm_lgkm0<IA>();
+        wait_vm_lgkm0<12>();
         __builtin_amdgcn_s_barrier();
-        compute(slot, b0);
+        stage_run(slot, s, b0, b1);
     }
     wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
     __builtin_amdgcn_s_barrier();
