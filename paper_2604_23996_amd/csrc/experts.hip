@@ -23,6 +23,8 @@
 //          same lane: the SwiGLU epilogue is register-local. H is bf16.
 //   GEMM2: Y = H W2^T, bf16.
 // f32 (exact path for float32 layers): 64 x 64 FMA tiles, same work table.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -111,9 +113,11 @@ __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, co
     const int slot = blockIdx.x >> 3;
     const int r_lo = min(xcd * r8, routed), r_hi = min(r_lo + r8, routed);
     const int s_lo = min(xcd * s8, shared), s_hi = min(s_lo + s8, shared);
+    // shared items first: their K can be longer (GEMM2), and blocks are
+    // dispatched in index order, so the longest tiles start earliest
     int w;
-    if (slot < r_hi - r_lo) w = r_lo + slot;
-    else if (slot < (r_hi - r_lo) + (s_hi - s_lo)) w = routed + s_lo + (slot - (r_hi - r_lo));
+    if (slot < s_hi - s_lo) w = routed + s_lo + slot;
+    else if (slot < (s_hi - s_lo) + (r_hi - r_lo)) w = r_lo + (slot - (s_hi - s_lo));
     else return false;
     int g;
     if (w >= routed) {
@@ -530,7 +534,10 @@ gemm_bf16_pk_kernel(GemmArgs p) {
 
     // A DMA: instruction q of this wave fills LDS rows (wave * IA + q) * 8 .. + 7 of the stage;
     // lane moves the 16-byte chunk (lane % 8) ^ swizzle(row) of its row into slot lane % 8.
-    int aoff[IA], achk[IA];
+    // aoff: element offset of the row start; rows past the tile get 2^30, whose
+    // byte offset (>= 2^31) is out of range: zero fill without memory traffic.
+    uint32_t aoff[IA];
+    int achk[IA];
 #pragma unroll
     for (int q = 0; q < IA; ++q) {
         const int R = (wave * IA + q) * 8 + lane / 8;
@@ -538,13 +545,14 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         int src;
         if (MODE == 1 && !shared) src = p.perm_token[t.row0 + rr];
         else src = static_cast<int>(t.row0 + rr);
-        aoff[q] = src * K;
+        aoff[q] = R < t.rows ? static_cast<uint32_t>(src) * static_cast<uint32_t>(K) : (1u << 30);
         achk[q] = ((lane % 8) ^ ((R / 2) % 8)) * 8;
     }
     // One A DMA instruction (rows (wave * IA + q) * 8 ..) of stage s into ring slot `slot`.
     auto issue_aq = [&](int slot, int s, int q) {
         const int k = s * BK + achk[q];
-        const int vo = ((aoff[q] + k) * 2) | (k < K ? 0 : kOutOfRange);
+        const int vo = static_cast<int>(((aoff[q] + static_cast<uint32_t>(k)) * 2u) |
+                                        (k < K ? 0u : static_cast<uint32_t>(kOutOfRange)));
         auto* dst = (__attribute__((address_space(3))) void*)(lds + slot * A_BYTES + (wave * IA + q) * 1024);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
     };
@@ -571,14 +579,17 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     // so spreading the memory instructions over the MFMAs keeps the matrix
     // pipe fed while the address unit drains them.
     static_assert(IA == 4, "one A DMA per K = 16 substep");
-    auto stage_run = [&](int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
+    // MT: 32-row sub-tiles that take part (4, or 2 for a tile of at most 64
+    // rows: a short last tile of an expert skips half of the MFMAs).
+    auto stage_run = [&](auto mt_c, int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
+        constexpr int MT = decltype(mt_c)::value;
         const uint8_t* base = lds + slot * A_BYTES;
         const int nslot = slot == 0 ? 2 : slot - 1;  // (slot + 2) % 3
         bf16x8_t af[2][4];
         auto rd = [&](int j, bf16x8_t (&a)[4]) {
             const int c = j * 2 + half;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < MT; ++i) {
                 const int R = i * 32 + l32;
                 a[i] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + ((c ^ ((R / 2) % 8)) * 16));
             }
@@ -591,24 +602,25 @@ gemm_bf16_pk_kernel(GemmArgs p) {
             issue_aq(nslot, s + 2, j);
             if (j < 3) rd(j + 1, af[(j + 1) & 1]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < MT; ++i)
 #pragma unroll
                 for (int g = 0; g < 2; ++g)
                     acc[i][g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         af[j & 1][i], __builtin_bit_cast(bf16x8_t, bc[j][g]), acc[i][g], 0, 0, 0);
-            // order: MFMA, VMEM x3 (one after each of the first three MFMAs), then one LDS read
-            // after each of the next four MFMAs, then the last MFMA
+            // order: one VMEM after each of the first MFMAs, then one LDS read after each of
+            // the following MFMAs, then the rest of the MFMAs
+            constexpr int NM = 2 * MT;
 #pragma unroll
             for (int q = 0; q < 3; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if (q < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
             }
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            for (int q = 0; q < MT; ++q) {
+                if (3 + q < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (NM > 3 + MT) __builtin_amdgcn_sched_group_barrier(0x008, NM - 3 - MT, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
     };
@@ -622,30 +634,34 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     // Past the end of K the loads go out of range and return zeros, so every
     // stage issues the same count and the waits stay exact.
     const int nk = static_cast<int>(ceil_div(K, BK));
-    i32x4_t b0[4][2], b1[4][2];
+    auto kloop = [&](auto mt_c) {
+        i32x4_t b0[4][2], b1[4][2];
 #pragma unroll
-    for (int q = 0; q < IA; ++q) issue_aq(0, 0, q);
+        for (int q = 0; q < IA; ++q) issue_aq(0, 0, q);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        issue_bj(b0, 0, j);
-        issue_aq(1, 1, j);
-    }
-    int s = 0, slot = 0;
-    for (; s + 2 <= nk; s += 2) {
-        wait_vm_lgkm0<12>();
-        __builtin_amdgcn_s_barrier();
-        stage_run(slot, s, b0, b1);
-        slot = slot == 2 ? 0 : slot + 1;
-        wait_vm_lgkm0<12>();
-        __builtin_amdgcn_s_barrier();
-        stage_run(slot, s + 1, b1, b0);
-        slot = slot == 2 ? 0 : slot + 1;
-    }
-    if (s < nk) {
-        wait_vm_lgkm0<12>();
-        __builtin_amdgcn_s_barrier();
-        stage_run(slot, s, b0, b1);
-    }
+        for (int j = 0; j < 4; ++j) {
+            issue_bj(b0, 0, j);
+            issue_aq(1, 1, j);
+        }
+        int s = 0, slot = 0;
+        for (; s + 2 <= nk; s += 2) {
+            wait_vm_lgkm0<12>();
+            __builtin_amdgcn_s_barrier();
+            stage_run(mt_c, slot, s, b0, b1);
+            slot = slot == 2 ? 0 : slot + 1;
+            wait_vm_lgkm0<12>();
+            __builtin_amdgcn_s_barrier();
+            stage_run(mt_c, slot, s + 1, b1, b0);
+            slot = slot == 2 ? 0 : slot + 1;
+        }
+        if (s < nk) {
+            wait_vm_lgkm0<12>();
+            __builtin_amdgcn_s_barrier();
+            stage_run(mt_c, slot, s, b0, b1);
+        }
+    };
+    if (uniform_int(t.rows) > 64) kloop(std::integral_constant<int, 4>{});
+    else kloop(std::integral_constant<int, 2>{});
     wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
     __builtin_amdgcn_s_barrier();
 
