@@ -159,9 +159,7 @@ def main():
                   gauss_n=torch.zeros(2, device=dev), gauss_smu=torch.zeros((2, cfg.d), device=dev),
                   gauss_ssig=torch.zeros((2, cfg.d), device=dev))
     if spec.weights_packed:  # weights are stored packed (converted once, when they are loaded)
-        for name, which in S.WEIGHT_NAMES.items():
-            if dev_in[name] is not None:
-                dev_in[name] = S.pack_weights(spec, which, dev_in[name])
+        S.pack_layer_inputs(spec, dev_in)
         torch.cuda.synchronize()
     if not cfg.update_stats:  # statistics estimated once from the batch, outside the timed call
         S.modality_score(dev_in["x"], dev_in["gauss_n"], dev_in["gauss_smu"], dev_in["gauss_ssig"],

@@ -91,7 +91,7 @@ size_t smoes_route_workspace_size(int64_t T, int d, int E, int x_dtype);
  *            lower index (decided on the float32 logits).
  * topk_w     [T, k] float32 output: combine weights.
  * Shapes: 1 <= d <= SMOES_D_MAX, d % 8 == 0; 1 <= E <= SMOES_E_MAX;
- *         1 <= k <= min(E, SMOES_K_MAX).
+ *         1 <= k <= min(E, SMOES_K_MAX); for SMOES_BF16, T * d * 2 < 2^31.
  */
 int smoes_route(const void* x, int x_dtype, int64_t T, int d,
                 const float* w_gate, const float* logit_bias, int E, int k, int renorm_topk,
@@ -216,6 +216,9 @@ typedef struct smoes_layer_io {
     const void* w2;                /* [E, d, inter] down projection */
     const void* ws13;              /* [2*shared_inter, d] or NULL when shared_inter == 0 */
     const void* ws2;               /* [d, shared_inter] or NULL when shared_inter == 0 */
+    const void* w_gate_packed;     /* weights_packed: the router weights packed by
+                                      smoes_pack_weights(SMOES_WGATE) (then w_gate may be
+                                      NULL); otherwise unused */
     /* caller-owned Gaussian state (in/out when update_stats) */
     float* gauss_n;   /* [2] */
     float* gauss_smu; /* [2, d] */
@@ -275,7 +278,7 @@ int smoes_moe_forward(const smoes_layer* desc, const smoes_layer_io* io,
 /* ------------------------------------------------------------------------ */
 
 /* Which expert weight tensor (shapes as in smoes_layer_io). */
-enum smoes_weight { SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3 };
+enum smoes_weight { SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3, SMOES_WGATE = 4 };
 
 /*
  * Layout: a matrix W[N][K] (N output rows, K the contraction) becomes
@@ -285,6 +288,11 @@ enum smoes_weight { SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3 }
  * gate rows 32q..32q+31, group 2q+1 = the up rows of the same columns),
  * N = 2*32*ceil(inter/32), K = d; one matrix per expert, experts back to
  * back. w2/ws2: W = w2[e] ([d][inter]), N = d, K = inter.
+ * SMOES_WGATE: the float32 router weights w_gate [E][d] as three bf16 terms
+ * (hi, mid, lo: their sum reproduces each weight to ~2^-24), each stored as
+ * ceil(E/16) groups of ceil(d/32) slices of 64 x 8 bf16,
+ *   P[p][g][c][l][e] = term p of w_gate[16g + l%16][32c + 8(l/16) + e],
+ * zero outside w_gate: the operand order of the 16x16x32 matrix instructions.
  * Returns the byte size of the packed tensor, 0 for an invalid desc or
  * `which` (ws13/ws2 need shared_inter > 0).
  */

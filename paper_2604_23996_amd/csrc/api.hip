@@ -93,6 +93,8 @@ int smoes_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gat
     if (!dtype_ok(x_dtype)) return SMOES_ERR_ARG;
     int st = check_router_shape(T, d, E, k);
     if (st != SMOES_OK) return st;
+    // bf16 activations are read through a buffer descriptor with 32-bit byte offsets
+    if (x_dtype == SMOES_BF16 && T * d * 2 > INT32_MAX) return SMOES_ERR_SHAPE;
     if (T == 0) return SMOES_OK;
     if (x == nullptr || w_gate == nullptr || probs == nullptr || topk_idx == nullptr || topk_w == nullptr)
         return SMOES_ERR_ARG;
@@ -100,7 +102,7 @@ int smoes_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gat
     if (x_dtype == SMOES_BF16 && (workspace == nullptr || workspace_bytes < need)) return SMOES_ERR_WORKSPACE;
     Carver c(workspace);
     void* ws = x_dtype == SMOES_BF16 ? c.take(router_workspace_bytes(d, E, x_dtype)) : nullptr;
-    return hip_status(launch_route(x, x_dtype, T, d, w_gate, logit_bias, E, k, renorm_topk ? 1 : 0,
+    return hip_status(launch_route(x, x_dtype, T, d, w_gate, nullptr, logit_bias, E, k, renorm_topk ? 1 : 0,
                                    logits, probs, topk_idx, topk_w, ws, as_stream(stream)));
 }
 
@@ -250,7 +252,8 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     if (st != SMOES_OK) return st;
     if (io == nullptr) return SMOES_ERR_ARG;
     if (L->T == 0) return SMOES_OK;
-    if (io->x == nullptr || io->w_gate == nullptr || io->expert_to_bin == nullptr || io->w13 == nullptr ||
+    if (io->x == nullptr || (L->weights_packed ? io->w_gate_packed == nullptr : io->w_gate == nullptr) ||
+        io->expert_to_bin == nullptr || io->w13 == nullptr ||
         io->w2 == nullptr || io->gauss_n == nullptr || io->gauss_smu == nullptr ||
         io->gauss_ssig == nullptr || io->probs == nullptr || io->topk_idx == nullptr ||
         io->topk_w == nullptr || io->M == nullptr || io->mi_per_sample == nullptr ||
@@ -277,7 +280,8 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     } while (0)
 
     SMOES_TRY(record(ev, SMOES_STAGE_ROUTE, s));
-    SMOES_TRY(launch_route(io->x, L->act_dtype, T, L->d, io->w_gate, io->logit_bias, L->E, L->k,
+    SMOES_TRY(launch_route(io->x, L->act_dtype, T, L->d, io->w_gate, L->weights_packed ? io->w_gate_packed : nullptr,
+                           io->logit_bias, L->E, L->k,
                            L->renorm_topk ? 1 : 0, logits, io->probs, io->topk_idx, io->topk_w, w.route, s));
     SMOES_TRY(record(ev, SMOES_STAGE_MODALITY, s));
     SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
@@ -327,6 +331,7 @@ bool weight_dims(const smoes_layer* L, int which, int* batch, int* n, int* k, in
         case SMOES_W2: *batch = L->E; *n = L->d; *k = L->inter; *interleave = 0; return true;
         case SMOES_WS13: *batch = 1; *n = L->shared_inter; *k = L->d; *interleave = 1; return L->shared_inter > 0;
         case SMOES_WS2: *batch = 1; *n = L->d; *k = L->shared_inter; *interleave = 0; return L->shared_inter > 0;
+        case SMOES_WGATE: *batch = 1; *n = L->E; *k = L->d; *interleave = 0; return true;
         default: return false;
     }
 }
@@ -336,6 +341,7 @@ size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which) {
     if (check_layer(desc) != SMOES_OK) return 0;
     int batch, n, k, il;
     if (!weight_dims(desc, which, &batch, &n, &k, &il)) return 0;
+    if (which == SMOES_WGATE) return router_packed_elems(desc->d, desc->E) * 2;
     return static_cast<size_t>(packed_weight_elems(batch, n, k, il)) * 2;
 }
 
@@ -346,8 +352,10 @@ int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void
     if (desc->act_dtype != SMOES_BF16 || !weight_dims(desc, which, &batch, &n, &k, &il) || src == nullptr ||
         dst == nullptr)
         return SMOES_ERR_ARG;
-    return launch_pack_weights(src, batch, n, k, il, dst, as_stream(stream)) == hipSuccess ? SMOES_OK
-                                                                                           : SMOES_ERR_HIP;
+    const hipError_t err = which == SMOES_WGATE
+                               ? launch_split_wgate(static_cast<const float*>(src), desc->E, desc->d, dst, as_stream(stream))
+                               : launch_pack_weights(src, batch, n, k, il, dst, as_stream(stream));
+    return err == hipSuccess ? SMOES_OK : SMOES_ERR_HIP;
 }
 
 int smoes_events_create(int n, void** events) {

@@ -2,6 +2,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 #include <stdint.h>
 
 #define SMOES_K_MAX_DEV 16
@@ -64,6 +66,49 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Wave reductions with a uniform result, built from DPP moves inside each
+// 16-lane row (quad swaps, half-row and row mirrors: every lane of a row ends
+// with the row's value) and one read of each row's lane 0; the four row
+// values are combined in a fixed order. Needs all 64 lanes active.
+template <int CTRL>
+__device__ __forceinline__ int dpp_mov(int v) {
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, false);
+}
+template <class T, class Op>
+__device__ __forceinline__ T row_allreduce(T v, Op op) {
+    auto mv = [](T x, auto ctrl) {
+        constexpr int C = decltype(ctrl)::value;
+        if constexpr (sizeof(T) == 4 && !__is_same(T, int)) return __int_as_float(dpp_mov<C>(__float_as_int(x)));
+        else return static_cast<T>(dpp_mov<C>(static_cast<int>(x)));
+    };
+    v = op(v, mv(v, std::integral_constant<int, 0xB1>{}));   // quad_perm [1,0,3,2]
+    v = op(v, mv(v, std::integral_constant<int, 0x4E>{}));   // quad_perm [2,3,0,1]
+    v = op(v, mv(v, std::integral_constant<int, 0x141>{}));  // row_half_mirror
+    v = op(v, mv(v, std::integral_constant<int, 0x140>{}));  // row_mirror
+    return v;
+}
+__device__ __forceinline__ float wave_max_u(float v) {
+    v = row_allreduce(v, [](float a, float b) { return fmaxf(a, b); });
+    const int i = __float_as_int(v);
+    const float a = __int_as_float(__builtin_amdgcn_readlane(i, 0)), b = __int_as_float(__builtin_amdgcn_readlane(i, 16));
+    const float c = __int_as_float(__builtin_amdgcn_readlane(i, 32)), d = __int_as_float(__builtin_amdgcn_readlane(i, 48));
+    return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+__device__ __forceinline__ float wave_sum_u(float v) {
+    v = row_allreduce(v, [](float a, float b) { return a + b; });
+    const int i = __float_as_int(v);
+    const float a = __int_as_float(__builtin_amdgcn_readlane(i, 0)), b = __int_as_float(__builtin_amdgcn_readlane(i, 16));
+    const float c = __int_as_float(__builtin_amdgcn_readlane(i, 32)), d = __int_as_float(__builtin_amdgcn_readlane(i, 48));
+    return (a + b) + (c + d);
+}
+__device__ __forceinline__ int wave_min_u(int v) {
+    v = row_allreduce(v, [](int a, int b) { return a < b ? a : b; });
+    const int a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+    const int c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+    const int ab = a < b ? a : b, cd = c < d ? c : d;
+    return ab < cd ? ab : cd;
+}
 
 __host__ __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -12,9 +12,13 @@ namespace smoes {
 // ---------------------------------------------------------------- router
 size_t router_workspace_bytes(int d, int E, int x_dtype);
 size_t router_lds_bytes(int E, int x_dtype);
+// w_split: router weights already in the split fragment order of
+// launch_split_wgate (bf16 x only), or NULL to split w_gate into ws first
 hipError_t launch_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gate,
-                        const float* bias, int E, int k, int renorm, float* logits, float* probs,
-                        int32_t* topk_idx, float* topk_w, void* ws, hipStream_t stream);
+                        const void* w_split, const float* bias, int E, int k, int renorm, float* logits,
+                        float* probs, int32_t* topk_idx, float* topk_w, void* ws, hipStream_t stream);
+size_t router_packed_elems(int d, int E);
+hipError_t launch_split_wgate(const float* w_gate, int E, int d, void* wpk, hipStream_t stream);
 
 // ---------------------------------------------------------------- modality score
 size_t modality_workspace_bytes(int64_t T, int d);

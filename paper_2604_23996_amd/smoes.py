@@ -48,7 +48,7 @@ class SmoesLayer(ctypes.Structure):
 
 
 _IO_FIELDS = ["x", "modality_id", "sample_offsets", "w_gate", "logit_bias", "expert_to_bin", "w13",
-              "w2", "ws13", "ws2", "gauss_n", "gauss_smu", "gauss_ssig", "logits", "probs", "topk_idx",
+              "w2", "ws13", "ws2", "w_gate_packed", "gauss_n", "gauss_smu", "gauss_ssig", "logits", "probs", "topk_idx",
               "topk_w", "M", "mi_per_sample", "loss", "dlogits", "expert_offsets", "perm_token",
               "perm_inv", "out", "stage_events"]
 
@@ -253,8 +253,18 @@ def workspace_bytes(spec: LayerSpec) -> int:
     return int(lib().smoes_workspace_bytes(ctypes.byref(desc)))
 
 
-SMOES_W13, SMOES_W2, SMOES_WS13, SMOES_WS2 = 0, 1, 2, 3
+SMOES_W13, SMOES_W2, SMOES_WS13, SMOES_WS2, SMOES_WGATE = 0, 1, 2, 3, 4
 WEIGHT_NAMES = {"w13": SMOES_W13, "w2": SMOES_W2, "ws13": SMOES_WS13, "ws2": SMOES_WS2}
+
+
+def pack_layer_inputs(spec: "LayerSpec", dev_in: Dict[str, Optional[torch.Tensor]]) -> None:
+    """Add the packed forms of a bf16 layer's weights to dev_in: the expert
+    weights replace w13/w2/ws13/ws2 and the router weights go to
+    w_gate_packed (w_gate stays). spec.weights_packed must be set."""
+    for name, which in WEIGHT_NAMES.items():
+        if dev_in.get(name) is not None:
+            dev_in[name] = pack_weights(spec, which, dev_in[name])
+    dev_in["w_gate_packed"] = pack_weights(spec, SMOES_WGATE, dev_in["w_gate"])
 
 
 def packed_weight_bytes(spec: LayerSpec, which: int) -> int:

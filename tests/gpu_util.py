@@ -79,9 +79,7 @@ def layer_spec(cfg: W.LayerConfig, T=None, **kw) -> S.LayerSpec:
 def pack_layer_weights(spec: S.LayerSpec, dev_in) -> None:
     """Replace the row-major bf16 expert weights in dev_in by their packed
     form (smoes_pack_weights); spec must have weights_packed set."""
-    for name, which in S.WEIGHT_NAMES.items():
-        if dev_in.get(name) is not None:
-            dev_in[name] = S.pack_weights(spec, which, dev_in[name])
+    S.pack_layer_inputs(spec, dev_in)
     torch.cuda.synchronize()
 
 

@@ -125,9 +125,9 @@ def test_layer_workspace_and_checks():
 
 
 def test_struct_layout_matches_header():
-    # smoes_layer: int64 + 8 int + 4 float + 4 int = 72 bytes; io: 26 pointers
+    # smoes_layer: int64 + 8 int + 4 float + 4 int = 72 bytes; io: 27 pointers
     assert ctypes.sizeof(S.SmoesLayer) == 72
-    assert ctypes.sizeof(S.SmoesLayerIO) == 26 * 8
+    assert ctypes.sizeof(S.SmoesLayerIO) == 27 * 8
     text = open(S.HEADER_PATH).read()
     import re
     lay = text[text.index("typedef struct smoes_layer {"):text.index("} smoes_layer;")]
@@ -148,7 +148,9 @@ def test_packed_weight_sizes_and_checks():
     assert S.packed_weight_bytes(spec, S.SMOES_W2) == 16 * (128 // 32) * (96 // 16) * 512 * 2
     assert S.packed_weight_bytes(spec, S.SMOES_WS13) == (2 * 2) * (128 // 16) * 512 * 2
     assert S.packed_weight_bytes(spec, S.SMOES_WS2) == (128 // 32) * (48 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, 4) == 0
+    # router weights: 3 bf16 terms x ceil(E/16)*16 experts x ceil(d/32)*32
+    assert S.packed_weight_bytes(spec, S.SMOES_WGATE) == 3 * 16 * 128 * 2
+    assert S.packed_weight_bytes(spec, 5) == 0
     assert S.packed_weight_bytes(_spec(shared_inter=0), S.SMOES_WS13) == 0
     desc = spec.c()
     assert L.smoes_pack_weights(ctypes.byref(desc), S.SMOES_W13, None, FAKE, None) == S.SMOES_ERR_ARG

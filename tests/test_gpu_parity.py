@@ -346,6 +346,36 @@ def _pack_reference(w, n, k, interleave):
     return v.reshape(-1)
 
 
+def _split3(w):
+    """fp32 -> three bf16 terms (hi, mid, lo), each rounded to nearest even."""
+    hi = W.f32_to_bf16_bits(w)
+    r1 = (w.astype(np.float32) - W.bf16_bits_to_f32(hi)).astype(np.float32)
+    mid = W.f32_to_bf16_bits(r1)
+    r2 = (r1 - W.bf16_bits_to_f32(mid)).astype(np.float32)
+    return hi, mid, W.f32_to_bf16_bits(r2)
+
+
+@pytest.mark.parametrize("d,E", [(128, 16), (136, 40), (2048, 64), (72, 3)])
+def test_pack_router_weights_layout(d, E):
+    rng = np.random.default_rng(6)
+    w = rng.standard_normal((E, d)).astype(np.float32)
+    spec = S.LayerSpec(T=16, d=d, E=E, k=1, inter=32, shared_inter=0, n_bins=1, n_batch=1,
+                       act_dtype=S.SMOES_BF16, weights_packed=True)
+    got = S.pack_weights(spec, S.SMOES_WGATE, t(w)).cpu().numpy().view(np.uint16)
+    ep, dp = -(-E // 16) * 16, -(-d // 32) * 32
+    parts = []
+    for term in _split3(w):
+        full = np.zeros((ep, dp), np.uint16)
+        full[:E, :d] = term
+        # [g][16 rows][c][2 halves... 4 quads][8] -> [g][c][quad][row][8]
+        parts.append(full.reshape(ep // 16, 16, dp // 32, 4, 8).transpose(0, 2, 3, 1, 4).reshape(-1))
+    assert np.array_equal(got, np.concatenate(parts))
+    # the three terms reproduce the weights to ~2^-24 relative
+    hi, mid, lo = _split3(w)
+    back = (W.bf16_bits_to_f32(hi).astype(np.float64) + W.bf16_bits_to_f32(mid) + W.bf16_bits_to_f32(lo))
+    assert np.all(np.abs(back - w) <= 2.0 ** -23 * np.abs(w))
+
+
 @pytest.mark.parametrize("d,E,inter,shared", [(128, 3, 96, 96), (136, 2, 48, 64), (64, 1, 32, 0)])
 def test_pack_weights_layout(d, E, inter, shared):
     rng = np.random.default_rng(5)
