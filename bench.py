@@ -190,7 +190,7 @@ def main():
 
     stage_ms = {}
     for si, name in enumerate(S.STAGES):
-        stage_ms[name] = float(np.mean([ev.elapsed_ms(si, si + 1) for ev in events]))
+        stage_ms[name] = float(np.mean([ev.stage_ms(si) for ev in events]))
     for ev in events:
         ev.close()
     work = stage_work(cfg, cfg.T)

@@ -236,13 +236,16 @@ typedef struct smoes_layer_io {
     int32_t* perm_token;    /* [T * k] or NULL */
     int32_t* perm_inv;      /* [T, k] or NULL */
     void* out;              /* [T, d] act_dtype: routed experts + shared experts */
-    /* optional stage timing: NULL, or SMOES_N_STAGES + 1 events made by
-     * smoes_events_create; event s is recorded on `stream` before stage s and
-     * the last one after the final stage. */
+    /* optional stage timing: NULL, or 2 * SMOES_N_STAGES events made by
+     * smoes_events_create (entries may be NULL); events 2s and 2s + 1 are
+     * recorded on the stream that runs stage s, before and after it. */
     void* const* stage_events;
 } smoes_layer_io;
 
-/* Stages of smoes_moe_forward, in launch order. */
+/* Stages of smoes_moe_forward. ROUTE, PERMUTE, GEMM1, GEMM2 and COMBINE run
+ * in this order on the caller's stream; MODALITY and then MI (after ROUTE)
+ * run on a side stream that the library keeps per device, and the caller's
+ * stream waits for it before the call's work is complete. */
 enum smoes_stage {
     SMOES_STAGE_ROUTE = 0,    /* router GEMM + softmax + top-k */
     SMOES_STAGE_MODALITY = 1, /* statistics update (optional) + modality score */

@@ -3,6 +3,8 @@
 // synchronises the host.
 #include <stdio.h>
 
+#include <mutex>
+
 #include "smoes.h"
 #include "common.h"
 #include "kernels.h"
@@ -60,9 +62,39 @@ size_t mi_ws(int64_t T, int E, int n_batch, int n_bins) {
 }
 size_t permute_ws(int64_t T, int E, int k) { return permute_workspace_bytes(T, E, k) + 2 * kAlign; }
 
-hipError_t record(void* const* ev, int s, hipStream_t st) {
-    if (ev == nullptr) return hipSuccess;
-    return hipEventRecord(static_cast<hipEvent_t>(ev[s]), st);
+// Stage s timing: start event 2 s, end event 2 s + 1 (either may be NULL).
+hipError_t record(void* const* ev, int idx, hipStream_t st) {
+    if (ev == nullptr || ev[idx] == nullptr) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(ev[idx]), st);
+}
+
+// Side stream of one device: the modality score and the MI chain run on it,
+// beside the permutation and the expert GEMMs on the caller's stream. Made on
+// first use (default priority, not blocking on the legacy default stream) and
+// kept until the process ends; one mutex orders the event records and waits
+// of concurrent calls.
+struct SideStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, routed = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_side_mu;
+SideStream g_side[kMaxDevices];
+
+hipError_t side_stream_locked(SideStream** out) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    SideStream& ss = g_side[dev];
+    if (ss.stream == nullptr) {
+        if ((err = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking)) != hipSuccess) return err;
+        if ((err = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess) return err;
+        if ((err = hipEventCreateWithFlags(&ss.routed, hipEventDisableTiming)) != hipSuccess) return err;
+        if ((err = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess) return err;
+    }
+    *out = &ss;
+    return hipSuccess;
 }
 
 }  // namespace
@@ -169,7 +201,7 @@ int smoes_permute(const int32_t* topk_idx, int64_t T, int E, int k, int32_t* exp
     if (T == 0) return hip_status(hipMemsetAsync(expert_offsets, 0, sizeof(int32_t) * (E + 1), s));
     Carver c(workspace);
     void* ws = c.take(permute_workspace_bytes(T, E, k));
-    hipError_t err = launch_permute(topk_idx, T, E, k, expert_offsets, perm_token, perm_inv, ws, s);
+    hipError_t err = launch_permute(topk_idx, T, E, k, expert_offsets, perm_token, perm_inv, ws, nullptr, s);
     if (err != hipSuccess) return SMOES_ERR_HIP;
     if (x_perm != nullptr) err = launch_gather_rows(x, x_dtype, d, perm_token, T * k, x_perm, s);
     return hip_status(err);
@@ -279,19 +311,6 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
         if ((err = (expr)) != hipSuccess) return SMOES_ERR_HIP; \
     } while (0)
 
-    SMOES_TRY(record(ev, SMOES_STAGE_ROUTE, s));
-    SMOES_TRY(launch_route(io->x, L->act_dtype, T, L->d, io->w_gate, L->weights_packed ? io->w_gate_packed : nullptr,
-                           io->logit_bias, L->E, L->k,
-                           L->renorm_topk ? 1 : 0, logits, io->probs, io->topk_idx, io->topk_w, w.route, s));
-    SMOES_TRY(record(ev, SMOES_STAGE_MODALITY, s));
-    SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
-                              io->gauss_ssig, L->update_stats ? 1 : 0, L->beta, L->tau, L->var_floor,
-                              io->M, w.modality, s));
-    SMOES_TRY(record(ev, SMOES_STAGE_MI, s));
-    SMOES_TRY(launch_mi(io->probs, io->M, T, L->E, io->sample_offsets, L->n_batch, io->expert_to_bin,
-                        L->n_bins, L->grad_scale, io->mi_per_sample, io->loss, io->dlogits, w.mi, s));
-    SMOES_TRY(record(ev, SMOES_STAGE_PERMUTE, s));
-    SMOES_TRY(launch_permute(io->topk_idx, T, L->E, L->k, offsets, perm_token, perm_inv, w.permute, s));
     ExpertArgs a;
     a.T = T;
     a.d = L->d;
@@ -311,14 +330,47 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     a.perm_inv = perm_inv;
     a.topk_w = io->topk_w;
     a.out = io->out;
-    SMOES_TRY(launch_experts_plan(a, w.experts, s));
-    SMOES_TRY(record(ev, SMOES_STAGE_GEMM1, s));
+    const WorkTables wt = experts_work_tables(a, w.experts);
+
+    // Caller's stream s: route -> permute -> GEMM1 -> GEMM2 -> combine.
+    // Side stream b: modality (after everything queued on s before this
+    // call) -> [route done] -> MI; s waits for b before returning.
+    std::lock_guard<std::mutex> lock(g_side_mu);
+    SideStream* ss = nullptr;
+    SMOES_TRY(side_stream_locked(&ss));
+    hipStream_t b = ss->stream;
+    SMOES_TRY(hipEventRecord(ss->fork, s));
+    SMOES_TRY(hipStreamWaitEvent(b, ss->fork, 0));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_MODALITY, b));
+    SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
+                              io->gauss_ssig, L->update_stats ? 1 : 0, L->beta, L->tau, L->var_floor,
+                              io->M, w.modality, b));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_MODALITY + 1, b));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_ROUTE, s));
+    SMOES_TRY(launch_route(io->x, L->act_dtype, T, L->d, io->w_gate, L->weights_packed ? io->w_gate_packed : nullptr,
+                           io->logit_bias, L->E, L->k, L->renorm_topk ? 1 : 0, logits, io->probs, io->topk_idx,
+                           io->topk_w, w.route, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_ROUTE + 1, s));
+    SMOES_TRY(hipEventRecord(ss->routed, s));
+    SMOES_TRY(hipStreamWaitEvent(b, ss->routed, 0));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_MI, b));
+    SMOES_TRY(launch_mi(io->probs, io->M, T, L->E, io->sample_offsets, L->n_batch, io->expert_to_bin,
+                        L->n_bins, L->grad_scale, io->mi_per_sample, io->loss, io->dlogits, w.mi, b));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_MI + 1, b));
+    SMOES_TRY(hipEventRecord(ss->join, b));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE, s));
+    SMOES_TRY(launch_permute(io->topk_idx, T, L->E, L->k, offsets, perm_token, perm_inv, w.permute, &wt, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE + 1, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1, s));
     SMOES_TRY(launch_experts_gemm1(a, w.experts, s));
-    SMOES_TRY(record(ev, SMOES_STAGE_GEMM2, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1 + 1, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2, s));
     SMOES_TRY(launch_experts_gemm2(a, w.experts, s));
-    SMOES_TRY(record(ev, SMOES_STAGE_COMBINE, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2 + 1, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
     SMOES_TRY(launch_experts_combine(a, w.experts, s));
-    SMOES_TRY(record(ev, SMOES_N_STAGES, s));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));
+    SMOES_TRY(hipStreamWaitEvent(s, ss->join, 0));
 #undef SMOES_TRY
     return SMOES_OK;
 }

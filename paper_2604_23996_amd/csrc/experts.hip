@@ -3,9 +3,9 @@
 // Groups: g < E is routed expert g over its expert-contiguous rows
 // [off[g], off[g+1]) (rows gathered from x through perm_token inside the
 // GEMM's loader, so no permuted copy of x is written); g = E is the merged
-// shared expert over all T tokens. A device-built work table (prefix over
-// groups of m_tiles * n_tiles) lets one launch cover every group without any
-// host synchronisation.
+// shared expert over all T tokens. A work table (prefix over groups of
+// m_tiles * n_tiles, written on the device by the permutation) lets one
+// launch cover every group without any host synchronisation.
 //
 // Block -> tile mapping: blocks are dealt round-robin to the 8 XCDs, so block b
 // runs on XCD b % 8. Each XCD takes one contiguous eighth of the work list,
@@ -66,29 +66,6 @@ ExpWs carve(void* ws, int64_t T, int d, int k, int inter, int shared_inter, int 
     p += align_up(sizeof(int32_t) * (E + 2), 256);
     w.work2 = reinterpret_cast<int32_t*>(p);
     return w;
-}
-
-// Work table: work[g + 1] = work[g] + m_tiles(g) * n_tiles(g) for g in [0, G):
-// one thread per group and a block-wide inclusive scan (E + 1 <= 257 groups).
-__global__ void __launch_bounds__(512)
-build_work_kernel(const int32_t* __restrict__ off, int E, int64_t T, int has_shared, int bm,
-                  int nt_routed, int nt_shared, int32_t* __restrict__ work) {
-    __shared__ int32_t sc[512];
-    const int g = threadIdx.x;
-    int32_t v = 0;
-    if (g < E) v = static_cast<int32_t>(ceil_div(off[g + 1] - off[g], bm)) * nt_routed;
-    else if (g == E && has_shared) v = static_cast<int32_t>(ceil_div(T, bm)) * nt_shared;
-    sc[g] = v;
-    __syncthreads();
-    for (int o = 1; o < 512; o <<= 1) {
-        const int32_t add = g >= o ? sc[g - o] : 0;
-        __syncthreads();
-        v += add;
-        sc[g] = v;
-        __syncthreads();
-    }
-    if (g == 0) work[0] = 0;
-    if (g <= E) work[g + 1] = v;
 }
 
 struct Tile {
@@ -937,16 +914,18 @@ size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int sh
            2 * align_up(sizeof(int32_t) * (E + 2), 256);
 }
 
-hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream) {
+WorkTables experts_work_tables(const ExpertArgs& a, void* ws) {
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
     const Plan p = plan_of(a);
-    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(512), 0, stream, a.expert_offsets, a.E, a.T,
-                       p.has_shared ? 1 : 0, p.bm, p.nt1_r, p.nt1_s, w.work1);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(build_work_kernel, dim3(1), dim3(512), 0, stream, a.expert_offsets, a.E, a.T,
-                       p.has_shared ? 1 : 0, p.bm2, p.nt2, p.nt2, w.work2);
-    return hipGetLastError();
+    WorkTables t;
+    t.work1 = w.work1;
+    t.work2 = w.work2;
+    t.bm = p.bm;  // both GEMMs use the same tile height
+    t.nt1_r = p.nt1_r;
+    t.nt1_s = p.nt1_s;
+    t.nt2 = p.nt2;
+    t.has_shared = p.has_shared ? 1 : 0;
+    return t;
 }
 
 hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream) {

@@ -36,9 +36,16 @@ hipError_t launch_mi(const float* probs, const float* M, int64_t T, int E,
 
 // ---------------------------------------------------------------- permutation
 size_t permute_workspace_bytes(int64_t T, int E, int k);
+// Work tables of the grouped GEMMs (filled by the permutation, which knows
+// the per-expert row counts): work[g + 1] = work[g] + m_tiles(g) * n_tiles.
+struct WorkTables {
+    int32_t* work1;  // [E + 2] GEMM1 (NULL: not wanted)
+    int32_t* work2;  // [E + 2] GEMM2
+    int bm, nt1_r, nt1_s, nt2, has_shared;
+};
 hipError_t launch_permute(const int32_t* topk_idx, int64_t T, int E, int k,
                           int32_t* expert_offsets, int32_t* perm_token, int32_t* perm_inv,
-                          void* ws, hipStream_t stream);
+                          void* ws, const WorkTables* work, hipStream_t stream);
 hipError_t launch_gather_rows(const void* x, int x_dtype, int d, const int32_t* perm_token,
                               int64_t R, void* x_perm, hipStream_t stream);
 
@@ -60,8 +67,8 @@ struct ExpertArgs {
 };
 size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int shared_inter,
                                int act_dtype);
-// work tables of both grouped GEMMs (reads expert_offsets on the device)
-hipError_t launch_experts_plan(const ExpertArgs& a, void* ws, hipStream_t stream);
+// work tables of both grouped GEMMs: where they live and their tiling
+WorkTables experts_work_tables(const ExpertArgs& a, void* ws);
 hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t stream);

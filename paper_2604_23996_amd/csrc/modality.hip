@@ -8,7 +8,8 @@
 //     gauss_merge: one thread per (modality, column) adds the chunk partials
 //       in chunk order and applies the EMA update.
 //  score: gauss_prep turns the state into per-column mu_m and 1 / sigma^2_m
-//     (fp64 division, stored fp32) and the fp64 constant sum_d log(s2_v / s2_t);
+//     (fp64 division, stored fp32) and the fp64 constant sum_d log(s2_v / s2_t)
+//     as per-block parts;
 //     modality_score evaluates, per token,
 //       Delta = sum_d [log s2_v - log s2_t + (x - mu_v)^2 / s2_v - (x - mu_t)^2 / s2_t]
 //     (each column's two squared terms in fp32, accumulated in fp64);
@@ -27,10 +28,12 @@ constexpr int kChunkRows = 256;   // tokens per gauss_partial block
 constexpr int kColsPerBlock = 512; // 64 lanes x 8 columns
 constexpr int kScoreTokPerWave = 2;
 constexpr int kScoreThreads = 256;
+constexpr int kPrepThreads = 256;   // columns per gauss_prep block
+constexpr int kPrepMaxBlocks = 64;  // SMOES_D_MAX / kPrepThreads
 
 struct ModalityWs {
     float* coef;       // [4][d]: mu_v, 1/s2_v, mu_t, 1/s2_t
-    double* cst;       // [1]: sum_d (log s2_v - log s2_t)
+    double* cst;       // [ceil(d / 256)]: per column block, sum (log s2_v - log s2_t)
     double* n_old;     // [2]: state counts before the update
     int32_t* counts;   // [nchunk][2]
     double* s1;        // [nchunk][2][d]
@@ -44,7 +47,7 @@ ModalityWs carve(void* ws, int64_t T, int d) {
     w.coef = reinterpret_cast<float*>(p);
     p += align_up(sizeof(float) * 4 * d, 256);
     w.cst = reinterpret_cast<double*>(p);
-    p += 256;
+    p += sizeof(double) * kPrepMaxBlocks;
     w.n_old = reinterpret_cast<double*>(p);
     p += 256;
     w.counts = reinterpret_cast<int32_t*>(p);
@@ -195,15 +198,18 @@ __global__ void gauss_merge_kernel(int d, int64_t nchunk, const int32_t* __restr
     if (col == 0) gauss_n[m] = static_cast<float>(b * nprev + nt);
 }
 
-// Per-column score coefficients and the fp64 constant, one block.
-__global__ void __launch_bounds__(1024)
+// Per-column score coefficients; each block of 256 columns also writes its
+// part of the fp64 constant (a fixed-order LDS tree), summed in block order
+// by modality_score.
+__global__ void __launch_bounds__(kPrepThreads)
 gauss_prep_kernel(int d, const float* __restrict__ gauss_n, const float* __restrict__ gauss_smu,
                   const float* __restrict__ gauss_ssig, float var_floor, float* __restrict__ coef,
-                  double* __restrict__ cst) {
-    __shared__ double part[1024];
+                  double* __restrict__ cst_part) {
+    __shared__ double part[kPrepThreads];
     const double nv = gauss_n[0], nt = gauss_n[1];
+    const int c = blockIdx.x * kPrepThreads + threadIdx.x;
     double acc = 0.0;
-    for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    if (c < d) {
         double mv = 0.0, vv = 1.0, mt = 0.0, vt = 1.0;
         if (nv > 0.0) {
             mv = gauss_smu[c] / nv;
@@ -217,25 +223,26 @@ gauss_prep_kernel(int d, const float* __restrict__ gauss_n, const float* __restr
         coef[d + c] = static_cast<float>(1.0 / vv);
         coef[2 * d + c] = static_cast<float>(mt);
         coef[3 * d + c] = static_cast<float>(1.0 / vt);
-        acc += log(vv) - log(vt);
+        acc = log(vv) - log(vt);
     }
     part[threadIdx.x] = acc;
     __syncthreads();
-    for (int s = 512; s > 0; s >>= 1) {
+    for (int s = kPrepThreads / 2; s > 0; s >>= 1) {
         if (threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
         __syncthreads();
     }
-    if (threadIdx.x == 0) cst[0] = part[0];
+    if (threadIdx.x == 0) cst_part[blockIdx.x] = part[0];
 }
 
 template <bool BF16>
 __global__ void __launch_bounds__(kScoreThreads)
 modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restrict__ coef,
-                      const double* __restrict__ cst, double inv2tau, float* __restrict__ M) {
+                      const double* __restrict__ cst_part, int n_part, double inv2tau, float* __restrict__ M) {
+    __shared__ double red[kScoreThreads / kWave][kScoreTokPerWave][kWave];
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
     const int64_t tok0 = (static_cast<int64_t>(blockIdx.x) * (kScoreThreads / kWave) + wave) * kScoreTokPerWave;
-    if (tok0 >= T) return;
+    if (tok0 >= T) return;  // whole waves only: the reduction below is wave-local
     int64_t rows[kScoreTokPerWave];
 #pragma unroll
     for (int t = 0; t < kScoreTokPerWave; ++t) rows[t] = tok0 + t < T ? tok0 + t : T - 1;
@@ -271,11 +278,20 @@ modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float*
             acc[t] += static_cast<double>(part);
         }
     }
-    const double c = cst[0];
+    // per token: the 64 lane partials in lane order, then the constant in block order
 #pragma unroll
-    for (int t = 0; t < kScoreTokPerWave; ++t) {
-        const double delta = wave_sum(acc[t]) + c;
-        if (lane == t && tok0 + t < T) {
+    for (int t = 0; t < kScoreTokPerWave; ++t) red[wave][t][lane] = acc[t];
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < kScoreTokPerWave) {
+        const int t = lane;
+        double sum = 0.0;
+        for (int l = 0; l < kWave; ++l) sum += red[wave][t][l];
+        double c = 0.0;
+        for (int b = 0; b < n_part; ++b) c += cst_part[b];
+        const double delta = sum + c;
+        if (tok0 + t < T) {
             const double s = -delta * inv2tau;
             double mv, mt;
             if (s >= 0.0) {
@@ -297,7 +313,7 @@ modality_score_kernel(const void* __restrict__ x, int64_t T, int d, const float*
 
 size_t modality_workspace_bytes(int64_t T, int d) {
     const int64_t nchunk = ceil_div(T, kChunkRows);
-    return align_up(sizeof(float) * 4 * d, 256) + 256 + 256 +
+    return align_up(sizeof(float) * 4 * d, 256) + sizeof(double) * kPrepMaxBlocks + 256 +
            align_up(sizeof(int32_t) * 2 * nchunk, 256) +
            2 * align_up(sizeof(double) * 2 * nchunk * d, 256);
 }
@@ -324,7 +340,8 @@ hipError_t launch_modality(const void* x, int x_dtype, int64_t T, int d, const u
                            gauss_n, gauss_smu, gauss_ssig);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    hipLaunchKernelGGL(gauss_prep_kernel, dim3(1), dim3(1024), 0, stream, d, gauss_n, gauss_smu,
+    const int n_part = static_cast<int>(ceil_div(d, kPrepThreads));
+    hipLaunchKernelGGL(gauss_prep_kernel, dim3(n_part), dim3(kPrepThreads), 0, stream, d, gauss_n, gauss_smu,
                        gauss_ssig, var_floor, w.coef, w.cst);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const double t = tau > 0.0f ? static_cast<double>(tau) : 0.5 * d;
@@ -333,10 +350,10 @@ hipError_t launch_modality(const void* x, int x_dtype, int64_t T, int d, const u
     const dim3 grid(static_cast<unsigned>(ceil_div(T, tok_per_block)));
     if (bf16)
         hipLaunchKernelGGL(modality_score_kernel<true>, grid, dim3(kScoreThreads), 0, stream, x, T,
-                           d, w.coef, w.cst, inv2tau, M);
+                           d, w.coef, w.cst, n_part, inv2tau, M);
     else
         hipLaunchKernelGGL(modality_score_kernel<false>, grid, dim3(kScoreThreads), 0, stream, x,
-                           T, d, w.coef, w.cst, inv2tau, M);
+                           T, d, w.coef, w.cst, n_part, inv2tau, M);
     return hipGetLastError();
 }
 

@@ -3,13 +3,14 @@
 //
 //   perm_count  : per 256-token chunk, per-expert counts (LDS integer adds:
 //                 counts do not depend on their order).
-//   perm_scan   : one block; per expert, exclusive prefix over chunks, then an
-//                 exclusive scan over experts -> expert_offsets and the base
-//                 row of every (chunk, expert).
-//   perm_scatter: per chunk; for every expert a wave ballot marks the lanes
-//                 (tokens) that chose it, so the rank of a token among the
-//                 chunk's earlier tokens is a popcount: the row order comes
-//                 from prefix sums only, never from atomics.
+//   perm_scatter: per chunk; every block sums the chunk counts itself (per
+//                 expert: the total and the part before its chunk), scans the
+//                 totals over experts, and places its rows: for every expert a
+//                 wave ballot marks the lanes (tokens) that chose it, so the
+//                 rank of a token among the chunk's earlier tokens is a
+//                 popcount. The row order comes from prefix sums only, never
+//                 from atomics. Block 0 also writes expert_offsets and, when
+//                 asked, the grouped GEMMs' work tables.
 // Row gathers (x_perm) copy 16-byte vectors with consecutive lanes on
 // consecutive addresses of one row.
 #include "common.h"
@@ -23,16 +24,11 @@ constexpr int kChunk = 256;
 
 struct PermWs {
     int32_t* hist;  // [nchunk][E]
-    int32_t* base;  // [nchunk][E]
 };
 
-PermWs carve(void* ws, int64_t T, int E) {
-    const int64_t nchunk = ceil_div(T, kChunk);
+PermWs carve(void* ws) {
     PermWs w;
-    char* p = static_cast<char*>(ws);
-    w.hist = reinterpret_cast<int32_t*>(p);
-    p += align_up(sizeof(int32_t) * nchunk * E, 256);
-    w.base = reinterpret_cast<int32_t*>(p);
+    w.hist = static_cast<int32_t*>(ws);
     return w;
 }
 
@@ -48,49 +44,78 @@ perm_count_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k, int3
     for (int e = threadIdx.x; e < E; e += blockDim.x) hist[static_cast<int64_t>(blockIdx.x) * E + e] = cnt[e];
 }
 
-__global__ void __launch_bounds__(256)
-perm_scan_kernel(int64_t nchunk, int E, const int32_t* __restrict__ hist, int32_t* __restrict__ base,
-                 int32_t* __restrict__ expert_offsets) {
-    __shared__ int tot[256];
-    const int e = threadIdx.x;
-    int running = 0;
-    if (e < E) {
-        for (int64_t c = 0; c < nchunk; ++c) {
-            base[c * E + e] = running;
-            running += hist[c * E + e];
-        }
-    }
-    tot[e] = e < E ? running : 0;
-    __syncthreads();
-    // exclusive scan of the per-expert totals (Hillis-Steele on 256 entries)
-    int v = tot[e];
-    for (int o = 1; o < 256; o <<= 1) {
-        const int add = e >= o ? tot[e - o] : 0;
-        __syncthreads();
-        v += add;
-        tot[e] = v;
-        __syncthreads();
-    }
-    const int excl = v - (e < E ? running : 0);
-    if (e < E) {
-        expert_offsets[e] = excl;
-        for (int64_t c = 0; c < nchunk; ++c) base[c * E + e] += excl;
-    }
-    if (e == E - 1) expert_offsets[E] = v;
-}
-
 __device__ __forceinline__ uint64_t lanemask_lt() {
     const int lane = lane_id();
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// Block-wide inclusive scan of one int per thread (256 threads).
+__device__ __forceinline__ int block_scan_incl(int v, int32_t* sc) {
+    const int t = threadIdx.x;
+    sc[t] = v;
+    __syncthreads();
+    for (int o = 1; o < kChunk; o <<= 1) {
+        const int add = t >= o ? sc[t - o] : 0;
+        __syncthreads();
+        v += add;
+        sc[t] = v;
+        __syncthreads();
+    }
+    return v;
+}
+
 __global__ void __launch_bounds__(kChunk)
-perm_scatter_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k,
-                    const int32_t* __restrict__ base, int32_t* __restrict__ perm_token,
-                    int32_t* __restrict__ perm_inv) {
+perm_scatter_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k, int64_t nchunk,
+                    const int32_t* __restrict__ hist, int32_t* __restrict__ expert_offsets,
+                    int32_t* __restrict__ perm_token, int32_t* __restrict__ perm_inv, WorkTables wt) {
     __shared__ uint64_t masks[kChunk / kWave][256];
+    __shared__ int32_t base_s[256];
+    __shared__ int32_t sc[kChunk];
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
+    {
+        // per expert: total over all chunks and the part before this chunk (fixed order)
+        const int e = threadIdx.x;
+        int tot = 0, pre = 0;
+        if (e < E) {
+            // eight independent loads in flight, summed in chunk order
+            for (int64_t c0 = 0; c0 < nchunk; c0 += 8) {
+                int h[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) h[q] = c0 + q < nchunk ? hist[(c0 + q) * E + e] : 0;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    tot += h[q];
+                    pre += c0 + q < blockIdx.x ? h[q] : 0;
+                }
+            }
+        }
+        const int incl = block_scan_incl(tot, sc);
+        const int excl = incl - tot;
+        if (e < E) base_s[e] = excl + pre;
+        if (blockIdx.x == 0) {
+            if (e < E) expert_offsets[e] = excl;
+            if (e == E - 1) expert_offsets[E] = incl;
+            if (wt.work1 != nullptr) {
+                // GEMM work tables: work[g + 1] = work[g] + m_tiles(g) * n_tiles
+                const int mt = e < E ? static_cast<int>(ceil_div(tot, wt.bm)) : 0;
+                const int mt_incl = block_scan_incl(mt, sc);
+                const int shared_mt = wt.has_shared ? static_cast<int>(ceil_div(T, wt.bm)) : 0;
+                if (e == 0) {
+                    wt.work1[0] = 0;
+                    wt.work2[0] = 0;
+                }
+                if (e < E) {
+                    wt.work1[e + 1] = mt_incl * wt.nt1_r;
+                    wt.work2[e + 1] = mt_incl * wt.nt2;
+                }
+                if (e == E - 1) {
+                    wt.work1[E + 1] = mt_incl * wt.nt1_r + shared_mt * wt.nt1_s;
+                    wt.work2[E + 1] = mt_incl * wt.nt2 + shared_mt * wt.nt2;
+                }
+            }
+        }
+    }
     const int64_t j = static_cast<int64_t>(blockIdx.x) * kChunk + threadIdx.x;
     const bool live = j < T;
     int sel[SMOES_K_MAX_DEV];
@@ -124,7 +149,7 @@ perm_scatter_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k,
     }
     __syncthreads();
     if (!live) return;
-    const int32_t* bc = base + static_cast<int64_t>(blockIdx.x) * E;
+    const int32_t* bc = base_s;
     const uint64_t lt = lanemask_lt();
 #pragma unroll
     for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
@@ -164,23 +189,22 @@ __global__ void gather_rows_kernel(const void* __restrict__ x, int d, const int3
 
 size_t permute_workspace_bytes(int64_t T, int E, int /*k*/) {
     const int64_t nchunk = ceil_div(T, kChunk);
-    return 2 * align_up(sizeof(int32_t) * nchunk * E, 256);
+    return align_up(sizeof(int32_t) * nchunk * E, 256);
 }
 
 hipError_t launch_permute(const int32_t* topk_idx, int64_t T, int E, int k,
                           int32_t* expert_offsets, int32_t* perm_token, int32_t* perm_inv,
-                          void* ws, hipStream_t stream) {
-    PermWs w = carve(ws, T, E);
+                          void* ws, const WorkTables* work, hipStream_t stream) {
+    PermWs w = carve(ws);
     const int64_t nchunk = ceil_div(T, kChunk);
+    WorkTables wt{};
+    if (work != nullptr) wt = *work;
     hipError_t err;
     hipLaunchKernelGGL(perm_count_kernel, dim3(static_cast<unsigned>(nchunk)), dim3(kChunk), 0, stream,
                        topk_idx, T, E, k, w.hist);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, stream, nchunk, E, w.hist, w.base,
-                       expert_offsets);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
     hipLaunchKernelGGL(perm_scatter_kernel, dim3(static_cast<unsigned>(nchunk)), dim3(kChunk), 0, stream,
-                       topk_idx, T, E, k, w.base, perm_token, perm_inv);
+                       topk_idx, T, E, k, nchunk, w.hist, expert_offsets, perm_token, perm_inv, wt);
     return hipGetLastError();
 }
 

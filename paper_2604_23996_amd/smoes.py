@@ -286,12 +286,16 @@ def pack_weights(spec: LayerSpec, which: int, src: torch.Tensor) -> torch.Tensor
 
 
 class Events:
-    """SMOES_N_STAGES + 1 HIP events for the forward's stage timing."""
+    """2 * SMOES_N_STAGES HIP events for the forward's stage timing: events
+    2s and 2s + 1 bracket stage s on the stream that runs it."""
 
-    def __init__(self, n: int = N_STAGES + 1):
+    def __init__(self, n: int = 2 * N_STAGES):
         self.n = n
         self.arr = (c_void * n)()
         _check(lib().smoes_events_create(n, self.arr), "smoes_events_create")
+
+    def stage_ms(self, stage: int) -> float:
+        return self.elapsed_ms(2 * stage, 2 * stage + 1)
 
     def elapsed_ms(self, a: int, b: int) -> float:
         ms = c_float()
