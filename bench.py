@@ -49,11 +49,11 @@ def stage_work(cfg, T):
         "modality": dict(flops=6 * T * d * upd, bytes=upd * T * d * s + T * 8 + T * (1 if upd > 1 else 0)),
         "mi": dict(flops=4 * T * E, bytes=T * (12 * E + 16)),
         "permute": dict(flops=0, bytes=2 * R * 4 + 2 * R * 4),
-        "gemm1": dict(flops=4 * R * d * I + 4 * T * d * SI,
-                      bytes=(E * 2 * I * d + 2 * SI * d + R * d + T * d + R * I + T * SI) * s),
-        "gemm2": dict(flops=2 * R * I * d + 2 * T * SI * d,
-                      bytes=(E * d * I + d * SI + R * I + T * SI + R * d + T * d) * s),
+        "gemm1": dict(flops=4 * R * d * I, bytes=(E * 2 * I * d + R * d + R * I) * s),
+        "gemm2": dict(flops=2 * R * I * d, bytes=(E * d * I + R * I + R * d) * s),
         "combine": dict(flops=2 * R * d, bytes=(R + (T if SI else 0) + T) * d * s + R * 8),
+        "gemm1_shared": dict(flops=4 * T * d * SI, bytes=(2 * SI * d + T * d + T * SI) * s),
+        "gemm2_shared": dict(flops=2 * T * SI * d, bytes=(d * SI + T * SI + T * d) * s),
     }
     return w
 

@@ -244,17 +244,21 @@ typedef struct smoes_layer_io {
 
 /* Stages of smoes_moe_forward. ROUTE, PERMUTE, GEMM1, GEMM2 and COMBINE run
  * in this order on the caller's stream; MODALITY and then MI (after ROUTE)
- * run on a side stream that the library keeps per device, and the caller's
- * stream waits for it before the call's work is complete. */
+ * run on one side stream, GEMM1_SHARED and GEMM2_SHARED on another (the
+ * library keeps both per device); COMBINE waits for the shared GEMMs and the
+ * caller's stream waits for both side streams before the call's work is
+ * complete. */
 enum smoes_stage {
-    SMOES_STAGE_ROUTE = 0,    /* router GEMM + softmax + top-k */
-    SMOES_STAGE_MODALITY = 1, /* statistics update (optional) + modality score */
-    SMOES_STAGE_MI = 2,       /* MI partials, loss, gradient */
-    SMOES_STAGE_PERMUTE = 3,  /* expert-contiguous order + work list */
-    SMOES_STAGE_GEMM1 = 4,    /* grouped gate/up GEMM + SwiGLU (routed + shared) */
-    SMOES_STAGE_GEMM2 = 5,    /* grouped down GEMM (routed + shared) */
-    SMOES_STAGE_COMBINE = 6,  /* weighted combine */
-    SMOES_N_STAGES = 7
+    SMOES_STAGE_ROUTE = 0,        /* router GEMM + softmax + top-k */
+    SMOES_STAGE_MODALITY = 1,     /* statistics update (optional) + modality score */
+    SMOES_STAGE_MI = 2,           /* MI partials, loss, gradient */
+    SMOES_STAGE_PERMUTE = 3,      /* expert-contiguous order + work lists */
+    SMOES_STAGE_GEMM1 = 4,        /* routed experts: grouped gate/up GEMM + SwiGLU */
+    SMOES_STAGE_GEMM2 = 5,        /* routed experts: grouped down GEMM */
+    SMOES_STAGE_COMBINE = 6,      /* weighted combine + shared output */
+    SMOES_STAGE_GEMM1_SHARED = 7, /* shared experts: gate/up GEMM + SwiGLU */
+    SMOES_STAGE_GEMM2_SHARED = 8, /* shared experts: down GEMM */
+    SMOES_N_STAGES = 9
 };
 
 size_t smoes_workspace_bytes(const smoes_layer* desc);

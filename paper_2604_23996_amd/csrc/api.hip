@@ -68,14 +68,16 @@ hipError_t record(void* const* ev, int idx, hipStream_t st) {
     return hipEventRecord(static_cast<hipEvent_t>(ev[idx]), st);
 }
 
-// Side stream of one device: the modality score and the MI chain run on it,
-// beside the permutation and the expert GEMMs on the caller's stream. Made on
-// first use (default priority, not blocking on the legacy default stream) and
-// kept until the process ends; one mutex orders the event records and waits
-// of concurrent calls.
+// Side streams of one device: the modality score and the MI chain run on
+// one, the shared expert's GEMMs on the other, beside the routing, the
+// permutation and the routed GEMMs on the caller's stream. Made on first use
+// (default priority, not blocking on the legacy default stream) and kept
+// until the process ends; one mutex orders the event records and waits of
+// concurrent calls.
 struct SideStream {
-    hipStream_t stream = nullptr;
-    hipEvent_t fork = nullptr, routed = nullptr, join = nullptr;
+    hipStream_t stream = nullptr;         // modality score, then the MI chain
+    hipStream_t shared_stream = nullptr;  // the shared expert's two GEMMs
+    hipEvent_t fork = nullptr, routed = nullptr, join = nullptr, shared_done = nullptr;
 };
 constexpr int kMaxDevices = 64;
 std::mutex g_side_mu;
@@ -87,11 +89,14 @@ hipError_t side_stream_locked(SideStream** out) {
     if (err != hipSuccess) return err;
     if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
     SideStream& ss = g_side[dev];
-    if (ss.stream == nullptr) {
-        if ((err = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking)) != hipSuccess) return err;
-        if ((err = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess) return err;
-        if ((err = hipEventCreateWithFlags(&ss.routed, hipEventDisableTiming)) != hipSuccess) return err;
-        if ((err = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess) return err;
+    if (ss.shared_done == nullptr) {
+        if (ss.stream == nullptr && (err = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking)) != hipSuccess)
+            return err;
+        if (ss.shared_stream == nullptr &&
+            (err = hipStreamCreateWithFlags(&ss.shared_stream, hipStreamNonBlocking)) != hipSuccess)
+            return err;
+        for (hipEvent_t* e : {&ss.fork, &ss.routed, &ss.join, &ss.shared_done})
+            if (*e == nullptr && (err = hipEventCreateWithFlags(e, hipEventDisableTiming)) != hipSuccess) return err;
     }
     *out = &ss;
     return hipSuccess;
@@ -332,15 +337,25 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     a.out = io->out;
     const WorkTables wt = experts_work_tables(a, w.experts);
 
-    // Caller's stream s: route -> permute -> GEMM1 -> GEMM2 -> combine.
-    // Side stream b: modality (after everything queued on s before this
-    // call) -> [route done] -> MI; s waits for b before returning.
+    // Caller's stream s: route -> permute -> routed GEMM1 -> routed GEMM2 ->
+    // [shared GEMMs done] -> combine. Side stream b: modality -> [route done]
+    // -> MI. Side stream c: shared GEMM1 -> shared GEMM2 (they need x only).
+    // Both side streams start after everything queued on s before this call,
+    // and s waits for both before the call's work is complete.
     std::lock_guard<std::mutex> lock(g_side_mu);
     SideStream* ss = nullptr;
     SMOES_TRY(side_stream_locked(&ss));
-    hipStream_t b = ss->stream;
+    hipStream_t b = ss->stream, c = ss->shared_stream;
     SMOES_TRY(hipEventRecord(ss->fork, s));
+    SMOES_TRY(hipStreamWaitEvent(c, ss->fork, 0));
     SMOES_TRY(hipStreamWaitEvent(b, ss->fork, 0));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED, c));
+    SMOES_TRY(launch_experts_gemm1(a, w.experts, 2, c));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED + 1, c));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED, c));
+    SMOES_TRY(launch_experts_gemm2(a, w.experts, 2, c));
+    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED + 1, c));
+    SMOES_TRY(hipEventRecord(ss->shared_done, c));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_MODALITY, b));
     SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
                               io->gauss_ssig, L->update_stats ? 1 : 0, L->beta, L->tau, L->var_floor,
@@ -362,11 +377,12 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     SMOES_TRY(launch_permute(io->topk_idx, T, L->E, L->k, offsets, perm_token, perm_inv, w.permute, &wt, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE + 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1, s));
-    SMOES_TRY(launch_experts_gemm1(a, w.experts, s));
+    SMOES_TRY(launch_experts_gemm1(a, w.experts, 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1 + 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2, s));
-    SMOES_TRY(launch_experts_gemm2(a, w.experts, s));
+    SMOES_TRY(launch_experts_gemm2(a, w.experts, 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2 + 1, s));
+    SMOES_TRY(hipStreamWaitEvent(s, ss->shared_done, 0));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
     SMOES_TRY(launch_experts_combine(a, w.experts, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));

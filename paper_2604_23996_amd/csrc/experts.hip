@@ -80,34 +80,46 @@ struct Tile {
 // each cut into 8 contiguous ranges, one per XCD, so every XCD gets the same
 // share of both kinds (shared tiles can have a longer K than routed ones).
 // Inside a group items run (super-row of 8 m-tiles, n-tile, m-tile).
+// part: 0 every item, 1 routed items only, 2 shared items only. The shared
+// part never reads the work table (its item count follows from T and the
+// tiling), so it can run before the routing has been permuted.
 __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, const int32_t* __restrict__ off,
                                             int E, int64_t T, int bm, int nt_routed, int nt_shared,
-                                            Tile& t) {
-    const int routed = work[E];
-    const int shared = work[E + 1] - routed;
-    const int r8 = (routed + 7) / 8, s8 = (shared + 7) / 8;
+                                            int part, Tile& t) {
     const int xcd = blockIdx.x & 7;
     const int slot = blockIdx.x >> 3;
-    const int r_lo = min(xcd * r8, routed), r_hi = min(r_lo + r8, routed);
-    const int s_lo = min(xcd * s8, shared), s_hi = min(s_lo + s8, shared);
-    // shared items first: their K can be longer (GEMM2), and blocks are
-    // dispatched in index order, so the longest tiles start earliest
-    int w;
-    if (slot < s_hi - s_lo) w = routed + s_lo + slot;
-    else if (slot < (s_hi - s_lo) + (r_hi - r_lo)) w = r_lo + (slot - (s_hi - s_lo));
-    else return false;
-    int g;
-    if (w >= routed) {
+    int g, local;
+    if (part == 2) {
+        const int ns = static_cast<int>(ceil_div(T, bm)) * nt_shared;
+        const int s8 = (ns + 7) / 8;
+        const int s_lo = min(xcd * s8, ns), s_hi = min(s_lo + s8, ns);
+        if (slot >= s_hi - s_lo) return false;
         g = E;
+        local = s_lo + slot;
     } else {
-        int lo = 0, hi = E - 1;  // last g with work[g] <= w
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (work[mid] <= w) lo = mid; else hi = mid - 1;
+        const int routed = work[E];
+        const int ns = part == 1 ? 0 : work[E + 1] - routed;
+        const int r8 = (routed + 7) / 8, s8 = (ns + 7) / 8;
+        const int r_lo = min(xcd * r8, routed), r_hi = min(r_lo + r8, routed);
+        const int s_lo = min(xcd * s8, ns), s_hi = min(s_lo + s8, ns);
+        // shared items first: their K can be longer (GEMM2), and blocks are
+        // dispatched in index order, so the longest tiles start earliest
+        int w;
+        if (slot < s_hi - s_lo) w = routed + s_lo + slot;
+        else if (slot < (s_hi - s_lo) + (r_hi - r_lo)) w = r_lo + (slot - (s_hi - s_lo));
+        else return false;
+        if (w >= routed) {
+            g = E;
+        } else {
+            int lo = 0, hi = E - 1;  // last g with work[g] <= w
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (work[mid] <= w) lo = mid; else hi = mid - 1;
+            }
+            g = lo;
         }
-        g = lo;
+        local = w - work[g];
     }
-    const int local = w - work[g];
     int64_t base, rows_g;
     int ntn;
     if (g < E) {
@@ -147,6 +159,7 @@ struct GemmArgs {
     int64_t T;
     int d, E, k, inter, shared_inter;
     int packed;  // expert weights in the fragment order of pack_weights_kernel
+    int part;    // work items of this launch: 0 all, 1 routed, 2 shared
     const void* x;
     const void* w13;
     const void* w2;
@@ -213,7 +226,7 @@ gemm_bf16_dma_kernel(GemmArgs p) {
     const int nt_r = static_cast<int>(ceil_div(MODE == 1 ? p.inter : p.d, TC));
     const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
-    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, t)) return;
+    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, p.part, t)) return;
     const bool shared = t.g == p.E;
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
@@ -470,7 +483,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     const int nt_r = static_cast<int>(ceil_div(MODE == 1 ? p.inter : p.d, TC));
     const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
-    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, t)) return;
+    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, p.part, t)) return;
     const bool shared = t.g == p.E;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
 
@@ -721,7 +734,7 @@ gemm_f32_kernel(GemmArgs p) {
     const int nt_r = MODE == 1 ? static_cast<int>(ceil_div(p.inter, 32)) : static_cast<int>(ceil_div(p.d, 64));
     const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, 32)) : nt_r;
     Tile t;
-    if (!decode_tile(p.work, p.off, p.E, p.T, FBM, nt_r, nt_s, t)) return;
+    if (!decode_tile(p.work, p.off, p.E, p.T, FBM, nt_r, nt_s, p.part, t)) return;
     const bool shared = t.g == p.E;
     const int tid = threadIdx.x;
     int K, n_out;
@@ -850,8 +863,9 @@ __global__ void combine_kernel(int64_t T, int d, int k, const int32_t* __restric
     }
 }
 
-GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work) {
+GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work, int part) {
     GemmArgs g;
+    g.part = part;
     g.T = a.T;
     g.d = a.d;
     g.E = a.E;
@@ -876,10 +890,10 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work) {
 
 // Grid size: 8 XCD ranges, each at most a bound on the routed items over 8
 // plus the shared items over 8 (host side; the exact split is made on the device).
-int64_t work_bound(int64_t T, int k, int E, int bm, int nt_r, int nt_s, bool has_shared) {
+int64_t work_bound(int64_t T, int k, int E, int bm, int nt_r, int nt_s, bool has_shared, int part) {
     const int64_t R = T * k;
-    const int64_t routed = (ceil_div(R, bm) + E) * nt_r;
-    const int64_t shared = has_shared ? ceil_div(T, bm) * nt_s : 0;
+    const int64_t routed = part == 2 ? 0 : (ceil_div(R, bm) + E) * nt_r;
+    const int64_t shared = (has_shared && part != 1) ? ceil_div(T, bm) * nt_s : 0;
     return 8 * (ceil_div(routed, 8) + ceil_div(shared, 8));
 }
 
@@ -928,11 +942,12 @@ WorkTables experts_work_tables(const ExpertArgs& a, void* ws) {
     return t;
 }
 
-hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream) {
+hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, int part, hipStream_t stream) {
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
     const Plan p = plan_of(a);
-    const GemmArgs g = make_args(a, w, w.work1);
-    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared)));
+    const GemmArgs g = make_args(a, w, w.work1, part);
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared, part)));
+    if (grid.x == 0) return hipSuccess;
     if (a.act_dtype == 1 && a.packed)
         hipLaunchKernelGGL(gemm_bf16_pk_kernel<1>, grid, dim3(PK_THREADS), 0, stream, g);
     else if (a.act_dtype == 1)
@@ -942,11 +957,12 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t strea
     return hipGetLastError();
 }
 
-hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream) {
+hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, int part, hipStream_t stream) {
     ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
     const Plan p = plan_of(a);
-    const GemmArgs g = make_args(a, w, w.work2);
-    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm2, p.nt2, p.nt2, p.has_shared)));
+    const GemmArgs g = make_args(a, w, w.work2, part);
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm2, p.nt2, p.nt2, p.has_shared, part)));
+    if (grid.x == 0) return hipSuccess;
     if (a.act_dtype == 1 && a.packed)
         hipLaunchKernelGGL(gemm_bf16_pk_kernel<2>, grid, dim3(PK_THREADS), 0, stream, g);
     else if (a.act_dtype == 1)

@@ -69,8 +69,11 @@ size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int sh
                                int act_dtype);
 // work tables of both grouped GEMMs: where they live and their tiling
 WorkTables experts_work_tables(const ExpertArgs& a, void* ws);
-hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, hipStream_t stream);
-hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, hipStream_t stream);
+// part: 0 every work item, 1 the routed experts only, 2 the shared expert only
+// (the two parts can run on different streams once the work tables exist;
+// the shared items' entries in the tables do not depend on the routing)
+hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, int part, hipStream_t stream);
+hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, int part, hipStream_t stream);
 hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t stream);
 // packed bf16 expert weights: elements of `batch` packed n x k matrices
 // (interleave: gate and up halves of a 2n-row source)

@@ -24,8 +24,8 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "smoes.h")
 
 SMOES_OK, SMOES_ERR_ARG, SMOES_ERR_SHAPE, SMOES_ERR_WORKSPACE, SMOES_ERR_HIP = 0, -1, -2, -3, -4
 SMOES_F32, SMOES_BF16 = 0, 1
-N_STAGES = 7
-STAGES = ("route", "modality", "mi", "permute", "gemm1", "gemm2", "combine")
+N_STAGES = 9
+STAGES = ("route", "modality", "mi", "permute", "gemm1", "gemm2", "combine", "gemm1_shared", "gemm2_shared")
 
 _lib = None
 
