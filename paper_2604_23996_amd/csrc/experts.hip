@@ -594,9 +594,9 @@ gemm_bf16_pk_kernel(GemmArgs p) {
 #pragma unroll
             for (int i = 0; i < MT; ++i)
 #pragma unroll
-                for (int g = 0; g < 2; ++g)
+                for (int g = 0; g < 2; ++g)  // transposed tile: rows = weight columns, columns = tokens
                     acc[i][g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        af[j & 1][i], __builtin_bit_cast(bf16x8_t, bc[j][g]), acc[i][g], 0, 0, 0);
+                        __builtin_bit_cast(bf16x8_t, bc[j][g]), af[j & 1][i], acc[i][g], 0, 0, 0);
             // order: one VMEM after each of the first MFMAs, then one LDS read after each of
             // the following MFMAs, then the rest of the MFMAs
             constexpr int NM = 2 * MT;
@@ -656,21 +656,34 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     __builtin_amdgcn_s_barrier();
 
     // Epilogue through LDS: [BM][TC + 8] bf16 tile, then 16-byte row chunks.
-    // Element v of a 32x32 MFMA tile sits at row 8*(v/4) + 4*half + v%4, column l32.
+    // The accumulators hold transposed 32x32 tiles: element v of lane l is
+    // output column 8*(v/4) + 4*half + v%4 of token row l32, so each lane
+    // writes four adjacent columns as one 8-byte store.
     constexpr int OP = TC + 8;
     uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
+    auto pack4 = [](float a, float b, float c, float d) {
+        return make_uint2(static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16),
+                          static_cast<uint32_t>(f32_to_bf16(c)) | (static_cast<uint32_t>(f32_to_bf16(d)) << 16));
+    };
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
+        const int r = i * 32 + l32;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int r = i * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+        for (int vq = 0; vq < 4; ++vq) {
+            const int c0 = 8 * vq + 4 * half;
             if constexpr (MODE == 1) {
-                otile[r * OP + wave * 32 + l32] = f32_to_bf16(silu(acc[i][0][v]) * acc[i][1][v]);
+                float h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) h[e] = silu(acc[i][0][4 * vq + e]) * acc[i][1][4 * vq + e];
+                *reinterpret_cast<uint2*>(otile + r * OP + wave * 32 + c0) = pack4(h[0], h[1], h[2], h[3]);
             } else {
 #pragma unroll
-                for (int g = 0; g < 2; ++g) otile[r * OP + wave * 64 + g * 32 + l32] = f32_to_bf16(acc[i][g][v]);
+                for (int g = 0; g < 2; ++g)
+                    *reinterpret_cast<uint2*>(otile + r * OP + wave * 64 + g * 32 + c0) =
+                        pack4(acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
             }
         }
+    }
     __syncthreads();
     uint16_t* O;
     if constexpr (MODE == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
