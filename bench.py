@@ -80,8 +80,20 @@ def measured_traffic(kernel_stage):
     return ent["bytes_per_launch"]
 
 
-def cpu_baseline(cfg, inp, n_samples):
-    """The float64 oracle, as it stands, on the first n_samples samples."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, inp, n_samples, runs=3):
+    """The float64 oracle, as it stands, on the first n_samples samples: one
+    warm-up run, then the median of `runs` timed runs."""
     import numpy as np
     import oracle as O
     try:
@@ -93,25 +105,32 @@ def cpu_baseline(cfg, inp, n_samples):
     off = inp.sample_offsets[:n_samples + 1]
     x = inp.x[:Ts]
     mid = inp.modality_id[:Ts]
-    t0 = time.perf_counter()
-    st = O.GaussState.zeros(cfg.d)
-    st = O.gauss_update(st, x, mid, cfg.beta)
-    O.layer_forward(x, mid, off, inp.w_gate, inp.logit_bias, inp.expert_to_bin, cfg.n_bins, cfg.k,
-                    inp.w13, inp.w2, inp.ws13, inp.ws2, st, update_stats=cfg.update_stats,
-                    beta=cfg.beta, tau=cfg.tau)
-    dt = time.perf_counter() - t0
-    cores = min(threads, len(os.sched_getaffinity(0)))
+
+    def once():
+        t0 = time.perf_counter()
+        st = O.GaussState.zeros(cfg.d)
+        st = O.gauss_update(st, x, mid, cfg.beta)
+        O.layer_forward(x, mid, off, inp.w_gate, inp.logit_bias, inp.expert_to_bin, cfg.n_bins, cfg.k,
+                        inp.w13, inp.w2, inp.ws13, inp.ws2, st, update_stats=cfg.update_stats,
+                        beta=cfg.beta, tau=cfg.tau)
+        return time.perf_counter() - t0
+
+    once()  # warm-up
+    dt = float(np.median([once() for _ in range(runs)]))
+    affinity = len(os.sched_getaffinity(0))
+    cores = min(threads, affinity)
     return {"value": Ts / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"first {n_samples} samples ({Ts} tokens) of the workload: full layer forward "
-                      f"(statistics, routing, MI + gradient, permutation, experts) in float64 NumPy, "
-                      f"{dt:.1f} s"}
+                      f"(statistics, routing, MI + gradient, permutation, experts) in float64 NumPy; "
+                      f"median of {runs} runs after one warm-up, {dt:.2f} s per run; "
+                      f"{threads} BLAS threads, {affinity} CPUs in the affinity mask ({cpu_model()})"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=2)
@@ -174,19 +193,27 @@ def main():
     outs = S.alloc_outputs(spec, dev, act)
     ws = torch.empty(S.workspace_bytes(spec), dtype=torch.uint8, device=dev)
     events = [S.Events() for _ in range(args.steps)]
+    streams = S.Streams()  # side streams: modality + MI, and the shared experts
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
-        S.moe_forward(spec, dev_in, outs, ws)
+        S.moe_forward(spec, dev_in, outs, ws, streams=streams)
     torch.cuda.synchronize()
     log(f"[bench] timing {args.steps} steps")
+    call_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        S.moe_forward(spec, dev_in, outs, ws, events=events[i])
+        call_ev[i][0].record()
+        S.moe_forward(spec, dev_in, outs, ws, events=events[i], streams=streams)
+        call_ev[i][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
     value = cfg.T / (ms * 1e-3)
+    call_ms = [a.elapsed_time(b) for a, b in call_ev]
+    ms_median = float(np.median(call_ms))
 
     stage_ms = {}
     for si, name in enumerate(S.STAGES):
@@ -221,6 +248,7 @@ def main():
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "ms_per_call_median": round(ms_median, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.dtype == W.BF16 else "f32", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: SMoES MoE layer, T={cfg.T} tokens "

@@ -204,6 +204,12 @@ typedef struct smoes_layer {
     int reserved;       /* must be 0 */
 } smoes_layer;
 
+/* Side streams for smoes_moe_forward (caller-owned; see smoes_streams_create). */
+typedef struct smoes_streams {
+    void* side[2];   /* hipStream_t: [0] modality score + MI chain, [1] shared-expert GEMMs */
+    void* events[4]; /* hipEvent_t (timing disabled) used to fork and join them */
+} smoes_streams;
+
 typedef struct smoes_layer_io {
     /* inputs */
     const void* x;                 /* [T, d] act_dtype */
@@ -240,14 +246,20 @@ typedef struct smoes_layer_io {
      * smoes_events_create (entries may be NULL); events 2s and 2s + 1 are
      * recorded on the stream that runs stage s, before and after it. */
     void* const* stage_events;
+    /* optional side streams: NULL runs every stage on `stream`; otherwise the
+     * modality score and the MI chain run on side[0] and the shared experts'
+     * GEMMs on side[1], forked from and joined back into `stream` with the
+     * given events. One smoes_streams may serve consecutive calls; calls that
+     * overlap in time need one each. */
+    const smoes_streams* streams;
 } smoes_layer_io;
 
 /* Stages of smoes_moe_forward. ROUTE, PERMUTE, GEMM1, GEMM2 and COMBINE run
  * in this order on the caller's stream; MODALITY and then MI (after ROUTE)
- * run on one side stream, GEMM1_SHARED and GEMM2_SHARED on another (the
- * library keeps both per device); COMBINE waits for the shared GEMMs and the
- * caller's stream waits for both side streams before the call's work is
- * complete. */
+ * run on io->streams->side[0], GEMM1_SHARED and GEMM2_SHARED on side[1]
+ * (all on the caller's stream when io->streams is NULL); COMBINE waits for
+ * the shared GEMMs and the caller's stream waits for both side streams
+ * before the call's work is complete. */
 enum smoes_stage {
     SMOES_STAGE_ROUTE = 0,        /* router GEMM + softmax + top-k */
     SMOES_STAGE_MODALITY = 1,     /* statistics update (optional) + modality score */
@@ -317,6 +329,12 @@ int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void
 /* ------------------------------------------------------------------------ */
 /* Timing helpers for stage_events (hipEvent_t handles behind void*).        */
 /* ------------------------------------------------------------------------ */
+
+/* Two non-blocking streams of default priority and four untimed events on
+ * the current device, for smoes_layer_io.streams. Destroy with
+ * smoes_streams_destroy (after their work has completed). */
+int smoes_streams_create(smoes_streams* st);
+int smoes_streams_destroy(smoes_streams* st);
 
 int smoes_events_create(int n, void** events);
 int smoes_events_destroy(int n, void** events);

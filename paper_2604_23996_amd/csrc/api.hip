@@ -3,8 +3,6 @@
 // synchronises the host.
 #include <stdio.h>
 
-#include <mutex>
-
 #include "smoes.h"
 #include "common.h"
 #include "kernels.h"
@@ -66,40 +64,6 @@ size_t permute_ws(int64_t T, int E, int k) { return permute_workspace_bytes(T, E
 hipError_t record(void* const* ev, int idx, hipStream_t st) {
     if (ev == nullptr || ev[idx] == nullptr) return hipSuccess;
     return hipEventRecord(static_cast<hipEvent_t>(ev[idx]), st);
-}
-
-// Side streams of one device: the modality score and the MI chain run on
-// one, the shared expert's GEMMs on the other, beside the routing, the
-// permutation and the routed GEMMs on the caller's stream. Made on first use
-// (default priority, not blocking on the legacy default stream) and kept
-// until the process ends; one mutex orders the event records and waits of
-// concurrent calls.
-struct SideStream {
-    hipStream_t stream = nullptr;         // modality score, then the MI chain
-    hipStream_t shared_stream = nullptr;  // the shared expert's two GEMMs
-    hipEvent_t fork = nullptr, routed = nullptr, join = nullptr, shared_done = nullptr;
-};
-constexpr int kMaxDevices = 64;
-std::mutex g_side_mu;
-SideStream g_side[kMaxDevices];
-
-hipError_t side_stream_locked(SideStream** out) {
-    int dev = 0;
-    hipError_t err = hipGetDevice(&dev);
-    if (err != hipSuccess) return err;
-    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-    SideStream& ss = g_side[dev];
-    if (ss.shared_done == nullptr) {
-        if (ss.stream == nullptr && (err = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking)) != hipSuccess)
-            return err;
-        if (ss.shared_stream == nullptr &&
-            (err = hipStreamCreateWithFlags(&ss.shared_stream, hipStreamNonBlocking)) != hipSuccess)
-            return err;
-        for (hipEvent_t* e : {&ss.fork, &ss.routed, &ss.join, &ss.shared_done})
-            if (*e == nullptr && (err = hipEventCreateWithFlags(e, hipEventDisableTiming)) != hipSuccess) return err;
-    }
-    *out = &ss;
-    return hipSuccess;
 }
 
 }  // namespace
@@ -300,6 +264,12 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     if (L->shared_inter > 0 && (io->ws13 == nullptr || io->ws2 == nullptr)) return SMOES_ERR_ARG;
     if (io->sample_offsets == nullptr && L->n_batch != 1) return SMOES_ERR_SHAPE;
     if (workspace == nullptr || workspace_bytes < smoes_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
+    if (io->streams != nullptr) {
+        for (void* p : io->streams->side)
+            if (p == nullptr) return SMOES_ERR_ARG;
+        for (void* p : io->streams->events)
+            if (p == nullptr) return SMOES_ERR_ARG;
+    }
 
     hipStream_t s = as_stream(stream);
     LayerWs w;
@@ -338,24 +308,33 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     const WorkTables wt = experts_work_tables(a, w.experts);
 
     // Caller's stream s: route -> permute -> routed GEMM1 -> routed GEMM2 ->
-    // [shared GEMMs done] -> combine. Side stream b: modality -> [route done]
-    // -> MI. Side stream c: shared GEMM1 -> shared GEMM2 (they need x only).
-    // Both side streams start after everything queued on s before this call,
-    // and s waits for both before the call's work is complete.
-    std::lock_guard<std::mutex> lock(g_side_mu);
-    SideStream* ss = nullptr;
-    SMOES_TRY(side_stream_locked(&ss));
-    hipStream_t b = ss->stream, c = ss->shared_stream;
-    SMOES_TRY(hipEventRecord(ss->fork, s));
-    SMOES_TRY(hipStreamWaitEvent(c, ss->fork, 0));
-    SMOES_TRY(hipStreamWaitEvent(b, ss->fork, 0));
+    // [shared GEMMs done] -> combine. With caller-owned side streams
+    // (io->streams): b runs modality -> [route done] -> MI, c runs the
+    // shared GEMM1 -> GEMM2 (they need x only); both start after everything
+    // queued on s before this call, and s waits for both before the call's
+    // work is complete. Without them every stage runs on s, in the same
+    // order of dependencies.
+    const smoes_streams* sides = io->streams;
+    hipStream_t b = s, c = s;
+    hipEvent_t e_fork = nullptr, e_routed = nullptr, e_join = nullptr, e_shared = nullptr;
+    if (sides != nullptr) {
+        b = as_stream(sides->side[0]);
+        c = as_stream(sides->side[1]);
+        e_fork = static_cast<hipEvent_t>(sides->events[0]);
+        e_routed = static_cast<hipEvent_t>(sides->events[1]);
+        e_join = static_cast<hipEvent_t>(sides->events[2]);
+        e_shared = static_cast<hipEvent_t>(sides->events[3]);
+        SMOES_TRY(hipEventRecord(e_fork, s));
+        SMOES_TRY(hipStreamWaitEvent(c, e_fork, 0));
+        SMOES_TRY(hipStreamWaitEvent(b, e_fork, 0));
+    }
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED, c));
     SMOES_TRY(launch_experts_gemm1(a, w.experts, 2, c));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED + 1, c));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED, c));
     SMOES_TRY(launch_experts_gemm2(a, w.experts, 2, c));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED + 1, c));
-    SMOES_TRY(hipEventRecord(ss->shared_done, c));
+    if (sides != nullptr) SMOES_TRY(hipEventRecord(e_shared, c));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_MODALITY, b));
     SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
                               io->gauss_ssig, L->update_stats ? 1 : 0, L->beta, L->tau, L->var_floor,
@@ -366,13 +345,15 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
                            io->logit_bias, L->E, L->k, L->renorm_topk ? 1 : 0, logits, io->probs, io->topk_idx,
                            io->topk_w, w.route, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_ROUTE + 1, s));
-    SMOES_TRY(hipEventRecord(ss->routed, s));
-    SMOES_TRY(hipStreamWaitEvent(b, ss->routed, 0));
+    if (sides != nullptr) {
+        SMOES_TRY(hipEventRecord(e_routed, s));
+        SMOES_TRY(hipStreamWaitEvent(b, e_routed, 0));
+    }
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_MI, b));
     SMOES_TRY(launch_mi(io->probs, io->M, T, L->E, io->sample_offsets, L->n_batch, io->expert_to_bin,
                         L->n_bins, L->grad_scale, io->mi_per_sample, io->loss, io->dlogits, w.mi, b));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_MI + 1, b));
-    SMOES_TRY(hipEventRecord(ss->join, b));
+    if (sides != nullptr) SMOES_TRY(hipEventRecord(e_join, b));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE, s));
     SMOES_TRY(launch_permute(io->topk_idx, T, L->E, L->k, offsets, perm_token, perm_inv, w.permute, &wt, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE + 1, s));
@@ -382,11 +363,11 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2, s));
     SMOES_TRY(launch_experts_gemm2(a, w.experts, 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2 + 1, s));
-    SMOES_TRY(hipStreamWaitEvent(s, ss->shared_done, 0));
+    if (sides != nullptr) SMOES_TRY(hipStreamWaitEvent(s, e_shared, 0));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
     SMOES_TRY(launch_experts_combine(a, w.experts, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));
-    SMOES_TRY(hipStreamWaitEvent(s, ss->join, 0));
+    if (sides != nullptr) SMOES_TRY(hipStreamWaitEvent(s, e_join, 0));
 #undef SMOES_TRY
     return SMOES_OK;
 }
@@ -424,6 +405,42 @@ int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void
                                ? launch_split_wgate(static_cast<const float*>(src), desc->E, desc->d, dst, as_stream(stream))
                                : launch_pack_weights(src, batch, n, k, il, dst, as_stream(stream));
     return err == hipSuccess ? SMOES_OK : SMOES_ERR_HIP;
+}
+
+int smoes_streams_create(smoes_streams* st) {
+    if (st == nullptr) return SMOES_ERR_ARG;
+    *st = smoes_streams{};
+    for (void*& p : st->side) {
+        hipStream_t h;
+        if (hipStreamCreateWithFlags(&h, hipStreamNonBlocking) != hipSuccess) {
+            smoes_streams_destroy(st);
+            return SMOES_ERR_HIP;
+        }
+        p = h;
+    }
+    for (void*& p : st->events) {
+        hipEvent_t e;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+            smoes_streams_destroy(st);
+            return SMOES_ERR_HIP;
+        }
+        p = e;
+    }
+    return SMOES_OK;
+}
+
+int smoes_streams_destroy(smoes_streams* st) {
+    if (st == nullptr) return SMOES_ERR_ARG;
+    int rc = SMOES_OK;
+    for (void*& p : st->events) {
+        if (p != nullptr && hipEventDestroy(static_cast<hipEvent_t>(p)) != hipSuccess) rc = SMOES_ERR_HIP;
+        p = nullptr;
+    }
+    for (void*& p : st->side) {
+        if (p != nullptr && hipStreamDestroy(static_cast<hipStream_t>(p)) != hipSuccess) rc = SMOES_ERR_HIP;
+        p = nullptr;
+    }
+    return rc;
 }
 
 int smoes_events_create(int n, void** events) {

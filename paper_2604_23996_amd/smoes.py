@@ -54,7 +54,11 @@ _IO_FIELDS = ["x", "modality_id", "sample_offsets", "w_gate", "logit_bias", "exp
 
 
 class SmoesLayerIO(ctypes.Structure):
-    _fields_ = [(n, c_void) for n in _IO_FIELDS]
+    _fields_ = [(n, c_void) for n in _IO_FIELDS] + [("streams", c_void)]
+
+
+class SmoesStreams(ctypes.Structure):
+    _fields_ = [("side", c_void * 2), ("events", c_void * 4)]
 
 
 def lib() -> ctypes.CDLL:
@@ -97,6 +101,10 @@ def lib() -> ctypes.CDLL:
         L.smoes_packed_weight_bytes.argtypes = [ctypes.POINTER(SmoesLayer), c_int]
         L.smoes_pack_weights.restype = c_int
         L.smoes_pack_weights.argtypes = [ctypes.POINTER(SmoesLayer), c_int, c_void, c_void, c_void]
+        L.smoes_streams_create.restype = c_int
+        L.smoes_streams_create.argtypes = [ctypes.POINTER(SmoesStreams)]
+        L.smoes_streams_destroy.restype = c_int
+        L.smoes_streams_destroy.argtypes = [ctypes.POINTER(SmoesStreams)]
         L.smoes_events_create.restype = c_int
         L.smoes_events_create.argtypes = [c_int, ctypes.POINTER(c_void)]
         L.smoes_events_destroy.restype = c_int
@@ -285,6 +293,26 @@ def pack_weights(spec: LayerSpec, which: int, src: torch.Tensor) -> torch.Tensor
     return dst
 
 
+class Streams:
+    """Caller-owned side streams for moe_forward (smoes_streams_create)."""
+
+    def __init__(self):
+        self.st = SmoesStreams()
+        _check(lib().smoes_streams_create(ctypes.byref(self.st)), "smoes_streams_create")
+
+    def close(self):
+        if self.st is not None:
+            torch.cuda.synchronize()
+            lib().smoes_streams_destroy(ctypes.byref(self.st))
+            self.st = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 class Events:
     """2 * SMOES_N_STAGES HIP events for the forward's stage timing: events
     2s and 2s + 1 bracket stage s on the stream that runs it."""
@@ -337,7 +365,8 @@ def alloc_outputs(spec: LayerSpec, device, act_torch_dtype, want_logits=True, wa
 
 def moe_forward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
                 outputs: Dict[str, Optional[torch.Tensor]], workspace: torch.Tensor,
-                events: Optional[Events] = None) -> Dict[str, Optional[torch.Tensor]]:
+                events: Optional[Events] = None,
+                streams: Optional[Streams] = None) -> Dict[str, Optional[torch.Tensor]]:
     """One layer forward. `inputs` holds x, modality_id, sample_offsets, w_gate,
     logit_bias, expert_to_bin, w13, w2, ws13, ws2, gauss_n, gauss_smu, gauss_ssig
     (the Gaussian state is updated in place when spec.update_stats)."""
@@ -349,6 +378,7 @@ def moe_forward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
         t = inputs.get(name) if name in inputs else outputs.get(name)
         setattr(io, name, None if t is None else _p(t).value)
     io.stage_events = ctypes.cast(events.arr, c_void).value if events is not None else None
+    io.streams = ctypes.cast(ctypes.byref(streams.st), c_void).value if streams is not None else None
     _check(lib().smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), _p(workspace),
                                    workspace.numel(), _stream()), "smoes_moe_forward")
     return outputs

@@ -83,7 +83,8 @@ def pack_layer_weights(spec: S.LayerSpec, dev_in) -> None:
     torch.cuda.synchronize()
 
 
-def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None, packed=None):
+def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None, packed=None,
+                  streams=None):
     """The full layer through smoes_moe_forward. For layers that do not update
     their statistics in the call, the Gaussian state is first estimated from
     the batch by smoes_modality_score(update=1) from the zero state. bf16
@@ -109,7 +110,7 @@ def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=Non
     act = torch.bfloat16 if cfg.dtype == W.BF16 else torch.float32
     outs = S.alloc_outputs(spec, DEV, act)
     ws = torch.empty(S.workspace_bytes(spec), dtype=torch.uint8, device=DEV)
-    S.moe_forward(spec, dev_in, outs, ws, events=events)
+    S.moe_forward(spec, dev_in, outs, ws, events=events, streams=streams)
     torch.cuda.synchronize()
     return spec, dev_in, outs
 

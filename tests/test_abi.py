@@ -116,6 +116,11 @@ def test_layer_workspace_and_checks():
         setattr(io, name, 0x1000)
     need = S.workspace_bytes(_spec())
     assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, need - 1, None) == S.SMOES_ERR_WORKSPACE
+    # side streams given but incomplete
+    st = S.SmoesStreams()
+    io.streams = ctypes.cast(ctypes.byref(st), ctypes.c_void_p).value
+    assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, need, None) == S.SMOES_ERR_ARG
+    io.streams = None
     # shared experts declared but weights missing
     io.ws13 = None
     assert L.smoes_moe_forward(ctypes.byref(desc), ctypes.byref(io), FAKE, need, None) == S.SMOES_ERR_ARG
@@ -125,9 +130,10 @@ def test_layer_workspace_and_checks():
 
 
 def test_struct_layout_matches_header():
-    # smoes_layer: int64 + 8 int + 4 float + 4 int = 72 bytes; io: 27 pointers
+    # smoes_layer: int64 + 8 int + 4 float + 4 int = 72 bytes; io: 28 pointers
     assert ctypes.sizeof(S.SmoesLayer) == 72
-    assert ctypes.sizeof(S.SmoesLayerIO) == 27 * 8
+    assert ctypes.sizeof(S.SmoesLayerIO) == 28 * 8
+    assert ctypes.sizeof(S.SmoesStreams) == 6 * 8
     text = open(S.HEADER_PATH).read()
     import re
     lay = text[text.index("typedef struct smoes_layer {"):text.index("} smoes_layer;")]
@@ -137,7 +143,7 @@ def test_struct_layout_matches_header():
     io_block = text[text.index("typedef struct smoes_layer_io"):text.index("} smoes_layer_io;")]
     io_block = re.sub(r"/\*.*?\*/", "", io_block, flags=re.S)
     fields = re.findall(r"\*\s*(?:const\s*\*\s*)?([A-Za-z_0-9]+);", io_block)
-    assert fields == S._IO_FIELDS
+    assert fields == S._IO_FIELDS + ["streams"]
 
 
 def test_packed_weight_sizes_and_checks():

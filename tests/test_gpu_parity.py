@@ -457,22 +457,24 @@ def test_stage_events():
     ev.close()
 
 
-def test_side_stream_results_match_serial_order():
-    """The modality score and the MI chain run on the library's side stream;
-    several calls in a row on the caller's stream, with outputs read right
-    after each, give identical results (the join makes them complete)."""
+def test_side_streams_match_single_stream():
+    """With caller-owned side streams the modality score, the MI chain and the
+    shared GEMMs run beside the routed path; several calls in a row, with
+    outputs read right after each, give the oracle's results and are
+    bit-identical to the single-stream order (the joins make them complete)."""
     cfg = W.small_config(seed=9, d=256, E=16, k=4, inter=96, n_shared=1, n_bins=4,
                          samples=((300, 100), (50, 60)), dtype=W.BF16, update_stats=True)
     inp = W.make_layer_inputs(cfg)
     wg = W.aligned_router(inp, 0.5)  # well-conditioned MI
     ref = run_oracle_layer(inp, w_gate=wg)
-    first = None
-    for _ in range(3):
-        spec, _, outs = run_gpu_layer(inp, w_gate=wg)
-        assert np.all(np.abs(host(outs["M"]) - ref["M"]) <= 1e-5 * np.abs(ref["M"]) + 1e-6)
-        assert rel_err(host(outs["dlogits"]), ref["dlogits"]) <= 1e-5
-        if first is None:
-            first = {k: outs[k].clone() for k in ("M", "dlogits", "loss", "out")}
-        else:
-            for k, v in first.items():
-                assert torch.equal(outs[k], v), k
+    _, _, serial = run_gpu_layer(inp, w_gate=wg)
+    st = S.Streams()
+    try:
+        for _ in range(3):
+            spec, _, outs = run_gpu_layer(inp, w_gate=wg, streams=st)
+            assert np.all(np.abs(host(outs["M"]) - ref["M"]) <= 1e-5 * np.abs(ref["M"]) + 1e-6)
+            assert rel_err(host(outs["dlogits"]), ref["dlogits"]) <= 1e-5
+            for k in ("M", "dlogits", "loss", "mi_per_sample", "out", "probs", "perm_token"):
+                assert torch.equal(outs[k], serial[k]), k
+    finally:
+        st.close()
