@@ -39,10 +39,26 @@ Readings where the paper is silent (each also listed in the design notes):
   R12 an MI term with P(m, B_k) = 0 contributes 0, and a modality with zero
       total score mass in a sample has S-bar = 0 for every bin;
   R13 column 0 of the modality score is vision, column 1 is text.
+  R14 bin-level load balance (Eq. 16, one layer): the "tokens in bin B_k" are
+      the tokens routed to bin k (at least one of their top-k experts lies in
+      B_k), T_k of them; f_e = (tokens whose top-k holds e) / T_k and P_e is
+      the mean gate value of e over those tokens; a bin no token reaches adds
+      0. The top-k counts are constants for the gradient, as in the standard
+      load-balance loss.
+  R15 momentum-adaptive binning (Eq. 10-11): C_{m,e} counts the tokens of
+      hard label m whose top-k holds e; the EMA is kept in float64 as
+      beta * C_bar + (1 - beta) * C with both products rounded before the
+      sum; f_spec = C_bar_text / (C_bar_text + C_bar_vision), 1/2 when both
+      are 0; experts are sorted by ascending f_spec, ties to the lower expert
+      index, and cut into consecutive bins: bin(e) = rank(e) // N_B.
+  R16 MSI (Eq. 18-19) for one layer from the batch counts; a modality with
+      no tokens has all normalised shares 0, and an expert that no token of
+      either modality reaches counts as unspecialised (C_tilde_text = 1/2).
 
 Parity pins live in tests/test_oracle_pins.py; no part of this file is
-"parity unpinned" except the conventions R3-R5, R8, R11, R12 above, which fix
-choices the paper does not make (both sides implement the same stated choice).
+"parity unpinned" except the conventions R3-R5, R8, R11, R12, R14-R16 above,
+which fix choices the paper does not make (both sides implement the same
+stated choice; the formulas that follow each choice are pinned).
 """
 from __future__ import annotations
 
@@ -420,14 +436,107 @@ def layer_forward(x, modality_id, sample_offsets, w_gate, logit_bias, expert_to_
 
 
 # ----------------------------------------------------------------------------
-# Sec. 4.1 diagnostic: modality specialization index (test utility)
+# Sec. 3.3: momentum-adaptive binning (Eq. 10-11); Sec. 3.5: bin-level load
+# balance (Eq. 16); Sec. 4.1 diagnostic: modality specialization index
+# (Eq. 18-19)
 # ----------------------------------------------------------------------------
 
+def modality_expert_counts(topk_idx, modality_id, E: int) -> np.ndarray:
+    """C[m][e]: tokens of hard label m whose top-k holds expert e (Eq. 10)."""
+    idx = np.asarray(topk_idx, dtype=np.int64)
+    mid = np.asarray(modality_id, dtype=np.int64)
+    C = np.zeros((2, E), dtype=np.int64)
+    for m in (VISION, TEXT):
+        rows = idx[mid == m]
+        if rows.size:
+            C[m] = np.bincount(rows.ravel(), minlength=E)
+    return C
+
+
+def load_ema_update(C_bar, C, beta: float) -> np.ndarray:
+    """Eq. 10: C_bar <- beta * C_bar + (1 - beta) * C, float64 (R15)."""
+    b = float(np.float32(beta))
+    return b * np.asarray(C_bar, dtype=np.float64) + (1.0 - b) * np.asarray(C, dtype=np.float64)
+
+
+def f_spec(C_bar) -> np.ndarray:
+    """Eq. 11: text-bias score of each expert; 1/2 where no load (R15)."""
+    cb = np.asarray(C_bar, dtype=np.float64)
+    tot = cb[TEXT] + cb[VISION]
+    out = np.full(cb.shape[1], 0.5)
+    nz = tot > 0
+    out[nz] = cb[TEXT][nz] / tot[nz]
+    return out
+
+
+def adaptive_bins(fs, n_bins: int) -> np.ndarray:
+    """Sort experts by f_spec (ascending, ties to the lower index) and cut the
+    order into n_bins consecutive bins of N_B experts (Sec. 3.3, R15)."""
+    fs = np.asarray(fs, dtype=np.float64)
+    E = fs.shape[0]
+    NB = E // n_bins
+    order = np.argsort(fs, kind="stable")
+    e2b = np.empty(E, dtype=np.int32)
+    e2b[order] = np.arange(E) // NB
+    return e2b
+
+
+def bin_balance_terms(g, topk_idx, expert_to_bin, n_bins: int) -> Dict[str, np.ndarray]:
+    """Per-bin token sets and per-expert f_e, P_e of Eq. 16 (R14)."""
+    g = np.asarray(g, dtype=np.float64)
+    idx = np.asarray(topk_idx, dtype=np.int64)
+    e2b = np.asarray(expert_to_bin, dtype=np.int64)
+    T, E = g.shape
+    in_bin = np.zeros((T, n_bins), dtype=bool)
+    in_bin[np.repeat(np.arange(T), idx.shape[1]), e2b[idx.ravel()]] = True
+    Tk = in_bin.sum(axis=0)
+    counts = np.bincount(idx.ravel(), minlength=E).astype(np.float64)
+    f = np.zeros(E)
+    P = np.zeros(E)
+    for e in range(E):
+        k = e2b[e]
+        if Tk[k] > 0:
+            f[e] = counts[e] / Tk[k]
+            P[e] = g[in_bin[:, k], e].sum() / Tk[k]
+    return dict(in_bin=in_bin, Tk=Tk, counts=counts, f=f, P=P)
+
+
+def bin_balance_loss(g, topk_idx, expert_to_bin, n_bins: int) -> float:
+    """Eq. 16 for one layer: sum_k N_B sum_{e in B_k} f_e P_e (R14)."""
+    E = np.asarray(g).shape[1]
+    NB = E // n_bins
+    t = bin_balance_terms(g, topk_idx, expert_to_bin, n_bins)
+    return float(NB * np.sum(t["f"] * t["P"]))
+
+
+def bin_balance_grad_logits(g, topk_idx, expert_to_bin, n_bins: int, grad_scale: float = 1.0) -> np.ndarray:
+    """grad_scale * d L_bal / d z with the top-k sets fixed (R14): through
+    P_e only, dL/dg_je = N_B f_e / T_k for tokens j routed to bin k = bin(e),
+    then the softmax Jacobian dz = g (dg - sum_e g dg)."""
+    g = np.asarray(g, dtype=np.float64)
+    E = g.shape[1]
+    NB = E // n_bins
+    e2b = np.asarray(expert_to_bin, dtype=np.int64)
+    t = bin_balance_terms(g, topk_idx, expert_to_bin, n_bins)
+    coef = np.zeros(E)
+    for e in range(E):
+        k = e2b[e]
+        if t["Tk"][k] > 0:
+            coef[e] = NB * t["f"][e] / t["Tk"][k]
+    dg = t["in_bin"][:, e2b] * coef[None, :]
+    dz = g * (dg - np.sum(g * dg, axis=1, keepdims=True))
+    return grad_scale * dz
+
+
 def msi(counts_text, counts_vision) -> float:
-    """MSI for one layer (Eq. 18-19) from per-expert token counts per modality."""
+    """MSI for one layer (Eq. 18-19) from per-expert token counts per
+    modality (R16)."""
     ct = np.asarray(counts_text, dtype=np.float64)
     cv = np.asarray(counts_vision, dtype=np.float64)
-    nt = ct / ct.sum()
-    nv = cv / cv.sum()
-    c_text = nt / (nt + nv)
+    nt = ct / ct.sum() if ct.sum() > 0 else np.zeros_like(ct)
+    nv = cv / cv.sum() if cv.sum() > 0 else np.zeros_like(cv)
+    den = nt + nv
+    c_text = np.full(ct.shape, 0.5)
+    nz = den > 0
+    c_text[nz] = nt[nz] / den[nz]
     return float(np.mean(2.0 * np.abs(c_text - 0.5)))

@@ -496,3 +496,141 @@ def test_layer_forward_consistency_small():
 def test_msi_extremes():
     assert O.msi([5, 0, 3], [0, 7, 0]) == 1.0
     assert O.msi([2, 4, 6], [1, 2, 3]) == pytest.approx(0.0, abs=1e-15)
+
+
+# ----------------------------------------------------------------------------
+# Momentum-adaptive binning (Eq. 10-11), bin-level load balance (Eq. 16),
+# modality specialization index (Eq. 18-19)
+# ----------------------------------------------------------------------------
+
+def _routing(rng, T, E, k):
+    z = rng.standard_normal((T, E))
+    idx = np.argsort(-z, axis=1, kind="stable")[:, :k]
+    g = np.exp(z - z.max(axis=1, keepdims=True))
+    return z, g / g.sum(axis=1, keepdims=True), idx
+
+
+def test_modality_expert_counts_brute_force():
+    rng = np.random.default_rng(30)
+    T, E, k = 57, 9, 3
+    _, _, idx = _routing(rng, T, E, k)
+    mid = rng.integers(0, 2, size=T)
+    C = O.modality_expert_counts(idx, mid, E)
+    brute = np.zeros((2, E), dtype=np.int64)
+    for j in range(T):
+        for s in range(k):
+            brute[mid[j], idx[j, s]] += 1
+    assert np.array_equal(C, brute)
+    assert C.sum() == T * k
+
+
+def test_load_ema_closed_form():
+    """Eq. 10 from zero equals (1 - b) sum_s b^(t - s) C_s."""
+    rng = np.random.default_rng(31)
+    beta = 0.99
+    b = float(np.float32(beta))
+    Cs = [rng.integers(0, 500, size=(2, 12)) for _ in range(6)]
+    cb = np.zeros((2, 12))
+    for C in Cs:
+        cb = O.load_ema_update(cb, C, beta)
+    t = len(Cs)
+    closed = (1 - b) * sum(b ** (t - 1 - s) * Cs[s] for s in range(t))
+    assert np.allclose(cb, closed, rtol=1e-13, atol=0)
+
+
+def test_f_spec_cases():
+    cb = np.array([[1.0, 0.0, 0.0, 2.0], [3.0, 5.0, 0.0, 2.0]])  # rows: vision, text
+    assert np.array_equal(O.f_spec(cb), [0.75, 1.0, 0.5, 0.5])
+
+
+def test_adaptive_bins_hand_example_and_brute_force():
+    # f = [0.9, 0.1, 0.5, 0.1] -> ascending order, ties to the lower index: 1, 3, 2, 0
+    assert np.array_equal(O.adaptive_bins([0.9, 0.1, 0.5, 0.1], 2), [1, 0, 1, 0])
+    rng = np.random.default_rng(32)
+    for E, nb in ((16, 4), (12, 3), (64, 8)):
+        fs = np.round(rng.random(E), 1)  # many ties
+        e2b = O.adaptive_bins(fs, nb)
+        NB = E // nb
+        for e in range(E):
+            rank = sum(1 for q in range(E) if fs[q] < fs[e] or (fs[q] == fs[e] and q < e))
+            assert e2b[e] == rank // NB
+        assert np.array_equal(np.bincount(e2b, minlength=nb), np.full(nb, NB))
+
+
+def _bal_brute(g, idx, e2b, n_bins):
+    T, E = g.shape
+    NB = E // n_bins
+    total = 0.0
+    for kb in range(n_bins):
+        toks = [j for j in range(T) if any(e2b[e] == kb for e in idx[j])]
+        if not toks:
+            continue
+        for e in range(E):
+            if e2b[e] != kb:
+                continue
+            fe = sum(1 for j in toks if e in idx[j]) / len(toks)
+            pe = sum(g[j, e] for j in toks) / len(toks)
+            total += NB * fe * pe
+    return total
+
+
+def test_bin_balance_loss_brute_force():
+    rng = np.random.default_rng(33)
+    for T, E, k, nb in ((40, 8, 2, 4), (31, 12, 3, 3), (25, 6, 1, 2)):
+        _, g, idx = _routing(rng, T, E, k)
+        e2b = rng.permutation(np.arange(E) // (E // nb))
+        assert abs(O.bin_balance_loss(g, idx, e2b, nb) - _bal_brute(g, idx, e2b, nb)) < 1e-12
+
+
+def test_bin_balance_loss_closed_forms():
+    T, E, nb = 30, 4, 2
+    g = np.full((T, E), 0.25)
+    e2b = np.array([0, 0, 1, 1])
+    # every token takes experts 0 and 2: f_0 = f_2 = 1, so L = N_B (P_0 + P_2) = 2 * 0.5
+    idx = np.tile([0, 2], (T, 1))
+    assert abs(O.bin_balance_loss(g, idx, e2b, nb) - 1.0) < 1e-15
+    # one expert per bin, spread evenly: f_e = 1/N_B, P_e = 1/E -> L = n_bins N_B / E = 1
+    idx = np.array([[j % 2, 2 + (j // 2) % 2] for j in range(T - 2)])
+    assert abs(O.bin_balance_loss(g[:T - 2], idx, e2b, nb) - 1.0) < 1e-15
+    # a bin that no token reaches contributes nothing
+    idx = np.tile([0, 1], (T, 1))
+    assert abs(O.bin_balance_loss(g, idx, e2b, nb) - 2 * (1 * 0.25 + 1 * 0.25)) < 1e-15
+
+
+def test_bin_balance_grad_finite_differences():
+    """d L_bal / dz with the routed sets held fixed: central differences of
+    L as a function of z through the softmax only."""
+    rng = np.random.default_rng(34)
+    T, E, k, nb = 12, 8, 2, 4
+    z, g, idx = _routing(rng, T, E, k)
+    e2b = rng.permutation(np.arange(E) // (E // nb))
+    t = O.bin_balance_terms(g, idx, e2b, nb)
+
+    def loss_of(zz):
+        gg = np.exp(zz - zz.max(axis=1, keepdims=True))
+        gg /= gg.sum(axis=1, keepdims=True)
+        tot = 0.0
+        for e in range(E):
+            kb = e2b[e]
+            if t["Tk"][kb]:
+                tot += (E // nb) * t["f"][e] * gg[t["in_bin"][:, kb], e].sum() / t["Tk"][kb]
+        return tot
+
+    dz = O.bin_balance_grad_logits(g, idx, e2b, nb, grad_scale=0.5)
+    h = 1e-6
+    fd = np.zeros_like(z)
+    for j in range(T):
+        for e in range(E):
+            zp, zm = z.copy(), z.copy()
+            zp[j, e] += h
+            zm[j, e] -= h
+            fd[j, e] = (loss_of(zp) - loss_of(zm)) / (2 * h)
+    assert np.allclose(dz, 0.5 * fd, rtol=1e-6, atol=1e-10)
+    assert np.allclose(dz.sum(axis=1), 0.0, atol=1e-15)
+
+
+def test_msi_cases():
+    assert O.msi([5, 7, 0, 0], [0, 0, 3, 9]) == 1.0       # every expert serves one modality
+    assert O.msi([2, 4, 6], [1, 2, 3]) == 0.0             # identical distributions
+    assert abs(O.msi([3, 1], [1, 3]) - 0.5) < 1e-15       # shares 0.75 / 0.25 each way
+    assert abs(O.msi([3, 1, 0], [1, 3, 0]) - (0.5 + 0.5 + 0.0) / 3) < 1e-15  # idle expert: unspecialised
