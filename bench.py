@@ -262,6 +262,40 @@ def main():
         "roofline": roof,
         "stages": stages,
     }
+    # Momentum-adaptive binning + bin-level balance loss (+ gradient, added onto
+    # the MI gradient) + MSI on this step's routing: timed on its own, not part
+    # of the layer step above.
+    T, E = cfg.T, cfg.E
+    e2b_next = torch.empty(E, dtype=torch.int32, device=dev)
+    load_ema = torch.zeros((2, E), dtype=torch.float64, device=dev)
+    nws = int(S.lib().smoes_binning_workspace_size(T, E, cfg.n_bins))
+    bws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    bin_out = dict(counts=torch.empty((2, E), dtype=torch.int32, device=dev),
+                   f_spec=torch.empty(E, dtype=torch.float64, device=dev),
+                   loss=torch.empty(1, dtype=torch.float32, device=dev),
+                   msi=torch.empty(1, dtype=torch.float32, device=dev))
+
+    def binning_call():
+        S._check(S.lib().smoes_binning(S._p(outs["probs"]), S._p(outs["topk_idx"]), S._p(dev_in["modality_id"]),
+                                       T, E, cfg.k, S._p(dev_in["expert_to_bin"]), cfg.n_bins, cfg.beta,
+                                       S._p(load_ema), S._p(bin_out["counts"]), S._p(bin_out["f_spec"]),
+                                       S._p(e2b_next), 1e-3, S._p(bin_out["loss"]), S._p(outs["dlogits"]), 1,
+                                       S._p(bin_out["msi"]), S._p(bws), bws.numel(), S._stream()), "smoes_binning")
+
+    for _ in range(3):
+        binning_call()
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record()
+    for _ in range(args.steps):
+        binning_call()
+    b1.record()
+    torch.cuda.synchronize()
+    bin_ms = b0.elapsed_time(b1) / args.steps
+    bin_bytes = T * (2 * 4 * E + 4 * cfg.k + 1)  # probs read, dlogits read+write, top-k, labels
+    line["extra"] = {"binning": {"what": "momentum-adaptive bins + bin-level load balance loss and gradient "
+                                         "(added onto dlogits) + MSI, one layer, this step's routing",
+                                 "ms": round(bin_ms, 5), "gbs": round(bin_bytes / (bin_ms * 1e-3) / 1e9, 1),
+                                 "frac_hbm": round(bin_bytes / (bin_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}}
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on {args.cpu_samples} samples")
         line["cpu_baseline"] = cpu_baseline(cfg, inp, min(args.cpu_samples, cfg.n_batch))

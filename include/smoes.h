@@ -10,6 +10,9 @@
  *   smoes_modality_score   EMA-Welford statistics + Gaussian score   (Sec. 3.2.2, Eq. 5-9)
  *   smoes_mi_loss          inter-bin MI, its loss and d loss / d logits (Sec. 3.3-3.4, Eq. 12-15)
  *   smoes_permute          expert-contiguous token order (+ optional row gather)
+ *   smoes_binning          momentum-adaptive bins, bin-level load balance loss
+ *                          (+ d loss / d logits) and MSI (Sec. 3.3, 3.5, 4.1;
+ *                          Eq. 10-11, 16, 18-19)
  *   smoes_moe_forward      all of the above + grouped SwiGLU experts, shared
  *                          experts and the weighted combine
  *
@@ -154,6 +157,50 @@ int smoes_mi_loss(const float* probs, const float* M, int64_t T, int E,
                   const int32_t* expert_to_bin, int n_bins, float grad_scale,
                   float* mi_per_sample, float* loss, float* dlogits,
                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Momentum-adaptive binning (Sec. 3.3, Eq. 10-11), bin-level load balance   */
+/* (Sec. 3.5, Eq. 16) and modality specialization index (Sec. 4.1, Eq. 18-19)*/
+/* ------------------------------------------------------------------------ */
+
+size_t smoes_binning_workspace_size(int64_t T, int E, int n_bins);
+
+/*
+ * From one batch's routing:
+ * probs         [T, E] float32 gate values (full softmax), topk_idx [T, k] int32,
+ * modality_id   [T] uint8 hard labels (0 vision, 1 text),
+ * expert_to_bin [E] int32: the bins the batch was routed and scored with.
+ * Counts C[m][e] = tokens of label m whose top-k holds e.
+ *
+ * load_ema [2][E] float64 (row 0 vision, row 1 text), in/out, or NULL: the
+ *   expert-load EMA of Eq. 10, C_bar = beta * C_bar + (1 - beta) * C (both
+ *   products rounded before the sum); NULL scores this batch's counts only.
+ * Outputs, each optional (NULL = not written):
+ *   counts [2][E] int32: C of this batch;
+ *   f_spec [E] float64: Eq. 11, C_bar_text / (C_bar_text + C_bar_vision), 1/2
+ *     for an expert without load;
+ *   expert_to_bin_next [E] int32: experts sorted by ascending f_spec (ties to
+ *     the lower index) cut into n_bins consecutive bins of E / n_bins: the
+ *     adaptive bins for the next batch (must not alias expert_to_bin);
+ *   bal_loss [1] float32: Eq. 16 for this layer, sum over bins k of
+ *     N_B sum_{e in B_k} f_e P_e, where the tokens of bin k are those with at
+ *     least one top-k expert in it (T_k of them), f_e = (tokens whose top-k
+ *     holds e) / T_k and P_e = mean gate of e over them;
+ *   dlogits [T, E] float32: grad_scale * d bal_loss / d logits with the top-k
+ *     sets held fixed; written, or added to the array when accumulate = 1
+ *     (e.g. onto the MI gradient);
+ *   msi [1] float32: Eq. 18-19 of this batch's counts (an expert no token
+ *     reaches counts as unspecialised).
+ * Sums run in a fixed order: results are bit-reproducible. T = 0 still
+ * updates load_ema (with zero counts) and the bins.
+ * Shapes: 1 <= E <= SMOES_E_MAX, 1 <= n_bins <= SMOES_BINS_MAX,
+ * E % n_bins == 0, 1 <= k <= min(E, SMOES_K_MAX); 0 <= beta <= 1.
+ */
+int smoes_binning(const float* probs, const int32_t* topk_idx, const uint8_t* modality_id, int64_t T, int E,
+                  int k, const int32_t* expert_to_bin, int n_bins, float beta, double* load_ema,
+                  int32_t* counts, double* f_spec, int32_t* expert_to_bin_next, float grad_scale,
+                  float* bal_loss, float* dlogits, int accumulate, float* msi, void* workspace,
+                  size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Expert-contiguous permutation of the routed (token, slot) pairs.          */

@@ -151,6 +151,32 @@ int smoes_mi_loss(const float* probs, const float* M, int64_t T, int E, const in
                                 as_stream(stream)));
 }
 
+size_t smoes_binning_workspace_size(int64_t T, int E, int n_bins) {
+    if (check_mi_shape(T, E, 1, n_bins) != SMOES_OK) return 0;
+    return binning_workspace_bytes(T, E, n_bins) + 2 * kAlign;
+}
+
+int smoes_binning(const float* probs, const int32_t* topk_idx, const uint8_t* modality_id, int64_t T, int E,
+                  int k, const int32_t* expert_to_bin, int n_bins, float beta, double* load_ema,
+                  int32_t* counts, double* f_spec, int32_t* expert_to_bin_next, float grad_scale,
+                  float* bal_loss, float* dlogits, int accumulate, float* msi, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+    int st = check_mi_shape(T, E, 1, n_bins);
+    if (st != SMOES_OK) return st;
+    if (k < 1 || k > E || k > SMOES_K_MAX) return SMOES_ERR_SHAPE;
+    if (!(beta >= 0.0f && beta <= 1.0f) || (accumulate != 0 && accumulate != 1)) return SMOES_ERR_ARG;
+    if (expert_to_bin == nullptr) return SMOES_ERR_ARG;
+    if (T > 0 && (probs == nullptr || topk_idx == nullptr || modality_id == nullptr)) return SMOES_ERR_ARG;
+    if (expert_to_bin_next != nullptr && expert_to_bin_next == expert_to_bin) return SMOES_ERR_ARG;
+    if (workspace == nullptr || workspace_bytes < smoes_binning_workspace_size(T, E, n_bins))
+        return SMOES_ERR_WORKSPACE;
+    Carver c(workspace);
+    void* ws = c.take(binning_workspace_bytes(T, E, n_bins));
+    return hip_status(launch_binning(probs, topk_idx, modality_id, T, E, k, expert_to_bin, n_bins, beta, load_ema,
+                                     counts, f_spec, expert_to_bin_next, grad_scale, bal_loss, dlogits, accumulate,
+                                     msi, ws, as_stream(stream)));
+}
+
 size_t smoes_permute_workspace_size(int64_t T, int E, int k) { return permute_ws(T, E, k); }
 
 int smoes_permute(const int32_t* topk_idx, int64_t T, int E, int k, int32_t* expert_offsets,

@@ -1,0 +1,304 @@
+// Momentum-adaptive binning (Sec. 3.3, Eq. 10-11), the bin-level load
+// balance loss with its logit gradient (Sec. 3.5, Eq. 16) and the modality
+// specialization index (Sec. 4.1, Eq. 18-19) of one layer, from one batch's
+// routing.
+//
+//   bal_partial : per 256-token chunk: per token the bins its top-k reaches
+//                 (kept for the gradient), counts C[m][e] of hard label m with
+//                 e in the token's top-k and tokens routed to each bin (LDS
+//                 integer adds), and per expert the gate mass over the tokens
+//                 routed to its bin (fp64, fixed order).
+//   bal_finalize: one block; sums the chunk partials in chunk order, then
+//                 L_bal = sum_e N_B (n_e / T_k)(S_e / T_k), the gradient
+//                 coefficients N_B n_e / T_k^2, the EMA of the expert loads
+//                 (fp64, products rounded before the sum), f_spec, the stable
+//                 ascending rank of f_spec -> next bin map, and MSI.
+//   bal_grad    : one wave per token: dz = scale * g * (dg - sum_e g dg) with
+//                 dg_e = coef_e for experts whose bin the token was routed to
+//                 (the token's bin mask from bal_partial).
+// Readings (the paper leaves them open): "tokens in bin B_k" are the tokens
+// routed to bin k; f_e = n_e / T_k, P_e = mean gate of e over them; the top-k
+// counts are constants for the gradient; f_spec = 1/2 for an expert with no
+// load; MSI counts an expert no token reaches as unspecialised.
+#include "common.h"
+#include "kernels.h"
+
+namespace smoes {
+
+namespace {
+
+constexpr int kBalChunk = 256;    // tokens per partial block
+constexpr int kBalThreads = 256;  // 4 waves
+constexpr int kBalWaves = kBalThreads / kWave;
+
+struct BalWs {
+    int32_t* cnt;    // [nchunk][2][E]
+    int32_t* tk;     // [nchunk][n_bins]
+    double* mass;    // [nchunk][E]
+    double* coef;    // [E]
+    uint64_t* mask;  // [T]: bins each token's top-k reaches
+};
+
+BalWs carve(void* ws, int64_t nchunk, int E, int n_bins) {
+    char* p = static_cast<char*>(ws);
+    BalWs w;
+    w.cnt = reinterpret_cast<int32_t*>(p);
+    p += align_up(sizeof(int32_t) * nchunk * 2 * E, 256);
+    w.tk = reinterpret_cast<int32_t*>(p);
+    p += align_up(sizeof(int32_t) * nchunk * n_bins, 256);
+    w.mass = reinterpret_cast<double*>(p);
+    p += align_up(sizeof(double) * nchunk * E, 256);
+    w.coef = reinterpret_cast<double*>(p);
+    p += align_up(sizeof(double) * E, 256);
+    w.mask = reinterpret_cast<uint64_t*>(p);
+    return w;
+}
+
+// Phase 1, one thread per token of the chunk: its top-k row (k loads in
+// flight), the bins it reaches as a bit mask (n_bins <= 64, bin map in LDS),
+// counts by label and expert and tokens per bin (LDS integer adds). Phase 2,
+// one wave per token with lanes over experts: gate mass of each expert over
+// the tokens routed to its bin (fp64, fixed order).
+__global__ void __launch_bounds__(kBalThreads)
+bal_partial_kernel(const float* __restrict__ probs, const int32_t* __restrict__ idx,
+                   const uint8_t* __restrict__ mid, int64_t T, int E, int k, const int32_t* __restrict__ e2b,
+                   int n_bins, int32_t* __restrict__ cnt_out, int32_t* __restrict__ tk_out,
+                   double* __restrict__ mass_out, uint64_t* __restrict__ mask_out) {
+    __shared__ int32_t cnt[2][256];
+    __shared__ int32_t tk[64];
+    __shared__ int32_t bin_s[256];
+    __shared__ uint64_t mask_s[kBalChunk];
+    __shared__ double mass[kBalWaves][256];
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    for (int i = threadIdx.x; i < 2 * 256; i += kBalThreads) cnt[i / 256][i % 256] = 0;
+    if (threadIdx.x < 64) tk[threadIdx.x] = 0;
+    for (int e = threadIdx.x; e < E; e += kBalThreads) bin_s[e] = e2b[e];
+    __syncthreads();
+    const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kBalChunk;
+    const int n = static_cast<int>(T - j0 < kBalChunk ? T - j0 : kBalChunk);
+    {
+        const int r = threadIdx.x;
+        uint64_t m = 0;
+        if (r < n) {
+            const int64_t j = j0 + r;
+            int ex[SMOES_K_MAX_DEV];
+#pragma unroll
+            for (int s = 0; s < SMOES_K_MAX_DEV; ++s) ex[s] = s < k ? idx[j * k + s] : 0;
+            const int lab = mid[j] ? 1 : 0;
+#pragma unroll
+            for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
+                if (s < k) {
+                    m |= 1ull << bin_s[ex[s]];
+                    atomicAdd(&cnt[lab][ex[s]], 1);
+                }
+            }
+            mask_out[j] = m;
+        }
+        mask_s[r] = m;
+        for (int b = 0; b < n_bins; ++b)
+            if ((m >> b) & 1ull) atomicAdd(&tk[b], 1);
+    }
+    __syncthreads();
+    int bin_of[4];
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane + q * kWave;
+        bin_of[q] = e < E ? bin_s[e] : 0;
+    }
+#pragma unroll 4
+    for (int r = wave; r < n; r += kBalWaves) {
+        const uint64_t bins = mask_s[r];
+        const float* row = probs + (j0 + r) * E;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + q * kWave;
+            if (e < E && ((bins >> bin_of[q]) & 1ull)) acc[q] += static_cast<double>(row[e]);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) mass[wave][lane + q * kWave] = acc[q];
+    __syncthreads();
+    int32_t* co = cnt_out + static_cast<int64_t>(blockIdx.x) * 2 * E;
+    for (int i = threadIdx.x; i < 2 * E; i += kBalThreads) co[i] = cnt[i / E][i % E];
+    if (threadIdx.x < n_bins) tk_out[static_cast<int64_t>(blockIdx.x) * n_bins + threadIdx.x] = tk[threadIdx.x];
+    for (int e = threadIdx.x; e < E; e += kBalThreads) {
+        double sum = 0.0;
+        for (int w = 0; w < kBalWaves; ++w) sum += mass[w][e];  // wave order
+        mass_out[static_cast<int64_t>(blockIdx.x) * E + e] = sum;
+    }
+}
+
+// Fixed-order sum of one double per thread over the block (256 threads).
+__device__ __forceinline__ double block_sum_f64(double v, double* sh) {
+    sh[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = kBalThreads / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+        __syncthreads();
+    }
+    const double r = sh[0];
+    __syncthreads();
+    return r;
+}
+
+__global__ void __launch_bounds__(kBalThreads)
+bal_finalize_kernel(int64_t nchunk, int E, int n_bins, const int32_t* __restrict__ cnt_in,
+                    const int32_t* __restrict__ tk_in, const double* __restrict__ mass_in, double beta,
+                    double* __restrict__ load_ema, int32_t* __restrict__ counts, double* __restrict__ fspec_out,
+                    int32_t* __restrict__ e2b_next, const int32_t* __restrict__ e2b, float* __restrict__ bal_loss,
+                    float* __restrict__ msi_out, double* __restrict__ coef) {
+    __shared__ int32_t tk[64];
+    __shared__ double fs[256];
+    __shared__ double red[kBalThreads];
+    const int e = threadIdx.x;  // E <= 256 = blockDim
+    const int NB = E / n_bins;
+    if (e < n_bins) {
+        int32_t s = 0;
+        for (int64_t c = 0; c < nchunk; ++c) s += tk_in[c * n_bins + e];
+        tk[e] = s;
+    }
+    int32_t cv = 0, ct = 0;
+    double S = 0.0;
+    if (e < E) {
+        for (int64_t c = 0; c < nchunk; ++c) {  // chunk order
+            cv += cnt_in[c * 2 * E + e];
+            ct += cnt_in[c * 2 * E + E + e];
+            S += mass_in[c * E + e];
+        }
+    }
+    __syncthreads();
+    // Eq. 16 and its gradient coefficients
+    double term = 0.0;
+    if (e < E) {
+        const int32_t Tk = tk[e2b[e]];
+        const double n_e = static_cast<double>(cv) + static_cast<double>(ct);
+        double c = 0.0;
+        if (Tk > 0) {
+            const double t = static_cast<double>(Tk);
+            term = NB * (n_e / t) * (S / t);
+            c = NB * (n_e / t) / t;
+        }
+        coef[e] = c;
+        if (counts != nullptr) {
+            counts[e] = cv;
+            counts[E + e] = ct;
+        }
+    }
+    const double L = block_sum_f64(term, red);
+    if (e == 0 && bal_loss != nullptr) bal_loss[0] = static_cast<float>(L);
+    // Eq. 10: EMA of the expert loads (rows: vision, text), products rounded before the sum
+    double f = 0.5;
+    if (e < E) {
+        double lv = cv, lt = ct;
+        if (load_ema != nullptr) {
+            const double a = 1.0 - beta;
+            lv = __dadd_rn(__dmul_rn(beta, load_ema[e]), __dmul_rn(a, static_cast<double>(cv)));
+            lt = __dadd_rn(__dmul_rn(beta, load_ema[E + e]), __dmul_rn(a, static_cast<double>(ct)));
+            load_ema[e] = lv;
+            load_ema[E + e] = lt;
+        }
+        const double tot = __dadd_rn(lt, lv);
+        if (tot > 0.0) f = __ddiv_rn(lt, tot);  // Eq. 11
+        fs[e] = f;
+        if (fspec_out != nullptr) fspec_out[e] = f;
+    }
+    __syncthreads();
+    // stable ascending rank -> consecutive bins of N_B
+    if (e < E && e2b_next != nullptr) {
+        int rank = 0;
+        for (int q = 0; q < E; ++q) rank += (fs[q] < f || (fs[q] == f && q < e)) ? 1 : 0;
+        e2b_next[e] = rank / NB;
+    }
+    // Eq. 18-19 on this batch's counts
+    const double tot_v = block_sum_f64(e < E ? static_cast<double>(cv) : 0.0, red);
+    const double tot_t = block_sum_f64(e < E ? static_cast<double>(ct) : 0.0, red);
+    double dev = 0.0;
+    if (e < E) {
+        const double nv = tot_v > 0.0 ? cv / tot_v : 0.0;
+        const double nt = tot_t > 0.0 ? ct / tot_t : 0.0;
+        const double den = nt + nv;
+        const double c_text = den > 0.0 ? nt / den : 0.5;
+        dev = 2.0 * fabs(c_text - 0.5);
+    }
+    const double msi = block_sum_f64(dev, red) / E;
+    if (e == 0 && msi_out != nullptr) msi_out[0] = static_cast<float>(msi);
+}
+
+__global__ void __launch_bounds__(kBalThreads)
+bal_grad_kernel(const float* __restrict__ probs, const uint64_t* __restrict__ mask, int64_t T, int E,
+                const int32_t* __restrict__ e2b, const double* __restrict__ coef, double scale, int accumulate,
+                float* __restrict__ dlogits) {
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    double cf[4];
+    int bin_of[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane + q * kWave;
+        cf[q] = e < E ? coef[e] : 0.0;
+        bin_of[q] = e < E ? e2b[e] : 0;
+    }
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBalWaves;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBalWaves + wave; j < T; j += stride) {
+        const uint64_t bins = mask[j];
+        double g[4], dg[4], part = 0.0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + q * kWave;
+            g[q] = e < E ? static_cast<double>(probs[j * E + e]) : 0.0;
+            dg[q] = (e < E && ((bins >> bin_of[q]) & 1ull)) ? cf[q] : 0.0;
+            part += g[q] * dg[q];
+        }
+        const double s = wave_sum_u(part);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + q * kWave;
+            if (e < E) {
+                float v = static_cast<float>(scale * g[q] * (dg[q] - s));
+                if (accumulate) v += dlogits[j * E + e];
+                dlogits[j * E + e] = v;
+            }
+        }
+    }
+}
+
+}  // namespace
+
+size_t binning_workspace_bytes(int64_t T, int E, int n_bins) {
+    const int64_t nchunk = ceil_div(T, kBalChunk) > 0 ? ceil_div(T, kBalChunk) : 1;
+    return align_up(sizeof(int32_t) * nchunk * 2 * E, 256) + align_up(sizeof(int32_t) * nchunk * n_bins, 256) +
+           align_up(sizeof(double) * nchunk * E, 256) + align_up(sizeof(double) * E, 256) +
+           align_up(sizeof(uint64_t) * (T > 0 ? T : 1), 256);
+}
+
+hipError_t launch_binning(const float* probs, const int32_t* topk_idx, const uint8_t* modality_id, int64_t T,
+                          int E, int k, const int32_t* expert_to_bin, int n_bins, float beta, double* load_ema,
+                          int32_t* counts, double* f_spec, int32_t* expert_to_bin_next, float grad_scale,
+                          float* bal_loss, float* dlogits, int accumulate, float* msi, void* ws,
+                          hipStream_t stream) {
+    const int64_t nchunk = ceil_div(T, kBalChunk);
+    BalWs w = carve(ws, nchunk > 0 ? nchunk : 1, E, n_bins);
+    hipError_t err;
+    if (nchunk > 0) {
+        hipLaunchKernelGGL(bal_partial_kernel, dim3(static_cast<unsigned>(nchunk)), dim3(kBalThreads), 0, stream,
+                           probs, topk_idx, modality_id, T, E, k, expert_to_bin, n_bins, w.cnt, w.tk, w.mass,
+                           w.mask);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    const double b = static_cast<double>(beta);
+    hipLaunchKernelGGL(bal_finalize_kernel, dim3(1), dim3(kBalThreads), 0, stream, nchunk, E, n_bins, w.cnt,
+                       w.tk, w.mass, b, load_ema, counts, f_spec, expert_to_bin_next, expert_to_bin, bal_loss,
+                       msi, w.coef);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if (dlogits != nullptr && T > 0) {
+        int64_t blocks = ceil_div(T, kBalWaves);
+        if (blocks > 4096) blocks = 4096;
+        hipLaunchKernelGGL(bal_grad_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kBalThreads), 0, stream,
+                           probs, w.mask, T, E, expert_to_bin, w.coef, static_cast<double>(grad_scale),
+                           accumulate, dlogits);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    return hipSuccess;
+}
+
+}  // namespace smoes

@@ -79,8 +79,15 @@ template <class T, class Op>
 __device__ __forceinline__ T row_allreduce(T v, Op op) {
     auto mv = [](T x, auto ctrl) {
         constexpr int C = decltype(ctrl)::value;
-        if constexpr (sizeof(T) == 4 && !__is_same(T, int)) return __int_as_float(dpp_mov<C>(__float_as_int(x)));
-        else return static_cast<T>(dpp_mov<C>(static_cast<int>(x)));
+        if constexpr (__is_same(T, double)) {
+            const long long b = __double_as_longlong(x);
+            const int lo = dpp_mov<C>(static_cast<int>(b)), hi = dpp_mov<C>(static_cast<int>(b >> 32));
+            return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+        } else if constexpr (sizeof(T) == 4 && !__is_same(T, int)) {
+            return __int_as_float(dpp_mov<C>(__float_as_int(x)));
+        } else {
+            return static_cast<T>(dpp_mov<C>(static_cast<int>(x)));
+        }
     };
     v = op(v, mv(v, std::integral_constant<int, 0xB1>{}));   // quad_perm [1,0,3,2]
     v = op(v, mv(v, std::integral_constant<int, 0x4E>{}));   // quad_perm [2,3,0,1]
@@ -101,6 +108,16 @@ __device__ __forceinline__ float wave_sum_u(float v) {
     const float a = __int_as_float(__builtin_amdgcn_readlane(i, 0)), b = __int_as_float(__builtin_amdgcn_readlane(i, 16));
     const float c = __int_as_float(__builtin_amdgcn_readlane(i, 32)), d = __int_as_float(__builtin_amdgcn_readlane(i, 48));
     return (a + b) + (c + d);
+}
+__device__ __forceinline__ double wave_sum_u(double v) {
+    v = row_allreduce(v, [](double a, double b) { return a + b; });
+    auto rl = [](double x, int l) {
+        const long long b = __double_as_longlong(x);
+        const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), l);
+        const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), l);
+        return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+    };
+    return (rl(v, 0) + rl(v, 16)) + (rl(v, 32) + rl(v, 48));
 }
 __device__ __forceinline__ int wave_min_u(int v) {
     v = row_allreduce(v, [](int a, int b) { return a < b ? a : b; });

@@ -81,4 +81,12 @@ int64_t packed_weight_elems(int batch, int n, int k, int interleave);
 hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, void* dst,
                                hipStream_t stream);
 
+// Momentum-adaptive binning, bin-level load balance loss (+ logit gradient) and MSI
+size_t binning_workspace_bytes(int64_t T, int E, int n_bins);
+hipError_t launch_binning(const float* probs, const int32_t* topk_idx, const uint8_t* modality_id, int64_t T,
+                          int E, int k, const int32_t* expert_to_bin, int n_bins, float beta, double* load_ema,
+                          int32_t* counts, double* f_spec, int32_t* expert_to_bin_next, float grad_scale,
+                          float* bal_loss, float* dlogits, int accumulate, float* msi, void* ws,
+                          hipStream_t stream);
+
 }  // namespace smoes

@@ -101,6 +101,12 @@ def lib() -> ctypes.CDLL:
         L.smoes_packed_weight_bytes.argtypes = [ctypes.POINTER(SmoesLayer), c_int]
         L.smoes_pack_weights.restype = c_int
         L.smoes_pack_weights.argtypes = [ctypes.POINTER(SmoesLayer), c_int, c_void, c_void, c_void]
+        L.smoes_binning_workspace_size.restype = c_size
+        L.smoes_binning_workspace_size.argtypes = [c_i64, c_int, c_int]
+        L.smoes_binning.restype = c_int
+        L.smoes_binning.argtypes = [c_void, c_void, c_void, c_i64, c_int, c_int, c_void, c_int, c_float, c_void,
+                                    c_void, c_void, c_void, c_float, c_void, c_void, c_int, c_void, c_void,
+                                    c_size, c_void]
         L.smoes_streams_create.restype = c_int
         L.smoes_streams_create.argtypes = [ctypes.POINTER(SmoesStreams)]
         L.smoes_streams_destroy.restype = c_int
@@ -206,6 +212,36 @@ def mi_loss(probs: torch.Tensor, M: torch.Tensor, sample_offsets: Optional[torch
                                n_bins, grad_scale, _p(mi), _p(loss), _p(dl), _p(ws), nbytes, _stream()),
            "smoes_mi_loss")
     return mi, loss, dl
+
+
+def binning(probs: torch.Tensor, topk_idx: torch.Tensor, modality_id: torch.Tensor, expert_to_bin: torch.Tensor,
+            n_bins: int, beta: float = 0.99, load_ema: Optional[torch.Tensor] = None, grad_scale: float = 1.0,
+            dlogits: Optional[torch.Tensor] = None, accumulate: bool = False,
+            want_grad: bool = True) -> Dict[str, torch.Tensor]:
+    """smoes_binning: adaptive bins for the next batch, the bin-level load
+    balance loss (+ its logit gradient) and MSI. load_ema ([2, E] float64) is
+    updated in place when given; dlogits is written (or added to) when given,
+    else a new array is returned when want_grad."""
+    T, E = probs.shape
+    k = topk_idx.shape[1]
+    dev = probs.device
+    out = {
+        "counts": torch.empty((2, E), dtype=torch.int32, device=dev),
+        "f_spec": torch.empty(E, dtype=torch.float64, device=dev),
+        "expert_to_bin_next": torch.empty(E, dtype=torch.int32, device=dev),
+        "bal_loss": torch.empty(1, dtype=torch.float32, device=dev),
+        "msi": torch.empty(1, dtype=torch.float32, device=dev),
+    }
+    if dlogits is None and want_grad:
+        dlogits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    out["dlogits"] = dlogits
+    nws = int(lib().smoes_binning_workspace_size(T, E, n_bins))
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    _check(lib().smoes_binning(_p(probs), _p(topk_idx), _p(modality_id), T, E, k, _p(expert_to_bin), n_bins,
+                               beta, _p(load_ema), _p(out["counts"]), _p(out["f_spec"]),
+                               _p(out["expert_to_bin_next"]), grad_scale, _p(out["bal_loss"]), _p(dlogits),
+                               int(accumulate), _p(out["msi"]), _p(ws), ws.numel(), _stream()), "smoes_binning")
+    return out
 
 
 def permute(topk_idx: torch.Tensor, E: int, x: Optional[torch.Tensor] = None):
