@@ -19,6 +19,10 @@ MoE-VLMs" (SMoES):
   * MoE layer  expert-contiguous permutation, SwiGLU experts, shared experts,
                weighted combine (the backbones of the supplementary backbone
                table: DeepSeekMoE with 2 shared experts, gated-SiLU FFNs)
+  * Sec. 3.3 / 3.5 / 4.1  momentum-adaptive binning (Eq. 10-11), bin-level
+               load balance (Eq. 16) and its logit gradient, MSI (Eq. 18-19)
+  * Sec. 3.2.1 attention-accumulated score: one-hot start (Eq. 2), head-averaged
+               attention aggregation (Eq. 3), norm-weighted residual mix (Eq. 4)
 
 Readings where the paper is silent (each also listed in the design notes):
   R1  logarithms are natural (MI in nats);
@@ -54,6 +58,15 @@ Readings where the paper is silent (each also listed in the design notes):
   R16 MSI (Eq. 18-19) for one layer from the batch counts; a modality with
       no tokens has all normalised shares 0, and an expert that no token of
       either modality reaches counts as unspecialised (C_tilde_text = 1/2).
+  R17 Attn in Eq. 3 is the decoder's causal softmax attention inside each
+      sample (a sample never attends to another), with logits q.k * scale
+      (scale 1/sqrt(d_head) by default), averaged over the query heads; with
+      grouped KV heads, query head h reads KV head h // (H / H_kv). Both
+      score columns are aggregated.
+  R18 In Eq. 4, x_attn is the attention sublayer's output that is added to
+      the residual stream (after its output projection) and x is that
+      sublayer's residual input; norms are Euclidean over D; a token with
+      both norms 0 keeps its score.
 
 Parity pins live in tests/test_oracle_pins.py; no part of this file is
 "parity unpinned" except the conventions R3-R5, R8, R11, R12, R14-R16 above,
@@ -62,6 +75,7 @@ stated choice; the formulas that follow each choice are pinned).
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass
 from typing import Dict, Optional, Tuple
 
@@ -540,3 +554,68 @@ def msi(counts_text, counts_vision) -> float:
     nz = den > 0
     c_text[nz] = nt[nz] / den[nz]
     return float(np.mean(2.0 * np.abs(c_text - 0.5)))
+
+
+# ----------------------------------------------------------------------------
+# Attention-accumulated modality score (Sec. 3.2.1, Eq. 2-4). The paper's
+# implementation note carries the scores as extra value channels through the
+# attention; here the attention matrix is formed explicitly, per sample and
+# head, as the definition reads.
+# ----------------------------------------------------------------------------
+
+def attn_score_init(modality_id) -> np.ndarray:
+    """Layer-0 scores (Eq. 2): the one-hot hard label; columns (vision, text) (R13)."""
+    mid = np.asarray(modality_id)
+    M = np.zeros((mid.shape[0], 2))
+    M[mid == VISION, 0] = 1.0
+    M[mid == TEXT, 1] = 1.0
+    return M
+
+
+def attention_heads(q, k, v, sample_offsets, M, scale: Optional[float] = None):
+    """Per query head h: Attn_h = causal softmax(q_h k_h^T * scale) inside each
+    sample (R17); returns O[T, H, d_head] = Attn_h v_h and A[T, H, 2] = Attn_h M
+    (Eq. 3 before the head average). q: [T, H, d_head]; k, v: [T, H_kv, d_head]."""
+    Q, K, V = widen(q), widen(k), widen(v)
+    Ms = np.asarray(M, dtype=np.float64)
+    T, H, dh = Q.shape
+    Hkv = K.shape[1]
+    group = H // Hkv
+    sc = 1.0 / math.sqrt(dh) if scale is None else float(scale)
+    O = np.zeros((T, H, V.shape[2]))
+    A = np.zeros((T, H, 2))
+    off = np.asarray(sample_offsets)
+    for i in range(len(off) - 1):
+        lo, hi = int(off[i]), int(off[i + 1])
+        L = hi - lo
+        if L == 0:
+            continue
+        causal = np.tril(np.ones((L, L), dtype=bool))
+        for h in range(H):
+            hk = h // group
+            logits = (Q[lo:hi, h] @ K[lo:hi, hk].T) * sc
+            logits = np.where(causal, logits, -np.inf)
+            logits = logits - logits.max(axis=1, keepdims=True)
+            P = np.exp(logits)
+            P = P / P.sum(axis=1, keepdims=True)
+            O[lo:hi, h] = P @ V[lo:hi, hk]
+            A[lo:hi, h] = P @ Ms[lo:hi]
+    return O, A
+
+
+def attn_aggregate(A) -> np.ndarray:
+    """M_tilde = Attn M with Attn averaged over heads (Eq. 3); A from attention_heads."""
+    return np.asarray(A, dtype=np.float64).mean(axis=1)
+
+
+def attn_score_update(x, x_attn, M, M_tilde) -> np.ndarray:
+    """M^(l+1) = (|x_attn| M_tilde + |x| M) / (|x_attn| + |x|)  (Eq. 4, R18)."""
+    nx = np.sqrt((widen(x) ** 2).sum(axis=1))
+    na = np.sqrt((widen(x_attn) ** 2).sum(axis=1))
+    M = np.asarray(M, dtype=np.float64)
+    Mt = np.asarray(M_tilde, dtype=np.float64)
+    out = M.copy()
+    den = nx + na
+    nz = den > 0
+    out[nz] = (na[nz, None] * Mt[nz] + nx[nz, None] * M[nz]) / den[nz, None]
+    return out

@@ -305,3 +305,50 @@ def random_gauss_state(rng: np.random.Generator, d: int, count: float = 1000.0) 
     mu = rng.standard_normal((2, d)).astype(np.float32) * np.float32(0.3)
     var = rng.uniform(0.5, 2.0, size=(2, d)).astype(np.float32)
     return n, (n[:, None] * mu).astype(np.float32), (n[:, None] * var).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------
+# Inputs of the attention-accumulated score (Sec. 3.2.1)
+# ----------------------------------------------------------------------------
+
+@dataclass
+class AttnInputs:
+    """One attention layer's tensors for the attention-accumulated score."""
+
+    samples: Tuple[Tuple[int, int], ...]
+    q: np.ndarray  # [T, H, d_head] bf16 bits
+    k: np.ndarray  # [T, H_kv, d_head] bf16 bits
+    v: np.ndarray  # [T, H_kv, d_head] bf16 bits
+    x: np.ndarray  # [T, D] residual input of the attention sublayer, bf16 bits
+    x_attn: np.ndarray  # [T, D] attention sublayer output, bf16 bits
+    m_in: np.ndarray  # [T, 2] float32 input scores (vision, text)
+    modality_id: np.ndarray  # [T] uint8, 0 vision / 1 text
+    sample_offsets: np.ndarray  # [n_batch + 1] int32
+
+    @property
+    def T(self) -> int:
+        return int(self.sample_offsets[-1])
+
+
+def make_attention_inputs(samples, d: int, n_heads: int, n_kv_heads: int, head_dim: int, seed: int,
+                          logit_std: float = 2.0) -> AttnInputs:
+    """Seeded draws: q, k, v ~ N(0, s^2) with s^2 = logit_std, so that the logits
+    q.k / sqrt(d_head) have standard deviation logit_std; x ~ N(0, 1) and
+    x_attn ~ N(0, 0.5^2) per element; m_in soft scores with vision share
+    U(0, 1). Samples are laid out vision block then text block, as in the
+    layer workloads."""
+    rng = np.random.default_rng(seed)
+    T = sum(v + t for v, t in samples)
+    s = np.float32(np.sqrt(logit_std))
+    def draw(shape, scale):
+        return f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(scale))
+    q = draw((T, n_heads, head_dim), s)
+    k = draw((T, n_kv_heads, head_dim), s)
+    v = draw((T, n_kv_heads, head_dim), 1.0)
+    x = draw((T, d), 1.0)
+    x_attn = draw((T, d), 0.5)
+    m_in = random_soft_scores(rng, T)
+    mid = np.concatenate([np.concatenate([np.zeros(a, np.uint8), np.ones(b, np.uint8)]) for a, b in samples]) \
+        if samples else np.zeros(0, np.uint8)
+    offsets = np.concatenate([[0], np.cumsum([a + b for a, b in samples])]).astype(np.int32)
+    return AttnInputs(tuple(samples), q, k, v, x, x_attn, m_in, mid, offsets)

@@ -634,3 +634,125 @@ def test_msi_cases():
     assert O.msi([2, 4, 6], [1, 2, 3]) == 0.0             # identical distributions
     assert abs(O.msi([3, 1], [1, 3]) - 0.5) < 1e-15       # shares 0.75 / 0.25 each way
     assert abs(O.msi([3, 1, 0], [1, 3, 0]) - (0.5 + 0.5 + 0.0) / 3) < 1e-15  # idle expert: unspecialised
+
+
+# ---------------------------------------------------------------- attention-accumulated score (Sec. 3.2.1)
+
+def _attn_case(rng, offsets, H, Hkv, dh):
+    T = offsets[-1]
+    q = rng.standard_normal((T, H, dh))
+    k = rng.standard_normal((T, Hkv, dh))
+    v = rng.standard_normal((T, Hkv, dh))
+    a = rng.uniform(0, 1, T)
+    M = np.stack([a, 1 - a], axis=1)
+    return q, k, v, M
+
+
+def test_attn_init_is_the_one_hot_label():
+    mid = np.array([0, 1, 1, 0, 1], np.uint8)
+    M = O.attn_score_init(mid)
+    assert M.tolist() == [[1, 0], [0, 1], [0, 1], [1, 0], [0, 1]]
+
+
+@pytest.mark.parametrize("H,Hkv", [(4, 4), (4, 2), (6, 1)])
+def test_attention_matches_torch_sdpa_with_scores_as_value_channels(H, Hkv):
+    # the paper's implementation note: concatenate the scores to V, run causal
+    # attention, read the aggregated scores from the extra output channels
+    rng = np.random.default_rng(7)
+    offsets = [0, 5, 5, 17, 30]  # an empty sample in the middle
+    dh = 8
+    q, k, v, M = _attn_case(rng, offsets, H, Hkv, dh)
+    Ob, A = O.attention_heads(q, k, v, offsets, M)
+    for i in range(len(offsets) - 1):
+        lo, hi = offsets[i], offsets[i + 1]
+        if hi == lo:
+            continue
+        for h in range(H):
+            hk = h // (H // Hkv)
+            vv = np.concatenate([v[lo:hi, hk], M[lo:hi]], axis=1)
+            out = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(q[lo:hi, h][None]), torch.from_numpy(k[lo:hi, hk][None]),
+                torch.from_numpy(vv[None]), is_causal=True)[0].numpy()
+            assert np.allclose(Ob[lo:hi, h], out[:, :dh], rtol=1e-12, atol=1e-12)
+            assert np.allclose(A[lo:hi, h], out[:, dh:], rtol=1e-12, atol=1e-12)
+
+
+def test_attention_uniform_queries_give_causal_prefix_means():
+    rng = np.random.default_rng(8)
+    offsets = [0, 9, 20]
+    q, k, v, M = _attn_case(rng, offsets, 3, 3, 4)
+    q[:] = 0.0
+    Ob, A = O.attention_heads(q, k, v, offsets, M)
+    for lo, hi in zip(offsets[:-1], offsets[1:]):
+        cnt = np.arange(1, hi - lo + 1)[:, None]
+        pm = np.cumsum(M[lo:hi], axis=0) / cnt
+        for h in range(3):
+            assert np.allclose(A[lo:hi, h], pm, atol=1e-13)
+            assert np.allclose(Ob[lo:hi, h], np.cumsum(v[lo:hi, h], axis=0) / cnt, atol=1e-13)
+
+
+def test_attention_first_token_of_each_sample_sees_only_itself():
+    rng = np.random.default_rng(9)
+    offsets = [0, 4, 11, 12]
+    q, k, v, M = _attn_case(rng, offsets, 2, 1, 4)
+    Ob, A = O.attention_heads(q, k, v, offsets, M)
+    for lo in offsets[:-1]:
+        assert np.allclose(A[lo], M[lo][None, :], atol=1e-15)
+        assert np.allclose(Ob[lo], v[lo, 0][None, :], atol=1e-15)
+
+
+def test_attention_samples_do_not_mix_and_the_future_is_masked():
+    rng = np.random.default_rng(10)
+    offsets = [0, 7, 15]
+    q, k, v, M = _attn_case(rng, offsets, 2, 2, 4)
+    O1, A1 = O.attention_heads(q, k, v, offsets, M)
+    k2, v2, M2 = k.copy(), v.copy(), M.copy()
+    k2[7:] += 1.0
+    v2[7:] -= 2.0
+    M2[7:] = M2[7:, ::-1]
+    O2, A2 = O.attention_heads(q, k2, v2, offsets, M2)
+    assert np.array_equal(O1[:7], O2[:7]) and np.array_equal(A1[:7], A2[:7])
+    assert not np.allclose(A1[7:], A2[7:])
+    # changing the last token of a sample leaves every earlier token alone
+    k3, v3 = k.copy(), v.copy()
+    k3[6] += 3.0
+    v3[6] += 3.0
+    O3, A3 = O.attention_heads(q, k3, v3, offsets, M)
+    assert np.array_equal(O1[:6], O3[:6]) and np.array_equal(A1[:6], A3[:6])
+    assert not np.allclose(O1[6], O3[6])
+
+
+def test_attention_scale_is_a_logit_multiplier():
+    rng = np.random.default_rng(11)
+    offsets = [0, 10]
+    q, k, v, M = _attn_case(rng, offsets, 2, 2, 16)
+    Oa, Aa = O.attention_heads(q * 3.0, k, v, offsets, M)
+    Ob, Ab = O.attention_heads(q, k, v, offsets, M, scale=3.0 / 4.0)  # 1/sqrt(16) = 1/4
+    assert np.allclose(Oa, Ob, atol=1e-13) and np.allclose(Aa, Ab, atol=1e-13)
+
+
+def test_attn_aggregate_is_the_head_mean_and_keeps_rows_summing_to_one():
+    rng = np.random.default_rng(12)
+    offsets = [0, 6, 19]
+    q, k, v, M = _attn_case(rng, offsets, 5, 5, 4)
+    _, A = O.attention_heads(q, k, v, offsets, M)
+    Mt = O.attn_aggregate(A)
+    for j in range(19):
+        assert abs(Mt[j, 0] - math.fsum(A[j, :, 0]) / 5) < 1e-15
+    assert np.allclose(Mt.sum(axis=1), 1.0, atol=1e-14)
+    assert np.all((Mt >= 0) & (Mt <= 1))
+
+
+def test_attn_update_norm_weighted_residual_mix():
+    x = np.array([[3.0, 4.0], [0.0, 0.0], [1.0, 0.0], [0.0, 2.0], [0.0, 0.0]])
+    xa = np.array([[0.0, 1.0], [2.0, 0.0], [0.0, 0.0], [2.0, 0.0], [0.0, 0.0]])
+    M = np.array([[1.0, 0.0], [0.2, 0.8], [0.3, 0.7], [0.9, 0.1], [0.4, 0.6]])
+    Mt = np.array([[0.5, 0.5], [0.6, 0.4], [0.1, 0.9], [0.1, 0.9], [0.0, 1.0]])
+    out = O.attn_score_update(x, xa, M, Mt)
+    # |x| = 5, |x_attn| = 1: (1 * [0.5, 0.5] + 5 * [1, 0]) / 6
+    assert np.allclose(out[0], [5.5 / 6, 0.5 / 6], atol=1e-15)
+    assert np.allclose(out[1], Mt[1], atol=1e-15)  # no residual: the aggregate
+    assert np.allclose(out[2], M[2], atol=1e-15)  # no attention output: unchanged
+    assert np.allclose(out[3], (M[3] + Mt[3]) / 2, atol=1e-15)  # equal norms: the mean
+    assert np.array_equal(out[4], M[4])  # both norms 0 (R18)
+    assert np.allclose(out.sum(axis=1), 1.0, atol=1e-15)
