@@ -374,6 +374,58 @@ size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which);
 int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void* dst, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Attention-accumulated modality score (Sec. 3.2.1, Eq. 2-4).               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Layer-0 scores (Eq. 2): M[j] = (1, 0) for a vision token (modality_id 0),
+ * (0, 1) for a text token (1), (0, 0) for any other label.
+ * modality_id  [T] uint8 (device).   M  [T, 2] float32 output (device).
+ * Asynchronous on `stream`; SMOES_ERR_ARG for a NULL pointer with T > 0.
+ */
+int smoes_attn_score_init(const uint8_t* modality_id, int64_t T, float* M, void* stream);
+
+/*
+ * Causal softmax attention inside each sample (a sample never attends to
+ * another; within a sample token j attends to tokens <= j), per query head h,
+ * with the modality scores carried as two extra value channels (the
+ * supplementary implementation note; here accumulated in float32):
+ *   o[j][h]       = sum_j' Attn_h(j, j') v[j'][h_kv]               (bf16)
+ *   m_heads[j][h] = sum_j' Attn_h(j, j') m_in[j']                   (Eq. 3
+ *                   before the head average; float32, 2 columns)
+ * with Attn_h(j, .) = softmax over j' of scale * q[j][h] . k[j'][h_kv] and
+ * h_kv = h / (n_heads / n_kv_heads) (grouped KV heads).
+ * q            [T, n_heads, head_dim] bf16 (device, row-major).
+ * k, v         [T, n_kv_heads, head_dim] bf16 (device).
+ * sample_offsets [n_batch + 1] int32 (device): 0 = off[0] <= ... <= off[n_batch] = T.
+ * m_in         [T, 2] float32 scores of this layer's input (column 0 vision).
+ * scale        logit scale; <= 0 selects 1 / sqrt(head_dim).
+ * o            [T, n_heads, head_dim] bf16 output (device).
+ * m_heads      [T, n_heads, 2] float32 output (device).
+ * Shapes: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ * T * n_heads * head_dim * 2 < 2^31. Sums run in a fixed order: results are
+ * reproducible. Asynchronous on `stream`; nothing is allocated.
+ */
+int smoes_attention_scores(const void* q, const void* k, const void* v, int64_t T, int n_heads,
+                           int n_kv_heads, int head_dim, const int32_t* sample_offsets, int n_batch,
+                           const float* m_in, float scale, void* o, float* m_heads, void* stream);
+
+/*
+ * Head average (Eq. 3) and norm-weighted residual mix (Eq. 4):
+ *   M_tilde[j] = (1 / n_heads) sum_h m_heads[j][h]
+ *   m_out[j]   = (|x_attn[j]| M_tilde[j] + |x[j]| m_in[j]) / (|x_attn[j]| + |x[j]|)
+ * with Euclidean norms over d; a token with both norms 0 keeps m_in[j].
+ * x            [T, d] residual input of the attention sublayer (act_dtype).
+ * x_attn       [T, d] attention sublayer output added to it (act_dtype).
+ * m_heads      [T, n_heads, 2] float32 from smoes_attention_scores.
+ * m_in, m_out  [T, 2] float32; m_out may equal m_in (updated in place).
+ * Shapes: 1 <= d <= SMOES_D_MAX, d % 8 == 0. Asynchronous on `stream`.
+ */
+int smoes_attn_score_update(const void* x, const void* x_attn, int act_dtype, int64_t T, int d,
+                            const float* m_heads, int n_heads, const float* m_in, float* m_out,
+                            void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Timing helpers for stage_events (hipEvent_t handles behind void*).        */
 /* ------------------------------------------------------------------------ */
 

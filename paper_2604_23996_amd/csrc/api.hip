@@ -177,6 +177,41 @@ int smoes_binning(const float* probs, const int32_t* topk_idx, const uint8_t* mo
                                      msi, ws, as_stream(stream)));
 }
 
+// ------------------------------------------------------------------ attention-accumulated score
+
+int smoes_attn_score_init(const uint8_t* modality_id, int64_t T, float* M, void* stream) {
+    if (T < 0) return SMOES_ERR_SHAPE;
+    if (T > 0 && (modality_id == nullptr || M == nullptr)) return SMOES_ERR_ARG;
+    return hip_status(launch_attn_init(modality_id, T, M, as_stream(stream)));
+}
+
+int smoes_attention_scores(const void* q, const void* k, const void* v, int64_t T, int n_heads,
+                           int n_kv_heads, int head_dim, const int32_t* sample_offsets, int n_batch,
+                           const float* m_in, float scale, void* o, float* m_heads, void* stream) {
+    if (T < 0 || n_batch < 1) return SMOES_ERR_SHAPE;
+    if (n_heads < 1 || n_heads > 65535 || n_kv_heads < 1 || (n_heads % n_kv_heads) != 0) return SMOES_ERR_SHAPE;
+    if (head_dim != 64 && head_dim != 128) return SMOES_ERR_SHAPE;
+    if (T * n_heads * head_dim * 2 > INT32_MAX) return SMOES_ERR_SHAPE;
+    if (scale != scale) return SMOES_ERR_ARG;
+    if (T > 0 && (q == nullptr || k == nullptr || v == nullptr || sample_offsets == nullptr || m_in == nullptr ||
+                  o == nullptr || m_heads == nullptr))
+        return SMOES_ERR_ARG;
+    const float sc = scale > 0.0f ? scale : 1.0f / sqrtf(static_cast<float>(head_dim));
+    return hip_status(launch_attention(q, k, v, T, n_heads, n_kv_heads, head_dim, sample_offsets, n_batch, m_in,
+                                       sc, o, m_heads, as_stream(stream)));
+}
+
+int smoes_attn_score_update(const void* x, const void* x_attn, int act_dtype, int64_t T, int d,
+                            const float* m_heads, int n_heads, const float* m_in, float* m_out,
+                            void* stream) {
+    if (!dtype_ok(act_dtype)) return SMOES_ERR_ARG;
+    if (T < 0 || d < 1 || d > SMOES_D_MAX || (d % 8) != 0 || n_heads < 1) return SMOES_ERR_SHAPE;
+    if (T > 0 && (x == nullptr || x_attn == nullptr || m_heads == nullptr || m_in == nullptr || m_out == nullptr))
+        return SMOES_ERR_ARG;
+    return hip_status(launch_attn_update(x, x_attn, act_dtype, T, d, m_heads, n_heads, m_in, m_out,
+                                         as_stream(stream)));
+}
+
 size_t smoes_permute_workspace_size(int64_t T, int E, int k) { return permute_ws(T, E, k); }
 
 int smoes_permute(const int32_t* topk_idx, int64_t T, int E, int k, int32_t* expert_offsets,

@@ -89,4 +89,12 @@ hipError_t launch_binning(const float* probs, const int32_t* topk_idx, const uin
                           float* bal_loss, float* dlogits, int accumulate, float* msi, void* ws,
                           hipStream_t stream);
 
+// ---------------------------------------------------------------- attention-accumulated score
+hipError_t launch_attention(const void* q, const void* k, const void* v, int64_t T, int H, int Hkv, int head_dim,
+                            const int32_t* sample_offsets, int n_batch, const float* m_in, float scale, void* o,
+                            float* m_heads, hipStream_t stream);
+hipError_t launch_attn_update(const void* x, const void* x_attn, int act_dtype, int64_t T, int d,
+                              const float* m_heads, int H, const float* m_in, float* m_out, hipStream_t stream);
+hipError_t launch_attn_init(const uint8_t* modality_id, int64_t T, float* M, hipStream_t stream);
+
 }  // namespace smoes

@@ -107,6 +107,14 @@ def lib() -> ctypes.CDLL:
         L.smoes_binning.argtypes = [c_void, c_void, c_void, c_i64, c_int, c_int, c_void, c_int, c_float, c_void,
                                     c_void, c_void, c_void, c_float, c_void, c_void, c_int, c_void, c_void,
                                     c_size, c_void]
+        L.smoes_attn_score_init.restype = c_int
+        L.smoes_attn_score_init.argtypes = [c_void, c_i64, c_void, c_void]
+        L.smoes_attention_scores.restype = c_int
+        L.smoes_attention_scores.argtypes = [c_void, c_void, c_void, c_i64, c_int, c_int, c_int, c_void, c_int,
+                                             c_void, c_float, c_void, c_void, c_void]
+        L.smoes_attn_score_update.restype = c_int
+        L.smoes_attn_score_update.argtypes = [c_void, c_void, c_int, c_i64, c_int, c_void, c_int, c_void, c_void,
+                                              c_void]
         L.smoes_streams_create.restype = c_int
         L.smoes_streams_create.argtypes = [ctypes.POINTER(SmoesStreams)]
         L.smoes_streams_destroy.restype = c_int
@@ -241,6 +249,45 @@ def binning(probs: torch.Tensor, topk_idx: torch.Tensor, modality_id: torch.Tens
                                beta, _p(load_ema), _p(out["counts"]), _p(out["f_spec"]),
                                _p(out["expert_to_bin_next"]), grad_scale, _p(out["bal_loss"]), _p(dlogits),
                                int(accumulate), _p(out["msi"]), _p(ws), ws.numel(), _stream()), "smoes_binning")
+    return out
+
+
+def attn_score_init(modality_id: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """smoes_attn_score_init: one-hot layer-0 scores [T, 2] (Eq. 2)."""
+    T = modality_id.shape[0]
+    if out is None:
+        out = torch.empty((T, 2), dtype=torch.float32, device=modality_id.device)
+    _check(lib().smoes_attn_score_init(_p(modality_id), T, _p(out), _stream()), "smoes_attn_score_init")
+    return out
+
+
+def attention_scores(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, sample_offsets: torch.Tensor,
+                     m_in: torch.Tensor, scale: float = 0.0, o: Optional[torch.Tensor] = None,
+                     m_heads: Optional[torch.Tensor] = None):
+    """smoes_attention_scores: causal per-sample attention O [T, H, d_head] (bf16)
+    and the per-head aggregated scores m_heads [T, H, 2] (Eq. 3 before the head mean)."""
+    T, H, dh = q.shape
+    Hkv = k.shape[1]
+    dev = q.device
+    if o is None:
+        o = torch.empty((T, H, dh), dtype=torch.bfloat16, device=dev)
+    if m_heads is None:
+        m_heads = torch.empty((T, H, 2), dtype=torch.float32, device=dev)
+    n_batch = sample_offsets.numel() - 1
+    _check(lib().smoes_attention_scores(_p(q), _p(k), _p(v), T, H, Hkv, dh, _p(sample_offsets), n_batch,
+                                        _p(m_in), scale, _p(o), _p(m_heads), _stream()), "smoes_attention_scores")
+    return o, m_heads
+
+
+def attn_score_update(x: torch.Tensor, x_attn: torch.Tensor, m_heads: torch.Tensor, m_in: torch.Tensor,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """smoes_attn_score_update: head mean (Eq. 3) and norm-weighted mix (Eq. 4) -> [T, 2]."""
+    T, d = x.shape
+    H = m_heads.shape[1]
+    if out is None:
+        out = torch.empty((T, 2), dtype=torch.float32, device=x.device)
+    _check(lib().smoes_attn_score_update(_p(x), _p(x_attn), _dtype_code(x), T, d, _p(m_heads), H, _p(m_in),
+                                         _p(out), _stream()), "smoes_attn_score_update")
     return out
 
 
