@@ -296,6 +296,52 @@ def main():
                                          "(added onto dlogits) + MSI, one layer, this step's routing",
                                  "ms": round(bin_ms, 5), "gbs": round(bin_bytes / (bin_ms * 1e-3) / 1e9, 1),
                                  "frac_hbm": round(bin_bytes / (bin_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}}
+    # Attention-accumulated score (Eq. 2-4) on the same token layout: causal
+    # per-sample attention of a 16-head, d_head = 128 attention layer (the
+    # backbone's hidden size 2048) with the scores as two extra value
+    # channels, then the head mean and the norm-weighted update. Timed on its
+    # own, not part of the layer step above.
+    n_heads, head_dim = 16, cfg.d // 16
+    if head_dim in (64, 128):
+        log("[bench] attention-accumulated score")
+        ai = W.make_attention_inputs(cfg.samples, cfg.d, n_heads, n_heads, head_dim, seed=cfg.seed + 100)
+        aq, ak, av, ax, axa = t(ai.q), t(ai.k), t(ai.v), t(ai.x), t(ai.x_attn)
+        aoff, am = t(ai.sample_offsets), t(ai.m_in)
+        ao = torch.empty((cfg.T, n_heads, head_dim), dtype=torch.bfloat16, device=dev)
+        amh = torch.empty((cfg.T, n_heads, 2), dtype=torch.float32, device=dev)
+        amo = torch.empty((cfg.T, 2), dtype=torch.float32, device=dev)
+
+        def attn_call():
+            S.attention_scores(aq, ak, av, aoff, am, o=ao, m_heads=amh)
+            S.attn_score_update(ax, axa, amh, am, out=amo)
+
+        for _ in range(3):
+            attn_call()
+        a_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        a_att = []
+        a_tot = []
+        for _ in range(args.steps):
+            a_ev[0].record()
+            S.attention_scores(aq, ak, av, aoff, am, o=ao, m_heads=amh)
+            a_ev[1].record()
+            S.attn_score_update(ax, axa, amh, am, out=amo)
+            a_ev[2].record()
+            torch.cuda.synchronize()
+            a_att.append(a_ev[0].elapsed_time(a_ev[1]))
+            a_tot.append(a_ev[0].elapsed_time(a_ev[2]))
+        att_ms = float(np.median(a_att))
+        tot_ms = float(np.median(a_tot))
+        lens = np.diff(ai.sample_offsets).astype(np.float64)
+        att_flops = float(n_heads * 4 * head_dim * np.sum(lens * (lens + 1) / 2))  # causal half only
+        upd_bytes = cfg.T * (2 * cfg.d * (2 if cfg.dtype == W.BF16 else 4) + n_heads * 8 + 16)
+        line["extra"]["attention_score"] = {
+            "what": f"causal per-sample attention ({n_heads} heads x {head_dim}) carrying the modality scores "
+                    "as fp32 value channels + head mean + norm-weighted update (Eq. 2-4), one layer",
+            "ms": round(tot_ms, 5), "attention_ms": round(att_ms, 5),
+            "tokens_per_s": round(cfg.T / (tot_ms * 1e-3), 1),
+            "attention_tflops": round(att_flops / (att_ms * 1e-3) / 1e12, 2),
+            "attention_frac_mfma": round(att_flops / (att_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "update_gbs": round(upd_bytes / ((tot_ms - att_ms) * 1e-3) / 1e9, 1) if tot_ms > att_ms else None}
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on {args.cpu_samples} samples")
         line["cpu_baseline"] = cpu_baseline(cfg, inp, min(args.cpu_samples, cfg.n_batch))

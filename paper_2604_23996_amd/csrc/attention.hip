@@ -16,8 +16,13 @@
 //   8*(v/4) + 4*(l/32) + v%4 of the 32-key tile and query l%32, so softmax
 //   statistics are per lane plus one exchange with lane l ^ 32.
 //   O^T += V^T P^T: P^T's B operand is the S^T accumulator itself, read in
-//   the order above; V is stored transposed in LDS ([d_head][64 keys]) so the
-//   A operand reads the matching keys with two 8-byte loads.
+//   the order above; V stays row-major in LDS and the A operand (4 keys of one
+//   dim per 8 bytes) comes from the transposing LDS read ds_read_b64_tr_b16:
+//   within each 16-lane group, lane j supplies the address of key j/4 and
+//   dims 4*(j%4) .. + 3 and receives dim j of those four keys.
+// The running maximum is rescaled lazily (only when a block's maximum exceeds
+// it by more than 8 in log2 units); blocks that every query of a wave sees
+// whole skip the mask.
 // Logits use exp2 with the scale folded into log2(e).
 #include "common.h"
 #include "kernels.h"
@@ -33,6 +38,8 @@ constexpr int kAtBufFlags = 0x00020000;
 constexpr uint32_t kAtOob = 0x80000000u;  // a byte offset past any buffer: reads return 0
 
 typedef int at_i32x4 __attribute__((ext_vector_type(4)));
+typedef short at_v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) at_v4i16 at_lds_v4i16;
 
 // Start of the sample that holds token q: offsets[s] for the largest s < n_batch
 // with offsets[s] <= q.
@@ -62,13 +69,18 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
     constexpr int CPK = DH / 8;           // 16-byte chunks per key row
     constexpr int KC = DH / 16;           // K = 16 slices of the QK^T contraction
     constexpr int DT = DH / 32;           // 32-row tiles of O^T
-    constexpr int KCH = AT_BK * CPK / AT_THREADS;      // K chunks per thread per block
-    constexpr int VPR = (AT_BK / 2) * CPK / AT_THREADS;  // V key-pair items per thread per block
-    static_assert(KCH >= 1 && VPR >= 1, "head size");
-    __shared__ __attribute__((aligned(16))) uint16_t k_lds[AT_BK * DH];
-    __shared__ __attribute__((aligned(16))) uint16_t vt_lds[DH * AT_BK];
+    constexpr int KCH = AT_BK * CPK / AT_THREADS;  // K (and V) 16-byte chunks per thread per block
+    static_assert(KCH >= 1, "head size");
+    // Padded rows instead of swizzles, so that every fragment address is a
+    // per-lane base plus an immediate. Pitches chosen so that the fragment
+    // reads hit distinct LDS banks: K rows of DH + 8 elements (16-byte reads of
+    // 16 consecutive keys), V rows of DH + 32 elements (the transposing reads
+    // of 8 keys x 64 bytes).
+    constexpr int KP = DH + 8;   // K row pitch (elements)
+    constexpr int VP = DH + 32;  // V row pitch (elements)
+    __shared__ __attribute__((aligned(16))) uint16_t k_lds[AT_BK * KP];
+    __shared__ __attribute__((aligned(16))) uint16_t v_lds[AT_BK * VP];
     __shared__ __attribute__((aligned(16))) float mv_lds[2][AT_BK];
-    __shared__ __attribute__((aligned(16))) uint16_t q_lds[AT_BQ * DH];
 
     const int nqb = static_cast<int>(ceil_div(T, AT_BQ));
     const int qb = nqb - 1 - static_cast<int>(blockIdx.x);  // longest (latest) blocks first
@@ -85,6 +97,13 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
     const bool q_ok = qi < Ti;
     const int qe = q_ok ? qi : Ti - 1;
     const int qstart = min(max(sample_start(offsets, n_batch, qe), 0), qe);
+    const int wq0 = row0 + wave * 32;  // first query row of this wave
+    // per-lane base of the transposing V reads: 16-lane group g = lane / 16
+    // covers dims 16 (g & 1) .. + 15 of a 32-dim tile and keys 4 (g >> 1) .. + 3
+    // of an 8-key half-slice; lane j of the group points at key j / 4, dims 4 (j % 4) ..
+    const int vtr_base = ((lane >> 5) * 4 + ((lane & 15) >> 2)) * VP + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    // sample start of the wave's last query: the largest start of its queries
+    const int wq_start_max = __builtin_amdgcn_readlane(qstart, 31);
 
     const __amdgpu_buffer_rsrc_t rsK = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(k), 0, static_cast<int>(T * Hkv * DH * 2), kAtBufFlags);
@@ -93,22 +112,25 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
     const __amdgpu_buffer_rsrc_t rsM = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(m_in), 0, static_cast<int>(T * 2 * 4), kAtBufFlags);
 
-    // the block's Q rows, staged once into LDS (16-byte chunks XOR-swizzled by
-    // row) and read back as B fragments: slice c = dims 16c + 8*half .. + 7
+    // the wave's Q rows as B fragments held in registers for the whole key
+    // loop: slice c = dims 16c + 8*half .. + 7 of query qe
+    at_i32x4 qf[KC];
+    {
+        const uint4* qrow = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(qe) * H + hq) * DH);
 #pragma unroll
-    for (int i = 0; i < AT_BQ * CPK / AT_THREADS; ++i) {
-        const int id = threadIdx.x + i * AT_THREADS;
-        const int r = id / CPK, c = id % CPK;
-        const int qr = min(row0 + r, Ti - 1);
-        *reinterpret_cast<uint4*>(q_lds + r * DH + ((c ^ (r % CPK)) * 8)) =
-            *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(qr) * H + hq) * DH + c * 8);
+        for (int c = 0; c < KC; ++c) {
+            const uint4 t = qrow[2 * c + half];
+            qf[c] = at_i32x4{static_cast<int>(t.x), static_cast<int>(t.y), static_cast<int>(t.z), static_cast<int>(t.w)};
+        }
     }
 
     // global -> register staging of one key block
-    auto key_off = [&](int key) -> uint32_t {  // byte offset of the row of `key` in K or V
-        return (key >= 0 && key < Ti) ? static_cast<uint32_t>((key * Hkv + hk) * DH * 2) : kAtOob;
+    // byte offset of the row of `key` in K or V; keys below 0 wrap to offsets
+    // >= 2^31 and keys >= T land past the buffer: the bounds check reads zeros
+    auto key_off = [&](int key) -> uint32_t {
+        return static_cast<uint32_t>((key * Hkv + hk) * DH * 2);
     };
-    at_i32x4 kr[KCH], vr[VPR][2];
+    at_i32x4 kr[KCH], vr[KCH];
     float2 mr;
     auto load_block = [&](int kb0_) {
         int kb0 = kb0_;
@@ -117,18 +139,13 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
         for (int i = 0; i < KCH; ++i) {
             const int id = threadIdx.x + i * AT_THREADS;
             const int key = id / CPK, c = id % CPK;
-            const uint32_t off = key_off(kb0 + key);
-            kr[i] = __builtin_amdgcn_raw_buffer_load_b128(rsK, static_cast<int>(off == kAtOob ? off : off + c * 16), 0, 0);
+            kr[i] = __builtin_amdgcn_raw_buffer_load_b128(rsK, static_cast<int>(key_off(kb0 + key) + c * 16), 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < VPR; ++i) {
+        for (int i = 0; i < KCH; ++i) {
             const int id = threadIdx.x + i * AT_THREADS;
-            const int kp = id / CPK, c = id % CPK;
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const uint32_t off = key_off(kb0 + 2 * kp + e);
-                vr[i][e] = __builtin_amdgcn_raw_buffer_load_b128(rsV, static_cast<int>(off == kAtOob ? off : off + c * 16), 0, 0);
-            }
+            const int key = id / CPK, c = id % CPK;
+            vr[i] = __builtin_amdgcn_raw_buffer_load_b128(rsV, static_cast<int>(key_off(kb0 + key) + c * 16), 0, 0);
         }
         if (threadIdx.x < AT_BK) {
             const int key = kb0 + static_cast<int>(threadIdx.x);
@@ -137,35 +154,18 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
             mr.y = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsM, static_cast<int>(off == kAtOob ? off : off + 4), 0, 0));
         }
     };
-    // register -> LDS: K rows with 16-byte chunks XOR-swizzled by key; V
-    // transposed, 8-byte units (4 keys) XOR-swizzled by dim / 2
+    // register -> LDS: K and V rows (16-byte chunks, padded rows)
     auto store_block = [&]() {
         int sz = 0;  // opaque zero: keeps the store addresses from being hoisted out of the key loop
         asm volatile("" : "+v"(sz));
         uint16_t* kst = k_lds + sz;
-        uint16_t* vst = vt_lds + sz;
+        uint16_t* vst = v_lds + sz;
 #pragma unroll
         for (int i = 0; i < KCH; ++i) {
             const int id = threadIdx.x + i * AT_THREADS;
             const int key = id / CPK, c = id % CPK;
-            *reinterpret_cast<at_i32x4*>(kst + key * DH + ((c ^ (key % CPK)) * 8)) = kr[i];
-        }
-#pragma unroll
-        for (int i = 0; i < VPR; ++i) {
-            const int id = threadIdx.x + i * AT_THREADS;
-            const int kp = id / CPK, c = id % CPK;
-            const int key = 2 * kp;
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const uint32_t a = static_cast<uint32_t>(vr[i][0][w]), b = static_cast<uint32_t>(vr[i][1][w]);
-#pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    const int dim = c * 8 + 2 * w + e;
-                    const uint32_t pair = e == 0 ? ((a & 0xffffu) | (b << 16)) : ((a >> 16) | (b & 0xffff0000u));
-                    const int unit = (key >> 2) ^ ((dim >> 1) & 15);
-                    *reinterpret_cast<uint32_t*>(vst + dim * AT_BK + unit * 4 + (key & 3)) = pair;
-                }
-            }
+            *reinterpret_cast<at_i32x4*>(kst + key * KP + c * 8) = kr[i];
+            *reinterpret_cast<at_i32x4*>(vst + key * VP + c * 8) = vr[i];
         }
         if (threadIdx.x < AT_BK) {
             mv_lds[0][threadIdx.x] = mr.x;
@@ -191,9 +191,8 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
         int lz = 0;
         asm volatile("" : "+v"(lz));
         const uint16_t* kl = k_lds + lz;
-        const uint16_t* vl = vt_lds + lz;
+        const uint16_t* vl = v_lds + lz;
         const float* ml = &mv_lds[0][0] + lz;
-        const uint16_t* ql = q_lds + lz;
 
         // S^T = K Q^T for the two 32-key tiles; K fragments read one slice ahead
         // (the scheduling barriers keep the compiler from hoisting every LDS
@@ -201,45 +200,60 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
         f32x16_t s[2] = {f32x16_t{}, f32x16_t{}};
         auto kfrag = [&](int c, int t) {
             const int key = t * 32 + l32;
-            return *reinterpret_cast<const bf16x8_t*>(kl + key * DH + (((2 * c + half) ^ (key % CPK)) * 8));
+            return *reinterpret_cast<const bf16x8_t*>(kl + key * KP + (2 * c + half) * 8);
         };
-        auto qfrag = [&](int c) {
-            const int r = wave * 32 + l32;
-            return *reinterpret_cast<const bf16x8_t*>(ql + r * DH + (((2 * c + half) ^ (r % CPK)) * 8));
-        };
-        bf16x8_t ka[2][3];
+        bf16x8_t ka[2][2];
         ka[0][0] = kfrag(0, 0);
         ka[0][1] = kfrag(0, 1);
-        ka[0][2] = qfrag(0);
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
             if (c + 1 < KC) {
                 ka[(c + 1) & 1][0] = kfrag(c + 1, 0);
                 ka[(c + 1) & 1][1] = kfrag(c + 1, 1);
-                ka[(c + 1) & 1][2] = qfrag(c + 1);
             }
 #pragma unroll
             for (int t = 0; t < 2; ++t)
-                s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[c & 1][t], ka[c & 1][2], s[t], 0, 0, 0);
+                s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[c & 1][t], __builtin_bit_cast(bf16x8_t, qf[c]), s[t], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
-        // mask (own sample, causal) and the block maximum of this query
+        // The block maximum of this query's logits; keys outside the query's
+        // sample or past its diagonal are masked, except in blocks that every
+        // query of the wave sees whole (the common case, checked per wave).
+        const bool full = kb0 >= wq_start_max && kb0 + AT_BK - 1 <= wq0;
         float mx = -INFINITY;
+        if (full) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int key = kb0 + t * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-                const bool ok = key >= qstart && key <= qe;
-                const float x = ok ? s[t][e] * scale_log2 : -INFINITY;
-                s[t][e] = x;
-                mx = fmaxf(mx, x);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        m_run = m_new;
+                for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[t][e]);
+        } else {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int key = kb0 + t * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+                    const float x = (key >= qstart && key <= qe) ? s[t][e] : -INFINITY;
+                    s[t][e] = x;
+                    mx = fmaxf(mx, x);
+                }
+        }
+        const float mblk = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
+        // Lazy rescaling: the reference m_run moves only when a block's maximum
+        // exceeds it by more than 8 (log2 units), so exp2 stays below 2^8 and
+        // the accumulators are rescaled in few blocks. Both halves of a query
+        // take the same decision.
+        const bool grow = mblk > m_run + 8.f;
+        if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+            const float m_new = grow ? mblk : m_run;
+            const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;  // m_run = -inf: 0
+            m_run = m_new;
+            l_run *= alpha;
+            a0 *= alpha;
+            a1 *= alpha;
+#pragma unroll
+            for (int i = 0; i < DT; ++i) oacc[i] *= alpha;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
         float ls = 0.f, s0 = 0.f, s1 = 0.f;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -252,18 +266,16 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
                 const float mva[4] = {mv.x, mv.y, mv.z, mv.w}, mta[4] = {mt.x, mt.y, mt.z, mt.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p = __builtin_amdgcn_exp2f(s[t][4 * g + e] - m_use);
+                    const float p = __builtin_amdgcn_exp2f(fmaf(s[t][4 * g + e], scale_log2, -m_use));
                     s[t][4 * g + e] = p;
                     ls += p;
-                    s0 += p * mva[e];
-                    s1 += p * mta[e];
+                    s0 = fmaf(p, mva[e], s0);
+                    s1 = fmaf(p, mta[e], s1);
                 }
             }
-        l_run = l_run * alpha + ls;
-        a0 = a0 * alpha + s0;
-        a1 = a1 * alpha + s1;
-#pragma unroll
-        for (int i = 0; i < DT; ++i) oacc[i] *= alpha;
+        l_run += ls;
+        a0 += s0;
+        a1 += s1;
         // O^T += V^T P^T over four 16-key slices
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -273,14 +285,15 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
                               static_cast<int>(pack_bf16x2(st[e0 + 2], st[e0 + 3])),
                               static_cast<int>(pack_bf16x2(st[e0 + 4], st[e0 + 5])),
                               static_cast<int>(pack_bf16x2(st[e0 + 6], st[e0 + 7]))};
-            const int u0 = 4 * c + half, u1 = 4 * c + 2 + half;  // keys 16c + 4 half + 0..3, 16c + 8 + 4 half + 0..3
 #pragma unroll
             for (int i = 0; i < DT; ++i) {
-                const int dim = i * 32 + l32;
-                const int sw = (dim >> 1) & 15;
-                const uint2 lo = *reinterpret_cast<const uint2*>(vl + dim * AT_BK + ((u0 ^ sw) * 4));
-                const uint2 hi = *reinterpret_cast<const uint2*>(vl + dim * AT_BK + ((u1 ^ sw) * 4));
-                const at_i32x4 va{static_cast<int>(lo.x), static_cast<int>(lo.y), static_cast<int>(hi.x), static_cast<int>(hi.y)};
+                // keys 16c + 4 half + 0..3 and 16c + 8 + 4 half + 0..3 of dim 32i + lane % 32
+                const at_v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (at_lds_v4i16*)(vl + vtr_base + (16 * c) * VP + 32 * i));
+                const at_v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (at_lds_v4i16*)(vl + vtr_base + (16 * c + 8) * VP + 32 * i));
+                const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+                const at_i32x4 va{static_cast<int>(l2.x), static_cast<int>(l2.y), static_cast<int>(h2.x), static_cast<int>(h2.y)};
                 oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va),
                                                                   __builtin_bit_cast(bf16x8_t, pb), oacc[i], 0, 0, 0);
             }
