@@ -23,6 +23,9 @@ MoE-VLMs" (SMoES):
                load balance (Eq. 16) and its logit gradient, MSI (Eq. 18-19)
   * Sec. 3.2.1 attention-accumulated score: one-hot start (Eq. 2), head-averaged
                attention aggregation (Eq. 3), norm-weighted residual mix (Eq. 4)
+  * Suppl. GMM estimator: a K-component diagonal mixture per modality in place
+               of the single Gaussian of Sec. 3.2.2 (mixture log-likelihood,
+               Eq. 9 score, stepwise-EM update built on Eq. 5-7)
 
 Readings where the paper is silent (each also listed in the design notes):
   R1  logarithms are natural (MI in nats);
@@ -67,6 +70,17 @@ Readings where the paper is silent (each also listed in the design notes):
       the residual stream (after its output projection) and x is that
       sublayer's residual input; norms are Euclidean over D; a token with
       both norms 0 keeps its score.
+  R19 GMM estimator (the supplementary GMM ablation gives only K in {2, 4}):
+      each modality is a mixture of K diagonal Gaussians with weights
+      pi_mc = N_mc / sum_c' N_mc' (uniform when all are 0), mu and sigma^2 as
+      in Sec. 3.2.2 per component (R11 per component); LL_m is the log of the
+      mixture density without the 2 pi constant, and the score is Eq. 9 with
+      it. The update is stepwise EM: responsibilities of the token's own
+      modality under the parameters before the update, then Eq. 5-7 per
+      component with |T_m|, mu_T and the centred sum of squares replaced by
+      their responsibility-weighted forms. K = 1 is exactly Sec. 3.2.2.
+      Components must be seeded apart by the caller (identical components
+      stay identical under EM).
 
 Parity pins live in tests/test_oracle_pins.py; no part of this file is
 "parity unpinned" except the conventions R3-R5, R8, R11, R12, R14-R16 above,
@@ -619,3 +633,120 @@ def attn_score_update(x, x_attn, M, M_tilde) -> np.ndarray:
     nz = den > 0
     out[nz] = (na[nz, None] * Mt[nz] + nx[nz, None] * M[nz]) / den[nz, None]
     return out
+
+
+# ----------------------------------------------------------------------------
+# GMM estimator (supplementary GMM ablation; R19): K diagonal components per
+# modality in place of the single Gaussian of Sec. 3.2.2.
+# ----------------------------------------------------------------------------
+
+@dataclass
+class GmmState:
+    """EMA state per modality m and component c: N[2, K], S_mu[2, K, D], S_sigma2[2, K, D]."""
+
+    n: np.ndarray
+    s_mu: np.ndarray
+    s_sig: np.ndarray
+
+    @staticmethod
+    def of(n, s_mu, s_sig) -> "GmmState":
+        return GmmState(widen(n).copy(), widen(s_mu).copy(), widen(s_sig).copy())
+
+
+def gmm_params(state: GmmState, var_floor: float):
+    """pi_mc = N_mc / sum_c N_mc, mu_mc = S_mu / N, sigma^2_mc = S_sigma2 / N floored (R19)."""
+    _, K, d = state.s_mu.shape
+    pi = np.full((2, K), 1.0 / K)
+    mu = np.zeros((2, K, d))
+    var = np.ones((2, K, d))
+    for m in (VISION, TEXT):
+        tot = state.n[m].sum()
+        if tot > 0:
+            pi[m] = state.n[m] / tot
+        for c in range(K):
+            if state.n[m, c] > 0:
+                mu[m, c] = state.s_mu[m, c] / state.n[m, c]
+                var[m, c] = np.maximum(state.s_sig[m, c] / state.n[m, c], var_floor)
+    return pi, mu, var
+
+
+def gmm_component_loglik(x, pi, mu, var) -> np.ndarray:
+    """log pi_mc - 1/2 sum_d (log sigma^2_mcd + (x_d - mu_mcd)^2 / sigma^2_mcd); [T, 2, K]."""
+    X = widen(x)
+    K = pi.shape[1]
+    out = np.empty((X.shape[0], 2, K))
+    for m in (VISION, TEXT):
+        for c in range(K):
+            with np.errstate(divide="ignore"):
+                lp = np.log(pi[m, c])
+            out[:, m, c] = lp - 0.5 * (np.log(var[m, c]).sum() + (((X - mu[m, c]) ** 2) / var[m, c]).sum(axis=1))
+    return out
+
+
+def _logsumexp_last(a) -> np.ndarray:
+    mx = a.max(axis=-1, keepdims=True)
+    mx = np.where(np.isfinite(mx), mx, 0.0)
+    return (mx + np.log(np.exp(a - mx).sum(axis=-1, keepdims=True)))[..., 0]
+
+
+def gmm_log_likelihood(x, pi, mu, var) -> np.ndarray:
+    """LL_jm = log sum_c exp(component log-likelihood); [T, 2] (R19)."""
+    return _logsumexp_last(gmm_component_loglik(x, pi, mu, var))
+
+
+def gmm_modality_score(x, pi, mu, var, tau: float) -> np.ndarray:
+    """Eq. 9 with the mixture log-likelihood; [T, 2]."""
+    ll = gmm_log_likelihood(x, pi, mu, var) / tau
+    ll = ll - ll.max(axis=1, keepdims=True)
+    e = np.exp(ll)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def gmm_responsibilities(x, modality_id, pi, mu, var) -> np.ndarray:
+    """r_jc = posterior of component c under the mixture of token j's own
+    modality (the E-step); [T, K]."""
+    cl = gmm_component_loglik(x, pi, mu, var)
+    mid = np.asarray(modality_id)
+    own = cl[np.arange(cl.shape[0]), mid]  # [T, K]
+    return np.exp(own - _logsumexp_last(own)[:, None])
+
+
+def gmm_update(state: GmmState, x, modality_id, beta: float, var_floor: float) -> GmmState:
+    """Stepwise EM (R19): responsibilities under the current parameters, then
+    per modality m and component c, with weights r_jc over the tokens T_m:
+        n      = sum r,  mu_T = sum r x / n,  Q = sum r (x - mu_T)^2
+        N_t    = beta N_{t-1} + n
+        S_mu,t = beta S_mu,t-1 + n mu_T
+        S_sig,t= beta S_sig,t-1 + Q + (mu_T - S_mu,t-1 / N_{t-1})^2 beta N_{t-1} n / (beta N_{t-1} + n)
+    (Eq. 5-7 with weighted batch statistics; the last term is 0 when
+    N_{t-1} = 0 or n = 0)."""
+    X = widen(x)
+    mid = np.asarray(modality_id)
+    pi, mu, var = gmm_params(state, var_floor)
+    r = gmm_responsibilities(X, mid, pi, mu, var)
+    _, K, d = state.s_mu.shape
+    n_new = state.n.copy()
+    s_mu_new = state.s_mu.copy()
+    s_sig_new = state.s_sig.copy()
+    for m in (VISION, TEXT):
+        sel = mid == m
+        Xm = X[sel]
+        for c in range(K):
+            w = r[sel, c]
+            n = w.sum()
+            if n > 0:
+                mu_T = (w[:, None] * Xm).sum(axis=0) / n
+                Q = (w[:, None] * (Xm - mu_T) ** 2).sum(axis=0)
+            else:
+                mu_T = np.zeros(d)
+                Q = np.zeros(d)
+            n_prev = state.n[m, c]
+            if n_prev > 0 and n > 0:
+                prev_mean = state.s_mu[m, c] / n_prev
+                cross = (mu_T - prev_mean) ** 2 * (beta * n_prev * n) / (beta * n_prev + n)
+            else:
+                cross = np.zeros(d)
+            n_new[m, c] = beta * n_prev + n
+            s_mu_new[m, c] = beta * state.s_mu[m, c] + n * mu_T
+            s_sig_new[m, c] = beta * state.s_sig[m, c] + Q + cross
+    return GmmState(n_new, s_mu_new, s_sig_new)

@@ -352,3 +352,14 @@ def make_attention_inputs(samples, d: int, n_heads: int, n_kv_heads: int, head_d
         if samples else np.zeros(0, np.uint8)
     offsets = np.concatenate([[0], np.cumsum([a + b for a, b in samples])]).astype(np.int32)
     return AttnInputs(tuple(samples), q, k, v, x, x_attn, m_in, mid, offsets)
+
+
+def random_gmm_state(rng: np.random.Generator, d: int, K: int, count: float = 1000.0,
+                     spread: float = 0.5) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """EMA state of a K-component mixture per modality, components seeded
+    apart: counts count * U(0.5, 1.5), means N(0, spread^2) per column,
+    variances U(0.5, 2); returns float32 (N[2, K], S_mu[2, K, d], S_sigma2[2, K, d])."""
+    n = (count * rng.uniform(0.5, 1.5, (2, K))).astype(np.float32)
+    mu = (rng.standard_normal((2, K, d)) * spread).astype(np.float32)
+    var = rng.uniform(0.5, 2.0, (2, K, d)).astype(np.float32)
+    return n, (n[:, :, None] * mu).astype(np.float32), (n[:, :, None] * var).astype(np.float32)

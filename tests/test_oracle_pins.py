@@ -756,3 +756,117 @@ def test_attn_update_norm_weighted_residual_mix():
     assert np.allclose(out[3], (M[3] + Mt[3]) / 2, atol=1e-15)  # equal norms: the mean
     assert np.array_equal(out[4], M[4])  # both norms 0 (R18)
     assert np.allclose(out.sum(axis=1), 1.0, atol=1e-15)
+
+
+# ---------------------------------------------------------------- GMM estimator (R19)
+
+def _gmm_case(rng, T=40, d=6, K=3):
+    x = rng.standard_normal((T, d)) * 1.5
+    mid = (rng.random(T) < 0.4).astype(np.uint8)
+    n, smu, ssig = W.random_gmm_state(rng, d, K, count=50.0, spread=1.0)
+    return x, mid, O.GmmState.of(n, smu, ssig)
+
+
+def test_gmm_with_one_component_is_the_single_gaussian():
+    rng = np.random.default_rng(30)
+    x, mid, st = _gmm_case(rng, K=1)
+    g = O.GaussState.of(st.n[:, 0], st.s_mu[:, 0], st.s_sig[:, 0])
+    pi, mu, var = O.gmm_params(st, 1e-6)
+    mu1, var1 = O.gauss_params(g, 1e-6)
+    assert np.array_equal(pi, np.ones((2, 1)))
+    assert np.allclose(O.gmm_log_likelihood(x, pi, mu, var), O.log_likelihood(x, mu1, var1), atol=1e-12)
+    assert np.allclose(O.gmm_modality_score(x, pi, mu, var, 3.0), O.modality_score(x, mu1, var1, 3.0), atol=1e-14)
+    up = O.gmm_update(st, x, mid, 0.9, 1e-6)
+    ug = O.gauss_update(g, x, mid, 0.9)
+    assert np.allclose(up.n[:, 0], ug.n, rtol=1e-14)
+    assert np.allclose(up.s_mu[:, 0], ug.s_mu, rtol=1e-12, atol=1e-12)
+    assert np.allclose(up.s_sig[:, 0], ug.s_sig, rtol=1e-12, atol=1e-12)
+
+
+def test_gmm_loglik_matches_scipy_mixture_density():
+    rng = np.random.default_rng(31)
+    x, mid, st = _gmm_case(rng)
+    pi, mu, var = O.gmm_params(st, 1e-6)
+    ll = O.gmm_log_likelihood(x, pi, mu, var)
+    d = x.shape[1]
+    for m in (0, 1):
+        comp = np.stack([np.log(pi[m, c]) + scipy.stats.norm.logpdf(x, mu[m, c], np.sqrt(var[m, c])).sum(axis=1)
+                         for c in range(pi.shape[1])], axis=1)
+        ref = scipy.special.logsumexp(comp, axis=1) + 0.5 * d * math.log(2 * math.pi)  # R11: no 2 pi
+        assert np.allclose(ll[:, m], ref, atol=1e-10)
+
+
+def test_gmm_identical_components_collapse_to_one_gaussian():
+    rng = np.random.default_rng(32)
+    x, mid, st = _gmm_case(rng, K=1)
+    two = O.GmmState(np.repeat(st.n, 2, axis=1) / 2, np.repeat(st.s_mu, 2, axis=1) / 2,
+                     np.repeat(st.s_sig, 2, axis=1) / 2)
+    p1, m1, v1 = O.gmm_params(st, 1e-6)
+    p2, m2, v2 = O.gmm_params(two, 1e-6)
+    assert np.allclose(O.gmm_log_likelihood(x, p2, m2, v2), O.gmm_log_likelihood(x, p1, m1, v1), atol=1e-12)
+    r = O.gmm_responsibilities(x, mid, p2, m2, v2)
+    assert np.allclose(r, 0.5, atol=1e-15)
+
+
+def test_gmm_responsibilities_pick_the_generating_component():
+    rng = np.random.default_rng(33)
+    d, K = 8, 2
+    means = np.stack([np.full(d, -3.0), np.full(d, 3.0)])
+    lab = rng.integers(0, K, 60)
+    x = means[lab] + 0.3 * rng.standard_normal((60, d))
+    mid = np.zeros(60, np.uint8)
+    n = np.full((2, K), 10.0)
+    smu = np.stack([means * 10.0, means * 10.0])
+    ssig = np.full((2, K, d), 10.0 * 0.09)
+    pi, mu, var = O.gmm_params(O.GmmState.of(n, smu, ssig), 1e-6)
+    r = O.gmm_responsibilities(x, mid, pi, mu, var)
+    assert np.all(r.sum(axis=1) > 1 - 1e-12)
+    assert np.array_equal(r.argmax(axis=1), lab) and r.max(axis=1).min() > 1 - 1e-9
+
+
+def test_gmm_update_is_the_weighted_ema_of_batches():
+    # after several batches the state equals brute-force statistics with
+    # weights beta^age * r_jc (Chan's merge is exact for weighted data); the
+    # responsibilities come from the oracle's own E-step of each batch
+    rng = np.random.default_rng(34)
+    d, K, beta = 5, 2, 0.8
+    # from a zero state every component ties, so start from a seeded state
+    # (counted as pseudo-data with weight beta^B) and track it
+    n, smu, ssig = (a.astype(np.float64) for a in W.random_gmm_state(rng, d, K, count=5.0, spread=2.0))
+    st = O.GmmState.of(n, smu, ssig)
+    hist = []  # (x, mid, r) per batch
+    for b in range(5):
+        x = rng.standard_normal((30, d)) * 2.0 + b * 0.1
+        mid = (rng.random(30) < 0.5).astype(np.uint8)
+        pi, mu, var = O.gmm_params(st, 1e-9)
+        hist.append((x, mid, O.gmm_responsibilities(x, mid, pi, mu, var)))
+        st = O.gmm_update(st, x, mid, beta, 1e-9)
+    B = len(hist)
+    for m in (0, 1):
+        for c in range(K):
+            # seed state as pseudo-data: its N, mean and M2 with weight beta^B
+            wx = []
+            for t, (x, mid, r) in enumerate(hist):
+                sel = mid == m
+                wx.append((beta ** (B - 1 - t)) * r[sel, c])
+            Nb = beta ** B * n[m, c] + sum(w.sum() for w in wx)
+            assert abs(st.n[m, c] - Nb) <= 1e-10 * Nb
+            tot = beta ** B * smu[m, c] + sum((w[:, None] * hist[t][0][hist[t][1] == m]).sum(axis=0)
+                                              for t, w in enumerate(wx))
+            assert np.allclose(st.s_mu[m, c], tot, rtol=1e-10, atol=1e-10)
+            mean = tot / Nb
+            m2 = beta ** B * (ssig[m, c] + n[m, c] * (smu[m, c] / n[m, c] - mean) ** 2)
+            for t, w in enumerate(wx):
+                xs = hist[t][0][hist[t][1] == m]
+                m2 = m2 + (w[:, None] * (xs - mean) ** 2).sum(axis=0)
+            assert np.allclose(st.s_sig[m, c], m2, rtol=1e-9, atol=1e-9)
+
+
+def test_gmm_score_swaps_with_the_modalities():
+    rng = np.random.default_rng(35)
+    x, mid, st = _gmm_case(rng)
+    pi, mu, var = O.gmm_params(st, 1e-6)
+    M = O.gmm_modality_score(x, pi, mu, var, 2.0)
+    Ms = O.gmm_modality_score(x, pi[::-1], mu[::-1], var[::-1], 2.0)
+    assert np.allclose(M, Ms[:, ::-1], atol=1e-15)
+    assert np.allclose(M.sum(axis=1), 1.0, atol=1e-15)
