@@ -374,6 +374,48 @@ size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which);
 int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void* dst, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* GMM estimator: a K-component diagonal mixture per modality in place of   */
+/* the single Gaussian of Sec. 3.2.2 (supplementary GMM ablation).           */
+/* ------------------------------------------------------------------------ */
+
+#define SMOES_GMM_K_MAX 4
+
+size_t smoes_gmm_workspace_size(int64_t T, int d, int K);
+
+/*
+ * x            [T, d] activations (x_dtype).
+ * modality_id  [T] uint8 hard labels (0 vision, 1 text); needed when update
+ *              = 1 or resp != NULL.
+ * gmm_n        [2, K] float32 EMA counts N_mc (device, read/write).
+ * gmm_smu      [2, K, d] float32 S_mu per component (device, read/write).
+ * gmm_ssig     [2, K, d] float32 S_sigma2 per component (device, read/write).
+ *              Row m = 0 is vision, 1 text. Mixture weights are
+ *              pi_mc = N_mc / sum_c N_mc (uniform for a modality with no
+ *              count); a component with N = 0 has mu = 0, sigma^2 = 1. The
+ *              caller seeds the components apart (identical components stay
+ *              identical under EM).
+ * update       1: one stepwise-EM step first: responsibilities of each
+ *              token's own modality under the current parameters, then Eq.
+ *              5-7 per component with the responsibility-weighted batch
+ *              count, mean and centred sum of squares (decay beta); 0: score
+ *              only.
+ * tau          temperature of Eq. 9; <= 0 selects 0.5 * d.
+ * var_floor    lower bound of sigma^2 (>= 0).
+ * M            [T, 2] float32 output: Eq. 9 with LL_m the log of the
+ *              mixture density (2 pi constant dropped); rows sum to 1.
+ * resp         [T, K] float32 output or NULL: the responsibilities of the
+ *              E-step (parameters before the update).
+ * K = 1 is the single-Gaussian score of smoes_modality_score.
+ * Shapes: 1 <= K <= SMOES_GMM_K_MAX, 1 <= d <= SMOES_D_MAX, d % 8 == 0.
+ * Sums are float64 in a fixed order: results are reproducible.
+ */
+int smoes_gmm_modality_score(const void* x, int x_dtype, int64_t T, int d, int K,
+                             const uint8_t* modality_id, float* gmm_n, float* gmm_smu,
+                             float* gmm_ssig, int update, float beta, float tau, float var_floor,
+                             float* M, float* resp, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Attention-accumulated modality score (Sec. 3.2.1, Eq. 2-4).               */
 /* ------------------------------------------------------------------------ */
 

@@ -177,6 +177,32 @@ int smoes_binning(const float* probs, const int32_t* topk_idx, const uint8_t* mo
                                      msi, ws, as_stream(stream)));
 }
 
+// ------------------------------------------------------------------ GMM estimator
+
+size_t smoes_gmm_workspace_size(int64_t T, int d, int K) {
+    if (T < 0 || d < 1 || d > SMOES_D_MAX || (d % 8) != 0 || K < 1 || K > SMOES_GMM_K_MAX) return 0;
+    return gmm_workspace_bytes(T, d, K) + 2 * kAlign;
+}
+
+int smoes_gmm_modality_score(const void* x, int x_dtype, int64_t T, int d, int K, const uint8_t* modality_id,
+                             float* gmm_n, float* gmm_smu, float* gmm_ssig, int update, float beta, float tau,
+                             float var_floor, float* M, float* resp, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+    if (!dtype_ok(x_dtype)) return SMOES_ERR_ARG;
+    if (T < 0 || d < 1 || d > SMOES_D_MAX || (d % 8) != 0 || K < 1 || K > SMOES_GMM_K_MAX) return SMOES_ERR_SHAPE;
+    if (!(beta >= 0.0f && beta <= 1.0f) || !(var_floor >= 0.0f) || tau != tau) return SMOES_ERR_ARG;
+    if (update != 0 && update != 1) return SMOES_ERR_ARG;
+    if (T == 0) return SMOES_OK;
+    if (x == nullptr || gmm_n == nullptr || gmm_smu == nullptr || gmm_ssig == nullptr || M == nullptr)
+        return SMOES_ERR_ARG;
+    if ((update || resp != nullptr) && modality_id == nullptr) return SMOES_ERR_ARG;
+    if (workspace == nullptr || workspace_bytes < smoes_gmm_workspace_size(T, d, K)) return SMOES_ERR_WORKSPACE;
+    Carver c(workspace);
+    void* ws = c.take(gmm_workspace_bytes(T, d, K));
+    return hip_status(launch_gmm(x, x_dtype, T, d, K, modality_id, gmm_n, gmm_smu, gmm_ssig, update, beta, tau,
+                                 var_floor, M, resp, ws, as_stream(stream)));
+}
+
 // ------------------------------------------------------------------ attention-accumulated score
 
 int smoes_attn_score_init(const uint8_t* modality_id, int64_t T, float* M, void* stream) {

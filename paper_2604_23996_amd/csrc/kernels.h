@@ -89,6 +89,12 @@ hipError_t launch_binning(const float* probs, const int32_t* topk_idx, const uin
                           float* bal_loss, float* dlogits, int accumulate, float* msi, void* ws,
                           hipStream_t stream);
 
+// ---------------------------------------------------------------- GMM estimator
+size_t gmm_workspace_bytes(int64_t T, int d, int K);
+hipError_t launch_gmm(const void* x, int x_dtype, int64_t T, int d, int K, const uint8_t* modality_id, float* gmm_n,
+                      float* gmm_smu, float* gmm_ssig, int update, float beta, float tau, float var_floor, float* M,
+                      float* resp, void* ws, hipStream_t stream);
+
 // ---------------------------------------------------------------- attention-accumulated score
 hipError_t launch_attention(const void* q, const void* k, const void* v, int64_t T, int H, int Hkv, int head_dim,
                             const int32_t* sample_offsets, int n_batch, const float* m_in, float scale, void* o,

@@ -107,6 +107,12 @@ def lib() -> ctypes.CDLL:
         L.smoes_binning.argtypes = [c_void, c_void, c_void, c_i64, c_int, c_int, c_void, c_int, c_float, c_void,
                                     c_void, c_void, c_void, c_float, c_void, c_void, c_int, c_void, c_void,
                                     c_size, c_void]
+        L.smoes_gmm_workspace_size.restype = c_size
+        L.smoes_gmm_workspace_size.argtypes = [c_i64, c_int, c_int]
+        L.smoes_gmm_modality_score.restype = c_int
+        L.smoes_gmm_modality_score.argtypes = [c_void, c_int, c_i64, c_int, c_int, c_void, c_void, c_void, c_void,
+                                               c_int, c_float, c_float, c_float, c_void, c_void, c_void, c_size,
+                                               c_void]
         L.smoes_attn_score_init.restype = c_int
         L.smoes_attn_score_init.argtypes = [c_void, c_i64, c_void, c_void]
         L.smoes_attention_scores.restype = c_int
@@ -250,6 +256,24 @@ def binning(probs: torch.Tensor, topk_idx: torch.Tensor, modality_id: torch.Tens
                                _p(out["expert_to_bin_next"]), grad_scale, _p(out["bal_loss"]), _p(dlogits),
                                int(accumulate), _p(out["msi"]), _p(ws), ws.numel(), _stream()), "smoes_binning")
     return out
+
+
+def gmm_modality_score(x: torch.Tensor, gmm_n: torch.Tensor, gmm_smu: torch.Tensor, gmm_ssig: torch.Tensor,
+                       modality_id: Optional[torch.Tensor] = None, update: bool = False, beta: float = 0.99,
+                       tau: float = 0.0, var_floor: float = 1e-6, want_resp: bool = False):
+    """smoes_gmm_modality_score: scores M [T, 2] under the K-component mixtures
+    (state updated in place by one stepwise-EM step when update); returns
+    (M, resp or None)."""
+    T, d = x.shape
+    K = gmm_n.shape[1]
+    M = torch.empty((T, 2), dtype=torch.float32, device=x.device)
+    resp = torch.empty((T, K), dtype=torch.float32, device=x.device) if want_resp else None
+    nbytes = int(lib().smoes_gmm_workspace_size(T, d, K))
+    ws = _workspace(max(nbytes, 1), x.device)
+    _check(lib().smoes_gmm_modality_score(_p(x), _dtype_code(x), T, d, K, _p(modality_id), _p(gmm_n), _p(gmm_smu),
+                                          _p(gmm_ssig), int(update), beta, tau, var_floor, _p(M), _p(resp), _p(ws),
+                                          nbytes, _stream()), "smoes_gmm_modality_score")
+    return M, resp
 
 
 def attn_score_init(modality_id: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
