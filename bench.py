@@ -296,6 +296,43 @@ def main():
                                          "(added onto dlogits) + MSI, one layer, this step's routing",
                                  "ms": round(bin_ms, 5), "gbs": round(bin_bytes / (bin_ms * 1e-3) / 1e9, 1),
                                  "frac_hbm": round(bin_bytes / (bin_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}}
+    # GMM estimator (K = 2 components per modality, the supplementary GMM
+    # ablation's best setting): one stepwise-EM update on this batch, then the
+    # score. Timed on its own, not part of the layer step above.
+    K_gmm = 2
+    rng_g = np.random.default_rng(cfg.seed + 200)
+    gst = W.random_gmm_state(rng_g, cfg.d, K_gmm, count=1000.0, spread=0.05)
+    g_n, g_smu, g_ssig = (torch.from_numpy(a).to(dev) for a in gst)
+    g_M = torch.empty((cfg.T, 2), dtype=torch.float32, device=dev)
+    g_nb = int(S.lib().smoes_gmm_workspace_size(cfg.T, cfg.d, K_gmm))
+    g_ws = torch.empty(g_nb, dtype=torch.uint8, device=dev)
+    x_code = S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32
+
+    def gmm_call():
+        S._check(S.lib().smoes_gmm_modality_score(S._p(dev_in["x"]), x_code, cfg.T, cfg.d, K_gmm,
+                                                  S._p(dev_in["modality_id"]), S._p(g_n), S._p(g_smu), S._p(g_ssig),
+                                                  1, cfg.beta, cfg.tau, 1e-6, S._p(g_M), None, S._p(g_ws), g_nb,
+                                                  S._stream()), "smoes_gmm_modality_score")
+
+    for _ in range(3):
+        gmm_call()
+    g_times = []
+    for _ in range(args.steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        gmm_call()
+        e1.record()
+        torch.cuda.synchronize()
+        g_times.append(e0.elapsed_time(e1))
+    g_ms = float(np.median(g_times))
+    x_bytes = cfg.T * cfg.d * (2 if cfg.dtype == W.BF16 else 4)
+    g_bytes = 3 * x_bytes + 2 * 3 * K_gmm * cfg.d * 4 * 2  # x read by the E-step, the statistics and the score; state
+    line["extra"]["gmm_score"] = {
+        "what": f"GMM estimator, K={K_gmm} diagonal components per modality: E-step, stepwise-EM update of the "
+                "state, mixture-likelihood score (one layer)",
+        "ms": round(g_ms, 5), "tokens_per_s": round(cfg.T / (g_ms * 1e-3), 1),
+        "gbs": round(g_bytes / (g_ms * 1e-3) / 1e9, 1),
+        "frac_hbm": round(g_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     # Attention-accumulated score (Eq. 2-4) on the same token layout: causal
     # per-sample attention of a 16-head, d_head = 128 attention layer (the
     # backbone's hidden size 2048) with the scores as two extra value

@@ -11,7 +11,7 @@
 //     the score (Eq. 9 over the per-modality log-sum-exp) or the
 //     responsibilities of the token's own modality (the E-step).
 //  update (stepwise EM): gmm_partial sums r (x - shift), r (x - shift)^2 and r
-//     per chunk of 256 tokens in fp64 (shift = the component's previous mean),
+//     per chunk of 64 tokens in fp64 (shift = the component's previous mean),
 //     gmm_merge adds the chunks in order and applies Eq. 5-7 with the weighted
 //     batch count, mean and centred sum of squares.
 #include "common.h"
@@ -21,7 +21,7 @@ namespace smoes {
 
 namespace {
 
-constexpr int kGChunk = 256;        // tokens per gmm_partial block
+constexpr int kGChunk = 64;         // tokens per gmm_partial block
 constexpr int kGPartCols = 256;     // columns per gmm_partial block (64 lanes x 4)
 constexpr int kGPrepThreads = 256;  // columns per gmm_prep block
 constexpr int kGMaxParts = 64;      // SMOES_D_MAX / kGPrepThreads
@@ -233,6 +233,7 @@ gmm_partial_kernel(const void* __restrict__ x, int64_t T, int d, const uint8_t* 
     }
     const int64_t r0 = chunk * kGChunk;
     const int64_t r1 = r0 + kGChunk < T ? r0 + kGChunk : T;
+#pragma unroll 4
     for (int64_t r = r0 + wave; r < r1; r += 4) {
         if ((mid[r] ? 1 : 0) != m) continue;
         double w[K];
