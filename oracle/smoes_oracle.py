@@ -26,6 +26,9 @@ MoE-VLMs" (SMoES):
   * Suppl. GMM estimator: a K-component diagonal mixture per modality in place
                of the single Gaussian of Sec. 3.2.2 (mixture log-likelihood,
                Eq. 9 score, stepwise-EM update built on Eq. 5-7)
+  * backward   the layer's gradients for the training step of the
+               supplementary cost table: experts (dgrad and wgrad), combine
+               weights, softmax router with the auxiliary logit gradients added
 
 Readings where the paper is silent (each also listed in the design notes):
   R1  logarithms are natural (MI in nats);
@@ -81,6 +84,14 @@ Readings where the paper is silent (each also listed in the design notes):
       their responsibility-weighted forms. K = 1 is exactly Sec. 3.2.2.
       Components must be seeded apart by the caller (identical components
       stay identical under EM).
+  R20 Layer backward: the top-k choice is piecewise constant (no gradient);
+      the gradient reaches the router through the combine weights (the gate
+      values at the chosen experts, or their renormalised form) and the full
+      softmax; logit gradients of auxiliary losses (MI, bin balance) are
+      added to the router's logit gradient; the modality scores are constants
+      (R9). Given dL/d out, the outputs are dx, the router weight (and bias)
+      gradient, the total logit gradient, the combine-weight gradient and the
+      routed and shared expert weight gradients.
 
 Parity pins live in tests/test_oracle_pins.py; no part of this file is
 "parity unpinned" except the conventions R3-R5, R8, R11, R12, R14-R16 above,
@@ -750,3 +761,82 @@ def gmm_update(state: GmmState, x, modality_id, beta: float, var_floor: float) -
             s_mu_new[m, c] = beta * state.s_mu[m, c] + n * mu_T
             s_sig_new[m, c] = beta * state.s_sig[m, c] + Q + cross
     return GmmState(n_new, s_mu_new, s_sig_new)
+
+
+# ----------------------------------------------------------------------------
+# Layer backward (R20): the gradients of a loss through the layer output,
+# dL/d out given, with auxiliary logit gradients folded into the router.
+# ----------------------------------------------------------------------------
+
+def swiglu_backward(x, w13, w2, dy):
+    """For rows y = W2 (silu(a) * b), a = W1 x, b = W3 x, given dy: returns dx,
+    dW13 = [dW1; dW3] ([2I, d]) and dW2 ([d, I])."""
+    X = widen(x)
+    W13 = widen(w13)
+    W2 = widen(w2)
+    dY = np.asarray(dy, dtype=np.float64)
+    inter = W13.shape[0] // 2
+    a = X @ W13[:inter].T
+    b = X @ W13[inter:].T
+    sig = 1.0 / (1.0 + np.exp(-a))
+    sa = a * sig
+    h = sa * b
+    dh = dY @ W2
+    da = dh * b * (sig * (1.0 + a * (1.0 - sig)))  # d silu / da = sig (1 + a (1 - sig))
+    db = dh * sa
+    dx = da @ W13[:inter] + db @ W13[inter:]
+    return dx, np.concatenate([da.T @ X, db.T @ X]), dY.T @ h
+
+
+def layer_backward(x, w_gate, logit_bias, k: int, w13, w2, ws13, ws2, dout, dlogits_aux=None,
+                   renorm_topk: bool = False) -> Dict[str, np.ndarray]:
+    """Gradients of the layer (R20) given dout = dL/d out [T, d]:
+    dw [T, k] combine weights, dz [T, E] logits (with dlogits_aux added),
+    dw_gate [E, d], dbias [E], dw13 [E, 2I, d], dw2 [E, d, I], dws13, dws2 and
+    dx [T, d] (experts, shared experts and router)."""
+    X = widen(x)
+    Wg = widen(w_gate)
+    dO = np.asarray(dout, dtype=np.float64)
+    z, g, idx, w = route(x, w_gate, k, logit_bias, renorm_topk)
+    T, d = X.shape
+    E = Wg.shape[0]
+    counts, offsets, perm_token, inv = permutation(idx, E)
+    Y = np.zeros((T * k, d))
+    for e in range(E):
+        a, b = offsets[e], offsets[e + 1]
+        if b > a:
+            Y[a:b] = swiglu(X[perm_token[a:b]], w13[e], w2[e])
+    # combine: out_j = sum_s w_js Y[inv(j, s)] + shared_j
+    dw = np.stack([(dO * Y[inv[:, s]]).sum(axis=1) for s in range(k)], axis=1)
+    dY = np.zeros((T * k, d))
+    for s in range(k):
+        dY[inv[:, s]] = w[:, s:s + 1] * dO
+    # routed experts
+    dx = np.zeros((T, d))
+    dw13 = np.zeros(widen(w13).shape)
+    dw2 = np.zeros(widen(w2).shape)
+    for e in range(E):
+        a, b = offsets[e], offsets[e + 1]
+        if b > a:
+            dxe, dw13[e], dw2[e] = swiglu_backward(X[perm_token[a:b]], w13[e], w2[e], dY[a:b])
+            np.add.at(dx, perm_token[a:b], dxe)
+    dws13 = dws2 = None
+    if ws13 is not None:
+        dxs, dws13, dws2 = swiglu_backward(X, ws13, ws2, dO)
+        dx += dxs
+    # combine weights -> gates at the chosen experts -> full softmax -> logits
+    gsel = np.take_along_axis(g, idx.astype(np.int64), axis=1)
+    if renorm_topk:
+        S = gsel.sum(axis=1, keepdims=True)
+        dsel = (dw - (w * dw).sum(axis=1, keepdims=True)) / S
+    else:
+        dsel = dw
+    dg = np.zeros((T, E))
+    for s in range(k):
+        dg[np.arange(T), idx[:, s]] += dsel[:, s]
+    dz = g * (dg - (g * dg).sum(axis=1, keepdims=True))
+    if dlogits_aux is not None:
+        dz = dz + np.asarray(dlogits_aux, dtype=np.float64)
+    dx += dz @ Wg
+    return {"dw": dw, "dz": dz, "dw_gate": dz.T @ X, "dbias": dz.sum(axis=0), "dw13": dw13, "dw2": dw2,
+            "dws13": dws13, "dws2": dws2, "dx": dx}

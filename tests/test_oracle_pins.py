@@ -870,3 +870,93 @@ def test_gmm_score_swaps_with_the_modalities():
     Ms = O.gmm_modality_score(x, pi[::-1], mu[::-1], var[::-1], 2.0)
     assert np.allclose(M, Ms[:, ::-1], atol=1e-15)
     assert np.allclose(M.sum(axis=1), 1.0, atol=1e-15)
+
+
+# ---------------------------------------------------------------- layer backward (R20)
+
+def _torch_layer_grads(x, w_gate, bias, k, w13, w2, ws13, ws2, dout, aux, renorm):
+    """Reference gradients by torch autograd (float64) of an independent torch
+    forward: the loss <dout, out> + <aux, z>."""
+    tt = lambda a: torch.tensor(np.asarray(a, dtype=np.float64), requires_grad=True)
+    X, Wg, B = tt(x), tt(w_gate), tt(bias)
+    W13, W2, S13, S2 = tt(w13), tt(w2), tt(ws13), tt(ws2)
+    z = X @ Wg.T + B
+    g = torch.softmax(z, dim=1)
+    top = torch.topk(z, k, dim=1).indices
+    wsel = torch.gather(g, 1, top)
+    if renorm:
+        wsel = wsel / wsel.sum(dim=1, keepdim=True)
+    inter = W13.shape[1] // 2
+    out = torch.zeros_like(X)
+    for s in range(k):
+        e = top[:, s]
+        a = torch.einsum("td,tid->ti", X, W13[e, :inter])
+        u = torch.einsum("td,tid->ti", X, W13[e, inter:])
+        y = torch.einsum("ti,tdi->td", torch.nn.functional.silu(a) * u, W2[e])
+        out = out + wsel[:, s:s + 1] * y
+    inter_s = S13.shape[0] // 2
+    out = out + (torch.nn.functional.silu(X @ S13[:inter_s].T) * (X @ S13[inter_s:].T)) @ S2.T
+    loss = (out * torch.tensor(dout)).sum() + (z * torch.tensor(aux)).sum()
+    loss.backward()
+    return {"dx": X.grad.numpy(), "dw_gate": Wg.grad.numpy(), "dbias": B.grad.numpy(), "dw13": W13.grad.numpy(),
+            "dw2": W2.grad.numpy(), "dws13": S13.grad.numpy(), "dws2": S2.grad.numpy()}
+
+
+@pytest.mark.parametrize("renorm", [False, True])
+def test_layer_backward_matches_torch_autograd(renorm):
+    rng = np.random.default_rng(70)
+    T, d, E, k, I = 23, 12, 6, 2, 8
+    x = rng.standard_normal((T, d))
+    wg = rng.standard_normal((E, d)) * 0.5
+    bias = rng.standard_normal(E) * 0.3
+    w13 = rng.standard_normal((E, 2 * I, d)) * 0.3
+    w2 = rng.standard_normal((E, d, I)) * 0.3
+    ws13 = rng.standard_normal((2 * I, d)) * 0.3
+    ws2 = rng.standard_normal((d, I)) * 0.3
+    dout = rng.standard_normal((T, d))
+    aux = rng.standard_normal((T, E)) * 0.1
+    got = O.layer_backward(x, wg, bias, k, w13, w2, ws13, ws2, dout, aux, renorm)
+    ref = _torch_layer_grads(x, wg, bias, k, w13, w2, ws13, ws2, dout, aux, renorm)
+    for key in ref:
+        assert np.allclose(got[key], ref[key], rtol=1e-10, atol=1e-10), key
+
+
+def test_layer_backward_finite_differences_of_the_combine_weights():
+    # dw is the derivative of <dout, out> with respect to the combine weights
+    rng = np.random.default_rng(71)
+    T, d, E, k, I = 7, 6, 4, 2, 4
+    x = rng.standard_normal((T, d))
+    wg = rng.standard_normal((E, d))
+    w13 = rng.standard_normal((E, 2 * I, d)) * 0.4
+    w2 = rng.standard_normal((E, d, I)) * 0.4
+    dout = rng.standard_normal((T, d))
+    got = O.layer_backward(x, wg, None, k, w13, w2, None, None, dout)
+    _, _, idx, w = O.route(x, wg, k)
+    eps = 1e-6
+    for j in range(T):
+        for s in range(k):
+            wp, wm = w.copy(), w.copy()
+            wp[j, s] += eps
+            wm[j, s] -= eps
+            fp = (O.experts_grouped(x, idx, wp, w13, w2, E=E)[0] * dout).sum()
+            fm = (O.experts_grouped(x, idx, wm, w13, w2, E=E)[0] * dout).sum()
+            assert abs((fp - fm) / (2 * eps) - got["dw"][j, s]) < 1e-6
+
+
+def test_swiglu_backward_finite_differences():
+    rng = np.random.default_rng(72)
+    x = rng.standard_normal((3, 5))
+    w13 = rng.standard_normal((8, 5)) * 0.5
+    w2 = rng.standard_normal((5, 4)) * 0.5
+    dy = rng.standard_normal((3, 5))
+    dx, dw13, dw2 = O.swiglu_backward(x, w13, w2, dy)
+    f = lambda xx, a, b: (O.swiglu(xx, a, b) * dy).sum()
+    eps = 1e-6
+    for (arr, grad) in ((x, dx), (w13, dw13), (w2, dw2)):
+        for i in range(arr.size):
+            p_, m_ = arr.copy(), arr.copy()
+            p_.flat[i] += eps
+            m_.flat[i] -= eps
+            args_p = [p_ if arr is q else q for q in (x, w13, w2)]
+            args_m = [m_ if arr is q else q for q in (x, w13, w2)]
+            assert abs((f(*args_p) - f(*args_m)) / (2 * eps) - grad.flat[i]) < 1e-6
