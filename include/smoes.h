@@ -344,7 +344,11 @@ int smoes_moe_forward(const smoes_layer* desc, const smoes_layer_io* io,
 /* ------------------------------------------------------------------------ */
 
 /* Which expert weight tensor (shapes as in smoes_layer_io). */
-enum smoes_weight { SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3, SMOES_WGATE = 4 };
+enum smoes_weight {
+    SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3, SMOES_WGATE = 4,
+    /* transposed forms read by smoes_moe_backward */
+    SMOES_W13T = 5, SMOES_W2T = 6, SMOES_WS13T = 7, SMOES_WS2T = 8
+};
 
 /*
  * Layout: a matrix W[N][K] (N output rows, K the contraction) becomes
@@ -359,6 +363,10 @@ enum smoes_weight { SMOES_W13 = 0, SMOES_W2 = 1, SMOES_WS13 = 2, SMOES_WS2 = 3, 
  * ceil(E/16) groups of ceil(d/32) slices of 64 x 8 bf16,
  *   P[p][g][c][l][e] = term p of w_gate[16g + l%16][32c + 8(l/16) + e],
  * zero outside w_gate: the operand order of the 16x16x32 matrix instructions.
+ * SMOES_W13T / SMOES_WS13T: W = the transpose of w13[e] / ws13 (N = d,
+ * K = 2 inter, gate rows then up rows along K, no interleave);
+ * SMOES_W2T / SMOES_WS2T: W = the transpose of w2[e] / ws2 (N = inter,
+ * K = d). `src` is the same row-major tensor as for SMOES_W13 / SMOES_W2.
  * Returns the byte size of the packed tensor, 0 for an invalid desc or
  * `which` (ws13/ws2 need shared_inter > 0).
  */
@@ -372,6 +380,55 @@ size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which);
  * as smoes_workspace_bytes.
  */
 int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void* dst, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Layer backward (the training step of the supplementary cost table).      */
+/* ------------------------------------------------------------------------ */
+
+/* Gradients written by smoes_moe_backward (device pointers). */
+typedef struct smoes_layer_grads {
+    float* dx;       /* [T, d] float32: experts, shared experts and router       */
+    float* dw_gate;  /* [E, d] float32 router weight gradient                    */
+    float* dbias;    /* [E] float32 logit bias gradient, or NULL                 */
+    float* dz;       /* [T, E] float32 total logit gradient (with dlogits_aux)   */
+    float* dw;       /* [T, k] float32 combine-weight gradient, or NULL          */
+    void* dw13;      /* [E, 2 inter, d] bf16 (gate rows then up rows, as w13)    */
+    void* dw2;       /* [E, d, inter] bf16                                       */
+    void* dws13;     /* [2 shared_inter, d] bf16 (needed when shared_inter > 0)  */
+    void* dws2;      /* [d, shared_inter] bf16                                   */
+} smoes_layer_grads;
+
+size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
+
+/*
+ * Gradients of a loss L through the layer output, given dout = dL/d out
+ * ([T, d] bf16), after smoes_moe_forward ran with the same desc, io and
+ * forward workspace (whose expert buffers, H and Y, and work tables must be
+ * intact). The top-k choice carries no gradient; the gradient reaches the
+ * router through the combine weights (the gate values at the chosen experts,
+ * or their renormalised form) and the full softmax; dlogits_aux ([T, E]
+ * float32, e.g. io->dlogits of the MI loss, plus the bin balance gradient),
+ * when not NULL, is added to the logit gradient; the modality scores are
+ * constants. The experts' gate and up pre-activations are recomputed.
+ * Reads from io: x, w13 and ws13 (packed), w_gate (float32 row-major),
+ * probs, topk_idx, topk_w, and expert_offsets / perm_token / perm_inv (or
+ * the forward workspace's copies when those are NULL).
+ * w13t, w2t, ws13t, ws2t: the transposed packed weights (SMOES_W13T, ...).
+ * Implemented for bf16 layers with packed weights (SMOES_ERR_ARG otherwise).
+ * SMOES_ERR_SHAPE when 4 T k inter or 4 T shared_inter exceeds INT32_MAX
+ * bytes; SMOES_ERR_WORKSPACE when either workspace is NULL or smaller than
+ * smoes_workspace_bytes / smoes_backward_workspace_bytes; SMOES_ERR_ARG for
+ * a NULL pointer that is needed. Differentiates the layer output of Sec. 3.1
+ * (softmax router, top-k combine, SwiGLU experts plus the shared experts).
+ * bf16 operands with float32 accumulation; the expert weight gradients are
+ * bf16, dx, dw_gate and the logit gradient float32. Sums run in a fixed
+ * order: results are reproducible. Asynchronous on `stream`; nothing is
+ * allocated.
+ */
+int smoes_moe_backward(const smoes_layer* desc, const smoes_layer_io* io, const void* w13t, const void* w2t,
+                       const void* ws13t, const void* ws2t, const void* dout, const float* dlogits_aux,
+                       const smoes_layer_grads* grads, void* fwd_workspace, size_t fwd_workspace_bytes,
+                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* GMM estimator: a K-component diagonal mixture per modality in place of   */

@@ -459,15 +459,156 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     return SMOES_OK;
 }
 
+// ------------------------------------------------------------------ layer backward
+
+namespace {
+struct BwdWs {
+    void* ab_r;
+    void* ab_s;
+    void* dab_r;
+    void* dab_s;
+    void* dx_r;
+    void* dx_s;
+    float* wrow;
+    int32_t* work4;
+    void* router;
+};
+size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
+    Carver c(base);
+    const int64_t T = L->T, R = L->T * L->k;
+    BwdWs w;
+    w.ab_r = c.take(sizeof(uint16_t) * R * 2 * L->inter);
+    w.ab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
+    w.dab_r = c.take(sizeof(uint16_t) * R * 2 * L->inter);
+    w.dab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
+    w.dx_r = c.take(sizeof(uint16_t) * R * L->d);
+    w.dx_s = c.take(sizeof(uint16_t) * T * L->d);
+    w.wrow = static_cast<float*>(c.take(sizeof(float) * R));
+    w.work4 = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 2)));
+    w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E));
+    if (out != nullptr) *out = w;
+    return c.used + kAlign;
+}
+}  // namespace
+
+size_t smoes_backward_workspace_bytes(const smoes_layer* desc) {
+    if (check_layer(desc) != SMOES_OK) return 0;
+    return bwd_ws_parts(desc, nullptr, reinterpret_cast<void*>(static_cast<uintptr_t>(kAlign)));
+}
+
+int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const void* w13t, const void* w2t,
+                       const void* ws13t, const void* ws2t, const void* dout, const float* dlogits_aux,
+                       const smoes_layer_grads* G, void* fwd_workspace, size_t fwd_workspace_bytes,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    int st = check_layer(L);
+    if (st != SMOES_OK) return st;
+    if (io == nullptr || G == nullptr) return SMOES_ERR_ARG;
+    if (L->act_dtype != SMOES_BF16 || !L->weights_packed) return SMOES_ERR_ARG;
+    // dX = [dA dB] W13 reads its A operand (2 inter columns per row) through a
+    // buffer descriptor with 32-bit byte offsets
+    if (2 * L->T * L->k * 2 * static_cast<int64_t>(L->inter) > INT32_MAX ||
+        2 * L->T * 2 * static_cast<int64_t>(L->shared_inter) > INT32_MAX)
+        return SMOES_ERR_SHAPE;
+    if (L->T == 0) return SMOES_OK;
+    const bool sh = L->shared_inter > 0;
+    if (io->x == nullptr || io->w13 == nullptr || io->w_gate == nullptr || io->probs == nullptr ||
+        io->topk_idx == nullptr || io->topk_w == nullptr || w13t == nullptr || w2t == nullptr || dout == nullptr ||
+        G->dx == nullptr || G->dw_gate == nullptr || G->dz == nullptr || G->dw13 == nullptr || G->dw2 == nullptr)
+        return SMOES_ERR_ARG;
+    if (sh && (io->ws13 == nullptr || ws13t == nullptr || ws2t == nullptr || G->dws13 == nullptr ||
+               G->dws2 == nullptr))
+        return SMOES_ERR_ARG;
+    if (fwd_workspace == nullptr || fwd_workspace_bytes < smoes_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
+    if (workspace == nullptr || workspace_bytes < smoes_backward_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    LayerWs fw;
+    layer_ws_parts(L, &fw, fwd_workspace);
+    BwdWs bw;
+    bwd_ws_parts(L, &bw, workspace);
+    const int64_t T = L->T;
+    const int32_t* offsets = io->expert_offsets != nullptr ? io->expert_offsets : fw.offsets;
+    const int32_t* perm_token = io->perm_token != nullptr ? io->perm_token : fw.perm_token;
+    const int32_t* perm_inv = io->perm_inv != nullptr ? io->perm_inv : fw.perm_inv;
+    ExpertArgs a;
+    a.T = T;
+    a.d = L->d;
+    a.E = L->E;
+    a.k = L->k;
+    a.inter = L->inter;
+    a.shared_inter = L->shared_inter;
+    a.act_dtype = L->act_dtype;
+    a.packed = 1;
+    a.x = io->x;
+    a.w13 = io->w13;
+    a.w2 = io->w2;
+    a.ws13 = io->ws13;
+    a.ws2 = io->ws2;
+    a.expert_offsets = offsets;
+    a.perm_token = perm_token;
+    a.perm_inv = perm_inv;
+    a.topk_w = io->topk_w;
+    a.out = nullptr;
+    const ExpertFwdBuffers fb = experts_fwd_buffers(a, fw.experts);
+    BwdGemmPtrs bp;
+    bp.dout = dout;
+    bp.w2t = w2t;
+    bp.ws2t = ws2t;
+    bp.w13t = w13t;
+    bp.ws13t = ws13t;
+    bp.ab_r = bw.ab_r;
+    bp.ab_s = bw.ab_s;
+    bp.dab_r = bw.dab_r;
+    bp.dab_s = bw.dab_s;
+    bp.dx_r = bw.dx_r;
+    bp.dx_s = bw.dx_s;
+    bp.wrow = bw.wrow;
+    bp.work4 = bw.work4;
+    hipError_t err;
+#define SMOES_BTRY(expr)                                        \
+    do {                                                        \
+        if ((err = (expr)) != hipSuccess) return SMOES_ERR_HIP; \
+    } while (0)
+    SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
+    SMOES_BTRY(launch_router_bwd(dout, fb.y_r, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T, L->d,
+                                 L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, s));
+    for (int mode = 3; mode <= 5; ++mode) {
+        SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 1, s));
+        if (sh) SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 2, s));
+    }
+    SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
+                                G->dx, s));
+    const int I = L->inter, SI = L->shared_inter, d = L->d;
+    SMOES_BTRY(launch_wgrad(T, L->E, d, I, offsets, dout, d, perm_token, bw.wrow, fb.h_r, I, nullptr, G->dw2, s));
+    SMOES_BTRY(launch_wgrad(T, L->E, 2 * I, d, offsets, bw.dab_r, 2 * I, nullptr, nullptr, io->x, d, perm_token,
+                            G->dw13, s));
+    if (sh) {
+        SMOES_BTRY(launch_wgrad(T, 1, d, SI, nullptr, dout, d, nullptr, nullptr, fb.h_s, SI, nullptr, G->dws2, s));
+        SMOES_BTRY(launch_wgrad(T, 1, 2 * SI, d, nullptr, bw.dab_s, 2 * SI, nullptr, nullptr, io->x, d, nullptr,
+                                G->dws13, s));
+    }
+    SMOES_BTRY(launch_dwgate(G->dz, io->x, T, d, L->E, G->dw_gate, G->dbias, bw.router, s));
+#undef SMOES_BTRY
+    return SMOES_OK;
+}
+
 namespace {
 // batch, rows n, contraction k and gate/up interleave of each packed tensor; false if invalid
-bool weight_dims(const smoes_layer* L, int which, int* batch, int* n, int* k, int* interleave) {
+bool weight_dims(const smoes_layer* L, int which, int* batch, int* n, int* k, int* interleave, int* transpose) {
+    *transpose = 0;
     switch (which) {
         case SMOES_W13: *batch = L->E; *n = L->inter; *k = L->d; *interleave = 1; return true;
         case SMOES_W2: *batch = L->E; *n = L->d; *k = L->inter; *interleave = 0; return true;
         case SMOES_WS13: *batch = 1; *n = L->shared_inter; *k = L->d; *interleave = 1; return L->shared_inter > 0;
         case SMOES_WS2: *batch = 1; *n = L->d; *k = L->shared_inter; *interleave = 0; return L->shared_inter > 0;
         case SMOES_WGATE: *batch = 1; *n = L->E; *k = L->d; *interleave = 0; return true;
+        case SMOES_W13T: *batch = L->E; *n = L->d; *k = 2 * L->inter; *interleave = 0; *transpose = 1; return true;
+        case SMOES_W2T: *batch = L->E; *n = L->inter; *k = L->d; *interleave = 0; *transpose = 1; return true;
+        case SMOES_WS13T:
+            *batch = 1; *n = L->d; *k = 2 * L->shared_inter; *interleave = 0; *transpose = 1;
+            return L->shared_inter > 0;
+        case SMOES_WS2T:
+            *batch = 1; *n = L->shared_inter; *k = L->d; *interleave = 0; *transpose = 1;
+            return L->shared_inter > 0;
         default: return false;
     }
 }
@@ -475,8 +616,8 @@ bool weight_dims(const smoes_layer* L, int which, int* batch, int* n, int* k, in
 
 size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which) {
     if (check_layer(desc) != SMOES_OK) return 0;
-    int batch, n, k, il;
-    if (!weight_dims(desc, which, &batch, &n, &k, &il)) return 0;
+    int batch, n, k, il, tr;
+    if (!weight_dims(desc, which, &batch, &n, &k, &il, &tr)) return 0;
     if (which == SMOES_WGATE) return router_packed_elems(desc->d, desc->E) * 2;
     return static_cast<size_t>(packed_weight_elems(batch, n, k, il)) * 2;
 }
@@ -484,13 +625,13 @@ size_t smoes_packed_weight_bytes(const smoes_layer* desc, int which) {
 int smoes_pack_weights(const smoes_layer* desc, int which, const void* src, void* dst, void* stream) {
     const int st = check_layer(desc);
     if (st != SMOES_OK) return st;
-    int batch, n, k, il;
-    if (desc->act_dtype != SMOES_BF16 || !weight_dims(desc, which, &batch, &n, &k, &il) || src == nullptr ||
+    int batch, n, k, il, tr;
+    if (desc->act_dtype != SMOES_BF16 || !weight_dims(desc, which, &batch, &n, &k, &il, &tr) || src == nullptr ||
         dst == nullptr)
         return SMOES_ERR_ARG;
     const hipError_t err = which == SMOES_WGATE
                                ? launch_split_wgate(static_cast<const float*>(src), desc->E, desc->d, dst, as_stream(stream))
-                               : launch_pack_weights(src, batch, n, k, il, dst, as_stream(stream));
+                               : launch_pack_weights(src, batch, n, k, il, tr, dst, as_stream(stream));
     return err == hipSuccess ? SMOES_OK : SMOES_ERR_HIP;
 }
 

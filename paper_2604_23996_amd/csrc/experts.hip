@@ -172,6 +172,19 @@ struct GemmArgs {
     void* h_s;
     void* y_r;
     void* y_s;
+    // backward (modes 3-5 of the packed kernel)
+    const void* dout;   // [T][d] upstream gradient
+    const void* w2t;    // packed W2^T per expert (N = inter, K = d)
+    const void* ws2t;   // packed Ws2^T (N = shared_inter, K = d)
+    const void* w13t;   // packed W13^T per expert (N = d, K = 2 inter)
+    const void* ws13t;  // packed Ws13^T (N = d, K = 2 shared_inter)
+    void* ab_r;         // [R][2 inter] pre-activations (gate | up), routed rows
+    void* ab_s;         // [T][2 shared_inter]
+    void* dab_r;        // [R][2 inter] their gradients
+    void* dab_s;        // [T][2 shared_inter]
+    void* dx_r;         // [R][d] input gradient of each routed row
+    void* dx_s;         // [T][d] shared experts' input gradient
+    const float* wrow;  // [R] combine weight of each routed row
 };
 
 // ============================================================== bf16 MFMA path
@@ -450,10 +463,17 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 //   GEMM2: 256 output columns per tile (64 per wave).
 constexpr int PK_BM = 128, PK_BK = 64, PK_WAVES = 4, PK_THREADS = PK_WAVES * 64, PK_ST = 3;
 constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instructions per wave per stage
-constexpr int pk_tile_cols(int mode) { return mode == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
+// Modes: 1 GEMM1 (+ SwiGLU), 2 GEMM2, and for the backward 3 GEMM1 with the
+// raw gate and up outputs, 4 dH = dout W2 (rows gathered, scaled by the combine
+// weight) with the SwiGLU backward in the epilogue, 5 dX = [dA dB] W13. Modes
+// 1 and 3 pair gate and up groups (32 H columns per wave); 2, 4 and 5 give each
+// wave two consecutive 32-column groups.
+constexpr int pk_family(int mode) { return (mode == 1 || mode == 3) ? 1 : 2; }
+constexpr int pk_tile_cols(int mode) { return pk_family(mode) == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
+constexpr int pk_out_cols(int mode) { return mode == 3 ? 2 * pk_tile_cols(mode) : pk_tile_cols(mode); }
 constexpr int pk_lds_bytes(int mode) {
-    return PK_ST * PK_BM * PK_BK * 2 > PK_BM * (pk_tile_cols(mode) + 8) * 2 ? PK_ST * PK_BM * PK_BK * 2
-                                                                             : PK_BM * (pk_tile_cols(mode) + 8) * 2;
+    return PK_ST * PK_BM * PK_BK * 2 > PK_BM * (pk_out_cols(mode) + 8) * 2 ? PK_ST * PK_BM * PK_BK * 2
+                                                                            : PK_BM * (pk_out_cols(mode) + 8) * 2;
 }
 
 // Elements of one packed matrix with n rows (n_groups = ceil(n / 32) groups) and contraction k.
@@ -480,8 +500,9 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     constexpr int A_BYTES = BM * BK * 2;
     constexpr int TC = pk_tile_cols(MODE);
     __shared__ __attribute__((aligned(1024))) uint8_t lds[pk_lds_bytes(MODE)];
-    const int nt_r = static_cast<int>(ceil_div(MODE == 1 ? p.inter : p.d, TC));
-    const int nt_s = MODE == 1 ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
+    constexpr int FAM = pk_family(MODE);
+    const int nt_r = static_cast<int>(ceil_div((MODE == 1 || MODE == 3 || MODE == 4) ? p.inter : p.d, TC));
+    const int nt_s = (MODE == 1 || MODE == 3 || MODE == 4) ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
     if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, p.part, t)) return;
     const bool shared = t.g == p.E;
@@ -492,7 +513,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     int64_t a_rows;
     const uint16_t* Bw;  // this wave's first packed group
     int b_groups;        // packed groups of this wave that hold weights (0..2)
-    if constexpr (MODE == 1) {
+    if constexpr (FAM == 1) {
         K = p.d;
         n_out = shared ? p.shared_inter : p.inter;
         Abase = static_cast<const uint16_t*>(p.x);
@@ -504,13 +525,32 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         b_groups = 2 * q < ng ? 2 : 0;
         Bw = W + packed_elems(b_groups ? 2 * q : 0, K);
     } else {
-        K = shared ? p.shared_inter : p.inter;
-        n_out = p.d;
-        Abase = shared ? static_cast<const uint16_t*>(p.h_s) : static_cast<const uint16_t*>(p.h_r);
-        a_rows = shared ? p.T : p.T * p.k;
-        const int ng = static_cast<int>(ceil_div(p.d, 32));
-        const uint16_t* W = shared ? static_cast<const uint16_t*>(p.ws2)
-                                   : static_cast<const uint16_t*>(p.w2) + t.g * packed_elems(ng, K);
+        const uint16_t* Wr;
+        const uint16_t* Ws;
+        if constexpr (MODE == 4) {  // dH = dout W2: rows of dout, contraction over d
+            K = p.d;
+            n_out = shared ? p.shared_inter : p.inter;
+            Abase = static_cast<const uint16_t*>(p.dout);
+            a_rows = p.T;
+            Wr = static_cast<const uint16_t*>(p.w2t);
+            Ws = static_cast<const uint16_t*>(p.ws2t);
+        } else if constexpr (MODE == 5) {  // dX = [dA dB] W13: contraction over 2 inter
+            K = 2 * (shared ? p.shared_inter : p.inter);
+            n_out = p.d;
+            Abase = shared ? static_cast<const uint16_t*>(p.dab_s) : static_cast<const uint16_t*>(p.dab_r);
+            a_rows = shared ? p.T : p.T * p.k;
+            Wr = static_cast<const uint16_t*>(p.w13t);
+            Ws = static_cast<const uint16_t*>(p.ws13t);
+        } else {
+            K = shared ? p.shared_inter : p.inter;
+            n_out = p.d;
+            Abase = shared ? static_cast<const uint16_t*>(p.h_s) : static_cast<const uint16_t*>(p.h_r);
+            a_rows = shared ? p.T : p.T * p.k;
+            Wr = static_cast<const uint16_t*>(p.w2);
+            Ws = static_cast<const uint16_t*>(p.ws2);
+        }
+        const int ng = static_cast<int>(ceil_div(n_out, 32));
+        const uint16_t* W = shared ? Ws : Wr + t.g * packed_elems(ng, K);
         const int g0 = t.nt * (2 * PK_WAVES) + 2 * wave;
         b_groups = ng - g0 >= 2 ? 2 : (ng - g0 > 0 ? ng - g0 : 0);
         Bw = W + packed_elems(b_groups ? g0 : 0, K);
@@ -533,7 +573,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         const int R = (wave * IA + q) * 8 + lane / 8;
         const int rr = R < t.rows ? R : 0;
         int src;
-        if (MODE == 1 && !shared) src = p.perm_token[t.row0 + rr];
+        if ((MODE == 1 || MODE == 3 || MODE == 4) && !shared) src = p.perm_token[t.row0 + rr];
         else src = static_cast<int>(t.row0 + rr);
         aoff[q] = R < t.rows ? static_cast<uint32_t>(src) * static_cast<uint32_t>(K) : (1u << 30);
         achk[q] = ((lane % 8) ^ ((R / 2) % 8)) * 8;
@@ -659,12 +699,52 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     // The accumulators hold transposed 32x32 tiles: element v of lane l is
     // output column 8*(v/4) + 4*half + v%4 of token row l32, so each lane
     // writes four adjacent columns as one 8-byte store.
-    constexpr int OP = TC + 8;
-    uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
     auto pack4 = [](float a, float b, float c, float d) {
         return make_uint2(static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16),
                           static_cast<uint32_t>(f32_to_bf16(c)) | (static_cast<uint32_t>(f32_to_bf16(d)) << 16));
     };
+    if constexpr (MODE == 4) {
+        // dH = w * (dout W2) and the SwiGLU backward with the saved gate (a) and
+        // up (b) pre-activations: dA = dH b silu'(a), dB = dH silu(a); each lane
+        // reads and writes its four adjacent columns directly.
+        const uint16_t* AB = static_cast<const uint16_t*>(shared ? p.ab_s : p.ab_r);
+        uint16_t* dAB = static_cast<uint16_t*>(shared ? p.dab_s : p.dab_r);
+        const int64_t ld = 2 * static_cast<int64_t>(n_out);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = i * 32 + l32;
+            if (r >= t.rows) continue;
+            const int64_t row = t.row0 + r;
+            const float w = shared ? 1.0f : p.wrow[row];
+#pragma unroll
+            for (int g = 0; g < 2; ++g)
+#pragma unroll
+                for (int vq = 0; vq < 4; ++vq) {
+                    const int col = t.nt * TC + wave * 64 + g * 32 + 8 * vq + 4 * half;
+                    if (col >= n_out) continue;  // n_out % 4 == 0: four columns are all in or all out
+                    const uint2 av = *reinterpret_cast<const uint2*>(AB + row * ld + col);
+                    const uint2 bv = *reinterpret_cast<const uint2*>(AB + row * ld + n_out + col);
+                    const float a[4] = {__uint_as_float(av.x << 16), __uint_as_float(av.x & 0xffff0000u),
+                                        __uint_as_float(av.y << 16), __uint_as_float(av.y & 0xffff0000u)};
+                    const float b[4] = {__uint_as_float(bv.x << 16), __uint_as_float(bv.x & 0xffff0000u),
+                                        __uint_as_float(bv.y << 16), __uint_as_float(bv.y & 0xffff0000u)};
+                    float da[4], db[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float dh = w * acc[i][g][4 * vq + e];
+                        const float sg = 1.0f / (1.0f + __expf(-a[e]));
+                        da[e] = dh * b[e] * (sg * (1.0f + a[e] * (1.0f - sg)));
+                        db[e] = dh * a[e] * sg;
+                    }
+                    *reinterpret_cast<uint2*>(dAB + row * ld + col) = pack4(da[0], da[1], da[2], da[3]);
+                    *reinterpret_cast<uint2*>(dAB + row * ld + n_out + col) = pack4(db[0], db[1], db[2], db[3]);
+                }
+        }
+        return;
+    }
+    constexpr int OC = pk_out_cols(MODE);  // tile columns written (mode 3: gate block then up block)
+    constexpr int OP = OC + 8;
+    uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = i * 32 + l32;
@@ -676,6 +756,11 @@ gemm_bf16_pk_kernel(GemmArgs p) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) h[e] = silu(acc[i][0][4 * vq + e]) * acc[i][1][4 * vq + e];
                 *reinterpret_cast<uint2*>(otile + r * OP + wave * 32 + c0) = pack4(h[0], h[1], h[2], h[3]);
+            } else if constexpr (MODE == 3) {
+#pragma unroll
+                for (int g = 0; g < 2; ++g)
+                    *reinterpret_cast<uint2*>(otile + r * OP + g * TC + wave * 32 + c0) =
+                        pack4(acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
             } else {
 #pragma unroll
                 for (int g = 0; g < 2; ++g)
@@ -687,24 +772,35 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     __syncthreads();
     uint16_t* O;
     if constexpr (MODE == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
+    else if constexpr (MODE == 3) O = shared ? static_cast<uint16_t*>(p.ab_s) : static_cast<uint16_t*>(p.ab_r);
+    else if constexpr (MODE == 5) O = shared ? static_cast<uint16_t*>(p.dx_s) : static_cast<uint16_t*>(p.dx_r);
     else O = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
-    constexpr int CH = TC / 8;
+    constexpr int CH = OC / 8;
     const int col0 = t.nt * TC;
     for (int q = threadIdx.x; q < BM * CH; q += PK_THREADS) {
         const int r = q / CH, ch = q % CH;
-        const int c = col0 + ch * 8;
-        if (r < t.rows && c < n_out)  // n_out % 8 == 0: a chunk is all in or all out
-            *reinterpret_cast<uint4*>(O + (t.row0 + r) * n_out + c) =
-                *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+        if constexpr (MODE == 3) {  // gate block to columns [0, n_out), up block to [n_out, 2 n_out)
+            const int part = (ch * 8) / TC;
+            const int c = col0 + ch * 8 - part * TC;
+            if (r < t.rows && c < n_out)
+                *reinterpret_cast<uint4*>(O + (t.row0 + r) * (2 * static_cast<int64_t>(n_out)) + part * n_out + c) =
+                    *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+        } else {
+            const int c = col0 + ch * 8;
+            if (r < t.rows && c < n_out)  // n_out % 8 == 0: a chunk is all in or all out
+                *reinterpret_cast<uint4*>(O + (t.row0 + r) * n_out + c) =
+                    *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+        }
     }
 }
 
 // Pack `batch` row-major matrices into the fragment order above. interleave:
 // the source has 2 * n rows (gate rows then up rows) and packed group 2q + h
-// takes rows 32q.. of half h; otherwise the source has n rows. One thread per
-// 16-byte fragment; k % 8 == 0.
+// takes rows 32q.. of half h; otherwise the source has n rows. transpose: the
+// source is stored [k][n] (the packed matrix is its transpose). One thread
+// per 16-byte fragment; k % 8 == 0.
 __global__ void pack_weights_kernel(const uint16_t* __restrict__ src, int batch, int n, int k, int interleave,
-                                    uint16_t* __restrict__ dst) {
+                                    int transpose, uint16_t* __restrict__ dst) {
     const int ng = interleave ? 2 * static_cast<int>(ceil_div(n, 32)) : static_cast<int>(ceil_div(n, 32));
     const int kc_n = (k + 15) / 16;
     const int64_t per = static_cast<int64_t>(ng) * kc_n * 64;  // fragments per matrix
@@ -731,7 +827,15 @@ __global__ void pack_weights_kernel(const uint16_t* __restrict__ src, int batch,
         const int kk = c * 16 + 8 * (l / 32);
         ok = ok && kk < k;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (ok) v = *reinterpret_cast<const uint4*>(src + (b * src_rows + row) * k + kk);
+        if (ok && transpose) {
+            uint16_t e8[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) e8[e] = src[(b * k + kk + e) * static_cast<int64_t>(n) + row];
+            v = make_uint4(e8[0] | (static_cast<uint32_t>(e8[1]) << 16), e8[2] | (static_cast<uint32_t>(e8[3]) << 16),
+                           e8[4] | (static_cast<uint32_t>(e8[5]) << 16), e8[6] | (static_cast<uint32_t>(e8[7]) << 16));
+        } else if (ok) {
+            v = *reinterpret_cast<const uint4*>(src + (b * src_rows + row) * k + kk);
+        }
         *reinterpret_cast<uint4*>(dst + f * 8) = v;
     }
 }
@@ -898,6 +1002,10 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work, int
     g.h_s = w.h_s;
     g.y_r = w.y_r;
     g.y_s = w.y_s;
+    g.dout = nullptr;
+    g.w2t = g.ws2t = g.w13t = g.ws13t = nullptr;
+    g.ab_r = g.ab_s = g.dab_r = g.dab_s = g.dx_r = g.dx_s = nullptr;
+    g.wrow = nullptr;
     return g;
 }
 
@@ -985,18 +1093,91 @@ hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, int part, hipStre
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- backward (modes 3-5)
+
+// Work table of one tiling (bm rows x nt column tiles per routed expert, then
+// the shared items): one thread, E <= 256.
+__global__ void bwd_work_kernel(const int32_t* __restrict__ off, int E, int64_t T, int bm, int nt_r, int nt_s,
+                                int has_shared, int32_t* __restrict__ work) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int32_t acc = 0;
+    work[0] = 0;
+    for (int g = 0; g < E; ++g) {
+        acc += static_cast<int32_t>(ceil_div(off[g + 1] - off[g], bm)) * nt_r;
+        work[g + 1] = acc;
+    }
+    work[E + 1] = acc + (has_shared ? static_cast<int32_t>(ceil_div(T, bm)) * nt_s : 0);
+}
+
+ExpertFwdBuffers experts_fwd_buffers(const ExpertArgs& a, void* ws) {
+    const ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
+    ExpertFwdBuffers b;
+    b.h_r = w.h_r;
+    b.h_s = w.h_s;
+    b.y_r = w.y_r;
+    b.y_s = w.y_s;
+    b.work1 = w.work1;
+    b.work2 = w.work2;
+    return b;
+}
+
+hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const BwdGemmPtrs& bp, int part,
+                           hipStream_t stream) {
+    const ExpWs w = carve(fwd_ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
+    const bool has_shared = a.shared_inter > 0;
+    int nt_r, nt_s;
+    const int32_t* work;
+    if (mode == 3) {
+        nt_r = static_cast<int>(ceil_div(a.inter, pk_tile_cols(3)));
+        nt_s = static_cast<int>(ceil_div(a.shared_inter, pk_tile_cols(3)));
+        work = w.work1;  // the forward GEMM1's table: same tiling
+    } else if (mode == 4) {
+        nt_r = static_cast<int>(ceil_div(a.inter, pk_tile_cols(4)));
+        nt_s = static_cast<int>(ceil_div(a.shared_inter, pk_tile_cols(4)));
+        work = bp.work4;
+        if (part != 2) {
+            hipLaunchKernelGGL(bwd_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T, PK_BM, nt_r,
+                               nt_s, has_shared ? 1 : 0, bp.work4);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+    } else {
+        nt_r = nt_s = static_cast<int>(ceil_div(a.d, pk_tile_cols(5)));
+        work = w.work2;  // the forward GEMM2's table: same tiling
+    }
+    GemmArgs g = make_args(a, w, work, part);
+    g.dout = bp.dout;
+    g.w2t = bp.w2t;
+    g.ws2t = bp.ws2t;
+    g.w13t = bp.w13t;
+    g.ws13t = bp.ws13t;
+    g.ab_r = bp.ab_r;
+    g.ab_s = bp.ab_s;
+    g.dab_r = bp.dab_r;
+    g.dab_s = bp.dab_s;
+    g.dx_r = bp.dx_r;
+    g.dx_s = bp.dx_s;
+    g.wrow = bp.wrow;
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, PK_BM, nt_r, nt_s, has_shared, part)));
+    if (grid.x == 0) return hipSuccess;
+    if (mode == 3) hipLaunchKernelGGL(gemm_bf16_pk_kernel<3>, grid, dim3(PK_THREADS), 0, stream, g);
+    else if (mode == 4) hipLaunchKernelGGL(gemm_bf16_pk_kernel<4>, grid, dim3(PK_THREADS), 0, stream, g);
+    else hipLaunchKernelGGL(gemm_bf16_pk_kernel<5>, grid, dim3(PK_THREADS), 0, stream, g);
+    return hipGetLastError();
+}
+
 int64_t packed_weight_elems(int batch, int n, int k, int interleave) {
     const int64_t ng = interleave ? 2 * ceil_div(n, 32) : ceil_div(n, 32);
     return batch * packed_elems(ng, k);
 }
 
-hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, void* dst,
+hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, int transpose, void* dst,
                                hipStream_t stream) {
     const int64_t frags = packed_weight_elems(batch, n, k, interleave) / 8;
     if (frags == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>(ceil_div(frags, 256) < 65536 ? ceil_div(frags, 256) : 65536);
     hipLaunchKernelGGL(pack_weights_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<const uint16_t*>(src),
-                       batch, n, k, interleave, static_cast<uint16_t*>(dst));
+                       batch, n, k, interleave, transpose, static_cast<uint16_t*>(dst));
     return hipGetLastError();
 }
 

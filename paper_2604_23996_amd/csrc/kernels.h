@@ -78,7 +78,7 @@ hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t str
 // packed bf16 expert weights: elements of `batch` packed n x k matrices
 // (interleave: gate and up halves of a 2n-row source)
 int64_t packed_weight_elems(int batch, int n, int k, int interleave);
-hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, void* dst,
+hipError_t launch_pack_weights(const void* src, int batch, int n, int k, int interleave, int transpose, void* dst,
                                hipStream_t stream);
 
 // Momentum-adaptive binning, bin-level load balance loss (+ logit gradient) and MSI
@@ -89,7 +89,52 @@ hipError_t launch_binning(const float* probs, const int32_t* topk_idx, const uin
                           float* bal_loss, float* dlogits, int accumulate, float* msi, void* ws,
                           hipStream_t stream);
 
-// ---------------------------------------------------------------- GMM estimator
+// ---------------------------------------------------------------- layer backward
+// The forward's expert buffers inside its workspace (H, Y and the work tables).
+struct ExpertFwdBuffers {
+    void* h_r;
+    void* h_s;
+    void* y_r;
+    void* y_s;
+    int32_t* work1;
+    int32_t* work2;
+};
+ExpertFwdBuffers experts_fwd_buffers(const ExpertArgs& a, void* ws);
+struct BwdGemmPtrs {
+    const void* dout;   // [T][d]
+    const void* w2t;    // packed W2^T per expert
+    const void* ws2t;
+    const void* w13t;   // packed W13^T per expert
+    const void* ws13t;
+    void* ab_r;         // [R][2 inter]
+    void* ab_s;         // [T][2 shared_inter]
+    void* dab_r;
+    void* dab_s;
+    void* dx_r;         // [R][d]
+    void* dx_s;         // [T][d]
+    const float* wrow;  // [R]
+    int32_t* work4;     // [E + 2] table of mode 4
+};
+// mode 3: recomputed gate/up pre-activations; 4: dH = w dout W2 with the SwiGLU
+// backward -> [dA dB]; 5: dX = [dA dB] W13. part: 1 routed, 2 shared.
+hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const BwdGemmPtrs& bp, int part,
+                           hipStream_t stream);
+// dW[g][m][n] = sum over the group's rows of A[amap(r)][m] * ascale(r) * B[bmap(r)][n] (bf16 out)
+hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int64_t lda,
+                        const int32_t* amap, const float* ascale, const void* B, int64_t ldb, const int32_t* bmap,
+                        void* out, hipStream_t stream);
+size_t router_bwd_workspace_bytes(int64_t T, int d, int E);
+hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int64_t T, int k, float* wrow,
+                              hipStream_t stream);
+hipError_t launch_router_bwd(const void* dout, const void* y_r, const int32_t* perm_inv, const float* probs,
+                             const int32_t* topk_idx, const float* topk_w, const float* dlogits_aux, int64_t T, int d,
+                             int E, int k, int renorm, float* dw, float* dz, hipStream_t stream);
+hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, const int32_t* perm_inv, const float* dz,
+                            const float* w_gate, int64_t T, int d, int E, int k, float* dx, hipStream_t stream);
+hipError_t launch_dwgate(const float* dz, const void* x, int64_t T, int d, int E, float* dw_gate, float* dbias,
+                         void* ws, hipStream_t stream);
+
+// ---------------------------------------------------------------- GMM estimator// ---------------------------------------------------------------- GMM estimator
 size_t gmm_workspace_bytes(int64_t T, int d, int K);
 hipError_t launch_gmm(const void* x, int x_dtype, int64_t T, int d, int K, const uint8_t* modality_id, float* gmm_n,
                       float* gmm_smu, float* gmm_ssig, int update, float beta, float tau, float var_floor, float* M,

@@ -57,6 +57,13 @@ class SmoesLayerIO(ctypes.Structure):
     _fields_ = [(n, c_void) for n in _IO_FIELDS] + [("streams", c_void)]
 
 
+_GRAD_FIELDS = ["dx", "dw_gate", "dbias", "dz", "dw", "dw13", "dw2", "dws13", "dws2"]
+
+
+class SmoesLayerGrads(ctypes.Structure):
+    _fields_ = [(n, c_void) for n in _GRAD_FIELDS]
+
+
 class SmoesStreams(ctypes.Structure):
     _fields_ = [("side", c_void * 2), ("events", c_void * 4)]
 
@@ -107,6 +114,12 @@ def lib() -> ctypes.CDLL:
         L.smoes_binning.argtypes = [c_void, c_void, c_void, c_i64, c_int, c_int, c_void, c_int, c_float, c_void,
                                     c_void, c_void, c_void, c_float, c_void, c_void, c_int, c_void, c_void,
                                     c_size, c_void]
+        L.smoes_backward_workspace_bytes.restype = c_size
+        L.smoes_backward_workspace_bytes.argtypes = [ctypes.POINTER(SmoesLayer)]
+        L.smoes_moe_backward.restype = c_int
+        L.smoes_moe_backward.argtypes = [ctypes.POINTER(SmoesLayer), ctypes.POINTER(SmoesLayerIO), c_void, c_void,
+                                         c_void, c_void, c_void, c_void, ctypes.POINTER(SmoesLayerGrads), c_void,
+                                         c_size, c_void, c_size, c_void]
         L.smoes_gmm_workspace_size.restype = c_size
         L.smoes_gmm_workspace_size.argtypes = [c_i64, c_int, c_int]
         L.smoes_gmm_modality_score.restype = c_int
@@ -369,6 +382,7 @@ def workspace_bytes(spec: LayerSpec) -> int:
 
 
 SMOES_W13, SMOES_W2, SMOES_WS13, SMOES_WS2, SMOES_WGATE = 0, 1, 2, 3, 4
+SMOES_W13T, SMOES_W2T, SMOES_WS13T, SMOES_WS2T = 5, 6, 7, 8
 WEIGHT_NAMES = {"w13": SMOES_W13, "w2": SMOES_W2, "ws13": SMOES_WS13, "ws2": SMOES_WS2}
 
 
@@ -468,6 +482,56 @@ def alloc_outputs(spec: LayerSpec, device, act_torch_dtype, want_logits=True, wa
         "perm_inv": torch.empty((T, k), **i) if want_perm else None,
         "out": torch.empty((T, spec.d), dtype=act_torch_dtype, device=device),
     }
+
+
+def pack_transposed_weights(spec: LayerSpec, dev_in: Dict[str, Optional[torch.Tensor]]) -> Dict[str, torch.Tensor]:
+    """The transposed packed expert weights the backward reads (from the
+    row-major bf16 weights in dev_in: w13, w2, ws13, ws2)."""
+    out = {"w13t": pack_weights(spec, SMOES_W13T, dev_in["w13"]), "w2t": pack_weights(spec, SMOES_W2T, dev_in["w2"])}
+    if spec.shared_inter > 0:
+        out["ws13t"] = pack_weights(spec, SMOES_WS13T, dev_in["ws13"])
+        out["ws2t"] = pack_weights(spec, SMOES_WS2T, dev_in["ws2"])
+    return out
+
+
+def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
+                 outputs: Dict[str, Optional[torch.Tensor]], fwd_workspace: torch.Tensor,
+                 packed_t: Dict[str, torch.Tensor], dout: torch.Tensor,
+                 dlogits_aux: Optional[torch.Tensor] = None, want_dw: bool = True) -> Dict[str, torch.Tensor]:
+    """smoes_moe_backward after moe_forward with the same inputs / outputs /
+    workspace. `inputs` must hold the packed w13 / ws13 and the float32
+    w_gate; returns the gradients (dx, dw_gate, dbias, dz, dw, dw13, dw2,
+    dws13, dws2)."""
+    desc = spec.c()
+    io = SmoesLayerIO()
+    for name in _IO_FIELDS:
+        if name == "stage_events":
+            continue
+        t = inputs.get(name) if name in inputs else outputs.get(name)
+        setattr(io, name, None if t is None else _p(t).value)
+    io.stage_events = None
+    io.streams = None
+    T, d, E, k, I, SI = spec.T, spec.d, spec.E, spec.k, spec.inter, spec.shared_inter
+    dev = dout.device
+    g = {"dx": torch.empty((T, d), dtype=torch.float32, device=dev),
+         "dw_gate": torch.empty((E, d), dtype=torch.float32, device=dev),
+         "dbias": torch.empty(E, dtype=torch.float32, device=dev),
+         "dz": torch.empty((T, E), dtype=torch.float32, device=dev),
+         "dw": torch.empty((T, k), dtype=torch.float32, device=dev) if want_dw else None,
+         "dw13": torch.empty((E, 2 * I, d), dtype=torch.bfloat16, device=dev),
+         "dw2": torch.empty((E, d, I), dtype=torch.bfloat16, device=dev),
+         "dws13": torch.empty((2 * SI, d), dtype=torch.bfloat16, device=dev) if SI > 0 else None,
+         "dws2": torch.empty((d, SI), dtype=torch.bfloat16, device=dev) if SI > 0 else None}
+    G = SmoesLayerGrads()
+    for name in _GRAD_FIELDS:
+        setattr(G, name, None if g[name] is None else _p(g[name]).value)
+    nbytes = int(lib().smoes_backward_workspace_bytes(ctypes.byref(desc)))
+    ws = _workspace(nbytes, dev)
+    _check(lib().smoes_moe_backward(ctypes.byref(desc), ctypes.byref(io), _p(packed_t["w13t"]), _p(packed_t["w2t"]),
+                                    _p(packed_t.get("ws13t")), _p(packed_t.get("ws2t")), _p(dout), _p(dlogits_aux),
+                                    ctypes.byref(G), _p(fwd_workspace), fwd_workspace.numel(), _p(ws), nbytes,
+                                    _stream()), "smoes_moe_backward")
+    return g
 
 
 def moe_forward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],

@@ -146,6 +146,47 @@ def test_struct_layout_matches_header():
     assert fields == S._IO_FIELDS + ["streams"]
 
 
+def test_backward_struct_and_host_checks():
+    text = open(S.HEADER_PATH).read()
+    import re
+    blk = text[text.index("typedef struct smoes_layer_grads"):text.index("} smoes_layer_grads;")]
+    blk = re.sub(r"/\*.*?\*/", "", blk, flags=re.S)
+    assert re.findall(r"\*\s*([A-Za-z_0-9]+);", blk) == S._GRAD_FIELDS
+    assert ctypes.sizeof(S.SmoesLayerGrads) == 9 * 8
+    L = S.lib()
+    spec = _spec(d=128, inter=96, shared_inter=48, weights_packed=True)
+    desc = spec.c()
+    n = L.smoes_backward_workspace_bytes(ctypes.byref(desc))
+    assert n > 0
+    bad = _spec().c()
+    bad.reserved = 1
+    assert L.smoes_backward_workspace_bytes(ctypes.byref(bad)) == 0
+    io = S.SmoesLayerIO()
+    G = S.SmoesLayerGrads()
+    args = lambda d_: (ctypes.byref(d_), ctypes.byref(io), FAKE, FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(G),
+                       FAKE, 1 << 40, FAKE, 1 << 40, None)
+    # float32 layers and row-major weights are not implemented; nothing is launched
+    assert L.smoes_moe_backward(*args(_spec(act_dtype=0).c())) == S.SMOES_ERR_ARG
+    assert L.smoes_moe_backward(*args(_spec(weights_packed=False).c())) == S.SMOES_ERR_ARG
+    # missing pointers and short workspaces are rejected before any launch
+    assert L.smoes_moe_backward(*args(desc)) == S.SMOES_ERR_ARG
+    assert L.smoes_moe_backward(ctypes.byref(desc), None, FAKE, FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(G),
+                                FAKE, 1 << 40, FAKE, 1 << 40, None) == S.SMOES_ERR_ARG
+    for name in S._IO_FIELDS:
+        if name in ("x", "w13", "ws13", "w_gate", "probs", "topk_idx", "topk_w"):
+            setattr(io, name, FAKE.value)
+    for name in S._GRAD_FIELDS:
+        setattr(G, name, FAKE.value)
+    assert L.smoes_moe_backward(ctypes.byref(desc), ctypes.byref(io), FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                ctypes.byref(G), FAKE, 16, FAKE, 1 << 40, None) == S.SMOES_ERR_WORKSPACE
+    assert L.smoes_moe_backward(ctypes.byref(desc), ctypes.byref(io), FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                ctypes.byref(G), FAKE, 1 << 40, FAKE, n - 1, None) == S.SMOES_ERR_WORKSPACE
+    # the dX GEMM's A operand must stay inside 32-bit byte offsets
+    big = _spec(T=1 << 17, d=64, E=8, k=8, inter=512, shared_inter=0, weights_packed=True).c()
+    assert L.smoes_workspace_bytes(ctypes.byref(big)) > 0  # the forward accepts it
+    assert L.smoes_moe_backward(*args(big)) == S.SMOES_ERR_SHAPE
+
+
 def test_packed_weight_sizes_and_checks():
     L = S.lib()
     spec = _spec(d=128, inter=96, shared_inter=48)
@@ -156,11 +197,17 @@ def test_packed_weight_sizes_and_checks():
     assert S.packed_weight_bytes(spec, S.SMOES_WS2) == (128 // 32) * (48 // 16) * 512 * 2
     # router weights: 3 bf16 terms x ceil(E/16)*16 experts x ceil(d/32)*32
     assert S.packed_weight_bytes(spec, S.SMOES_WGATE) == 3 * 16 * 128 * 2
-    assert S.packed_weight_bytes(spec, 5) == 0
+    # transposed forms for the backward: W13^T has d rows over 2 inter, W2^T inter rows over d
+    assert S.packed_weight_bytes(spec, S.SMOES_W13T) == 16 * (128 // 32) * (192 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_W2T) == 16 * (96 // 32) * (128 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS13T) == (128 // 32) * (96 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS2T) == (48 // 32 + 1) * (128 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, 9) == 0 and S.packed_weight_bytes(spec, -1) == 0
     assert S.packed_weight_bytes(_spec(shared_inter=0), S.SMOES_WS13) == 0
+    assert S.packed_weight_bytes(_spec(shared_inter=0), S.SMOES_WS2T) == 0
     desc = spec.c()
     assert L.smoes_pack_weights(ctypes.byref(desc), S.SMOES_W13, None, FAKE, None) == S.SMOES_ERR_ARG
-    assert L.smoes_pack_weights(ctypes.byref(desc), 7, FAKE, FAKE, None) == S.SMOES_ERR_ARG
+    assert L.smoes_pack_weights(ctypes.byref(desc), 9, FAKE, FAKE, None) == S.SMOES_ERR_ARG
     f32 = _spec(act_dtype=0).c()
     assert L.smoes_pack_weights(ctypes.byref(f32), S.SMOES_W13, FAKE, FAKE, None) == S.SMOES_ERR_ARG
     # packed weights are a bf16 layout; reserved must stay 0

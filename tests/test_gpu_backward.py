@@ -1,0 +1,210 @@
+"""GPU parity of the layer backward (smoes_moe_backward after
+smoes_moe_forward) against oracle.layer_backward: combine-weight and logit
+gradients, the router weight and bias gradients, the routed and shared
+expert weight gradients and the input gradient.
+
+The routing must agree with the oracle's wherever the oracle's k-th and
+(k+1)-th logits are more than 1e-4 apart. The upstream gradient is zero on
+tokens whose gap is below 1e-3, so that no gradient depends on how a near
+tie was broken (such a token then contributes only its auxiliary logit
+gradient, which does not depend on the routing). Bars,
+normwise relative error (the GPU path stores the recomputed pre-activations,
+their gradients, H and each routed row's dX in bf16, relative rounding
+2^-9 per stored element, and scales dout by the combine weight in bf16):
+  dw, dz, dw_gate          <= 5e-3  (observed 1e-3 .. 2.7e-3: the forward's
+                                     Y and H are bf16, rms rounding 1.1e-3 each)
+  dbias                    <= 1e-2  (column sums of signed logit gradients
+                                     cancel, observed up to 3.9e-3)
+  dx                       <= 1e-2  (observed up to 3.1e-3)
+  dw13, dw2, dws13, dws2   <= 1e-2  (observed up to 3.3e-3)
+plus an elementwise bar of 6e-2 x max|ref| on every gradient (no single
+element far off while the norm is fine)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2604_23996_amd import smoes as S
+from paper_2604_23996_amd import workloads as W
+from tests.gpu_util import DEV, check_topk, host, layer_spec, rel_err, run_gpu_layer, say, t
+
+pytestmark = pytest.mark.gpu
+
+BARS = {"dw": 5e-3, "dz": 5e-3, "dbias": 1e-2, "dw_gate": 5e-3, "dx": 1e-2,
+        "dw13": 1e-2, "dw2": 1e-2, "dws13": 1e-2, "dws2": 1e-2}
+ELEM = 6e-2
+
+LAYERS = [
+    dict(d=128, E=16, k=4, inter=96, n_shared=1, n_bins=4, samples=((200, 100), (40, 60))),
+    dict(d=256, E=12, k=3, inter=64, n_shared=0, n_bins=3, samples=((500, 200),)),
+    # ragged packed groups: d % 32 == 8, inter % 32 == 16
+    dict(d=136, E=10, k=3, inter=48, n_shared=2, n_bins=5, samples=((150, 70), (33, 17))),
+    dict(d=512, E=64, k=6, inter=128, n_shared=2, n_bins=8, samples=((700, 300),), logit_bias=True),
+    # several experts without tokens
+    dict(d=64, E=32, k=2, inter=32, n_shared=1, n_bins=4, samples=((9, 5),)),
+    # three tokens
+    dict(d=64, E=4, k=2, inter=32, n_shared=0, n_bins=2, samples=((2, 1),)),
+]
+
+
+def _inputs(case, seed):
+    cfg = W.small_config(seed=seed, dtype=W.BF16, **case)
+    inp = W.make_layer_inputs(cfg)
+    rng = np.random.default_rng(seed + 7)
+    dout = _mask_ties(inp, W.f32_to_bf16_bits(rng.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
+    aux = (1e-3 * rng.standard_normal((cfg.T, cfg.E))).astype(np.float32)
+    return cfg, inp, dout, aux
+
+
+def _mask_ties(inp, dout, gap=1e-3):
+    """Zero the upstream gradient of the tokens whose oracle top-k gap is
+    below `gap`."""
+    z, _, _, _ = O.route(inp.x, inp.w_gate, inp.cfg.k, inp.logit_bias)
+    dout = dout.copy()
+    dout[O.topk_gap(z, inp.cfg.k) < gap] = 0
+    return dout
+
+
+def run_gpu_backward(inp, dout, aux, renorm, want_dw=True):
+    """Forward then backward on the device; returns (spec, outs, grads)."""
+    cfg = inp.cfg
+    rowmajor = {"w13": t(inp.w13), "w2": t(inp.w2), "ws13": t(inp.ws13), "ws2": t(inp.ws2)}
+    spec_t = layer_spec(cfg, weights_packed=True)
+    packed_t = S.pack_transposed_weights(spec_t, rowmajor)
+    torch.cuda.synchronize()
+    spec, dev_in, outs, ws = run_gpu_layer(inp, renorm_topk=renorm, keep_workspace=True)
+    g = S.moe_backward(spec, dev_in, outs, ws, packed_t, t(dout), None if aux is None else t(aux), want_dw=want_dw)
+    torch.cuda.synchronize()
+    return spec, outs, g
+
+
+def _compare(g, ref, inp, outs, cfg, extra=""):
+    z_ref, _, idx_ref, _ = O.route(inp.x, inp.w_gate, cfg.k, inp.logit_bias)
+    check_topk(host(outs["topk_idx"]), idx_ref, z_ref, cfg.k)
+    errs = {}
+    for name, bar in BARS.items():
+        r = ref[name]
+        if r is None:
+            assert g.get(name) is None
+            continue
+        if g.get(name) is None:
+            continue
+        got = host(g[name]).reshape(r.shape)
+        e = rel_err(got, r)
+        errs[name] = e
+        scale = np.abs(r).max()
+        assert e <= bar, (name, e, extra)
+        assert np.abs(got - r).max() <= ELEM * scale + 1e-30, (name, np.abs(got - r).max(), scale, extra)
+    say("backward errors", extra, {k: f"{v:.2e}" for k, v in errs.items()})
+    return errs
+
+
+@pytest.mark.parametrize("layer", range(len(LAYERS)))
+@pytest.mark.parametrize("renorm", [False, True])
+@pytest.mark.parametrize("with_aux", [False, True])
+def test_backward_small(layer, renorm, with_aux):
+    cfg, inp, dout, aux = _inputs(LAYERS[layer], 300 + layer)
+    if not with_aux:
+        aux = None
+    say("backward", layer, "renorm", renorm, "aux", with_aux, "T", cfg.T)
+    spec, outs, g = run_gpu_backward(inp, dout, aux, renorm)
+    ref = O.layer_backward(inp.x, inp.w_gate, inp.logit_bias, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
+                           W.bf16_bits_to_f32(dout), aux, renorm_topk=renorm)
+    _compare(g, ref, inp, outs, cfg, extra=f"layer {layer}")
+
+
+def test_backward_experts_without_tokens_have_zero_gradient():
+    cfg, inp, dout, aux = _inputs(LAYERS[4], 304)
+    say("backward empty experts")
+    spec, outs, g = run_gpu_backward(inp, dout, None, False)
+    idx = host(outs["topk_idx"])
+    used = np.zeros(cfg.E, bool)
+    used[idx.ravel()] = True
+    assert (~used).any()
+    dw13, dw2 = host(g["dw13"]), host(g["dw2"])
+    assert np.all(dw13[~used] == 0.0) and np.all(dw2[~used] == 0.0)
+    assert np.all(np.abs(dw13[used]).reshape(int(used.sum()), -1).max(axis=1) > 0)
+
+
+def test_backward_is_reproducible():
+    cfg, inp, dout, aux = _inputs(LAYERS[0], 300)
+    say("backward reproducible")
+    _, _, a = run_gpu_backward(inp, dout, aux, False)
+    _, _, b = run_gpu_backward(inp, dout, aux, False)
+    for name in a:
+        if a[name] is not None:
+            assert torch.equal(a[name], b[name]), name
+
+
+def test_backward_without_dw_output():
+    cfg, inp, dout, aux = _inputs(LAYERS[2], 302)
+    say("backward no dw")
+    _, _, g = run_gpu_backward(inp, dout, aux, True, want_dw=False)
+    _, _, h = run_gpu_backward(inp, dout, aux, True, want_dw=True)
+    for name in g:
+        if g[name] is not None:
+            assert torch.equal(g[name], h[name]), name
+
+
+def test_backward_rejects_fp32_and_rowmajor_layers():
+    cfg = W.small_config(d=64, E=8, k=2, inter=32, n_shared=0, samples=((8, 8),), dtype=W.F32, seed=5)
+    spec = layer_spec(cfg)
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
+    x = torch.zeros((cfg.T, cfg.d), dtype=torch.float32, device=DEV)
+    with pytest.raises(S.SmoesError):
+        S.moe_backward(spec, {"x": x}, {}, ws, {"w13t": x, "w2t": x}, x)
+    cfg = W.small_config(d=64, E=8, k=2, inter=32, n_shared=0, samples=((8, 8),), dtype=W.BF16, seed=5)
+    spec = layer_spec(cfg, weights_packed=False)
+    with pytest.raises(S.SmoesError):
+        S.moe_backward(spec, {"x": x}, {}, ws, {"w13t": x, "w2t": x}, x)
+
+
+def test_backward_bench_layer_sampled():
+    """The 4096-token DeepSeekMoE-like layer (d 2048, 64 experts, top-6,
+    inter 1408, two shared experts), in the launch configuration of the
+    timed training step. The oracle computes dw, dz and dx of 128 sampled
+    tokens (the per-token gradients depend on that token alone), the weight
+    gradients of three routed experts over their rows and the shared
+    experts' weight gradients over all tokens; the router weight and bias
+    gradients are checked as dz^T x and the column sums of dz in float64."""
+    cfg = W.CONFIGS[1]
+    inp = W.make_layer_inputs(cfg)
+    rng = np.random.default_rng(77)
+    dout = _mask_ties(inp, W.f32_to_bf16_bits(rng.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
+    say("backward bench layer")
+    spec, outs, g = run_gpu_backward(inp, dout, None, False)
+    X = O.widen(inp.x)
+    dO = W.bf16_bits_to_f32(dout).astype(np.float64)
+    z, _, idx, w = O.route(inp.x, inp.w_gate, cfg.k, inp.logit_bias)
+    check_topk(host(outs["topk_idx"]), idx, z, cfg.k)
+    # per-token gradients of sampled tokens
+    sample = np.sort(rng.choice(cfg.T, size=128, replace=False))
+    ref = O.layer_backward(inp.x[sample], inp.w_gate, inp.logit_bias, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
+                           dO[sample], None)
+    for name in ("dw", "dz", "dx"):
+        got = host(g[name])[sample]
+        assert rel_err(got, ref[name]) <= BARS[name], (name, rel_err(got, ref[name]))
+        assert np.abs(got - ref[name]).max() <= ELEM * np.abs(ref[name]).max()
+    # routed experts over all their rows
+    _, offsets, perm_token, inv = O.permutation(idx, cfg.E)
+    for e in (0, 29, 63):
+        a, b = offsets[e], offsets[e + 1]
+        toks = perm_token[a:b]
+        slot = np.argmax(inv[toks] == np.arange(a, b)[:, None], axis=1)
+        dY = w[toks, slot][:, None] * dO[toks]
+        _, dw13, dw2 = O.swiglu_backward(X[toks], inp.w13[e], inp.w2[e], dY)
+        for name, got, r in (("dw13", host(g["dw13"][e]), dw13), ("dw2", host(g["dw2"][e]), dw2)):
+            assert rel_err(got, r) <= BARS[name], (name, e, rel_err(got, r))
+            assert np.abs(got - r).max() <= ELEM * np.abs(r).max(), (name, e)
+    # shared experts over all tokens
+    _, dws13, dws2 = O.swiglu_backward(X, inp.ws13, inp.ws2, dO)
+    for name, r in (("dws13", dws13), ("dws2", dws2)):
+        got = host(g[name])
+        assert rel_err(got, r) <= BARS[name], (name, rel_err(got, r))
+        assert np.abs(got - r).max() <= ELEM * np.abs(r).max(), name
+    # router: dW_gate = dz^T x and dbias = column sums of dz, float32 chunked sums
+    dz = host(g["dz"]).astype(np.float64)
+    assert rel_err(host(g["dw_gate"]), dz.T @ X) <= 1e-5
+    assert rel_err(host(g["dbias"]), dz.sum(axis=0)) <= 1e-5
