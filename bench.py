@@ -379,6 +379,48 @@ def main():
             "attention_tflops": round(att_flops / (att_ms * 1e-3) / 1e12, 2),
             "attention_frac_mfma": round(att_flops / (att_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "update_gbs": round(upd_bytes / ((tot_ms - att_ms) * 1e-3) / 1e9, 1) if tot_ms > att_ms else None}
+    # Training step of the layer: the forward above, then the backward with a
+    # synthetic upstream gradient and the MI gradient as the auxiliary logit
+    # gradient (every gradient: combine weights, logits, router weight and
+    # bias, routed and shared expert weights, input). Timed on its own.
+    if spec.weights_packed:
+        log("[bench] training step (forward + backward)")
+        rm = {n: t(getattr(inp, n)) for n in ("w13", "w2", "ws13", "ws2")}
+        packed_t = S.pack_transposed_weights(spec, rm)
+        del rm
+        rng_b = np.random.default_rng(cfg.seed + 300)
+        dout = t(W.f32_to_bf16_bits(rng_b.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
+        bws_t = torch.empty(S.backward_workspace_bytes(spec), dtype=torch.uint8, device=dev)
+        S.moe_forward(spec, dev_in, outs, ws, streams=streams)
+        grads = S.moe_backward(spec, dev_in, outs, ws, packed_t, dout, outs["dlogits"], workspace=bws_t)
+        for _ in range(3):
+            S.moe_forward(spec, dev_in, outs, ws, streams=streams)
+            S.moe_backward(spec, dev_in, outs, ws, packed_t, dout, outs["dlogits"], grads=grads, workspace=bws_t)
+        tr_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        f_ms, b_ms = [], []
+        for _ in range(args.steps):
+            tr_ev[0].record()
+            S.moe_forward(spec, dev_in, outs, ws, streams=streams)
+            tr_ev[1].record()
+            S.moe_backward(spec, dev_in, outs, ws, packed_t, dout, outs["dlogits"], grads=grads, workspace=bws_t)
+            tr_ev[2].record()
+            torch.cuda.synchronize()
+            f_ms.append(tr_ev[0].elapsed_time(tr_ev[1]))
+            b_ms.append(tr_ev[1].elapsed_time(tr_ev[2]))
+        fm, bm = float(np.median(f_ms)), float(np.median(b_ms))
+        R = cfg.T * cfg.k
+        # dgrad (dH, dX) and wgrad (dW2, dW13): 12 d inter flops per routed row and per token for the
+        # shared block; the recompute of the gate / up pre-activations adds 4 more
+        bwd_flops = 12.0 * cfg.d * (R * cfg.inter + cfg.T * cfg.shared_inter)
+        rec_flops = 4.0 * cfg.d * (R * cfg.inter + cfg.T * cfg.shared_inter)
+        line["extra"]["training_step"] = {
+            "what": "forward + backward of the layer (all gradients; MI gradient added to the logit gradient)",
+            "ms": round(fm + bm, 5), "forward_ms": round(fm, 5), "backward_ms": round(bm, 5),
+            "tokens_per_s": round(cfg.T / ((fm + bm) * 1e-3), 1),
+            "backward_tflops": round(bwd_flops / (bm * 1e-3) / 1e12, 2),
+            "backward_tflops_with_recompute": round((bwd_flops + rec_flops) / (bm * 1e-3) / 1e12, 2),
+            "backward_frac_mfma": round((bwd_flops + rec_flops) / (bm * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        del packed_t, grads, bws_t
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on {args.cpu_samples} samples")
         line["cpu_baseline"] = cpu_baseline(cfg, inp, min(args.cpu_samples, cfg.n_batch))

@@ -470,6 +470,7 @@ struct BwdWs {
     void* dx_r;
     void* dx_s;
     float* wrow;
+    void* wh_r;
     int32_t* work4;
     void* router;
 };
@@ -484,6 +485,7 @@ size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     w.dx_r = c.take(sizeof(uint16_t) * R * L->d);
     w.dx_s = c.take(sizeof(uint16_t) * T * L->d);
     w.wrow = static_cast<float*>(c.take(sizeof(float) * R));
+    w.wh_r = c.take(sizeof(uint16_t) * R * L->inter);
     w.work4 = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 2)));
     w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E));
     if (out != nullptr) *out = w;
@@ -562,6 +564,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     bp.dx_r = bw.dx_r;
     bp.dx_s = bw.dx_s;
     bp.wrow = bw.wrow;
+    bp.wh_r = bw.wh_r;
     bp.work4 = bw.work4;
     hipError_t err;
 #define SMOES_BTRY(expr)                                        \
@@ -578,12 +581,14 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
                                 G->dx, s));
     const int I = L->inter, SI = L->shared_inter, d = L->d;
-    SMOES_BTRY(launch_wgrad(T, L->E, d, I, offsets, dout, d, perm_token, bw.wrow, fb.h_r, I, nullptr, G->dw2, s));
-    SMOES_BTRY(launch_wgrad(T, L->E, 2 * I, d, offsets, bw.dab_r, 2 * I, nullptr, nullptr, io->x, d, perm_token,
+    const int Ti = static_cast<int>(T), R = static_cast<int>(T * L->k);
+    // dW2 = dout^T (w H) over each expert's rows (dout gathered); dW13 = [dA dB]^T X (x gathered)
+    SMOES_BTRY(launch_wgrad(T, L->E, d, I, offsets, dout, d, Ti, perm_token, bw.wh_r, I, R, nullptr, R, G->dw2, s));
+    SMOES_BTRY(launch_wgrad(T, L->E, 2 * I, d, offsets, bw.dab_r, 2 * I, R, nullptr, io->x, d, Ti, perm_token, R,
                             G->dw13, s));
     if (sh) {
-        SMOES_BTRY(launch_wgrad(T, 1, d, SI, nullptr, dout, d, nullptr, nullptr, fb.h_s, SI, nullptr, G->dws2, s));
-        SMOES_BTRY(launch_wgrad(T, 1, 2 * SI, d, nullptr, bw.dab_s, 2 * SI, nullptr, nullptr, io->x, d, nullptr,
+        SMOES_BTRY(launch_wgrad(T, 1, d, SI, nullptr, dout, d, Ti, nullptr, fb.h_s, SI, Ti, nullptr, 0, G->dws2, s));
+        SMOES_BTRY(launch_wgrad(T, 1, 2 * SI, d, nullptr, bw.dab_s, 2 * SI, Ti, nullptr, io->x, d, Ti, nullptr, 0,
                                 G->dws13, s));
     }
     SMOES_BTRY(launch_dwgate(G->dz, io->x, T, d, L->E, G->dw_gate, G->dbias, bw.router, s));

@@ -7,7 +7,7 @@
 //     dz_je = g_je (dg_je - sum_e' g_je' dg_je'), plus the auxiliary logit
 //     gradients (MI, bin balance) when given.
 //  dx_gather: dx_j = dz_j W_gate + sum_s dX[inv(j, s)] + dXs_j in float32, in
-//     that order (16 tokens x 256 columns per block, dz staged in LDS).
+//     that order (8 tokens x 1024 columns per block, dz staged in LDS).
 //  dwgate: dW_gate[e][c] = sum_j dz_je x_jc and dbias_e = sum_j dz_je: per
 //     256-token chunk partials, then a chunk-ordered sum.
 #include "common.h"
@@ -17,7 +17,7 @@ namespace smoes {
 
 namespace {
 
-constexpr int kDxTok = 16;
+constexpr int kDxTok = 8;
 constexpr int kDwChunk = 256;  // tokens per dwgate partial
 constexpr int kDwExp = 16;     // experts per dwgate block
 
@@ -74,13 +74,15 @@ router_bwd_kernel(const uint16_t* __restrict__ dout, const uint16_t* __restrict_
         for (int s = 0; s < k; ++s) dw[j * k + s] = dws[s];
 }
 
+// Each thread: 4 adjacent columns of kDxTok tokens (8-byte loads of the bf16
+// row gradients, 16 bytes of W_gate per expert).
 __global__ void __launch_bounds__(256)
 dx_gather_kernel(const uint16_t* __restrict__ dx_r, const uint16_t* __restrict__ dx_s, const int32_t* __restrict__ inv,
                  const float* __restrict__ dz, const float* __restrict__ w_gate, int64_t T, int d, int E, int k,
                  float* __restrict__ dx) {
     extern __shared__ float dz_s[];  // [kDxTok][E]
     const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kDxTok;
-    const int c = blockIdx.y * 256 + threadIdx.x;
+    const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
     const int nt = static_cast<int>(T - j0 < kDxTok ? T - j0 : kDxTok);
     for (int i = threadIdx.x; i < kDxTok * E; i += 256) {
         const int t = i / E;
@@ -88,20 +90,37 @@ dx_gather_kernel(const uint16_t* __restrict__ dx_r, const uint16_t* __restrict__
     }
     __syncthreads();
     if (c >= d) return;
-    float acc[kDxTok];
+    float acc[kDxTok][4];
 #pragma unroll
-    for (int t = 0; t < kDxTok; ++t) acc[t] = 0.0f;
+    for (int t = 0; t < kDxTok; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[t][q] = 0.0f;
     for (int e = 0; e < E; ++e) {
-        const float w = w_gate[static_cast<int64_t>(e) * d + c];
+        const float4 w = *reinterpret_cast<const float4*>(w_gate + static_cast<int64_t>(e) * d + c);
 #pragma unroll
-        for (int t = 0; t < kDxTok; ++t) acc[t] = fmaf(dz_s[t * E + e], w, acc[t]);
+        for (int t = 0; t < kDxTok; ++t) {
+            const float z = dz_s[t * E + e];
+            acc[t][0] = fmaf(z, w.x, acc[t][0]);
+            acc[t][1] = fmaf(z, w.y, acc[t][1]);
+            acc[t][2] = fmaf(z, w.z, acc[t][2]);
+            acc[t][3] = fmaf(z, w.w, acc[t][3]);
+        }
     }
-    for (int t = 0; t < nt; ++t) {
+    auto add4 = [](float (&v)[4], uint2 u) {
+        v[0] += __uint_as_float(u.x << 16);
+        v[1] += __uint_as_float(u.x & 0xffff0000u);
+        v[2] += __uint_as_float(u.y << 16);
+        v[3] += __uint_as_float(u.y & 0xffff0000u);
+    };
+#pragma unroll
+    for (int t = 0; t < kDxTok; ++t) {
+        if (t >= nt) break;
         const int64_t j = j0 + t;
-        float v = acc[t];
-        for (int s = 0; s < k; ++s) v += bf16_to_f32(dx_r[static_cast<int64_t>(inv[j * k + s]) * d + c]);
-        if (dx_s != nullptr) v += bf16_to_f32(dx_s[j * d + c]);
-        dx[j * d + c] = v;
+        float v[4] = {acc[t][0], acc[t][1], acc[t][2], acc[t][3]};
+        for (int s2 = 0; s2 < k; ++s2)
+            add4(v, *reinterpret_cast<const uint2*>(dx_r + static_cast<int64_t>(inv[j * k + s2]) * d + c));
+        if (dx_s != nullptr) add4(v, *reinterpret_cast<const uint2*>(dx_s + j * d + c));
+        *reinterpret_cast<float4*>(dx + j * d + c) = make_float4(v[0], v[1], v[2], v[3]);
     }
 }
 
@@ -185,7 +204,7 @@ hipError_t launch_router_bwd(const void* dout, const void* y_r, const int32_t* p
 hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, const int32_t* perm_inv, const float* dz,
                             const float* w_gate, int64_t T, int d, int E, int k, float* dx, hipStream_t stream) {
     if (T == 0) return hipSuccess;
-    const dim3 grid(static_cast<unsigned>(ceil_div(T, kDxTok)), static_cast<unsigned>(ceil_div(d, 256)));
+    const dim3 grid(static_cast<unsigned>(ceil_div(T, kDxTok)), static_cast<unsigned>(ceil_div(d, 256 * 4)));
     hipLaunchKernelGGL(dx_gather_kernel, grid, dim3(256), sizeof(float) * kDxTok * E, stream,
                        static_cast<const uint16_t*>(dx_r), static_cast<const uint16_t*>(dx_s), perm_inv, dz, w_gate,
                        T, d, E, k, dx);

@@ -131,4 +131,30 @@ __host__ __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { ret
 
 __host__ __device__ __forceinline__ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// ---------------------------------------------------------------- buffer loads and waits
+
+// Raw buffer descriptors (gfx9 word 3) and an offset that is always past the record count.
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kOutOfRange = 0x7fffffff;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// s_waitcnt with vmcnt(N) and lgkmcnt(0) (gfx9 encoding; expcnt left free)
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | 0x70);
+}
+
+// Values that are the same in every lane but that the compiler cannot prove
+// uniform (they derive from loads): pin them to SGPRs so buffer descriptors
+// built from them stay scalar.
+__device__ __forceinline__ int uniform_int(int v) { return __builtin_amdgcn_readfirstlane(v); }
+template <class T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return reinterpret_cast<T*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 }  // namespace smoes

@@ -146,10 +146,6 @@ __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, co
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
 
-// Raw buffer descriptors (gfx9 word 3) and an offset that is always past the record count.
-constexpr int kBufferFlags = 0x00020000;
-constexpr int kOutOfRange = 0x7fffffff;
-typedef int i32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 as_uint4(i32x4_t v) {
     return make_uint4(static_cast<uint32_t>(v.x), static_cast<uint32_t>(v.y), static_cast<uint32_t>(v.z),
                       static_cast<uint32_t>(v.w));
@@ -185,6 +181,7 @@ struct GemmArgs {
     void* dx_r;         // [R][d] input gradient of each routed row
     void* dx_s;         // [T][d] shared experts' input gradient
     const float* wrow;  // [R] combine weight of each routed row
+    void* wh_r;         // [R][inter] w H of each routed row (mode 4 output)
 };
 
 // ============================================================== bf16 MFMA path
@@ -221,12 +218,6 @@ __device__ __forceinline__ int dma_slot(int row, int chunk) {
     return chunk ^ ((row / C::SWZ_DIV) % C::CPR);
 }
 
-// s_waitcnt with vmcnt(N) and lgkmcnt(0) (gfx9 encoding; expcnt left free)
-template <int N>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | 0x70);
-}
 
 template <int MODE, class C>
 __global__ void __launch_bounds__(C::THREADS, 1)
@@ -471,9 +462,11 @@ constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instruction
 constexpr int pk_family(int mode) { return (mode == 1 || mode == 3) ? 1 : 2; }
 constexpr int pk_tile_cols(int mode) { return pk_family(mode) == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
 constexpr int pk_out_cols(int mode) { return mode == 3 ? 2 * pk_tile_cols(mode) : pk_tile_cols(mode); }
+constexpr int pk_epi_bytes(int mode) {
+    return mode == 4 ? 32 * (3 * pk_tile_cols(mode) + 8) * 2 : PK_BM * (pk_out_cols(mode) + 8) * 2;
+}
 constexpr int pk_lds_bytes(int mode) {
-    return PK_ST * PK_BM * PK_BK * 2 > PK_BM * (pk_out_cols(mode) + 8) * 2 ? PK_ST * PK_BM * PK_BK * 2
-                                                                            : PK_BM * (pk_out_cols(mode) + 8) * 2;
+    return PK_ST * PK_BM * PK_BK * 2 > pk_epi_bytes(mode) ? PK_ST * PK_BM * PK_BK * 2 : pk_epi_bytes(mode);
 }
 
 // Elements of one packed matrix with n rows (n_groups = ceil(n / 32) groups) and contraction k.
@@ -481,17 +474,6 @@ __host__ __device__ inline int64_t packed_elems(int64_t n_groups, int k) {
     return n_groups * ((k + 15) / 16) * 512;
 }
 
-// Values that are the same in every lane but that the compiler cannot prove
-// uniform (they derive from loads): pin them to SGPRs so buffer descriptors
-// built from them stay scalar.
-__device__ __forceinline__ int uniform_int(int v) { return __builtin_amdgcn_readfirstlane(v); }
-template <class T>
-__device__ __forceinline__ T* uniform_ptr(T* p) {
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
-    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
-    return reinterpret_cast<T*>((static_cast<uint64_t>(hi) << 32) | lo);
-}
 
 template <int MODE>
 __global__ void __launch_bounds__(PK_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -704,41 +686,92 @@ gemm_bf16_pk_kernel(GemmArgs p) {
                           static_cast<uint32_t>(f32_to_bf16(c)) | (static_cast<uint32_t>(f32_to_bf16(d)) << 16));
     };
     if constexpr (MODE == 4) {
-        // dH = w * (dout W2) and the SwiGLU backward with the saved gate (a) and
-        // up (b) pre-activations: dA = dH b silu'(a), dB = dH silu(a); each lane
-        // reads and writes its four adjacent columns directly.
+        // dH = w * (dout W2) and the SwiGLU backward with the saved gate (a)
+        // and up (b) pre-activations: dA = dH b silu'(a), dB = dH silu(a),
+        // plus w H = w silu(a) b for the dW2 product (routed rows). In four
+        // passes of 32 rows: the rows' a | b slices come into LDS as whole
+        // rows, each lane turns its four adjacent columns into dA | dB | w H
+        // in place, and the three slices go out as whole rows.
         const uint16_t* AB = static_cast<const uint16_t*>(shared ? p.ab_s : p.ab_r);
         uint16_t* dAB = static_cast<uint16_t*>(shared ? p.dab_s : p.dab_r);
+        uint16_t* WH = shared ? nullptr : static_cast<uint16_t*>(p.wh_r);
         const int64_t ld = 2 * static_cast<int64_t>(n_out);
+        constexpr int EP = 3 * TC + 8;  // LDS row: a | b | w H (pitch = 4 mod 64 dwords)
+        uint16_t* el = reinterpret_cast<uint16_t*>(lds);
+        const int col0 = t.nt * TC;
+        const int ncols = n_out - col0 < TC ? n_out - col0 : TC;  // multiple of 16
+        // 16-byte chunks of a pass's a | b rows held by each thread; the next
+        // pass's chunks are loaded while the current one is processed
+        constexpr int LCH = 32 * (2 * TC / 8) / PK_THREADS;
+        auto load_pass = [&](int i, uint4 (&v)[LCH]) {
+            const int rows_here = t.rows - i * 32;
+            const int64_t rbase = t.row0 + i * 32;
+#pragma unroll
+            for (int u = 0; u < LCH; ++u) {
+                const int q = threadIdx.x + u * PK_THREADS;
+                const int r = q / (2 * TC / 8), ch = q % (2 * TC / 8);
+                const int part = ch / (TC / 8), c = (ch % (TC / 8)) * 8;
+                v[u] = (r < rows_here && c < ncols)
+                           ? *reinterpret_cast<const uint4*>(AB + (rbase + r) * ld + part * n_out + col0 + c)
+                           : make_uint4(0, 0, 0, 0);
+            }
+        };
+        uint4 cur[LCH], nxt[LCH];
+        load_pass(0, cur);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int r = i * 32 + l32;
-            if (r >= t.rows) continue;
-            const int64_t row = t.row0 + r;
-            const float w = shared ? 1.0f : p.wrow[row];
+            const int rows_here = t.rows - i * 32;
+            if (rows_here <= 0) break;  // uniform
+            const int64_t rbase = t.row0 + i * 32;
+#pragma unroll
+            for (int u = 0; u < LCH; ++u) {
+                const int q = threadIdx.x + u * PK_THREADS;
+                const int r = q / (2 * TC / 8), ch = q % (2 * TC / 8);
+                *reinterpret_cast<uint4*>(el + r * EP + (ch / (TC / 8)) * TC + (ch % (TC / 8)) * 8) = cur[u];
+            }
+            if (i + 1 < 4) load_pass(i + 1, nxt);
+            __syncthreads();
+            const float w = shared ? 1.0f : (l32 < rows_here ? p.wrow[rbase + l32] : 0.0f);
+            uint16_t* er = el + l32 * EP;
 #pragma unroll
             for (int g = 0; g < 2; ++g)
 #pragma unroll
                 for (int vq = 0; vq < 4; ++vq) {
-                    const int col = t.nt * TC + wave * 64 + g * 32 + 8 * vq + 4 * half;
-                    if (col >= n_out) continue;  // n_out % 4 == 0: four columns are all in or all out
-                    const uint2 av = *reinterpret_cast<const uint2*>(AB + row * ld + col);
-                    const uint2 bv = *reinterpret_cast<const uint2*>(AB + row * ld + n_out + col);
+                    const int col = wave * 64 + g * 32 + 8 * vq + 4 * half;
+                    const uint2 av = *reinterpret_cast<const uint2*>(er + col);
+                    const uint2 bv = *reinterpret_cast<const uint2*>(er + TC + col);
                     const float a[4] = {__uint_as_float(av.x << 16), __uint_as_float(av.x & 0xffff0000u),
                                         __uint_as_float(av.y << 16), __uint_as_float(av.y & 0xffff0000u)};
-                    const float b[4] = {__uint_as_float(bv.x << 16), __uint_as_float(bv.x & 0xffff0000u),
-                                        __uint_as_float(bv.y << 16), __uint_as_float(bv.y & 0xffff0000u)};
-                    float da[4], db[4];
+                    const float bb[4] = {__uint_as_float(bv.x << 16), __uint_as_float(bv.x & 0xffff0000u),
+                                         __uint_as_float(bv.y << 16), __uint_as_float(bv.y & 0xffff0000u)};
+                    float da[4], db[4], wh[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float dh = w * acc[i][g][4 * vq + e];
                         const float sg = 1.0f / (1.0f + __expf(-a[e]));
-                        da[e] = dh * b[e] * (sg * (1.0f + a[e] * (1.0f - sg)));
-                        db[e] = dh * a[e] * sg;
+                        const float sa = a[e] * sg;  // silu(a)
+                        da[e] = dh * bb[e] * (sg + sa * (1.0f - sg));
+                        db[e] = dh * sa;
+                        wh[e] = w * sa * bb[e];
                     }
-                    *reinterpret_cast<uint2*>(dAB + row * ld + col) = pack4(da[0], da[1], da[2], da[3]);
-                    *reinterpret_cast<uint2*>(dAB + row * ld + n_out + col) = pack4(db[0], db[1], db[2], db[3]);
+                    *reinterpret_cast<uint2*>(er + col) = pack4(da[0], da[1], da[2], da[3]);
+                    *reinterpret_cast<uint2*>(er + TC + col) = pack4(db[0], db[1], db[2], db[3]);
+                    *reinterpret_cast<uint2*>(er + 2 * TC + col) = pack4(wh[0], wh[1], wh[2], wh[3]);
                 }
+            __syncthreads();
+            const int nparts = WH != nullptr ? 3 : 2;
+            for (int q = threadIdx.x; q < 32 * (3 * TC / 8); q += PK_THREADS) {
+                const int r = q / (3 * TC / 8), ch = q % (3 * TC / 8);
+                const int part = ch / (TC / 8), c = (ch % (TC / 8)) * 8;
+                if (r < rows_here && c < ncols && part < nparts) {
+                    const uint4 v = *reinterpret_cast<const uint4*>(el + r * EP + part * TC + c);
+                    if (part < 2) *reinterpret_cast<uint4*>(dAB + (rbase + r) * ld + part * n_out + col0 + c) = v;
+                    else *reinterpret_cast<uint4*>(WH + (rbase + r) * n_out + col0 + c) = v;
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int u = 0; u < LCH; ++u) cur[u] = nxt[u];
         }
         return;
     }
@@ -1006,6 +1039,7 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work, int
     g.w2t = g.ws2t = g.w13t = g.ws13t = nullptr;
     g.ab_r = g.ab_s = g.dab_r = g.dab_s = g.dx_r = g.dx_s = nullptr;
     g.wrow = nullptr;
+    g.wh_r = nullptr;
     return g;
 }
 
@@ -1158,6 +1192,7 @@ hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const Bw
     g.dx_r = bp.dx_r;
     g.dx_s = bp.dx_s;
     g.wrow = bp.wrow;
+    g.wh_r = bp.wh_r;
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, PK_BM, nt_r, nt_s, has_shared, part)));
     if (grid.x == 0) return hipSuccess;
     if (mode == 3) hipLaunchKernelGGL(gemm_bf16_pk_kernel<3>, grid, dim3(PK_THREADS), 0, stream, g);

@@ -113,16 +113,19 @@ struct BwdGemmPtrs {
     void* dx_r;         // [R][d]
     void* dx_s;         // [T][d]
     const float* wrow;  // [R]
+    void* wh_r;         // [R][inter] w H of the routed rows (written by mode 4)
     int32_t* work4;     // [E + 2] table of mode 4
 };
 // mode 3: recomputed gate/up pre-activations; 4: dH = w dout W2 with the SwiGLU
-// backward -> [dA dB]; 5: dX = [dA dB] W13. part: 1 routed, 2 shared.
+// backward -> [dA dB] (and w H for routed rows); 5: dX = [dA dB] W13. part: 1
+// routed, 2 shared.
 hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const BwdGemmPtrs& bp, int part,
                            hipStream_t stream);
-// dW[g][m][n] = sum over the group's rows of A[amap(r)][m] * ascale(r) * B[bmap(r)][n] (bf16 out)
-hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int64_t lda,
-                        const int32_t* amap, const float* ascale, const void* B, int64_t ldb, const int32_t* bmap,
-                        void* out, hipStream_t stream);
+// dW[g][m][n] = sum over the group's rows r of A[amap(r)][m] * B[bmap(r)][n] (bf16 out); at most
+// one of amap / bmap (map_len entries) is given; A has a_rows rows of lda elements, B b_rows of ldb.
+hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int lda,
+                        int a_rows, const int32_t* amap, const void* B, int ldb, int b_rows, const int32_t* bmap,
+                        int map_len, void* out, hipStream_t stream);
 size_t router_bwd_workspace_bytes(int64_t T, int d, int E);
 hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int64_t T, int k, float* wrow,
                               hipStream_t stream);

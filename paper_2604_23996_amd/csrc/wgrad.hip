@@ -1,18 +1,23 @@
 // Expert weight gradients of the layer backward: for each group g (a routed
 // expert over its expert-contiguous rows, or the merged shared expert over
 // all tokens)
-//   dW_g[m][n] = sum_r A[ra(r)][m] * sa(r) * B[rb(r)][n]
-// with optional row maps (the permutation's token of a routed row) and a row
-// scale (the combine weight): dW2 = (w dout)^T H, dW13 = [dA dB]^T X.
+//   dW_g[m][n] = sum_r A[ra(r)][m] * B[rb(r)][n]
+// where at most one operand has a row map (the permutation's token of a
+// routed row): dW2 = dout^T (w H) with dout gathered, dW13 = [dA dB]^T X
+// with x gathered.
 //
 // Tiles of 128 (m) x 256 (n), 4 waves of 64 x 128, K = the group's rows in
-// slices of 32. Both operands are staged row-major in LDS (rows = K) and the
-// MFMA fragments, which need 8 consecutive rows of one column per lane, come
-// from the transposing LDS read ds_read_b64_tr_b16 (in each 16-lane group,
-// lane j gives the address of row j/4, columns 4 (j%4) .. + 3 and receives
-// column j of those four rows). The accumulators hold n x m tiles, so each
-// lane stores four adjacent n of one m as 8 bytes. bf16 operands, fp32
-// accumulation, bf16 gradients.
+// stages of 32 through a 3-stage LDS ring filled by buffer loads straight to
+// LDS (no staging registers), two stages in flight while one is consumed.
+// Both operands sit row-major in LDS (rows = K, 256 or 512 bytes) with the
+// 16-byte chunks of row r XOR-swizzled by 4 (r % 4); the MFMA fragments, 8
+// consecutive rows of one column per lane, come from the transposing read
+// ds_read_b64_tr_b16 (in each 16-lane group, lane j gives the address of row
+// j / 4, columns 4 (j % 4) .. + 3, and receives column j of those four rows),
+// which with that swizzle touches 64 distinct banks per 32 lanes. A row map
+// is itself brought into LDS by a buffer load one stage ahead of the data it
+// addresses. bf16 operands, fp32 accumulation, bf16 gradients written as
+// full rows through LDS.
 #include "common.h"
 #include "kernels.h"
 
@@ -20,46 +25,70 @@ namespace smoes {
 
 namespace {
 
-constexpr int WG_TM = 128, WG_TN = 256, WG_BK = 32, WG_THREADS = 256;
-// row pitches (elements) at which the transposing reads hit distinct banks
-constexpr int WG_PA = WG_TM + 32, WG_PB = WG_TN + 32;
-constexpr int WG_ACH = WG_BK * WG_TM / 8 / WG_THREADS;  // 16-byte A chunks per thread per slice (2)
-constexpr int WG_BCH = WG_BK * WG_TN / 8 / WG_THREADS;  // B chunks (4)
+constexpr int WG_TM = 128, WG_TN = 256, WG_BK = 32, WG_ST = 3, WG_THREADS = 256;
+constexpr int WG_ARB = WG_TM * 2, WG_BRB = WG_TN * 2;          // row bytes in LDS
+constexpr int WG_AB = WG_BK * WG_ARB, WG_BB = WG_BK * WG_BRB;  // 8 KB + 16 KB per stage
+constexpr int WG_SB = WG_AB + WG_BB;
+constexpr int WG_IA = WG_AB / 1024 / 4, WG_IB = WG_BB / 1024 / 4;  // 1 KB loads per wave per stage (2, 4)
+constexpr int WG_IDX = 1024;                                      // row-map bytes per stage (4 waves x 256)
+constexpr int WG_LDS = WG_ST * WG_SB + WG_ST * WG_IDX;
+constexpr int WG_OP = WG_TN + 8;  // epilogue row pitch (elements)
+static_assert(WG_TM * WG_OP * 2 <= WG_ST * WG_SB, "epilogue tile fits the ring");
 
-typedef int wg_i32x4 __attribute__((ext_vector_type(4)));
 typedef short wg_v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) wg_v4i16 wg_lds_v4i16;
+
+// Buffer loads straight to LDS, as inline assembly. With the builtin form the
+// compiler sees the LDS writes and, unable to tell them apart from the
+// transposing reads of other ring slots, waits for every outstanding load
+// before each read, which would drain the ring. Here the kernel orders them
+// itself: vmcnt waits plus a barrier before a slot is read.
+// Descriptor words: base (48 bits, stride 0), record count in bytes, format.
+__device__ __forceinline__ i32x4_t wg_rsrc(const void* base, int bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return i32x4_t{__builtin_amdgcn_readfirstlane(static_cast<int>(a & 0xffffffffu)),
+                   __builtin_amdgcn_readfirstlane(static_cast<int>((a >> 32) & 0xffffu)),
+                   __builtin_amdgcn_readfirstlane(bytes), kBufferFlags};
+}
+__device__ __forceinline__ uint32_t wg_lds_addr(const void* p) {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)p));
+}
+// 16 bytes per lane from byte offset voff into LDS at lds + 16 lane (lds uniform)
+__device__ __forceinline__ void wg_dma16(i32x4_t rsrc, int voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds))), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
+// 4 bytes per lane into LDS at lds + 4 lane
+__device__ __forceinline__ void wg_dma4(i32x4_t rsrc, int voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds))), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
 
 struct WgArgs {
     int64_t T;
     int n_groups;           // E routed experts, or 1 (shared)
     int M, N;               // output rows / columns of every group
     const int32_t* off;     // [E + 1] row ranges of the routed groups; NULL: one group of T rows
-    const uint16_t* A;      // row-major, lda columns
-    int64_t lda;
-    const int32_t* amap;    // A row of each K row (NULL: identity)
-    const float* ascale;    // scale of each K row (NULL: 1)
+    const uint16_t* A;      // row-major, lda columns, a_rows rows
+    int lda, a_rows;
     const uint16_t* B;
-    int64_t ldb;
-    const int32_t* bmap;
+    int ldb, b_rows;
+    const int32_t* map;     // row map of the gathered operand ([map_len]); NULL: none
+    int map_len;
     uint16_t* out;          // [n_groups][M][N]
 };
 
-__device__ __forceinline__ uint4 scale_bf16x8(uint4 v, float s) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t o[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float lo = __uint_as_float(w[i] << 16) * s, hi = __uint_as_float(w[i] & 0xffff0000u) * s;
-        o[i] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
-    }
-    return make_uint4(o[0], o[1], o[2], o[3]);
-}
+__device__ __forceinline__ int wg_swz(int row) { return 4 * (row & 3); }
 
+// G: 0 no row map, 1 A's rows through the map, 2 B's rows through the map.
+template <int G>
 __global__ void __launch_bounds__(WG_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 wgrad_kernel(WgArgs p) {
-    __shared__ __attribute__((aligned(16))) uint16_t a_lds[2][WG_BK * WG_PA];
-    __shared__ __attribute__((aligned(16))) uint16_t b_lds[2][WG_BK * WG_PB];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[WG_LDS];
     const int tiles_m = static_cast<int>(ceil_div(p.M, WG_TM)), tiles_n = static_cast<int>(ceil_div(p.N, WG_TN));
     const int per = tiles_m * tiles_n;
     const int nblk = p.n_groups * per;
@@ -69,52 +98,68 @@ wgrad_kernel(WgArgs p) {
     if (b >= nblk) return;
     const int g = b / per, tt = b % per;
     const int m0 = (tt / tiles_n) * WG_TM, n0 = (tt % tiles_n) * WG_TN;
-    const int64_t r0 = p.off ? p.off[g] : 0, r1 = p.off ? p.off[g + 1] : p.T;
+    const int r0 = uniform_int(p.off ? p.off[g] : 0);
+    const int r1 = uniform_int(p.off ? p.off[g + 1] : static_cast<int>(p.T));
     const int nk = static_cast<int>(ceil_div(r1 - r0, WG_BK));
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int wm = wave >> 1, wn = wave & 1;
+    uint8_t* idx_lds = lds + WG_ST * WG_SB;
 
-    uint4 ar[WG_ACH], br[WG_BCH];
-    auto load_slice = [&](int kb) {
+    const i32x4_t rsA = wg_rsrc(p.A, p.a_rows * p.lda * 2);
+    const i32x4_t rsB = wg_rsrc(p.B, p.b_rows * p.ldb * 2);
+    const i32x4_t rsM = wg_rsrc(G ? p.map : nullptr, G ? p.map_len * 4 : 0);
+    const uint32_t lds0 = wg_lds_addr(lds);
+
+    // Load q of this wave (A: rows (wave * IA + q) * 4 + lane / 16, B: rows
+    // (wave * IB + q) * 2 + lane / 32 of a stage) moves global chunk
+    // (slot ^ swizzle(row)) of its row into slot lane % 16 (A) / lane % 32 (B).
+    // Column offsets (elements) and the row in the stage are fixed per tile.
+    int a_row[WG_IA], a_col[WG_IA], b_row[WG_IB], b_col[WG_IB];
 #pragma unroll
-        for (int i = 0; i < WG_ACH; ++i) {
-            const int id = threadIdx.x + i * WG_THREADS;
-            const int row = id / (WG_TM / 8), c = id % (WG_TM / 8);
-            const int64_t r = r0 + static_cast<int64_t>(kb) * WG_BK + row;
-            const int col = m0 + c * 8;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (r < r1 && col < p.M) {
-                const int64_t src = p.amap ? p.amap[r] : r;
-                v = *reinterpret_cast<const uint4*>(p.A + src * p.lda + col);
-                if (p.ascale) v = scale_bf16x8(v, p.ascale[r]);
-            }
-            ar[i] = v;
-        }
+    for (int q = 0; q < WG_IA; ++q) {
+        a_row[q] = (wave * WG_IA + q) * 4 + lane / 16;
+        const int col = m0 + ((lane % 16) ^ wg_swz(a_row[q])) * 8;
+        a_col[q] = col < p.M ? col : -1;
+    }
 #pragma unroll
-        for (int i = 0; i < WG_BCH; ++i) {
-            const int id = threadIdx.x + i * WG_THREADS;
-            const int row = id / (WG_TN / 8), c = id % (WG_TN / 8);
-            const int64_t r = r0 + static_cast<int64_t>(kb) * WG_BK + row;
-            const int col = n0 + c * 8;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (r < r1 && col < p.N) {
-                const int64_t src = p.bmap ? p.bmap[r] : r;
-                v = *reinterpret_cast<const uint4*>(p.B + src * p.ldb + col);
-            }
-            br[i] = v;
+    for (int q = 0; q < WG_IB; ++q) {
+        b_row[q] = (wave * WG_IB + q) * 2 + lane / 32;
+        const int col = n0 + ((lane % 32) ^ wg_swz(b_row[q])) * 8;
+        b_col[q] = col < p.N ? col : -1;
+    }
+    // Row map of stage s into index slot s % 3: wave w loads rows 8 w .. 8 w + 7
+    // (lanes 0..7; the other lanes' loads are out of range and write zeros).
+    auto issue_idx = [&](int s) {
+        if constexpr (G != 0) {
+            const int r = r0 + s * WG_BK + wave * 8 + lane;
+            const int vo = (lane < 8 && r < r1) ? r * 4 : kOutOfRange;
+            wg_dma4(rsM, vo, lds0 + WG_ST * WG_SB + (s % WG_ST) * WG_IDX + wave * 256);
         }
     };
-    auto store_slice = [&](int buf) {
+    auto map_of = [&](int s, int row) {
+        return *reinterpret_cast<const int32_t*>(idx_lds + (s % WG_ST) * WG_IDX + (row / 8) * 256 + (row % 8) * 4);
+    };
+    // Byte offsets of this lane's loads for stage s (the map read from LDS);
+    // kOutOfRange for rows past K and columns past the matrix.
+    auto src_offs = [&](int s, int (&va)[WG_IA], int (&vb)[WG_IB]) {
 #pragma unroll
-        for (int i = 0; i < WG_ACH; ++i) {
-            const int id = threadIdx.x + i * WG_THREADS;
-            *reinterpret_cast<uint4*>(&a_lds[buf][(id / (WG_TM / 8)) * WG_PA + (id % (WG_TM / 8)) * 8]) = ar[i];
+        for (int q = 0; q < WG_IA; ++q) {
+            const int r = r0 + s * WG_BK + a_row[q];
+            const int src = r < r1 ? (G == 1 ? map_of(s, a_row[q]) : r) : -1;
+            va[q] = (src >= 0 && a_col[q] >= 0) ? (src * p.lda + a_col[q]) * 2 : kOutOfRange;
         }
 #pragma unroll
-        for (int i = 0; i < WG_BCH; ++i) {
-            const int id = threadIdx.x + i * WG_THREADS;
-            *reinterpret_cast<uint4*>(&b_lds[buf][(id / (WG_TN / 8)) * WG_PB + (id % (WG_TN / 8)) * 8]) = br[i];
+        for (int q = 0; q < WG_IB; ++q) {
+            const int r = r0 + s * WG_BK + b_row[q];
+            const int src = r < r1 ? (G == 2 ? map_of(s, b_row[q]) : r) : -1;
+            vb[q] = (src >= 0 && b_col[q] >= 0) ? (src * p.ldb + b_col[q]) * 2 : kOutOfRange;
         }
+    };
+    auto issue_a = [&](int s, int q, int vo) {
+        wg_dma16(rsA, vo, lds0 + (s % WG_ST) * WG_SB + (wave * WG_IA + q) * 1024);
+    };
+    auto issue_b = [&](int s, int q, int vo) {
+        wg_dma16(rsB, vo, lds0 + (s % WG_ST) * WG_SB + WG_AB + (wave * WG_IB + q) * 1024);
     };
 
     f32x16_t acc[4][2];  // [n tile][m tile]: rows n, columns m
@@ -123,66 +168,135 @@ wgrad_kernel(WgArgs p) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) acc[q][i] = f32x16_t{};
     // per-lane part of the transposing reads: 16-lane group grp covers columns
-    // 16 (grp & 1) .. + 15 of a 32-column tile and rows 8 (grp >> 1) .. + 7
+    // 16 (grp & 1) .. + 15 of a 32-column tile and rows 8 (grp >> 1) .. + 7;
+    // byte offsets in a stage for substep ks (rows 16 ks ..), the hi half 4
+    // rows further (r % 4 is the same for both halves)
     const int grp = lane >> 4, j = lane & 15;
     const int trow = 8 * (grp >> 1) + (j >> 2), tcol = 16 * (grp & 1) + 4 * (j & 3);
-    auto frag = [&](const uint16_t* base, int pitch, int k0, int c0) {
-        const wg_v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wg_lds_v4i16*)(base + (k0 + trow) * pitch + c0 + tcol));
-        const wg_v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wg_lds_v4i16*)(base + (k0 + 4 + trow) * pitch + c0 + tcol));
-        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
-        return __builtin_bit_cast(bf16x8_t, wg_i32x4{static_cast<int>(l2.x), static_cast<int>(l2.y),
-                                                     static_cast<int>(h2.x), static_cast<int>(h2.y)});
+    auto frag_off = [&](int rb, int k0, int c0) {
+        const int col = c0 + tcol, r = k0 + trow;
+        return static_cast<uint32_t>(r * rb + ((col >> 3) ^ wg_swz(r)) * 16 + (col & 7) * 2);
     };
+    uint32_t fa[2][2], fb[2][4];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) fa[ks][i] = frag_off(WG_ARB, ks * 16, wm * 64 + i * 32);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) fb[ks][q] = WG_AB + frag_off(WG_BRB, ks * 16, wn * 128 + q * 32);
+    }
+    auto frag = [&](uint32_t addr, auto rb4_c) {
+        constexpr int RB4 = decltype(rb4_c)::value;
+        const wg_v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wg_lds_v4i16*)(uintptr_t)addr);
+        const wg_v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wg_lds_v4i16*)(uintptr_t)(addr + RB4));
+        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        return __builtin_bit_cast(bf16x8_t, i32x4_t{static_cast<int>(l2.x), static_cast<int>(l2.y),
+                                                    static_cast<int>(h2.x), static_cast<int>(h2.y)});
+    };
+    using RA4 = std::integral_constant<int, 4 * WG_ARB>;
+    using RB4 = std::integral_constant<int, 4 * WG_BRB>;
 
-    if (nk > 0) load_slice(0);
-    for (int kb = 0; kb < nk; ++kb) {
-        const int buf = kb & 1;
-        store_slice(buf);
-        __syncthreads();  // the slice is visible; the other buffer's readers (slice kb - 1) are done
-        if (kb + 1 < nk) load_slice(kb + 1);
-        const uint16_t* al = a_lds[buf];
-        const uint16_t* bl = b_lds[buf];
+    // Issue order: I(0), I(1) | D(0), I(2), D(1) | per stage s: I(s + 3), D(s + 2).
+    // Before stage s, at most D(s + 1) (IA + IB loads) may still fly: D(s) and
+    // I(s + 2) have landed. The barrier then makes every wave's loads visible
+    // and frees the data slot D(s + 2) overwrites (read in stage s - 1) and the
+    // index slot I(s + 3) overwrites (read when D(s) was issued). Past the end
+    // of K every load is out of range and writes zeros, so the counts stay exact.
+    if constexpr (G != 0) {
+        issue_idx(0);
+        issue_idx(1);
+        wait_vm_lgkm0<0>();
+        __builtin_amdgcn_s_barrier();
+    }
+    {
+        int va[WG_IA], vb[WG_IB];
+        src_offs(0, va, vb);
+#pragma unroll
+        for (int q = 0; q < WG_IA; ++q) issue_a(0, q, va[q]);
+#pragma unroll
+        for (int q = 0; q < WG_IB; ++q) issue_b(0, q, vb[q]);
+        issue_idx(2);
+        src_offs(1, va, vb);
+#pragma unroll
+        for (int q = 0; q < WG_IA; ++q) issue_a(1, q, va[q]);
+#pragma unroll
+        for (int q = 0; q < WG_IB; ++q) issue_b(1, q, vb[q]);
+    }
+    for (int s = 0; s < nk; ++s) {
+        wait_vm_lgkm0<WG_IA + WG_IB>();
+        __builtin_amdgcn_s_barrier();
+        int va[WG_IA], vb[WG_IB];
+        src_offs(s + 2, va, vb);
+        issue_idx(s + 3);
+        const uint32_t sb = lds0 + (s % WG_ST) * WG_SB;
+        bf16x8_t mf[2][2], nf[2][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) mf[0][i] = frag(sb + fa[0][i], RA4{});
+#pragma unroll
+        for (int q = 0; q < 4; ++q) nf[0][q] = frag(sb + fb[0][q], RB4{});
 #pragma unroll
         for (int ks = 0; ks < WG_BK / 16; ++ks) {
-            bf16x8_t mf[2], nf[4];
+            // this substep's share of the next loads: A and half of B, then the rest of B
+            if (ks == 0) {
 #pragma unroll
-            for (int i = 0; i < 2; ++i) mf[i] = frag(al, WG_PA, ks * 16, wm * 64 + i * 32);
+                for (int q = 0; q < WG_IA; ++q) issue_a(s + 2, q, va[q]);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) nf[q] = frag(bl, WG_PB, ks * 16, wn * 128 + q * 32);
+                for (int q = 0; q < WG_IB / 2; ++q) issue_b(s + 2, q, vb[q]);
+#pragma unroll
+                for (int i = 0; i < 2; ++i) mf[1][i] = frag(sb + fa[1][i], RA4{});
+#pragma unroll
+                for (int q = 0; q < 4; ++q) nf[1][q] = frag(sb + fb[1][q], RB4{});
+            } else {
+#pragma unroll
+                for (int q = WG_IB / 2; q < WG_IB; ++q) issue_b(s + 2, q, vb[q]);
+            }
 #pragma unroll
             for (int q = 0; q < 4; ++q)
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
-                    acc[q][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(nf[q], mf[i], acc[q][i], 0, 0, 0);
+                    acc[q][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(nf[ks][q], mf[ks][i], acc[q][i], 0, 0, 0);
         }
     }
-    // element v of lane l of acc[q][i]: n = 8 (v / 4) + 4 (l / 32) + v % 4 of tile q, m = l % 32 of tile i
-    uint16_t* O = p.out + static_cast<int64_t>(g) * p.M * p.N;
+    wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
+    __builtin_amdgcn_s_barrier();
+
+    // element v of lane l of acc[q][i]: n = 8 (v / 4) + 4 (l / 32) + v % 4 of
+    // tile q, m = l % 32 of tile i; four adjacent n go to LDS as 8 bytes, then
+    // whole 512-byte rows to memory
+    uint16_t* ot = reinterpret_cast<uint16_t*>(lds);
     const int half = lane >> 5, l32 = lane & 31;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int m = m0 + wm * 64 + i * 32 + l32;
-        if (m >= p.M) continue;
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
 #pragma unroll
             for (int vq = 0; vq < 4; ++vq) {
-                const int n = n0 + wn * 128 + q * 32 + 8 * vq + 4 * half;
-                if (n >= p.N) continue;  // N % 4 == 0
                 const f32x16_t& a = acc[q][i];
-                *reinterpret_cast<uint2*>(O + static_cast<int64_t>(m) * p.N + n) = make_uint2(
-                    static_cast<uint32_t>(f32_to_bf16(a[4 * vq])) | (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 1])) << 16),
-                    static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 2])) | (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 3])) << 16));
+                *reinterpret_cast<uint2*>(ot + (wm * 64 + i * 32 + l32) * WG_OP + wn * 128 + q * 32 + 8 * vq +
+                                          4 * half) =
+                    make_uint2(static_cast<uint32_t>(f32_to_bf16(a[4 * vq])) |
+                                   (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 1])) << 16),
+                               static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 2])) |
+                                   (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 3])) << 16));
             }
+    __syncthreads();
+    uint16_t* O = p.out + static_cast<int64_t>(g) * p.M * p.N;
+    constexpr int CH = WG_TN / 8;
+    for (int q = threadIdx.x; q < WG_TM * CH; q += WG_THREADS) {
+        const int r = q / CH, c = (q % CH) * 8;
+        if (m0 + r < p.M && n0 + c < p.N)  // N % 8 == 0: a chunk is all in or all out
+            *reinterpret_cast<uint4*>(O + static_cast<int64_t>(m0 + r) * p.N + n0 + c) =
+                *reinterpret_cast<const uint4*>(ot + r * WG_OP + c);
     }
 }
 
 }  // namespace
 
-hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int64_t lda,
-                        const int32_t* amap, const float* ascale, const void* B, int64_t ldb, const int32_t* bmap,
-                        void* out, hipStream_t stream) {
+hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int lda,
+                        int a_rows, const int32_t* amap, const void* B, int ldb, int b_rows, const int32_t* bmap,
+                        int map_len, void* out, hipStream_t stream) {
     if (n_groups == 0 || M == 0 || N == 0) return hipSuccess;
+    if (amap != nullptr && bmap != nullptr) return hipErrorInvalidValue;  // one row map at most
     WgArgs p;
     p.T = T;
     p.n_groups = n_groups;
@@ -191,15 +305,18 @@ hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* of
     p.off = off;
     p.A = static_cast<const uint16_t*>(A);
     p.lda = lda;
-    p.amap = amap;
-    p.ascale = ascale;
+    p.a_rows = a_rows;
     p.B = static_cast<const uint16_t*>(B);
     p.ldb = ldb;
-    p.bmap = bmap;
+    p.b_rows = b_rows;
+    p.map = amap != nullptr ? amap : bmap;
+    p.map_len = map_len;
     p.out = static_cast<uint16_t*>(out);
     const int64_t nblk = static_cast<int64_t>(n_groups) * ceil_div(M, WG_TM) * ceil_div(N, WG_TN);
-    hipLaunchKernelGGL(wgrad_kernel, dim3(static_cast<unsigned>(8 * ceil_div(nblk, 8))), dim3(WG_THREADS), 0, stream,
-                       p);
+    const dim3 grid(static_cast<unsigned>(8 * ceil_div(nblk, 8)));
+    if (amap != nullptr) hipLaunchKernelGGL(wgrad_kernel<1>, grid, dim3(WG_THREADS), 0, stream, p);
+    else if (bmap != nullptr) hipLaunchKernelGGL(wgrad_kernel<2>, grid, dim3(WG_THREADS), 0, stream, p);
+    else hipLaunchKernelGGL(wgrad_kernel<0>, grid, dim3(WG_THREADS), 0, stream, p);
     return hipGetLastError();
 }
 

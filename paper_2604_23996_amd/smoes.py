@@ -484,6 +484,11 @@ def alloc_outputs(spec: LayerSpec, device, act_torch_dtype, want_logits=True, wa
     }
 
 
+def backward_workspace_bytes(spec: LayerSpec) -> int:
+    desc = spec.c()
+    return int(lib().smoes_backward_workspace_bytes(ctypes.byref(desc)))
+
+
 def pack_transposed_weights(spec: LayerSpec, dev_in: Dict[str, Optional[torch.Tensor]]) -> Dict[str, torch.Tensor]:
     """The transposed packed expert weights the backward reads (from the
     row-major bf16 weights in dev_in: w13, w2, ws13, ws2)."""
@@ -497,11 +502,14 @@ def pack_transposed_weights(spec: LayerSpec, dev_in: Dict[str, Optional[torch.Te
 def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
                  outputs: Dict[str, Optional[torch.Tensor]], fwd_workspace: torch.Tensor,
                  packed_t: Dict[str, torch.Tensor], dout: torch.Tensor,
-                 dlogits_aux: Optional[torch.Tensor] = None, want_dw: bool = True) -> Dict[str, torch.Tensor]:
+                 dlogits_aux: Optional[torch.Tensor] = None, want_dw: bool = True,
+                 grads: Optional[Dict[str, Optional[torch.Tensor]]] = None,
+                 workspace: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
     """smoes_moe_backward after moe_forward with the same inputs / outputs /
     workspace. `inputs` must hold the packed w13 / ws13 and the float32
     w_gate; returns the gradients (dx, dw_gate, dbias, dz, dw, dw13, dw2,
-    dws13, dws2)."""
+    dws13, dws2), written into `grads` when given (as returned by an earlier
+    call), with `workspace` reused when given."""
     desc = spec.c()
     io = SmoesLayerIO()
     for name in _IO_FIELDS:
@@ -513,7 +521,8 @@ def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
     io.streams = None
     T, d, E, k, I, SI = spec.T, spec.d, spec.E, spec.k, spec.inter, spec.shared_inter
     dev = dout.device
-    g = {"dx": torch.empty((T, d), dtype=torch.float32, device=dev),
+    g = grads if grads is not None else {
+         "dx": torch.empty((T, d), dtype=torch.float32, device=dev),
          "dw_gate": torch.empty((E, d), dtype=torch.float32, device=dev),
          "dbias": torch.empty(E, dtype=torch.float32, device=dev),
          "dz": torch.empty((T, E), dtype=torch.float32, device=dev),
@@ -526,7 +535,10 @@ def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
     for name in _GRAD_FIELDS:
         setattr(G, name, None if g[name] is None else _p(g[name]).value)
     nbytes = int(lib().smoes_backward_workspace_bytes(ctypes.byref(desc)))
-    ws = _workspace(nbytes, dev)
+    if workspace is not None and workspace.numel() >= nbytes:
+        ws, nbytes = workspace, workspace.numel()
+    else:
+        ws = _workspace(nbytes, dev)
     _check(lib().smoes_moe_backward(ctypes.byref(desc), ctypes.byref(io), _p(packed_t["w13t"]), _p(packed_t["w2t"]),
                                     _p(packed_t.get("ws13t")), _p(packed_t.get("ws2t")), _p(dout), _p(dlogits_aux),
                                     ctypes.byref(G), _p(fwd_workspace), fwd_workspace.numel(), _p(ws), nbytes,
