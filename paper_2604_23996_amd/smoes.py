@@ -438,10 +438,18 @@ class Events:
     """2 * SMOES_N_STAGES HIP events for the forward's stage timing: events
     2s and 2s + 1 bracket stage s on the stream that runs it."""
 
-    def __init__(self, n: int = 2 * N_STAGES):
+    def __init__(self, n: int = 2 * N_STAGES, only: Optional[int] = None):
+        """only: make just the two events of that stage (the others stay NULL,
+        so the forward records nothing for them)."""
         self.n = n
         self.arr = (c_void * n)()
-        _check(lib().smoes_events_create(n, self.arr), "smoes_events_create")
+        if only is None:
+            self._own, self._own_n = self.arr, n
+        else:
+            self._own, self._own_n = (c_void * 2)(), 2
+        _check(lib().smoes_events_create(self._own_n, self._own), "smoes_events_create")
+        if only is not None:
+            self.arr[2 * only], self.arr[2 * only + 1] = self._own[0], self._own[1]
 
     def stage_ms(self, stage: int) -> float:
         return self.elapsed_ms(2 * stage, 2 * stage + 1)
@@ -453,8 +461,8 @@ class Events:
 
     def close(self):
         if self.arr is not None:
-            lib().smoes_events_destroy(self.n, self.arr)
-            self.arr = None
+            lib().smoes_events_destroy(self._own_n, self._own)
+            self.arr = self._own = None
 
     def __del__(self):
         try:
