@@ -248,7 +248,10 @@ typedef struct smoes_layer {
     int update_stats; /* fold the batch into the Gaussian state before scoring */
     int weights_packed; /* 1: w13, w2, ws13, ws2 are in the packed order of smoes_pack_weights
                            (SMOES_BF16 only); 0: row-major as in smoes_layer_io */
-    int reserved;       /* must be 0 */
+    int save_preact;    /* 1: smoes_moe_forward also keeps the experts' gate and up
+                           pre-activations (bf16, in its workspace) for
+                           smoes_moe_backward, which then skips recomputing them
+                           (packed bf16 layers only); 0: it does not */
 } smoes_layer;
 
 /* Side streams for smoes_moe_forward (caller-owned; see smoes_streams_create). */
@@ -409,7 +412,9 @@ size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
  * or their renormalised form) and the full softmax; dlogits_aux ([T, E]
  * float32, e.g. io->dlogits of the MI loss, plus the bin balance gradient),
  * when not NULL, is added to the logit gradient; the modality scores are
- * constants. The experts' gate and up pre-activations are recomputed.
+ * constants. The experts' gate and up pre-activations are read from the
+ * forward workspace when desc->save_preact is 1 (the forward kept them),
+ * else recomputed.
  * Reads from io: x, w13 and ws13 (packed), w_gate (float32 row-major),
  * probs, topk_idx, topk_w, and expert_offsets / perm_token / perm_inv (or
  * the forward workspace's copies when those are NULL).

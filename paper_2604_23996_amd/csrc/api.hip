@@ -278,6 +278,8 @@ struct LayerWs {
     void* mi;
     void* permute;
     void* experts;
+    void* ab_r;  // kept pre-activations (save_preact), else NULL
+    void* ab_s;
 };
 
 int check_layer(const smoes_layer* L) {
@@ -300,7 +302,9 @@ int check_layer(const smoes_layer* L) {
             2 * static_cast<int64_t>(L->inter > L->shared_inter ? L->inter : L->shared_inter) * L->d * es > lim)
             return SMOES_ERR_SHAPE;
     }
-    if ((L->weights_packed != 0 && L->weights_packed != 1) || L->reserved != 0) return SMOES_ERR_ARG;
+    if ((L->weights_packed != 0 && L->weights_packed != 1) || (L->save_preact != 0 && L->save_preact != 1))
+        return SMOES_ERR_ARG;
+    if (L->save_preact && !L->weights_packed) return SMOES_ERR_ARG;
     if (L->weights_packed && L->act_dtype != SMOES_BF16) return SMOES_ERR_ARG;
     if (!(L->beta >= 0.0f && L->beta <= 1.0f) || !(L->var_floor >= 0.0f) || L->tau != L->tau ||
         L->grad_scale != L->grad_scale)
@@ -322,6 +326,11 @@ size_t layer_ws_parts(const smoes_layer* L, LayerWs* out, void* base) {
     w.mi = c.take(mi_workspace_bytes(T, L->E, L->n_batch, L->n_bins));
     w.permute = c.take(permute_workspace_bytes(T, L->E, L->k));
     w.experts = c.take(experts_workspace_bytes(T, L->d, L->E, L->k, L->inter, L->shared_inter, L->act_dtype));
+    w.ab_r = w.ab_s = nullptr;
+    if (L->save_preact) {
+        w.ab_r = c.take(sizeof(uint16_t) * T * L->k * 2 * L->inter);
+        w.ab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
+    }
     if (out != nullptr) *out = w;
     return c.used + kAlign;
 }
@@ -392,6 +401,8 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     a.perm_inv = perm_inv;
     a.topk_w = io->topk_w;
     a.out = io->out;
+    a.ab_r = w.ab_r;
+    a.ab_s = L->shared_inter > 0 ? w.ab_s : nullptr;
     const WorkTables wt = experts_work_tables(a, w.experts);
 
     // Caller's stream s: route -> permute -> routed GEMM1 -> routed GEMM2 ->
@@ -478,8 +489,9 @@ size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     Carver c(base);
     const int64_t T = L->T, R = L->T * L->k;
     BwdWs w;
-    w.ab_r = c.take(sizeof(uint16_t) * R * 2 * L->inter);
-    w.ab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
+    // the pre-activations are recomputed here unless the forward kept them
+    w.ab_r = c.take(L->save_preact ? 0 : sizeof(uint16_t) * R * 2 * L->inter);
+    w.ab_s = c.take(L->save_preact ? 0 : sizeof(uint16_t) * T * 2 * L->shared_inter);
     w.dab_r = c.take(sizeof(uint16_t) * R * 2 * L->inter);
     w.dab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
     w.dx_r = c.take(sizeof(uint16_t) * R * L->d);
@@ -550,6 +562,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     a.perm_inv = perm_inv;
     a.topk_w = io->topk_w;
     a.out = nullptr;
+    a.ab_r = a.ab_s = nullptr;
     const ExpertFwdBuffers fb = experts_fwd_buffers(a, fw.experts);
     BwdGemmPtrs bp;
     bp.dout = dout;
@@ -557,8 +570,8 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     bp.ws2t = ws2t;
     bp.w13t = w13t;
     bp.ws13t = ws13t;
-    bp.ab_r = bw.ab_r;
-    bp.ab_s = bw.ab_s;
+    bp.ab_r = L->save_preact ? fw.ab_r : bw.ab_r;
+    bp.ab_s = L->save_preact ? fw.ab_s : bw.ab_s;
     bp.dab_r = bw.dab_r;
     bp.dab_s = bw.dab_s;
     bp.dx_r = bw.dx_r;
@@ -574,7 +587,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
     SMOES_BTRY(launch_router_bwd(dout, fb.y_r, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T, L->d,
                                  L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, s));
-    for (int mode = 3; mode <= 5; ++mode) {
+    for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode) {
         SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 1, s));
         if (sh) SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 2, s));
     }

@@ -456,12 +456,15 @@ constexpr int PK_BM = 128, PK_BK = 64, PK_WAVES = 4, PK_THREADS = PK_WAVES * 64,
 constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instructions per wave per stage
 // Modes: 1 GEMM1 (+ SwiGLU), 2 GEMM2, and for the backward 3 GEMM1 with the
 // raw gate and up outputs, 4 dH = dout W2 (rows gathered, scaled by the combine
-// weight) with the SwiGLU backward in the epilogue, 5 dX = [dA dB] W13. Modes
-// 1 and 3 pair gate and up groups (32 H columns per wave); 2, 4 and 5 give each
-// wave two consecutive 32-column groups.
-constexpr int pk_family(int mode) { return (mode == 1 || mode == 3) ? 1 : 2; }
+// weight) with the SwiGLU backward in the epilogue, 5 dX = [dA dB] W13, and 6
+// GEMM1 writing both H and the gate and up outputs (a forward that keeps them
+// for the backward). Modes 1, 3 and 6 pair gate and up groups (32 H columns
+// per wave); 2, 4 and 5 give each wave two consecutive 32-column groups.
+constexpr int pk_family(int mode) { return (mode == 1 || mode == 3 || mode == 6) ? 1 : 2; }
 constexpr int pk_tile_cols(int mode) { return pk_family(mode) == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
-constexpr int pk_out_cols(int mode) { return mode == 3 ? 2 * pk_tile_cols(mode) : pk_tile_cols(mode); }
+constexpr int pk_out_cols(int mode) {
+    return (mode == 3 || mode == 6) ? 2 * pk_tile_cols(mode) : pk_tile_cols(mode);
+}
 constexpr int pk_epi_bytes(int mode) {
     return mode == 4 ? 32 * (3 * pk_tile_cols(mode) + 8) * 2 : PK_BM * (pk_out_cols(mode) + 8) * 2;
 }
@@ -483,8 +486,8 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     constexpr int TC = pk_tile_cols(MODE);
     __shared__ __attribute__((aligned(1024))) uint8_t lds[pk_lds_bytes(MODE)];
     constexpr int FAM = pk_family(MODE);
-    const int nt_r = static_cast<int>(ceil_div((MODE == 1 || MODE == 3 || MODE == 4) ? p.inter : p.d, TC));
-    const int nt_s = (MODE == 1 || MODE == 3 || MODE == 4) ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
+    const int nt_r = static_cast<int>(ceil_div((FAM == 1 || MODE == 4) ? p.inter : p.d, TC));
+    const int nt_s = (FAM == 1 || MODE == 4) ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
     if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, p.part, t)) return;
     const bool shared = t.g == p.E;
@@ -555,7 +558,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         const int R = (wave * IA + q) * 8 + lane / 8;
         const int rr = R < t.rows ? R : 0;
         int src;
-        if ((MODE == 1 || MODE == 3 || MODE == 4) && !shared) src = p.perm_token[t.row0 + rr];
+        if ((FAM == 1 || MODE == 4) && !shared) src = p.perm_token[t.row0 + rr];
         else src = static_cast<int>(t.row0 + rr);
         aoff[q] = R < t.rows ? static_cast<uint32_t>(src) * static_cast<uint32_t>(K) : (1u << 30);
         achk[q] = ((lane % 8) ^ ((R / 2) % 8)) * 8;
@@ -775,55 +778,67 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         }
         return;
     }
-    constexpr int OC = pk_out_cols(MODE);  // tile columns written (mode 3: gate block then up block)
-    constexpr int OP = OC + 8;
-    uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
+    // OK: 1 H = silu(gate) * up, 3 the gate | up pre-activations, 2 / 5 the
+    // plain accumulators. Mode 6 writes H, then the pre-activations.
+    auto epilogue = [&](auto ok_c) {
+        constexpr int OK = decltype(ok_c)::value;
+        constexpr int OC = OK == 3 ? 2 * TC : TC;  // tile columns written (3: gate block then up block)
+        constexpr int OP = OC + 8;
+        uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int r = i * 32 + l32;
+        for (int i = 0; i < 4; ++i) {
+            const int r = i * 32 + l32;
 #pragma unroll
-        for (int vq = 0; vq < 4; ++vq) {
-            const int c0 = 8 * vq + 4 * half;
-            if constexpr (MODE == 1) {
-                float h[4];
+            for (int vq = 0; vq < 4; ++vq) {
+                const int c0 = 8 * vq + 4 * half;
+                if constexpr (OK == 1) {
+                    float h[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) h[e] = silu(acc[i][0][4 * vq + e]) * acc[i][1][4 * vq + e];
-                *reinterpret_cast<uint2*>(otile + r * OP + wave * 32 + c0) = pack4(h[0], h[1], h[2], h[3]);
-            } else if constexpr (MODE == 3) {
+                    for (int e = 0; e < 4; ++e) h[e] = silu(acc[i][0][4 * vq + e]) * acc[i][1][4 * vq + e];
+                    *reinterpret_cast<uint2*>(otile + r * OP + wave * 32 + c0) = pack4(h[0], h[1], h[2], h[3]);
+                } else if constexpr (OK == 3) {
 #pragma unroll
-                for (int g = 0; g < 2; ++g)
-                    *reinterpret_cast<uint2*>(otile + r * OP + g * TC + wave * 32 + c0) =
-                        pack4(acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
-            } else {
+                    for (int g = 0; g < 2; ++g)
+                        *reinterpret_cast<uint2*>(otile + r * OP + g * TC + wave * 32 + c0) = pack4(
+                            acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
+                } else {
 #pragma unroll
-                for (int g = 0; g < 2; ++g)
-                    *reinterpret_cast<uint2*>(otile + r * OP + wave * 64 + g * 32 + c0) =
-                        pack4(acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
+                    for (int g = 0; g < 2; ++g)
+                        *reinterpret_cast<uint2*>(otile + r * OP + wave * 64 + g * 32 + c0) = pack4(
+                            acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
+                }
             }
         }
-    }
-    __syncthreads();
-    uint16_t* O;
-    if constexpr (MODE == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
-    else if constexpr (MODE == 3) O = shared ? static_cast<uint16_t*>(p.ab_s) : static_cast<uint16_t*>(p.ab_r);
-    else if constexpr (MODE == 5) O = shared ? static_cast<uint16_t*>(p.dx_s) : static_cast<uint16_t*>(p.dx_r);
-    else O = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
-    constexpr int CH = OC / 8;
-    const int col0 = t.nt * TC;
-    for (int q = threadIdx.x; q < BM * CH; q += PK_THREADS) {
-        const int r = q / CH, ch = q % CH;
-        if constexpr (MODE == 3) {  // gate block to columns [0, n_out), up block to [n_out, 2 n_out)
-            const int part = (ch * 8) / TC;
-            const int c = col0 + ch * 8 - part * TC;
-            if (r < t.rows && c < n_out)
-                *reinterpret_cast<uint4*>(O + (t.row0 + r) * (2 * static_cast<int64_t>(n_out)) + part * n_out + c) =
-                    *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
-        } else {
-            const int c = col0 + ch * 8;
-            if (r < t.rows && c < n_out)  // n_out % 8 == 0: a chunk is all in or all out
-                *reinterpret_cast<uint4*>(O + (t.row0 + r) * n_out + c) =
-                    *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+        __syncthreads();
+        uint16_t* O;
+        if constexpr (OK == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
+        else if constexpr (OK == 3) O = shared ? static_cast<uint16_t*>(p.ab_s) : static_cast<uint16_t*>(p.ab_r);
+        else if constexpr (OK == 5) O = shared ? static_cast<uint16_t*>(p.dx_s) : static_cast<uint16_t*>(p.dx_r);
+        else O = shared ? static_cast<uint16_t*>(p.y_s) : static_cast<uint16_t*>(p.y_r);
+        constexpr int CH = OC / 8;
+        const int col0 = t.nt * TC;
+        for (int q = threadIdx.x; q < BM * CH; q += PK_THREADS) {
+            const int r = q / CH, ch = q % CH;
+            if constexpr (OK == 3) {  // gate block to columns [0, n_out), up block to [n_out, 2 n_out)
+                const int part = (ch * 8) / TC;
+                const int c = col0 + ch * 8 - part * TC;
+                if (r < t.rows && c < n_out)
+                    *reinterpret_cast<uint4*>(O + (t.row0 + r) * (2 * static_cast<int64_t>(n_out)) + part * n_out +
+                                              c) = *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+            } else {
+                const int c = col0 + ch * 8;
+                if (r < t.rows && c < n_out)  // n_out % 8 == 0: a chunk is all in or all out
+                    *reinterpret_cast<uint4*>(O + (t.row0 + r) * n_out + c) =
+                        *reinterpret_cast<const uint4*>(otile + r * OP + ch * 8);
+            }
         }
+    };
+    if constexpr (MODE == 6) {
+        epilogue(std::integral_constant<int, 1>{});
+        __syncthreads();  // every H row chunk has left the tile
+        epilogue(std::integral_constant<int, 3>{});
+    } else {
+        epilogue(std::integral_constant<int, MODE>{});
     }
 }
 
@@ -1037,7 +1052,9 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work, int
     g.y_s = w.y_s;
     g.dout = nullptr;
     g.w2t = g.ws2t = g.w13t = g.ws13t = nullptr;
-    g.ab_r = g.ab_s = g.dab_r = g.dab_s = g.dx_r = g.dx_s = nullptr;
+    g.ab_r = a.ab_r;
+    g.ab_s = a.ab_s;
+    g.dab_r = g.dab_s = g.dx_r = g.dx_s = nullptr;
     g.wrow = nullptr;
     g.wh_r = nullptr;
     return g;
@@ -1103,7 +1120,9 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, int part, hipStre
     const GemmArgs g = make_args(a, w, w.work1, part);
     const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm, p.nt1_r, p.nt1_s, p.has_shared, part)));
     if (grid.x == 0) return hipSuccess;
-    if (a.act_dtype == 1 && a.packed)
+    if (a.act_dtype == 1 && a.packed && a.ab_r != nullptr)
+        hipLaunchKernelGGL(gemm_bf16_pk_kernel<6>, grid, dim3(PK_THREADS), 0, stream, g);
+    else if (a.act_dtype == 1 && a.packed)
         hipLaunchKernelGGL(gemm_bf16_pk_kernel<1>, grid, dim3(PK_THREADS), 0, stream, g);
     else if (a.act_dtype == 1)
         hipLaunchKernelGGL((gemm_bf16_dma_kernel<1, DCfg>), grid, dim3(DCfg::THREADS), 0, stream, g);

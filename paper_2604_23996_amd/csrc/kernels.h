@@ -64,6 +64,8 @@ struct ExpertArgs {
     const int32_t* perm_inv;        // [T, k]
     const float* topk_w;            // [T, k]
     void* out;                      // [T, d]
+    void* ab_r;                     // NULL, or [T k][2 inter]: GEMM1 also keeps the gate | up
+    void* ab_s;                     //   pre-activations (packed bf16 path); [T][2 shared_inter]
 };
 size_t experts_workspace_bytes(int64_t T, int d, int E, int k, int inter, int shared_inter,
                                int act_dtype);

@@ -44,7 +44,7 @@ class SmoesLayer(ctypes.Structure):
                 ("shared_inter", c_int), ("n_bins", c_int), ("n_batch", c_int), ("act_dtype", c_int),
                 ("tau", c_float), ("beta", c_float), ("var_floor", c_float), ("grad_scale", c_float),
                 ("renorm_topk", c_int), ("update_stats", c_int), ("weights_packed", c_int),
-                ("reserved", c_int)]
+                ("save_preact", c_int)]
 
 
 _IO_FIELDS = ["x", "modality_id", "sample_offsets", "w_gate", "logit_bias", "expert_to_bin", "w13",
@@ -368,12 +368,13 @@ class LayerSpec:
     renorm_topk: bool = False
     update_stats: bool = False
     weights_packed: bool = False
+    save_preact: bool = False
 
     def c(self) -> SmoesLayer:
         return SmoesLayer(self.T, self.d, self.E, self.k, self.inter, self.shared_inter, self.n_bins,
                           self.n_batch, self.act_dtype, self.tau, self.beta, self.var_floor,
                           self.grad_scale, int(self.renorm_topk), int(self.update_stats),
-                          int(self.weights_packed), 0)
+                          int(self.weights_packed), int(self.save_preact))
 
 
 def workspace_bytes(spec: LayerSpec) -> int:

@@ -84,7 +84,7 @@ def pack_layer_weights(spec: S.LayerSpec, dev_in) -> None:
 
 
 def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None, packed=None,
-                  streams=None, renorm_topk=False, keep_workspace=False):
+                  streams=None, renorm_topk=False, keep_workspace=False, save_preact=False):
     """The full layer through smoes_moe_forward. For layers that do not update
     their statistics in the call, the Gaussian state is first estimated from
     the batch by smoes_modality_score(update=1) from the zero state. bf16
@@ -93,7 +93,8 @@ def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=Non
     upd = cfg.update_stats if update_stats is None else update_stats
     if packed is None:
         packed = cfg.dtype == W.BF16
-    spec = layer_spec(cfg, update_stats=upd, weights_packed=packed, renorm_topk=renorm_topk)
+    spec = layer_spec(cfg, update_stats=upd, weights_packed=packed, renorm_topk=renorm_topk,
+                      save_preact=save_preact)
     dev_in = {
         "x": t(inp.x), "modality_id": t(inp.modality_id), "sample_offsets": t(inp.sample_offsets),
         "w_gate": t(inp.w_gate if w_gate is None else w_gate), "logit_bias": t(inp.logit_bias),

@@ -159,8 +159,10 @@ def test_backward_struct_and_host_checks():
     n = L.smoes_backward_workspace_bytes(ctypes.byref(desc))
     assert n > 0
     bad = _spec().c()
-    bad.reserved = 1
+    bad.save_preact = 3
     assert L.smoes_backward_workspace_bytes(ctypes.byref(bad)) == 0
+    kept = _spec(d=128, inter=96, shared_inter=48, weights_packed=True, save_preact=True).c()
+    assert 0 < L.smoes_backward_workspace_bytes(ctypes.byref(kept)) < n
     io = S.SmoesLayerIO()
     G = S.SmoesLayerGrads()
     args = lambda d_: (ctypes.byref(d_), ctypes.byref(io), FAKE, FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(G),
@@ -210,8 +212,11 @@ def test_packed_weight_sizes_and_checks():
     assert L.smoes_pack_weights(ctypes.byref(desc), 9, FAKE, FAKE, None) == S.SMOES_ERR_ARG
     f32 = _spec(act_dtype=0).c()
     assert L.smoes_pack_weights(ctypes.byref(f32), S.SMOES_W13, FAKE, FAKE, None) == S.SMOES_ERR_ARG
-    # packed weights are a bf16 layout; reserved must stay 0
+    # packed weights are a bf16 layout; save_preact is 0 or 1
     assert S.workspace_bytes(_spec(act_dtype=0, weights_packed=True)) == 0
     bad = _spec().c()
-    bad.reserved = 1
+    bad.save_preact = 2
     assert L.smoes_workspace_bytes(ctypes.byref(bad)) == 0
+    # keeping the pre-activations is a packed bf16 feature, and it grows the workspace
+    assert S.workspace_bytes(_spec(save_preact=True)) == 0
+    assert S.workspace_bytes(_spec(weights_packed=True, save_preact=True)) > S.workspace_bytes(_spec(weights_packed=True))

@@ -67,14 +67,14 @@ def _mask_ties(inp, dout, gap=1e-3):
     return dout
 
 
-def run_gpu_backward(inp, dout, aux, renorm, want_dw=True):
+def run_gpu_backward(inp, dout, aux, renorm, want_dw=True, save_preact=False):
     """Forward then backward on the device; returns (spec, outs, grads)."""
     cfg = inp.cfg
     rowmajor = {"w13": t(inp.w13), "w2": t(inp.w2), "ws13": t(inp.ws13), "ws2": t(inp.ws2)}
     spec_t = layer_spec(cfg, weights_packed=True)
     packed_t = S.pack_transposed_weights(spec_t, rowmajor)
     torch.cuda.synchronize()
-    spec, dev_in, outs, ws = run_gpu_layer(inp, renorm_topk=renorm, keep_workspace=True)
+    spec, dev_in, outs, ws = run_gpu_layer(inp, renorm_topk=renorm, keep_workspace=True, save_preact=save_preact)
     g = S.moe_backward(spec, dev_in, outs, ws, packed_t, t(dout), None if aux is None else t(aux), want_dw=want_dw)
     torch.cuda.synchronize()
     return spec, outs, g
@@ -126,6 +126,20 @@ def test_backward_experts_without_tokens_have_zero_gradient():
     dw13, dw2 = host(g["dw13"]), host(g["dw2"])
     assert np.all(dw13[~used] == 0.0) and np.all(dw2[~used] == 0.0)
     assert np.all(np.abs(dw13[used]).reshape(int(used.sum()), -1).max(axis=1) > 0)
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2, 4])
+def test_backward_with_kept_preactivations_matches_recompute(layer):
+    # the forward that keeps the gate / up pre-activations (save_preact) runs
+    # the same MFMA sequence as the backward's recompute: identical bits
+    cfg, inp, dout, aux = _inputs(LAYERS[layer], 300 + layer)
+    say("backward kept pre-activations", layer)
+    _, o1, g1 = run_gpu_backward(inp, dout, aux, True)
+    _, o2, g2 = run_gpu_backward(inp, dout, aux, True, save_preact=True)
+    assert torch.equal(o1["out"], o2["out"])
+    for name in g1:
+        if g1[name] is not None:
+            assert torch.equal(g1[name], g2[name]), name
 
 
 def test_backward_is_reproducible():
