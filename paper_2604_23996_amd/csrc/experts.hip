@@ -1149,17 +1149,24 @@ hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, int part, hipStre
 // ---------------------------------------------------------------- backward (modes 3-5)
 
 // Work table of one tiling (bm rows x nt column tiles per routed expert, then
-// the shared items): one thread, E <= 256.
-__global__ void bwd_work_kernel(const int32_t* __restrict__ off, int E, int64_t T, int bm, int nt_r, int nt_s,
-                                int has_shared, int32_t* __restrict__ work) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    int32_t acc = 0;
-    work[0] = 0;
-    for (int g = 0; g < E; ++g) {
-        acc += static_cast<int32_t>(ceil_div(off[g + 1] - off[g], bm)) * nt_r;
-        work[g + 1] = acc;
+// the shared items): one block of 256 threads, thread g counts expert g's items
+// and an LDS scan forms the prefix sums (E <= 256).
+__global__ void __launch_bounds__(256)
+bwd_work_kernel(const int32_t* __restrict__ off, int E, int64_t T, int bm, int nt_r, int nt_s, int has_shared,
+                int32_t* __restrict__ work) {
+    __shared__ int32_t sc[256];
+    const int g = threadIdx.x;
+    sc[g] = g < E ? static_cast<int32_t>(ceil_div(off[g + 1] - off[g], bm)) * nt_r : 0;
+    __syncthreads();
+    for (int o = 1; o < 256; o <<= 1) {  // inclusive scan
+        const int32_t v = g >= o ? sc[g - o] : 0;
+        __syncthreads();
+        sc[g] += v;
+        __syncthreads();
     }
-    work[E + 1] = acc + (has_shared ? static_cast<int32_t>(ceil_div(T, bm)) * nt_s : 0);
+    if (g == 0) work[0] = 0;
+    if (g < E) work[g + 1] = sc[g];
+    if (g == 0) work[E + 1] = sc[E - 1] + (has_shared ? static_cast<int32_t>(ceil_div(T, bm)) * nt_s : 0);
 }
 
 ExpertFwdBuffers experts_fwd_buffers(const ExpertArgs& a, void* ws) {
@@ -1189,7 +1196,7 @@ hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const Bw
         nt_s = static_cast<int>(ceil_div(a.shared_inter, pk_tile_cols(4)));
         work = bp.work4;
         if (part != 2) {
-            hipLaunchKernelGGL(bwd_work_kernel, dim3(1), dim3(64), 0, stream, a.expert_offsets, a.E, a.T, PK_BM, nt_r,
+            hipLaunchKernelGGL(bwd_work_kernel, dim3(1), dim3(256), 0, stream, a.expert_offsets, a.E, a.T, PK_BM, nt_r,
                                nt_s, has_shared ? 1 : 0, bp.work4);
             const hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
