@@ -31,7 +31,8 @@ constexpr int WG_AB = WG_BK * WG_ARB, WG_BB = WG_BK * WG_BRB;  // 8 KB + 16 KB p
 constexpr int WG_SB = WG_AB + WG_BB;
 constexpr int WG_IA = WG_AB / 1024 / 4, WG_IB = WG_BB / 1024 / 4;  // 1 KB loads per wave per stage (2, 4)
 constexpr int WG_IDX = 1024;                                      // row-map bytes per stage (4 waves x 256)
-constexpr int WG_LDS = WG_ST * WG_SB + WG_ST * WG_IDX;
+constexpr int WG_NI = 4;                                          // row-map slots
+constexpr int WG_LDS = WG_ST * WG_SB + WG_NI * WG_IDX;
 constexpr int WG_OP = WG_TN + 8;  // epilogue row pitch (elements)
 static_assert(WG_TM * WG_OP * 2 <= WG_ST * WG_SB, "epilogue tile fits the ring");
 
@@ -127,17 +128,17 @@ wgrad_kernel(WgArgs p) {
         const int col = n0 + ((lane % 32) ^ wg_swz(b_row[q])) * 8;
         b_col[q] = col < p.N ? col : -1;
     }
-    // Row map of stage s into index slot s % 3: wave w loads rows 8 w .. 8 w + 7
+    // Row map of stage s into index slot s % 4: wave w loads rows 8 w .. 8 w + 7
     // (lanes 0..7; the other lanes' loads are out of range and write zeros).
     auto issue_idx = [&](int s) {
         if constexpr (G != 0) {
             const int r = r0 + s * WG_BK + wave * 8 + lane;
             const int vo = (lane < 8 && r < r1) ? r * 4 : kOutOfRange;
-            wg_dma4(rsM, vo, lds0 + WG_ST * WG_SB + (s % WG_ST) * WG_IDX + wave * 256);
+            wg_dma4(rsM, vo, lds0 + WG_ST * WG_SB + (s % WG_NI) * WG_IDX + wave * 256);
         }
     };
     auto map_of = [&](int s, int row) {
-        return *reinterpret_cast<const int32_t*>(idx_lds + (s % WG_ST) * WG_IDX + (row / 8) * 256 + (row % 8) * 4);
+        return *reinterpret_cast<const int32_t*>(idx_lds + (s % WG_NI) * WG_IDX + (row / 8) * 256 + (row % 8) * 4);
     };
     // Byte offsets of this lane's loads for stage s (the map read from LDS);
     // kOutOfRange for rows past K and columns past the matrix.
@@ -196,12 +197,32 @@ wgrad_kernel(WgArgs p) {
     using RA4 = std::integral_constant<int, 4 * WG_ARB>;
     using RB4 = std::integral_constant<int, 4 * WG_BRB>;
 
-    // Issue order: I(0), I(1) | D(0), I(2), D(1) | per stage s: I(s + 3), D(s + 2).
-    // Before stage s, at most D(s + 1) (IA + IB loads) may still fly: D(s) and
-    // I(s + 2) have landed. The barrier then makes every wave's loads visible
-    // and frees the data slot D(s + 2) overwrites (read in stage s - 1) and the
-    // index slot I(s + 3) overwrites (read when D(s) was issued). Past the end
-    // of K every load is out of range and writes zeros, so the counts stay exact.
+    // Issue order: I(0), I(1) | D(0), I(2), D(1), I(3) | per stage s: I(s + 4),
+    // D(s + 2). Stage s starts with its first substep's fragments in registers
+    // (read at the end of stage s - 1). Halfway through it waits until at most
+    // I(s + 4) and D(s + 2) may still fly (so D(s + 1) and I(s + 3) have
+    // landed) and lgkmcnt is 0 (its second substep's fragments are in
+    // registers), passes a barrier, and reads stage s + 1's first fragments
+    // while its second substep's MFMAs run. After that barrier no wave reads
+    // stage s's data slot any more (D(s + 3) overwrites it) nor the index slot
+    // of stage s + 1 (I(s + 5) overwrites it). Past the end of K every load is
+    // out of range and writes zeros, so the counts stay exact.
+    constexpr int PEND = WG_IA + WG_IB + (G != 0 ? 1 : 0);
+    const uint32_t sb0 = lds0;
+    bf16x8_t mf[2][2], nf[2][4];
+    auto read_frags = [&](uint32_t sb, int ks, bf16x8_t (&m)[2], bf16x8_t (&n)[4]) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) m[i] = frag(sb + fa[ks][i], RA4{});
+#pragma unroll
+        for (int q = 0; q < 4; ++q) n[q] = frag(sb + fb[ks][q], RB4{});
+    };
+    auto mfma_step = [&](const bf16x8_t (&m)[2], const bf16x8_t (&n)[4]) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                acc[q][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(n[q], m[i], acc[q][i], 0, 0, 0);
+    };
     if constexpr (G != 0) {
         issue_idx(0);
         issue_idx(1);
@@ -221,41 +242,28 @@ wgrad_kernel(WgArgs p) {
         for (int q = 0; q < WG_IA; ++q) issue_a(1, q, va[q]);
 #pragma unroll
         for (int q = 0; q < WG_IB; ++q) issue_b(1, q, vb[q]);
+        issue_idx(3);
+        wait_vm_lgkm0<PEND>();  // D(0) and I(2) have landed
+        __builtin_amdgcn_s_barrier();
+        read_frags(sb0, 0, mf[0], nf[0]);
     }
     for (int s = 0; s < nk; ++s) {
-        wait_vm_lgkm0<WG_IA + WG_IB>();
-        __builtin_amdgcn_s_barrier();
         int va[WG_IA], vb[WG_IB];
         src_offs(s + 2, va, vb);
-        issue_idx(s + 3);
+        issue_idx(s + 4);
         const uint32_t sb = lds0 + (s % WG_ST) * WG_SB;
-        bf16x8_t mf[2][2], nf[2][4];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) mf[0][i] = frag(sb + fa[0][i], RA4{});
+        for (int q = 0; q < WG_IA; ++q) issue_a(s + 2, q, va[q]);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) nf[0][q] = frag(sb + fb[0][q], RB4{});
+        for (int q = 0; q < WG_IB / 2; ++q) issue_b(s + 2, q, vb[q]);
+        read_frags(sb, 1, mf[1], nf[1]);
+        mfma_step(mf[0], nf[0]);
 #pragma unroll
-        for (int ks = 0; ks < WG_BK / 16; ++ks) {
-            // this substep's share of the next loads: A and half of B, then the rest of B
-            if (ks == 0) {
-#pragma unroll
-                for (int q = 0; q < WG_IA; ++q) issue_a(s + 2, q, va[q]);
-#pragma unroll
-                for (int q = 0; q < WG_IB / 2; ++q) issue_b(s + 2, q, vb[q]);
-#pragma unroll
-                for (int i = 0; i < 2; ++i) mf[1][i] = frag(sb + fa[1][i], RA4{});
-#pragma unroll
-                for (int q = 0; q < 4; ++q) nf[1][q] = frag(sb + fb[1][q], RB4{});
-            } else {
-#pragma unroll
-                for (int q = WG_IB / 2; q < WG_IB; ++q) issue_b(s + 2, q, vb[q]);
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-                    acc[q][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(nf[ks][q], mf[ks][i], acc[q][i], 0, 0, 0);
-        }
+        for (int q = WG_IB / 2; q < WG_IB; ++q) issue_b(s + 2, q, vb[q]);
+        wait_vm_lgkm0<PEND>();
+        __builtin_amdgcn_s_barrier();
+        if (s + 1 < nk) read_frags(lds0 + ((s + 1) % WG_ST) * WG_SB, 0, mf[0], nf[0]);
+        mfma_step(mf[1], nf[1]);
     }
     wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
     __builtin_amdgcn_s_barrier();
