@@ -51,8 +51,7 @@ int check_mi_shape(int64_t T, int E, int n_batch, int n_bins) {
 
 // Total workspace of the standalone entry points (max alignment slack included).
 size_t route_ws(int64_t T, int d, int E, int x_dtype) {
-    (void)T;
-    return router_workspace_bytes(d, E, x_dtype) + 2 * kAlign;
+    return router_workspace_bytes(T, d, E, x_dtype) + 2 * kAlign;
 }
 size_t modality_ws(int64_t T, int d) { return modality_workspace_bytes(T, d) + 2 * kAlign; }
 size_t mi_ws(int64_t T, int E, int n_batch, int n_bins) {
@@ -102,7 +101,7 @@ int smoes_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gat
     const size_t need = route_ws(T, d, E, x_dtype);
     if (x_dtype == SMOES_BF16 && (workspace == nullptr || workspace_bytes < need)) return SMOES_ERR_WORKSPACE;
     Carver c(workspace);
-    void* ws = x_dtype == SMOES_BF16 ? c.take(router_workspace_bytes(d, E, x_dtype)) : nullptr;
+    void* ws = x_dtype == SMOES_BF16 ? c.take(router_workspace_bytes(T, d, E, x_dtype)) : nullptr;
     return hip_status(launch_route(x, x_dtype, T, d, w_gate, nullptr, logit_bias, E, k, renorm_topk ? 1 : 0,
                                    logits, probs, topk_idx, topk_w, ws, as_stream(stream)));
 }
@@ -321,7 +320,7 @@ size_t layer_ws_parts(const smoes_layer* L, LayerWs* out, void* base) {
     w.offsets = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 1)));
     w.perm_token = static_cast<int32_t*>(c.take(sizeof(int32_t) * T * L->k));
     w.perm_inv = static_cast<int32_t*>(c.take(sizeof(int32_t) * T * L->k));
-    w.route = c.take(router_workspace_bytes(L->d, L->E, L->act_dtype));
+    w.route = c.take(router_workspace_bytes(T, L->d, L->E, L->act_dtype));
     w.modality = c.take(modality_workspace_bytes(T, L->d));
     w.mi = c.take(mi_workspace_bytes(T, L->E, L->n_batch, L->n_bins));
     w.permute = c.take(permute_workspace_bytes(T, L->E, L->k));

@@ -10,8 +10,7 @@
 namespace smoes {
 
 // ---------------------------------------------------------------- router
-size_t router_workspace_bytes(int d, int E, int x_dtype);
-size_t router_lds_bytes(int E, int x_dtype);
+size_t router_workspace_bytes(int64_t T, int d, int E, int x_dtype);
 // w_split: router weights already in the split fragment order of
 // launch_split_wgate (bf16 x only), or NULL to split w_gate into ws first
 hipError_t launch_route(const void* x, int x_dtype, int64_t T, int d, const float* w_gate,

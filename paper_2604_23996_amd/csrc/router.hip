@@ -1,15 +1,21 @@
 // Router: logits z = W_gate x (+ b), full softmax g and top-k (Sec. 3.1).
 //
-// One workgroup (8 waves) owns 16 * TT tokens (TT = 1) and every expert. For bf16 activations the logits are fp32-faithful on the
-// matrix cores: the fp32 router weights are split into three bf16 terms
-// (hi + mid + lo reproduces the weight to ~2^-24), each product with the
-// exact bf16 activation is exact, and v_mfma_f32_16x16x32_bf16 accumulates in
-// fp32. The split weights are stored in the order the MFMA reads them, so a
-// wave loads each fragment as one contiguous 1 KB. The eight waves split the
-// hidden dimension; their partial tiles are summed in LDS in a fixed order,
-// then each wave runs the softmax and the top-k of its tokens (one lane per
-// expert, DPP reductions).
-// For fp32 activations the dot products are accumulated in fp64.
+// bf16 activations, two kernels:
+//   router_logits_kernel: the logits on the matrix cores, fp32-faithful: the
+//     fp32 router weights are split into three bf16 terms (hi + mid + lo
+//     reproduces each weight to ~2^-24), every product of a term with an exact
+//     bf16 activation is exact, and v_mfma_f32_16x16x32_bf16 accumulates in
+//     fp32. The split weights are stored in the order the MFMA reads them, so
+//     a wave loads a fragment as one contiguous 1 KB. A workgroup owns a tile
+//     of 64 or 128 tokens and one of KS ranges of the hidden dimension (KS
+//     chosen so that the grid fills the chip); its four waves split the
+//     experts, so every weight byte reaches a workgroup once per token tile.
+//     Each range's partial logits go to the workspace.
+//   router_topk_kernel: one wave per token sums the KS partials in range
+//     order, adds the bias, and runs the softmax and the top-k (one lane per
+//     expert, DPP reductions).
+// fp32 activations: one kernel, dot products accumulated in fp64, then the
+// same per-token softmax and top-k.
 #include "common.h"
 #include "kernels.h"
 
@@ -17,16 +23,37 @@ namespace smoes {
 
 namespace {
 
-constexpr int kRouterTokens = 16;  // tokens per MFMA tile
-constexpr int kRouterWaves = 8;
+constexpr int kRouterTokens = 16;  // tokens per fp32-path workgroup
+constexpr int kRouterWaves = 8;    // fp32 path
 constexpr int kRouterThreads = kRouterWaves * 64;
-constexpr int kRouterSlots = 4;  // LDS tree buffers of [16 TT][E_pad] floats (<= 64 KB)
+constexpr int kLogitWaves = 4;     // bf16 logits kernel: waves split the expert tiles
+constexpr int kTopkWaves = 4;      // top-k kernel: one wave per token
 
 __host__ __device__ inline int router_epad(int E) { return static_cast<int>(ceil_div(E, 16) * 16); }
-// Token tiles per workgroup. One (16 tokens) is fastest: larger tiles cut the
-// weight traffic but leave fewer workgroups to share the per-token softmax
-// and top-k, which then dominate.
-__host__ __device__ constexpr int router_tt(int /*NT*/) { return 1; }
+
+// Tiling of the bf16 logits kernel: NTW expert tiles of 16 per wave (4 waves
+// cover E_pad), TMT token tiles of 16 per workgroup, KS ranges of the hidden
+// dimension of `steps` 32-wide k-steps each (the last may be shorter).
+struct RouterPlan {
+    int ntw, tmt, ks, steps;
+};
+RouterPlan router_plan(int64_t T, int d, int E) {
+    RouterPlan p;
+    const int nt = router_epad(E) / 16;
+    p.ntw = static_cast<int>(ceil_div(nt, kLogitWaves));
+    p.tmt = (p.ntw == 2 || p.ntw == 3) ? 8 : 4;  // VGPRs: accumulators + the fragment sets
+    const int64_t tiles = ceil_div(T, 16 * p.tmt);
+    const int nsteps = static_cast<int>(ceil_div(d, 32));
+    // about one workgroup per CU, each range at least 8 k-steps long (a sweep
+    // of 1, 2, 4, 8 ranges and 32, 64, 128-token tiles at the four bf16
+    // workload shapes found this the fastest or within 3 % of it)
+    int ks = static_cast<int>(ceil_div(256, tiles > 0 ? tiles : 1));
+    const int ks_max = nsteps / 8 > 1 ? nsteps / 8 : 1;
+    ks = ks < 1 ? 1 : (ks > ks_max ? ks_max : ks);
+    p.steps = static_cast<int>(ceil_div(nsteps, ks));
+    p.ks = static_cast<int>(ceil_div(nsteps, p.steps));
+    return p;
+}
 
 // w_gate [E, d] f32 -> three bf16 parts (hi, mid, lo) in MFMA fragment order:
 // wpk[p][n][s][l][e] = part p of W[16 n + l % 16][32 s + 8 (l / 16) + e], zero
@@ -63,282 +90,281 @@ __global__ void split_wgate_kernel(const float* __restrict__ w, int E, int E_pad
     }
 }
 
-// Logits of one wave over its share of the hidden dimension (k-steps of 32,
-// s = wave, wave + 8, ...), bf16x3 MFMA over TT token tiles and NT expert
-// tiles; for small tiles the next step's fragments are loaded before the
-// current step's MFMAs. Then a fixed-order tree over the 8 waves through LDS
-// (wave w adds wave w + h, h = 4, 2, 1). The logits end at the start of the
-// buffer as [16 TT][E_pad + 1] (odd pitch: one lane per token reads them
-// without bank conflicts).
+// Partial logits of 16 * TMT tokens over k-steps [s0, s1) of the hidden
+// dimension (range blockIdx.y), all experts. Wave w owns expert tiles
+// w, w + 4, ... (NTW of them) and computes D = W x^T on the matrix cores
+// (experts as rows, tokens as columns), so a lane ends with four consecutive
+// experts of one token and stores them as one 16-byte vector. Each k-step
+// loads the wave's weight fragments (three bf16 terms) and the token
+// fragments, the next step's while this step's MFMAs run; the terms are
+// accumulated lo, mid, hi. NBUF fragment sets rotate, so the loads of the
+// next NBUF - 1 steps are in flight while a step's MFMAs run (two sets
+// measured as fast as three, four or six). Loads past the
+// hidden dimension, the range or the expert tiles are out of range and
+// return zeros (zero products add nothing).
 // 16x16x32 operands: lane l holds row (A) / column (B) l % 16 at k = 8 (l / 16) + 0..7;
 // result element i of lane l sits at row 4 (l / 16) + i, column l % 16.
-template <int TT, int NT>
-__device__ __forceinline__ void router_mfma_logits(const uint16_t* __restrict__ x, int64_t T, int d,
-                                   const uint16_t* __restrict__ wpk, int E_pad,
-                                   int64_t tok0, int wave, float* __restrict__ buf) {
+template <int TMT, int NTW, int NBUF>
+__global__ void __launch_bounds__(kLogitWaves * 64)
+router_logits_kernel(const uint16_t* __restrict__ x, int64_t T, int d, const uint16_t* __restrict__ wpk, int E_pad,
+                     int steps, float* __restrict__ part) {
     const int lane = lane_id();
-    const int quad = lane >> 4;
-    const int r = lane & 15;
-    // Buffer loads: an offset past the record count returns zeros, so the
-    // k tail and the steps past the end need no selects on loaded values.
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+    const int quad = lane >> 4, r = lane & 15;
+    const int nt = E_pad / 16;
+    const int nsteps = static_cast<int>(ceil_div(d, 32));
+    const int s0 = static_cast<int>(blockIdx.y) * steps;
+    const int s1 = s0 + steps < nsteps ? s0 + steps : nsteps;
+    const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * (16 * TMT);
     constexpr int kOob = 0x7fffffff;
     const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(x), 0, static_cast<int>(T * d * 2), 0x00020000);
-    const int nsteps = static_cast<int>(ceil_div(d, 32));
-    const int64_t part = static_cast<int64_t>(E_pad / 16) * nsteps * 512;
+    const int64_t term = static_cast<int64_t>(nt) * nsteps * 512;  // elements per weight term
     const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(wpk), 0, static_cast<int>(3 * part * 2), 0x00020000);
-    int xoff[TT];
+        const_cast<uint16_t*>(wpk), 0, static_cast<int>(3 * term * 2), 0x00020000);
+    int xoff[TMT];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
+    for (int tt = 0; tt < TMT; ++tt) {
         int64_t tok = tok0 + tt * 16 + r;
-        if (tok >= T) tok = T - 1;
+        if (tok >= T) tok = T - 1;  // computed but never stored
         xoff[tt] = static_cast<int>(tok * d * 2);
     }
-    f32x4_t acc[TT][NT];
+    f32x4_t acc[NTW][TMT];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt)
+    for (int j = 0; j < NTW; ++j)
 #pragma unroll
-        for (int n = 0; n < NT; ++n) acc[tt][n] = f32x4_t{};
-    typedef int i32x4 __attribute__((ext_vector_type(4)));
-    auto fetch = [&](int s, bf16x8_t (&a)[TT], bf16x8_t (&b)[NT][3]) {
+        for (int tt = 0; tt < TMT; ++tt) acc[j][tt] = f32x4_t{};
+    auto fetch = [&](int s, bf16x8_t (&a)[TMT], bf16x8_t (&b)[NTW][3]) {
         const int kk = s * 32 + quad * 8;
-        const int oob = (s < nsteps && kk < d) ? 0 : kOob;  // d % 8 == 0: an 8-chunk is all in or all out
+        const int oob = s < s1 ? 0 : kOob;  // d % 8 == 0: an 8-chunk is all in or all out
 #pragma unroll
-        for (int tt = 0; tt < TT; ++tt)
-            a[tt] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rsx, (xoff[tt] + kk * 2) | oob, 0, 0));
-        const int soob = s < nsteps ? 0 : kOob;
+        for (int tt = 0; tt < TMT; ++tt)
+            a[tt] = __builtin_bit_cast(bf16x8_t,
+                                       __builtin_amdgcn_raw_buffer_load_b128(rsx, (xoff[tt] + kk * 2) | oob, 0, 0));
 #pragma unroll
-        for (int n = 0; n < NT; ++n) {
+        for (int j = 0; j < NTW; ++j) {
+            const int n = wave + kLogitWaves * j;
+            const int noob = n < nt ? oob : kOob;
             const int off = static_cast<int>(((static_cast<int64_t>(n) * nsteps + s) * 64 + lane) * 16);
 #pragma unroll
             for (int p = 0; p < 3; ++p)
-                b[n][p] = __builtin_bit_cast(
-                    bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rsw, (static_cast<int>(p * part * 2) + off) | soob, 0, 0));
+                b[j][p] = __builtin_bit_cast(
+                    bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rsw, (static_cast<int>(p * term * 2) + off) | noob,
+                                                                     0, 0));
         }
     };
-    auto mfma3 = [&](const bf16x8_t (&a)[TT], const bf16x8_t (&b)[NT][3]) {
+    auto mfma3 = [&](const bf16x8_t (&a)[TMT], const bf16x8_t (&b)[NTW][3]) {
 #pragma unroll
-        for (int n = 0; n < NT; ++n)
+        for (int j = 0; j < NTW; ++j)
 #pragma unroll
-            for (int tt = 0; tt < TT; ++tt) {
-                acc[tt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[tt], b[n][2], acc[tt][n], 0, 0, 0);  // lo
-                acc[tt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[tt], b[n][1], acc[tt][n], 0, 0, 0);  // mid
-                acc[tt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[tt], b[n][0], acc[tt][n], 0, 0, 0);  // hi
+            for (int tt = 0; tt < TMT; ++tt) {
+                acc[j][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j][2], a[tt], acc[j][tt], 0, 0, 0);  // lo
+                acc[j][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j][1], a[tt], acc[j][tt], 0, 0, 0);  // mid
+                acc[j][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j][0], a[tt], acc[j][tt], 0, 0, 0);  // hi
             }
     };
-    if constexpr (TT * 4 + NT * 12 <= 72) {
-        // two named fragment sets: the loads of one step fly while the other's MFMAs run
-        bf16x8_t a0[TT], b0[NT][3], a1[TT], b1[NT][3];
-        fetch(wave, a0, b0);
-        for (int s = wave; s < nsteps; s += 2 * kRouterWaves) {
+    bf16x8_t a[NBUF][TMT], b[NBUF][NTW][3];
+#pragma unroll
+    for (int u = 0; u < NBUF - 1; ++u) fetch(s0 + u, a[u], b[u]);
+    for (int s = s0; s < s1; s += NBUF) {
+#pragma unroll
+        for (int u = 0; u < NBUF; ++u) {
             __builtin_amdgcn_sched_barrier(0);
-            fetch(s + kRouterWaves, a1, b1);
+            fetch(s + u + NBUF - 1, a[(u + NBUF - 1) % NBUF], b[(u + NBUF - 1) % NBUF]);
             __builtin_amdgcn_sched_barrier(0);
-            mfma3(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            fetch(s + 2 * kRouterWaves, a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma3(a1, b1);
-        }
-    } else {  // wide expert counts: no room for a second fragment set
-        bf16x8_t a0[TT], b0[NT][3];
-        for (int s = wave; s < nsteps; s += kRouterWaves) {
-            fetch(s, a0, b0);
-            mfma3(a0, b0);
+            mfma3(a[u], b[u]);
         }
     }
-    const int64_t tile = static_cast<int64_t>(kRouterTokens) * TT * E_pad;
-    auto at = [&](int which, int tt, int n, int i) -> float& {
-        return buf[which * tile + (tt * 16 + quad * 4 + i) * E_pad + n * 16 + r];
-    };
-    for (int h = kRouterWaves / 2; h >= 1; h >>= 1) {
-        // writers [h, 2h) hand their partials to readers [0, h)
-        if (wave >= h && wave < 2 * h) {
+    float* out = part + static_cast<int64_t>(blockIdx.y) * T * E_pad;
 #pragma unroll
-            for (int tt = 0; tt < TT; ++tt)
+    for (int j = 0; j < NTW; ++j) {
+        const int n = wave + kLogitWaves * j;
+        if (n >= nt) continue;
 #pragma unroll
-                for (int n = 0; n < NT; ++n)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) at(wave - h, tt, n, i) = acc[tt][n][i];
+        for (int tt = 0; tt < TMT; ++tt) {
+            const int64_t tok = tok0 + tt * 16 + r;
+            if (tok < T)
+                *reinterpret_cast<f32x4_t*>(out + tok * E_pad + n * 16 + quad * 4) = acc[j][tt];
         }
-        __syncthreads();
-        if (wave < h) {
-#pragma unroll
-            for (int tt = 0; tt < TT; ++tt)
-#pragma unroll
-                for (int n = 0; n < NT; ++n)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[tt][n][i] += at(wave, tt, n, i);
-        }
-        __syncthreads();
-    }
-    if (wave == 0) {  // final tile with an odd row pitch (the other tree slots are free by now)
-        const int zp = E_pad + 1;
-#pragma unroll
-        for (int tt = 0; tt < TT; ++tt)
-#pragma unroll
-            for (int n = 0; n < NT; ++n)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) buf[(tt * 16 + quad * 4 + i) * zp + n * 16 + r] = acc[tt][n][i];
     }
 }
 
-template <bool BF16, int NT, int TT>
-__global__ void __launch_bounds__(kRouterThreads)
-router_kernel(const void* __restrict__ x, int64_t T, int d, const float* __restrict__ w_gate,
-              const uint16_t* __restrict__ wsplit, const float* __restrict__ bias, int E, int E_pad,
-              int k, int renorm, float* __restrict__ logits, float* __restrict__ probs,
-              int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
-    extern __shared__ float smem[];
-    // bf16 path: smem = [4][16 TT][E_pad] tree buffers; fp32 path: the logits only.
-    // Either way the logits end as [16 TT][E_pad + 1] at the start of smem.
-    constexpr int WG_TOKENS = kRouterTokens * TT;
-    const int zp = E_pad + 1;
-    float* zrow = smem;
-    const int wave = threadIdx.x / kWave;
-    const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * WG_TOKENS;
-    const int ntok = static_cast<int>(T - tok0 < WG_TOKENS ? T - tok0 : WG_TOKENS);
-
-    if constexpr (BF16) {
-        router_mfma_logits<TT, NT>(static_cast<const uint16_t*>(x), T, d, wsplit, E_pad, tok0, wave, smem);
-    } else {
-        const float* xf = static_cast<const float*>(x);
-        for (int i = threadIdx.x; i < WG_TOKENS * E_pad; i += kRouterThreads) {
-            const int t = i / E_pad, e = i % E_pad;
-            float z = 0.0f;
-            if (t < ntok && e < E) {
-                const float* xr = xf + (tok0 + t) * d;
-                const float* wr = w_gate + static_cast<int64_t>(e) * d;
-                double acc = 0.0;
-                for (int c = 0; c < d; ++c) acc = fma(static_cast<double>(xr[c]), static_cast<double>(wr[c]), acc);
-                z = static_cast<float>(acc);
-            }
-            zrow[t * zp + e] = z;
+// Softmax and top-k of one token by one wave: lane l holds experts l + 64 q
+// (z[q], -inf past E). Each top-k round takes the wave maximum of the
+// untaken logits and then the lowest expert index that holds it (ties to the
+// lower index).
+template <int Q>
+__device__ __forceinline__ void softmax_topk_token(const float (&z)[Q], int64_t tok, int E, int k, int renorm,
+                                                   float* __restrict__ logits, float* __restrict__ probs,
+                                                   int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+    const int lane = lane_id();
+    float lm = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) lm = fmaxf(lm, z[q]);
+    const float m = wave_max_u(lm);
+    float ls = 0.0f, g[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int e = lane + q * kWave;
+        g[q] = e < E ? expf(z[q] - m) : 0.0f;
+        ls += g[q];
+    }
+    const float inv = 1.0f / wave_sum_u(ls);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int e = lane + q * kWave;
+        if (e < E) {
+            probs[tok * E + e] = g[q] * inv;
+            if (logits != nullptr) logits[tok * E + e] = z[q];
         }
+    }
+    unsigned taken = 0;
+    int my_i = 0;
+    float my_w = 0.0f;
+    for (int rr = 0; rr < k; ++rr) {
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int e = lane + q * kWave;
+            if (e < E && !((taken >> q) & 1u) && (bi == 0x7fffffff || z[q] > bv)) {
+                bv = z[q];
+                bi = e;
+            }
+        }
+        const float gm = wave_max_u(bi == 0x7fffffff ? -INFINITY : bv);
+        const int gi = wave_min_u(bi != 0x7fffffff && bv == gm ? bi : 0x7fffffff);
+        if ((gi % kWave) == lane) taken |= 1u << (gi / kWave);
+        if (lane == rr) {
+            my_i = gi;
+            my_w = expf(gm - m) * inv;  // the chosen expert's gate value, as in probs
+        }
+    }
+    if (renorm) my_w = my_w / wave_sum_u(lane < k ? my_w : 0.0f);
+    if (lane < k) {
+        topk_idx[tok * k + lane] = my_i;
+        topk_w[tok * k + lane] = my_w;
+    }
+}
+
+// One wave per token: z = the KS partial logits summed in range order, plus
+// the bias; then softmax and top-k.
+template <int Q>
+__global__ void __launch_bounds__(kTopkWaves * 64)
+router_topk_kernel(const float* __restrict__ part, int ks_n, int64_t T, int E, int E_pad,
+                   const float* __restrict__ bias, int k, int renorm, float* __restrict__ logits,
+                   float* __restrict__ probs, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+    const int64_t tok = static_cast<int64_t>(blockIdx.x) * kTopkWaves + threadIdx.x / kWave;
+    if (tok >= T) return;  // wave-uniform
+    const int lane = lane_id();
+    float z[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int e = lane + q * kWave;
+        if (e < E) {
+            float v = part[tok * E_pad + e];
+#pragma unroll 4
+            for (int ks = 1; ks < ks_n; ++ks) v += part[(static_cast<int64_t>(ks) * T + tok) * E_pad + e];
+            z[q] = v + (bias != nullptr ? bias[e] : 0.0f);
+        } else {
+            z[q] = -INFINITY;
+        }
+    }
+    softmax_topk_token<Q>(z, tok, E, k, renorm, logits, probs, topk_idx, topk_w);
+}
+
+// fp32 activations: 16 tokens per workgroup, dot products in fp64 into an
+// LDS tile [16][E_pad + 1] (odd pitch), then one wave per token runs the
+// softmax and the top-k.
+__global__ void __launch_bounds__(kRouterThreads)
+router_f32_kernel(const float* __restrict__ x, int64_t T, int d, const float* __restrict__ w_gate,
+                  const float* __restrict__ bias, int E, int E_pad, int k, int renorm, float* __restrict__ logits,
+                  float* __restrict__ probs, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+    extern __shared__ float smem[];
+    const int zp = E_pad + 1;
+    const int wave = threadIdx.x / kWave;
+    const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * kRouterTokens;
+    const int ntok = static_cast<int>(T - tok0 < kRouterTokens ? T - tok0 : kRouterTokens);
+    for (int i = threadIdx.x; i < kRouterTokens * E_pad; i += kRouterThreads) {
+        const int t = i / E_pad, e = i % E_pad;
+        float z = 0.0f;
+        if (t < ntok && e < E) {
+            const float* xr = x + (tok0 + t) * d;
+            const float* wr = w_gate + static_cast<int64_t>(e) * d;
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c) acc = fma(static_cast<double>(xr[c]), static_cast<double>(wr[c]), acc);
+            z = static_cast<float>(acc);
+        }
+        smem[t * zp + e] = z;
     }
     __syncthreads();
-
-    // Softmax and top-k: one wave per token, lane l holds experts l + 64 q.
-    // Each top-k round takes the wave maximum of the untaken logits and then
-    // the lowest expert index that holds it (ties to the lower index).
-    constexpr int Q = BF16 ? (16 * NT + 63) / 64 : 4;
     const int lane = lane_id();
     for (int t = wave; t < ntok; t += kRouterWaves) {
-        const float* zr = zrow + t * zp;
-        const int64_t tok = tok0 + t;
-        float z[Q];
-        float lm = -INFINITY;
+        float z[4];
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
+        for (int q = 0; q < 4; ++q) {
             const int e = lane + q * kWave;
-            z[q] = e < E ? zr[e] + (bias != nullptr ? bias[e] : 0.0f) : -INFINITY;
-            lm = fmaxf(lm, z[q]);
+            z[q] = e < E ? smem[t * zp + e] + (bias != nullptr ? bias[e] : 0.0f) : -INFINITY;
         }
-        const float m = wave_max_u(lm);
-        float ls = 0.0f, g[Q];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            const int e = lane + q * kWave;
-            g[q] = e < E ? expf(z[q] - m) : 0.0f;
-            ls += g[q];
-        }
-        const float inv = 1.0f / wave_sum_u(ls);
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            const int e = lane + q * kWave;
-            if (e < E) {
-                probs[tok * E + e] = g[q] * inv;
-                if (logits != nullptr) logits[tok * E + e] = z[q];
-            }
-        }
-        unsigned taken = 0;
-        int my_i = 0;
-        float my_w = 0.0f;
-        for (int rr = 0; rr < k; ++rr) {
-            float bv = -INFINITY;
-            int bi = 0x7fffffff;
-#pragma unroll
-            for (int q = 0; q < Q; ++q) {
-                const int e = lane + q * kWave;
-                if (e < E && !((taken >> q) & 1u) && (bi == 0x7fffffff || z[q] > bv)) {
-                    bv = z[q];
-                    bi = e;
-                }
-            }
-            const float gm = wave_max_u(bi == 0x7fffffff ? -INFINITY : bv);
-            const int gi = wave_min_u(bi != 0x7fffffff && bv == gm ? bi : 0x7fffffff);
-            if ((gi % kWave) == lane) taken |= 1u << (gi / kWave);
-            if (lane == rr) {
-                my_i = gi;
-                my_w = expf(gm - m) * inv;  // the chosen expert's gate value, as in probs
-            }
-        }
-        if (renorm) my_w = my_w / wave_sum_u(lane < k ? my_w : 0.0f);
-        if (lane < k) {
-            topk_idx[tok * k + lane] = my_i;
-            topk_w[tok * k + lane] = my_w;
-        }
+        softmax_topk_token<4>(z, tok0 + t, E, k, renorm, logits, probs, topk_idx, topk_w);
     }
 }
 
-template <bool BF16>
-hipError_t launch_router_nt(int NT, const void* x, int64_t T, int d, const float* w_gate,
-                            const uint16_t* wsplit, const float* bias, int E, int E_pad, int k,
-                            int renorm, float* logits, float* probs, int32_t* topk_idx,
-                            float* topk_w, hipStream_t stream) {
-    const int TT = BF16 ? router_tt(NT) : 1;
-    const dim3 grid(static_cast<unsigned>(ceil_div(T, kRouterTokens * TT)));
-    const size_t lds = router_lds_bytes(E, BF16 ? 1 : 0);
-#define SMOES_ROUTER_CASE(N)                                                                        \
-    case N:                                                                                         \
-        hipLaunchKernelGGL((router_kernel<BF16, N, BF16 ? router_tt(N) : 1>), grid, dim3(kRouterThreads), \
-                           lds, stream, x, T, d, w_gate, wsplit, bias, E, E_pad, k, renorm, logits, probs, \
-                           topk_idx, topk_w);                                                     \
-        break;
-    if constexpr (BF16) {
-        switch (NT) {
-            SMOES_ROUTER_CASE(1)
-            SMOES_ROUTER_CASE(2)
-            SMOES_ROUTER_CASE(3)
-            SMOES_ROUTER_CASE(4)
-            SMOES_ROUTER_CASE(5)
-            SMOES_ROUTER_CASE(6)
-            SMOES_ROUTER_CASE(7)
-            SMOES_ROUTER_CASE(8)
-            SMOES_ROUTER_CASE(9)
-            SMOES_ROUTER_CASE(10)
-            SMOES_ROUTER_CASE(11)
-            SMOES_ROUTER_CASE(12)
-            SMOES_ROUTER_CASE(13)
-            SMOES_ROUTER_CASE(14)
-            SMOES_ROUTER_CASE(15)
-            SMOES_ROUTER_CASE(16)
-            default:
-                return hipErrorInvalidValue;
-        }
-    } else {
-        switch (1) { SMOES_ROUTER_CASE(1) }
+// bf16 path: partial logits into part[KS][T][E_pad], then the top-k kernel.
+hipError_t launch_router_bf16(const uint16_t* x, int64_t T, int d, const uint16_t* wsplit, const float* bias,
+                              int E, int k, int renorm, float* part, float* logits, float* probs,
+                              int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+    const int E_pad = router_epad(E);
+    const RouterPlan p = router_plan(T, d, E);
+    const dim3 grid(static_cast<unsigned>(ceil_div(T, 16 * p.tmt)), static_cast<unsigned>(p.ks));
+    const dim3 block(kLogitWaves * 64);
+    if (p.ntw == 1 && p.tmt == 4)
+        hipLaunchKernelGGL((router_logits_kernel<4, 1, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
+    else if (p.ntw == 2 && p.tmt == 8)
+        hipLaunchKernelGGL((router_logits_kernel<8, 2, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
+    else if (p.ntw == 3 && p.tmt == 8)
+        hipLaunchKernelGGL((router_logits_kernel<8, 3, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
+    else if (p.ntw == 4 && p.tmt == 4)
+        hipLaunchKernelGGL((router_logits_kernel<4, 4, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
+    else
+        return hipErrorInvalidValue;
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const dim3 tgrid(static_cast<unsigned>(ceil_div(T, kTopkWaves)));
+    const dim3 tblock(kTopkWaves * 64);
+    switch ((E + kWave - 1) / kWave) {
+        case 1:
+            hipLaunchKernelGGL(router_topk_kernel<1>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
+                               renorm, logits, probs, topk_idx, topk_w);
+            break;
+        case 2:
+            hipLaunchKernelGGL(router_topk_kernel<2>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
+                               renorm, logits, probs, topk_idx, topk_w);
+            break;
+        case 3:
+            hipLaunchKernelGGL(router_topk_kernel<3>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
+                               renorm, logits, probs, topk_idx, topk_w);
+            break;
+        case 4:
+            hipLaunchKernelGGL(router_topk_kernel<4>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
+                               renorm, logits, probs, topk_idx, topk_w);
+            break;
+        default:
+            return hipErrorInvalidValue;
     }
-#undef SMOES_ROUTER_CASE
     return hipGetLastError();
 }
 
 }  // namespace
 
-size_t router_workspace_bytes(int d, int E, int x_dtype) {
+// bf16: the split weights (used when the caller passes row-major weights)
+// and the partial logits [KS][T][E_pad]; fp32: nothing.
+size_t router_workspace_bytes(int64_t T, int d, int E, int x_dtype) {
     if (x_dtype != 1) return 0;
     const int E_pad = router_epad(E);
-    return align_up(sizeof(uint16_t) * 3 * static_cast<size_t>(E_pad) * ceil_div(d, 32) * 32, 256);
-}
-
-size_t router_lds_bytes(int E, int x_dtype) {
-    const int E_pad = router_epad(E);
-    const int TT = x_dtype == 1 ? router_tt(E_pad / 16) : 1;
-    const size_t tokens = static_cast<size_t>(kRouterTokens) * TT;
-    const size_t tree = x_dtype == 1 ? tokens * E_pad * kRouterSlots : 0;
-    const size_t fin = tokens * (E_pad + 1);  // logits with an odd row pitch
-    return sizeof(float) * (tree > fin ? tree : fin);
+    const RouterPlan p = router_plan(T, d, E);
+    return align_up(sizeof(uint16_t) * 3 * static_cast<size_t>(E_pad) * ceil_div(d, 32) * 32, 256) +
+           align_up(sizeof(float) * static_cast<size_t>(p.ks) * T * E_pad, 256);
 }
 
 size_t router_packed_elems(int d, int E) {
@@ -358,23 +384,24 @@ hipError_t launch_route(const void* x, int x_dtype, int64_t T, int d, const floa
                         const void* w_split, const float* bias, int E, int k, int renorm, float* logits,
                         float* probs, int32_t* topk_idx, float* topk_w, void* ws, hipStream_t stream) {
     const int E_pad = router_epad(E);
-    const int NT = E_pad / 16;
-    if (x_dtype == 1 && w_split != nullptr)
-        return launch_router_nt<true>(NT, x, T, d, w_gate, static_cast<const uint16_t*>(w_split), bias, E,
-                                      E_pad, k, renorm, logits, probs, topk_idx, topk_w, stream);
     if (x_dtype == 1) {
-        uint16_t* wsplit = static_cast<uint16_t*>(ws);
-        const int64_t n = static_cast<int64_t>(E_pad / 16) * ceil_div(d, 32) * 64;  // fragments
-        const unsigned blocks = static_cast<unsigned>(ceil_div(n, 256) < 4096 ? ceil_div(n, 256) : 4096);
-        hipLaunchKernelGGL(split_wgate_kernel, dim3(blocks), dim3(256), 0, stream, w_gate, E, E_pad,
-                           d, wsplit);
-        hipError_t err = hipGetLastError();
-        if (err != hipSuccess) return err;
-        return launch_router_nt<true>(NT, x, T, d, w_gate, wsplit, bias, E, E_pad, k, renorm,
-                                      logits, probs, topk_idx, topk_w, stream);
+        uint8_t* base = static_cast<uint8_t*>(ws);
+        const size_t split_bytes = align_up(sizeof(uint16_t) * 3 * static_cast<size_t>(E_pad) * ceil_div(d, 32) * 32, 256);
+        float* part = reinterpret_cast<float*>(base + split_bytes);
+        const uint16_t* wsplit = static_cast<const uint16_t*>(w_split);
+        if (wsplit == nullptr) {
+            hipError_t err = launch_split_wgate(w_gate, E, d, base, stream);
+            if (err != hipSuccess) return err;
+            wsplit = reinterpret_cast<const uint16_t*>(base);
+        }
+        return launch_router_bf16(static_cast<const uint16_t*>(x), T, d, wsplit, bias, E, k, renorm, part, logits,
+                                  probs, topk_idx, topk_w, stream);
     }
-    return launch_router_nt<false>(NT, x, T, d, w_gate, nullptr, bias, E, E_pad, k, renorm, logits,
-                                   probs, topk_idx, topk_w, stream);
+    const dim3 grid(static_cast<unsigned>(ceil_div(T, kRouterTokens)));
+    const size_t lds = sizeof(float) * kRouterTokens * (E_pad + 1);
+    hipLaunchKernelGGL(router_f32_kernel, grid, dim3(kRouterThreads), lds, stream, static_cast<const float*>(x), T,
+                       d, w_gate, bias, E, E_pad, k, renorm, logits, probs, topk_idx, topk_w);
+    return hipGetLastError();
 }
 
 }  // namespace smoes
