@@ -40,6 +40,10 @@ ROUTE_CASES = [
     (257, 256, 64, 6, W.BF16, False),
     (64, 64, 160, 6, W.BF16, True),
     (33, 512, 256, 16, W.BF16, False),  # maximum E and k
+    (300, 1032, 100, 8, W.BF16, True),  # two expert tiles per wave, the last wave's second one empty;
+                                        # 33 k-steps in 4 ranges (the last one shorter), partial last step
+    (2000, 2048, 128, 8, W.BF16, False),  # 128-token tiles split over 4 ranges of the hidden dimension
+    (5000, 512, 64, 6, W.BF16, False),  # ragged last token tile, 2 ranges
     (31, 2048, 8, 2, W.BF16, False),
     (1, 8, 1, 1, W.BF16, False),        # degenerate: one token, one expert
     (100, 72, 8, 2, W.F32, False),
