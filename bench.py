@@ -253,6 +253,27 @@ def main():
     roof["kernel_ms"] = round(dom_ms, 5)  # mean over the timed calls (HIP events on its stream)
     roof["traffic"] = measured_traffic(dom)
 
+    # The same stages with every stage on the caller's stream (no side
+    # streams): each kernel owns the chip, so these are the kernels' own
+    # rates (the layer step above overlaps the shared experts with the routed
+    # path and is faster as a whole).
+    log(f"[bench] serial stage breakdown over {n_stage} calls")
+    ser_events = [S.Events() for _ in range(n_stage)]
+    for i in range(n_stage):
+        S.moe_forward(spec, dev_in, outs, ws, events=ser_events[i])
+    torch.cuda.synchronize()
+    stages_serial = {}
+    for si, name in enumerate(S.STAGES):
+        ms_i = float(np.median([ev.stage_ms(si) for ev in ser_events]))
+        wk = work[name]
+        stages_serial[name] = {"ms": round(ms_i, 5),
+                               "tflops": round(wk["flops"] / (ms_i * 1e-3) / 1e12, 3) if wk["flops"] else 0.0,
+                               "gbs": round(wk["bytes"] / (ms_i * 1e-3) / 1e9, 1)}
+        if name in ("gemm1", "gemm2", "gemm1_shared", "gemm2_shared") and cfg.dtype == W.BF16:
+            stages_serial[name]["frac_mfma"] = round(stages_serial[name]["tflops"] / PEAK_BF16_TFLOPS, 4)
+    for ev in ser_events:
+        ev.close()
+
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
@@ -268,6 +289,7 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "stages": stages,
+        "stages_serial": stages_serial,
     }
     # Momentum-adaptive binning + bin-level balance loss (+ gradient, added onto
     # the MI gradient) + MSI on this step's routing: timed on its own, not part

@@ -140,16 +140,23 @@ mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batc
     __shared__ double term[2][64];
     __shared__ double Wm[2];
     __shared__ int32_t mem[256];
+    __shared__ int32_t bin_s[256];
     const int NB = E / n_bins;
     const int tid = threadIdx.x;
     const int i = blockIdx.x;
-    // bin member lists in ascending expert order
-    if (tid < n_bins) {
-        const int k = tid;
-        int n = 0;
-        for (int e = 0; e < E; ++e)
-            if (e2b[e] == k && n < NB) mem[k * NB + n++] = e;
-        for (; n < NB; ++n) mem[k * NB + n] = -1;  // violated precondition (bin too small): empty slot
+    // bin member lists in ascending expert order: expert e takes slot
+    // (its bin, the number of lower experts in that bin); slots no expert
+    // takes stay -1 (violated precondition: a bin with fewer than N_B experts)
+    for (int q = tid; q < E; q += blockDim.x) {
+        bin_s[q] = e2b[q];
+        mem[q] = -1;
+    }
+    __syncthreads();
+    for (int q = tid; q < E; q += blockDim.x) {
+        const int k = bin_s[q];
+        int rank = 0;
+        for (int e = 0; e < q; ++e) rank += bin_s[e] == k ? 1 : 0;
+        if (k >= 0 && k < n_bins && rank < NB) mem[k * NB + rank] = q;
     }
     // chunk partials: thread (cg, e) sums chunks cg, cg + RG, ... in order
     const int EP = static_cast<int>(ceil_div(E, kWave) * kWave);

@@ -49,19 +49,23 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Block-wide inclusive scan of one int per thread (256 threads).
+// Block-wide inclusive scan of one int per thread (256 threads = 4 waves):
+// each wave scans with shuffles, then adds the totals of the waves before it.
+// sc holds at least 4 ints; it is free again when the function returns.
 __device__ __forceinline__ int block_scan_incl(int v, int32_t* sc) {
-    const int t = threadIdx.x;
-    sc[t] = v;
-    __syncthreads();
-    for (int o = 1; o < kChunk; o <<= 1) {
-        const int add = t >= o ? sc[t - o] : 0;
-        __syncthreads();
-        v += add;
-        sc[t] = v;
-        __syncthreads();
+    const int lane = lane_id();
+    const int wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int t = __shfl_up(v, o);
+        if (lane >= o) v += t;
     }
-    return v;
+    if (lane == kWave - 1) sc[wave] = v;
+    __syncthreads();
+    int add = 0;
+    for (int w = 0; w < wave; ++w) add += sc[w];
+    __syncthreads();
+    return v + add;
 }
 
 __global__ void __launch_bounds__(kChunk)
