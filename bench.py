@@ -424,11 +424,12 @@ def main():
         ws_tr = torch.empty(S.workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
         bws_t = torch.empty(S.backward_workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
         S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-        grads = S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], workspace=bws_t)
+        grads = S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], workspace=bws_t,
+                               streams=streams)
         for _ in range(3):
             S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
             S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
-                           workspace=bws_t)
+                           workspace=bws_t, streams=streams)
         tr_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         f_ms, b_ms = [], []
         for _ in range(args.steps):
@@ -436,7 +437,7 @@ def main():
             S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
             tr_ev[1].record()
             S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
-                           workspace=bws_t)
+                           workspace=bws_t, streams=streams)
             tr_ev[2].record()
             torch.cuda.synchronize()
             f_ms.append(tr_ev[0].elapsed_time(tr_ev[1]))

@@ -254,7 +254,8 @@ typedef struct smoes_layer {
                            (packed bf16 layers only); 0: it does not */
 } smoes_layer;
 
-/* Side streams for smoes_moe_forward (caller-owned; see smoes_streams_create). */
+/* Side streams for smoes_moe_forward and smoes_moe_backward (caller-owned;
+ * see smoes_streams_create). */
 typedef struct smoes_streams {
     void* side[2];   /* hipStream_t: [0] modality score + MI chain, [1] shared-expert GEMMs */
     void* events[4]; /* hipEvent_t (timing disabled) used to fork and join them */
@@ -428,7 +429,11 @@ size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
  * bf16 operands with float32 accumulation; the expert weight gradients are
  * bf16, dx, dw_gate and the logit gradient float32. Sums run in a fixed
  * order: results are reproducible. Asynchronous on `stream`; nothing is
- * allocated.
+ * allocated. With io->streams set, the router backward, dW_gate / dbias and
+ * the shared experts' gradients run on io->streams->side[1], forked from
+ * `stream` at the start of the call and joined back before the input
+ * gradient (events[0] and events[3]); the results are the same bits as on
+ * one stream. NULL runs every step on `stream`.
  */
 int smoes_moe_backward(const smoes_layer* desc, const smoes_layer_io* io, const void* w13t, const void* w2t,
                        const void* ws13t, const void* ws2t, const void* dout, const float* dlogits_aux,

@@ -533,6 +533,12 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
         return SMOES_ERR_ARG;
     if (fwd_workspace == nullptr || fwd_workspace_bytes < smoes_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
     if (workspace == nullptr || workspace_bytes < smoes_backward_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
+    if (io->streams != nullptr) {
+        for (void* p : io->streams->side)
+            if (p == nullptr) return SMOES_ERR_ARG;
+        for (void* p : io->streams->events)
+            if (p == nullptr) return SMOES_ERR_ARG;
+    }
     hipStream_t s = as_stream(stream);
     LayerWs fw;
     layer_ws_parts(L, &fw, fwd_workspace);
@@ -583,27 +589,49 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     do {                                                        \
         if ((err = (expr)) != hipSuccess) return SMOES_ERR_HIP; \
     } while (0)
-    SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
-    SMOES_BTRY(launch_router_bwd(dout, fb.y_r, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T, L->d,
-                                 L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, s));
-    for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode) {
-        SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 1, s));
-        if (sh) SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 2, s));
+    // Caller's stream s: combine weights, the routed experts' dgrad GEMMs
+    // (pre-activation recompute unless kept, dH with the SwiGLU backward,
+    // dX) and weight gradients, then the input gradient. With caller-owned
+    // side streams (io->streams) the router backward, dW_gate and the shared
+    // experts' GEMMs and weight gradients (independent of the routed chain)
+    // run on side[1], forked from s at the start of the call and joined back
+    // before the input gradient, which needs both chains; without them every
+    // step runs on s in the same dependency order.
+    const smoes_streams* sides = io->streams;
+    hipStream_t c = s;
+    hipEvent_t e_fork = nullptr, e_join = nullptr;
+    if (sides != nullptr) {
+        c = as_stream(sides->side[1]);
+        e_fork = static_cast<hipEvent_t>(sides->events[0]);
+        e_join = static_cast<hipEvent_t>(sides->events[3]);
+        SMOES_BTRY(hipEventRecord(e_fork, s));
+        SMOES_BTRY(hipStreamWaitEvent(c, e_fork, 0));
     }
-    SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
-                                G->dx, s));
     const int I = L->inter, SI = L->shared_inter, d = L->d;
     const int Ti = static_cast<int>(T), R = static_cast<int>(T * L->k);
+    // side chain: router backward (dz, dw), dW_gate and dbias, shared experts
+    SMOES_BTRY(launch_router_bwd(dout, fb.y_r, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T, L->d,
+                                 L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, c));
+    SMOES_BTRY(launch_dwgate(G->dz, io->x, T, d, L->E, G->dw_gate, G->dbias, bw.router, c));
+    if (sh) {
+        for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode)
+            SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 2, c));
+        SMOES_BTRY(launch_wgrad(T, 1, d, SI, nullptr, dout, d, Ti, nullptr, fb.h_s, SI, Ti, nullptr, 0, G->dws2, c));
+        SMOES_BTRY(launch_wgrad(T, 1, 2 * SI, d, nullptr, bw.dab_s, 2 * SI, Ti, nullptr, io->x, d, Ti, nullptr, 0,
+                                G->dws13, c));
+    }
+    if (sides != nullptr) SMOES_BTRY(hipEventRecord(e_join, c));
+    // routed chain
+    SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
+    for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode)
+        SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 1, s));
     // dW2 = dout^T (w H) over each expert's rows (dout gathered); dW13 = [dA dB]^T X (x gathered)
     SMOES_BTRY(launch_wgrad(T, L->E, d, I, offsets, dout, d, Ti, perm_token, bw.wh_r, I, R, nullptr, R, G->dw2, s));
     SMOES_BTRY(launch_wgrad(T, L->E, 2 * I, d, offsets, bw.dab_r, 2 * I, R, nullptr, io->x, d, Ti, perm_token, R,
                             G->dw13, s));
-    if (sh) {
-        SMOES_BTRY(launch_wgrad(T, 1, d, SI, nullptr, dout, d, Ti, nullptr, fb.h_s, SI, Ti, nullptr, 0, G->dws2, s));
-        SMOES_BTRY(launch_wgrad(T, 1, 2 * SI, d, nullptr, bw.dab_s, 2 * SI, Ti, nullptr, io->x, d, Ti, nullptr, 0,
-                                G->dws13, s));
-    }
-    SMOES_BTRY(launch_dwgate(G->dz, io->x, T, d, L->E, G->dw_gate, G->dbias, bw.router, s));
+    if (sides != nullptr) SMOES_BTRY(hipStreamWaitEvent(s, e_join, 0));
+    SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
+                                G->dx, s));
 #undef SMOES_BTRY
     return SMOES_OK;
 }

@@ -513,12 +513,14 @@ def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
                  packed_t: Dict[str, torch.Tensor], dout: torch.Tensor,
                  dlogits_aux: Optional[torch.Tensor] = None, want_dw: bool = True,
                  grads: Optional[Dict[str, Optional[torch.Tensor]]] = None,
-                 workspace: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
+                 workspace: Optional[torch.Tensor] = None,
+                 streams: Optional["Streams"] = None) -> Dict[str, torch.Tensor]:
     """smoes_moe_backward after moe_forward with the same inputs / outputs /
     workspace. `inputs` must hold the packed w13 / ws13 and the float32
     w_gate; returns the gradients (dx, dw_gate, dbias, dz, dw, dw13, dw2,
     dws13, dws2), written into `grads` when given (as returned by an earlier
-    call), with `workspace` reused when given."""
+    call), with `workspace` reused when given; `streams` (side streams) lets
+    the router and shared-expert gradients run beside the routed ones."""
     desc = spec.c()
     io = SmoesLayerIO()
     for name in _IO_FIELDS:
@@ -527,7 +529,7 @@ def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
         t = inputs.get(name) if name in inputs else outputs.get(name)
         setattr(io, name, None if t is None else _p(t).value)
     io.stage_events = None
-    io.streams = None
+    io.streams = ctypes.cast(ctypes.byref(streams.st), c_void).value if streams is not None else None
     T, d, E, k, I, SI = spec.T, spec.d, spec.E, spec.k, spec.inter, spec.shared_inter
     dev = dout.device
     g = grads if grads is not None else {

@@ -67,15 +67,18 @@ def _mask_ties(inp, dout, gap=1e-3):
     return dout
 
 
-def run_gpu_backward(inp, dout, aux, renorm, want_dw=True, save_preact=False):
-    """Forward then backward on the device; returns (spec, outs, grads)."""
+def run_gpu_backward(inp, dout, aux, renorm, want_dw=True, save_preact=False, streams=None):
+    """Forward then backward on the device (the backward's router and shared
+    experts on side streams when `streams` is given); returns (spec, outs,
+    grads)."""
     cfg = inp.cfg
     rowmajor = {"w13": t(inp.w13), "w2": t(inp.w2), "ws13": t(inp.ws13), "ws2": t(inp.ws2)}
     spec_t = layer_spec(cfg, weights_packed=True)
     packed_t = S.pack_transposed_weights(spec_t, rowmajor)
     torch.cuda.synchronize()
     spec, dev_in, outs, ws = run_gpu_layer(inp, renorm_topk=renorm, keep_workspace=True, save_preact=save_preact)
-    g = S.moe_backward(spec, dev_in, outs, ws, packed_t, t(dout), None if aux is None else t(aux), want_dw=want_dw)
+    g = S.moe_backward(spec, dev_in, outs, ws, packed_t, t(dout), None if aux is None else t(aux), want_dw=want_dw,
+                       streams=streams)
     torch.cuda.synchronize()
     return spec, outs, g
 
@@ -140,6 +143,23 @@ def test_backward_with_kept_preactivations_matches_recompute(layer):
     for name in g1:
         if g1[name] is not None:
             assert torch.equal(g1[name], g2[name]), name
+
+
+@pytest.mark.parametrize("layer", [0, 2, 3])
+def test_backward_side_streams_match_single_stream(layer):
+    # the router and shared-expert gradients on a side stream run the same
+    # kernels in the same order within each chain: identical bits
+    cfg, inp, dout, aux = _inputs(LAYERS[layer], 300 + layer)
+    say("backward side streams", layer)
+    streams = S.Streams()
+    _, _, a = run_gpu_backward(inp, dout, aux, True, save_preact=True)
+    _, _, b = run_gpu_backward(inp, dout, aux, True, save_preact=True, streams=streams)
+    _, _, c = run_gpu_backward(inp, dout, aux, True, save_preact=False, streams=streams)
+    for name in a:
+        if a[name] is not None:
+            assert torch.equal(a[name], b[name]), name
+            assert torch.equal(a[name], c[name]), name
+    streams.close()
 
 
 def test_backward_is_reproducible():
