@@ -43,7 +43,8 @@ typedef __attribute__((address_space(3))) wg_v4i16 wg_lds_v4i16;
 // compiler sees the LDS writes and, unable to tell them apart from the
 // transposing reads of other ring slots, waits for every outstanding load
 // before each read, which would drain the ring. Here the kernel orders them
-// itself: vmcnt waits plus a barrier before a slot is read.
+// itself: vmcnt waits plus a barrier before a slot is read. The LDS address
+// goes in through M0 as an operand, so the compiler sets M0 itself.
 // Descriptor words: base (48 bits, stride 0), record count in bytes, format.
 __device__ __forceinline__ i32x4_t wg_rsrc(const void* base, int bytes) {
     const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -56,17 +57,17 @@ __device__ __forceinline__ uint32_t wg_lds_addr(const void* p) {
 }
 // 16 bytes per lane from byte offset voff into LDS at lds + 16 lane (lds uniform)
 __device__ __forceinline__ void wg_dma16(i32x4_t rsrc, int voff, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
                  :
-                 : "s"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds))), "v"(voff), "s"(rsrc)
-                 : "memory", "m0");
+                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)))
+                 : "memory");
 }
 // 4 bytes per lane into LDS at lds + 4 lane
 __device__ __forceinline__ void wg_dma4(i32x4_t rsrc, int voff, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+    asm volatile("buffer_load_dword %0, %1, 0 offen lds"
                  :
-                 : "s"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds))), "v"(voff), "s"(rsrc)
-                 : "memory", "m0");
+                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)))
+                 : "memory");
 }
 
 struct WgArgs {
