@@ -136,7 +136,9 @@ router_logits_kernel(const uint16_t* __restrict__ x, int64_t T, int d, const uin
         for (int tt = 0; tt < TMT; ++tt) acc[j][tt] = f32x4_t{};
     auto fetch = [&](int s, bf16x8_t (&a)[TMT], bf16x8_t (&b)[NTW][3]) {
         const int kk = s * 32 + quad * 8;
-        const int oob = s < s1 ? 0 : kOob;  // d % 8 == 0: an 8-chunk is all in or all out
+        // d % 8 == 0: an 8-chunk is all in or all out; chunks past d would read
+        // the next token's row (zero weights there, but 0 * inf is NaN)
+        const int oob = (s < s1 && kk < d) ? 0 : kOob;
 #pragma unroll
         for (int tt = 0; tt < TMT; ++tt)
             a[tt] = __builtin_bit_cast(bf16x8_t,

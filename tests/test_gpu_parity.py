@@ -71,6 +71,25 @@ def test_route(T, d, E, k, dt, bias, renorm):
     assert np.all(np.abs(wg[clear] - wt[clear]) <= 1e-5 * wt[clear] + 1e-12)
 
 
+def test_route_partial_last_step_reads_no_next_row():
+    # d = 40: the last 32-wide k-step is partly past d; its lanes past d must
+    # not read the next token's row (an inf there would give 0 * inf = NaN)
+    T, d, E, k = 40, 40, 64, 6
+    rng = np.random.default_rng(11)
+    x32 = rng.standard_normal((T, d)).astype(np.float32)
+    x32[5, :8] = np.inf
+    x = W.f32_to_bf16_bits(x32)
+    w = (0.05 * rng.standard_normal((E, d))).astype(np.float32)
+    r = S.route(t(x), t(w), k)
+    ok = np.arange(T) != 5
+    z, g, idx, _ = O.route(x[ok], w, k, None, False)
+    zg, gg = host(r["logits"])[ok], host(r["probs"])[ok]
+    assert np.all(np.isfinite(zg)) and np.all(np.isfinite(gg))
+    scale = np.abs(O.widen(x[ok])) @ np.abs(w.astype(np.float64)).T
+    assert np.all(np.abs(zg - z) <= 4e-7 * scale + 1e-30)
+    check_topk(host(r["topk_idx"])[ok], idx, z, k)
+
+
 # ---------------------------------------------------------------- modality score
 
 MOD_CASES = [
