@@ -83,8 +83,14 @@ __device__ __forceinline__ void attn_fwd_body(const uint16_t* __restrict__ q, co
     __shared__ __attribute__((aligned(16))) float mv_lds[2][AT_BK];
 
     const int nqb = static_cast<int>(ceil_div(T, AT_BQ));
-    const int qb = nqb - 1 - static_cast<int>(blockIdx.x);  // longest (latest) blocks first
     const int hq = blockIdx.y;
+    // Two workgroups share a CU: those L and L + N / 2 in dispatch order (N =
+    // all of them), i.e. heads h and h + H / 2 at the same blockIdx.x. The
+    // lower half of the heads takes the query blocks from the last (longest
+    // causal range) down, the upper half from the first up, so a CU holds a
+    // long and a short block rather than two of the same length.
+    const int qb = 2 * hq < static_cast<int>(gridDim.y) ? nqb - 1 - static_cast<int>(blockIdx.x)
+                                                      : static_cast<int>(blockIdx.x);
     const int hk = hq / (H / Hkv);
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int half = lane >> 5, l32 = lane & 31;
