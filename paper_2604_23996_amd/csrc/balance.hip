@@ -153,18 +153,38 @@ bal_finalize_kernel(int64_t nchunk, int E, int n_bins, const int32_t* __restrict
     __shared__ double red[kBalThreads];
     const int e = threadIdx.x;  // E <= 256 = blockDim
     const int NB = E / n_bins;
+    constexpr int B = 8;  // chunk loads in flight; the sums still run in chunk order
     if (e < n_bins) {
         int32_t s = 0;
-        for (int64_t c = 0; c < nchunk; ++c) s += tk_in[c * n_bins + e];
+        for (int64_t c0 = 0; c0 < nchunk; c0 += B) {
+            int32_t v[B];
+#pragma unroll
+            for (int q = 0; q < B; ++q) v[q] = c0 + q < nchunk ? tk_in[(c0 + q) * n_bins + e] : 0;
+#pragma unroll
+            for (int q = 0; q < B; ++q) s += v[q];
+        }
         tk[e] = s;
     }
     int32_t cv = 0, ct = 0;
     double S = 0.0;
     if (e < E) {
-        for (int64_t c = 0; c < nchunk; ++c) {  // chunk order
-            cv += cnt_in[c * 2 * E + e];
-            ct += cnt_in[c * 2 * E + E + e];
-            S += mass_in[c * E + e];
+        for (int64_t c0 = 0; c0 < nchunk; c0 += B) {
+            int32_t vv[B], vt[B];
+            double vm[B];
+#pragma unroll
+            for (int q = 0; q < B; ++q) {
+                const int64_t c = c0 + q < nchunk ? c0 + q : c0;
+                vv[q] = cnt_in[c * 2 * E + e];
+                vt[q] = cnt_in[c * 2 * E + E + e];
+                vm[q] = mass_in[c * E + e];
+            }
+#pragma unroll
+            for (int q = 0; q < B; ++q)
+                if (c0 + q < nchunk) {
+                    cv += vv[q];
+                    ct += vt[q];
+                    S += vm[q];
+                }
         }
     }
     __syncthreads();

@@ -320,10 +320,23 @@ __global__ void gmm_merge_kernel(int d, int K, int64_t nchunk, const double* __r
     const int col = blockIdx.x * blockDim.x + threadIdx.x;
     if (col >= d) return;
     double n = 0.0, S1 = 0.0, S2 = 0.0;
-    for (int64_t ch = 0; ch < nchunk; ++ch) {
-        n += wsum[ch * 2 * K + mc];
-        S1 += s1g[(ch * 2 * K + mc) * d + col];
-        S2 += s2g[(ch * 2 * K + mc) * d + col];
+    constexpr int B = 8;  // chunk loads in flight; the sums still run in chunk order
+    for (int64_t c0 = 0; c0 < nchunk; c0 += B) {
+        double vn[B], v1[B], v2[B];
+#pragma unroll
+        for (int q = 0; q < B; ++q) {
+            const int64_t ch = c0 + q < nchunk ? c0 + q : c0;
+            vn[q] = wsum[ch * 2 * K + mc];
+            v1[q] = s1g[(ch * 2 * K + mc) * d + col];
+            v2[q] = s2g[(ch * 2 * K + mc) * d + col];
+        }
+#pragma unroll
+        for (int q = 0; q < B; ++q)
+            if (c0 + q < nchunk) {
+                n += vn[q];
+                S1 += v1[q];
+                S2 += v2[q];
+            }
     }
     const double nprev = n_old[mc];
     const int64_t o = static_cast<int64_t>(mc) * d + col;

@@ -172,10 +172,24 @@ __global__ void gauss_merge_kernel(int d, int64_t nchunk, const int32_t* __restr
     if (col >= d) return;
     int64_t n = 0;
     double S1 = 0.0, S2 = 0.0;
-    for (int64_t c = 0; c < nchunk; ++c) {
-        n += counts[c * 2 + m];
-        S1 += s1g[(c * 2 + m) * d + col];
-        S2 += s2g[(c * 2 + m) * d + col];
+    constexpr int B = 8;  // chunk loads in flight; the sums still run in chunk order
+    for (int64_t c0 = 0; c0 < nchunk; c0 += B) {
+        int32_t vn[B];
+        double v1[B], v2[B];
+#pragma unroll
+        for (int q = 0; q < B; ++q) {
+            const int64_t c = c0 + q < nchunk ? c0 + q : c0;
+            vn[q] = counts[c * 2 + m];
+            v1[q] = s1g[(c * 2 + m) * d + col];
+            v2[q] = s2g[(c * 2 + m) * d + col];
+        }
+#pragma unroll
+        for (int q = 0; q < B; ++q)
+            if (c0 + q < nchunk) {
+                n += vn[q];
+                S1 += v1[q];
+                S2 += v2[q];
+            }
     }
     const double nprev = n_old[m];
     const double smu_old = gauss_smu[static_cast<int64_t>(m) * d + col];
