@@ -291,6 +291,32 @@ def main():
         "stages": stages,
         "stages_serial": stages_serial,
     }
+    # Gaussian statistics update (Eq. 5-7) followed by the score (Eq. 8-9) on
+    # this workload's tokens: the modality stage of a layer that re-estimates
+    # its statistics from the batch. Timed on its own, on copies of the state.
+    T_, d_ = cfg.T, cfg.d
+    g_n, g_mu, g_sig = dev_in["gauss_n"].clone(), dev_in["gauss_smu"].clone(), dev_in["gauss_ssig"].clone()
+    M_u = torch.empty((T_, 2), dtype=torch.float32, device=dev)
+    nws_u = int(S.lib().smoes_modality_workspace_size(T_, d_))
+    ws_u = torch.empty(nws_u, dtype=torch.uint8, device=dev)
+    xdt = 1 if cfg.dtype == W.BF16 else 0
+
+    def update_call():
+        S._check(S.lib().smoes_modality_score(S._p(dev_in["x"]), xdt, T_, d_, S._p(dev_in["modality_id"]),
+                                              S._p(g_n), S._p(g_mu), S._p(g_sig), 1, cfg.beta, cfg.tau, 1e-6,
+                                              S._p(M_u), S._p(ws_u), nws_u, S._stream()), "smoes_modality_score")
+    for _ in range(3):
+        update_call()
+    ev_u = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    u_ms = []
+    for _ in range(args.steps):
+        ev_u[0].record()
+        update_call()
+        ev_u[1].record()
+        torch.cuda.synchronize()
+        u_ms.append(ev_u[0].elapsed_time(ev_u[1]))
+    um = float(np.median(u_ms))
+    u_bytes = 2 * T_ * d_ * (2 if cfg.dtype == W.BF16 else 4) + T_ + T_ * 8
     # Momentum-adaptive binning + bin-level balance loss (+ gradient, added onto
     # the MI gradient) + MSI on this step's routing: timed on its own, not part
     # of the layer step above.
@@ -321,7 +347,11 @@ def main():
     torch.cuda.synchronize()
     bin_ms = b0.elapsed_time(b1) / args.steps
     bin_bytes = T * (2 * 4 * E + 4 * cfg.k + 1)  # probs read, dlogits read+write, top-k, labels
-    line["extra"] = {"binning": {"what": "momentum-adaptive bins + bin-level load balance loss and gradient "
+    line["extra"] = {"gauss_update": {"what": "Gaussian statistics update from the batch (EMA-Welford, Eq. 5-7) then "
+                                              "the modality score (Eq. 8-9), one layer; x read twice",
+                                      "ms": round(um, 5), "gbs": round(u_bytes / (um * 1e-3) / 1e9, 1),
+                                      "frac_hbm": round(u_bytes / (um * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+                     "binning": {"what": "momentum-adaptive bins + bin-level load balance loss and gradient "
                                          "(added onto dlogits) + MSI, one layer, this step's routing",
                                  "ms": round(bin_ms, 5), "gbs": round(bin_bytes / (bin_ms * 1e-3) / 1e9, 1),
                                  "frac_hbm": round(bin_bytes / (bin_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}}

@@ -3,8 +3,9 @@
 //  update (optional): per-modality batch count, mean and centred sum of
 //     squares, folded into the caller's EMA-Welford state (Eq. 5-7).
 //     gauss_partial: 4 waves share 512 columns (8 per lane) and split a
-//       256-token chunk; fp64 sums of (x - shift) and (x - shift)^2, where
-//       the shift is the previous mean, then a fixed-order LDS tree.
+//       64-token chunk (rows loaded eight at a time); fp64 sums of
+//       (x - shift) and (x - shift)^2, where the shift is the previous mean,
+//       then a fixed-order LDS tree.
 //     gauss_merge: one thread per (modality, column) adds the chunk partials
 //       in chunk order and applies the EMA update.
 //  score: gauss_prep turns the state into per-column mu_m and 1 / sigma^2_m
@@ -24,7 +25,7 @@ namespace smoes {
 
 namespace {
 
-constexpr int kChunkRows = 256;   // tokens per gauss_partial block
+constexpr int kChunkRows = 64;    // tokens per gauss_partial block (16 per wave)
 constexpr int kColsPerBlock = 512; // 64 lanes x 8 columns
 constexpr int kScoreTokPerWave = 2;
 constexpr int kScoreThreads = 256;
@@ -90,25 +91,39 @@ gauss_partial_kernel(const void* __restrict__ x, int64_t T, int d, const uint8_t
     int cnt[2] = {0, 0};
     const int64_t r0 = chunk * kChunkRows;
     const int64_t r1 = r0 + kChunkRows < T ? r0 + kChunkRows : T;
-    for (int64_t r = r0 + wave; r < r1; r += 4) {
-        const int m = mid[r] ? 1 : 0;
-        cnt[m] += 1;
-        if (!active) continue;
-        float v[8];
-        load8<BF16>(x, r * d + col0, v);
-        if (m == 0) {
+    // rows r0 + wave, + 4, ... in groups of U: the group's labels and row
+    // chunks are loaded first, then accumulated in row order
+    constexpr int U = 8;
+    for (int64_t g = r0 + wave; g < r1; g += 4 * U) {
+        int mm[U];
+        float v[U][8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const double y = static_cast<double>(v[i]) - sh[0][i];
-                s1[0][i] += y;
-                s2[0][i] = fma(y, y, s2[0][i]);
-            }
-        } else {
+        for (int u = 0; u < U; ++u) {
+            const int64_t r = g + 4 * u;
+            const int64_t rr = r < r1 ? r : g;
+            mm[u] = mid[rr] ? 1 : 0;
+            if (active) load8<BF16>(x, rr * d + col0, v[u]);
+        }
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const double y = static_cast<double>(v[i]) - sh[1][i];
-                s1[1][i] += y;
-                s2[1][i] = fma(y, y, s2[1][i]);
+        for (int u = 0; u < U; ++u) {
+            if (g + 4 * u >= r1) break;  // wave-uniform
+            const int m = mm[u];
+            cnt[m] += 1;
+            if (!active) continue;
+            if (m == 0) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const double y = static_cast<double>(v[u][i]) - sh[0][i];
+                    s1[0][i] += y;
+                    s2[0][i] = fma(y, y, s2[0][i]);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const double y = static_cast<double>(v[u][i]) - sh[1][i];
+                    s1[1][i] += y;
+                    s2[1][i] = fma(y, y, s2[1][i]);
+                }
             }
         }
     }
@@ -172,7 +187,7 @@ __global__ void gauss_merge_kernel(int d, int64_t nchunk, const int32_t* __restr
     if (col >= d) return;
     int64_t n = 0;
     double S1 = 0.0, S2 = 0.0;
-    constexpr int B = 8;  // chunk loads in flight; the sums still run in chunk order
+    constexpr int B = 16;  // chunk loads in flight; the sums still run in chunk order
     for (int64_t c0 = 0; c0 < nchunk; c0 += B) {
         int32_t vn[B];
         double v1[B], v2[B];
@@ -349,8 +364,8 @@ hipError_t launch_modality(const void* x, int x_dtype, int64_t T, int d, const u
             hipLaunchKernelGGL(gauss_partial_kernel<false>, grid, dim3(256), 0, stream, x, T, d,
                                modality_id, gauss_n, gauss_smu, w.counts, w.s1, w.s2, w.n_old);
         if ((err = hipGetLastError()) != hipSuccess) return err;
-        hipLaunchKernelGGL(gauss_merge_kernel, dim3(static_cast<unsigned>(ceil_div(d, 256)), 2),
-                           dim3(256), 0, stream, d, nchunk, w.counts, w.s1, w.s2, w.n_old, beta,
+        hipLaunchKernelGGL(gauss_merge_kernel, dim3(static_cast<unsigned>(ceil_div(d, 64)), 2),
+                           dim3(64), 0, stream, d, nchunk, w.counts, w.s1, w.s2, w.n_old, beta,
                            gauss_n, gauss_smu, gauss_ssig);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
