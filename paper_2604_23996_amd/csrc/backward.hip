@@ -36,19 +36,29 @@ router_bwd_kernel(const uint16_t* __restrict__ dout, const uint16_t* __restrict_
     const int64_t j = static_cast<int64_t>(blockIdx.x) * 4 + threadIdx.x / kWave;
     if (j >= T) return;  // whole waves
     const int lane = lane_id();
+    // dw_s = <dout_j, Y[inv(j, s)]>: one pass over the columns loads dout once
+    // and every slot's row chunk; each slot's partial runs over the columns in
+    // order
     float dws[SMOES_K_MAX_DEV];
-    for (int s = 0; s < k; ++s) {
-        const int64_t r = inv[j * k + s];
-        float part = 0.0f;
-        for (int c = lane * 8; c < d; c += kWave * 8) {
-            float a[8], y[8];
-            load8<true>(dout, j * d + c, a);
-            load8<true>(y_r, r * d + c, y);
+    int64_t rows[SMOES_K_MAX_DEV];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) part = fmaf(a[e], y[e], part);
-        }
-        dws[s] = wave_sum_u(part);
+    for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
+        rows[s] = s < k ? static_cast<int64_t>(inv[j * k + s]) : 0;
+        dws[s] = 0.0f;
     }
+    for (int c = lane * 8; c < d; c += kWave * 8) {
+        float a[8];
+        load8<true>(dout, j * d + c, a);
+#pragma unroll
+        for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
+            if (s >= k) break;
+            float y[8];
+            load8<true>(y_r, rows[s] * d + c, y);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dws[s] = fmaf(a[e], y[e], dws[s]);
+        }
+    }
+    for (int s = 0; s < k; ++s) dws[s] = wave_sum_u(dws[s]);
     // gradient at the chosen experts: dw itself, or through w = g_sel / S
     float dsel[SMOES_K_MAX_DEV], gsel[SMOES_K_MAX_DEV];
     float S = 0.0f, wd = 0.0f;
