@@ -7,7 +7,7 @@ the workload re-estimates them); inter-bin MI loss and its logit gradient;
 expert-contiguous permutation; grouped SwiGLU expert GEMMs with shared
 experts; weighted combine. Inputs are resident in HBM before timing starts.
 
-    python bench.py [--steps K] [--warmup W] [--config I] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
 Prints one JSON line (the last line on stdout). `value` is tokens/s; the
 `roofline` object covers the stage that takes the most time, with its
@@ -132,7 +132,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--workload", default=None,
+                    help="workload name (default: the DeepSeekMoE-like layer, deepseekmoe-vlm)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=2)
     ap.add_argument("--rowmajor-weights", action="store_true",
@@ -155,7 +156,7 @@ def main():
     S.lib()  # fail loudly if the HIP library is missing
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda:0"
-    cfg = W.CONFIGS[args.config]
+    cfg = W.workload(args.workload or W.BENCH_WORKLOAD)
     log(f"[bench] generating workload {cfg.name} (seed {cfg.seed})")
     inp = W.make_layer_inputs(cfg)
 

@@ -74,8 +74,9 @@ def _rep(n: int, v: int, t: int) -> Tuple[Tuple[int, int], ...]:
     return tuple((v, t) for _ in range(n))
 
 
-# The five workloads. Index 0 is the small fp32 parity case; index 1 is the
-# DeepSeekMoE-like layer that throughput is quoted on.
+# The five workloads: the small fp32 parity case, the DeepSeekMoE-like layer
+# that throughput is quoted on, a fine-grained-expert layer, the
+# DeepSeekMoE-like layer at training batch size, and a large skewed layer.
 CONFIGS: List[LayerConfig] = [
     LayerConfig("tiny-fp32", _rep(1, 384, 128), d=256, E=8, k=2, inter=512,
                 n_shared=0, n_bins=2, dtype=F32, seed=0),
@@ -91,6 +92,18 @@ CONFIGS: List[LayerConfig] = [
                 inter=1536, n_shared=2, n_bins=8, dtype=BF16, seed=4,
                 logit_bias=True),
 ]
+
+
+BENCH_WORKLOAD = "deepseekmoe-vlm"
+
+
+def workload(name: str) -> LayerConfig:
+    """The workload of that name (tiny-fp32, deepseekmoe-vlm, finegrained-vlm,
+    deepseekmoe-vlm-train, large-skewed-vlm)."""
+    for c in CONFIGS:
+        if c.name == name:
+            return c
+    raise KeyError(f"unknown workload {name!r}; known: {[c.name for c in CONFIGS]}")
 
 
 def small_config(d=64, E=8, k=2, inter=64, n_shared=1, n_bins=2, samples=((24, 8), (10, 22)),

@@ -13,8 +13,8 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests run only where a GPU is visible; on the CPU they are skipped
-    # (the driver selects them explicitly with -m gpu on the GPU machine).
+    # GPU tests run only where a GPU is visible; on a machine without one they
+    # are skipped (select them with -m gpu).
     try:
         import torch
         have_gpu = torch.cuda.is_available()

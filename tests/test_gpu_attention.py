@@ -87,7 +87,7 @@ def test_attention_bench_shape_sampled_samples():
     # the bench workload's shape (4 samples x 1024 tokens, 16 heads of 128);
     # samples are independent (pinned in the oracle), so the oracle runs on
     # the first and the last sample alone
-    cfg = W.CONFIGS[1]
+    cfg = W.workload(W.BENCH_WORKLOAD)
     a = W.make_attention_inputs(cfg.samples, cfg.d, 16, 16, 128, seed=cfg.seed)
     say("attention bench shape", a.T)
     o, mh = _run_attention(a)

@@ -203,7 +203,7 @@ def test_backward_bench_layer_sampled():
     gradients of three routed experts over their rows and the shared
     experts' weight gradients over all tokens; the router weight and bias
     gradients are checked as dz^T x and the column sums of dz in float64."""
-    cfg = W.CONFIGS[1]
+    cfg = W.workload(W.BENCH_WORKLOAD)
     inp = W.make_layer_inputs(cfg)
     rng = np.random.default_rng(77)
     dout = _mask_ties(inp, W.f32_to_bf16_bits(rng.standard_normal((cfg.T, cfg.d)).astype(np.float32)))

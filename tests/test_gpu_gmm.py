@@ -140,7 +140,7 @@ def test_gmm_single_token_and_no_tokens():
 
 def test_gmm_bench_shape():
     # the bench layer's tokens (4096 x 2048, bf16), K = 2, one update then the score
-    cfg = W.CONFIGS[1]
+    cfg = W.workload(W.BENCH_WORKLOAD)
     inp = W.make_layer_inputs(cfg, with_weights=False)
     rng = np.random.default_rng(64)
     n, smu, ssig = W.random_gmm_state(rng, cfg.d, 2, count=1000.0, spread=0.05)

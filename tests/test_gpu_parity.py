@@ -415,19 +415,20 @@ def test_pack_weights_layout(d, E, inter, shared):
         assert np.array_equal(got.cpu().numpy().view(np.uint16), exp), name
 
 
-def test_layer_config0_full():
-    inp = W.make_layer_inputs(W.CONFIGS[0])
+def test_layer_tiny_fp32_full():
+    inp = W.make_layer_inputs(W.workload("tiny-fp32"))
     spec, _, outs = run_gpu_layer(inp)
     ref = run_oracle_layer(inp)
     _check_layer(inp, spec, outs, ref, fp32=True)
     assert _check_mi(outs, ref, inp, strict=False) <= 1e-3
 
 
-@pytest.mark.parametrize("ci", [1, 2, 3, 4])
-def test_layer_config_full(ci):
-    """The full-size workloads in the launch configuration the benchmark times;
-    routing, scores and MI on every token, the output on a seeded sample."""
-    cfg = W.CONFIGS[ci]
+@pytest.mark.parametrize("name", ["deepseekmoe-vlm", "finegrained-vlm", "deepseekmoe-vlm-train", "large-skewed-vlm"])
+def test_layer_full_size(name):
+    """The full-size bf16 workloads in the launch configuration the benchmark
+    times; routing, scores and MI on every token, the output on a seeded
+    sample."""
+    cfg = W.workload(name)
     inp = W.make_layer_inputs(cfg)
     spec, _, outs = run_gpu_layer(inp)
     rows = np.sort(np.random.default_rng(ci).choice(cfg.T, size=192, replace=False))
@@ -437,9 +438,9 @@ def test_layer_config_full(ci):
     assert err <= 1e-3, err
 
 
-def test_layer_config1_full_rowmajor_weights():
+def test_layer_deepseekmoe_full_rowmajor_weights():
     """The benchmark workload through the row-major bf16 weight path."""
-    cfg = W.CONFIGS[1]
+    cfg = W.workload(W.BENCH_WORKLOAD)
     inp = W.make_layer_inputs(cfg)
     spec, _, outs = run_gpu_layer(inp, packed=False)
     rows = np.sort(np.random.default_rng(11).choice(cfg.T, size=128, replace=False))
@@ -447,10 +448,10 @@ def test_layer_config1_full_rowmajor_weights():
     _check_layer(inp, spec, outs, ref, rows=rows)
 
 
-def test_layer_aligned_router_config1_strict_mi():
+def test_layer_deepseekmoe_aligned_router_strict_mi():
     """Config-1 shapes with a modality-aligned router: MI ~1e-3, so the
     end-to-end MI and gradient meet the 1e-5 bound directly."""
-    cfg = W.CONFIGS[1]
+    cfg = W.workload(W.BENCH_WORKLOAD)
     inp = W.make_layer_inputs(cfg)
     wg = W.aligned_router(inp, 0.5)
     spec, _, outs = run_gpu_layer(inp, w_gate=wg)
