@@ -144,8 +144,8 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures the single-GPU layer only: this build runs on one MI355X, with no "
-              "expert parallelism or collectives; use --gpus 1", file=sys.stderr)
+        print("bench.py measures the single-GPU layer only: the library runs one layer on one MI355X, "
+              "with no expert parallelism or collectives; use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -1,7 +1,7 @@
 """CPU oracle of one SMoES-routed MoE layer (test infrastructure only).
 
-This is the checker, not the product: only the tests, the smoke entry and the
-CPU-baseline leg of the benchmark may import it. It shares no code with the
+It is the reference the GPU path is checked against, not part of it: only the
+tests, the smoke entry and the CPU-baseline leg of the benchmark may import it. It shares no code with the
 HIP path. Everything is plain NumPy in float64 on the exact stored input values
 (bf16 inputs are widened exactly), written step by step in the order and
 notation of the paper, "Soft Modality-Guided Expert Specialization in
