@@ -303,6 +303,12 @@ SMALL_LAYERS = [
     dict(d=136, E=10, k=3, inter=48, n_shared=2, n_bins=5, samples=((150, 70), (33, 17)), dtype=W.BF16),
     # three tokens
     dict(d=64, E=4, k=2, inter=32, n_shared=0, n_bins=2, samples=((2, 1),), dtype=W.BF16),
+    # the maxima: 256 experts, top-16, 64 bins of 4 (about 25 rows per expert: short tiles everywhere)
+    dict(d=256, E=256, k=16, inter=64, n_shared=1, n_bins=64, samples=((300, 100),), dtype=W.BF16),
+    # no vision token at all (the vision statistics stay empty)
+    dict(d=128, E=16, k=4, inter=64, n_shared=1, n_bins=4, samples=((0, 200), (0, 57)), dtype=W.BF16),
+    # an empty sample between two others (its MI is 0)
+    dict(d=128, E=16, k=4, inter=64, n_shared=0, n_bins=4, samples=((100, 50), (0, 0), (30, 20)), dtype=W.BF16),
 ]
 
 
@@ -431,7 +437,7 @@ def test_layer_full_size(name):
     cfg = W.workload(name)
     inp = W.make_layer_inputs(cfg)
     spec, _, outs = run_gpu_layer(inp)
-    rows = np.sort(np.random.default_rng(ci).choice(cfg.T, size=192, replace=False))
+    rows = np.sort(np.random.default_rng(cfg.seed).choice(cfg.T, size=192, replace=False))
     ref = run_oracle_layer(inp, rows=rows)
     _check_layer(inp, spec, outs, ref, rows=rows)
     err = _check_mi(outs, ref, inp, strict=False)
