@@ -46,6 +46,8 @@ LAYERS = [
     dict(d=64, E=32, k=2, inter=32, n_shared=1, n_bins=4, samples=((9, 5),)),
     # three tokens
     dict(d=64, E=4, k=2, inter=32, n_shared=0, n_bins=2, samples=((2, 1),)),
+    # the maxima: 256 experts, top-16 (about 25 rows per expert)
+    dict(d=128, E=256, k=16, inter=64, n_shared=1, n_bins=64, samples=((300, 100),)),
 ]
 
 
