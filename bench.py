@@ -64,13 +64,16 @@ def source_digest(path):
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(kernel_stage):
+def measured_traffic(kernel_stage, workload):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when it is missing or the kernel source changed since it was taken."""
+    None when it is missing, was taken on another workload, or the kernel
+    source changed since it was taken."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
     except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload:
         return None
     ent = rec.get(kernel_stage)
     if not ent:
@@ -94,7 +97,8 @@ def cpu_model():
 
 def cpu_baseline(cfg, inp, n_samples, runs=3):
     """The float64 oracle, as it stands, on the first n_samples samples: one
-    warm-up run, then the median of `runs` timed runs."""
+    warm-up run, then the median of `runs` timed runs (runs=1: one run, no
+    warm-up)."""
     import numpy as np
     import oracle as O
     try:
@@ -116,15 +120,107 @@ def cpu_baseline(cfg, inp, n_samples, runs=3):
                         beta=cfg.beta, tau=cfg.tau)
         return time.perf_counter() - t0
 
-    once()  # warm-up
+    if runs > 1:
+        once()  # warm-up
     dt = float(np.median([once() for _ in range(runs)]))
     affinity = len(os.sched_getaffinity(0))
     cores = min(threads, affinity)
     return {"value": Ts / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {n_samples} samples ({Ts} tokens) of the workload: full layer forward "
+            "sample": f"first {n_samples} sample(s) ({Ts} tokens) of the workload: full layer forward "
                       f"(statistics, routing, MI + gradient, permutation, experts) in float64 NumPy; "
-                      f"median of {runs} runs after one warm-up, {dt:.2f} s per run; "
+                      + (f"median of {runs} runs after one warm-up" if runs > 1 else "one run") +
+                      f", {dt:.2f} s per run; "
                       f"{threads} BLAS threads, {affinity} CPUs in the affinity mask ({cpu_model()})"}
+
+
+def memory_bound_rows(S, W, cfg, spec, dev_in, outs, ws, work, reps):
+    """Per-call times of the memory-bound entry points with the MALL flushed
+    before each call (a 1 GiB write), their algorithmic GB/s against the 8 TB/s
+    peak and against a measured 1 GiB device-to-device copy; the combine is
+    timed inside a single-stream layer call (its input, the routed rows, is
+    written by the GEMM just before it)."""
+    import numpy as np
+    import torch
+    dev = dev_in["x"].device
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, flushed=True):
+        fn()
+        ts = []
+        for _ in range(max(reps, 5)):
+            if flushed:
+                flush.fill_(1.0)
+            ev[0].record()
+            fn()
+            ev[1].record()
+            torch.cuda.synchronize()
+            ts.append(ev[0].elapsed_time(ev[1]))
+        return float(np.median(ts))
+
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    src.fill_(2.0)
+    dst = torch.empty_like(src)
+    copy_ms = timed(lambda: dst.copy_(src))
+    copy_gbs = 2 * (1 << 30) / (copy_ms * 1e-3) / 1e9
+    del src, dst
+    L = S.lib()
+    T, d, E, k = cfg.T, cfg.d, cfg.E, cfg.k
+    xdt = S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32
+    nr = int(L.smoes_route_workspace_size(T, d, E, xdt))
+    wr = torch.empty(max(nr, 1), dtype=torch.uint8, device=dev)
+    nm = int(L.smoes_modality_workspace_size(T, d))
+    wm = torch.empty(nm, dtype=torch.uint8, device=dev)
+    nmi = int(L.smoes_mi_workspace_size(T, E, cfg.n_batch, cfg.n_bins))
+    wmi = torch.empty(nmi, dtype=torch.uint8, device=dev)
+    npm = int(L.smoes_permute_workspace_size(T, E, k))
+    wpm = torch.empty(npm, dtype=torch.uint8, device=dev)
+    M = torch.empty((T, 2), dtype=torch.float32, device=dev)
+    p = S._p
+    calls = {
+        "route": lambda: S._check(L.smoes_route(p(dev_in["x"]), xdt, T, d, p(dev_in["w_gate"]), p(dev_in["logit_bias"]),
+                                                E, k, 0, p(outs["logits"]), p(outs["probs"]), p(outs["topk_idx"]),
+                                                p(outs["topk_w"]), p(wr), nr, S._stream()), "smoes_route"),
+        "modality": lambda: S._check(L.smoes_modality_score(p(dev_in["x"]), xdt, T, d, p(dev_in["modality_id"]),
+                                                            p(dev_in["gauss_n"]), p(dev_in["gauss_smu"]),
+                                                            p(dev_in["gauss_ssig"]), 0, cfg.beta, cfg.tau, 1e-6,
+                                                            p(M), p(wm), nm, S._stream()), "smoes_modality_score"),
+        "mi": lambda: S._check(L.smoes_mi_loss(p(outs["probs"]), p(M), T, E, p(dev_in["sample_offsets"]), cfg.n_batch,
+                                               p(dev_in["expert_to_bin"]), cfg.n_bins, 1.0, p(outs["mi_per_sample"]),
+                                               p(outs["loss"]), p(outs["dlogits"]), p(wmi), nmi, S._stream()),
+                               "smoes_mi_loss"),
+        "permute": lambda: S._check(L.smoes_permute(p(outs["topk_idx"]), T, E, k, p(outs["expert_offsets"]),
+                                                    p(outs["perm_token"]), p(outs["perm_inv"]), None, xdt, d, None,
+                                                    p(wpm), npm, S._stream()), "smoes_permute"),
+    }
+    rows = {"copy_ceiling": {"what": "device-to-device copy of 1 GiB (read + write), MALL flushed",
+                             "ms": round(copy_ms, 5), "gbs": round(copy_gbs, 1),
+                             "frac_hbm": round(copy_gbs / PEAK_HBM_GBS, 4)}}
+    for name, fn in calls.items():
+        ms_f = timed(fn)
+        ms_w = timed(fn, flushed=False)
+        # the modality score alone (update = 0) reads x once and writes M
+        b = T * d * (2 if cfg.dtype == W.BF16 else 4) + 8 * T if name == "modality" else work[name]["bytes"]
+        gbs = b / (ms_f * 1e-3) / 1e9
+        rows[name] = {"ms": round(ms_f, 5), "ms_warm": round(ms_w, 5), "bytes": int(b), "gbs": round(gbs, 1),
+                      "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "frac_copy": round(gbs / copy_gbs, 4)}
+    # combine inside a single-stream layer call, MALL flushed before the call
+    ci = S.STAGES.index("combine")
+    cms = []
+    for _ in range(max(reps, 5)):
+        e = S.Events(only=ci)
+        flush.fill_(1.0)
+        S.moe_forward(spec, dev_in, outs, ws, events=e)
+        torch.cuda.synchronize()
+        cms.append(e.stage_ms(ci))
+        e.close()
+    c_ms = float(np.median(cms))
+    gbs = work["combine"]["bytes"] / (c_ms * 1e-3) / 1e9
+    rows["combine"] = {"ms": round(c_ms, 5), "bytes": int(work["combine"]["bytes"]), "gbs": round(gbs, 1),
+                       "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "frac_copy": round(gbs / copy_gbs, 4),
+                       "note": "inside the layer call, after the routed down GEMM wrote its input"}
+    del flush
+    return rows
 
 
 def main():
@@ -133,9 +229,13 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=None,
-                    help="workload name (default: the DeepSeekMoE-like layer, deepseekmoe-vlm)")
+                    help="workload name (default: the largest single-GPU layer, large-skewed-vlm)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-samples", type=int, default=2)
+    ap.add_argument("--cpu-samples", type=int, default=None,
+                    help="samples the CPU oracle runs on (default: 1 at hidden size >= 4096, else 2)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the rows timed beside the layer (memory-bound kernels, statistics update, "
+                         "binning, GMM, attention score, training step)")
     ap.add_argument("--rowmajor-weights", action="store_true",
                     help="bf16 expert weights row-major instead of the packed fragment order")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -252,7 +352,7 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom
     roof["kernel_ms"] = round(dom_ms, 5)  # mean over the timed calls (HIP events on its stream)
-    roof["traffic"] = measured_traffic(dom)
+    roof["traffic"] = measured_traffic(dom, cfg.name)
 
     # The same stages with every stage on the caller's stream (no side
     # streams): each kernel owns the chip, so these are the kernels' own
@@ -292,203 +392,213 @@ def main():
         "stages": stages,
         "stages_serial": stages_serial,
     }
-    # Gaussian statistics update (Eq. 5-7) followed by the score (Eq. 8-9) on
-    # this workload's tokens: the modality stage of a layer that re-estimates
-    # its statistics from the batch. Timed on its own, on copies of the state.
-    T_, d_ = cfg.T, cfg.d
-    g_n, g_mu, g_sig = dev_in["gauss_n"].clone(), dev_in["gauss_smu"].clone(), dev_in["gauss_ssig"].clone()
-    M_u = torch.empty((T_, 2), dtype=torch.float32, device=dev)
-    nws_u = int(S.lib().smoes_modality_workspace_size(T_, d_))
-    ws_u = torch.empty(nws_u, dtype=torch.uint8, device=dev)
-    xdt = 1 if cfg.dtype == W.BF16 else 0
+    # Memory-bound kernels with the 256 MB MALL flushed: a 1 GiB write before
+    # every timed call, each entry point called on its own (HIP events on the
+    # stream it runs on), next to a plain device copy of 1 GiB (the measured
+    # copy ceiling) and the 8 TB/s HBM peak.
+    if not args.no_extras:
+        log("[bench] memory-bound kernels, MALL flushed")
+        line["memory_bound"] = memory_bound_rows(S, W, cfg, spec, dev_in, outs, ws, work, args.steps)
+    if not args.no_extras:
+        # Gaussian statistics update (Eq. 5-7) followed by the score (Eq. 8-9) on
+        # this workload's tokens: the modality stage of a layer that re-estimates
+        # its statistics from the batch. Timed on its own, on copies of the state.
+        T_, d_ = cfg.T, cfg.d
+        g_n, g_mu, g_sig = dev_in["gauss_n"].clone(), dev_in["gauss_smu"].clone(), dev_in["gauss_ssig"].clone()
+        M_u = torch.empty((T_, 2), dtype=torch.float32, device=dev)
+        nws_u = int(S.lib().smoes_modality_workspace_size(T_, d_))
+        ws_u = torch.empty(nws_u, dtype=torch.uint8, device=dev)
+        xdt = 1 if cfg.dtype == W.BF16 else 0
 
-    def update_call():
-        S._check(S.lib().smoes_modality_score(S._p(dev_in["x"]), xdt, T_, d_, S._p(dev_in["modality_id"]),
-                                              S._p(g_n), S._p(g_mu), S._p(g_sig), 1, cfg.beta, cfg.tau, 1e-6,
-                                              S._p(M_u), S._p(ws_u), nws_u, S._stream()), "smoes_modality_score")
-    for _ in range(3):
-        update_call()
-    ev_u = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    u_ms = []
-    for _ in range(args.steps):
-        ev_u[0].record()
-        update_call()
-        ev_u[1].record()
-        torch.cuda.synchronize()
-        u_ms.append(ev_u[0].elapsed_time(ev_u[1]))
-    um = float(np.median(u_ms))
-    u_bytes = 2 * T_ * d_ * (2 if cfg.dtype == W.BF16 else 4) + T_ + T_ * 8
-    # Momentum-adaptive binning + bin-level balance loss (+ gradient, added onto
-    # the MI gradient) + MSI on this step's routing: timed on its own, not part
-    # of the layer step above.
-    T, E = cfg.T, cfg.E
-    e2b_next = torch.empty(E, dtype=torch.int32, device=dev)
-    load_ema = torch.zeros((2, E), dtype=torch.float64, device=dev)
-    nws = int(S.lib().smoes_binning_workspace_size(T, E, cfg.n_bins))
-    bws = torch.empty(nws, dtype=torch.uint8, device=dev)
-    bin_out = dict(counts=torch.empty((2, E), dtype=torch.int32, device=dev),
-                   f_spec=torch.empty(E, dtype=torch.float64, device=dev),
-                   loss=torch.empty(1, dtype=torch.float32, device=dev),
-                   msi=torch.empty(1, dtype=torch.float32, device=dev))
+        def update_call():
+            S._check(S.lib().smoes_modality_score(S._p(dev_in["x"]), xdt, T_, d_, S._p(dev_in["modality_id"]),
+                                                  S._p(g_n), S._p(g_mu), S._p(g_sig), 1, cfg.beta, cfg.tau, 1e-6,
+                                                  S._p(M_u), S._p(ws_u), nws_u, S._stream()), "smoes_modality_score")
+        for _ in range(3):
+            update_call()
+        ev_u = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        u_ms = []
+        for _ in range(args.steps):
+            ev_u[0].record()
+            update_call()
+            ev_u[1].record()
+            torch.cuda.synchronize()
+            u_ms.append(ev_u[0].elapsed_time(ev_u[1]))
+        um = float(np.median(u_ms))
+        u_bytes = 2 * T_ * d_ * (2 if cfg.dtype == W.BF16 else 4) + T_ + T_ * 8
+        # Momentum-adaptive binning + bin-level balance loss (+ gradient, added onto
+        # the MI gradient) + MSI on this step's routing: timed on its own, not part
+        # of the layer step above.
+        T, E = cfg.T, cfg.E
+        e2b_next = torch.empty(E, dtype=torch.int32, device=dev)
+        load_ema = torch.zeros((2, E), dtype=torch.float64, device=dev)
+        nws = int(S.lib().smoes_binning_workspace_size(T, E, cfg.n_bins))
+        bws = torch.empty(nws, dtype=torch.uint8, device=dev)
+        bin_out = dict(counts=torch.empty((2, E), dtype=torch.int32, device=dev),
+                       f_spec=torch.empty(E, dtype=torch.float64, device=dev),
+                       loss=torch.empty(1, dtype=torch.float32, device=dev),
+                       msi=torch.empty(1, dtype=torch.float32, device=dev))
 
-    def binning_call():
-        S._check(S.lib().smoes_binning(S._p(outs["probs"]), S._p(outs["topk_idx"]), S._p(dev_in["modality_id"]),
-                                       T, E, cfg.k, S._p(dev_in["expert_to_bin"]), cfg.n_bins, cfg.beta,
-                                       S._p(load_ema), S._p(bin_out["counts"]), S._p(bin_out["f_spec"]),
-                                       S._p(e2b_next), 1e-3, S._p(bin_out["loss"]), S._p(outs["dlogits"]), 1,
-                                       S._p(bin_out["msi"]), S._p(bws), bws.numel(), S._stream()), "smoes_binning")
-
-    for _ in range(3):
-        binning_call()
-    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    b0.record()
-    for _ in range(args.steps):
-        binning_call()
-    b1.record()
-    torch.cuda.synchronize()
-    bin_ms = b0.elapsed_time(b1) / args.steps
-    bin_bytes = T * (2 * 4 * E + 4 * cfg.k + 1)  # probs read, dlogits read+write, top-k, labels
-    line["extra"] = {"gauss_update": {"what": "Gaussian statistics update from the batch (EMA-Welford, Eq. 5-7) then "
-                                              "the modality score (Eq. 8-9), one layer; x read twice",
-                                      "ms": round(um, 5), "gbs": round(u_bytes / (um * 1e-3) / 1e9, 1),
-                                      "frac_hbm": round(u_bytes / (um * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
-                     "binning": {"what": "momentum-adaptive bins + bin-level load balance loss and gradient "
-                                         "(added onto dlogits) + MSI, one layer, this step's routing",
-                                 "ms": round(bin_ms, 5), "gbs": round(bin_bytes / (bin_ms * 1e-3) / 1e9, 1),
-                                 "frac_hbm": round(bin_bytes / (bin_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}}
-    # GMM estimator (K = 2 components per modality, the supplementary GMM
-    # ablation's best setting): one stepwise-EM update on this batch, then the
-    # score. Timed on its own, not part of the layer step above.
-    K_gmm = 2
-    rng_g = np.random.default_rng(cfg.seed + 200)
-    gst = W.random_gmm_state(rng_g, cfg.d, K_gmm, count=1000.0, spread=0.05)
-    g_n, g_smu, g_ssig = (torch.from_numpy(a).to(dev) for a in gst)
-    g_M = torch.empty((cfg.T, 2), dtype=torch.float32, device=dev)
-    g_nb = int(S.lib().smoes_gmm_workspace_size(cfg.T, cfg.d, K_gmm))
-    g_ws = torch.empty(g_nb, dtype=torch.uint8, device=dev)
-    x_code = S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32
-
-    def gmm_call():
-        S._check(S.lib().smoes_gmm_modality_score(S._p(dev_in["x"]), x_code, cfg.T, cfg.d, K_gmm,
-                                                  S._p(dev_in["modality_id"]), S._p(g_n), S._p(g_smu), S._p(g_ssig),
-                                                  1, cfg.beta, cfg.tau, 1e-6, S._p(g_M), None, S._p(g_ws), g_nb,
-                                                  S._stream()), "smoes_gmm_modality_score")
-
-    for _ in range(3):
-        gmm_call()
-    g_times = []
-    for _ in range(args.steps):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        gmm_call()
-        e1.record()
-        torch.cuda.synchronize()
-        g_times.append(e0.elapsed_time(e1))
-    g_ms = float(np.median(g_times))
-    x_bytes = cfg.T * cfg.d * (2 if cfg.dtype == W.BF16 else 4)
-    g_bytes = 3 * x_bytes + 2 * 3 * K_gmm * cfg.d * 4 * 2  # x read by the E-step, the statistics and the score; state
-    line["extra"]["gmm_score"] = {
-        "what": f"GMM estimator, K={K_gmm} diagonal components per modality: E-step, stepwise-EM update of the "
-                "state, mixture-likelihood score (one layer)",
-        "ms": round(g_ms, 5), "tokens_per_s": round(cfg.T / (g_ms * 1e-3), 1),
-        "gbs": round(g_bytes / (g_ms * 1e-3) / 1e9, 1),
-        "frac_hbm": round(g_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
-    # Attention-accumulated score (Eq. 2-4) on the same token layout: causal
-    # per-sample attention of a 16-head, d_head = 128 attention layer (the
-    # backbone's hidden size 2048) with the scores as two extra value
-    # channels, then the head mean and the norm-weighted update. Timed on its
-    # own, not part of the layer step above.
-    n_heads, head_dim = 16, cfg.d // 16
-    if head_dim in (64, 128):
-        log("[bench] attention-accumulated score")
-        ai = W.make_attention_inputs(cfg.samples, cfg.d, n_heads, n_heads, head_dim, seed=cfg.seed + 100)
-        aq, ak, av, ax, axa = t(ai.q), t(ai.k), t(ai.v), t(ai.x), t(ai.x_attn)
-        aoff, am = t(ai.sample_offsets), t(ai.m_in)
-        ao = torch.empty((cfg.T, n_heads, head_dim), dtype=torch.bfloat16, device=dev)
-        amh = torch.empty((cfg.T, n_heads, 2), dtype=torch.float32, device=dev)
-        amo = torch.empty((cfg.T, 2), dtype=torch.float32, device=dev)
-
-        def attn_call():
-            S.attention_scores(aq, ak, av, aoff, am, o=ao, m_heads=amh)
-            S.attn_score_update(ax, axa, amh, am, out=amo)
+        def binning_call():
+            S._check(S.lib().smoes_binning(S._p(outs["probs"]), S._p(outs["topk_idx"]), S._p(dev_in["modality_id"]),
+                                           T, E, cfg.k, S._p(dev_in["expert_to_bin"]), cfg.n_bins, cfg.beta,
+                                           S._p(load_ema), S._p(bin_out["counts"]), S._p(bin_out["f_spec"]),
+                                           S._p(e2b_next), 1e-3, S._p(bin_out["loss"]), S._p(outs["dlogits"]), 1,
+                                           S._p(bin_out["msi"]), S._p(bws), bws.numel(), S._stream()), "smoes_binning")
 
         for _ in range(3):
-            attn_call()
-        a_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-        a_att = []
-        a_tot = []
+            binning_call()
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record()
         for _ in range(args.steps):
-            a_ev[0].record()
-            S.attention_scores(aq, ak, av, aoff, am, o=ao, m_heads=amh)
-            a_ev[1].record()
-            S.attn_score_update(ax, axa, amh, am, out=amo)
-            a_ev[2].record()
-            torch.cuda.synchronize()
-            a_att.append(a_ev[0].elapsed_time(a_ev[1]))
-            a_tot.append(a_ev[0].elapsed_time(a_ev[2]))
-        att_ms = float(np.median(a_att))
-        tot_ms = float(np.median(a_tot))
-        lens = np.diff(ai.sample_offsets).astype(np.float64)
-        att_flops = float(n_heads * 4 * head_dim * np.sum(lens * (lens + 1) / 2))  # causal half only
-        upd_bytes = cfg.T * (2 * cfg.d * (2 if cfg.dtype == W.BF16 else 4) + n_heads * 8 + 16)
-        line["extra"]["attention_score"] = {
-            "what": f"causal per-sample attention ({n_heads} heads x {head_dim}) carrying the modality scores "
-                    "as fp32 value channels + head mean + norm-weighted update (Eq. 2-4), one layer",
-            "ms": round(tot_ms, 5), "attention_ms": round(att_ms, 5),
-            "tokens_per_s": round(cfg.T / (tot_ms * 1e-3), 1),
-            "attention_tflops": round(att_flops / (att_ms * 1e-3) / 1e12, 2),
-            "attention_frac_mfma": round(att_flops / (att_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-            "update_gbs": round(upd_bytes / ((tot_ms - att_ms) * 1e-3) / 1e9, 1) if tot_ms > att_ms else None}
-    # Training step of the layer: the forward above, then the backward with a
-    # synthetic upstream gradient and the MI gradient as the auxiliary logit
-    # gradient (every gradient: combine weights, logits, router weight and
-    # bias, routed and shared expert weights, input). Timed on its own.
-    if spec.weights_packed:
-        log("[bench] training step (forward + backward)")
-        rm = {n: t(getattr(inp, n)) for n in ("w13", "w2", "ws13", "ws2")}
-        packed_t = S.pack_transposed_weights(spec, rm)
-        del rm
-        rng_b = np.random.default_rng(cfg.seed + 300)
-        dout = t(W.f32_to_bf16_bits(rng_b.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
-        # the training forward keeps the experts' gate / up pre-activations for the backward
-        spec_tr = dataclasses.replace(spec, save_preact=True)
-        ws_tr = torch.empty(S.workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
-        bws_t = torch.empty(S.backward_workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
-        S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-        grads = S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], workspace=bws_t,
-                               streams=streams)
+            binning_call()
+        b1.record()
+        torch.cuda.synchronize()
+        bin_ms = b0.elapsed_time(b1) / args.steps
+        bin_bytes = T * (2 * 4 * E + 4 * cfg.k + 1)  # probs read, dlogits read+write, top-k, labels
+        line["extra"] = {"gauss_update": {"what": "Gaussian statistics update from the batch (EMA-Welford, Eq. 5-7) then "
+                                                  "the modality score (Eq. 8-9), one layer; x read twice",
+                                          "ms": round(um, 5), "gbs": round(u_bytes / (um * 1e-3) / 1e9, 1),
+                                          "frac_hbm": round(u_bytes / (um * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+                         "binning": {"what": "momentum-adaptive bins + bin-level load balance loss and gradient "
+                                             "(added onto dlogits) + MSI, one layer, this step's routing",
+                                     "ms": round(bin_ms, 5), "gbs": round(bin_bytes / (bin_ms * 1e-3) / 1e9, 1),
+                                     "frac_hbm": round(bin_bytes / (bin_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}}
+        # GMM estimator (K = 2 components per modality, the supplementary GMM
+        # ablation's best setting): one stepwise-EM update on this batch, then the
+        # score. Timed on its own, not part of the layer step above.
+        K_gmm = 2
+        rng_g = np.random.default_rng(cfg.seed + 200)
+        gst = W.random_gmm_state(rng_g, cfg.d, K_gmm, count=1000.0, spread=0.05)
+        g_n, g_smu, g_ssig = (torch.from_numpy(a).to(dev) for a in gst)
+        g_M = torch.empty((cfg.T, 2), dtype=torch.float32, device=dev)
+        g_nb = int(S.lib().smoes_gmm_workspace_size(cfg.T, cfg.d, K_gmm))
+        g_ws = torch.empty(g_nb, dtype=torch.uint8, device=dev)
+        x_code = S.SMOES_BF16 if cfg.dtype == W.BF16 else S.SMOES_F32
+
+        def gmm_call():
+            S._check(S.lib().smoes_gmm_modality_score(S._p(dev_in["x"]), x_code, cfg.T, cfg.d, K_gmm,
+                                                      S._p(dev_in["modality_id"]), S._p(g_n), S._p(g_smu), S._p(g_ssig),
+                                                      1, cfg.beta, cfg.tau, 1e-6, S._p(g_M), None, S._p(g_ws), g_nb,
+                                                      S._stream()), "smoes_gmm_modality_score")
+
         for _ in range(3):
-            S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-            S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
-                           workspace=bws_t, streams=streams)
-        tr_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-        f_ms, b_ms = [], []
+            gmm_call()
+        g_times = []
         for _ in range(args.steps):
-            tr_ev[0].record()
-            S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-            tr_ev[1].record()
-            S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
-                           workspace=bws_t, streams=streams)
-            tr_ev[2].record()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            gmm_call()
+            e1.record()
             torch.cuda.synchronize()
-            f_ms.append(tr_ev[0].elapsed_time(tr_ev[1]))
-            b_ms.append(tr_ev[1].elapsed_time(tr_ev[2]))
-        fm, bm = float(np.median(f_ms)), float(np.median(b_ms))
-        R = cfg.T * cfg.k
-        # dgrad (dH, dX) and wgrad (dW2, dW13): 12 d inter flops per routed row and per token for the
-        # shared block; the recompute of the gate / up pre-activations adds 4 more
-        bwd_flops = 12.0 * cfg.d * (R * cfg.inter + cfg.T * cfg.shared_inter)
-        line["extra"]["training_step"] = {
-            "what": "forward keeping the experts' gate / up pre-activations + backward of the layer (all "
-                    "gradients; MI gradient added to the logit gradient)",
-            "ms": round(fm + bm, 5), "forward_ms": round(fm, 5), "backward_ms": round(bm, 5),
-            "tokens_per_s": round(cfg.T / ((fm + bm) * 1e-3), 1),
-            "backward_tflops": round(bwd_flops / (bm * 1e-3) / 1e12, 2),
-            "backward_frac_mfma": round(bwd_flops / (bm * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
-        del packed_t, grads, bws_t, ws_tr
+            g_times.append(e0.elapsed_time(e1))
+        g_ms = float(np.median(g_times))
+        x_bytes = cfg.T * cfg.d * (2 if cfg.dtype == W.BF16 else 4)
+        g_bytes = 3 * x_bytes + 2 * 3 * K_gmm * cfg.d * 4 * 2  # x read by the E-step, the statistics and the score; state
+        line["extra"]["gmm_score"] = {
+            "what": f"GMM estimator, K={K_gmm} diagonal components per modality: E-step, stepwise-EM update of the "
+                    "state, mixture-likelihood score (one layer)",
+            "ms": round(g_ms, 5), "tokens_per_s": round(cfg.T / (g_ms * 1e-3), 1),
+            "gbs": round(g_bytes / (g_ms * 1e-3) / 1e9, 1),
+            "frac_hbm": round(g_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        # Attention-accumulated score (Eq. 2-4) on the same token layout: causal
+        # per-sample attention of a 16-head, d_head = 128 attention layer (the
+        # backbone's hidden size 2048) with the scores as two extra value
+        # channels, then the head mean and the norm-weighted update. Timed on its
+        # own, not part of the layer step above.
+        head_dim = 128
+        n_heads = cfg.d // head_dim
+        if head_dim in (64, 128):
+            log("[bench] attention-accumulated score")
+            ai = W.make_attention_inputs(cfg.samples, cfg.d, n_heads, n_heads, head_dim, seed=cfg.seed + 100)
+            aq, ak, av, ax, axa = t(ai.q), t(ai.k), t(ai.v), t(ai.x), t(ai.x_attn)
+            aoff, am = t(ai.sample_offsets), t(ai.m_in)
+            ao = torch.empty((cfg.T, n_heads, head_dim), dtype=torch.bfloat16, device=dev)
+            amh = torch.empty((cfg.T, n_heads, 2), dtype=torch.float32, device=dev)
+            amo = torch.empty((cfg.T, 2), dtype=torch.float32, device=dev)
+
+            def attn_call():
+                S.attention_scores(aq, ak, av, aoff, am, o=ao, m_heads=amh)
+                S.attn_score_update(ax, axa, amh, am, out=amo)
+
+            for _ in range(3):
+                attn_call()
+            a_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            a_att = []
+            a_tot = []
+            for _ in range(args.steps):
+                a_ev[0].record()
+                S.attention_scores(aq, ak, av, aoff, am, o=ao, m_heads=amh)
+                a_ev[1].record()
+                S.attn_score_update(ax, axa, amh, am, out=amo)
+                a_ev[2].record()
+                torch.cuda.synchronize()
+                a_att.append(a_ev[0].elapsed_time(a_ev[1]))
+                a_tot.append(a_ev[0].elapsed_time(a_ev[2]))
+            att_ms = float(np.median(a_att))
+            tot_ms = float(np.median(a_tot))
+            lens = np.diff(ai.sample_offsets).astype(np.float64)
+            att_flops = float(n_heads * 4 * head_dim * np.sum(lens * (lens + 1) / 2))  # causal half only
+            upd_bytes = cfg.T * (2 * cfg.d * (2 if cfg.dtype == W.BF16 else 4) + n_heads * 8 + 16)
+            line["extra"]["attention_score"] = {
+                "what": f"causal per-sample attention ({n_heads} heads x {head_dim}) carrying the modality scores "
+                        "as fp32 value channels + head mean + norm-weighted update (Eq. 2-4), one layer",
+                "ms": round(tot_ms, 5), "attention_ms": round(att_ms, 5),
+                "tokens_per_s": round(cfg.T / (tot_ms * 1e-3), 1),
+                "attention_tflops": round(att_flops / (att_ms * 1e-3) / 1e12, 2),
+                "attention_frac_mfma": round(att_flops / (att_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "update_gbs": round(upd_bytes / ((tot_ms - att_ms) * 1e-3) / 1e9, 1) if tot_ms > att_ms else None}
+        # Training step of the layer: the forward above, then the backward with a
+        # synthetic upstream gradient and the MI gradient as the auxiliary logit
+        # gradient (every gradient: combine weights, logits, router weight and
+        # bias, routed and shared expert weights, input). Timed on its own.
+        if spec.weights_packed:
+            log("[bench] training step (forward + backward)")
+            rm = {n: t(getattr(inp, n)) for n in ("w13", "w2", "ws13", "ws2")}
+            packed_t = S.pack_transposed_weights(spec, rm)
+            del rm
+            rng_b = np.random.default_rng(cfg.seed + 300)
+            dout = t(W.f32_to_bf16_bits(rng_b.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
+            # the training forward keeps the experts' gate / up pre-activations for the backward
+            spec_tr = dataclasses.replace(spec, save_preact=True)
+            ws_tr = torch.empty(S.workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
+            bws_t = torch.empty(S.backward_workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
+            S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
+            grads = S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], workspace=bws_t,
+                                   streams=streams)
+            for _ in range(3):
+                S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
+                S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
+                               workspace=bws_t, streams=streams)
+            tr_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            f_ms, b_ms = [], []
+            for _ in range(args.steps):
+                tr_ev[0].record()
+                S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
+                tr_ev[1].record()
+                S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
+                               workspace=bws_t, streams=streams)
+                tr_ev[2].record()
+                torch.cuda.synchronize()
+                f_ms.append(tr_ev[0].elapsed_time(tr_ev[1]))
+                b_ms.append(tr_ev[1].elapsed_time(tr_ev[2]))
+            fm, bm = float(np.median(f_ms)), float(np.median(b_ms))
+            R = cfg.T * cfg.k
+            # dgrad (dH, dX) and wgrad (dW2, dW13): 12 d inter flops per routed row and per token for the
+            # shared block; the recompute of the gate / up pre-activations adds 4 more
+            bwd_flops = 12.0 * cfg.d * (R * cfg.inter + cfg.T * cfg.shared_inter)
+            line["extra"]["training_step"] = {
+                "what": "forward keeping the experts' gate / up pre-activations + backward of the layer (all "
+                        "gradients; MI gradient added to the logit gradient)",
+                "ms": round(fm + bm, 5), "forward_ms": round(fm, 5), "backward_ms": round(bm, 5),
+                "tokens_per_s": round(cfg.T / ((fm + bm) * 1e-3), 1),
+                "backward_tflops": round(bwd_flops / (bm * 1e-3) / 1e12, 2),
+                "backward_frac_mfma": round(bwd_flops / (bm * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            del packed_t, grads, bws_t, ws_tr
     if not args.no_cpu_baseline:
-        log(f"[bench] CPU oracle on {args.cpu_samples} samples")
-        line["cpu_baseline"] = cpu_baseline(cfg, inp, min(args.cpu_samples, cfg.n_batch))
+        n_cpu = args.cpu_samples if args.cpu_samples is not None else (1 if cfg.d >= 4096 else 2)
+        log(f"[bench] CPU oracle on {n_cpu} sample(s)")
+        line["cpu_baseline"] = cpu_baseline(cfg, inp, min(n_cpu, cfg.n_batch), runs=1 if cfg.d >= 4096 else 3)
     print(json.dumps(line), flush=True)
 
 

@@ -30,11 +30,13 @@
  *   - Return value: SMOES_OK (0) or a negative smoes_status. Argument checks
  *     happen on the host before anything is enqueued; on an error nothing is
  *     launched and no output is written. T = 0 is a successful no-op.
- *   - Values that live on the device are NOT checked (that would need a
- *     synchronisation); the caller guarantees them: modality ids in {0, 1},
- *     sample offsets non-decreasing with offsets[0] = 0 and offsets[n_batch] = T,
- *     expert_to_bin entries in [0, n_bins) with exactly E / n_bins experts per
- *     bin, top-k indices in [0, E) and distinct within a token.
+ *   - Values that live on the device are NOT checked on the host (that would
+ *     need a synchronisation); the caller guarantees them: modality ids in
+ *     {0, 1}, sample offsets non-decreasing with offsets[0] = 0 and
+ *     offsets[n_batch] = T, expert_to_bin entries in [0, n_bins) with exactly
+ *     E / n_bins experts per bin, top-k indices in [0, E) and distinct within
+ *     a token. smoes_check_inputs (or smoes_layer.check_inputs = 1) checks the
+ *     first three on the device and reports them in a flag word.
  *   - Activation dtype codes: SMOES_F32 (float) or SMOES_BF16 (bfloat16 bits,
  *     uint16 storage). Router weights, logits, gate probabilities, modality
  *     scores and losses are always float32.
@@ -252,6 +254,10 @@ typedef struct smoes_layer {
                            pre-activations (bf16, in its workspace) for
                            smoes_moe_backward, which then skips recomputing them
                            (packed bf16 layers only); 0: it does not */
+    int check_inputs;   /* 1: smoes_moe_forward first checks the device-resident
+                           preconditions (as smoes_check_inputs) and writes the
+                           flag word into its workspace (SMOES_BUF_CHECK_FLAGS);
+                           0: no check (the production setting) */
 } smoes_layer;
 
 /* Side streams for smoes_moe_forward and smoes_moe_backward (caller-owned;
@@ -327,7 +333,10 @@ enum smoes_stage {
 size_t smoes_workspace_bytes(const smoes_layer* desc);
 
 /*
- * One SMoES MoE layer forward. Shapes as in the entry points above, plus
+ * One SMoES MoE layer forward (Sec. 3.1: softmax router and top-k experts;
+ * Sec. 3.2.2, Eq. 5-9: Gaussian modality score; Sec. 3.3-3.4, Eq. 12-15:
+ * inter-bin MI loss and its logit gradient; the MoE layer's experts with the
+ * backbone's always-on shared experts). Shapes as in the entry points above, plus
  * inter >= 16, inter % 16 == 0 and shared_inter % 16 == 0. The expert FFN is
  * SwiGLU: down(silu(gate x) * up x), silu(a) = a / (1 + exp(-a)); the shared
  * experts (ungated, weight 1) are one SwiGLU of inner size shared_inter.
@@ -340,6 +349,51 @@ size_t smoes_workspace_bytes(const smoes_layer* desc);
  */
 int smoes_moe_forward(const smoes_layer* desc, const smoes_layer_io* io,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Intermediate buffers inside the workspace of smoes_moe_forward. */
+enum smoes_buffer {
+    SMOES_BUF_H_ROUTED = 0,   /* [T*k, inter] act_dtype: silu(gate) * up of every routed row */
+    SMOES_BUF_H_SHARED = 1,   /* [T, shared_inter] act_dtype: the same for the shared experts */
+    SMOES_BUF_Y_ROUTED = 2,   /* [T*k, d] act_dtype: expert output of every routed row */
+    SMOES_BUF_Y_SHARED = 3,   /* [T, d] act_dtype: shared experts' output */
+    SMOES_BUF_CHECK_FLAGS = 4 /* [1] int32: flag word of check_inputs (SMOES_CHECK_* bits) */
+};
+
+/*
+ * Device address (*ptr) and byte size (*bytes) of one intermediate buffer of
+ * smoes_moe_forward inside `workspace` (the same pointer the forward got).
+ * Routed rows are in the expert-contiguous order of expert_offsets /
+ * perm_token (row r belongs to token perm_token[r]). The contents are those
+ * of the last forward call on this workspace, once it has completed; they
+ * stay valid until the workspace is reused. Host-side arithmetic only: no
+ * device access. SMOES_ERR_ARG for a NULL pointer, an invalid desc or an
+ * unknown `which`; the shared buffers have 0 bytes when shared_inter == 0.
+ */
+int smoes_workspace_buffer(const smoes_layer* desc, void* workspace, int which, void** ptr, size_t* bytes);
+
+/* Bits of the input-check flag word. */
+enum smoes_check_flag {
+    SMOES_CHECK_MODALITY_ID = 1,    /* a modality id is neither 0 nor 1 */
+    SMOES_CHECK_SAMPLE_OFFSETS = 2, /* offsets[0] != 0, offsets[n_batch] != T, or a decrease */
+    SMOES_CHECK_EXPERT_TO_BIN = 4   /* a bin index outside [0, n_bins), or a bin without
+                                       exactly E / n_bins experts */
+};
+
+/*
+ * Debug check of the device-resident inputs of a layer call: io->modality_id
+ * (when not NULL), io->sample_offsets (when not NULL) and io->expert_to_bin
+ * are read on the device by one workgroup, and the OR of the violated
+ * SMOES_CHECK_* bits (0 when all hold) is written to flags[0] (device int32).
+ * Nothing else is read or written. With desc->check_inputs = 1,
+ * smoes_moe_forward runs the same check as its first step and writes the flag
+ * word into its workspace (SMOES_BUF_CHECK_FLAGS); the check reports, it does
+ * not stop the later kernels: with a non-zero flag the outputs of that call
+ * are undefined, and an out-of-range modality id or bin can make later
+ * kernels read out of bounds, so untrusted inputs go through this call alone
+ * first. Asynchronous on `stream`; SMOES_ERR_ARG for a NULL desc, io, flags
+ * or io->expert_to_bin; desc errors as smoes_workspace_bytes.
+ */
+int smoes_check_inputs(const smoes_layer* desc, const smoes_layer_io* io, int32_t* flags, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Packed expert weights (bf16). Same products and sums as the row-major    */

@@ -279,6 +279,7 @@ struct LayerWs {
     void* experts;
     void* ab_r;  // kept pre-activations (save_preact), else NULL
     void* ab_s;
+    int32_t* flags;  // input-check flag word
 };
 
 int check_layer(const smoes_layer* L) {
@@ -304,6 +305,7 @@ int check_layer(const smoes_layer* L) {
     if ((L->weights_packed != 0 && L->weights_packed != 1) || (L->save_preact != 0 && L->save_preact != 1))
         return SMOES_ERR_ARG;
     if (L->save_preact && !L->weights_packed) return SMOES_ERR_ARG;
+    if (L->check_inputs != 0 && L->check_inputs != 1) return SMOES_ERR_ARG;
     if (L->weights_packed && L->act_dtype != SMOES_BF16) return SMOES_ERR_ARG;
     if (!(L->beta >= 0.0f && L->beta <= 1.0f) || !(L->var_floor >= 0.0f) || L->tau != L->tau ||
         L->grad_scale != L->grad_scale)
@@ -330,6 +332,7 @@ size_t layer_ws_parts(const smoes_layer* L, LayerWs* out, void* base) {
         w.ab_r = c.take(sizeof(uint16_t) * T * L->k * 2 * L->inter);
         w.ab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
     }
+    w.flags = static_cast<int32_t*>(c.take(sizeof(int32_t)));
     if (out != nullptr) *out = w;
     return c.used + kAlign;
 }
@@ -370,6 +373,10 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     LayerWs w;
     layer_ws_parts(L, &w, workspace);
     const int64_t T = L->T;
+    if (L->check_inputs &&
+        launch_check_inputs(io->modality_id, T, io->sample_offsets, L->n_batch, io->expert_to_bin, L->E, L->n_bins,
+                            w.flags, s) != hipSuccess)
+        return SMOES_ERR_HIP;
     float* logits = io->logits != nullptr ? io->logits : w.logits;
     int32_t* offsets = io->expert_offsets != nullptr ? io->expert_offsets : w.offsets;
     int32_t* perm_token = io->perm_token != nullptr ? io->perm_token : w.perm_token;
@@ -467,6 +474,44 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     if (sides != nullptr) SMOES_TRY(hipStreamWaitEvent(s, e_join, 0));
 #undef SMOES_TRY
     return SMOES_OK;
+}
+
+int smoes_workspace_buffer(const smoes_layer* L, void* workspace, int which, void** ptr, size_t* bytes) {
+    if (check_layer(L) != SMOES_OK || workspace == nullptr || ptr == nullptr || bytes == nullptr)
+        return SMOES_ERR_ARG;
+    LayerWs w;
+    layer_ws_parts(L, &w, workspace);
+    if (which == SMOES_BUF_CHECK_FLAGS) {
+        *ptr = w.flags;
+        *bytes = sizeof(int32_t);
+        return SMOES_OK;
+    }
+    ExpertArgs a{};
+    a.T = L->T;
+    a.d = L->d;
+    a.E = L->E;
+    a.k = L->k;
+    a.inter = L->inter;
+    a.shared_inter = L->shared_inter;
+    a.act_dtype = L->act_dtype;
+    const ExpertFwdBuffers fb = experts_fwd_buffers(a, w.experts);
+    const size_t es = L->act_dtype == SMOES_BF16 ? 2 : 4;
+    const size_t R = static_cast<size_t>(L->T) * L->k, T = static_cast<size_t>(L->T);
+    switch (which) {
+        case SMOES_BUF_H_ROUTED: *ptr = fb.h_r; *bytes = es * R * L->inter; return SMOES_OK;
+        case SMOES_BUF_H_SHARED: *ptr = fb.h_s; *bytes = es * T * L->shared_inter; return SMOES_OK;
+        case SMOES_BUF_Y_ROUTED: *ptr = fb.y_r; *bytes = es * R * L->d; return SMOES_OK;
+        case SMOES_BUF_Y_SHARED: *ptr = fb.y_s; *bytes = L->shared_inter > 0 ? es * T * L->d : 0; return SMOES_OK;
+        default: return SMOES_ERR_ARG;
+    }
+}
+
+int smoes_check_inputs(const smoes_layer* L, const smoes_layer_io* io, int32_t* flags, void* stream) {
+    const int st = check_layer(L);
+    if (st != SMOES_OK) return st;
+    if (io == nullptr || flags == nullptr || io->expert_to_bin == nullptr) return SMOES_ERR_ARG;
+    return hip_status(launch_check_inputs(io->modality_id, L->T, io->sample_offsets, L->n_batch, io->expert_to_bin,
+                                          L->E, L->n_bins, flags, as_stream(stream)));
 }
 
 // ------------------------------------------------------------------ layer backward

@@ -138,7 +138,13 @@ hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, const int32_t* p
 hipError_t launch_dwgate(const float* dz, const void* x, int64_t T, int d, int E, float* dw_gate, float* dbias,
                          void* ws, hipStream_t stream);
 
-// ---------------------------------------------------------------- GMM estimator// ---------------------------------------------------------------- GMM estimator
+// ---------------------------------------------------------------- input checks
+// One block: bitmask of violated device-resident preconditions (SMOES_CHECK_*) into flags[0].
+hipError_t launch_check_inputs(const uint8_t* modality_id, int64_t T, const int32_t* sample_offsets, int n_batch,
+                               const int32_t* expert_to_bin, int E, int n_bins, int32_t* flags,
+                               hipStream_t stream);
+
+// ---------------------------------------------------------------- GMM estimator
 size_t gmm_workspace_bytes(int64_t T, int d, int K);
 hipError_t launch_gmm(const void* x, int x_dtype, int64_t T, int d, int K, const uint8_t* modality_id, float* gmm_n,
                       float* gmm_smu, float* gmm_ssig, int update, float beta, float tau, float var_floor, float* M,

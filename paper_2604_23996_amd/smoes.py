@@ -44,7 +44,7 @@ class SmoesLayer(ctypes.Structure):
                 ("shared_inter", c_int), ("n_bins", c_int), ("n_batch", c_int), ("act_dtype", c_int),
                 ("tau", c_float), ("beta", c_float), ("var_floor", c_float), ("grad_scale", c_float),
                 ("renorm_topk", c_int), ("update_stats", c_int), ("weights_packed", c_int),
-                ("save_preact", c_int)]
+                ("save_preact", c_int), ("check_inputs", c_int)]
 
 
 _IO_FIELDS = ["x", "modality_id", "sample_offsets", "w_gate", "logit_bias", "expert_to_bin", "w13",
@@ -134,6 +134,11 @@ def lib() -> ctypes.CDLL:
         L.smoes_attn_score_update.restype = c_int
         L.smoes_attn_score_update.argtypes = [c_void, c_void, c_int, c_i64, c_int, c_void, c_int, c_void, c_void,
                                               c_void]
+        L.smoes_workspace_buffer.restype = c_int
+        L.smoes_workspace_buffer.argtypes = [ctypes.POINTER(SmoesLayer), c_void, c_int, ctypes.POINTER(c_void),
+                                             ctypes.POINTER(c_size)]
+        L.smoes_check_inputs.restype = c_int
+        L.smoes_check_inputs.argtypes = [ctypes.POINTER(SmoesLayer), ctypes.POINTER(SmoesLayerIO), c_void, c_void]
         L.smoes_streams_create.restype = c_int
         L.smoes_streams_create.argtypes = [ctypes.POINTER(SmoesStreams)]
         L.smoes_streams_destroy.restype = c_int
@@ -369,17 +374,63 @@ class LayerSpec:
     update_stats: bool = False
     weights_packed: bool = False
     save_preact: bool = False
+    check_inputs: bool = False
 
     def c(self) -> SmoesLayer:
         return SmoesLayer(self.T, self.d, self.E, self.k, self.inter, self.shared_inter, self.n_bins,
                           self.n_batch, self.act_dtype, self.tau, self.beta, self.var_floor,
                           self.grad_scale, int(self.renorm_topk), int(self.update_stats),
-                          int(self.weights_packed), int(self.save_preact))
+                          int(self.weights_packed), int(self.save_preact), int(self.check_inputs))
 
 
 def workspace_bytes(spec: LayerSpec) -> int:
     desc = spec.c()
     return int(lib().smoes_workspace_bytes(ctypes.byref(desc)))
+
+
+SMOES_BUF_H_ROUTED, SMOES_BUF_H_SHARED, SMOES_BUF_Y_ROUTED, SMOES_BUF_Y_SHARED, SMOES_BUF_CHECK_FLAGS = 0, 1, 2, 3, 4
+SMOES_CHECK_MODALITY_ID, SMOES_CHECK_SAMPLE_OFFSETS, SMOES_CHECK_EXPERT_TO_BIN = 1, 2, 4
+
+
+def workspace_buffer(spec: LayerSpec, workspace: torch.Tensor, which: int) -> torch.Tensor:
+    """smoes_workspace_buffer: the bytes of one intermediate buffer of the
+    forward (SMOES_BUF_*) as a uint8 view into `workspace`."""
+    desc = spec.c()
+    ptr, nb = c_void(), c_size()
+    _check(lib().smoes_workspace_buffer(ctypes.byref(desc), _p(workspace), which, ctypes.byref(ptr),
+                                        ctypes.byref(nb)), "smoes_workspace_buffer")
+    off = (ptr.value or 0) - workspace.data_ptr()
+    if nb.value == 0:
+        return workspace[:0]
+    if off < 0 or off + nb.value > workspace.numel():
+        raise SmoesError(SMOES_ERR_WORKSPACE, "smoes_workspace_buffer")
+    return workspace[off:off + nb.value]
+
+
+def _layer_io(inputs, outputs=None) -> SmoesLayerIO:
+    io = SmoesLayerIO()
+    outputs = outputs or {}
+    for name in _IO_FIELDS:
+        if name == "stage_events":
+            continue
+        t = inputs.get(name) if name in inputs else outputs.get(name)
+        setattr(io, name, None if t is None else _p(t).value)
+    io.stage_events = None
+    io.streams = None
+    return io
+
+
+def check_inputs(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
+                 flags: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """smoes_check_inputs: the SMOES_CHECK_* bitmask of the device-resident
+    inputs (modality_id, sample_offsets, expert_to_bin) as a device int32 [1]."""
+    if flags is None:
+        flags = torch.empty(1, dtype=torch.int32, device=inputs["expert_to_bin"].device)
+    desc = spec.c()
+    io = _layer_io(inputs)
+    _check(lib().smoes_check_inputs(ctypes.byref(desc), ctypes.byref(io), _p(flags), _stream()),
+           "smoes_check_inputs")
+    return flags
 
 
 SMOES_W13, SMOES_W2, SMOES_WS13, SMOES_WS2, SMOES_WGATE = 0, 1, 2, 3, 4

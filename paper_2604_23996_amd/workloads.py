@@ -94,7 +94,8 @@ CONFIGS: List[LayerConfig] = [
 ]
 
 
-BENCH_WORKLOAD = "deepseekmoe-vlm"
+# The benchmark's default: the largest layer that fits one GPU.
+BENCH_WORKLOAD = "large-skewed-vlm"
 
 
 def workload(name: str) -> LayerConfig:

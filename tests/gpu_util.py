@@ -84,22 +84,28 @@ def pack_layer_weights(spec: S.LayerSpec, dev_in) -> None:
 
 
 def run_gpu_layer(inp: W.LayerInputs, w_gate=None, update_stats=None, events=None, packed=None,
-                  streams=None, renorm_topk=False, keep_workspace=False, save_preact=False):
+                  streams=None, renorm_topk=False, keep_workspace=False, save_preact=False,
+                  zero_shared_down=False, check_inputs=False):
     """The full layer through smoes_moe_forward. For layers that do not update
     their statistics in the call, the Gaussian state is first estimated from
     the batch by smoes_modality_score(update=1) from the zero state. bf16
-    layers use packed expert weights unless packed=False."""
+    layers use packed expert weights unless packed=False. zero_shared_down
+    replaces the shared experts' down projection by zeros: their output is
+    then exactly 0 and `out` holds the routed part alone."""
     cfg = inp.cfg
     upd = cfg.update_stats if update_stats is None else update_stats
     if packed is None:
         packed = cfg.dtype == W.BF16
     spec = layer_spec(cfg, update_stats=upd, weights_packed=packed, renorm_topk=renorm_topk,
-                      save_preact=save_preact)
+                      save_preact=save_preact, check_inputs=check_inputs)
+    ws2 = inp.ws2
+    if zero_shared_down and ws2 is not None:
+        ws2 = np.zeros_like(ws2)
     dev_in = {
         "x": t(inp.x), "modality_id": t(inp.modality_id), "sample_offsets": t(inp.sample_offsets),
         "w_gate": t(inp.w_gate if w_gate is None else w_gate), "logit_bias": t(inp.logit_bias),
         "expert_to_bin": t(inp.expert_to_bin), "w13": t(inp.w13), "w2": t(inp.w2),
-        "ws13": t(inp.ws13), "ws2": t(inp.ws2),
+        "ws13": t(inp.ws13), "ws2": t(ws2),
     }
     if packed:
         pack_layer_weights(spec, dev_in)
@@ -128,3 +134,40 @@ def run_oracle_layer(inp: W.LayerInputs, w_gate=None, rows=None, update_stats=No
                            inp.w_gate if w_gate is None else w_gate, inp.logit_bias,
                            inp.expert_to_bin, cfg.n_bins, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
                            st, update_stats=upd, beta=cfg.beta, tau=cfg.tau, rows=rows)
+
+
+def routed_rows(spec: S.LayerSpec, ws: torch.Tensor) -> np.ndarray:
+    """Y_r [T*k, d] of the last forward on `ws` (smoes_workspace_buffer), as
+    float64; rows in the expert-contiguous order of perm_token."""
+    buf = S.workspace_buffer(spec, ws, S.SMOES_BUF_Y_ROUTED)
+    R = spec.T * spec.k
+    if spec.act_dtype == S.SMOES_BF16:
+        y = buf.view(torch.int16).reshape(R, spec.d).cpu().numpy().view(np.uint16)
+        return W.bf16_bits_to_f32(y).astype(np.float64)
+    return buf.view(torch.float32).reshape(R, spec.d).cpu().numpy().astype(np.float64)
+
+
+def check_expert_rows(inp: W.LayerInputs, spec: S.LayerSpec, ws: torch.Tensor, outs, experts=None,
+                      max_rows=None, fp32=False):
+    """Every routed row's expert output Y_r[r] = FFN_e(x[perm_token[r]]) of the
+    GPU's own permutation against the oracle's SwiGLU of the same rows, expert
+    by expert: normwise relative error <= 2e-2 (bf16) / 1e-5 (fp32) and
+    elementwise |gpu - ref| <= 1e-2 + 2e-2 |ref|. Returns the worst normwise error."""
+    cfg = inp.cfg
+    Y = routed_rows(spec, ws)
+    off = host(outs["expert_offsets"]).astype(np.int64)
+    perm = host(outs["perm_token"]).astype(np.int64)
+    worst = 0.0
+    for e in (range(cfg.E) if experts is None else experts):
+        a, b = off[e], off[e + 1]
+        if max_rows is not None:
+            b = min(b, a + max_rows)
+        if b <= a:
+            continue
+        ref = O.swiglu(inp.x[perm[a:b]], inp.w13[e], inp.w2[e])
+        got = Y[a:b]
+        err = rel_err(got, ref)
+        assert err <= (1e-5 if fp32 else 2e-2), (e, err)
+        assert np.all(np.abs(got - ref) <= 1e-2 + 2e-2 * np.abs(ref)), (e, np.max(np.abs(got - ref)))
+        worst = max(worst, err)
+    return worst

@@ -130,8 +130,8 @@ def test_layer_workspace_and_checks():
 
 
 def test_struct_layout_matches_header():
-    # smoes_layer: int64 + 8 int + 4 float + 4 int = 72 bytes; io: 28 pointers
-    assert ctypes.sizeof(S.SmoesLayer) == 72
+    # smoes_layer: int64 + 8 int + 4 float + 5 int = 76 bytes, padded to 80; io: 28 pointers
+    assert ctypes.sizeof(S.SmoesLayer) == 80
     assert ctypes.sizeof(S.SmoesLayerIO) == 28 * 8
     assert ctypes.sizeof(S.SmoesStreams) == 6 * 8
     text = open(S.HEADER_PATH).read()
@@ -220,3 +220,51 @@ def test_packed_weight_sizes_and_checks():
     # keeping the pre-activations is a packed bf16 feature, and it grows the workspace
     assert S.workspace_bytes(_spec(save_preact=True)) == 0
     assert S.workspace_bytes(_spec(weights_packed=True, save_preact=True)) > S.workspace_bytes(_spec(weights_packed=True))
+
+
+def test_workspace_buffers_lie_inside_the_workspace():
+    """smoes_workspace_buffer is host arithmetic: every buffer of the forward
+    lies inside the workspace the size query asks for, with the documented
+    byte size, and the buffers do not overlap."""
+    L = S.lib()
+    for sh, dt in ((48, S.SMOES_BF16), (0, S.SMOES_F32)):
+        spec = _spec(d=128, inter=96, shared_inter=sh, act_dtype=dt)
+        desc = spec.c()
+        n = L.smoes_workspace_bytes(ctypes.byref(desc))
+        base = 1 << 40
+        es = 2 if dt == S.SMOES_BF16 else 4
+        R = spec.T * spec.k
+        want = {S.SMOES_BUF_H_ROUTED: es * R * spec.inter, S.SMOES_BUF_H_SHARED: es * spec.T * sh,
+                S.SMOES_BUF_Y_ROUTED: es * R * spec.d, S.SMOES_BUF_Y_SHARED: es * spec.T * spec.d if sh else 0,
+                S.SMOES_BUF_CHECK_FLAGS: 4}
+        spans = []
+        for which, nbytes in want.items():
+            ptr, nb = ctypes.c_void_p(), ctypes.c_size_t()
+            assert L.smoes_workspace_buffer(ctypes.byref(desc), ctypes.c_void_p(base), which, ctypes.byref(ptr),
+                                            ctypes.byref(nb)) == S.SMOES_OK
+            assert nb.value == nbytes
+            assert base <= ptr.value and ptr.value + nb.value <= base + n
+            if nb.value:
+                spans.append((ptr.value, ptr.value + nb.value))
+        spans.sort()
+        assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+        ptr, nb = ctypes.c_void_p(), ctypes.c_size_t()
+        assert L.smoes_workspace_buffer(ctypes.byref(desc), ctypes.c_void_p(base), 9, ctypes.byref(ptr),
+                                        ctypes.byref(nb)) == S.SMOES_ERR_ARG
+        assert L.smoes_workspace_buffer(ctypes.byref(desc), None, 0, ctypes.byref(ptr),
+                                        ctypes.byref(nb)) == S.SMOES_ERR_ARG
+
+
+def test_check_inputs_host_errors():
+    L = S.lib()
+    desc = _spec().c()
+    io = S.SmoesLayerIO()
+    # no expert_to_bin, no flags, no io: rejected on the host, nothing launched
+    assert L.smoes_check_inputs(ctypes.byref(desc), ctypes.byref(io), FAKE, None) == S.SMOES_ERR_ARG
+    io.expert_to_bin = FAKE.value
+    assert L.smoes_check_inputs(ctypes.byref(desc), ctypes.byref(io), None, None) == S.SMOES_ERR_ARG
+    assert L.smoes_check_inputs(ctypes.byref(desc), None, FAKE, None) == S.SMOES_ERR_ARG
+    bad = _spec().c()
+    bad.check_inputs = 2
+    assert L.smoes_workspace_bytes(ctypes.byref(bad)) == 0
+    assert L.smoes_check_inputs(ctypes.byref(bad), ctypes.byref(io), FAKE, None) == S.SMOES_ERR_ARG

@@ -84,11 +84,11 @@ def test_attention_single_token_and_empty():
 
 
 def test_attention_bench_shape_sampled_samples():
-    # the bench workload's shape (4 samples x 1024 tokens, 16 heads of 128);
-    # samples are independent (pinned in the oracle), so the oracle runs on
-    # the first and the last sample alone
+    # the bench workload's shape (16 samples x 1024 tokens, hidden 4096 as 32
+    # heads of 128); samples are independent (pinned in the oracle), so the
+    # oracle runs on the first and the last sample alone
     cfg = W.workload(W.BENCH_WORKLOAD)
-    a = W.make_attention_inputs(cfg.samples, cfg.d, 16, 16, 128, seed=cfg.seed)
+    a = W.make_attention_inputs(cfg.samples, cfg.d, cfg.d // 128, cfg.d // 128, 128, seed=cfg.seed)
     say("attention bench shape", a.T)
     o, mh = _run_attention(a)
     for s in (0, len(cfg.samples) - 1):

@@ -197,15 +197,21 @@ def test_backward_rejects_fp32_and_rowmajor_layers():
         S.moe_backward(spec, {"x": x}, {}, ws, {"w13t": x, "w2t": x}, x)
 
 
-def test_backward_bench_layer_sampled():
-    """The 4096-token DeepSeekMoE-like layer (d 2048, 64 experts, top-6,
-    inter 1408, two shared experts), in the launch configuration of the
-    timed training step. The oracle computes dw, dz and dx of 128 sampled
-    tokens (the per-token gradients depend on that token alone), the weight
-    gradients of three routed experts over their rows and the shared
-    experts' weight gradients over all tokens; the router weight and bias
-    gradients are checked as dz^T x and the column sums of dz in float64."""
-    cfg = W.workload(W.BENCH_WORKLOAD)
+@pytest.mark.parametrize("name", ["deepseekmoe-vlm", W.BENCH_WORKLOAD])
+def test_backward_bench_layer_sampled(name):
+    """The full-size layers in the launch configuration of the timed training
+    step: the 4096-token DeepSeekMoE-like layer (d 2048, 64 experts, top-6,
+    inter 1408, two shared experts) and the benchmark's 16384-token layer
+    (d 4096, 160 experts, top-6, inter 1536, two shared experts, logit bias).
+    The oracle computes dw, dz and dx of 128 sampled tokens (the per-token
+    gradients depend on that token alone), the weight gradients of three
+    routed experts over their rows and the shared experts' weight gradients
+    over all tokens (at d 4096 on 64 sampled inner columns: the SwiGLU is
+    separable over its inner columns, so the gradient rows and columns of a
+    column subset are those of the sub-network of those columns); the router
+    weight and bias gradients are checked as dz^T x and the column sums of
+    dz in float64."""
+    cfg = W.workload(name)
     inp = W.make_layer_inputs(cfg)
     rng = np.random.default_rng(77)
     dout = _mask_ties(inp, W.f32_to_bf16_bits(rng.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
@@ -225,7 +231,7 @@ def test_backward_bench_layer_sampled():
         assert np.abs(got - ref[name]).max() <= ELEM * np.abs(ref[name]).max()
     # routed experts over all their rows
     _, offsets, perm_token, inv = O.permutation(idx, cfg.E)
-    for e in (0, 29, 63):
+    for e in (0, cfg.E // 2 - 3, cfg.E - 1):
         a, b = offsets[e], offsets[e + 1]
         toks = perm_token[a:b]
         slot = np.argmax(inv[toks] == np.arange(a, b)[:, None], axis=1)
@@ -235,11 +241,14 @@ def test_backward_bench_layer_sampled():
             assert rel_err(got, r) <= BARS[name], (name, e, rel_err(got, r))
             assert np.abs(got - r).max() <= ELEM * np.abs(r).max(), (name, e)
     # shared experts over all tokens
-    _, dws13, dws2 = O.swiglu_backward(X, inp.ws13, inp.ws2, dO)
-    for name, r in (("dws13", dws13), ("dws2", dws2)):
-        got = host(g[name])
-        assert rel_err(got, r) <= BARS[name], (name, rel_err(got, r))
-        assert np.abs(got - r).max() <= ELEM * np.abs(r).max(), name
+    SI = cfg.shared_inter
+    cols = np.arange(SI) if cfg.d <= 2048 else np.sort(rng.choice(SI, size=64, replace=False))
+    _, dws13, dws2 = O.swiglu_backward(X, inp.ws13[np.concatenate([cols, SI + cols])], inp.ws2[:, cols], dO)
+    got13 = host(g["dws13"])[np.concatenate([cols, SI + cols])]
+    got2 = host(g["dws2"])[:, cols]
+    for wname, got, r in (("dws13", got13, dws13), ("dws2", got2, dws2)):
+        assert rel_err(got, r) <= BARS[wname], (wname, rel_err(got, r))
+        assert np.abs(got - r).max() <= ELEM * np.abs(r).max(), wname
     # router: dW_gate = dz^T x and dbias = column sums of dz, float32 chunked sums
     dz = host(g["dz"]).astype(np.float64)
     assert rel_err(host(g["dw_gate"]), dz.T @ X) <= 1e-5

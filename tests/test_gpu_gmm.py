@@ -2,7 +2,8 @@
 mixture log-likelihood, Eq. 9 score, stepwise-EM update on Eq. 5-7) against
 the oracle.
 
-Bars: scores within 1e-5 absolute and responsibilities within 2e-5 (float32
+Bars: scores within 1e-5 relative, elementwise (the benchmark spec's bar for
+modality scores), and responsibilities within 2e-5 absolute (float32
 per-column terms, float64 sums); the float32 state after an update within
 1e-5 relative (normwise per array; counts elementwise), after three updates
 within 3e-5."""
@@ -40,6 +41,11 @@ def _gpu(x, mid, n, smu, ssig, update, tau=0.0, beta=0.9, want_resp=True):
     return host(M), (host(r) if r is not None else None), host(gn), host(gm), host(gs)
 
 
+def _check_scores(M, ref):
+    """Elementwise relative error of both score columns <= 1e-5."""
+    assert np.all(np.abs(M - ref) <= 1e-5 * np.abs(ref) + 1e-30), np.max(np.abs(M - ref) / np.abs(ref))
+
+
 def _check_state(st_ref: O.GmmState, gn, gm, gs, tol):
     assert np.allclose(gn, st_ref.n, rtol=tol, atol=0), (gn, st_ref.n)
     assert rel_err(gm, st_ref.s_mu) <= tol, rel_err(gm, st_ref.s_mu)
@@ -55,7 +61,7 @@ def test_gmm_score_and_responsibilities(K, dtype):
     st = O.GmmState.of(n, smu, ssig)
     pi, mu, var = O.gmm_params(st, VF)
     ref = O.gmm_modality_score(x, pi, mu, var, 0.5 * 136)
-    assert np.abs(M - ref).max() <= 1e-5
+    _check_scores(M, ref)
     assert np.abs(r - O.gmm_responsibilities(x, mid, pi, mu, var)).max() <= 2e-5
     assert np.array_equal(gn, n) and np.array_equal(gm, smu) and np.array_equal(gs, ssig)  # no update
 
@@ -72,7 +78,7 @@ def test_gmm_update_then_score(K, dtype):
     st1 = O.gmm_update(st, x, mid, 0.9, VF)
     _check_state(st1, gn, gm, gs, 1e-5)
     p1, m1, v1 = O.gmm_params(st1, VF)
-    assert np.abs(M - O.gmm_modality_score(x, p1, m1, v1, 30.0)).max() <= 1e-5
+    _check_scores(M, O.gmm_modality_score(x, p1, m1, v1, 30.0))
 
 
 def test_gmm_three_updates():
@@ -90,7 +96,7 @@ def test_gmm_three_updates():
         st = O.gmm_update(st, x, mid, 0.95, VF)
     _check_state(st, host(gn), host(gm), host(gs), 3e-5)
     p, m, v = O.gmm_params(st, VF)
-    assert np.abs(host(M) - O.gmm_modality_score(x, p, m, v, 0.5 * d)).max() <= 1e-5
+    _check_scores(host(M), O.gmm_modality_score(x, p, m, v, 0.5 * d))
 
 
 def test_gmm_with_one_component_matches_the_gaussian_score():
@@ -101,7 +107,7 @@ def test_gmm_with_one_component_matches_the_gaussian_score():
                           var_floor=VF)
     torch.cuda.synchronize()
     Mg = host(Mg[0] if isinstance(Mg, tuple) else Mg)
-    assert np.abs(M - Mg).max() <= 1e-6
+    assert np.all(np.abs(M - Mg) <= 1e-6 * np.abs(Mg) + 1e-30)
 
 
 def test_gmm_empty_modality_and_empty_component():
@@ -139,7 +145,7 @@ def test_gmm_single_token_and_no_tokens():
 
 
 def test_gmm_bench_shape():
-    # the bench layer's tokens (4096 x 2048, bf16), K = 2, one update then the score
+    # the bench layer's tokens (16384 x 4096, bf16), K = 2, one update then the score
     cfg = W.workload(W.BENCH_WORKLOAD)
     inp = W.make_layer_inputs(cfg, with_weights=False)
     rng = np.random.default_rng(64)
@@ -152,7 +158,7 @@ def test_gmm_bench_shape():
     st1 = O.gmm_update(st, inp.x, inp.modality_id, cfg.beta, VF)
     _check_state(st1, gn, gm, gs, 1e-5)
     p1, m1, v1 = O.gmm_params(st1, VF)
-    assert np.abs(M - O.gmm_modality_score(inp.x, p1, m1, v1, 0.5 * cfg.d)).max() <= 1e-5
+    _check_scores(M, O.gmm_modality_score(inp.x, p1, m1, v1, 0.5 * cfg.d))
 
 
 def test_gmm_is_reproducible():
