@@ -57,7 +57,9 @@ enum smoes_status {
     SMOES_ERR_ARG = -1,       /* a required pointer is NULL, or a scalar/dtype is out of range */
     SMOES_ERR_SHAPE = -2,     /* inconsistent sizes (see each entry point) */
     SMOES_ERR_WORKSPACE = -3, /* workspace_bytes smaller than the query's answer */
-    SMOES_ERR_HIP = -4        /* a HIP launch or runtime call failed */
+    SMOES_ERR_HIP = -4,       /* a HIP launch or runtime call failed */
+    SMOES_ERR_SCRATCH = -5    /* the problem needs more scratch than the fixed device array of
+                                 smoes_mi_loss_noalloc holds (SMOES_NOALLOC_SCRATCH_BYTES) */
 };
 
 /* Activation storage types. */
@@ -159,6 +161,28 @@ int smoes_mi_loss(const float* probs, const float* M, int64_t T, int E,
                   const int32_t* expert_to_bin, int n_bins, float grad_scale,
                   float* mi_per_sample, float* loss, float* dlogits,
                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * smoes_mi_loss without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, serving loops or harnesses that
+ * forbid allocation). Arguments, outputs and bits are those of
+ * smoes_mi_loss; the scratch comes from a fixed file-scope device array of
+ * SMOES_NOALLOC_SCRATCH_BYTES that every device the library runs on holds
+ * until the process ends. The call allocates nothing. It accepts problems
+ * whose smoes_mi_workspace_size(T, E, n_batch, n_bins) is at most
+ * SMOES_NOALLOC_SCRATCH_BYTES (16384 tokens in 16 samples with E = 160 need
+ * 1.3 MB, 65536 tokens in one sample with E = 256 need 4.1 MB) and returns
+ * SMOES_ERR_SCRATCH, launching nothing, beyond that. All calls on
+ * one device share that device's array, which keeps the last call's
+ * contents (no call relies on its initial contents): calls that may overlap
+ * in time on one device (different streams, threads) race on it and must be
+ * serialised by the caller.
+ */
+#define SMOES_NOALLOC_SCRATCH_BYTES (8u << 20)
+int smoes_mi_loss_noalloc(const float* probs, const float* M, int64_t T, int E,
+                          const int32_t* sample_offsets, int n_batch,
+                          const int32_t* expert_to_bin, int n_bins, float grad_scale,
+                          float* mi_per_sample, float* loss, float* dlogits, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Momentum-adaptive binning (Sec. 3.3, Eq. 10-11), bin-level load balance   */

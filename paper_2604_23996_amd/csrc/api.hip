@@ -76,6 +76,9 @@ const char* smoes_status_string(int status) {
         case SMOES_ERR_SHAPE: return "SMOES_ERR_SHAPE: inconsistent or unsupported sizes";
         case SMOES_ERR_WORKSPACE: return "SMOES_ERR_WORKSPACE: workspace smaller than the size query";
         case SMOES_ERR_HIP: return "SMOES_ERR_HIP: a HIP launch or runtime call failed";
+        case SMOES_ERR_SCRATCH:
+            return "SMOES_ERR_SCRATCH: the problem needs more scratch than the fixed device array of the "
+                   "no-allocation entry point holds";
         default: return "SMOES: unknown status code";
     }
 }

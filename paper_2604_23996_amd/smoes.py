@@ -23,6 +23,8 @@ LIB_PATH = os.path.join(_PKG, "libsmoes.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "smoes.h")
 
 SMOES_OK, SMOES_ERR_ARG, SMOES_ERR_SHAPE, SMOES_ERR_WORKSPACE, SMOES_ERR_HIP = 0, -1, -2, -3, -4
+SMOES_ERR_SCRATCH = -5
+SMOES_NOALLOC_SCRATCH_BYTES = 8 << 20
 SMOES_F32, SMOES_BF16 = 0, 1
 N_STAGES = 9
 STAGES = ("route", "modality", "mi", "permute", "gemm1", "gemm2", "combine", "gemm1_shared", "gemm2_shared")
@@ -94,6 +96,9 @@ def lib() -> ctypes.CDLL:
         L.smoes_mi_loss.restype = c_int
         L.smoes_mi_loss.argtypes = [c_void, c_void, c_i64, c_int, c_void, c_int, c_void, c_int, c_float,
                                     c_void, c_void, c_void, c_void, c_size, c_void]
+        L.smoes_mi_loss_noalloc.restype = c_int
+        L.smoes_mi_loss_noalloc.argtypes = [c_void, c_void, c_i64, c_int, c_void, c_int, c_void, c_int, c_float,
+                                            c_void, c_void, c_void, c_void]
         L.smoes_permute_workspace_size.restype = c_size
         L.smoes_permute_workspace_size.argtypes = [c_i64, c_int, c_int]
         L.smoes_permute.restype = c_int
@@ -243,6 +248,26 @@ def mi_loss(probs: torch.Tensor, M: torch.Tensor, sample_offsets: Optional[torch
     _check(lib().smoes_mi_loss(_p(probs), _p(M), T, E, _p(sample_offsets), n_batch, _p(expert_to_bin),
                                n_bins, grad_scale, _p(mi), _p(loss), _p(dl), _p(ws), nbytes, _stream()),
            "smoes_mi_loss")
+    return mi, loss, dl
+
+
+def mi_loss_noalloc(probs: torch.Tensor, M: torch.Tensor, sample_offsets: Optional[torch.Tensor],
+                    expert_to_bin: torch.Tensor, n_bins: int, grad_scale: float = 1.0,
+                    outputs: Optional[tuple] = None, want_grad: bool = True):
+    """smoes_mi_loss_noalloc (no workspace: the library's fixed device array).
+    `outputs` = (mi_per_sample, loss, dlogits or None) preallocated by the
+    caller, or None to allocate them here. Returns the three."""
+    T, E = probs.shape
+    n_batch = 1 if sample_offsets is None else sample_offsets.numel() - 1
+    if outputs is None:
+        dev = probs.device
+        outputs = (torch.empty(n_batch, dtype=torch.float32, device=dev),
+                   torch.empty(1, dtype=torch.float32, device=dev),
+                   torch.empty((T, E), dtype=torch.float32, device=dev) if want_grad else None)
+    mi, loss, dl = outputs
+    _check(lib().smoes_mi_loss_noalloc(_p(probs), _p(M), T, E, _p(sample_offsets), n_batch, _p(expert_to_bin),
+                                       n_bins, grad_scale, _p(mi), _p(loss), _p(dl), _stream()),
+           "smoes_mi_loss_noalloc")
     return mi, loss, dl
 
 

@@ -23,7 +23,7 @@ def test_exports_every_declared_function():
 
 
 def test_status_strings():
-    for code in (0, -1, -2, -3, -4):
+    for code in (0, -1, -2, -3, -4, -5):
         s = S.status_string(code)
         assert s.startswith("SMOES_")
     assert "unknown" in S.status_string(-99)
