@@ -287,7 +287,8 @@ typedef struct smoes_layer {
 /* Side streams for smoes_moe_forward and smoes_moe_backward (caller-owned;
  * see smoes_streams_create). */
 typedef struct smoes_streams {
-    void* side[2];   /* hipStream_t: [0] modality score + MI chain, [1] shared-expert GEMMs */
+    void* side[2];   /* hipStream_t: [0] the forward's modality score + MI chain, [1] the
+                        backward's router and shared-expert gradients */
     void* events[4]; /* hipEvent_t (timing disabled) used to fork and join them */
 } smoes_streams;
 
@@ -327,27 +328,31 @@ typedef struct smoes_layer_io {
      * smoes_events_create (entries may be NULL); events 2s and 2s + 1 are
      * recorded on the stream that runs stage s, before and after it. */
     void* const* stage_events;
-    /* optional side streams: NULL runs every stage on `stream`; otherwise the
-     * modality score and the MI chain run on side[0] and the shared experts'
-     * GEMMs on side[1], forked from and joined back into `stream` with the
-     * given events. One smoes_streams may serve consecutive calls; calls that
-     * overlap in time need one each. */
+    /* optional side streams: NULL runs every stage on `stream`, the routed and
+     * the shared experts' GEMMs in launches of their own; otherwise the
+     * modality score and the MI chain run on side[0], forked from and joined
+     * back into `stream` with the given events, and each expert GEMM covers
+     * the routed and the shared experts in one launch on `stream`. One
+     * smoes_streams may serve consecutive calls; calls that overlap in time
+     * need one each. */
     const smoes_streams* streams;
 } smoes_layer_io;
 
-/* Stages of smoes_moe_forward. ROUTE, PERMUTE, GEMM1, GEMM2 and COMBINE run
- * in this order on the caller's stream; MODALITY and then MI (after ROUTE)
- * run on io->streams->side[0], GEMM1_SHARED and GEMM2_SHARED on side[1]
- * (all on the caller's stream when io->streams is NULL); COMBINE waits for
- * the shared GEMMs and the caller's stream waits for both side streams
- * before the call's work is complete. */
+/* Stages of smoes_moe_forward. Without side streams every stage runs on the
+ * caller's stream in the order GEMM1_SHARED, GEMM2_SHARED, MODALITY, ROUTE,
+ * MI, PERMUTE, GEMM1, GEMM2, COMBINE. With io->streams, ROUTE, PERMUTE,
+ * GEMM1, GEMM2 and COMBINE run in this order on the caller's stream, GEMM1
+ * and GEMM2 each covering the routed and the shared experts (the two
+ * *_SHARED stages are then empty event pairs), MODALITY and then MI (after
+ * ROUTE) on side[0]; the caller's stream waits for side[0] before the
+ * call's work is complete. */
 enum smoes_stage {
     SMOES_STAGE_ROUTE = 0,        /* router GEMM + softmax + top-k */
     SMOES_STAGE_MODALITY = 1,     /* statistics update (optional) + modality score */
     SMOES_STAGE_MI = 2,           /* MI partials, loss, gradient */
     SMOES_STAGE_PERMUTE = 3,      /* expert-contiguous order + work lists */
-    SMOES_STAGE_GEMM1 = 4,        /* routed experts: grouped gate/up GEMM + SwiGLU */
-    SMOES_STAGE_GEMM2 = 5,        /* routed experts: grouped down GEMM */
+    SMOES_STAGE_GEMM1 = 4,        /* routed (+ shared, with side streams) experts: grouped gate/up GEMM + SwiGLU */
+    SMOES_STAGE_GEMM2 = 5,        /* routed (+ shared, with side streams) experts: grouped down GEMM */
     SMOES_STAGE_COMBINE = 6,      /* weighted combine + shared output */
     SMOES_STAGE_GEMM1_SHARED = 7, /* shared experts: gate/up GEMM + SwiGLU */
     SMOES_STAGE_GEMM2_SHARED = 8, /* shared experts: down GEMM */

@@ -414,34 +414,35 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     a.ab_s = L->shared_inter > 0 ? w.ab_s : nullptr;
     const WorkTables wt = experts_work_tables(a, w.experts);
 
-    // Caller's stream s: route -> permute -> routed GEMM1 -> routed GEMM2 ->
-    // [shared GEMMs done] -> combine. With caller-owned side streams
-    // (io->streams): b runs modality -> [route done] -> MI, c runs the
-    // shared GEMM1 -> GEMM2 (they need x only); both start after everything
-    // queued on s before this call, and s waits for both before the call's
-    // work is complete. Without them every stage runs on s, in the same
-    // order of dependencies.
+    // Without side streams every stage runs on the caller's stream s, each
+    // GEMM part in a launch of its own: shared GEMM1 -> shared GEMM2 ->
+    // modality -> route -> MI -> permute -> routed GEMM1 -> routed GEMM2 ->
+    // combine. With caller-owned side streams (io->streams) the modality
+    // score and then the MI chain (after the route) run on side[0], forked
+    // from s at the start of the call and joined back at its end, and each
+    // GEMM covers the routed and the shared experts in one launch on s
+    // (route -> permute -> GEMM1 -> GEMM2 -> combine): two concurrent GEMM
+    // launches slow each other down more than they gain from overlapping.
     const smoes_streams* sides = io->streams;
-    hipStream_t b = s, c = s;
-    hipEvent_t e_fork = nullptr, e_routed = nullptr, e_join = nullptr, e_shared = nullptr;
+    const bool merged = sides != nullptr;
+    hipStream_t b = s;
+    hipEvent_t e_fork = nullptr, e_routed = nullptr, e_join = nullptr;
     if (sides != nullptr) {
         b = as_stream(sides->side[0]);
-        c = as_stream(sides->side[1]);
         e_fork = static_cast<hipEvent_t>(sides->events[0]);
         e_routed = static_cast<hipEvent_t>(sides->events[1]);
         e_join = static_cast<hipEvent_t>(sides->events[2]);
-        e_shared = static_cast<hipEvent_t>(sides->events[3]);
         SMOES_TRY(hipEventRecord(e_fork, s));
-        SMOES_TRY(hipStreamWaitEvent(c, e_fork, 0));
         SMOES_TRY(hipStreamWaitEvent(b, e_fork, 0));
     }
-    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED, c));
-    SMOES_TRY(launch_experts_gemm1(a, w.experts, 2, c));
-    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED + 1, c));
-    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED, c));
-    SMOES_TRY(launch_experts_gemm2(a, w.experts, 2, c));
-    SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED + 1, c));
-    if (sides != nullptr) SMOES_TRY(hipEventRecord(e_shared, c));
+    if (!merged) {
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED, s));
+        SMOES_TRY(launch_experts_gemm1(a, w.experts, 2, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1_SHARED + 1, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED, s));
+        SMOES_TRY(launch_experts_gemm2(a, w.experts, 2, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED + 1, s));
+    }
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_MODALITY, b));
     SMOES_TRY(launch_modality(io->x, L->act_dtype, T, L->d, io->modality_id, io->gauss_n, io->gauss_smu,
                               io->gauss_ssig, L->update_stats ? 1 : 0, L->beta, L->tau, L->var_floor,
@@ -464,13 +465,18 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE, s));
     SMOES_TRY(launch_permute(io->topk_idx, T, L->E, L->k, offsets, perm_token, perm_inv, w.permute, &wt, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE + 1, s));
+    if (merged) {  // the shared stages are part of the merged launches: empty pairs
+        for (int st2 : {SMOES_STAGE_GEMM1_SHARED, SMOES_STAGE_GEMM2_SHARED}) {
+            SMOES_TRY(record(ev, 2 * st2, s));
+            SMOES_TRY(record(ev, 2 * st2 + 1, s));
+        }
+    }
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1, s));
-    SMOES_TRY(launch_experts_gemm1(a, w.experts, 1, s));
+    SMOES_TRY(launch_experts_gemm1(a, w.experts, merged ? 0 : 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1 + 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2, s));
-    SMOES_TRY(launch_experts_gemm2(a, w.experts, 1, s));
+    SMOES_TRY(launch_experts_gemm2(a, w.experts, merged ? 0 : 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2 + 1, s));
-    if (sides != nullptr) SMOES_TRY(hipStreamWaitEvent(s, e_shared, 0));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
     SMOES_TRY(launch_experts_combine(a, w.experts, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));
