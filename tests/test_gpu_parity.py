@@ -337,6 +337,10 @@ SMALL_LAYERS = [
     dict(d=128, E=16, k=4, inter=64, n_shared=1, n_bins=4, samples=((0, 200), (0, 57)), dtype=W.BF16),
     # an empty sample between two others (its MI is 0)
     dict(d=128, E=16, k=4, inter=64, n_shared=0, n_bins=4, samples=((100, 50), (0, 0), (30, 20)), dtype=W.BF16),
+    # at least 256 routed rows per expert on average: the forward GEMMs take
+    # 256-row tiles, with last tiles of every height (ragged d and inter too)
+    dict(d=136, E=4, k=2, inter=48, n_shared=1, n_bins=2, samples=((500, 300),), dtype=W.BF16),
+    dict(d=256, E=6, k=3, inter=160, n_shared=0, n_bins=3, samples=((700, 300), (200, 100)), dtype=W.BF16),
 ]
 
 
