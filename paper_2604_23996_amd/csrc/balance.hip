@@ -5,8 +5,9 @@
 //
 //   bal_partial : per 256-token chunk: per token the bins its top-k reaches
 //                 (kept for the gradient), counts C[m][e] of hard label m with
-//                 e in the token's top-k and tokens routed to each bin (LDS
-//                 integer adds), and per expert the gate mass over the tokens
+//                 e in the token's top-k and tokens routed to each bin (wave
+//                 ballots and popcounts, summed over the four waves in wave
+//                 order: no atomics), and per expert the gate mass over the tokens
 //                 routed to its bin (fp64, fixed order).
 //   bal_finalize: one block; sums the chunk partials in chunk order, then
 //                 L_bal = sum_e N_B (n_e / T_k)(S_e / T_k), the gradient
@@ -30,6 +31,7 @@ namespace {
 constexpr int kBalChunk = 256;    // tokens per partial block
 constexpr int kBalThreads = 256;  // 4 waves
 constexpr int kBalWaves = kBalThreads / kWave;
+static_assert(kBalWaves == 4, "per-wave counts are summed as four terms");
 
 struct BalWs {
     int32_t* cnt;    // [nchunk][2][E]
@@ -55,23 +57,22 @@ BalWs carve(void* ws, int64_t nchunk, int E, int n_bins) {
 }
 
 // Phase 1, one thread per token of the chunk: its top-k row (k loads in
-// flight), the bins it reaches as a bit mask (n_bins <= 64, bin map in LDS),
-// counts by label and expert and tokens per bin (LDS integer adds). Phase 2,
-// one wave per token with lanes over experts: gate mass of each expert over
-// the tokens routed to its bin (fp64, fixed order).
+// flight), the bins it reaches as a bit mask (n_bins <= 64, bin map in LDS);
+// counts by label and expert and tokens per bin from wave ballots (lane t of a
+// wave ends with the count of expert e0 + t, or of bin t) and popcounts, one
+// LDS row per wave. Phase 2, one wave per token with lanes over experts: gate
+// mass of each expert over the tokens routed to its bin (fp64, fixed order).
 __global__ void __launch_bounds__(kBalThreads)
 bal_partial_kernel(const float* __restrict__ probs, const int32_t* __restrict__ idx,
                    const uint8_t* __restrict__ mid, int64_t T, int E, int k, const int32_t* __restrict__ e2b,
                    int n_bins, int32_t* __restrict__ cnt_out, int32_t* __restrict__ tk_out,
                    double* __restrict__ mass_out, uint64_t* __restrict__ mask_out) {
-    __shared__ int32_t cnt[2][256];
-    __shared__ int32_t tk[64];
+    __shared__ int32_t cnt[kBalWaves][2][256];
+    __shared__ int32_t tk[kBalWaves][64];
     __shared__ int32_t bin_s[256];
     __shared__ uint64_t mask_s[kBalChunk];
     __shared__ double mass[kBalWaves][256];
     const int wave = threadIdx.x / kWave, lane = lane_id();
-    for (int i = threadIdx.x; i < 2 * 256; i += kBalThreads) cnt[i / 256][i % 256] = 0;
-    if (threadIdx.x < 64) tk[threadIdx.x] = 0;
     for (int e = threadIdx.x; e < E; e += kBalThreads) bin_s[e] = e2b[e];
     __syncthreads();
     const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kBalChunk;
@@ -79,24 +80,56 @@ bal_partial_kernel(const float* __restrict__ probs, const int32_t* __restrict__ 
     {
         const int r = threadIdx.x;
         uint64_t m = 0;
+        uint64_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;  // experts chosen: bit e & 63 of word e >> 6
+        int lab = 0;
         if (r < n) {
             const int64_t j = j0 + r;
             int ex[SMOES_K_MAX_DEV];
 #pragma unroll
             for (int s = 0; s < SMOES_K_MAX_DEV; ++s) ex[s] = s < k ? idx[j * k + s] : 0;
-            const int lab = mid[j] ? 1 : 0;
+            lab = mid[j] ? 1 : 0;
 #pragma unroll
             for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
                 if (s < k) {
-                    m |= 1ull << bin_s[ex[s]];
-                    atomicAdd(&cnt[lab][ex[s]], 1);
+                    const int e = ex[s];
+                    m |= 1ull << bin_s[e];
+                    const uint64_t bit = 1ull << (e & 63);
+                    const int blk = e >> 6;
+                    b0 |= blk == 0 ? bit : 0ull;
+                    b1 |= blk == 1 ? bit : 0ull;
+                    b2 |= blk == 2 ? bit : 0ull;
+                    b3 |= blk == 3 ? bit : 0ull;
                 }
             }
             mask_out[j] = m;
         }
         mask_s[r] = m;
-        for (int b = 0; b < n_bins; ++b)
-            if ((m >> b) & 1ull) atomicAdd(&tk[b], 1);
+        const uint64_t eb[4] = {b0, b1, b2, b3};
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk) {
+            const int e0 = blk * 64;
+            if (e0 >= E) break;
+            const int ne = E - e0 < 64 ? E - e0 : 64;
+            const uint64_t mine = eb[blk];
+            int c0 = 0, c1 = 0;
+            for (int t = 0; t < ne; ++t) {
+                const int bit = static_cast<int>((mine >> t) & 1ull);
+                const int n0 = __popcll(__ballot(bit & (lab ^ 1)));
+                const int n1 = __popcll(__ballot(bit & lab));
+                c0 = lane == t ? n0 : c0;
+                c1 = lane == t ? n1 : c1;
+            }
+            if (lane < ne) {
+                cnt[wave][0][e0 + lane] = c0;
+                cnt[wave][1][e0 + lane] = c1;
+            }
+        }
+        int cb = 0;
+        for (int b = 0; b < n_bins; ++b) {
+            const int nb = __popcll(__ballot(static_cast<int>((m >> b) & 1ull)));
+            cb = lane == b ? nb : cb;
+        }
+        if (lane < n_bins) tk[wave][lane] = cb;
     }
     __syncthreads();
     int bin_of[4];
@@ -120,8 +153,13 @@ bal_partial_kernel(const float* __restrict__ probs, const int32_t* __restrict__ 
     for (int q = 0; q < 4; ++q) mass[wave][lane + q * kWave] = acc[q];
     __syncthreads();
     int32_t* co = cnt_out + static_cast<int64_t>(blockIdx.x) * 2 * E;
-    for (int i = threadIdx.x; i < 2 * E; i += kBalThreads) co[i] = cnt[i / E][i % E];
-    if (threadIdx.x < n_bins) tk_out[static_cast<int64_t>(blockIdx.x) * n_bins + threadIdx.x] = tk[threadIdx.x];
+    for (int i = threadIdx.x; i < 2 * E; i += kBalThreads) {
+        const int l = i / E, e = i % E;
+        co[i] = (cnt[0][l][e] + cnt[1][l][e]) + (cnt[2][l][e] + cnt[3][l][e]);
+    }
+    if (threadIdx.x < n_bins)
+        tk_out[static_cast<int64_t>(blockIdx.x) * n_bins + threadIdx.x] =
+            (tk[0][threadIdx.x] + tk[1][threadIdx.x]) + (tk[2][threadIdx.x] + tk[3][threadIdx.x]);
     for (int e = threadIdx.x; e < E; e += kBalThreads) {
         double sum = 0.0;
         for (int w = 0; w < kBalWaves; ++w) sum += mass[w][e];  // wave order

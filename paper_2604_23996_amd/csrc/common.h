@@ -145,6 +145,38 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
     __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | 0x70);
 }
 
+// ---------------------------------------------------------------- buffer-to-LDS loads as inline assembly
+//
+// With the builtin form the compiler sees the LDS writes of a buffer-to-LDS
+// load and, unable to tell them apart from reads of other ring slots, may wait
+// for every outstanding load before each LDS read, which drains the ring. The
+// kernels that use these order them with explicit vmcnt waits and barriers.
+// Descriptor words: base (48 bits, stride 0), record count in bytes, format.
+__device__ __forceinline__ i32x4_t buf_rsrc(const void* base, int bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return i32x4_t{__builtin_amdgcn_readfirstlane(static_cast<int>(a & 0xffffffffu)),
+                   __builtin_amdgcn_readfirstlane(static_cast<int>((a >> 32) & 0xffffu)),
+                   __builtin_amdgcn_readfirstlane(bytes), kBufferFlags};
+}
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)p));
+}
+// 16 bytes per lane from byte offset voff into LDS at lds + 16 lane (lds uniform;
+// it goes in through M0 as an operand, so the compiler sets M0 itself)
+__device__ __forceinline__ void dma16(i32x4_t rsrc, int voff, uint32_t lds) {
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)))
+                 : "memory");
+}
+// 4 bytes per lane into LDS at lds + 4 lane
+__device__ __forceinline__ void dma4(i32x4_t rsrc, int voff, uint32_t lds) {
+    asm volatile("buffer_load_dword %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)))
+                 : "memory");
+}
+
 // Values that are the same in every lane but that the compiler cannot prove
 // uniform (they derive from loads): pin them to SGPRs so buffer descriptors
 // built from them stay scalar.

@@ -1,16 +1,18 @@
 // Expert-contiguous permutation of the routed (token, slot) pairs: a stable
 // counting sort by expert with tokens ascending inside each expert.
 //
-//   perm_count  : per 256-token chunk, per-expert counts (LDS integer adds:
-//                 counts do not depend on their order).
+//   perm_count  : per 256-token chunk, per-expert counts: for every expert a
+//                 wave ballot of the lanes (tokens) that chose it and a
+//                 popcount, the four waves' counts summed in wave order.
 //   perm_scatter: per chunk; every block sums the chunk counts itself (per
 //                 expert: the total and the part before its chunk), scans the
 //                 totals over experts, and places its rows: for every expert a
 //                 wave ballot marks the lanes (tokens) that chose it, so the
 //                 rank of a token among the chunk's earlier tokens is a
-//                 popcount. The row order comes from prefix sums only, never
-//                 from atomics. Block 0 also writes expert_offsets and, when
-//                 asked, the grouped GEMMs' work tables.
+//                 popcount. Counts and row order come from ballots and
+//                 prefix sums only, never from atomics. Block 0 also writes
+//                 expert_offsets and, when asked, the grouped GEMMs' work
+//                 tables.
 // Row gathers (x_perm) copy 16-byte vectors with consecutive lanes on
 // consecutive addresses of one row.
 #include "common.h"
@@ -21,6 +23,7 @@ namespace smoes {
 namespace {
 
 constexpr int kChunk = 256;
+static_assert(kChunk / kWave == 4, "per-wave counts are summed as four terms");
 
 struct PermWs {
     int32_t* hist;  // [nchunk][E]
@@ -32,16 +35,54 @@ PermWs carve(void* ws) {
     return w;
 }
 
+// Bit e & 63 of word e >> 6: the experts a token chose (E <= 256).
+struct ExpertBits {
+    uint64_t w[4];
+};
+
+__device__ __forceinline__ ExpertBits chosen_bits(const int32_t* __restrict__ idx, int64_t j, bool live, int k,
+                                                  int (&sel)[SMOES_K_MAX_DEV]) {
+    uint64_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;
+#pragma unroll
+    for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
+        sel[s] = 0;
+        if (live && s < k) {
+            const int e = idx[j * k + s];
+            sel[s] = e;
+            const uint64_t bit = 1ull << (e & 63);
+            const int blk = e >> 6;
+            b0 |= blk == 0 ? bit : 0ull;
+            b1 |= blk == 1 ? bit : 0ull;
+            b2 |= blk == 2 ? bit : 0ull;
+            b3 |= blk == 3 ? bit : 0ull;
+        }
+    }
+    return ExpertBits{{b0, b1, b2, b3}};
+}
+
 __global__ void __launch_bounds__(kChunk)
 perm_count_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k, int32_t* __restrict__ hist) {
-    __shared__ int cnt[256];
-    for (int e = threadIdx.x; e < E; e += blockDim.x) cnt[e] = 0;
-    __syncthreads();
+    __shared__ int32_t cnt[kChunk / kWave][256];
+    const int wave = threadIdx.x / kWave, lane = lane_id();
     const int64_t j = static_cast<int64_t>(blockIdx.x) * kChunk + threadIdx.x;
-    if (j < T)
-        for (int s = 0; s < k; ++s) atomicAdd(&cnt[idx[j * k + s]], 1);
+    int sel[SMOES_K_MAX_DEV];
+    const ExpertBits eb = chosen_bits(idx, j, j < T, k, sel);
+    // lane t of the wave ends with the count of expert e0 + t
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+        const int e0 = blk * 64;
+        if (e0 >= E) break;
+        const int ne = E - e0 < 64 ? E - e0 : 64;
+        int c = 0;
+        for (int t = 0; t < ne; ++t) {
+            const int n = __popcll(__ballot(static_cast<int>((eb.w[blk] >> t) & 1ull)));
+            c = lane == t ? n : c;
+        }
+        if (lane < ne) cnt[wave][e0 + lane] = c;
+    }
     __syncthreads();
-    for (int e = threadIdx.x; e < E; e += blockDim.x) hist[static_cast<int64_t>(blockIdx.x) * E + e] = cnt[e];
+    for (int e = threadIdx.x; e < E; e += blockDim.x)
+        hist[static_cast<int64_t>(blockIdx.x) * E + e] = (cnt[0][e] + cnt[1][e]) + (cnt[2][e] + cnt[3][e]);
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
@@ -123,29 +164,14 @@ perm_scatter_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k, in
     const int64_t j = static_cast<int64_t>(blockIdx.x) * kChunk + threadIdx.x;
     const bool live = j < T;
     int sel[SMOES_K_MAX_DEV];
-    uint64_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;
-#pragma unroll
-    for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
-        sel[s] = 0;
-        if (live && s < k) {
-            const int e = idx[j * k + s];
-            sel[s] = e;
-            const uint64_t bit = 1ull << (e & 63);
-            const int blk = e >> 6;
-            b0 |= blk == 0 ? bit : 0ull;
-            b1 |= blk == 1 ? bit : 0ull;
-            b2 |= blk == 2 ? bit : 0ull;
-            b3 |= blk == 3 ? bit : 0ull;
-        }
-    }
+    const ExpertBits eb = chosen_bits(idx, j, live, k, sel);
     // one ballot per expert: which tokens of this wave chose it
-    const uint64_t bits[4] = {b0, b1, b2, b3};
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
         const int e0 = blk * 64;
         if (e0 >= E) break;
         const int ne = E - e0 < 64 ? E - e0 : 64;
-        const uint64_t mine = bits[blk];
+        const uint64_t mine = eb.w[blk];
         for (int t = 0; t < ne; ++t) {
             const uint64_t m = __ballot(static_cast<int>((mine >> t) & 1ull));
             if (lane == 0) masks[wave][e0 + t] = m;

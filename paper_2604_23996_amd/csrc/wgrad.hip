@@ -39,37 +39,6 @@ static_assert(WG_TM * WG_OP * 2 <= WG_ST * WG_SB, "epilogue tile fits the ring")
 typedef short wg_v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) wg_v4i16 wg_lds_v4i16;
 
-// Buffer loads straight to LDS, as inline assembly. With the builtin form the
-// compiler sees the LDS writes and, unable to tell them apart from the
-// transposing reads of other ring slots, waits for every outstanding load
-// before each read, which would drain the ring. Here the kernel orders them
-// itself: vmcnt waits plus a barrier before a slot is read. The LDS address
-// goes in through M0 as an operand, so the compiler sets M0 itself.
-// Descriptor words: base (48 bits, stride 0), record count in bytes, format.
-__device__ __forceinline__ i32x4_t wg_rsrc(const void* base, int bytes) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    return i32x4_t{__builtin_amdgcn_readfirstlane(static_cast<int>(a & 0xffffffffu)),
-                   __builtin_amdgcn_readfirstlane(static_cast<int>((a >> 32) & 0xffffu)),
-                   __builtin_amdgcn_readfirstlane(bytes), kBufferFlags};
-}
-__device__ __forceinline__ uint32_t wg_lds_addr(const void* p) {
-    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)p));
-}
-// 16 bytes per lane from byte offset voff into LDS at lds + 16 lane (lds uniform)
-__device__ __forceinline__ void wg_dma16(i32x4_t rsrc, int voff, uint32_t lds) {
-    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :
-                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)))
-                 : "memory");
-}
-// 4 bytes per lane into LDS at lds + 4 lane
-__device__ __forceinline__ void wg_dma4(i32x4_t rsrc, int voff, uint32_t lds) {
-    asm volatile("buffer_load_dword %0, %1, 0 offen lds"
-                 :
-                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)))
-                 : "memory");
-}
-
 struct WgArgs {
     int64_t T;
     int n_groups;           // E routed experts, or 1 (shared)
@@ -107,10 +76,10 @@ wgrad_kernel(WgArgs p) {
     const int wm = wave >> 1, wn = wave & 1;
     uint8_t* idx_lds = lds + WG_ST * WG_SB;
 
-    const i32x4_t rsA = wg_rsrc(p.A, p.a_rows * p.lda * 2);
-    const i32x4_t rsB = wg_rsrc(p.B, p.b_rows * p.ldb * 2);
-    const i32x4_t rsM = wg_rsrc(G ? p.map : nullptr, G ? p.map_len * 4 : 0);
-    const uint32_t lds0 = wg_lds_addr(lds);
+    const i32x4_t rsA = buf_rsrc(p.A, p.a_rows * p.lda * 2);
+    const i32x4_t rsB = buf_rsrc(p.B, p.b_rows * p.ldb * 2);
+    const i32x4_t rsM = buf_rsrc(G ? p.map : nullptr, G ? p.map_len * 4 : 0);
+    const uint32_t lds0 = lds_address(lds);
 
     // Load q of this wave (A: rows (wave * IA + q) * 4 + lane / 16, B: rows
     // (wave * IB + q) * 2 + lane / 32 of a stage) moves global chunk
@@ -135,7 +104,7 @@ wgrad_kernel(WgArgs p) {
         if constexpr (G != 0) {
             const int r = r0 + s * WG_BK + wave * 8 + lane;
             const int vo = (lane < 8 && r < r1) ? r * 4 : kOutOfRange;
-            wg_dma4(rsM, vo, lds0 + WG_ST * WG_SB + (s % WG_NI) * WG_IDX + wave * 256);
+            dma4(rsM, vo, lds0 + WG_ST * WG_SB + (s % WG_NI) * WG_IDX + wave * 256);
         }
     };
     auto map_of = [&](int s, int row) {
@@ -158,10 +127,10 @@ wgrad_kernel(WgArgs p) {
         }
     };
     auto issue_a = [&](int s, int q, int vo) {
-        wg_dma16(rsA, vo, lds0 + (s % WG_ST) * WG_SB + (wave * WG_IA + q) * 1024);
+        dma16(rsA, vo, lds0 + (s % WG_ST) * WG_SB + (wave * WG_IA + q) * 1024);
     };
     auto issue_b = [&](int s, int q, int vo) {
-        wg_dma16(rsB, vo, lds0 + (s % WG_ST) * WG_SB + WG_AB + (wave * WG_IB + q) * 1024);
+        dma16(rsB, vo, lds0 + (s % WG_ST) * WG_SB + WG_AB + (wave * WG_IB + q) * 1024);
     };
 
     f32x16_t acc[4][2];  // [n tile][m tile]: rows n, columns m
