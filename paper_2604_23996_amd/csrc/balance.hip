@@ -105,28 +105,34 @@ bal_partial_kernel(const float* __restrict__ probs, const int32_t* __restrict__ 
         }
         mask_s[r] = m;
         const uint64_t eb[4] = {b0, b1, b2, b3};
+        const uint32_t l1 = static_cast<uint32_t>(lab), l0 = l1 ^ 1u;
+        // lane t ends with the counts of expert e0 + t (experts past E are never chosen)
 #pragma unroll
         for (int blk = 0; blk < 4; ++blk) {
             const int e0 = blk * 64;
             if (e0 >= E) break;
-            const int ne = E - e0 < 64 ? E - e0 : 64;
-            const uint64_t mine = eb[blk];
+            const uint32_t lo = static_cast<uint32_t>(eb[blk]), hi = static_cast<uint32_t>(eb[blk] >> 32);
             int c0 = 0, c1 = 0;
-            for (int t = 0; t < ne; ++t) {
-                const int bit = static_cast<int>((mine >> t) & 1ull);
-                const int n0 = __popcll(__ballot(bit & (lab ^ 1)));
-                const int n1 = __popcll(__ballot(bit & lab));
+#pragma unroll
+            for (int t = 0; t < 64; ++t) {
+                const uint32_t bit = t < 32 ? (lo >> t) & 1u : (hi >> (t - 32)) & 1u;
+                const int n0 = __popcll(__ballot(static_cast<int>(bit & l0)));  // every lane takes part
+                const int n1 = __popcll(__ballot(static_cast<int>(bit & l1)));
                 c0 = lane == t ? n0 : c0;
                 c1 = lane == t ? n1 : c1;
             }
-            if (lane < ne) {
+            if (e0 + lane < E) {
                 cnt[wave][0][e0 + lane] = c0;
                 cnt[wave][1][e0 + lane] = c1;
             }
         }
+        // lane b ends with the tokens routed to bin b (bins past n_bins are never reached)
+        const uint32_t mlo = static_cast<uint32_t>(m), mhi = static_cast<uint32_t>(m >> 32);
         int cb = 0;
-        for (int b = 0; b < n_bins; ++b) {
-            const int nb = __popcll(__ballot(static_cast<int>((m >> b) & 1ull)));
+#pragma unroll
+        for (int b = 0; b < 64; ++b) {
+            const uint32_t bit = b < 32 ? (mlo >> b) & 1u : (mhi >> (b - 32)) & 1u;
+            const int nb = __popcll(__ballot(static_cast<int>(bit)));  // every lane takes part
             cb = lane == b ? nb : cb;
         }
         if (lane < n_bins) tk[wave][lane] = cb;

@@ -67,18 +67,21 @@ perm_count_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k, int3
     const int64_t j = static_cast<int64_t>(blockIdx.x) * kChunk + threadIdx.x;
     int sel[SMOES_K_MAX_DEV];
     const ExpertBits eb = chosen_bits(idx, j, j < T, k, sel);
-    // lane t of the wave ends with the count of expert e0 + t
+    // lane t of the wave ends with the count of expert e0 + t (experts past E
+    // are never chosen: their ballots are empty)
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
         const int e0 = blk * 64;
         if (e0 >= E) break;
-        const int ne = E - e0 < 64 ? E - e0 : 64;
+        const uint32_t lo = static_cast<uint32_t>(eb.w[blk]), hi = static_cast<uint32_t>(eb.w[blk] >> 32);
         int c = 0;
-        for (int t = 0; t < ne; ++t) {
-            const int n = __popcll(__ballot(static_cast<int>((eb.w[blk] >> t) & 1ull)));
+#pragma unroll
+        for (int t = 0; t < 64; ++t) {
+            const uint32_t bit = t < 32 ? (lo >> t) & 1u : (hi >> (t - 32)) & 1u;
+            const int n = __popcll(__ballot(static_cast<int>(bit)));  // every lane takes part in the ballot
             c = lane == t ? n : c;
         }
-        if (lane < ne) cnt[wave][e0 + lane] = c;
+        if (e0 + lane < E) cnt[wave][e0 + lane] = c;
     }
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += blockDim.x)

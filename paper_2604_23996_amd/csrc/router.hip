@@ -5,12 +5,16 @@
 //     fp32 router weights are split into three bf16 terms (hi + mid + lo
 //     reproduces each weight to ~2^-24), every product of a term with an exact
 //     bf16 activation is exact, and v_mfma_f32_16x16x32_bf16 accumulates in
-//     fp32. The split weights are stored in the order the MFMA reads them, so
-//     a wave loads a fragment as one contiguous 1 KB. A workgroup owns a tile
-//     of 64 or 128 tokens and one of KS ranges of the hidden dimension (KS
-//     chosen so that the grid fills the chip); its four waves split the
-//     experts, so every weight byte reaches a workgroup once per token tile.
-//     Each range's partial logits go to the workspace.
+//     fp32 (per 32-wide k-step the terms lo, mid, hi). The split weights are
+//     stored in the order the MFMA reads them (one contiguous 1 KB per
+//     fragment). A workgroup owns 128 tokens and one of KS ranges of the
+//     hidden dimension (KS chosen so that the grid fills the chip). Per
+//     k-step every weight fragment (three terms of every 16-expert tile) and
+//     every token fragment goes HBM -> LDS once, by buffer-to-LDS loads
+//     through a ring of 2-4 slots, and its four waves split the work two by
+//     two: expert half x token half, so each fragment read from LDS feeds four
+//     (weights) or 3 x NE (tokens) MFMAs. Each range's partial logits go to the
+//     workspace.
 //   router_topk_kernel: one wave per token sums the KS partials in range
 //     order, adds the bias, and runs the softmax and the top-k (one lane per
 //     expert, DPP reductions).
@@ -26,27 +30,32 @@ namespace {
 constexpr int kRouterTokens = 16;  // tokens per fp32-path workgroup
 constexpr int kRouterWaves = 8;    // fp32 path
 constexpr int kRouterThreads = kRouterWaves * 64;
-constexpr int kLogitWaves = 4;     // bf16 logits kernel: waves split the expert tiles
+constexpr int kLogitWaves = 4;     // bf16 logits kernel: expert half x token half
+constexpr int kLogitTT = 4;        // 16-token tiles per wave: 128 tokens per workgroup
+constexpr int kLogitTokens = 2 * kLogitTT * 16;
 constexpr int kTopkWaves = 4;      // top-k kernel: one wave per token
 
 __host__ __device__ inline int router_epad(int E) { return static_cast<int>(ceil_div(E, 16) * 16); }
 
-// Tiling of the bf16 logits kernel: NTW expert tiles of 16 per wave (4 waves
-// cover E_pad), TMT token tiles of 16 per workgroup, KS ranges of the hidden
-// dimension of `steps` 32-wide k-steps each (the last may be shorter).
+// Expert tiles of 16 per wave (half of the E_pad / 16 tiles, rounded up).
+__host__ __device__ inline int router_ne(int E) { return static_cast<int>(ceil_div(router_epad(E) / 16, 2)); }
+
+// LDS per ring slot: three weight terms of 2 NE expert tiles and 2 TT token
+// tiles, 1 KB each; the ring has as many slots (at most four) as fit in 160 KB.
+__host__ __device__ constexpr int router_slot_bytes(int ne) { return (6 * ne + 2 * kLogitTT) * 1024; }
+__host__ __device__ constexpr int router_ring(int ne) {
+    return 4 * router_slot_bytes(ne) <= 160 * 1024 ? 4 : (3 * router_slot_bytes(ne) <= 160 * 1024 ? 3 : 2);
+}
+
+// KS ranges of the hidden dimension of `steps` 32-wide k-steps each (the last
+// may be shorter): about one workgroup per CU, each range at least 8 k-steps.
 struct RouterPlan {
-    int ntw, tmt, ks, steps;
+    int ks, steps;
 };
-RouterPlan router_plan(int64_t T, int d, int E) {
+RouterPlan router_plan(int64_t T, int d, int /*E*/) {
     RouterPlan p;
-    const int nt = router_epad(E) / 16;
-    p.ntw = static_cast<int>(ceil_div(nt, kLogitWaves));
-    p.tmt = (p.ntw == 2 || p.ntw == 3) ? 8 : 4;  // VGPRs: accumulators + the fragment sets
-    const int64_t tiles = ceil_div(T, 16 * p.tmt);
+    const int64_t tiles = ceil_div(T, kLogitTokens);
     const int nsteps = static_cast<int>(ceil_div(d, 32));
-    // about one workgroup per CU, each range at least 8 k-steps long (a sweep
-    // of 1, 2, 4, 8 ranges and 32, 64, 128-token tiles at the four bf16
-    // workload shapes found this the fastest or within 3 % of it)
     int ks = static_cast<int>(ceil_div(256, tiles > 0 ? tiles : 1));
     const int ks_max = nsteps / 8 > 1 ? nsteps / 8 : 1;
     ks = ks < 1 ? 1 : (ks > ks_max ? ks_max : ks);
@@ -90,103 +99,161 @@ __global__ void split_wgate_kernel(const float* __restrict__ w, int E, int E_pad
     }
 }
 
-// Partial logits of 16 * TMT tokens over k-steps [s0, s1) of the hidden
-// dimension (range blockIdx.y), all experts. Wave w owns expert tiles
-// w, w + 4, ... (NTW of them) and computes D = W x^T on the matrix cores
-// (experts as rows, tokens as columns), so a lane ends with four consecutive
-// experts of one token and stores them as one 16-byte vector. Each k-step
-// loads the wave's weight fragments (three bf16 terms) and the token
-// fragments, the next step's while this step's MFMAs run; the terms are
-// accumulated lo, mid, hi. NBUF fragment sets rotate, so the loads of the
-// next NBUF - 1 steps are in flight while a step's MFMAs run (two sets
-// measured as fast as three, four or six). Loads past the
-// hidden dimension, the range or the expert tiles are out of range and
-// return zeros (zero products add nothing).
+// Partial logits of 128 tokens over k-steps [s0, s1) of the hidden dimension
+// (range blockIdx.y), all experts. Wave w takes expert tiles (w % 2) NE ..
+// + NE - 1 and token tiles (w / 2) TT .. + TT - 1 and computes D = W x^T on
+// the matrix cores (experts as rows, tokens as columns), so a lane ends with
+// four consecutive experts of one token and stores them as one 16-byte
+// vector. Ring slot layout: weight fragment (term p, tile n) at
+// (p * 2 NE + n) KB, token tile t at (6 NE + t) KB; the weight fragments of a
+// k-step are dealt to the waves round-robin, the token tiles two per wave.
+// Fragments are read from LDS one k-step ahead: while k-step t's MFMAs run on
+// registers, k-step t + 1's fragments come in. Before that, a wait for
+// k-step t + 1's DMAs and a barrier show every wave's part of it landed and
+// every wave done reading slot t % ST, which then takes k-step t + ST. Loads
+// past the hidden dimension, the range, the tokens or the expert tiles are
+// out of range and fill zeros (zero products add nothing; chunks past d are
+// never read from the next token's row, where 0 * inf would be NaN).
 // 16x16x32 operands: lane l holds row (A) / column (B) l % 16 at k = 8 (l / 16) + 0..7;
 // result element i of lane l sits at row 4 (l / 16) + i, column l % 16.
-template <int TMT, int NTW, int NBUF>
+template <int NE>
 __global__ void __launch_bounds__(kLogitWaves * 64)
 router_logits_kernel(const uint16_t* __restrict__ x, int64_t T, int d, const uint16_t* __restrict__ wpk, int E_pad,
                      int steps, float* __restrict__ part) {
+    constexpr int TT = kLogitTT, ST = router_ring(NE), SLOT = router_slot_bytes(NE);
+    constexpr int NW = 6 * NE;                            // weight fragments per k-step
+    constexpr int QW = (NW + kLogitWaves - 1) / kLogitWaves;  // weight DMAs of waves 0 .. NW % 4 - 1
+    constexpr int DMIN = NW / kLogitWaves + 2;            // DMAs every wave issues per k-step (at least)
+    constexpr int NF = TT + 3 * NE;                       // fragments a wave reads per k-step
+    static_assert(2 * TT == 2 * kLogitWaves, "two token tiles per wave");
+    static_assert(3 * DMIN < 64, "vmcnt range");
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[ST * SLOT];
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+    const int eh = wave & 1, th = wave >> 1;
     const int quad = lane >> 4, r = lane & 15;
     const int nt = E_pad / 16;
     const int nsteps = static_cast<int>(ceil_div(d, 32));
     const int s0 = static_cast<int>(blockIdx.y) * steps;
     const int s1 = s0 + steps < nsteps ? s0 + steps : nsteps;
-    const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * (16 * TMT);
-    constexpr int kOob = 0x7fffffff;
-    const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(x), 0, static_cast<int>(T * d * 2), 0x00020000);
-    const int64_t term = static_cast<int64_t>(nt) * nsteps * 512;  // elements per weight term
-    const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(wpk), 0, static_cast<int>(3 * term * 2), 0x00020000);
-    int xoff[TMT];
+    const int nk = s1 - s0;
+    const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * kLogitTokens;
+    const i32x4_t rsx = buf_rsrc(x, static_cast<int>(T * d * 2));
+    const i32x4_t rsw = buf_rsrc(wpk, static_cast<int>(3 * static_cast<int64_t>(nt) * nsteps * 1024));
+    const uint32_t lds0 = lds_address(lds);
+    // Byte offsets at k-step 0 (weight fragments: + 1 KB per k-step; token
+    // chunks: + 64 B) and LDS offsets of this wave's DMAs; -1: out of range.
+    int wvo[QW], xvo[2];
+    const bool last_w = wave + kLogitWaves * (QW - 1) < NW;  // this wave issues QW weight DMAs (else QW - 1)
 #pragma unroll
-    for (int tt = 0; tt < TMT; ++tt) {
-        int64_t tok = tok0 + tt * 16 + r;
-        if (tok >= T) tok = T - 1;  // computed but never stored
-        xoff[tt] = static_cast<int>(tok * d * 2);
+    for (int q = 0; q < QW; ++q) {
+        const int i = wave + kLogitWaves * q;
+        const int pt = i / (2 * NE), n = i % (2 * NE);
+        wvo[q] = (i < NW && n < nt) ? ((pt * nt + n) * nsteps + s0) * 1024 + lane * 16 : -1;
     }
-    f32x4_t acc[NTW][TMT];
 #pragma unroll
-    for (int j = 0; j < NTW; ++j)
+    for (int q = 0; q < 2; ++q) {
+        const int64_t tok = tok0 + (wave + kLogitWaves * q) * 16 + r;
+        xvo[q] = tok < T ? static_cast<int>((tok * d + s0 * 32 + quad * 8) * 2) : -1;
+    }
+    const int kq = s0 * 32 + quad * 8;  // this lane's k at k-step 0 of the range
+    auto issue = [&](int t) {
+        const uint32_t slot = lds0 + static_cast<uint32_t>((t % ST) * SLOT);
 #pragma unroll
-        for (int tt = 0; tt < TMT; ++tt) acc[j][tt] = f32x4_t{};
-    auto fetch = [&](int s, bf16x8_t (&a)[TMT], bf16x8_t (&b)[NTW][3]) {
-        const int kk = s * 32 + quad * 8;
-        // d % 8 == 0: an 8-chunk is all in or all out; chunks past d would read
-        // the next token's row (zero weights there, but 0 * inf is NaN)
-        const int oob = (s < s1 && kk < d) ? 0 : kOob;
+        for (int q = 0; q < QW; ++q) {
+            if (q == QW - 1 && !last_w) break;  // wave-uniform
+            const int vo = wvo[q] >= 0 ? wvo[q] + t * 1024 : kOutOfRange;
+            dma16(rsw, vo, slot + static_cast<uint32_t>(wave + kLogitWaves * q) * 1024u);
+        }
+        const bool kin = kq + t * 32 < d;
 #pragma unroll
-        for (int tt = 0; tt < TMT; ++tt)
-            a[tt] = __builtin_bit_cast(bf16x8_t,
-                                       __builtin_amdgcn_raw_buffer_load_b128(rsx, (xoff[tt] + kk * 2) | oob, 0, 0));
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) {
-            const int n = wave + kLogitWaves * j;
-            const int noob = n < nt ? oob : kOob;
-            const int off = static_cast<int>(((static_cast<int64_t>(n) * nsteps + s) * 64 + lane) * 16);
-#pragma unroll
-            for (int p = 0; p < 3; ++p)
-                b[j][p] = __builtin_bit_cast(
-                    bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rsw, (static_cast<int>(p * term * 2) + off) | noob,
-                                                                     0, 0));
+        for (int q = 0; q < 2; ++q) {
+            const int vo = (xvo[q] >= 0 && kin) ? xvo[q] + t * 64 : kOutOfRange;
+            dma16(rsx, vo, slot + static_cast<uint32_t>(NW + wave + kLogitWaves * q) * 1024u);
         }
     };
-    auto mfma3 = [&](const bf16x8_t (&a)[TMT], const bf16x8_t (&b)[NTW][3]) {
+    // wait until at most `later` k-steps of this wave's DMAs issued after the awaited one fly
+    auto wait_later = [&](int later) {
+        if (later <= 0) wait_vm_lgkm0<0>();
+        else if (later == 1) wait_vm_lgkm0<DMIN>();
+        else if (later == 2) wait_vm_lgkm0<2 * DMIN>();
+        else wait_vm_lgkm0<3 * DMIN>();
+    };
+    auto read_frags = [&](int t, bf16x8_t (&f)[NF]) {
+        const uint8_t* base = lds + (t % ST) * SLOT + lane * 16;
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
+        for (int i = 0; i < TT; ++i) f[i] = *reinterpret_cast<const bf16x8_t*>(base + (NW + th * TT + i) * 1024);
 #pragma unroll
-            for (int tt = 0; tt < TMT; ++tt) {
-                acc[j][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j][2], a[tt], acc[j][tt], 0, 0, 0);  // lo
-                acc[j][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j][1], a[tt], acc[j][tt], 0, 0, 0);  // mid
-                acc[j][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j][0], a[tt], acc[j][tt], 0, 0, 0);  // hi
+        for (int j = 0; j < NE; ++j)
+#pragma unroll
+            for (int pt = 0; pt < 3; ++pt)
+                f[TT + 3 * j + pt] = *reinterpret_cast<const bf16x8_t*>(base + (pt * 2 * NE + eh * NE + j) * 1024);
+    };
+    auto lgkm_wait0 = [] { __builtin_amdgcn_s_waitcnt(0xc07f); };  // lgkmcnt(0), vmcnt and expcnt free
+    f32x4_t acc[NE][TT];
+#pragma unroll
+    for (int j = 0; j < NE; ++j)
+#pragma unroll
+        for (int i = 0; i < TT; ++i) acc[j][i] = f32x4_t{};
+    auto mma = [&](const bf16x8_t (&f)[NF]) {
+#pragma unroll
+        for (int j = 0; j < NE; ++j)
+#pragma unroll
+            for (int i = 0; i < TT; ++i) {
+                acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[TT + 3 * j + 2], f[i], acc[j][i], 0, 0, 0);  // lo
+                acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[TT + 3 * j + 1], f[i], acc[j][i], 0, 0, 0);  // mid
+                acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[TT + 3 * j + 0], f[i], acc[j][i], 0, 0, 0);  // hi
             }
     };
-    bf16x8_t a[NBUF][TMT], b[NBUF][NTW][3];
+    // k-step t (t + 1 < nk) from registers `cur`; k-step t + 1's fragments into
+    // `nxt`. The wait also completes `cur`'s reads (issued one step earlier),
+    // so the MFMAs need no wait on the reads issued here.
+    auto step = [&](int t, const bf16x8_t (&cur)[NF], bf16x8_t (&nxt)[NF]) {
+        const int rest = nk - 2 - t;
+        wait_later(rest < ST - 2 ? rest : ST - 2);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");  // no LDS read moves above the barrier
+        if (t + ST < nk) issue(t + ST);
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(t + 1, nxt);
+        mma(cur);
+        // one LDS read after every three MFMAs, the rest of the MFMAs after them
 #pragma unroll
-    for (int u = 0; u < NBUF - 1; ++u) fetch(s0 + u, a[u], b[u]);
-    for (int s = s0; s < s1; s += NBUF) {
-#pragma unroll
-        for (int u = 0; u < NBUF; ++u) {
-            __builtin_amdgcn_sched_barrier(0);
-            fetch(s + u + NBUF - 1, a[(u + NBUF - 1) % NBUF], b[(u + NBUF - 1) % NBUF]);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma3(a[u], b[u]);
+        for (int q = 0; q < NF; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    const int pro = nk < ST ? nk : ST;
+    for (int t = 0; t < pro; ++t) issue(t);
+    wait_later(pro - 1);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    bf16x8_t fa[NF], fb[NF];
+    read_frags(0, fa);
+    int t = 0;
+    for (; t + 2 < nk; t += 2) {
+        step(t, fa, fb);
+        step(t + 1, fb, fa);
+    }
+    if (t + 1 < nk) {  // two k-steps left
+        step(t, fa, fb);
+        lgkm_wait0();
+        mma(fb);
+    } else {
+        lgkm_wait0();
+        mma(fa);
     }
     float* out = part + static_cast<int64_t>(blockIdx.y) * T * E_pad;
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) {
-        const int n = wave + kLogitWaves * j;
+    for (int j = 0; j < NE; ++j) {
+        const int n = eh * NE + j;
         if (n >= nt) continue;
 #pragma unroll
-        for (int tt = 0; tt < TMT; ++tt) {
-            const int64_t tok = tok0 + tt * 16 + r;
-            if (tok < T)
-                *reinterpret_cast<f32x4_t*>(out + tok * E_pad + n * 16 + quad * 4) = acc[j][tt];
+        for (int i = 0; i < TT; ++i) {
+            const int64_t tok = tok0 + (th * TT + i) * 16 + r;
+            if (tok < T) *reinterpret_cast<f32x4_t*>(out + tok * E_pad + n * 16 + quad * 4) = acc[j][i];
         }
     }
 }
@@ -318,18 +385,25 @@ hipError_t launch_router_bf16(const uint16_t* x, int64_t T, int d, const uint16_
                               int32_t* topk_idx, float* topk_w, hipStream_t stream) {
     const int E_pad = router_epad(E);
     const RouterPlan p = router_plan(T, d, E);
-    const dim3 grid(static_cast<unsigned>(ceil_div(T, 16 * p.tmt)), static_cast<unsigned>(p.ks));
+    const dim3 grid(static_cast<unsigned>(ceil_div(T, kLogitTokens)), static_cast<unsigned>(p.ks));
     const dim3 block(kLogitWaves * 64);
-    if (p.ntw == 1 && p.tmt == 4)
-        hipLaunchKernelGGL((router_logits_kernel<4, 1, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
-    else if (p.ntw == 2 && p.tmt == 8)
-        hipLaunchKernelGGL((router_logits_kernel<8, 2, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
-    else if (p.ntw == 3 && p.tmt == 8)
-        hipLaunchKernelGGL((router_logits_kernel<8, 3, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
-    else if (p.ntw == 4 && p.tmt == 4)
-        hipLaunchKernelGGL((router_logits_kernel<4, 4, 2>), grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part);
-    else
-        return hipErrorInvalidValue;
+    switch (router_ne(E)) {
+#define SMOES_ROUTER_NE(NE)                                                                                     \
+    case NE:                                                                                                    \
+        hipLaunchKernelGGL(router_logits_kernel<NE>, grid, block, 0, stream, x, T, d, wsplit, E_pad, p.steps, part); \
+        break;
+        SMOES_ROUTER_NE(1)
+        SMOES_ROUTER_NE(2)
+        SMOES_ROUTER_NE(3)
+        SMOES_ROUTER_NE(4)
+        SMOES_ROUTER_NE(5)
+        SMOES_ROUTER_NE(6)
+        SMOES_ROUTER_NE(7)
+        SMOES_ROUTER_NE(8)
+#undef SMOES_ROUTER_NE
+        default:
+            return hipErrorInvalidValue;
+    }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const dim3 tgrid(static_cast<unsigned>(ceil_div(T, kTopkWaves)));

@@ -40,9 +40,11 @@ ROUTE_CASES = [
     (257, 256, 64, 6, W.BF16, False),
     (64, 64, 160, 6, W.BF16, True),
     (33, 512, 256, 16, W.BF16, False),  # maximum E and k
-    (300, 1032, 100, 8, W.BF16, True),  # two expert tiles per wave, the last wave's second one empty;
+    (300, 1032, 100, 8, W.BF16, True),  # 7 expert tiles: 4 per expert half, the last one empty;
                                         # 33 k-steps in 4 ranges (the last one shorter), partial last step
-    (2000, 2048, 128, 8, W.BF16, False),  # 128-token tiles split over 4 ranges of the hidden dimension
+    (2000, 2048, 128, 8, W.BF16, False),  # 16 tiles of 128 tokens, 8 ranges of the hidden dimension
+    (200, 512, 224, 8, W.BF16, True),   # 7 expert tiles per half: three ring slots
+    (129, 320, 192, 4, W.BF16, False),  # 6 expert tiles per half, one token past a 128-token tile
     (5000, 512, 64, 6, W.BF16, False),  # ragged last token tile, 2 ranges
     (31, 2048, 8, 2, W.BF16, False),
     (1, 8, 1, 1, W.BF16, False),        # degenerate: one token, one expert
