@@ -45,14 +45,34 @@ def rel_err(a, b):
     return np.linalg.norm((a - b).ravel()) / (den if den > 0 else 1.0)
 
 
+def gate_rtol(x, w_gate, bias=None):
+    """Per-token relative tolerance of the gate values g = softmax(z). The
+    logits are fp32-faithful: |z_gpu - z| <= 4e-7 sum_d |x_d w_ed| (+ |b_e|).
+    The softmax turns an absolute logit error into a relative gate error,
+    |dg_e / g_e| <= |dz_e| + |d logsumexp| <= 2 max_e |dz_e|, so the bar is
+    8e-7 times the token's largest such sum, and never below 1e-5."""
+    scale = np.abs(O.widen(x)) @ np.abs(np.asarray(w_gate, dtype=np.float64)).T
+    if bias is not None:
+        scale = scale + np.abs(np.asarray(bias, dtype=np.float64))
+    return np.maximum(1e-5, 8e-7 * scale.max(axis=1))[:, None]
+
+
 def check_topk(idx_gpu, idx_ref, z_ref, k, gap_tol=1e-4):
-    """Bit-exact top-k wherever the oracle's k-th vs (k+1)-th logit gap exceeds
-    gap_tol; elsewhere every chosen expert must be a valid choice (its logit
+    """Top-k against the oracle. Wherever the oracle's k-th vs (k+1)-th logit
+    gap exceeds gap_tol the chosen set is bit-exact, and the order is the
+    oracle's except among chosen experts whose logits lie within gap_tol of
+    each other (the s-th chosen logit equals the oracle's s-th within gap_tol):
+    the logits are fp32-faithful, so keys closer than that may come in either
+    order. Elsewhere every chosen expert must be a valid choice (its logit
     within gap_tol of the k-th largest). Returns the mask of clear tokens."""
     gap = O.topk_gap(z_ref, k)
     clear = gap > gap_tol
-    assert np.array_equal(idx_gpu[clear], idx_ref[clear]), \
-        f"top-k mismatch on {np.sum(np.any(idx_gpu[clear] != idx_ref[clear], axis=1))} clear tokens"
+    same_set = np.all(np.sort(idx_gpu[clear], axis=1) == np.sort(idx_ref[clear], axis=1), axis=1)
+    assert same_set.all(), f"top-k set mismatch on {np.sum(~same_set)} clear tokens"
+    zg = np.take_along_axis(z_ref[clear], idx_gpu[clear].astype(np.int64), axis=1)
+    zr = np.take_along_axis(z_ref[clear], idx_ref[clear].astype(np.int64), axis=1)
+    assert np.all(np.abs(zg - zr) <= gap_tol), "top-k order differs beyond near-equal logits"
+    assert np.all(zg[:, :-1] >= zg[:, 1:] - gap_tol), "top-k not in descending logit order"
     if (~clear).any():
         zs = -np.sort(-z_ref[~clear], axis=1)
         kth = zs[:, k - 1]
