@@ -479,17 +479,17 @@ typedef struct smoes_layer_grads {
     float* dbias;    /* [E] float32 logit bias gradient, or NULL                 */
     float* dz;       /* [T, E] float32 total logit gradient (with dlogits_aux)   */
     float* dw;       /* [T, k] float32 combine-weight gradient, or NULL          */
-    void* dw13;      /* [E, 2 inter, d] bf16 (gate rows then up rows, as w13)    */
-    void* dw2;       /* [E, d, inter] bf16                                       */
-    void* dws13;     /* [2 shared_inter, d] bf16 (needed when shared_inter > 0)  */
-    void* dws2;      /* [d, shared_inter] bf16                                   */
+    void* dw13;      /* [E, 2 inter, d] act_dtype (gate rows then up rows, as w13) */
+    void* dw2;       /* [E, d, inter] act_dtype                                  */
+    void* dws13;     /* [2 shared_inter, d] act_dtype (when shared_inter > 0)    */
+    void* dws2;      /* [d, shared_inter] act_dtype                              */
 } smoes_layer_grads;
 
 size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
 
 /*
  * Gradients of a loss L through the layer output, given dout = dL/d out
- * ([T, d] bf16), after smoes_moe_forward ran with the same desc, io and
+ * ([T, d] act_dtype), after smoes_moe_forward ran with the same desc, io and
  * forward workspace (whose expert buffers, H and Y, and work tables must be
  * intact). The top-k choice carries no gradient; the gradient reaches the
  * router through the combine weights (the gate values at the chosen experts,
@@ -499,24 +499,30 @@ size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
  * constants. The experts' gate and up pre-activations are read from the
  * forward workspace when desc->save_preact is 1 (the forward kept them),
  * else recomputed.
- * Reads from io: x, w13 and ws13 (packed), w_gate (float32 row-major),
- * probs, topk_idx, topk_w, and expert_offsets / perm_token / perm_inv (or
- * the forward workspace's copies when those are NULL).
- * w13t, w2t, ws13t, ws2t: the transposed packed weights (SMOES_W13T, ...).
- * Implemented for bf16 layers with packed weights (SMOES_ERR_ARG otherwise).
- * SMOES_ERR_SHAPE when 4 T k inter or 4 T shared_inter exceeds INT32_MAX
- * bytes; SMOES_ERR_WORKSPACE when either workspace is NULL or smaller than
- * smoes_workspace_bytes / smoes_backward_workspace_bytes; SMOES_ERR_ARG for
- * a NULL pointer that is needed. Differentiates the layer output of Sec. 3.1
- * (softmax router, top-k combine, SwiGLU experts plus the shared experts).
- * bf16 operands with float32 accumulation; the expert weight gradients are
- * bf16, dx, dw_gate and the logit gradient float32. Sums run in a fixed
- * order: results are reproducible. Asynchronous on `stream`; nothing is
- * allocated. With io->streams set, the router backward, dW_gate / dbias and
- * the shared experts' gradients run on io->streams->side[1], forked from
- * `stream` at the start of the call and joined back before the input
- * gradient (events[0] and events[3]); the results are the same bits as on
- * one stream. NULL runs every step on `stream`.
+ * Reads from io: x, w13 and ws13 (packed when desc->weights_packed),
+ * w2 and ws2 (row-major; fp32 layers and bf16 layers with row-major
+ * weights), w_gate (float32 row-major), probs, topk_idx, topk_w, and
+ * expert_offsets / perm_token / perm_inv (or the forward workspace's copies
+ * when those are NULL).
+ * w13t, w2t, ws13t, ws2t: the transposed packed weights (SMOES_W13T, ...),
+ * read for bf16 layers with packed weights only (may be NULL otherwise).
+ * Two paths: bf16 layers with packed weights run matrix-core GEMMs with bf16
+ * operands and bf16 intermediates; fp32 layers and bf16 layers with
+ * row-major weights run float32 FMA tiles with float32 intermediates, every
+ * step on `stream` (io->streams is not used there). The expert weight
+ * gradients are in act_dtype; dx, dw_gate and the logit gradient float32.
+ * SMOES_ERR_SHAPE (packed path) when 4 T k inter or 4 T shared_inter exceeds
+ * INT32_MAX bytes; SMOES_ERR_WORKSPACE when either workspace is NULL or
+ * smaller than smoes_workspace_bytes / smoes_backward_workspace_bytes;
+ * SMOES_ERR_ARG for a NULL pointer that is needed. Differentiates the layer
+ * output of Sec. 3.1 (softmax router, top-k combine, SwiGLU experts plus the
+ * shared experts). Sums run in a fixed order: results are reproducible.
+ * Asynchronous on `stream`; nothing is allocated. Packed path with
+ * io->streams set: the router backward, dW_gate / dbias and the shared
+ * experts' gradients run on io->streams->side[1], forked from `stream` at
+ * the start of the call and joined back before the input gradient
+ * (events[0] and events[3]); the results are the same bits as on one
+ * stream. NULL runs every step on `stream`.
  */
 int smoes_moe_backward(const smoes_layer* desc, const smoes_layer_io* io, const void* w13t, const void* w2t,
                        const void* ws13t, const void* ws2t, const void* dout, const float* dlogits_aux,

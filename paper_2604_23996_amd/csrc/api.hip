@@ -526,6 +526,9 @@ int smoes_check_inputs(const smoes_layer* L, const smoes_layer_io* io, int32_t* 
 // ------------------------------------------------------------------ layer backward
 
 namespace {
+// fp32 layers and bf16 layers with row-major weights take the float32 FMA backward
+bool generic_bwd(const smoes_layer* L) { return L->act_dtype != SMOES_BF16 || !L->weights_packed; }
+
 struct BwdWs {
     void* ab_r;
     void* ab_s;
@@ -535,22 +538,27 @@ struct BwdWs {
     void* dx_s;
     float* wrow;
     void* wh_r;
+    void* wh_s;  // float32 H of the shared experts (float32 backward only)
     int32_t* work4;
     void* router;
 };
 size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     Carver c(base);
     const int64_t T = L->T, R = L->T * L->k;
+    const bool gen = generic_bwd(L);
+    // intermediates: bf16 on the packed matrix-core path, float32 on the FMA path
+    const size_t es = gen ? sizeof(float) : sizeof(uint16_t);
     BwdWs w;
     // the pre-activations are recomputed here unless the forward kept them
-    w.ab_r = c.take(L->save_preact ? 0 : sizeof(uint16_t) * R * 2 * L->inter);
-    w.ab_s = c.take(L->save_preact ? 0 : sizeof(uint16_t) * T * 2 * L->shared_inter);
-    w.dab_r = c.take(sizeof(uint16_t) * R * 2 * L->inter);
-    w.dab_s = c.take(sizeof(uint16_t) * T * 2 * L->shared_inter);
-    w.dx_r = c.take(sizeof(uint16_t) * R * L->d);
-    w.dx_s = c.take(sizeof(uint16_t) * T * L->d);
+    w.ab_r = c.take(L->save_preact ? 0 : es * R * 2 * L->inter);
+    w.ab_s = c.take(L->save_preact ? 0 : es * T * 2 * L->shared_inter);
+    w.dab_r = c.take(es * R * 2 * L->inter);
+    w.dab_s = c.take(es * T * 2 * L->shared_inter);
+    w.dx_r = c.take(es * R * L->d);
+    w.dx_s = c.take(es * T * L->d);
     w.wrow = static_cast<float*>(c.take(sizeof(float) * R));
-    w.wh_r = c.take(sizeof(uint16_t) * R * L->inter);
+    w.wh_r = c.take(es * R * L->inter);
+    w.wh_s = c.take(gen ? es * T * L->shared_inter : 0);
     w.work4 = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 2)));
     w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E));
     if (out != nullptr) *out = w;
@@ -570,20 +578,21 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     int st = check_layer(L);
     if (st != SMOES_OK) return st;
     if (io == nullptr || G == nullptr) return SMOES_ERR_ARG;
-    if (L->act_dtype != SMOES_BF16 || !L->weights_packed) return SMOES_ERR_ARG;
-    // dX = [dA dB] W13 reads its A operand (2 inter columns per row) through a
-    // buffer descriptor with 32-bit byte offsets
-    if (2 * L->T * L->k * 2 * static_cast<int64_t>(L->inter) > INT32_MAX ||
-        2 * L->T * 2 * static_cast<int64_t>(L->shared_inter) > INT32_MAX)
+    const bool gen = generic_bwd(L);
+    // dX = [dA dB] W13 of the packed path reads its A operand (2 inter columns
+    // per row) through a buffer descriptor with 32-bit byte offsets
+    if (!gen && (2 * L->T * L->k * 2 * static_cast<int64_t>(L->inter) > INT32_MAX ||
+                 2 * L->T * 2 * static_cast<int64_t>(L->shared_inter) > INT32_MAX))
         return SMOES_ERR_SHAPE;
     if (L->T == 0) return SMOES_OK;
     const bool sh = L->shared_inter > 0;
     if (io->x == nullptr || io->w13 == nullptr || io->w_gate == nullptr || io->probs == nullptr ||
-        io->topk_idx == nullptr || io->topk_w == nullptr || w13t == nullptr || w2t == nullptr || dout == nullptr ||
-        G->dx == nullptr || G->dw_gate == nullptr || G->dz == nullptr || G->dw13 == nullptr || G->dw2 == nullptr)
+        io->topk_idx == nullptr || io->topk_w == nullptr || dout == nullptr || G->dx == nullptr ||
+        G->dw_gate == nullptr || G->dz == nullptr || G->dw13 == nullptr || G->dw2 == nullptr)
         return SMOES_ERR_ARG;
-    if (sh && (io->ws13 == nullptr || ws13t == nullptr || ws2t == nullptr || G->dws13 == nullptr ||
-               G->dws2 == nullptr))
+    if (gen ? io->w2 == nullptr : (w13t == nullptr || w2t == nullptr)) return SMOES_ERR_ARG;
+    if (sh && (io->ws13 == nullptr || G->dws13 == nullptr || G->dws2 == nullptr ||
+               (gen ? io->ws2 == nullptr : (ws13t == nullptr || ws2t == nullptr))))
         return SMOES_ERR_ARG;
     if (fwd_workspace == nullptr || fwd_workspace_bytes < smoes_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
     if (workspace == nullptr || workspace_bytes < smoes_backward_workspace_bytes(L)) return SMOES_ERR_WORKSPACE;
@@ -610,7 +619,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     a.inter = L->inter;
     a.shared_inter = L->shared_inter;
     a.act_dtype = L->act_dtype;
-    a.packed = 1;
+    a.packed = gen ? 0 : 1;
     a.x = io->x;
     a.w13 = io->w13;
     a.w2 = io->w2;
@@ -623,6 +632,40 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     a.out = nullptr;
     a.ab_r = a.ab_s = nullptr;
     const ExpertFwdBuffers fb = experts_fwd_buffers(a, fw.experts);
+    hipError_t err;
+#define SMOES_BTRY(expr)                                        \
+    do {                                                        \
+        if ((err = (expr)) != hipSuccess) return SMOES_ERR_HIP; \
+    } while (0)
+    const int bf16 = L->act_dtype == SMOES_BF16 ? 1 : 0;
+    if (gen) {
+        // float32 FMA path, every step on s: router backward and dW_gate, then
+        // the experts (routed and shared in each launch), then the input gradient
+        GenericBwdPtrs gp;
+        gp.dout = dout;
+        gp.ab_r = static_cast<float*>(bw.ab_r);
+        gp.ab_s = static_cast<float*>(bw.ab_s);
+        gp.dab_r = static_cast<float*>(bw.dab_r);
+        gp.dab_s = static_cast<float*>(bw.dab_s);
+        gp.wh_r = static_cast<float*>(bw.wh_r);
+        gp.wh_s = static_cast<float*>(bw.wh_s);
+        gp.dx_r = static_cast<float*>(bw.dx_r);
+        gp.dx_s = static_cast<float*>(bw.dx_s);
+        gp.wrow = bw.wrow;
+        gp.work = bw.work4;
+        gp.dw13 = G->dw13;
+        gp.dw2 = G->dw2;
+        gp.dws13 = G->dws13;
+        gp.dws2 = G->dws2;
+        SMOES_BTRY(launch_router_bwd(dout, fb.y_r, bf16, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux,
+                                     T, L->d, L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, s));
+        SMOES_BTRY(launch_dwgate(G->dz, io->x, bf16, T, L->d, L->E, G->dw_gate, G->dbias, bw.router, s));
+        SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
+        for (int step = 0; step < 5; ++step) SMOES_BTRY(launch_generic_bwd(step, a, gp, s));
+        SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, 0, perm_inv, G->dz, io->w_gate, T, L->d, L->E,
+                                    L->k, G->dx, s));
+        return SMOES_OK;
+    }
     BwdGemmPtrs bp;
     bp.dout = dout;
     bp.w2t = w2t;
@@ -638,11 +681,6 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     bp.wrow = bw.wrow;
     bp.wh_r = bw.wh_r;
     bp.work4 = bw.work4;
-    hipError_t err;
-#define SMOES_BTRY(expr)                                        \
-    do {                                                        \
-        if ((err = (expr)) != hipSuccess) return SMOES_ERR_HIP; \
-    } while (0)
     // Caller's stream s: combine weights, the routed experts' dgrad GEMMs
     // (pre-activation recompute unless kept, dH with the SwiGLU backward,
     // dX) and weight gradients, then the input gradient. With caller-owned
@@ -664,9 +702,9 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     const int I = L->inter, SI = L->shared_inter, d = L->d;
     const int Ti = static_cast<int>(T), R = static_cast<int>(T * L->k);
     // side chain: router backward (dz, dw), dW_gate and dbias, shared experts
-    SMOES_BTRY(launch_router_bwd(dout, fb.y_r, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T, L->d,
-                                 L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, c));
-    SMOES_BTRY(launch_dwgate(G->dz, io->x, T, d, L->E, G->dw_gate, G->dbias, bw.router, c));
+    SMOES_BTRY(launch_router_bwd(dout, fb.y_r, 1, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T,
+                                 L->d, L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, c));
+    SMOES_BTRY(launch_dwgate(G->dz, io->x, 1, T, d, L->E, G->dw_gate, G->dbias, bw.router, c));
     if (sh) {
         for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode)
             SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 2, c));
@@ -684,7 +722,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     SMOES_BTRY(launch_wgrad(T, L->E, 2 * I, d, offsets, bw.dab_r, 2 * I, R, nullptr, io->x, d, Ti, perm_token, R,
                             G->dw13, s));
     if (sides != nullptr) SMOES_BTRY(hipStreamWaitEvent(s, e_join, 0));
-    SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
+    SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, 1, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
                                 G->dx, s));
 #undef SMOES_BTRY
     return SMOES_OK;

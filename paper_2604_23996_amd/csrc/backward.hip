@@ -28,8 +28,9 @@ __global__ void row_weights_kernel(const int32_t* __restrict__ inv, const float*
         wrow[inv[i]] = topk_w[i];
 }
 
+template <bool BF16>
 __global__ void __launch_bounds__(256)
-router_bwd_kernel(const uint16_t* __restrict__ dout, const uint16_t* __restrict__ y_r, const int32_t* __restrict__ inv,
+router_bwd_kernel(const void* __restrict__ dout, const void* __restrict__ y_r, const int32_t* __restrict__ inv,
                   const float* __restrict__ probs, const int32_t* __restrict__ topk_idx,
                   const float* __restrict__ topk_w, const float* __restrict__ aux, int64_t T, int d, int E, int k,
                   int renorm, float* __restrict__ dw, float* __restrict__ dz) {
@@ -48,12 +49,12 @@ router_bwd_kernel(const uint16_t* __restrict__ dout, const uint16_t* __restrict_
     }
     for (int c = lane * 8; c < d; c += kWave * 8) {
         float a[8];
-        load8<true>(dout, j * d + c, a);
+        load8<BF16>(dout, j * d + c, a);
 #pragma unroll
         for (int s = 0; s < SMOES_K_MAX_DEV; ++s) {
             if (s >= k) break;
             float y[8];
-            load8<true>(y_r, rows[s] * d + c, y);
+            load8<BF16>(y_r, rows[s] * d + c, y);
 #pragma unroll
             for (int e = 0; e < 8; ++e) dws[s] = fmaf(a[e], y[e], dws[s]);
         }
@@ -84,10 +85,11 @@ router_bwd_kernel(const uint16_t* __restrict__ dout, const uint16_t* __restrict_
         for (int s = 0; s < k; ++s) dw[j * k + s] = dws[s];
 }
 
-// Each thread: 4 adjacent columns of kDxTok tokens (8-byte loads of the bf16
-// row gradients, 16 bytes of W_gate per expert).
+// Each thread: 4 adjacent columns of kDxTok tokens (8-byte loads of bf16 row
+// gradients or 16-byte loads of float32 ones, 16 bytes of W_gate per expert).
+template <bool BF16>
 __global__ void __launch_bounds__(256)
-dx_gather_kernel(const uint16_t* __restrict__ dx_r, const uint16_t* __restrict__ dx_s, const int32_t* __restrict__ inv,
+dx_gather_kernel(const void* __restrict__ dx_r, const void* __restrict__ dx_s, const int32_t* __restrict__ inv,
                  const float* __restrict__ dz, const float* __restrict__ w_gate, int64_t T, int d, int E, int k,
                  float* __restrict__ dx) {
     extern __shared__ float dz_s[];  // [kDxTok][E]
@@ -116,28 +118,38 @@ dx_gather_kernel(const uint16_t* __restrict__ dx_r, const uint16_t* __restrict__
             acc[t][3] = fmaf(z, w.w, acc[t][3]);
         }
     }
-    auto add4 = [](float (&v)[4], uint2 u) {
-        v[0] += __uint_as_float(u.x << 16);
-        v[1] += __uint_as_float(u.x & 0xffff0000u);
-        v[2] += __uint_as_float(u.y << 16);
-        v[3] += __uint_as_float(u.y & 0xffff0000u);
+    // the four columns of row r of a row-gradient matrix, added onto v
+    auto add4 = [&](float (&v)[4], const void* m, int64_t r) {
+        if constexpr (BF16) {
+            const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(m) + r * d + c);
+            v[0] += __uint_as_float(u.x << 16);
+            v[1] += __uint_as_float(u.x & 0xffff0000u);
+            v[2] += __uint_as_float(u.y << 16);
+            v[3] += __uint_as_float(u.y & 0xffff0000u);
+        } else {
+            const float4 u = *reinterpret_cast<const float4*>(static_cast<const float*>(m) + r * d + c);
+            v[0] += u.x;
+            v[1] += u.y;
+            v[2] += u.z;
+            v[3] += u.w;
+        }
     };
 #pragma unroll
     for (int t = 0; t < kDxTok; ++t) {
         if (t >= nt) break;
         const int64_t j = j0 + t;
         float v[4] = {acc[t][0], acc[t][1], acc[t][2], acc[t][3]};
-        for (int s2 = 0; s2 < k; ++s2)
-            add4(v, *reinterpret_cast<const uint2*>(dx_r + static_cast<int64_t>(inv[j * k + s2]) * d + c));
-        if (dx_s != nullptr) add4(v, *reinterpret_cast<const uint2*>(dx_s + j * d + c));
+        for (int s2 = 0; s2 < k; ++s2) add4(v, dx_r, static_cast<int64_t>(inv[j * k + s2]));
+        if (dx_s != nullptr) add4(v, dx_s, j);
         *reinterpret_cast<float4*>(dx + j * d + c) = make_float4(v[0], v[1], v[2], v[3]);
     }
 }
 
 // partial[chunk][e][c] = sum over the chunk's tokens of dz[j][e] x[j][c]; bias
 // partials by the blocks of column tile 0.
+template <bool BF16>
 __global__ void __launch_bounds__(256)
-dwgate_partial_kernel(const float* __restrict__ dz, const uint16_t* __restrict__ x, int64_t T, int d, int E,
+dwgate_partial_kernel(const float* __restrict__ dz, const void* __restrict__ x, int64_t T, int d, int E,
                       float* __restrict__ part, float* __restrict__ bpart) {
     __shared__ float dz_s[kDwChunk][kDwExp];
     const int c = blockIdx.x * 256 + threadIdx.x;
@@ -160,7 +172,8 @@ dwgate_partial_kernel(const float* __restrict__ dz, const uint16_t* __restrict__
 #pragma unroll
     for (int e = 0; e < kDwExp; ++e) acc[e] = 0.0f;
     for (int t = 0; t < nt; ++t) {
-        const float xv = bf16_to_f32(x[(j0 + t) * d + c]);
+        const float xv = BF16 ? bf16_to_f32(static_cast<const uint16_t*>(x)[(j0 + t) * d + c])
+                              : static_cast<const float*>(x)[(j0 + t) * d + c];
 #pragma unroll
         for (int e = 0; e < kDwExp; ++e) acc[e] = fmaf(dz_s[t][e], xv, acc[e]);
     }
@@ -201,28 +214,37 @@ hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int6
     return hipGetLastError();
 }
 
-hipError_t launch_router_bwd(const void* dout, const void* y_r, const int32_t* perm_inv, const float* probs,
-                             const int32_t* topk_idx, const float* topk_w, const float* dlogits_aux, int64_t T, int d,
-                             int E, int k, int renorm, float* dw, float* dz, hipStream_t stream) {
+hipError_t launch_router_bwd(const void* dout, const void* y_r, int bf16, const int32_t* perm_inv,
+                             const float* probs, const int32_t* topk_idx, const float* topk_w,
+                             const float* dlogits_aux, int64_t T, int d, int E, int k, int renorm, float* dw,
+                             float* dz, hipStream_t stream) {
     if (T == 0) return hipSuccess;
-    hipLaunchKernelGGL(router_bwd_kernel, dim3(static_cast<unsigned>(ceil_div(T, 4))), dim3(256), 0, stream,
-                       static_cast<const uint16_t*>(dout), static_cast<const uint16_t*>(y_r), perm_inv, probs,
-                       topk_idx, topk_w, dlogits_aux, T, d, E, k, renorm, dw, dz);
+    const dim3 grid(static_cast<unsigned>(ceil_div(T, 4)));
+    if (bf16)
+        hipLaunchKernelGGL(router_bwd_kernel<true>, grid, dim3(256), 0, stream, dout, y_r, perm_inv, probs, topk_idx,
+                           topk_w, dlogits_aux, T, d, E, k, renorm, dw, dz);
+    else
+        hipLaunchKernelGGL(router_bwd_kernel<false>, grid, dim3(256), 0, stream, dout, y_r, perm_inv, probs, topk_idx,
+                           topk_w, dlogits_aux, T, d, E, k, renorm, dw, dz);
     return hipGetLastError();
 }
 
-hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, const int32_t* perm_inv, const float* dz,
+hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, int bf16, const int32_t* perm_inv, const float* dz,
                             const float* w_gate, int64_t T, int d, int E, int k, float* dx, hipStream_t stream) {
     if (T == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(ceil_div(T, kDxTok)), static_cast<unsigned>(ceil_div(d, 256 * 4)));
-    hipLaunchKernelGGL(dx_gather_kernel, grid, dim3(256), sizeof(float) * kDxTok * E, stream,
-                       static_cast<const uint16_t*>(dx_r), static_cast<const uint16_t*>(dx_s), perm_inv, dz, w_gate,
-                       T, d, E, k, dx);
+    const size_t lds = sizeof(float) * kDxTok * E;
+    if (bf16)
+        hipLaunchKernelGGL(dx_gather_kernel<true>, grid, dim3(256), lds, stream, dx_r, dx_s, perm_inv, dz, w_gate, T, d,
+                           E, k, dx);
+    else
+        hipLaunchKernelGGL(dx_gather_kernel<false>, grid, dim3(256), lds, stream, dx_r, dx_s, perm_inv, dz, w_gate, T,
+                           d, E, k, dx);
     return hipGetLastError();
 }
 
-hipError_t launch_dwgate(const float* dz, const void* x, int64_t T, int d, int E, float* dw_gate, float* dbias,
-                         void* ws, hipStream_t stream) {
+hipError_t launch_dwgate(const float* dz, const void* x, int bf16, int64_t T, int d, int E, float* dw_gate,
+                         float* dbias, void* ws, hipStream_t stream) {
     const int64_t nchunk = ceil_div(T, kDwChunk);
     float* part = static_cast<float*>(ws);
     float* bpart = reinterpret_cast<float*>(static_cast<char*>(ws) + align_up(sizeof(float) * nchunk * E * d, 256));
@@ -230,8 +252,10 @@ hipError_t launch_dwgate(const float* dz, const void* x, int64_t T, int d, int E
     if (nchunk > 0) {
         const dim3 grid(static_cast<unsigned>(ceil_div(d, 256)), static_cast<unsigned>(ceil_div(E, kDwExp)),
                         static_cast<unsigned>(nchunk));
-        hipLaunchKernelGGL(dwgate_partial_kernel, grid, dim3(256), 0, stream, dz, static_cast<const uint16_t*>(x), T,
-                           d, E, part, bpart);
+        if (bf16)
+            hipLaunchKernelGGL(dwgate_partial_kernel<true>, grid, dim3(256), 0, stream, dz, x, T, d, E, part, bpart);
+        else
+            hipLaunchKernelGGL(dwgate_partial_kernel<false>, grid, dim3(256), 0, stream, dz, x, T, d, E, part, bpart);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     const int64_t n = static_cast<int64_t>(E) * d;

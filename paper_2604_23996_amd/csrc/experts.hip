@@ -987,6 +987,229 @@ gemm_f32_kernel(GemmArgs p) {
     }
 }
 
+// ============================================================== f32 FMA backward
+
+// Backward of fp32 layers and of bf16 layers whose weights are row-major: the
+// same contractions as the forward's f32 tiles (64 x 64 outputs per block, 4 x 4
+// per thread, K steps of 16 through LDS), with float32 intermediates. Steps:
+//   GB_AB   [A | B] = X W13^T          rows: routed rows (x gathered) / tokens
+//   GB_DH   dH = w dout W2, then the SwiGLU backward: dA, dB and w H
+//   GB_DX   dX = [dA dB] W13
+//   GB_DW2  dW2[n][c]  = sum over the group's rows of dout[tok][n] (w H)[c]
+//   GB_DW13 dW13[m][n] = sum over the group's rows of [dA dB][m] x[tok][n]
+// Row steps take their tiles from the work table (decode_tile, both parts);
+// weight steps run one block per (output tile, group), group E the shared
+// experts. An expert without rows gets a zero gradient.
+enum { GB_AB = 0, GB_DH = 1, GB_DX = 2, GB_DW2 = 3, GB_DW13 = 4 };
+
+struct GenBwdArgs {
+    int64_t T;
+    int d, E, inter, shared_inter;
+    const int32_t* off;
+    const int32_t* perm_token;
+    const int32_t* work;
+    const void* x;     // [T][d] layer dtype
+    const void* dout;  // [T][d]
+    const void* w13;   // [E][2 inter][d]
+    const void* w2;    // [E][d][inter]
+    const void* ws13;  // [2 shared_inter][d]
+    const void* ws2;   // [d][shared_inter]
+    float* ab_r;       // [R][2 inter]
+    float* ab_s;       // [T][2 shared_inter]
+    float* dab_r;
+    float* dab_s;
+    float* wh_r;       // [R][inter]
+    float* wh_s;       // [T][shared_inter]
+    float* dx_r;       // [R][d]
+    float* dx_s;       // [T][d]
+    const float* wrow; // [R]
+    void* dw13;        // layer dtype, shapes of w13 ...
+    void* dw2;
+    void* dws13;
+    void* dws2;
+};
+
+template <bool BF16>
+__device__ __forceinline__ float ldv(const void* p, int64_t i) {
+    if constexpr (BF16) return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
+    else return static_cast<const float*>(p)[i];
+}
+
+// output column tiles of a row step for a group with n_out inner columns
+__host__ __device__ __forceinline__ int gb_row_tiles(int mode, int n_out, int d) {
+    return static_cast<int>(ceil_div(mode == GB_AB ? 2 * n_out : mode == GB_DH ? n_out : d, FBNB));
+}
+
+template <int MODE, bool BF16>
+__global__ void __launch_bounds__(kThreads)
+gemm_f32_bwd_kernel(GenBwdArgs p) {
+    __shared__ __align__(16) float As[FBK][FBM + 4];
+    __shared__ __align__(16) float Bs[FBK][FBNB + 4];
+    constexpr bool kRows = MODE <= GB_DX;
+    const int tid = threadIdx.x;
+    int g, m0, n0, M, N, K, rows = 0;
+    int64_t row0;
+    if constexpr (kRows) {
+        Tile t;
+        if (!decode_tile(p.work, p.off, p.E, p.T, FBM, gb_row_tiles(MODE, p.inter, p.d),
+                         gb_row_tiles(MODE, p.shared_inter, p.d), 0, t))
+            return;
+        g = t.g;
+        row0 = t.row0;
+        rows = t.rows;
+        m0 = 0;
+        n0 = t.nt * FBNB;
+        const int n_out = g == p.E ? p.shared_inter : p.inter;
+        M = rows;
+        N = MODE == GB_AB ? 2 * n_out : MODE == GB_DH ? n_out : p.d;
+        K = MODE == GB_DX ? 2 * n_out : p.d;
+    } else {
+        g = blockIdx.y;
+        const int n_out = g == p.E ? p.shared_inter : p.inter;
+        M = MODE == GB_DW2 ? p.d : 2 * n_out;
+        N = MODE == GB_DW2 ? n_out : p.d;
+        const int tn = static_cast<int>(ceil_div(N, FBNB));
+        if (static_cast<int>(blockIdx.x) >= static_cast<int>(ceil_div(M, FBM)) * tn) return;
+        m0 = static_cast<int>(blockIdx.x) / tn * FBM;
+        n0 = static_cast<int>(blockIdx.x) % tn * FBNB;
+        row0 = g == p.E ? 0 : p.off[g];
+        K = g == p.E ? static_cast<int>(p.T) : p.off[g + 1] - p.off[g];
+    }
+    const bool shared = g == p.E;
+    const int n_out = shared ? p.shared_inter : p.inter;
+    const int ldab = 2 * n_out;
+    const void* W13 = shared ? p.ws13
+                             : static_cast<const char*>(p.w13) + (BF16 ? 2 : 4) * static_cast<int64_t>(g) * 2 * p.inter * p.d;
+    const void* W2 = shared ? p.ws2
+                            : static_cast<const char*>(p.w2) + (BF16 ? 2 : 4) * static_cast<int64_t>(g) * p.d * p.inter;
+    float* ab = shared ? p.ab_s : p.ab_r;
+    float* dab = shared ? p.dab_s : p.dab_r;
+    float* wh = shared ? p.wh_s : p.wh_r;
+    // token of row r (row space of this group: routed rows in expert order, or tokens)
+    auto token = [&](int64_t r) -> int64_t { return shared ? r : p.perm_token[r]; };
+
+    // loader coordinates: "kc" operands are contiguous along K (thread: one row, 4 k),
+    // "ic" operands along the output index (thread: one k, 4 indices)
+    const int kc_i = tid >> 2, kc_k = (tid & 3) * 4;
+    const int ic_k = tid >> 4, ic_i = (tid & 15) * 4;
+    // row-step A operand (kc): x / dout gathered by token, or [dA dB] by row
+    int64_t a_base = 0;
+    const bool a_ok = kc_i < rows;
+    if constexpr (kRows) {
+        if (a_ok) a_base = MODE == GB_DX ? (row0 + kc_i) * ldab : token(row0 + kc_i) * p.d;
+    }
+    // GB_AB B operand (kc): row n0 + kc_i of W13
+    const bool b_kc_ok = n0 + kc_i < N;
+    const int64_t b_kc_base = static_cast<int64_t>(n0 + kc_i) * p.d;
+
+    const int ty = tid >> 4, tx = tid & 15;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < K; k0 += FBK) {
+        float a[4], b[4];
+        if constexpr (kRows) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int kk = k0 + kc_k + q;
+                const bool ok = a_ok && kk < K;
+                if constexpr (MODE == GB_DX) a[q] = ok ? dab[a_base + kk] : 0.0f;
+                else if constexpr (MODE == GB_AB) a[q] = ok ? ldv<BF16>(p.x, a_base + kk) : 0.0f;
+                else a[q] = ok ? ldv<BF16>(p.dout, a_base + kk) : 0.0f;
+            }
+            if constexpr (MODE == GB_AB) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int kk = k0 + kc_k + q;
+                    b[q] = b_kc_ok && kk < K ? ldv<BF16>(W13, b_kc_base + kk) : 0.0f;
+                }
+            } else {
+                // B(j, kk) = W2[kk][j] (dH) or W13[kk][j] (dX): contiguous along j
+                const int kk = k0 + ic_k;
+                const int ld = MODE == GB_DH ? n_out : p.d;
+                const void* Wb = MODE == GB_DH ? W2 : W13;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int j = n0 + ic_i + q;
+                    b[q] = kk < K && j < N ? ldv<BF16>(Wb, static_cast<int64_t>(kk) * ld + j) : 0.0f;
+                }
+            }
+        } else {
+            // contraction over the group's rows: row k0 + ic_k
+            const int kk = k0 + ic_k;
+            const bool rok = kk < K;
+            const int64_t r = row0 + (rok ? kk : 0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = m0 + ic_i + q, j = n0 + ic_i + q;
+                if constexpr (MODE == GB_DW2) {
+                    a[q] = rok && i < M ? ldv<BF16>(p.dout, token(r) * p.d + i) : 0.0f;
+                    b[q] = rok && j < N ? wh[r * n_out + j] : 0.0f;
+                } else {
+                    a[q] = rok && i < M ? dab[r * ldab + i] : 0.0f;
+                    b[q] = rok && j < N ? ldv<BF16>(p.x, token(r) * p.d + j) : 0.0f;
+                }
+            }
+        }
+        if constexpr (kRows) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) As[kc_k + q][kc_i] = a[q];
+        } else {
+            *reinterpret_cast<float4*>(&As[ic_k][ic_i]) = make_float4(a[0], a[1], a[2], a[3]);
+        }
+        if constexpr (MODE == GB_AB) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) Bs[kc_k + q][kc_i] = b[q];
+        } else {
+            *reinterpret_cast<float4*>(&Bs[ic_k][ic_i]) = make_float4(b[0], b[1], b[2], b[3]);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < FBK; ++kk) {
+            const float4 av = *reinterpret_cast<const float4*>(&As[kk][ty * 4]);
+            const float4 bv = *reinterpret_cast<const float4*>(&Bs[kk][tx * 4]);
+            const float ar[4] = {av.x, av.y, av.z, av.w}, br[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], br[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rr = m0 + ty * 4 + i;
+        if (rr >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int col = n0 + tx * 4 + j;
+            if (col >= N) continue;
+            const float v = acc[i][j];
+            if constexpr (MODE == GB_AB) {
+                ab[(row0 + rr) * ldab + col] = v;
+            } else if constexpr (MODE == GB_DH) {
+                // SwiGLU backward of h = silu(a) b with dh = w (dout W2)
+                const int64_t r = row0 + rr;
+                const float w = shared ? 1.0f : p.wrow[r];
+                const float dh = w * v;
+                const float av = ab[r * ldab + col], bv = ab[r * ldab + n_out + col];
+                const float sg = 1.0f / (1.0f + expf(-av));
+                const float sa = av * sg;
+                dab[r * ldab + col] = dh * bv * sg * (1.0f + av * (1.0f - sg));
+                dab[r * ldab + n_out + col] = dh * sa;
+                wh[r * n_out + col] = w * sa * bv;
+            } else if constexpr (MODE == GB_DX) {
+                (shared ? p.dx_s : p.dx_r)[(row0 + rr) * p.d + col] = v;
+            } else {
+                const int64_t gi = MODE == GB_DW2 ? static_cast<int64_t>(g) * p.d * p.inter
+                                                  : static_cast<int64_t>(g) * 2 * p.inter * p.d;
+                void* out = shared ? (MODE == GB_DW2 ? p.dws2 : p.dws13) : (MODE == GB_DW2 ? p.dw2 : p.dw13);
+                const int64_t e = (shared ? 0 : gi) + static_cast<int64_t>(rr) * N + col;
+                if constexpr (BF16) static_cast<uint16_t*>(out)[e] = f32_to_bf16(v);
+                else static_cast<float*>(out)[e] = v;
+            }
+        }
+    }
+}
+
 // ============================================================== combine
 
 template <bool BF16>
@@ -1224,6 +1447,71 @@ hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const Bw
     if (mode == 3) hipLaunchKernelGGL(gemm_bf16_pk_kernel<3>, grid, dim3(PK_THREADS), 0, stream, g);
     else if (mode == 4) hipLaunchKernelGGL(gemm_bf16_pk_kernel<4>, grid, dim3(PK_THREADS), 0, stream, g);
     else hipLaunchKernelGGL(gemm_bf16_pk_kernel<5>, grid, dim3(PK_THREADS), 0, stream, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_generic_bwd(int step, const ExpertArgs& a, const GenericBwdPtrs& bp, hipStream_t stream) {
+    GenBwdArgs g;
+    g.T = a.T;
+    g.d = a.d;
+    g.E = a.E;
+    g.inter = a.inter;
+    g.shared_inter = a.shared_inter;
+    g.off = a.expert_offsets;
+    g.perm_token = a.perm_token;
+    g.work = bp.work;
+    g.x = a.x;
+    g.dout = bp.dout;
+    g.w13 = a.w13;
+    g.w2 = a.w2;
+    g.ws13 = a.ws13;
+    g.ws2 = a.ws2;
+    g.ab_r = bp.ab_r;
+    g.ab_s = bp.ab_s;
+    g.dab_r = bp.dab_r;
+    g.dab_s = bp.dab_s;
+    g.wh_r = bp.wh_r;
+    g.wh_s = bp.wh_s;
+    g.dx_r = bp.dx_r;
+    g.dx_s = bp.dx_s;
+    g.wrow = bp.wrow;
+    g.dw13 = bp.dw13;
+    g.dw2 = bp.dw2;
+    g.dws13 = bp.dws13;
+    g.dws2 = bp.dws2;
+    const bool bf16 = a.act_dtype == 1;
+    const bool has_shared = a.shared_inter > 0;
+    dim3 grid;
+    if (step <= GB_DX) {
+        const int nt_r = gb_row_tiles(step, a.inter, a.d), nt_s = gb_row_tiles(step, a.shared_inter, a.d);
+        hipLaunchKernelGGL(bwd_work_kernel, dim3(1), dim3(256), 0, stream, a.expert_offsets, a.E, a.T, FBM, nt_r, nt_s,
+                           has_shared ? 1 : 0, bp.work);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        grid = dim3(static_cast<unsigned>(work_bound(a.T, a.k, a.E, FBM, nt_r, nt_s, has_shared, 0)));
+    } else {
+        auto tiles = [&](int n_out) {
+            const int64_t M = step == GB_DW2 ? a.d : 2 * n_out, N = step == GB_DW2 ? n_out : a.d;
+            return ceil_div(M, FBM) * ceil_div(N, FBNB);
+        };
+        const int64_t t_r = tiles(a.inter), t_s = has_shared ? tiles(a.shared_inter) : 0;
+        grid = dim3(static_cast<unsigned>(t_r > t_s ? t_r : t_s), static_cast<unsigned>(a.E + (has_shared ? 1 : 0)));
+    }
+    if (grid.x == 0) return hipSuccess;
+#define SMOES_GB(M)                                                                                    \
+    do {                                                                                               \
+        if (bf16) hipLaunchKernelGGL((gemm_f32_bwd_kernel<M, true>), grid, dim3(kThreads), 0, stream, g);  \
+        else hipLaunchKernelGGL((gemm_f32_bwd_kernel<M, false>), grid, dim3(kThreads), 0, stream, g);      \
+    } while (0)
+    switch (step) {
+        case GB_AB: SMOES_GB(GB_AB); break;
+        case GB_DH: SMOES_GB(GB_DH); break;
+        case GB_DX: SMOES_GB(GB_DX); break;
+        case GB_DW2: SMOES_GB(GB_DW2); break;
+        case GB_DW13: SMOES_GB(GB_DW13); break;
+        default: return hipErrorInvalidValue;
+    }
+#undef SMOES_GB
     return hipGetLastError();
 }
 

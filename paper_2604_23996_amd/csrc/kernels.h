@@ -122,6 +122,28 @@ struct BwdGemmPtrs {
 // routed, 2 shared.
 hipError_t launch_bwd_gemm(int mode, const ExpertArgs& a, void* fwd_ws, const BwdGemmPtrs& bp, int part,
                            hipStream_t stream);
+// Backward of fp32 layers and of bf16 layers with row-major weights: float32
+// FMA tiles, float32 intermediates, weight gradients in the layer dtype.
+struct GenericBwdPtrs {
+    const void* dout;   // [T][d] layer dtype
+    float* ab_r;        // [R][2 inter] gate | up pre-activations
+    float* ab_s;        // [T][2 shared_inter]
+    float* dab_r;       // their gradients
+    float* dab_s;
+    float* wh_r;        // [R][inter] w H
+    float* wh_s;        // [T][shared_inter] H
+    float* dx_r;        // [R][d]
+    float* dx_s;        // [T][d]
+    const float* wrow;  // [R] combine weight of each routed row
+    int32_t* work;      // [E + 2] work table, rebuilt by each row step
+    void* dw13;
+    void* dw2;
+    void* dws13;
+    void* dws2;
+};
+// step 0: pre-activations; 1: dH and the SwiGLU backward (dA dB, w H); 2: dX;
+// 3: dW2 and dWs2; 4: dW13 and dWs13. Routed and shared experts in one launch.
+hipError_t launch_generic_bwd(int step, const ExpertArgs& a, const GenericBwdPtrs& bp, hipStream_t stream);
 // dW[g][m][n] = sum over the group's rows r of A[amap(r)][m] * B[bmap(r)][n] (bf16 out); at most
 // one of amap / bmap (map_len entries) is given; A has a_rows rows of lda elements, B b_rows of ldb.
 hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int lda,
@@ -130,13 +152,16 @@ hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* of
 size_t router_bwd_workspace_bytes(int64_t T, int d, int E);
 hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int64_t T, int k, float* wrow,
                               hipStream_t stream);
-hipError_t launch_router_bwd(const void* dout, const void* y_r, const int32_t* perm_inv, const float* probs,
-                             const int32_t* topk_idx, const float* topk_w, const float* dlogits_aux, int64_t T, int d,
-                             int E, int k, int renorm, float* dw, float* dz, hipStream_t stream);
-hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, const int32_t* perm_inv, const float* dz,
+// bf16: dout and y_r (router_bwd), the row gradients dx_r / dx_s (dx_gather), x (dwgate) are
+// bf16, else float32
+hipError_t launch_router_bwd(const void* dout, const void* y_r, int bf16, const int32_t* perm_inv,
+                             const float* probs, const int32_t* topk_idx, const float* topk_w,
+                             const float* dlogits_aux, int64_t T, int d, int E, int k, int renorm, float* dw,
+                             float* dz, hipStream_t stream);
+hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, int bf16, const int32_t* perm_inv, const float* dz,
                             const float* w_gate, int64_t T, int d, int E, int k, float* dx, hipStream_t stream);
-hipError_t launch_dwgate(const float* dz, const void* x, int64_t T, int d, int E, float* dw_gate, float* dbias,
-                         void* ws, hipStream_t stream);
+hipError_t launch_dwgate(const float* dz, const void* x, int bf16, int64_t T, int d, int E, float* dw_gate,
+                         float* dbias, void* ws, hipStream_t stream);
 
 // ---------------------------------------------------------------- input checks
 // One block: bitmask of violated device-resident preconditions (SMOES_CHECK_*) into flags[0].

@@ -586,17 +586,21 @@ def pack_transposed_weights(spec: LayerSpec, dev_in: Dict[str, Optional[torch.Te
 
 def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
                  outputs: Dict[str, Optional[torch.Tensor]], fwd_workspace: torch.Tensor,
-                 packed_t: Dict[str, torch.Tensor], dout: torch.Tensor,
+                 packed_t: Optional[Dict[str, torch.Tensor]], dout: torch.Tensor,
                  dlogits_aux: Optional[torch.Tensor] = None, want_dw: bool = True,
                  grads: Optional[Dict[str, Optional[torch.Tensor]]] = None,
                  workspace: Optional[torch.Tensor] = None,
                  streams: Optional["Streams"] = None) -> Dict[str, torch.Tensor]:
     """smoes_moe_backward after moe_forward with the same inputs / outputs /
-    workspace. `inputs` must hold the packed w13 / ws13 and the float32
-    w_gate; returns the gradients (dx, dw_gate, dbias, dz, dw, dw13, dw2,
-    dws13, dws2), written into `grads` when given (as returned by an earlier
-    call), with `workspace` reused when given; `streams` (side streams) lets
-    the router and shared-expert gradients run beside the routed ones."""
+    workspace. `inputs` holds the layer's w13 / ws13 (packed when
+    spec.weights_packed) and the float32 w_gate, and w2 / ws2 for fp32 layers
+    and row-major bf16 layers; `packed_t` the transposed packed weights
+    (pack_transposed_weights), needed for packed bf16 layers only (else None).
+    Returns the gradients (dx, dw_gate, dbias, dz, dw, dw13, dw2, dws13, dws2;
+    the expert weight gradients in the layer's dtype), written into `grads`
+    when given (as returned by an earlier call), with `workspace` reused when
+    given; `streams` (side streams) lets the router and shared-expert
+    gradients of a packed bf16 layer run beside the routed ones."""
     desc = spec.c()
     io = SmoesLayerIO()
     for name in _IO_FIELDS:
@@ -608,16 +612,18 @@ def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
     io.streams = ctypes.cast(ctypes.byref(streams.st), c_void).value if streams is not None else None
     T, d, E, k, I, SI = spec.T, spec.d, spec.E, spec.k, spec.inter, spec.shared_inter
     dev = dout.device
+    wdt = torch.bfloat16 if spec.act_dtype == SMOES_BF16 else torch.float32
+    pt = packed_t or {}
     g = grads if grads is not None else {
          "dx": torch.empty((T, d), dtype=torch.float32, device=dev),
          "dw_gate": torch.empty((E, d), dtype=torch.float32, device=dev),
          "dbias": torch.empty(E, dtype=torch.float32, device=dev),
          "dz": torch.empty((T, E), dtype=torch.float32, device=dev),
          "dw": torch.empty((T, k), dtype=torch.float32, device=dev) if want_dw else None,
-         "dw13": torch.empty((E, 2 * I, d), dtype=torch.bfloat16, device=dev),
-         "dw2": torch.empty((E, d, I), dtype=torch.bfloat16, device=dev),
-         "dws13": torch.empty((2 * SI, d), dtype=torch.bfloat16, device=dev) if SI > 0 else None,
-         "dws2": torch.empty((d, SI), dtype=torch.bfloat16, device=dev) if SI > 0 else None}
+         "dw13": torch.empty((E, 2 * I, d), dtype=wdt, device=dev),
+         "dw2": torch.empty((E, d, I), dtype=wdt, device=dev),
+         "dws13": torch.empty((2 * SI, d), dtype=wdt, device=dev) if SI > 0 else None,
+         "dws2": torch.empty((d, SI), dtype=wdt, device=dev) if SI > 0 else None}
     G = SmoesLayerGrads()
     for name in _GRAD_FIELDS:
         setattr(G, name, None if g[name] is None else _p(g[name]).value)
@@ -626,8 +632,8 @@ def moe_backward(spec: LayerSpec, inputs: Dict[str, Optional[torch.Tensor]],
         ws, nbytes = workspace, workspace.numel()
     else:
         ws = _workspace(nbytes, dev)
-    _check(lib().smoes_moe_backward(ctypes.byref(desc), ctypes.byref(io), _p(packed_t["w13t"]), _p(packed_t["w2t"]),
-                                    _p(packed_t.get("ws13t")), _p(packed_t.get("ws2t")), _p(dout), _p(dlogits_aux),
+    _check(lib().smoes_moe_backward(ctypes.byref(desc), ctypes.byref(io), _p(pt.get("w13t")), _p(pt.get("w2t")),
+                                    _p(pt.get("ws13t")), _p(pt.get("ws2t")), _p(dout), _p(dlogits_aux),
                                     ctypes.byref(G), _p(fwd_workspace), fwd_workspace.numel(), _p(ws), nbytes,
                                     _stream()), "smoes_moe_backward")
     return g

@@ -18,7 +18,16 @@ their gradients, H and each routed row's dX in bf16, relative rounding
   dx                       <= 1e-2  (observed up to 3.1e-3)
   dw13, dw2, dws13, dws2   <= 1e-2  (observed up to 3.3e-3)
 plus an elementwise bar of 6e-2 x max|ref| on every gradient (no single
-element far off while the norm is fine)."""
+element far off while the norm is fine).
+
+fp32 layers and bf16 layers with row-major weights take the float32 FMA
+backward (float32 intermediates). For fp32 layers every stored value is
+float32 and each gradient entry is a float32 sum of at most a few thousand
+products, so the normwise error is a small multiple of the unit roundoff
+6e-8 amplified by the cancellation in the sum: bars 1e-5 (dbias, a column
+sum of signed logit gradients, 1e-4) and an elementwise bar of 1e-4 x
+max|ref|. Row-major bf16 layers keep the packed layers' bars (their forward
+Y and H are still bf16)."""
 from __future__ import annotations
 
 import numpy as np
@@ -35,6 +44,9 @@ pytestmark = pytest.mark.gpu
 BARS = {"dw": 5e-3, "dz": 5e-3, "dbias": 1e-2, "dw_gate": 5e-3, "dx": 1e-2,
         "dw13": 1e-2, "dw2": 1e-2, "dws13": 1e-2, "dws2": 1e-2}
 ELEM = 6e-2
+BARS_F32 = {"dw": 1e-5, "dz": 1e-5, "dbias": 1e-4, "dw_gate": 1e-5, "dx": 1e-5,
+            "dw13": 1e-5, "dw2": 1e-5, "dws13": 1e-5, "dws2": 1e-5}
+ELEM_F32 = 1e-4
 
 LAYERS = [
     dict(d=128, E=16, k=4, inter=96, n_shared=1, n_bins=4, samples=((200, 100), (40, 60))),
@@ -51,13 +63,22 @@ LAYERS = [
 ]
 
 
-def _inputs(case, seed):
-    cfg = W.small_config(seed=seed, dtype=W.BF16, **case)
+def _inputs(case, seed, dtype=W.BF16):
+    cfg = W.small_config(seed=seed, dtype=dtype, **case)
+    return _inputs_of(cfg, seed)
+
+
+def _inputs_of(cfg, seed):
     inp = W.make_layer_inputs(cfg)
     rng = np.random.default_rng(seed + 7)
-    dout = _mask_ties(inp, W.f32_to_bf16_bits(rng.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
+    g = rng.standard_normal((cfg.T, cfg.d)).astype(np.float32)
+    dout = _mask_ties(inp, W.f32_to_bf16_bits(g) if cfg.dtype == W.BF16 else g)
     aux = (1e-3 * rng.standard_normal((cfg.T, cfg.E))).astype(np.float32)
     return cfg, inp, dout, aux
+
+
+def _dout_f(cfg, dout):
+    return W.bf16_bits_to_f32(dout) if cfg.dtype == W.BF16 else dout
 
 
 def _mask_ties(inp, dout, gap=1e-3):
@@ -69,27 +90,32 @@ def _mask_ties(inp, dout, gap=1e-3):
     return dout
 
 
-def run_gpu_backward(inp, dout, aux, renorm, want_dw=True, save_preact=False, streams=None):
+def run_gpu_backward(inp, dout, aux, renorm, want_dw=True, save_preact=False, streams=None, packed=None):
     """Forward then backward on the device (the backward's router and shared
-    experts on side streams when `streams` is given); returns (spec, outs,
-    grads)."""
+    experts on side streams when `streams` is given); bf16 layers use packed
+    weights unless packed=False; returns (spec, outs, grads)."""
     cfg = inp.cfg
-    rowmajor = {"w13": t(inp.w13), "w2": t(inp.w2), "ws13": t(inp.ws13), "ws2": t(inp.ws2)}
-    spec_t = layer_spec(cfg, weights_packed=True)
-    packed_t = S.pack_transposed_weights(spec_t, rowmajor)
-    torch.cuda.synchronize()
-    spec, dev_in, outs, ws = run_gpu_layer(inp, renorm_topk=renorm, keep_workspace=True, save_preact=save_preact)
+    if packed is None:
+        packed = cfg.dtype == W.BF16
+    packed_t = None
+    if packed:
+        rowmajor = {"w13": t(inp.w13), "w2": t(inp.w2), "ws13": t(inp.ws13), "ws2": t(inp.ws2)}
+        spec_t = layer_spec(cfg, weights_packed=True)
+        packed_t = S.pack_transposed_weights(spec_t, rowmajor)
+        torch.cuda.synchronize()
+    spec, dev_in, outs, ws = run_gpu_layer(inp, renorm_topk=renorm, keep_workspace=True, save_preact=save_preact,
+                                           packed=packed)
     g = S.moe_backward(spec, dev_in, outs, ws, packed_t, t(dout), None if aux is None else t(aux), want_dw=want_dw,
                        streams=streams)
     torch.cuda.synchronize()
     return spec, outs, g
 
 
-def _compare(g, ref, inp, outs, cfg, extra=""):
+def _compare(g, ref, inp, outs, cfg, extra="", bars=BARS, elem=ELEM):
     z_ref, _, idx_ref, _ = O.route(inp.x, inp.w_gate, cfg.k, inp.logit_bias)
     check_topk(host(outs["topk_idx"]), idx_ref, z_ref, cfg.k)
     errs = {}
-    for name, bar in BARS.items():
+    for name, bar in bars.items():
         r = ref[name]
         if r is None:
             assert g.get(name) is None
@@ -101,7 +127,7 @@ def _compare(g, ref, inp, outs, cfg, extra=""):
         errs[name] = e
         scale = np.abs(r).max()
         assert e <= bar, (name, e, extra)
-        assert np.abs(got - r).max() <= ELEM * scale + 1e-30, (name, np.abs(got - r).max(), scale, extra)
+        assert np.abs(got - r).max() <= elem * scale + 1e-30, (name, np.abs(got - r).max(), scale, extra)
     say("backward errors", extra, {k: f"{v:.2e}" for k, v in errs.items()})
     return errs
 
@@ -115,22 +141,24 @@ def test_backward_small(layer, renorm, with_aux):
         aux = None
     say("backward", layer, "renorm", renorm, "aux", with_aux, "T", cfg.T)
     spec, outs, g = run_gpu_backward(inp, dout, aux, renorm)
-    ref = O.layer_backward(inp.x, inp.w_gate, inp.logit_bias, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
-                           W.bf16_bits_to_f32(dout), aux, renorm_topk=renorm)
-    _compare(g, ref, inp, outs, cfg, extra=f"layer {layer}")
+    _compare(g, _ref(inp, cfg, dout, aux, renorm), inp, outs, cfg, extra=f"layer {layer}")
 
 
-def test_backward_experts_without_tokens_have_zero_gradient():
-    cfg, inp, dout, aux = _inputs(LAYERS[4], 304)
-    say("backward empty experts")
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+def test_backward_experts_without_tokens_have_zero_gradient(dtype):
+    cfg, inp, dout, aux = _inputs(LAYERS[4], 304, dtype=dtype)
+    say("backward empty experts", dtype)
     spec, outs, g = run_gpu_backward(inp, dout, None, False)
     idx = host(outs["topk_idx"])
     used = np.zeros(cfg.E, bool)
     used[idx.ravel()] = True
-    assert (~used).any()
+    # experts with a token whose upstream gradient is not masked to zero
+    live = np.zeros(cfg.E, bool)
+    live[idx[np.abs(_dout_f(cfg, dout)).max(axis=1) > 0].ravel()] = True
+    assert (~used).any() and live.any()
     dw13, dw2 = host(g["dw13"]), host(g["dw2"])
     assert np.all(dw13[~used] == 0.0) and np.all(dw2[~used] == 0.0)
-    assert np.all(np.abs(dw13[used]).reshape(int(used.sum()), -1).max(axis=1) > 0)
+    assert np.all(np.abs(dw13[live]).reshape(int(live.sum()), -1).max(axis=1) > 0)
 
 
 @pytest.mark.parametrize("layer", [0, 1, 2, 4])
@@ -184,17 +212,64 @@ def test_backward_without_dw_output():
             assert torch.equal(g[name], h[name]), name
 
 
-def test_backward_rejects_fp32_and_rowmajor_layers():
+def _ref(inp, cfg, dout, aux, renorm):
+    return O.layer_backward(inp.x, inp.w_gate, inp.logit_bias, cfg.k, inp.w13, inp.w2, inp.ws13, inp.ws2,
+                            _dout_f(cfg, dout), aux, renorm_topk=renorm)
+
+
+@pytest.mark.parametrize("layer", range(len(LAYERS)))
+@pytest.mark.parametrize("renorm", [False, True])
+def test_backward_fp32(layer, renorm):
+    cfg, inp, dout, aux = _inputs(LAYERS[layer], 400 + layer, dtype=W.F32)
+    say("backward fp32", layer, "renorm", renorm, "T", cfg.T)
+    spec, outs, g = run_gpu_backward(inp, dout, aux, renorm)
+    assert g["dw13"].dtype == torch.float32
+    _compare(g, _ref(inp, cfg, dout, aux, renorm), inp, outs, cfg, extra=f"fp32 layer {layer}", bars=BARS_F32,
+             elem=ELEM_F32)
+
+
+def test_backward_tiny_fp32_workload():
+    # the small fp32 workload (T=512, d=256, E=8, top-2, inter=512, no shared experts) in full
+    cfg = W.workload("tiny-fp32")
+    cfg, inp, dout, aux = _inputs_of(cfg, cfg.seed)
+    say("backward tiny-fp32", cfg.T)
+    for renorm in (False, True):
+        spec, outs, g = run_gpu_backward(inp, dout, aux, renorm)
+        _compare(g, _ref(inp, cfg, dout, aux, renorm), inp, outs, cfg, extra=f"tiny-fp32 renorm {renorm}",
+                 bars=BARS_F32, elem=ELEM_F32)
+
+
+@pytest.mark.parametrize("layer", range(len(LAYERS)))
+def test_backward_rowmajor_bf16(layer):
+    cfg, inp, dout, aux = _inputs(LAYERS[layer], 300 + layer)
+    say("backward row-major bf16", layer, "T", cfg.T)
+    spec, outs, g = run_gpu_backward(inp, dout, aux, True, packed=False)
+    assert g["dw13"].dtype == torch.bfloat16
+    _compare(g, _ref(inp, cfg, dout, aux, True), inp, outs, cfg, extra=f"row-major layer {layer}")
+
+
+def test_backward_fp32_is_reproducible():
+    cfg, inp, dout, aux = _inputs(LAYERS[0], 400, dtype=W.F32)
+    say("backward fp32 reproducible")
+    _, _, a = run_gpu_backward(inp, dout, aux, True)
+    _, _, b = run_gpu_backward(inp, dout, aux, True)
+    for name in a:
+        if a[name] is not None:
+            assert torch.equal(a[name], b[name]), name
+
+
+def test_backward_rejects_missing_weights():
+    # the float32 path reads the row-major w2 / ws2; the packed path needs the transposed packs
     cfg = W.small_config(d=64, E=8, k=2, inter=32, n_shared=0, samples=((8, 8),), dtype=W.F32, seed=5)
     spec = layer_spec(cfg)
     ws = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
     x = torch.zeros((cfg.T, cfg.d), dtype=torch.float32, device=DEV)
     with pytest.raises(S.SmoesError):
-        S.moe_backward(spec, {"x": x}, {}, ws, {"w13t": x, "w2t": x}, x)
+        S.moe_backward(spec, {"x": x}, {}, ws, None, x)
     cfg = W.small_config(d=64, E=8, k=2, inter=32, n_shared=0, samples=((8, 8),), dtype=W.BF16, seed=5)
-    spec = layer_spec(cfg, weights_packed=False)
+    spec = layer_spec(cfg, weights_packed=True)
     with pytest.raises(S.SmoesError):
-        S.moe_backward(spec, {"x": x}, {}, ws, {"w13t": x, "w2t": x}, x)
+        S.moe_backward(spec, {"x": x}, {}, ws, None, x)
 
 
 @pytest.mark.parametrize("name", ["deepseekmoe-vlm", W.BENCH_WORKLOAD])
