@@ -83,18 +83,31 @@ mi_partial_kernel(const float* __restrict__ probs, const float* __restrict__ M, 
     const int64_t s0 = a + c * L;
     const int64_t s1 = s0 + L < b ? s0 + L : b;
     double a0 = 0.0, a1 = 0.0, w0 = 0.0, w1 = 0.0;
-    if (rg < RG) {
-        for (int64_t j = s0 + rg; j < s1; j += RG) {
-            const float2 mj = *reinterpret_cast<const float2*>(M + 2 * j);
-            const double m0 = mj.x, m1 = mj.y;
-            if (e < E) {
-                const double g = probs[j * E + e];
-                a0 = fma(m0, g, a0);
-                a1 = fma(m1, g, a1);
-            }
-            w0 += m0;
-            w1 += m1;
+    // rows in order; the loads of 8 rows go out before their sums
+    auto add = [&](float2 mj, float gv) {
+        const double m0 = mj.x, m1 = mj.y;
+        if (e < E) {
+            a0 = fma(m0, static_cast<double>(gv), a0);
+            a1 = fma(m1, static_cast<double>(gv), a1);
         }
+        w0 += m0;
+        w1 += m1;
+    };
+    if (rg < RG) {
+        constexpr int U = 8;
+        int64_t j = s0 + rg;
+        for (; j + (U - 1) * RG < s1; j += U * RG) {
+            float2 mj[U];
+            float gv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                mj[u] = *reinterpret_cast<const float2*>(M + 2 * (j + u * RG));
+                gv[u] = e < E ? probs[(j + u * RG) * E + e] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) add(mj[u], gv[u]);
+        }
+        for (; j < s1; j += RG) add(*reinterpret_cast<const float2*>(M + 2 * j), e < E ? probs[j * E + e] : 0.0f);
     }
     red[threadIdx.x][0] = a0;
     red[threadIdx.x][1] = a1;
@@ -144,6 +157,58 @@ mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batc
     const int NB = E / n_bins;
     const int tid = threadIdx.x;
     const int i = blockIdx.x;
+    // chunk partials: thread (cg, e) sums chunks cg, cg + RG, ... in order
+    const int EP = static_cast<int>(ceil_div(E, kWave) * kWave);
+    const int RG = kMiThreads / EP;
+    const int cg = tid / EP, e = tid % EP;
+    const double* pi = part + static_cast<int64_t>(i) * C * (2 * E + 2);
+    double s0 = 0.0, s1 = 0.0, w0 = 0.0, w1 = 0.0;
+    auto add = [&](const double* pc) {
+        if (e < E) {
+            s0 += pc[e];
+            s1 += pc[E + e];
+        }
+        if (e == 0) {
+            w0 += pc[2 * E];
+            w1 += pc[2 * E + 1];
+        }
+    };
+    if (cg < RG) {
+        // chunks in order; the loads of 16 chunks go out before their sums
+        constexpr int U = 16;
+        int c = cg;
+        for (; c + (U - 1) * RG < C; c += U * RG) {
+            double v[U][2];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const double* pc = pi + static_cast<int64_t>(c + u * RG) * (2 * E + 2);
+                v[u][0] = e < E ? pc[e] : 0.0;
+                v[u][1] = e < E ? pc[E + e] : 0.0;
+            }
+            if (e == 0) {
+                double q[U][2];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const double* pc = pi + static_cast<int64_t>(c + u * RG) * (2 * E + 2);
+                    q[u][0] = pc[2 * E];
+                    q[u][1] = pc[2 * E + 1];
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    w0 += q[u][0];
+                    w1 += q[u][1];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (e < E) {
+                    s0 += v[u][0];
+                    s1 += v[u][1];
+                }
+            }
+        }
+        for (; c < C; c += RG) add(pi + static_cast<int64_t>(c) * (2 * E + 2));
+    }
     // bin member lists in ascending expert order: expert e takes slot
     // (its bin, the number of lower experts in that bin); slots no expert
     // takes stay -1 (violated precondition: a bin with fewer than N_B experts)
@@ -157,26 +222,6 @@ mi_finalize_kernel(int64_t T, int E, const int32_t* __restrict__ off, int n_batc
         int rank = 0;
         for (int e = 0; e < q; ++e) rank += bin_s[e] == k ? 1 : 0;
         if (k >= 0 && k < n_bins && rank < NB) mem[k * NB + rank] = q;
-    }
-    // chunk partials: thread (cg, e) sums chunks cg, cg + RG, ... in order
-    const int EP = static_cast<int>(ceil_div(E, kWave) * kWave);
-    const int RG = kMiThreads / EP;
-    const int cg = tid / EP, e = tid % EP;
-    const double* pi = part + static_cast<int64_t>(i) * C * (2 * E + 2);
-    double s0 = 0.0, s1 = 0.0, w0 = 0.0, w1 = 0.0;
-    if (cg < RG) {
-#pragma unroll 4
-        for (int c = cg; c < C; c += RG) {
-            const double* pc = pi + static_cast<int64_t>(c) * (2 * E + 2);
-            if (e < E) {
-                s0 += pc[e];
-                s1 += pc[E + e];
-            }
-            if (e == 0) {
-                w0 += pc[2 * E];
-                w1 += pc[2 * E + 1];
-            }
-        }
     }
     red[tid][0] = s0;
     red[tid][1] = s1;
@@ -279,59 +324,93 @@ mi_grad_kernel(const float* __restrict__ probs, const float* __restrict__ M, int
         bin[e] = e2b[e];
     }
     const int QE = static_cast<int>(ceil_div(E, kWave));
-    const int64_t per_iter = static_cast<int64_t>(gridDim.x) * kWaves;
-    const int64_t iters = ceil_div(T, per_iter);
-    __syncthreads();
-    for (int64_t it = 0; it < iters; ++it) {
-        const int64_t j = it * per_iter + static_cast<int64_t>(blockIdx.x) * kWaves + wave;
-        const bool live = j < T;
-        float g[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        int si = 0;
-        if (live) {
-            if (off != nullptr) {  // sample of token j: last i with off[i] <= j
-                int lo = 0, hi = n_batch - 1;
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (off[mid] <= j) lo = mid; else hi = mid - 1;
-                }
-                si = lo;
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int e = lane + q * kWave;
-                if (q < QE && e < E) {
-                    g[q] = probs[j * E + e];
-                    gl[wave][e] = g[q];
-                }
-            }
+    // block b takes tokens [j_lo, j_hi); wave w every kWaves-th of them from j_lo + w
+    const int64_t per_block = ceil_div(ceil_div(T, gridDim.x), kWaves) * kWaves;
+    const int64_t j_lo = static_cast<int64_t>(blockIdx.x) * per_block;
+    const int64_t j_hi = j_lo + per_block < T ? j_lo + per_block : T;
+    // sample of the wave's token: last i with off[i] <= j, found once and then
+    // advanced as the tokens pass the ends of samples
+    int si = 0;
+    int64_t next = INT64_MAX;
+    const int64_t jw = j_lo + wave;
+    if (off != nullptr && jw < j_hi) {
+        int lo = 0, hi = n_batch - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (off[mid] <= jw) lo = mid; else hi = mid - 1;
         }
-        __syncthreads();
+        si = lo;
+        next = si + 1 < n_batch ? off[si + 1] : INT64_MAX;
+    }
+    // the coefficients c[m][lane] of the wave's current sample, reloaded when the sample changes
+    auto load_coef = [&](int i, double& c0, double& c1) {
+        c0 = c1 = 0.0;
+        if (lane < n_bins) {
+            const double* cf = coef + static_cast<int64_t>(i) * 2 * n_bins;
+            c0 = cf[lane];
+            c1 = cf[n_bins + lane];
+        }
+    };
+    double cf0, cf1;
+    load_coef(si, cf0, cf1);
+    // the gates and scores of token j (0 past the wave's range)
+    auto load_tok = [&](int64_t j, float (&g)[4], float2& mj) {
+        const bool ok = j < j_hi;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + q * kWave;
+            g[q] = ok && q < QE && e < E ? probs[j * E + e] : 0.0f;
+        }
+        mj = ok ? *reinterpret_cast<const float2*>(M + 2 * j) : make_float2(0.0f, 0.0f);
+    };
+    __syncthreads();  // mem, bin
+    auto wave_lds_sync = [] {
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+    float gn[4];
+    float2 mn;
+    load_tok(jw, gn, mn);
+    for (int64_t j = jw; j < j_hi; j += kWaves) {
+        const float g[4] = {gn[0], gn[1], gn[2], gn[3]};
+        const float2 mj = mn;
+        load_tok(j + kWaves, gn, mn);  // the wave's next token, in flight during this one
+        if (j >= next) {
+            while (j >= next) {
+                ++si;
+                next = si + 1 < n_batch ? off[si + 1] : INT64_MAX;
+            }
+            load_coef(si, cf0, cf1);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + q * kWave;
+            if (q < QE && e < E) gl[wave][e] = g[q];
+        }
+        wave_lds_sync();
         double gh = 0.0;
-        if (live && lane < n_bins) {
+        if (lane < n_bins) {
             double G = 0.0;
             for (int n = 0; n < NB; ++n) {
                 const int e = mem[lane * NB + n];
                 if (e >= 0) G += static_cast<double>(gl[wave][e]);
             }
-            const float2 mj = *reinterpret_cast<const float2*>(M + 2 * j);
-            const double* cf = coef + static_cast<int64_t>(si) * 2 * n_bins;
-            const double h = static_cast<double>(mj.x) * cf[lane] + static_cast<double>(mj.y) * cf[n_bins + lane];
+            const double h = static_cast<double>(mj.x) * cf0 + static_cast<double>(mj.y) * cf1;
             hl[wave][lane] = h;
             gh = G * h;
         }
         gh = wave_sum(gh);
-        __syncthreads();
-        if (live) {
+        wave_lds_sync();
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int e = lane + q * kWave;
-                if (q < QE && e < E) {
-                    const double dv = scale * static_cast<double>(g[q]) * (hl[wave][bin[e]] - gh);
-                    dlogits[j * E + e] = static_cast<float>(dv);
-                }
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + q * kWave;
+            if (q < QE && e < E) {
+                const double dv = scale * static_cast<double>(g[q]) * (hl[wave][bin[e]] - gh);
+                dlogits[j * E + e] = static_cast<float>(dv);
             }
         }
-        __syncthreads();
+        wave_lds_sync();
     }
 }
 

@@ -126,13 +126,13 @@ perm_scatter_kernel(const int32_t* __restrict__ idx, int64_t T, int E, int k, in
         const int e = threadIdx.x;
         int tot = 0, pre = 0;
         if (e < E) {
-            // eight independent loads in flight, summed in chunk order
-            for (int64_t c0 = 0; c0 < nchunk; c0 += 8) {
-                int h[8];
+            // 32 independent loads in flight, summed in chunk order
+            for (int64_t c0 = 0; c0 < nchunk; c0 += 32) {
+                int h[32];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) h[q] = c0 + q < nchunk ? hist[(c0 + q) * E + e] : 0;
+                for (int q = 0; q < 32; ++q) h[q] = c0 + q < nchunk ? hist[(c0 + q) * E + e] : 0;
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
+                for (int q = 0; q < 32; ++q) {
                     tot += h[q];
                     pre += c0 + q < blockIdx.x ? h[q] : 0;
                 }
