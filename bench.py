@@ -230,6 +230,49 @@ def memory_bound_rows(S, W, cfg, spec, dev_in, outs, ws, work, reps):
     return rows
 
 
+def gemm_ceiling_rows(cfg, counts, reps):
+    """The vendor GEMM (torch.matmul, hipBLASLt) at this layer's expert GEMM
+    shapes, bf16 operands and float32 accumulation: a measured reference for
+    the grouped expert kernels on this chip and clock. The routed rows are
+    timed as one dense GEMM (an upper bound for the grouped work: no row
+    gather, no ragged groups, no fused SwiGLU), and the largest expert's rows
+    as one GEMM."""
+    import numpy as np
+    import torch
+    dev = "cuda:0"
+    R, d, I, SI = cfg.T * cfg.k, cfg.d, cfg.inter, cfg.shared_inter
+    big = int(np.max(counts))
+    shapes = {"routed_gate_up_dense": (R, 2 * I, d), "routed_down_dense": (R, d, I),
+              "largest_expert_gate_up": (big, 2 * I, d), "largest_expert_down": (big, d, I)}
+    if SI > 0:
+        shapes["shared_gate_up"] = (cfg.T, 2 * SI, d)
+        shapes["shared_down"] = (cfg.T, d, SI)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    rows = {}
+    for name, (m, n, k) in shapes.items():
+        if m == 0:
+            continue
+        a = torch.randn((m, k), device=dev, dtype=torch.bfloat16)
+        b = torch.randn((k, n), device=dev, dtype=torch.bfloat16)  # contiguous right operand
+        for _ in range(2):
+            c = a @ b
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(max(reps, 5)):
+            ev[0].record()
+            c = a @ b
+            ev[1].record()
+            torch.cuda.synchronize()
+            ts.append(ev[0].elapsed_time(ev[1]))
+        ms = float(np.median(ts))
+        tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+        rows[name] = {"m": m, "n": n, "k": k, "ms": round(ms, 5), "tflops": round(tf, 1),
+                      "frac_mfma": round(tf / PEAK_BF16_TFLOPS, 4)}
+        del a, b, c
+    torch.cuda.empty_cache()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -410,6 +453,10 @@ def main():
     if not args.no_extras:
         log("[bench] memory-bound kernels, MALL flushed")
         line["memory_bound"] = memory_bound_rows(S, W, cfg, spec, dev_in, outs, ws, work, args.steps)
+        # the vendor GEMM at the same shapes (reference for the expert kernels)
+        log("[bench] vendor GEMM at the expert shapes")
+        counts = np.diff(outs["expert_offsets"].cpu().numpy())
+        line["gemm_ceiling"] = gemm_ceiling_rows(cfg, counts, args.steps)
     if not args.no_extras:
         # Gaussian statistics update (Eq. 5-7) followed by the score (Eq. 8-9) on
         # this workload's tokens: the modality stage of a layer that re-estimates
