@@ -594,8 +594,8 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     // so spreading the memory instructions over the MFMAs keeps the matrix
     // pipe fed while the address unit drains them.
     static_assert(IA == 4, "one A DMA per K = 16 substep");
-    // MT: 32-row sub-tiles that take part (4, or 2 for a tile of at most 64
-    // rows: a short last tile of an expert skips half of the MFMAs).
+    // MT: 32-row sub-tiles that take part (1-4: a short last tile of an
+    // expert skips the MFMAs and fragment reads of its empty sub-tiles).
     auto stage_run = [&](auto mt_c, int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
         constexpr int MT = decltype(mt_c)::value;
         const uint8_t* base = lds + slot * A_BYTES;
@@ -675,8 +675,11 @@ gemm_bf16_pk_kernel(GemmArgs p) {
             stage_run(mt_c, slot, s, b0, b1);
         }
     };
-    if (uniform_int(t.rows) > 64) kloop(std::integral_constant<int, 4>{});
-    else kloop(std::integral_constant<int, 2>{});
+    const int trows = uniform_int(t.rows);
+    if (trows > 96) kloop(std::integral_constant<int, 4>{});
+    else if (trows > 64) kloop(std::integral_constant<int, 3>{});
+    else if (trows > 32) kloop(std::integral_constant<int, 2>{});
+    else kloop(std::integral_constant<int, 1>{});
     wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
     __builtin_amdgcn_s_barrier();
 
