@@ -518,11 +518,13 @@ size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
  * output of Sec. 3.1 (softmax router, top-k combine, SwiGLU experts plus the
  * shared experts). Sums run in a fixed order: results are reproducible.
  * Asynchronous on `stream`; nothing is allocated. Packed path with
- * io->streams set: the router backward, dW_gate / dbias and the shared
- * experts' gradients run on io->streams->side[1], forked from `stream` at
- * the start of the call and joined back before the input gradient
- * (events[0] and events[3]); the results are the same bits as on one
- * stream. NULL runs every step on `stream`.
+ * io->streams set and fewer than 65536 routed rows (T k): the router
+ * backward, dW_gate / dbias and the shared experts' gradients run on
+ * io->streams->side[1], forked from `stream` at the start of the call and
+ * joined back before the input gradient (events[0] and events[3]); the
+ * results are the same bits as on one stream. From 65536 routed rows, or with
+ * NULL, every step runs on `stream` (there the routed GEMMs alone fill the
+ * GPU and the side chain would only take compute units from them).
  */
 int smoes_moe_backward(const smoes_layer* desc, const smoes_layer_io* io, const void* w13t, const void* w2t,
                        const void* ws13t, const void* ws2t, const void* dout, const float* dlogits_aux,

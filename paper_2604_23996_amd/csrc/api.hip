@@ -528,6 +528,8 @@ int smoes_check_inputs(const smoes_layer* L, const smoes_layer_io* io, int32_t* 
 namespace {
 // fp32 layers and bf16 layers with row-major weights take the float32 FMA backward
 bool generic_bwd(const smoes_layer* L) { return L->act_dtype != SMOES_BF16 || !L->weights_packed; }
+// routed rows (T k) from which the packed backward runs on the caller's stream alone
+constexpr int64_t kBwdOverlapRows = 65536;
 
 struct BwdWs {
     void* ab_r;
@@ -541,7 +543,20 @@ struct BwdWs {
     void* wh_s;  // float32 H of the shared experts (float32 backward only)
     int32_t* work4;
     void* router;
+    // k-packed weight-gradient operands (packed bf16 path): routed rows (dout,
+    // then x, gathered), w H, [dA dB]; the same for the shared experts' tokens
+    int32_t* kp;
+    void* pt_rows_r;
+    void* pt_wh_r;
+    void* pt_dab_r;
+    void* pt_rows_s;
+    void* pt_h_s;
+    void* pt_dab_s;
 };
+// padded row totals of the k-packed operands: routed (a bound: each expert
+// pads to 16 rows) and shared
+int64_t kpad_routed(const smoes_layer* L) { return L->T * L->k + 15 * static_cast<int64_t>(L->E); }
+int64_t kpad_shared(const smoes_layer* L) { return ceil_div(L->T, 16) * 16; }
 size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     Carver c(base);
     const int64_t T = L->T, R = L->T * L->k;
@@ -561,6 +576,14 @@ size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     w.wh_s = c.take(gen ? es * T * L->shared_inter : 0);
     w.work4 = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 2)));
     w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E));
+    const int64_t kr = gen ? 0 : kpad_routed(L), ksh = gen || L->shared_inter == 0 ? 0 : kpad_shared(L);
+    w.kp = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * (L->E + 1)));
+    w.pt_rows_r = c.take(2 * kpack_elems(L->d, kr));
+    w.pt_wh_r = c.take(2 * kpack_elems(L->inter, kr));
+    w.pt_dab_r = c.take(2 * kpack_elems(2 * L->inter, kr));
+    w.pt_rows_s = c.take(2 * kpack_elems(L->d, ksh));
+    w.pt_h_s = c.take(2 * kpack_elems(L->shared_inter, ksh));
+    w.pt_dab_s = c.take(2 * kpack_elems(2 * L->shared_inter, ksh));
     if (out != nullptr) *out = w;
     return c.used + kAlign;
 }
@@ -584,6 +607,14 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     if (!gen && (2 * L->T * L->k * 2 * static_cast<int64_t>(L->inter) > INT32_MAX ||
                  2 * L->T * 2 * static_cast<int64_t>(L->shared_inter) > INT32_MAX))
         return SMOES_ERR_SHAPE;
+    // the k-packed weight-gradient operands are read with 32-bit byte offsets as well
+    if (!gen) {
+        const int64_t kr = kpad_routed(L), ks = kpad_shared(L);
+        const int wide = L->d > 2 * L->inter ? L->d : 2 * L->inter;
+        const int wide_s = L->d > 2 * L->shared_inter ? L->d : 2 * L->shared_inter;
+        if (2 * kpack_elems(wide, kr) > INT32_MAX || (L->shared_inter > 0 && 2 * kpack_elems(wide_s, ks) > INT32_MAX))
+            return SMOES_ERR_SHAPE;
+    }
     if (L->T == 0) return SMOES_OK;
     const bool sh = L->shared_inter > 0;
     if (io->x == nullptr || io->w13 == nullptr || io->w_gate == nullptr || io->probs == nullptr ||
@@ -689,7 +720,9 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     // run on side[1], forked from s at the start of the call and joined back
     // before the input gradient, which needs both chains; without them every
     // step runs on s in the same dependency order.
-    const smoes_streams* sides = io->streams;
+    // Side streams only below kBwdOverlapRows routed rows: above it the routed
+    // GEMMs alone fill the chip and the side chain only takes CUs from them.
+    const smoes_streams* sides = L->T * L->k < kBwdOverlapRows ? io->streams : nullptr;
     hipStream_t c = s;
     hipEvent_t e_fork = nullptr, e_join = nullptr;
     if (sides != nullptr) {
@@ -700,7 +733,6 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
         SMOES_BTRY(hipStreamWaitEvent(c, e_fork, 0));
     }
     const int I = L->inter, SI = L->shared_inter, d = L->d;
-    const int Ti = static_cast<int>(T), R = static_cast<int>(T * L->k);
     // side chain: router backward (dz, dw), dW_gate and dbias, shared experts
     SMOES_BTRY(launch_router_bwd(dout, fb.y_r, 1, perm_inv, io->probs, io->topk_idx, io->topk_w, dlogits_aux, T,
                                  L->d, L->E, L->k, L->renorm_topk ? 1 : 0, G->dw, G->dz, c));
@@ -708,19 +740,30 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     if (sh) {
         for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode)
             SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 2, c));
-        SMOES_BTRY(launch_wgrad(T, 1, d, SI, nullptr, dout, d, Ti, nullptr, fb.h_s, SI, Ti, nullptr, 0, G->dws2, c));
-        SMOES_BTRY(launch_wgrad(T, 1, 2 * SI, d, nullptr, bw.dab_s, 2 * SI, Ti, nullptr, io->x, d, Ti, nullptr, 0,
-                                G->dws13, c));
+        // dWs2 = dout^T H_s and dWs13 = [dA dB]_s^T X over all tokens, from k-packed copies
+        const int64_t ksh = kpad_shared(L);
+        SMOES_BTRY(launch_kpack(dout, d, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_rows_s, c));
+        SMOES_BTRY(launch_kpack(fb.h_s, SI, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_h_s, c));
+        SMOES_BTRY(launch_wgrad_pk(1, d, SI, nullptr, T, bw.pt_rows_s, bw.pt_h_s, G->dws2, c));
+        SMOES_BTRY(launch_kpack(bw.dab_s, 2 * SI, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_dab_s, c));
+        SMOES_BTRY(launch_kpack(io->x, d, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_rows_s, c));
+        SMOES_BTRY(launch_wgrad_pk(1, 2 * SI, d, nullptr, T, bw.pt_dab_s, bw.pt_rows_s, G->dws13, c));
     }
     if (sides != nullptr) SMOES_BTRY(hipEventRecord(e_join, c));
     // routed chain
     SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
     for (int mode = L->save_preact ? 4 : 3; mode <= 5; ++mode)
         SMOES_BTRY(launch_bwd_gemm(mode, a, fw.experts, bp, 1, s));
-    // dW2 = dout^T (w H) over each expert's rows (dout gathered); dW13 = [dA dB]^T X (x gathered)
-    SMOES_BTRY(launch_wgrad(T, L->E, d, I, offsets, dout, d, Ti, perm_token, bw.wh_r, I, R, nullptr, R, G->dw2, s));
-    SMOES_BTRY(launch_wgrad(T, L->E, 2 * I, d, offsets, bw.dab_r, 2 * I, R, nullptr, io->x, d, Ti, perm_token, R,
-                            G->dw13, s));
+    // dW2 = dout^T (w H) over each expert's rows (dout gathered); dW13 = [dA dB]^T X (x
+    // gathered): both operands k-packed per expert first (rows padded to 16)
+    const int64_t kr = kpad_routed(L);
+    SMOES_BTRY(launch_kpad_offsets(offsets, L->E, bw.kp, s));
+    SMOES_BTRY(launch_kpack(dout, d, perm_token, offsets, bw.kp, L->E, T, kr, bw.pt_rows_r, s));
+    SMOES_BTRY(launch_kpack(bw.wh_r, I, nullptr, offsets, bw.kp, L->E, T, kr, bw.pt_wh_r, s));
+    SMOES_BTRY(launch_wgrad_pk(L->E, d, I, bw.kp, T, bw.pt_rows_r, bw.pt_wh_r, G->dw2, s));
+    SMOES_BTRY(launch_kpack(bw.dab_r, 2 * I, nullptr, offsets, bw.kp, L->E, T, kr, bw.pt_dab_r, s));
+    SMOES_BTRY(launch_kpack(io->x, d, perm_token, offsets, bw.kp, L->E, T, kr, bw.pt_rows_r, s));
+    SMOES_BTRY(launch_wgrad_pk(L->E, 2 * I, d, bw.kp, T, bw.pt_dab_r, bw.pt_rows_r, G->dw13, s));
     if (sides != nullptr) SMOES_BTRY(hipStreamWaitEvent(s, e_join, 0));
     SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, 1, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
                                 G->dx, s));

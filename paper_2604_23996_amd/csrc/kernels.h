@@ -144,11 +144,20 @@ struct GenericBwdPtrs {
 // step 0: pre-activations; 1: dH and the SwiGLU backward (dA dB, w H); 2: dX;
 // 3: dW2 and dWs2; 4: dW13 and dWs13. Routed and shared experts in one launch.
 hipError_t launch_generic_bwd(int step, const ExpertArgs& a, const GenericBwdPtrs& bp, hipStream_t stream);
-// dW[g][m][n] = sum over the group's rows r of A[amap(r)][m] * B[bmap(r)][n] (bf16 out); at most
-// one of amap / bmap (map_len entries) is given; A has a_rows rows of lda elements, B b_rows of ldb.
-hipError_t launch_wgrad(int64_t T, int n_groups, int M, int N, const int32_t* off, const void* A, int lda,
-                        int a_rows, const int32_t* amap, const void* B, int ldb, int b_rows, const int32_t* bmap,
-                        int map_len, void* out, hipStream_t stream);
+// k-packed operands (fragment order, rows contiguous, each group padded to 16
+// rows) and the weight gradients from them: kp = padded row prefix of the
+// groups given by off; kpack_elems = elements of a packed copy of C columns.
+int64_t kpack_elems(int C, int64_t padded_rows);
+hipError_t launch_kpad_offsets(const int32_t* off, int E, int32_t* kp, hipStream_t stream);
+// S [.][C] bf16 row-major; group g's rows are off[g] .. off[g + 1] (through map
+// when given); off == NULL: one group of T rows. max_padded_rows bounds kp's
+// total (the grid).
+hipError_t launch_kpack(const void* S, int C, const int32_t* map, const int32_t* off, const int32_t* kp,
+                        int n_groups, int64_t T, int64_t max_padded_rows, void* P, hipStream_t stream);
+// out[g][m][n] = sum over group g's rows of A[row][m] B[row][n] (bf16), from the
+// k-packed A (M columns) and B (N columns); kp == NULL: one group of T rows.
+hipError_t launch_wgrad_pk(int n_groups, int M, int N, const int32_t* kp, int64_t T, const void* PA, const void* PB,
+                           void* out, hipStream_t stream);
 size_t router_bwd_workspace_bytes(int64_t T, int d, int E);
 hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int64_t T, int k, float* wrow,
                               hipStream_t stream);
