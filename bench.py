@@ -610,49 +610,56 @@ def main():
         # synthetic upstream gradient and the MI gradient as the auxiliary logit
         # gradient (every gradient: combine weights, logits, router weight and
         # bias, routed and shared expert weights, input). Timed on its own.
+        log("[bench] training step (forward + backward)")
+        packed_t = None  # fp32 layers and row-major bf16 weights: the backward reads the row-major weights
         if spec.weights_packed:
-            log("[bench] training step (forward + backward)")
             rm = {n: t(getattr(inp, n)) for n in ("w13", "w2", "ws13", "ws2")}
             packed_t = S.pack_transposed_weights(spec, rm)
             del rm
-            rng_b = np.random.default_rng(cfg.seed + 300)
-            dout = t(W.f32_to_bf16_bits(rng_b.standard_normal((cfg.T, cfg.d)).astype(np.float32)))
-            # the training forward keeps the experts' gate / up pre-activations for the backward
-            spec_tr = dataclasses.replace(spec, save_preact=True)
-            ws_tr = torch.empty(S.workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
-            bws_t = torch.empty(S.backward_workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
+        rng_b = np.random.default_rng(cfg.seed + 300)
+        g32 = rng_b.standard_normal((cfg.T, cfg.d)).astype(np.float32)
+        dout = t(W.f32_to_bf16_bits(g32) if cfg.dtype == W.BF16 else g32)
+        # the packed training forward keeps the experts' gate / up pre-activations for the backward
+        spec_tr = dataclasses.replace(spec, save_preact=spec.weights_packed)
+        ws_tr = torch.empty(S.workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
+        bws_t = torch.empty(S.backward_workspace_bytes(spec_tr), dtype=torch.uint8, device=dev)
+        S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
+        grads = S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], workspace=bws_t,
+                               streams=streams)
+        for _ in range(3):
             S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-            grads = S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], workspace=bws_t,
-                                   streams=streams)
-            for _ in range(3):
-                S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-                S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
-                               workspace=bws_t, streams=streams)
-            tr_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-            f_ms, b_ms = [], []
-            for _ in range(args.steps):
-                tr_ev[0].record()
-                S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
-                tr_ev[1].record()
-                S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
-                               workspace=bws_t, streams=streams)
-                tr_ev[2].record()
-                torch.cuda.synchronize()
-                f_ms.append(tr_ev[0].elapsed_time(tr_ev[1]))
-                b_ms.append(tr_ev[1].elapsed_time(tr_ev[2]))
-            fm, bm = float(np.median(f_ms)), float(np.median(b_ms))
-            R = cfg.T * cfg.k
-            # dgrad (dH, dX) and wgrad (dW2, dW13): 12 d inter flops per routed row and per token for the
-            # shared block; the recompute of the gate / up pre-activations adds 4 more
-            bwd_flops = 12.0 * cfg.d * (R * cfg.inter + cfg.T * cfg.shared_inter)
-            line["extra"]["training_step"] = {
-                "what": "forward keeping the experts' gate / up pre-activations + backward of the layer (all "
-                        "gradients; MI gradient added to the logit gradient)",
-                "ms": round(fm + bm, 5), "forward_ms": round(fm, 5), "backward_ms": round(bm, 5),
-                "tokens_per_s": round(cfg.T / ((fm + bm) * 1e-3), 1),
-                "backward_tflops": round(bwd_flops / (bm * 1e-3) / 1e12, 2),
-                "backward_frac_mfma": round(bwd_flops / (bm * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
-            del packed_t, grads, bws_t, ws_tr
+            S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
+                           workspace=bws_t, streams=streams)
+        tr_ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        f_ms, b_ms = [], []
+        for _ in range(args.steps):
+            tr_ev[0].record()
+            S.moe_forward(spec_tr, dev_in, outs, ws_tr, streams=streams)
+            tr_ev[1].record()
+            S.moe_backward(spec_tr, dev_in, outs, ws_tr, packed_t, dout, outs["dlogits"], grads=grads,
+                           workspace=bws_t, streams=streams)
+            tr_ev[2].record()
+            torch.cuda.synchronize()
+            f_ms.append(tr_ev[0].elapsed_time(tr_ev[1]))
+            b_ms.append(tr_ev[1].elapsed_time(tr_ev[2]))
+        fm, bm = float(np.median(f_ms)), float(np.median(b_ms))
+        R = cfg.T * cfg.k
+        # dgrad (dH, dX) and wgrad (dW2, dW13): 12 d inter flops per routed row and per token for the
+        # shared block; the recompute of the gate / up pre-activations adds 4 more
+        bwd_flops = 12.0 * cfg.d * (R * cfg.inter + cfg.T * cfg.shared_inter)
+        bwd_peak = PEAK_BF16_TFLOPS if spec.weights_packed else PEAK_FP32_TFLOPS
+        line["extra"]["training_step"] = {
+            "what": ("forward keeping the experts' gate / up pre-activations" if spec.weights_packed
+                     else "forward") + " + backward of the layer (all gradients; MI gradient added to the "
+                    "logit gradient)",
+            "ms": round(fm + bm, 5), "forward_ms": round(fm, 5), "backward_ms": round(bm, 5),
+            "tokens_per_s": round(cfg.T / ((fm + bm) * 1e-3), 1),
+            "backward_tflops": round(bwd_flops / (bm * 1e-3) / 1e12, 2),
+            # the packed path's matrix cores against the dense bf16 peak; the float32
+            # FMA path (fp32 layers, row-major bf16 weights) against the fp32 vector peak
+            "backward_peak_tflops": bwd_peak,
+            "backward_frac_peak": round(bwd_flops / (bm * 1e-3) / 1e12 / bwd_peak, 4)}
+        del packed_t, grads, bws_t, ws_tr
     if not args.no_cpu_baseline:
         n_cpu = args.cpu_samples if args.cpu_samples is not None else (1 if cfg.d >= 4096 else 2)
         log(f"[bench] CPU oracle on {n_cpu} sample(s)")
