@@ -485,6 +485,14 @@ typedef struct smoes_layer_grads {
     void* dws2;      /* [d, shared_inter] act_dtype                              */
 } smoes_layer_grads;
 
+/*
+ * Bytes of the backward's workspace for desc (0 for an invalid desc): the
+ * recomputed pre-activations and their gradients, each routed row's input
+ * gradient and w H, and for bf16 layers with packed weights the k-packed
+ * copies of the weight-gradient operands (each expert's rows padded to 16;
+ * about 2.2 GB at T = 16384, d = 4096, 160 experts of inter 1536, top-6, two
+ * shared experts). Host arithmetic only.
+ */
 size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
 
 /*
@@ -512,7 +520,9 @@ size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
  * step on `stream` (io->streams is not used there). The expert weight
  * gradients are in act_dtype; dx, dw_gate and the logit gradient float32.
  * SMOES_ERR_SHAPE (packed path) when 4 T k inter or 4 T shared_inter exceeds
- * INT32_MAX bytes; SMOES_ERR_WORKSPACE when either workspace is NULL or
+ * INT32_MAX bytes, or a k-packed operand copy (2 (T k + 15 E) max(d, 2 inter)
+ * bytes, or 2 T max(d, 2 shared_inter) for the shared experts) would;
+ * SMOES_ERR_WORKSPACE when either workspace is NULL or
  * smaller than smoes_workspace_bytes / smoes_backward_workspace_bytes;
  * SMOES_ERR_ARG for a NULL pointer that is needed. Differentiates the layer
  * output of Sec. 3.1 (softmax router, top-k combine, SwiGLU experts plus the
