@@ -489,9 +489,10 @@ typedef struct smoes_layer_grads {
  * Bytes of the backward's workspace for desc (0 for an invalid desc): the
  * recomputed pre-activations and their gradients, each routed row's input
  * gradient and w H, and for bf16 layers with packed weights the k-packed
- * copies of the weight-gradient operands (each expert's rows padded to 16;
- * about 2.2 GB at T = 16384, d = 4096, 160 experts of inter 1536, top-6, two
- * shared experts). Host arithmetic only.
+ * copies of the weight-gradient operands (each expert's rows padded to 16).
+ * At T = 16384, d = 4096, 160 experts of inter 1536, top-6 and two shared
+ * experts the copies take 2.2 GB and the whole workspace 4.4 GB (5.2 GB when
+ * the forward did not keep the pre-activations). Host arithmetic only.
  */
 size_t smoes_backward_workspace_bytes(const smoes_layer* desc);
 
