@@ -546,6 +546,7 @@ struct BwdWs {
     // k-packed weight-gradient operands (packed bf16 path): routed rows (dout,
     // then x, gathered), w H, [dA dB]; the same for the shared experts' tokens
     int32_t* kp;
+    int32_t* ranges;  // [2][9] XCD tile ranges of the two routed weight-gradient launches
     void* pt_rows_r;
     void* pt_wh_r;
     void* pt_dab_r;
@@ -578,6 +579,7 @@ size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E));
     const int64_t kr = gen ? 0 : kpad_routed(L), ksh = gen || L->shared_inter == 0 ? 0 : kpad_shared(L);
     w.kp = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * (L->E + 1)));
+    w.ranges = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * 18));
     w.pt_rows_r = c.take(2 * kpack_elems(L->d, kr));
     w.pt_wh_r = c.take(2 * kpack_elems(L->inter, kr));
     w.pt_dab_r = c.take(2 * kpack_elems(2 * L->inter, kr));
@@ -744,10 +746,10 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
         const int64_t ksh = kpad_shared(L);
         SMOES_BTRY(launch_kpack(dout, d, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_rows_s, c));
         SMOES_BTRY(launch_kpack(fb.h_s, SI, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_h_s, c));
-        SMOES_BTRY(launch_wgrad_pk(1, d, SI, nullptr, T, bw.pt_rows_s, bw.pt_h_s, G->dws2, c));
+        SMOES_BTRY(launch_wgrad_pk(1, d, SI, nullptr, nullptr, T, bw.pt_rows_s, bw.pt_h_s, G->dws2, c));
         SMOES_BTRY(launch_kpack(bw.dab_s, 2 * SI, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_dab_s, c));
         SMOES_BTRY(launch_kpack(io->x, d, nullptr, nullptr, nullptr, 1, T, ksh, bw.pt_rows_s, c));
-        SMOES_BTRY(launch_wgrad_pk(1, 2 * SI, d, nullptr, T, bw.pt_dab_s, bw.pt_rows_s, G->dws13, c));
+        SMOES_BTRY(launch_wgrad_pk(1, 2 * SI, d, nullptr, nullptr, T, bw.pt_dab_s, bw.pt_rows_s, G->dws13, c));
     }
     if (sides != nullptr) SMOES_BTRY(hipEventRecord(e_join, c));
     // routed chain
@@ -757,13 +759,14 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     // dW2 = dout^T (w H) over each expert's rows (dout gathered); dW13 = [dA dB]^T X (x
     // gathered): both operands k-packed per expert first (rows padded to 16)
     const int64_t kr = kpad_routed(L);
-    SMOES_BTRY(launch_kpad_offsets(offsets, L->E, bw.kp, s));
+    SMOES_BTRY(launch_kpad_offsets(offsets, L->E, bw.kp, wgrad_tiles_per_group(d, I), wgrad_tiles_per_group(2 * I, d),
+                                   bw.ranges, s));
     SMOES_BTRY(launch_kpack(dout, d, perm_token, offsets, bw.kp, L->E, T, kr, bw.pt_rows_r, s));
     SMOES_BTRY(launch_kpack(bw.wh_r, I, nullptr, offsets, bw.kp, L->E, T, kr, bw.pt_wh_r, s));
-    SMOES_BTRY(launch_wgrad_pk(L->E, d, I, bw.kp, T, bw.pt_rows_r, bw.pt_wh_r, G->dw2, s));
+    SMOES_BTRY(launch_wgrad_pk(L->E, d, I, bw.kp, bw.ranges, T, bw.pt_rows_r, bw.pt_wh_r, G->dw2, s));
     SMOES_BTRY(launch_kpack(bw.dab_r, 2 * I, nullptr, offsets, bw.kp, L->E, T, kr, bw.pt_dab_r, s));
     SMOES_BTRY(launch_kpack(io->x, d, perm_token, offsets, bw.kp, L->E, T, kr, bw.pt_rows_r, s));
-    SMOES_BTRY(launch_wgrad_pk(L->E, 2 * I, d, bw.kp, T, bw.pt_dab_r, bw.pt_rows_r, G->dw13, s));
+    SMOES_BTRY(launch_wgrad_pk(L->E, 2 * I, d, bw.kp, bw.ranges + 9, T, bw.pt_dab_r, bw.pt_rows_r, G->dw13, s));
     if (sides != nullptr) SMOES_BTRY(hipStreamWaitEvent(s, e_join, 0));
     SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, 1, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
                                 G->dx, s));

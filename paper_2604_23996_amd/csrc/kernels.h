@@ -148,16 +148,22 @@ hipError_t launch_generic_bwd(int step, const ExpertArgs& a, const GenericBwdPtr
 // rows) and the weight gradients from them: kp = padded row prefix of the
 // groups given by off; kpack_elems = elements of a packed copy of C columns.
 int64_t kpack_elems(int C, int64_t padded_rows);
-hipError_t launch_kpad_offsets(const int32_t* off, int E, int32_t* kp, hipStream_t stream);
+// ranges (may be NULL): [2][9] first tiles of the 8 XCDs' work-balanced tile
+// ranges for two launch_wgrad_pk calls over these groups with per0 and per1
+// tiles per group (wgrad_tiles_per_group). 1 <= E <= 256.
+int wgrad_tiles_per_group(int M, int N);
+hipError_t launch_kpad_offsets(const int32_t* off, int E, int32_t* kp, int per0, int per1, int32_t* ranges,
+                               hipStream_t stream);
 // S [.][C] bf16 row-major; group g's rows are off[g] .. off[g + 1] (through map
 // when given); off == NULL: one group of T rows. max_padded_rows bounds kp's
 // total (the grid).
 hipError_t launch_kpack(const void* S, int C, const int32_t* map, const int32_t* off, const int32_t* kp,
                         int n_groups, int64_t T, int64_t max_padded_rows, void* P, hipStream_t stream);
 // out[g][m][n] = sum over group g's rows of A[row][m] B[row][n] (bf16), from the
-// k-packed A (M columns) and B (N columns); kp == NULL: one group of T rows.
-hipError_t launch_wgrad_pk(int n_groups, int M, int N, const int32_t* kp, int64_t T, const void* PA, const void* PB,
-                           void* out, hipStream_t stream);
+// k-packed A (M columns) and B (N columns); kp == NULL: one group of T rows;
+// ranges: 9 entries from launch_kpad_offsets, or NULL: equal tile counts per XCD.
+hipError_t launch_wgrad_pk(int n_groups, int M, int N, const int32_t* kp, const int32_t* ranges, int64_t T,
+                           const void* PA, const void* PB, void* out, hipStream_t stream);
 size_t router_bwd_workspace_bytes(int64_t T, int d, int E);
 hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int64_t T, int k, float* wrow,
                               hipStream_t stream);

@@ -32,11 +32,16 @@ namespace {
 constexpr int KP_COLS = 256;  // source columns per k-pack block (8 column groups)
 
 // Padded row prefix of the routed groups: kp[g + 1] = kp[g] + 16 ceil(rows_g / 16).
+// a weight-gradient tile's fixed cost in 16-row slices: its start and its output
+constexpr int kWpTileCost = 8;
+
 __global__ void __launch_bounds__(256)
-kpad_offsets_kernel(const int32_t* __restrict__ off, int E, int32_t* __restrict__ kp) {
+kpad_offsets_kernel(const int32_t* __restrict__ off, int E, int32_t* __restrict__ kp, int per0, int per1,
+                    int32_t* __restrict__ ranges) {
     __shared__ int32_t sc[256];
     const int g = threadIdx.x;
-    sc[g] = g < E ? ((off[g + 1] - off[g] + 15) / 16) * 16 : 0;
+    const int32_t rows = g < E ? ((off[g + 1] - off[g] + 15) / 16) * 16 : 0;
+    sc[g] = rows;
     __syncthreads();
     for (int o = 1; o < 256; o <<= 1) {  // inclusive scan
         const int32_t v = g >= o ? sc[g - o] : 0;
@@ -46,6 +51,30 @@ kpad_offsets_kernel(const int32_t* __restrict__ off, int E, int32_t* __restrict_
     }
     if (g == 0) kp[0] = 0;
     if (g < E) kp[g + 1] = sc[g];
+    if (ranges == nullptr || g >= E) return;
+    // Tile ranges of the 8 XCDs with equal work for the two weight-gradient
+    // launches (per0 and per1 tiles per group): a tile of group g costs its
+    // 16-row slices plus kWpTileCost for its start and its output, and range
+    // x starts at the first tile whose work ends after x / 8 of the total.
+    // The group holding a boundary writes it.
+    const int64_t w = rows / 16 + kWpTileCost;
+    const int64_t pre = (sc[g] - rows) / 16 + static_cast<int64_t>(kWpTileCost) * g;  // work before g, per tile
+    const int64_t all = sc[E - 1] / 16 + static_cast<int64_t>(kWpTileCost) * E;
+    for (int h = 0; h < 2; ++h) {
+        const int64_t per = h == 0 ? per0 : per1;
+        int32_t* rg = ranges + 9 * h;
+        if (g == 0) {
+            rg[0] = 0;
+            rg[8] = static_cast<int32_t>(per * E);
+        }
+        for (int x = 1; x < 8; ++x) {
+            const int64_t target = per * all * x / 8;
+            if (per * pre <= target && target < per * (pre + w)) {
+                const int64_t o = (target - per * pre + w - 1) / w;
+                rg[x] = static_cast<int32_t>(per * g + (o < per ? o : per));
+            }
+        }
+    }
 }
 
 // One block per (16-row slice of the padded row space, 256 source columns):
@@ -113,22 +142,35 @@ constexpr int WP_LDS = WP_ST * WP_A_BYTES > WP_BM * WP_OP * 2 ? WP_ST * WP_A_BYT
 struct WpArgs {
     int n_groups, M, N;
     const int32_t* kp;   // [n_groups + 1] padded row prefix, or NULL: one group of T rows
+    const int32_t* ranges;  // [9] first tile of each XCD's range (work-balanced), or NULL: equal counts
     int64_t T;
     const uint16_t* PA;  // k-packed m operand (M source columns)
     const uint16_t* PB;  // k-packed n operand (N source columns)
     uint16_t* out;       // [n_groups][M][N] bf16
 };
 
+// Persistent: block (x = blockIdx % 8, seat) runs on XCD x and takes the
+// tiles seat, seat + S, ... of XCD x's range (S blocks per XCD), so the
+// resident blocks of an XCD work on consecutive tiles.
 __global__ void __launch_bounds__(WP_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 wgrad_pk_kernel(WpArgs p) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[WP_LDS];
     const int tiles_m = static_cast<int>(ceil_div(p.M, WP_BM)), tiles_n = static_cast<int>(ceil_div(p.N, WP_TN));
     const int per = tiles_m * tiles_n;
     const int nblk = p.n_groups * per;
-    // the tiles of one group run back to back on one XCD (block b runs on XCD b % 8)
-    const int nb8 = static_cast<int>(ceil_div(nblk, 8));
-    const int b = (blockIdx.x & 7) * nb8 + (blockIdx.x >> 3);
-    if (b >= nblk) return;
+    const int xcd = blockIdx.x & 7, seat = blockIdx.x >> 3, seats = gridDim.x >> 3;
+    int lo, hi;
+    if (p.ranges != nullptr) {
+        lo = p.ranges[xcd];
+        hi = p.ranges[xcd + 1];
+    } else {
+        const int nb8 = static_cast<int>(ceil_div(nblk, 8));
+        lo = xcd * nb8 < nblk ? xcd * nb8 : nblk;
+        hi = lo + nb8 < nblk ? lo + nb8 : nblk;
+    }
+    lo = uniform_int(lo);
+    hi = uniform_int(hi);
+    for (int b = lo + seat; b < hi; b += seats) {
     const int g = b / per, tt = b % per;
     // inside a group: super-rows of 8 m tiles; each n tile's operand slice serves the 8 m tiles
     // of a super-row back to back
@@ -209,7 +251,8 @@ wgrad_pk_kernel(WpArgs p) {
         }
         __builtin_amdgcn_sched_barrier(0);
     };
-    // Loads retire in order: before stage s reads its slot, at most the 12
+    // Vector memory operations retire in order (the previous tile's stores
+    // first): before stage s reads its slot, at most the 12
     // loads issued after the last DMA of stage s (the n fragments of stage s
     // and the DMA of stage s + 1) may still fly; the barrier makes every wave's
     // DMA visible and frees the slot the DMA of stage s + 2 overwrites. Past
@@ -270,14 +313,20 @@ wgrad_pk_kernel(WpArgs p) {
             *reinterpret_cast<uint4*>(O + static_cast<int64_t>(m0 + r) * p.N + n0 + c) =
                 *reinterpret_cast<const uint4*>(ot + r * WP_OP + c);
     }
+    __syncthreads();  // the tile's LDS reads are done before the next tile's DMA
+    }
 }
 
 }  // namespace
 
 int64_t kpack_elems(int C, int64_t padded_rows) { return 32 * ceil_div(C, 32) * padded_rows; }
 
-hipError_t launch_kpad_offsets(const int32_t* off, int E, int32_t* kp, hipStream_t stream) {
-    hipLaunchKernelGGL(kpad_offsets_kernel, dim3(1), dim3(256), 0, stream, off, E, kp);
+int wgrad_tiles_per_group(int M, int N) { return static_cast<int>(ceil_div(M, WP_BM) * ceil_div(N, WP_TN)); }
+
+hipError_t launch_kpad_offsets(const int32_t* off, int E, int32_t* kp, int per0, int per1, int32_t* ranges,
+                               hipStream_t stream) {
+    if (E < 1 || E > 256) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kpad_offsets_kernel, dim3(1), dim3(256), 0, stream, off, E, kp, per0, per1, ranges);
     return hipGetLastError();
 }
 
@@ -291,21 +340,23 @@ hipError_t launch_kpack(const void* S, int C, const int32_t* map, const int32_t*
     return hipGetLastError();
 }
 
-hipError_t launch_wgrad_pk(int n_groups, int M, int N, const int32_t* kp, int64_t T, const void* PA, const void* PB,
-                           void* out, hipStream_t stream) {
+hipError_t launch_wgrad_pk(int n_groups, int M, int N, const int32_t* kp, const int32_t* ranges, int64_t T,
+                           const void* PA, const void* PB, void* out, hipStream_t stream) {
     if (n_groups == 0 || M == 0 || N == 0) return hipSuccess;
     WpArgs p;
     p.n_groups = n_groups;
     p.M = M;
     p.N = N;
     p.kp = kp;
+    p.ranges = ranges;
     p.T = T;
     p.PA = static_cast<const uint16_t*>(PA);
     p.PB = static_cast<const uint16_t*>(PB);
     p.out = static_cast<uint16_t*>(out);
+    // two resident workgroups per CU, 32 CUs per XCD; fewer when there are fewer tiles
     const int64_t nblk = static_cast<int64_t>(n_groups) * ceil_div(M, WP_BM) * ceil_div(N, WP_TN);
-    hipLaunchKernelGGL(wgrad_pk_kernel, dim3(static_cast<unsigned>(8 * ceil_div(nblk, 8))), dim3(WP_THREADS), 0,
-                       stream, p);
+    const int64_t per_xcd = ceil_div(nblk, 8) < 64 ? ceil_div(nblk, 8) : 64;
+    hipLaunchKernelGGL(wgrad_pk_kernel, dim3(static_cast<unsigned>(8 * per_xcd)), dim3(WP_THREADS), 0, stream, p);
     return hipGetLastError();
 }
 
