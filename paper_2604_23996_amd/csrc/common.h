@@ -136,6 +136,7 @@ __host__ __device__ __forceinline__ size_t align_up(size_t v, size_t a) { return
 // Raw buffer descriptors (gfx9 word 3) and an offset that is always past the record count.
 constexpr int kBufferFlags = 0x00020000;
 constexpr int kOutOfRange = 0x7fffffff;
+constexpr int kBufferNonTemporal = 2;  // cache-policy operand of a buffer access: streaming (nt)
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 
 // s_waitcnt with vmcnt(N) and lgkmcnt(0) (gfx9 encoding; expcnt left free)

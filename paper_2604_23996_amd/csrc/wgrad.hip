@@ -137,7 +137,9 @@ kpack_kernel(const uint16_t* __restrict__ S, int C, const int32_t* __restrict__ 
 constexpr int WP_BM = 128, WP_TN = 256, WP_BK = 64, WP_ST = 3, WP_THREADS = 256;
 constexpr int WP_A_BYTES = WP_BM * WP_BK * 2;  // 16 fragments of 1 KB per stage
 constexpr int WP_OP = WP_TN + 8;               // epilogue row pitch (elements)
-constexpr int WP_LDS = WP_ST * WP_A_BYTES > WP_BM * WP_OP * 2 ? WP_ST * WP_A_BYTES : WP_BM * WP_OP * 2;
+constexpr int WP_EPI = 2 * WP_A_BYTES;         // epilogue staging: past ring slots 0 and 1
+constexpr int WP_LDS = WP_EPI + (WP_BM / 2) * WP_OP * 2;
+static_assert(WP_LDS >= WP_ST * WP_A_BYTES, "the ring fits");
 
 struct WpArgs {
     int n_groups, M, N;
@@ -151,7 +153,11 @@ struct WpArgs {
 
 // Persistent: block (x = blockIdx % 8, seat) runs on XCD x and takes the
 // tiles seat, seat + S, ... of XCD x's range (S blocks per XCD), so the
-// resident blocks of an XCD work on consecutive tiles.
+// resident blocks of an XCD work on consecutive tiles. The first two stages
+// of a block's next tile are requested before the output of the current one
+// is written (staged through LDS past ring slots 0 and 1, half a tile at a
+// time, with buffer stores that every lane issues whatever the bounds), so
+// the next tile's first data arrives while the stores drain.
 __global__ void __launch_bounds__(WP_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 wgrad_pk_kernel(WpArgs p) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[WP_LDS];
@@ -170,53 +176,75 @@ wgrad_pk_kernel(WpArgs p) {
     }
     lo = uniform_int(lo);
     hi = uniform_int(hi);
-    for (int b = lo + seat; b < hi; b += seats) {
-    const int g = b / per, tt = b % per;
-    // inside a group: super-rows of 8 m tiles; each n tile's operand slice serves the 8 m tiles
-    // of a super-row back to back
-    const int sr = tt / (8 * tiles_n), r8 = tt % (8 * tiles_n);
-    const int gm = tiles_m - sr * 8 < 8 ? tiles_m - sr * 8 : 8;
-    const int m0 = (sr * 8 + r8 % gm) * WP_BM, n0 = (r8 / gm) * WP_TN;
-    const int64_t kp0 = p.kp != nullptr ? p.kp[g] : 0;
-    const int64_t kp1 = p.kp != nullptr ? p.kp[g + 1] : ceil_div(p.T, 16) * 16;
-    const int Ks = uniform_int(static_cast<int>((kp1 - kp0) / 16));  // 16-row slices of the group
+    int b = lo + seat;
+    if (b >= hi) return;
     const int MG = static_cast<int>(ceil_div(p.M, 32)), NG = static_cast<int>(ceil_div(p.N, 32));
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
-    const uint16_t* PAg = p.PA + 32 * static_cast<int64_t>(MG) * kp0;
-    const uint16_t* PBg = p.PB + 32 * static_cast<int64_t>(NG) * kp0;
-    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(uniform_ptr(PAg)), 0, uniform_int(MG * Ks * 1024), kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(uniform_ptr(PBg)), 0, uniform_int(NG * Ks * 1024), kBufferFlags);
-    const int mg0 = m0 / 32 + wave;   // m group this wave's DMA brings in
-    const int ng0 = n0 / 32 + 2 * wave;  // this wave's two n groups
-    // A DMA q of stage s: fragment (m group mg0, slice 4 s + q) into LDS block wave * 4 + q of the slot
-    auto issue_aq = [&](int slot, int s, int q) {
-        const int ks = 4 * s + q;
-        const int vo = (mg0 < MG && ks < Ks) ? ((mg0 * Ks + ks) * 64 + lane) * 16 : kOutOfRange;
-        auto* dst = (__attribute__((address_space(3))) void*)(lds + slot * WP_A_BYTES + (wave * 4 + q) * 1024);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
+    const int half = lane >> 5, l32 = lane & 31;
+
+    // the tile whose operands are being requested: its group, corner and
+    // 16-row slice count, the operand descriptors, and this lane's byte
+    // offsets of slice 0 of its m fragment and its two n fragments (out of
+    // range past the matrix edge)
+    struct Tile {
+        int g, m0, n0, Ks, va, vb0, vb1;
+        i32x4_t rsA;
+        __amdgpu_buffer_rsrc_t rsB;
     };
-    // the two n fragments of slice 4 s + j
-    auto issue_bj = [&](i32x4_t (&bq)[4][2], int s, int j) {
+    auto decode = [&](int bb) {
+        Tile t;
+        t.g = bb / per;
+        const int tt = bb % per;
+        // inside a group: super-rows of 8 m tiles; each n tile's operand slice serves the 8 m tiles
+        // of a super-row back to back
+        const int sr = tt / (8 * tiles_n), r8 = tt % (8 * tiles_n);
+        const int gm = tiles_m - sr * 8 < 8 ? tiles_m - sr * 8 : 8;
+        t.m0 = (sr * 8 + r8 % gm) * WP_BM;
+        t.n0 = (r8 / gm) * WP_TN;
+        const int64_t kp0 = p.kp != nullptr ? p.kp[t.g] : 0;
+        const int64_t kp1 = p.kp != nullptr ? p.kp[t.g + 1] : ceil_div(p.T, 16) * 16;
+        t.Ks = uniform_int(static_cast<int>((kp1 - kp0) / 16));  // 16-row slices of the group
+        const uint16_t* PAg = p.PA + 32 * static_cast<int64_t>(MG) * kp0;
+        const uint16_t* PBg = p.PB + 32 * static_cast<int64_t>(NG) * kp0;
+        t.rsA = buf_rsrc(PAg, MG * t.Ks * 1024);
+        t.rsB = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(uniform_ptr(PBg)), 0,
+                                                  uniform_int(NG * t.Ks * 1024), kBufferFlags);
+        const int mg = t.m0 / 32 + wave, ng = t.n0 / 32 + 2 * wave;
+        t.va = mg < MG ? (mg * t.Ks * 64 + lane) * 16 : kOutOfRange;
+        t.vb0 = ng < NG ? (ng * t.Ks * 64 + lane) * 16 : kOutOfRange;
+        t.vb1 = ng + 1 < NG ? ((ng + 1) * t.Ks * 64 + lane) * 16 : kOutOfRange;
+        return t;
+    };
+    const uint32_t lds_base = lds_address(lds);
+    // A DMA q of stage s: fragment (m group m0 / 32 + wave, slice 4 s + q) into LDS block wave * 4 + q of the slot
+    auto issue_aq = [&](const Tile& t, int slot, int s, int q) {
+        const int ks = 4 * s + q;
+        const int vo = (t.va + ks * 1024) | (ks < t.Ks ? 0 : kOutOfRange);
+        dma16(t.rsA, vo, lds_base + slot * WP_A_BYTES + (wave * 4 + q) * 1024);
+    };
+    // the two n fragments (n groups n0 / 32 + 2 wave + gg) of slice 4 s + j
+    auto issue_bj = [&](const Tile& t, i32x4_t (&bq)[4][2], int s, int j) {
         const int ks = 4 * s + j;
+        const int past = ks < t.Ks ? 0 : kOutOfRange;
+        bq[j][0] = __builtin_amdgcn_raw_buffer_load_b128(t.rsB, (t.vb0 + ks * 1024) | past, 0, 0);
+        bq[j][1] = __builtin_amdgcn_raw_buffer_load_b128(t.rsB, (t.vb1 + ks * 1024) | past, 0, 0);
+    };
+    i32x4_t b0[4][2], b1[4][2];
+    // stages 0 and 1 of the decoded tile: 16 loads per wave, the 4 DMAs of stage 0 first
+    auto prologue = [&](const Tile& t) {
 #pragma unroll
-        for (int gg = 0; gg < 2; ++gg) {
-            const int ng = ng0 + gg;
-            const int vo = (ng < NG && ks < Ks) ? ((ng * Ks + ks) * 64 + lane) * 16 : kOutOfRange;
-            bq[j][gg] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0);
+        for (int q = 0; q < 4; ++q) issue_aq(t, 0, 0, q);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            issue_bj(t, b0, 0, j);
+            issue_aq(t, 1, 1, j);
         }
     };
     f32x16_t acc[4][2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int gg = 0; gg < 2; ++gg) acc[i][gg] = f32x16_t{};
-    const int half = lane >> 5, l32 = lane & 31;
     // stage s from ring slot `slot`: substep j issues the n fragments of stage
     // s + 1 (2 loads) and the DMA q = j of stage s + 2, reads the m fragments
     // of substep j + 1 and runs 8 MFMAs
-    auto stage_run = [&](int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
+    auto stage_run = [&](const Tile& t, int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
         const uint8_t* base = lds + slot * WP_A_BYTES;
         const int nslot = slot == 0 ? 2 : slot - 1;  // (slot + 2) % 3
         bf16x8_t af[2][4];
@@ -228,8 +256,8 @@ wgrad_pk_kernel(WpArgs p) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             __builtin_amdgcn_sched_barrier(0);
-            issue_bj(bn, s + 1, j);
-            issue_aq(nslot, s + 2, j);
+            issue_bj(t, bn, s + 1, j);
+            issue_aq(t, nslot, s + 2, j);
             if (j < 3) rd(j + 1, af[(j + 1) & 1]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -251,69 +279,106 @@ wgrad_pk_kernel(WpArgs p) {
         }
         __builtin_amdgcn_sched_barrier(0);
     };
-    // Vector memory operations retire in order (the previous tile's stores
-    // first): before stage s reads its slot, at most the 12
-    // loads issued after the last DMA of stage s (the n fragments of stage s
-    // and the DMA of stage s + 1) may still fly; the barrier makes every wave's
-    // DMA visible and frees the slot the DMA of stage s + 2 overwrites. Past
-    // the group's rows every load is out of range and returns zeros, so every
-    // stage issues the same count and the waits stay exact.
-    const int nk = static_cast<int>(ceil_div(Ks, 4));
-    {
-        i32x4_t b0[4][2], b1[4][2];
+    // Vector memory operations retire in order. Before stage s reads its
+    // slot, at most the loads issued after the last DMA of stage s may still
+    // fly: for s >= 2 the 12 of stage s - 1's run (n fragments of stage s,
+    // DMA of stage s + 1); for s = 0 and 1 of every tile but a block's first
+    // also the 16 output stores of the previous tile, issued after this
+    // tile's first two stages were requested. The barrier makes every
+    // wave's DMA visible and frees the slot the DMA of stage s + 2
+    // overwrites. Past the group's rows every load is out of range and
+    // returns zeros, so every stage issues the same count and the waits stay
+    // exact.
+    constexpr int kStoresPerTile = (WP_BM * WP_TN / 8) / WP_THREADS;  // 16-byte stores per lane
+    Tile cur = decode(b);
+    prologue(cur);
+    bool after_stores = false;
+    for (;;) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) issue_aq(0, 0, q);
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            issue_bj(b0, 0, j);
-            issue_aq(1, 1, j);
-        }
-        int s = 0, slot = 0;
-        for (; s + 2 <= nk; s += 2) {
-            wait_vm_lgkm0<12>();
-            __builtin_amdgcn_s_barrier();
-            stage_run(slot, s, b0, b1);
-            slot = slot == 2 ? 0 : slot + 1;
-            wait_vm_lgkm0<12>();
-            __builtin_amdgcn_s_barrier();
-            stage_run(slot, s + 1, b1, b0);
-            slot = slot == 2 ? 0 : slot + 1;
-        }
-        if (s < nk) {
-            wait_vm_lgkm0<12>();
-            __builtin_amdgcn_s_barrier();
-            stage_run(slot, s, b0, b1);
-        }
-    }
-    wait_vm_lgkm0<0>();  // drain: the epilogue reuses the ring
-    __builtin_amdgcn_s_barrier();
-    // element v of lane l of acc[i][gg]: n = 8 (v / 4) + 4 half + v % 4 of n group
-    // ng0 + gg, m = l32 of m group i; four adjacent n go to LDS as 8 bytes,
-    // then whole rows of the tile to memory
-    uint16_t* ot = reinterpret_cast<uint16_t*>(lds);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq)
-#pragma unroll
-            for (int gg = 0; gg < 2; ++gg) {
-                const f32x16_t& a = acc[i][gg];
-                *reinterpret_cast<uint2*>(ot + (i * 32 + l32) * WP_OP + wave * 64 + gg * 32 + 8 * vq + 4 * half) =
-                    make_uint2(static_cast<uint32_t>(f32_to_bf16(a[4 * vq])) |
-                                   (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 1])) << 16),
-                               static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 2])) |
-                                   (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 3])) << 16));
+            for (int gg = 0; gg < 2; ++gg) acc[i][gg] = f32x16_t{};
+        const int nk = static_cast<int>(ceil_div(cur.Ks, 4));
+        {
+            int s = 0, slot = 0;
+            if (nk > 0) {
+                if (after_stores) wait_vm_lgkm0<12 + kStoresPerTile>();
+                else wait_vm_lgkm0<12>();
+                __builtin_amdgcn_s_barrier();
+                stage_run(cur, 0, 0, b0, b1);
             }
-    __syncthreads();
-    uint16_t* O = p.out + static_cast<int64_t>(g) * p.M * p.N;
-    constexpr int CH = WP_TN / 8;
-    for (int q = threadIdx.x; q < WP_BM * CH; q += WP_THREADS) {
-        const int r = q / CH, c = (q % CH) * 8;
-        if (m0 + r < p.M && n0 + c < p.N)  // N % 8 == 0: a chunk is all in or all out
-            *reinterpret_cast<uint4*>(O + static_cast<int64_t>(m0 + r) * p.N + n0 + c) =
-                *reinterpret_cast<const uint4*>(ot + r * WP_OP + c);
-    }
-    __syncthreads();  // the tile's LDS reads are done before the next tile's DMA
+            if (nk > 1) {
+                if (after_stores) wait_vm_lgkm0<12 + kStoresPerTile>();
+                else wait_vm_lgkm0<12>();
+                __builtin_amdgcn_s_barrier();
+                stage_run(cur, 1, 1, b1, b0);
+            }
+            s = 2;
+            slot = 2;
+            for (; s + 2 <= nk; s += 2) {
+                wait_vm_lgkm0<12>();
+                __builtin_amdgcn_s_barrier();
+                stage_run(cur, slot, s, b0, b1);
+                slot = slot == 2 ? 0 : slot + 1;
+                wait_vm_lgkm0<12>();
+                __builtin_amdgcn_s_barrier();
+                stage_run(cur, slot, s + 1, b1, b0);
+                slot = slot == 2 ? 0 : slot + 1;
+            }
+            if (s < nk) {
+                wait_vm_lgkm0<12>();
+                __builtin_amdgcn_s_barrier();
+                stage_run(cur, slot, s, b0, b1);
+            }
+        }
+        wait_vm_lgkm0<0>();  // drain: the next tile's DMA reuses the ring
+        __builtin_amdgcn_s_barrier();
+        // output of this tile, then the next tile's first two stages
+        const int og = cur.g, om0 = cur.m0, on0 = cur.n0;
+        const int nb = b + seats;
+        if (nb < hi) {
+            cur = decode(nb);
+            prologue(cur);
+        }
+        const __amdgpu_buffer_rsrc_t rsO = __builtin_amdgcn_make_buffer_rsrc(
+            uniform_ptr(p.out + static_cast<int64_t>(og) * p.M * p.N), 0, uniform_int(p.M * p.N * 2), kBufferFlags);
+        uint16_t* ot = reinterpret_cast<uint16_t*>(lds + WP_EPI);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            // element v of lane l of acc[i][gg]: n = 8 (v / 4) + 4 half + v % 4 of n group
+            // 2 wave + gg of the tile, m = l32 of m group i; four adjacent n go to LDS as
+            // 8 bytes, then whole rows of the half tile to memory
+#pragma unroll
+            for (int i = 2 * h; i < 2 * h + 2; ++i)
+#pragma unroll
+                for (int vq = 0; vq < 4; ++vq)
+#pragma unroll
+                    for (int gg = 0; gg < 2; ++gg) {
+                        const f32x16_t& a = acc[i][gg];
+                        *reinterpret_cast<uint2*>(ot + ((i - 2 * h) * 32 + l32) * WP_OP + wave * 64 + gg * 32 + 8 * vq +
+                                                  4 * half) =
+                            make_uint2(static_cast<uint32_t>(f32_to_bf16(a[4 * vq])) |
+                                           (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 1])) << 16),
+                                       static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 2])) |
+                                           (static_cast<uint32_t>(f32_to_bf16(a[4 * vq + 3])) << 16));
+                    }
+            __syncthreads();
+            constexpr int CH = WP_TN / 8;
+#pragma unroll
+            for (int u = 0; u < kStoresPerTile / 2; ++u) {
+                const int q = u * WP_THREADS + static_cast<int>(threadIdx.x);
+                const int r = q / CH, c = (q % CH) * 8;
+                const int row = om0 + 64 * h + r, col = on0 + c;
+                // N % 8 == 0: a chunk is all in or all out; out of range the store is dropped
+                const int vo = (row < p.M && col < p.N) ? (row * p.N + col) * 2 : kOutOfRange;
+                __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const i32x4_t*>(ot + r * WP_OP + c), rsO,
+                                                       vo, 0, kBufferNonTemporal);
+            }
+            __syncthreads();  // the half tile's LDS reads are done before the next writes
+        }
+        if (nb >= hi) break;
+        b = nb;
+        after_stores = true;
     }
 }
 
