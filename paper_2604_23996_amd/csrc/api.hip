@@ -576,7 +576,7 @@ size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     w.wh_r = c.take(es * R * L->inter);
     w.wh_s = c.take(gen ? es * T * L->shared_inter : 0);
     w.work4 = static_cast<int32_t*>(c.take(sizeof(int32_t) * (L->E + 2)));
-    w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E));
+    w.router = c.take(router_bwd_workspace_bytes(T, L->d, L->E, L->act_dtype == SMOES_BF16 ? 1 : 0));
     const int64_t kr = gen ? 0 : kpad_routed(L), ksh = gen || L->shared_inter == 0 ? 0 : kpad_shared(L);
     w.kp = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * (L->E + 1)));
     w.ranges = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * 18));

@@ -8,8 +8,12 @@
 //     gradients (MI, bin balance) when given.
 //  dx_gather: dx_j = dz_j W_gate + sum_s dX[inv(j, s)] + dXs_j in float32, in
 //     that order (8 tokens x 1024 columns per block, dz staged in LDS).
-//  dwgate: dW_gate[e][c] = sum_j dz_je x_jc and dbias_e = sum_j dz_je: per
-//     256-token chunk partials, then a chunk-ordered sum.
+//  dwgate: dW_gate[e][c] = sum_j dz_je x_jc and dbias_e = sum_j dz_je. For
+//     bf16 x on the matrix cores: dz is split into three bf16 terms whose sum
+//     is dz exactly (every product with a bf16 x is then exact in float32),
+//     packed in MFMA fragment order; workgroups of 256 columns x up to 160
+//     experts sum token ranges into partials; a range-ordered sum finishes.
+//     float32 x: FMA partials per 256-token chunk, then a chunk-ordered sum.
 #include "common.h"
 #include "kernels.h"
 
@@ -182,24 +186,285 @@ dwgate_partial_kernel(const float* __restrict__ dz, const void* __restrict__ x, 
         if (e0 + e < E) part[(chunk * E + e0 + e) * d + c] = acc[e];
 }
 
-__global__ void dwgate_reduce_kernel(const float* __restrict__ part, const float* __restrict__ bpart, int64_t nchunk,
-                                     int d, int E, float* __restrict__ dw_gate, float* __restrict__ dbias) {
-    const int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
-    if (i < static_cast<int64_t>(E) * d) {
+// dw_gate = sum over the nchunk partials in chunk order (4 consecutive
+// entries per thread, 8 partials in flight). dbias: workgroup b < ceil(E / 32)
+// sums experts 32 b .. 32 b + 31, thread group j over the partials j, j + 8,
+// ..., then the 8 group sums in order. The grid covers both.
+__global__ void __launch_bounds__(256)
+dwgate_reduce_kernel(const float* __restrict__ part, int64_t nchunk, const float* __restrict__ bpart, int64_t nbchunk,
+                     int d, int E, float* __restrict__ dw_gate, float* __restrict__ dbias) {
+    __shared__ float bsum[8][32];
+    if (dbias != nullptr && static_cast<int>(blockIdx.x) * 32 < E) {  // uniform per workgroup
+        const int j = threadIdx.x >> 5, e = blockIdx.x * 32 + (threadIdx.x & 31);
         float acc = 0.0f;
-        for (int64_t ch = 0; ch < nchunk; ++ch) acc += part[ch * E * d + i];
-        dw_gate[i] = acc;
+        if (e < E) {
+            int64_t ch = j;
+            for (; ch + 24 < nbchunk; ch += 32) {
+                float v[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) v[u] = bpart[(ch + 8 * u) * E + e];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc += v[u];
+            }
+            for (; ch < nbchunk; ch += 8) acc += bpart[ch * E + e];
+        }
+        bsum[j][threadIdx.x & 31] = acc;
+        __syncthreads();
+        if (threadIdx.x < 32 && e < E) {
+            float t = 0.0f;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) t += bsum[q][threadIdx.x];
+            dbias[e] = t;
+        }
     }
-    if (dbias != nullptr && i < E) {
+    const int64_t n = static_cast<int64_t>(E) * d;  // d % 8 == 0: n % 4 == 0
+    const int64_t i = 4 * (blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x);
+    if (i < n) {
+        float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        int64_t ch = 0;
+        for (; ch + 8 <= nchunk; ch += 8) {
+            float4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const float4*>(part + (ch + u) * n + i);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                acc.x += v[u].x;
+                acc.y += v[u].y;
+                acc.z += v[u].z;
+                acc.w += v[u].w;
+            }
+        }
+        for (; ch < nchunk; ++ch) {
+            const float4 v = *reinterpret_cast<const float4*>(part + ch * n + i);
+            acc.x += v.x;
+            acc.y += v.y;
+            acc.z += v.z;
+            acc.w += v.w;
+        }
+        dw_gate[i] = acc.x;  // the caller's array may be only 4-byte aligned
+        dw_gate[i + 1] = acc.y;
+        dw_gate[i + 2] = acc.z;
+        dw_gate[i + 3] = acc.w;
+    }
+}
+
+// ---- dW_gate on the matrix cores (bf16 x)
+//
+// v_mfma_f32_32x32x16_bf16 with A = x (rows: 32 columns of x, contraction:
+// 16 tokens) and B = dz (columns: 32 experts). A wave owns 64 columns as two
+// interleaved tiles (tile q holds the columns c0 + 2 i + q), so each lane
+// builds both A fragments from 8 dword reads (one token each) of x rows kept
+// as rows in LDS. The three dz terms of an expert tile come pre-packed as B
+// fragments. Both operands reach LDS by buffer-to-LDS DMA through a 3-slot
+// ring of one 16-token slice each.
+constexpr int kDgCols = 256;     // columns per workgroup (4 waves x 64)
+constexpr int kDgMaxET = 5;      // 32-expert tiles per workgroup at most
+constexpr int kDgSt = 3;         // ring slots
+constexpr int kDgXPair = 1056;   // LDS bytes per token pair of x: two 512-byte rows + 32 (the two halves of a
+                                 // wave then read disjoint banks)
+constexpr int kDgTerms = 3;
+__host__ __device__ constexpr int dg_slot_bytes(int et) { return et * kDgTerms * 1024 + 8 * kDgXPair; }
+__host__ __device__ constexpr int dg_dmas(int et) { return (et * kDgTerms + 8 + 3) / 4; }  // per wave per slice
+
+// Pz fragment (ks, et, term), lane l: dz[16 ks + 8 (l / 32) + i][32 et + l % 32] term, i < 8 (zero
+// outside T x E). bpart[b][e]: sum of dz over the 64 tokens of slices 4 b .. 4 b + 3.
+__global__ void __launch_bounds__(256)
+dg_pack_kernel(const float* __restrict__ dz, int64_t T, int E, int ETt, int64_t KS, uint16_t* __restrict__ Pz,
+               float* __restrict__ bpart) {
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, sl = threadIdx.x >> 6;
+    const int64_t ks = static_cast<int64_t>(blockIdx.x) * 4 + sl;
+    const int et = blockIdx.y;
+    const int64_t t0 = 16 * ks + 8 * (lane >> 5);
+    const int e = 32 * et + (lane & 31);
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (ks < KS && t0 + i < T && e < E) ? dz[(t0 + i) * E + e] : 0.0f;
+    if (ks < KS) {
+        uint32_t w[kDgTerms][4];
+#pragma unroll
+        for (int i = 0; i < 8; i += 2) {
+            uint16_t h[kDgTerms][2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                float r = v[i + u];
+#pragma unroll
+                for (int term = 0; term < kDgTerms; ++term) {  // r - bf16(r) is exact in float32
+                    h[term][u] = f32_to_bf16(r);
+                    r -= bf16_to_f32(h[term][u]);
+                }
+            }
+#pragma unroll
+            for (int term = 0; term < kDgTerms; ++term)
+                w[term][i / 2] = static_cast<uint32_t>(h[term][0]) | (static_cast<uint32_t>(h[term][1]) << 16);
+        }
+#pragma unroll
+        for (int term = 0; term < kDgTerms; ++term)
+            *reinterpret_cast<uint4*>(Pz + (((ks * ETt + et) * kDgTerms + term) * 64 + lane) * 8) =
+                make_uint4(w[term][0], w[term][1], w[term][2], w[term][3]);
+    }
+    float b = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) b += v[i];
+    red[sl][lane] = b;
+    __syncthreads();
+    if (threadIdx.x < 32 && e < E) {
         float acc = 0.0f;
-        for (int64_t ch = 0; ch < nchunk; ++ch) acc += bpart[ch * E + i];
-        dbias[i] = acc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc += red[q][threadIdx.x] + red[q][threadIdx.x + 32];
+        bpart[static_cast<int64_t>(blockIdx.x) * E + e] = acc;
     }
+}
+
+// Workgroup (column block, token range s, expert group): part[s][e][c] for its 256
+// columns and EG expert tiles over slices s * kps .. min(KS, (s + 1) * kps).
+template <int EG>
+__global__ void __launch_bounds__(256, 2)
+dg_mfma_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ Pz, int64_t T, int d, int E, int ETt,
+               int64_t KS, int kps, float* __restrict__ part) {
+    constexpr int SLOT = dg_slot_bytes(EG), ND = dg_dmas(EG), NF = EG * kDgTerms + 8;
+    constexpr int XOFF = EG * kDgTerms * 1024;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[kDgSt * SLOT + 1024];  // + 1 KB sink for padding DMAs
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
+    const int cb = blockIdx.x, s = blockIdx.y, et0 = blockIdx.z * EG;
+    const int64_t ks0 = static_cast<int64_t>(s) * kps;
+    const int64_t ks1 = ks0 + kps < KS ? ks0 + kps : KS;
+    const int nks = static_cast<int>(ks1 - ks0);
+    const i32x4_t rsX = buf_rsrc(x, static_cast<int>(T * d * 2));
+    const i32x4_t rsZ = buf_rsrc(Pz, static_cast<int>(KS * ETt * kDgTerms * 1024));
+    const uint32_t lds0 = lds_address(lds);
+    const int xcol = cb * kDgCols + (lane & 31) * 8;  // the 8 columns this lane's x DMA moves
+    // the DMAs of slice n (relative to ks0) into ring slot `slot`: wave w moves fragments w, w + 4, ...
+    auto issue = [&](int n, int slot) {
+        const int64_t ks = ks0 + n;
+#pragma unroll
+        for (int i = 0; i < ND; ++i) {
+            const int f = wave + 4 * i;
+            int vo = kOutOfRange;
+            uint32_t dst = lds0 + kDgSt * SLOT;  // sink
+            if (f < EG * kDgTerms) {
+                const int et = et0 + f / kDgTerms;
+                if (ks < ks1 && et < ETt)
+                    vo = static_cast<int>(((ks * ETt + et) * kDgTerms + f % kDgTerms) * 1024) + lane * 16;
+                dst = lds0 + slot * SLOT + f * 1024;
+            } else if (f < NF) {
+                const int pr = f - EG * kDgTerms;  // token pair
+                const int64_t t = 16 * ks + 2 * pr + (lane >> 5);
+                if (ks < ks1 && t < T && xcol < d) vo = static_cast<int>((t * d + xcol) * 2);
+                dst = lds0 + slot * SLOT + XOFF + pr * kDgXPair;
+            }
+            dma16(f < EG * kDgTerms ? rsZ : rsX, vo, dst);
+        }
+    };
+    f32x16_t acc[2][EG];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int et = 0; et < EG; ++et) acc[q][et] = f32x16_t{};
+    issue(0, 0);
+    issue(1, 1);
+    int slot = 0;
+    // Slice n waits for its own DMAs (only slice n + 1's, ND per wave, may fly);
+    // the barrier frees the slot that slice n + 2 then overwrites.
+    for (int n = 0; n < nks; ++n) {
+        wait_vm_lgkm0<ND>();
+        __builtin_amdgcn_s_barrier();
+        issue(n + 2, slot == 0 ? 2 : slot - 1);
+        const uint8_t* base = lds + slot * SLOT;
+        // x: token 8 (lane / 32) + r of the slice, columns c0 + 2 (lane % 32) and + 1
+        uint32_t w[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int tt = 8 * (lane >> 5) + r;
+            w[r] = *reinterpret_cast<const uint32_t*>(base + XOFF + (tt >> 1) * kDgXPair + (tt & 1) * 512 +
+                                                      (wave * 64 + 2 * (lane & 31)) * 2);
+        }
+        bf16x8_t a[2];
+        {
+            uint32_t lo[4], hi[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                lo[r] = (w[2 * r] & 0xffffu) | (w[2 * r + 1] << 16);
+                hi[r] = (w[2 * r] >> 16) | (w[2 * r + 1] & 0xffff0000u);
+            }
+            a[0] = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+            a[1] = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+        }
+#pragma unroll
+        for (int et = 0; et < EG; ++et)
+#pragma unroll
+            for (int term = 0; term < kDgTerms; ++term) {
+                const bf16x8_t bz = *reinterpret_cast<const bf16x8_t*>(base + (et * kDgTerms + term) * 1024 + lane * 16);
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    acc[q][et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q], bz, acc[q][et], 0, 0, 0);
+            }
+        slot = slot == 2 ? 0 : slot + 1;
+    }
+    wait_vm_lgkm0<0>();  // no DMA may still write LDS when the workgroup ends
+    // element v of lane l of acc[q][et]: expert 32 (et0 + et) + l % 32, column c0 + 2 i + q with
+    // i = 8 (v / 4) + 4 (l / 32) + v % 4: for each v / 4 the lane holds 8 consecutive columns
+    const int c0 = cb * kDgCols + wave * 64;
+    float* P = part + static_cast<int64_t>(s) * E * d;
+#pragma unroll
+    for (int et = 0; et < EG; ++et) {
+        const int e = 32 * (et0 + et) + (lane & 31);
+        if (e >= E) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int c = c0 + 16 * g + 8 * (lane >> 5);
+            if (c >= d) continue;  // d % 8 == 0: 8 columns are all in or all out
+            const f32x16_t& u = acc[0][et];
+            const f32x16_t& v = acc[1][et];
+            float4* o = reinterpret_cast<float4*>(P + static_cast<int64_t>(e) * d + c);
+            o[0] = make_float4(u[4 * g], v[4 * g], u[4 * g + 1], v[4 * g + 1]);
+            o[1] = make_float4(u[4 * g + 2], v[4 * g + 2], u[4 * g + 3], v[4 * g + 3]);
+        }
+    }
+}
+
+// workgroups of dwgate_reduce_kernel: 4 entries per thread, and one per 32 experts for dbias
+int64_t dwgate_reduce_blocks(int64_t n, int E) {
+    const int64_t a = ceil_div(n / 4, 256), b = ceil_div(E, 32);
+    return a > b ? a : b;
+}
+
+struct DgGeom {
+    int ETt, G, EG, colb, S, kps;
+    int64_t KS;
+};
+
+// Launch shape of the matrix-core dW_gate: expert tiles split into G groups of
+// at most kDgMaxET, token ranges sized so there are about 512 workgroups.
+DgGeom dg_geom(int64_t T, int d, int E) {
+    DgGeom g;
+    g.ETt = static_cast<int>(ceil_div(E, 32));
+    g.G = static_cast<int>(ceil_div(g.ETt, kDgMaxET));
+    g.EG = static_cast<int>(ceil_div(g.ETt, g.G));
+    g.colb = static_cast<int>(ceil_div(d, kDgCols));
+    g.KS = ceil_div(T, 16);
+    int64_t S = ceil_div(512, static_cast<int64_t>(g.colb) * g.G);
+    S = S < 64 ? S : 64;
+    S = S < g.KS ? S : g.KS;
+    S = S > 1 ? S : 1;
+    g.kps = static_cast<int>(ceil_div(g.KS, S));
+    g.S = static_cast<int>(ceil_div(g.KS, g.kps));
+    return g;
+}
+
+// the packed dz is addressed with 32-bit byte offsets
+bool dg_fits(int64_t T, int E) {
+    return ceil_div(T, 16) * ceil_div(E, 32) * kDgTerms * 1024 <= INT32_MAX;
 }
 
 }  // namespace
 
-size_t router_bwd_workspace_bytes(int64_t T, int d, int E) {
+size_t router_bwd_workspace_bytes(int64_t T, int d, int E, int bf16) {
+    if (bf16 && dg_fits(T, E)) {
+        const DgGeom g = dg_geom(T, d, E);
+        return align_up(sizeof(float) * g.S * E * d, 256) + align_up(sizeof(uint16_t) * g.KS * g.ETt * kDgTerms * 512, 256) +
+               align_up(sizeof(float) * ceil_div(g.KS, 4) * E, 256);
+    }
     const int64_t nchunk = ceil_div(T, kDwChunk);
     return align_up(sizeof(float) * nchunk * E * d, 256) + align_up(sizeof(float) * nchunk * E, 256);
 }
@@ -245,10 +510,38 @@ hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, int bf16, const 
 
 hipError_t launch_dwgate(const float* dz, const void* x, int bf16, int64_t T, int d, int E, float* dw_gate,
                          float* dbias, void* ws, hipStream_t stream) {
+    hipError_t err;
+    const int64_t n = static_cast<int64_t>(E) * d;
+    if (bf16 && dg_fits(T, E)) {
+        const DgGeom g = dg_geom(T, d, E);
+        float* part = static_cast<float*>(ws);
+        uint16_t* Pz = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + align_up(sizeof(float) * g.S * E * d, 256));
+        float* bpart = reinterpret_cast<float*>(reinterpret_cast<char*>(Pz) +
+                                                align_up(sizeof(uint16_t) * g.KS * g.ETt * kDgTerms * 512, 256));
+        const int64_t nb = ceil_div(g.KS, 4);
+        if (g.KS > 0) {
+            hipLaunchKernelGGL(dg_pack_kernel, dim3(static_cast<unsigned>(nb), static_cast<unsigned>(g.ETt)), dim3(256),
+                               0, stream, dz, T, E, g.ETt, g.KS, Pz, bpart);
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+            const dim3 grid(static_cast<unsigned>(g.colb), static_cast<unsigned>(g.S), static_cast<unsigned>(g.G));
+            const uint16_t* xb = static_cast<const uint16_t*>(x);
+            switch (g.EG) {
+                case 1: hipLaunchKernelGGL(dg_mfma_kernel<1>, grid, dim3(256), 0, stream, xb, Pz, T, d, E, g.ETt, g.KS, g.kps, part); break;
+                case 2: hipLaunchKernelGGL(dg_mfma_kernel<2>, grid, dim3(256), 0, stream, xb, Pz, T, d, E, g.ETt, g.KS, g.kps, part); break;
+                case 3: hipLaunchKernelGGL(dg_mfma_kernel<3>, grid, dim3(256), 0, stream, xb, Pz, T, d, E, g.ETt, g.KS, g.kps, part); break;
+                case 4: hipLaunchKernelGGL(dg_mfma_kernel<4>, grid, dim3(256), 0, stream, xb, Pz, T, d, E, g.ETt, g.KS, g.kps, part); break;
+                default: hipLaunchKernelGGL(dg_mfma_kernel<5>, grid, dim3(256), 0, stream, xb, Pz, T, d, E, g.ETt, g.KS, g.kps, part); break;
+            }
+            if ((err = hipGetLastError()) != hipSuccess) return err;
+        }
+        hipLaunchKernelGGL(dwgate_reduce_kernel, dim3(static_cast<unsigned>(dwgate_reduce_blocks(n, E))),
+                           dim3(256), 0, stream, part, static_cast<int64_t>(g.KS > 0 ? g.S : 0), bpart, nb, d, E, dw_gate,
+                           dbias);
+        return hipGetLastError();
+    }
     const int64_t nchunk = ceil_div(T, kDwChunk);
     float* part = static_cast<float*>(ws);
     float* bpart = reinterpret_cast<float*>(static_cast<char*>(ws) + align_up(sizeof(float) * nchunk * E * d, 256));
-    hipError_t err;
     if (nchunk > 0) {
         const dim3 grid(static_cast<unsigned>(ceil_div(d, 256)), static_cast<unsigned>(ceil_div(E, kDwExp)),
                         static_cast<unsigned>(nchunk));
@@ -258,9 +551,8 @@ hipError_t launch_dwgate(const float* dz, const void* x, int bf16, int64_t T, in
             hipLaunchKernelGGL(dwgate_partial_kernel<false>, grid, dim3(256), 0, stream, dz, x, T, d, E, part, bpart);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    const int64_t n = static_cast<int64_t>(E) * d;
-    hipLaunchKernelGGL(dwgate_reduce_kernel, dim3(static_cast<unsigned>(ceil_div(n, 256))), dim3(256), 0, stream, part,
-                       bpart, nchunk, d, E, dw_gate, dbias);
+    hipLaunchKernelGGL(dwgate_reduce_kernel, dim3(static_cast<unsigned>(dwgate_reduce_blocks(n, E))),
+                       dim3(256), 0, stream, part, nchunk, bpart, nchunk, d, E, dw_gate, dbias);
     return hipGetLastError();
 }
 

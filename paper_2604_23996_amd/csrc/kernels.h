@@ -164,7 +164,7 @@ hipError_t launch_kpack(const void* S, int C, const int32_t* map, const int32_t*
 // ranges: 9 entries from launch_kpad_offsets, or NULL: equal tile counts per XCD.
 hipError_t launch_wgrad_pk(int n_groups, int M, int N, const int32_t* kp, const int32_t* ranges, int64_t T,
                            const void* PA, const void* PB, void* out, hipStream_t stream);
-size_t router_bwd_workspace_bytes(int64_t T, int d, int E);
+size_t router_bwd_workspace_bytes(int64_t T, int d, int E, int bf16);  // bf16: x is bf16 (launch_dwgate)
 hipError_t launch_row_weights(const int32_t* perm_inv, const float* topk_w, int64_t T, int k, float* wrow,
                               hipStream_t stream);
 // bf16: dout and y_r (router_bwd), the row gradients dx_r / dx_s (dx_gather), x (dwgate) are
