@@ -547,6 +547,7 @@ struct BwdWs {
     // then x, gathered), w H, [dA dB]; the same for the shared experts' tokens
     int32_t* kp;
     int32_t* ranges;  // [2][9] XCD tile ranges of the two routed weight-gradient launches
+    void* dxg;        // packed W_gate and dz fragments of the input gradient
     void* pt_rows_r;
     void* pt_wh_r;
     void* pt_dab_r;
@@ -580,6 +581,7 @@ size_t bwd_ws_parts(const smoes_layer* L, BwdWs* out, void* base) {
     const int64_t kr = gen ? 0 : kpad_routed(L), ksh = gen || L->shared_inter == 0 ? 0 : kpad_shared(L);
     w.kp = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * (L->E + 1)));
     w.ranges = static_cast<int32_t*>(c.take(gen ? 0 : sizeof(int32_t) * 18));
+    w.dxg = c.take(gen ? 0 : dx_mfma_workspace_bytes(T, L->d, L->E));
     w.pt_rows_r = c.take(2 * kpack_elems(L->d, kr));
     w.pt_wh_r = c.take(2 * kpack_elems(L->inter, kr));
     w.pt_dab_r = c.take(2 * kpack_elems(2 * L->inter, kr));
@@ -696,7 +698,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
         SMOES_BTRY(launch_row_weights(perm_inv, io->topk_w, T, L->k, bw.wrow, s));
         for (int step = 0; step < 5; ++step) SMOES_BTRY(launch_generic_bwd(step, a, gp, s));
         SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, 0, perm_inv, G->dz, io->w_gate, T, L->d, L->E,
-                                    L->k, G->dx, s));
+                                    L->k, G->dx, nullptr, s));
         return SMOES_OK;
     }
     BwdGemmPtrs bp;
@@ -769,7 +771,7 @@ int smoes_moe_backward(const smoes_layer* L, const smoes_layer_io* io, const voi
     SMOES_BTRY(launch_wgrad_pk(L->E, 2 * I, d, bw.kp, bw.ranges + 9, T, bw.pt_dab_r, bw.pt_rows_r, G->dw13, s));
     if (sides != nullptr) SMOES_BTRY(hipStreamWaitEvent(s, e_join, 0));
     SMOES_BTRY(launch_dx_gather(bw.dx_r, sh ? bw.dx_s : nullptr, 1, perm_inv, G->dz, io->w_gate, T, L->d, L->E, L->k,
-                                G->dx, s));
+                                G->dx, bw.dxg, s));
 #undef SMOES_BTRY
     return SMOES_OK;
 }

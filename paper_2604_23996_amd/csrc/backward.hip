@@ -429,6 +429,179 @@ int64_t dwgate_reduce_blocks(int64_t n, int E) {
     return a > b ? a : b;
 }
 
+// ---- dx on the matrix cores (bf16 layers)
+//
+// dx_j = dz_j W_gate + sum_s dX_r[inv(j, s)] + dXs_j: D[c][j] = sum_e
+// W_gate[e][c] dz[j][e] on v_mfma_f32_32x32x16_bf16 with both float32
+// operands split into two bf16 terms (hi * hi + hi * lo + lo * hi: relative
+// error about 2^-16 per product), from fragments packed beforehand. The 64
+// tokens x 256 columns of a workgroup then go through LDS as rows, and the
+// gathered row gradients are added in the order above with whole-row loads.
+constexpr int kDxTerms = 2;
+constexpr int kDxBT = 64;    // tokens per workgroup
+constexpr int kDxBC = 256;   // columns per workgroup (4 waves x 2 tiles of 32)
+constexpr int kDxPitch = kDxBC + 4;  // LDS row pitch in floats
+
+// Fragment (a, ks, term), lane l, element r: src[m * sm + kk * sk] term with
+// m = 32 a + l % 32 < M, kk = 16 ks + 8 (l / 32) + r < K (zero outside).
+__global__ void __launch_bounds__(256)
+frag_pack_kernel(const float* __restrict__ src, int64_t M, int K, int64_t sm, int64_t sk, int KS, int64_t n_frag,
+                 uint16_t* __restrict__ out) {
+    const int64_t q = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;  // (fragment, lane)
+    const int64_t f = q >> 6;
+    if (f >= n_frag) return;
+    const int lane = static_cast<int>(q & 63);
+    const int64_t a = f / KS;
+    const int ks = static_cast<int>(f % KS);
+    const int64_t m = 32 * a + (lane & 31);
+    const int kk0 = 16 * ks + 8 * (lane >> 5);
+    uint32_t w[kDxTerms][4];
+#pragma unroll
+    for (int r = 0; r < 8; r += 2) {
+        uint16_t h[kDxTerms][2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            float v = (m < M && kk0 + r + u < K) ? src[m * sm + static_cast<int64_t>(kk0 + r + u) * sk] : 0.0f;
+#pragma unroll
+            for (int term = 0; term < kDxTerms; ++term) {
+                h[term][u] = f32_to_bf16(v);
+                v -= bf16_to_f32(h[term][u]);
+            }
+        }
+#pragma unroll
+        for (int term = 0; term < kDxTerms; ++term)
+            w[term][r / 2] = static_cast<uint32_t>(h[term][0]) | (static_cast<uint32_t>(h[term][1]) << 16);
+    }
+#pragma unroll
+    for (int term = 0; term < kDxTerms; ++term)
+        *reinterpret_cast<uint4*>(out + ((f * kDxTerms + term) * 64 + lane) * 8) =
+            make_uint4(w[term][0], w[term][1], w[term][2], w[term][3]);
+}
+
+__global__ void __launch_bounds__(256, 2)
+dx_mfma_kernel(const uint16_t* __restrict__ PW, const uint16_t* __restrict__ PZ, int KS, const uint16_t* __restrict__ dx_r,
+               const uint16_t* __restrict__ dx_s, const int32_t* __restrict__ inv, int64_t T, int d, int k,
+               float* __restrict__ dx) {
+    __shared__ __attribute__((aligned(16))) float tile[kDxBT][kDxPitch];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
+    const int64_t tb = blockIdx.x;
+    const int cb = blockIdx.y;
+    const int CT = static_cast<int>(ceil_div(d, 32));
+    const int64_t TT = ceil_div(T, 32);
+    const int ct0 = cb * (kDxBC / 32) + 2 * wave;
+    const int64_t tt0 = 2 * tb;
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) acc[q][u] = f32x16_t{};
+    // D rows: 32 columns of W_gate (A = W_gate^T), D columns: 32 tokens (B = dz^T)
+    for (int ks = 0; ks < KS; ++ks) {
+        bf16x8_t a[2][kDxTerms], b[2][kDxTerms];
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int term = 0; term < kDxTerms; ++term) {
+                const int ct = ct0 + q;
+                a[q][term] = ct < CT ? *reinterpret_cast<const bf16x8_t*>(
+                                           PW + ((static_cast<int64_t>(ct) * KS + ks) * kDxTerms + term) * 512 + lane * 8)
+                                     : bf16x8_t{};
+                const int64_t tt = tt0 + q;
+                b[q][term] = tt < TT ? *reinterpret_cast<const bf16x8_t*>(
+                                           PZ + ((tt * KS + ks) * kDxTerms + term) * 512 + lane * 8)
+                                     : bf16x8_t{};
+            }
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                acc[q][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q][0], b[u][0], acc[q][u], 0, 0, 0);
+                acc[q][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q][0], b[u][1], acc[q][u], 0, 0, 0);
+                acc[q][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q][1], b[u][0], acc[q][u], 0, 0, 0);
+            }
+    }
+    // element v of lane l of acc[q][u]: column 64 wave + 32 q + 8 (v / 4) + 4 (l / 32) + v % 4 of the
+    // workgroup, token 32 u + l % 32
+    const int half = lane >> 5, l32 = lane & 31;
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<float4*>(&tile[32 * u + l32][64 * wave + 32 * q + 8 * g + 4 * half]) =
+                    make_float4(acc[q][u][4 * g], acc[q][u][4 * g + 1], acc[q][u][4 * g + 2], acc[q][u][4 * g + 3]);
+    __syncthreads();
+    // 8 columns of one token per item; 32 threads cover a row
+    constexpr int NIT = kDxBT * (kDxBC / 8) / 256;  // 8 items per thread
+    constexpr int BATCH = 4;
+#pragma unroll
+    for (int p0 = 0; p0 < NIT; p0 += BATCH) {
+        float v[BATCH][8];
+        int64_t j[BATCH];
+        int c[BATCH];
+        bool ok[BATCH];
+#pragma unroll
+        for (int u = 0; u < BATCH; ++u) {
+            const int it = static_cast<int>(threadIdx.x) + 256 * (p0 + u);
+            const int r = it / (kDxBC / 8), ch = it % (kDxBC / 8);
+            j[u] = tb * kDxBT + r;
+            c[u] = cb * kDxBC + 8 * ch;
+            ok[u] = j[u] < T && c[u] < d;  // d % 8 == 0: 8 columns are all in or all out
+            const float4 x0 = *reinterpret_cast<const float4*>(&tile[r][8 * ch]);
+            const float4 x1 = *reinterpret_cast<const float4*>(&tile[r][8 * ch + 4]);
+            v[u][0] = x0.x; v[u][1] = x0.y; v[u][2] = x0.z; v[u][3] = x0.w;
+            v[u][4] = x1.x; v[u][5] = x1.y; v[u][6] = x1.z; v[u][7] = x1.w;
+        }
+        auto add8 = [](float (&acc8)[8], const uint4 w) {
+            acc8[0] += __uint_as_float(w.x << 16);
+            acc8[1] += __uint_as_float(w.x & 0xffff0000u);
+            acc8[2] += __uint_as_float(w.y << 16);
+            acc8[3] += __uint_as_float(w.y & 0xffff0000u);
+            acc8[4] += __uint_as_float(w.z << 16);
+            acc8[5] += __uint_as_float(w.z & 0xffff0000u);
+            acc8[6] += __uint_as_float(w.w << 16);
+            acc8[7] += __uint_as_float(w.w & 0xffff0000u);
+        };
+        // four slots at a time: the row indices, then all their row loads, then the sums in slot order
+        for (int s0 = 0; s0 < k; s0 += 4) {
+            int row[BATCH][4];
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) row[u][q] = (ok[u] && s0 + q < k) ? inv[j[u] * k + s0 + q] : -1;
+            uint4 w[BATCH][4];
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    w[u][q] = row[u][q] >= 0
+                                  ? *reinterpret_cast<const uint4*>(dx_r + static_cast<int64_t>(row[u][q]) * d + c[u])
+                                  : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (s0 + q < k) add8(v[u], w[u][q]);
+        }
+        if (dx_s != nullptr) {
+            uint4 w[BATCH];
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u)
+                w[u] = ok[u] ? *reinterpret_cast<const uint4*>(dx_s + j[u] * d + c[u]) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) add8(v[u], w[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < BATCH; ++u)
+            if (ok[u]) {
+                float4* o = reinterpret_cast<float4*>(dx + j[u] * d + c[u]);
+                o[0] = make_float4(v[u][0], v[u][1], v[u][2], v[u][3]);
+                o[1] = make_float4(v[u][4], v[u][5], v[u][6], v[u][7]);
+            }
+    }
+}
+
 struct DgGeom {
     int ETt, G, EG, colb, S, kps;
     int64_t KS;
@@ -447,7 +620,7 @@ DgGeom dg_geom(int64_t T, int d, int E) {
     S = S < 64 ? S : 64;
     S = S < g.KS ? S : g.KS;
     S = S > 1 ? S : 1;
-    g.kps = static_cast<int>(ceil_div(g.KS, S));
+    g.kps = g.KS > 0 ? static_cast<int>(ceil_div(g.KS, S)) : 1;  // no tokens: S = 0 partial slabs
     g.S = static_cast<int>(ceil_div(g.KS, g.kps));
     return g;
 }
@@ -494,9 +667,36 @@ hipError_t launch_router_bwd(const void* dout, const void* y_r, int bf16, const 
     return hipGetLastError();
 }
 
+size_t dx_mfma_workspace_bytes(int64_t T, int d, int E) {
+    const int64_t KS = ceil_div(E, 16);
+    return align_up(sizeof(uint16_t) * ceil_div(d, 32) * KS * kDxTerms * 512, 256) +
+           align_up(sizeof(uint16_t) * ceil_div(T, 32) * KS * kDxTerms * 512, 256);
+}
+
 hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, int bf16, const int32_t* perm_inv, const float* dz,
-                            const float* w_gate, int64_t T, int d, int E, int k, float* dx, hipStream_t stream) {
+                            const float* w_gate, int64_t T, int d, int E, int k, float* dx, void* ws,
+                            hipStream_t stream) {
     if (T == 0) return hipSuccess;
+    if (bf16 && ws != nullptr) {
+        const int KS = static_cast<int>(ceil_div(E, 16));
+        const int64_t CT = ceil_div(d, 32), TT = ceil_div(T, 32);
+        uint16_t* PW = static_cast<uint16_t*>(ws);
+        uint16_t* PZ = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) +
+                                                   align_up(sizeof(uint16_t) * CT * KS * kDxTerms * 512, 256));
+        hipError_t err;
+        hipLaunchKernelGGL(frag_pack_kernel, dim3(static_cast<unsigned>(ceil_div(CT * KS * 64, 256))), dim3(256), 0,
+                           stream, w_gate, static_cast<int64_t>(d), E, static_cast<int64_t>(1), static_cast<int64_t>(d),
+                           KS, CT * KS, PW);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+        hipLaunchKernelGGL(frag_pack_kernel, dim3(static_cast<unsigned>(ceil_div(TT * KS * 64, 256))), dim3(256), 0,
+                           stream, dz, T, E, static_cast<int64_t>(E), static_cast<int64_t>(1), KS, TT * KS, PZ);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+        const dim3 grid(static_cast<unsigned>(ceil_div(T, kDxBT)), static_cast<unsigned>(ceil_div(d, kDxBC)));
+        hipLaunchKernelGGL(dx_mfma_kernel, grid, dim3(256), 0, stream, PW, PZ, KS,
+                           static_cast<const uint16_t*>(dx_r), static_cast<const uint16_t*>(dx_s), perm_inv, T, d, k,
+                           dx);
+        return hipGetLastError();
+    }
     const dim3 grid(static_cast<unsigned>(ceil_div(T, kDxTok)), static_cast<unsigned>(ceil_div(d, 256 * 4)));
     const size_t lds = sizeof(float) * kDxTok * E;
     if (bf16)

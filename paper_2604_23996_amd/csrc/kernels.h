@@ -173,8 +173,11 @@ hipError_t launch_router_bwd(const void* dout, const void* y_r, int bf16, const 
                              const float* probs, const int32_t* topk_idx, const float* topk_w,
                              const float* dlogits_aux, int64_t T, int d, int E, int k, int renorm, float* dw,
                              float* dz, hipStream_t stream);
+// ws (bf16 only; NULL: the FMA kernel): dx_mfma_workspace_bytes for the packed W_gate and dz fragments
+size_t dx_mfma_workspace_bytes(int64_t T, int d, int E);
 hipError_t launch_dx_gather(const void* dx_r, const void* dx_s, int bf16, const int32_t* perm_inv, const float* dz,
-                            const float* w_gate, int64_t T, int d, int E, int k, float* dx, hipStream_t stream);
+                            const float* w_gate, int64_t T, int d, int E, int k, float* dx, void* ws,
+                            hipStream_t stream);
 hipError_t launch_dwgate(const float* dz, const void* x, int bf16, int64_t T, int d, int E, float* dw_gate,
                          float* dbias, void* ws, hipStream_t stream);
 
