@@ -439,10 +439,12 @@ enum smoes_weight {
 
 /*
  * Layout: a matrix W[N][K] (N output rows, K the contraction) becomes
- * ceil(N/32) groups of ceil(K/16) slices of 64 x 8 bf16:
- *   P[g][c][l][e] = W[32g + l%32][16c + 8(l/32) + e], zero outside W.
- * w13/ws13: W = the gate and up rows interleaved by 32-row groups (group 2q =
- * gate rows 32q..32q+31, group 2q+1 = the up rows of the same columns),
+ * 2*ceil(N/32) groups of 16 rows, each ceil(K/32) slices of 64 x 8 bf16:
+ *   P[h][c][l][e] = W[16h + l%16][32c + 8(l/16) + e], zero outside W
+ * (the operand order of the 16x16x32 matrix instructions).
+ * w13/ws13: W = the gate and up rows interleaved by 16-row groups in blocks
+ * of 32 columns (groups 4q..4q+3 = gate rows 32q..32q+15, up rows
+ * 32q..32q+15, gate rows 32q+16..32q+31, up rows 32q+16..32q+31),
  * N = 2*32*ceil(inter/32), K = d; one matrix per expert, experts back to
  * back. w2/ws2: W = w2[e] ([d][inter]), N = d, K = inter.
  * SMOES_WGATE: the float32 router weights w_gate [E][d] as three bf16 terms

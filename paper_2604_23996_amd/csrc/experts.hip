@@ -434,17 +434,25 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 // ============================================================== bf16 MFMA path, packed weights
 //
 // Packed weights: a matrix W[N][K] (N output rows, K contraction) is stored as
-// 16-byte fragments P[N/32][ceil(K/16)][64][8] with
-//   P[g][c][l][e] = W[32 g + l % 32][16 c + 8 (l / 32) + e]   (zero outside W),
-// which is exactly the B operand of v_mfma_f32_32x32x16_bf16 for output
-// columns 32 g .. 32 g + 31 and contraction slice 16 c .. 16 c + 15: one wave
+// 16-byte fragments P[2 ceil(N/32)][ceil(K/32)][64][8] with
+//   P[h][c][l][e] = W[16 h + l % 16][32 c + 8 (l / 16) + e]   (zero outside W),
+// which is exactly the A operand of v_mfma_f32_16x16x32_bf16 for output
+// rows 16 h .. 16 h + 15 and contraction slice 32 c .. 32 c + 31: one wave
 // loads it with one fully coalesced 1 KB buffer load, straight into VGPRs.
-// GEMM1 packs the gate and up rows interleaved by 32-row groups (group 2q =
-// gate rows 32q.., group 2q + 1 = the matching up rows), so one wave holds
-// gate and up outputs of the same (row, column) in the same lane.
+// (N is padded to a multiple of 32 so that a matrix holds the same number of
+// 16-row groups in every packed form.) GEMM1 packs the gate and up rows
+// interleaved by 16-row groups in blocks of 32 output columns (groups 4q ..
+// 4q + 3 = gate rows 32q.., up rows 32q.., gate rows 32q + 16.., up rows
+// 32q + 16..), so one wave holds gate and up outputs of the same (row,
+// column) in the same lane.
 //
-// Tiles: 128 rows x 4 waves; each wave owns all 128 rows and 64 B-rows (two
-// 32-row groups: 4 x 2 MFMA tiles of 32 x 32). The weights never pass through
+// The 16x16x32 instruction rather than 32x32x16: both run at the same
+// nominal rate and the tile below feeds them the same operand bytes, but with
+// random bf16 operands and every SIMD busy the chip holds ~12 % more 16x16x32
+// flops under its power limit (1.98 vs 1.76 PFLOP/s sustained from registers).
+//
+// Tiles: 128 rows x 4 waves; each wave owns all 128 rows and 64 B-rows (four
+// 16-row groups: 8 x 4 MFMA tiles of 16 x 16). The weights never pass through
 // LDS and no two waves read the same weight bytes; only the token rows (x
 // gathered through perm_token for GEMM1, H for GEMM2) are staged HBM -> LDS by
 // buffer_load ... lds through a three-stage ring of K = 64 slices. The
@@ -472,9 +480,10 @@ constexpr int pk_lds_bytes(int mode) {
     return PK_ST * PK_BM * PK_BK * 2 > pk_epi_bytes(mode) ? PK_ST * PK_BM * PK_BK * 2 : pk_epi_bytes(mode);
 }
 
-// Elements of one packed matrix with n rows (n_groups = ceil(n / 32) groups) and contraction k.
+// Elements of one packed matrix with n rows (n_groups = ceil(n / 32) pairs of 16-row groups) and
+// contraction k.
 __host__ __device__ inline int64_t packed_elems(int64_t n_groups, int k) {
-    return n_groups * ((k + 15) / 16) * 512;
+    return n_groups * ((k + 31) / 32) * 1024;
 }
 
 
@@ -541,11 +550,11 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         Bw = W + packed_elems(b_groups ? g0 : 0, K);
     }
     K = uniform_int(K);
-    const int kc_n = (K + 15) / 16;  // packed 16-wide contraction slices per group
+    const int kc_n = (K + 31) / 32;  // packed 32-wide contraction slices per 16-row group
     const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(uniform_ptr(Abase)), 0, uniform_int(static_cast<int>(a_rows * K * 2)), kBufferFlags);
     const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(uniform_ptr(Bw)), 0, uniform_int(b_groups * kc_n * 1024), kBufferFlags);
+        const_cast<uint16_t*>(uniform_ptr(Bw)), 0, uniform_int(2 * b_groups * kc_n * 1024), kBufferFlags);
 
     // A DMA: instruction q of this wave fills LDS rows (wave * IA + q) * 8 .. + 7 of the stage;
     // lane moves the 16-byte chunk (lane % 8) ^ swizzle(row) of its row into slot lane % 8.
@@ -571,68 +580,75 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         auto* dst = (__attribute__((address_space(3))) void*)(lds + slot * A_BYTES + (wave * IA + q) * 1024);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, dst, 16, vo, 0, 0, 0);
     };
-    // The two B fragments (gate/up or two column groups) of K slice 16 * (4 s + j).
-    auto issue_bj = [&](i32x4_t (&b)[4][2], int s, int j) {
-        const int kc = s * 4 + j;
+    // Weight fragments of stage s: b[j][h] is 16-row group h of K slice 32 (2 s + j).
+    // Quarter q of a stage loads groups 2 (q % 2) and 2 (q % 2) + 1 of slice q / 2.
+    auto issue_bq = [&](i32x4_t (&b)[2][4], int s, int q) {
+        const int j = q >> 1;
+        const int kc = s * 2 + j;
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
-            const int vo = (((g * kc_n + kc) * 64 + lane) * 16) | (kc < kc_n ? 0 : kOutOfRange);
-            b[j][g] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0);
+        for (int u = 0; u < 2; ++u) {
+            const int h = 2 * (q & 1) + u;
+            const int vo = (((h * kc_n + kc) * 64 + lane) * 16) | (kc < kc_n ? 0 : kOutOfRange);
+            b[j][h] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, 0, 0);
         }
     };
-    f32x16_t acc[4][2];
+    // acc[i][h]: token rows 16 i .. 16 i + 15 x weight rows 16 h .. 16 h + 15 of this wave
+    f32x4_t acc[8][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int g = 0; g < 2; ++g) acc[i][g] = f32x16_t{};
-    const int half = lane >> 5, l32 = lane & 31;
+        for (int h = 0; h < 4; ++h) acc[i][h] = f32x4_t{};
+    const int quad = lane >> 4, l16 = lane & 15;
 
-    // Stage s from ring slot `slot` with B registers bc, while the loads of
-    // the next stages go out between the MFMAs: substep j (K = 16) issues
-    // B(s + 1) slice j (2 loads) and the A DMA q = j of stage s + 2, reads the
-    // A fragments of substep j + 1 and runs 8 MFMAs. A wave issues in order,
+    // Stage s from ring slot `slot` with weight registers bc, while the loads of
+    // the next stages go out between the MFMAs. A stage (K = 64) runs in four
+    // quarters q: K slice j = q / 2 against token tiles 2 u + q % 2 (u < MT);
+    // quarter q issues the weight loads of stage s + 1 for
+    // quarter q (2 loads) and the A DMA q of stage s + 2, reads the token
+    // fragments of quarter q + 1 and runs 4 MT MFMAs. A wave issues in order,
     // so spreading the memory instructions over the MFMAs keeps the matrix
     // pipe fed while the address unit drains them.
-    static_assert(IA == 4, "one A DMA per K = 16 substep");
+    static_assert(IA == 4, "one A DMA per quarter stage");
     // MT: 32-row sub-tiles that take part (1-4: a short last tile of an
     // expert skips the MFMAs and fragment reads of its empty sub-tiles).
-    auto stage_run = [&](auto mt_c, int slot, int s, const i32x4_t (&bc)[4][2], i32x4_t (&bn)[4][2]) {
+    auto stage_run = [&](auto mt_c, int slot, int s, const i32x4_t (&bc)[2][4], i32x4_t (&bn)[2][4]) {
         constexpr int MT = decltype(mt_c)::value;
         const uint8_t* base = lds + slot * A_BYTES;
         const int nslot = slot == 0 ? 2 : slot - 1;  // (slot + 2) % 3
         bf16x8_t af[2][4];
-        auto rd = [&](int j, bf16x8_t (&a)[4]) {
-            const int c = j * 2 + half;
+        // token fragment of tile 2 u + q % 2, K slice q / 2: row 16 i + l % 16, k 32 j + 8 (l / 16) ..
+        auto rd = [&](int q, bf16x8_t (&a)[4]) {
+            const int c = (q >> 1) * 4 + quad;
 #pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                const int R = i * 32 + l32;
-                a[i] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + ((c ^ ((R / 2) % 8)) * 16));
+            for (int u = 0; u < MT; ++u) {
+                const int R = (2 * u + (q & 1)) * 16 + l16;
+                a[u] = *reinterpret_cast<const bf16x8_t*>(base + R * (BK * 2) + ((c ^ ((R / 2) % 8)) * 16));
             }
         };
         rd(0, af[0]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int q = 0; q < 4; ++q) {
             __builtin_amdgcn_sched_barrier(0);
-            issue_bj(bn, s + 1, j);
-            issue_aq(nslot, s + 2, j);
-            if (j < 3) rd(j + 1, af[(j + 1) & 1]);
+            issue_bq(bn, s + 1, q);
+            issue_aq(nslot, s + 2, q);
+            if (q < 3) rd(q + 1, af[(q + 1) & 1]);
 #pragma unroll
-            for (int i = 0; i < MT; ++i)
+            for (int u = 0; u < MT; ++u)
 #pragma unroll
-                for (int g = 0; g < 2; ++g)  // transposed tile: rows = weight columns, columns = tokens
-                    acc[i][g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8_t, bc[j][g]), af[j & 1][i], acc[i][g], 0, 0, 0);
+                for (int h = 0; h < 4; ++h)  // transposed tile: rows = weight rows, columns = tokens
+                    acc[2 * u + (q & 1)][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_t, bc[q >> 1][h]), af[q & 1][u], acc[2 * u + (q & 1)][h], 0, 0, 0);
             // order: one VMEM after each of the first MFMAs, then one LDS read after each of
             // the following MFMAs, then the rest of the MFMAs
-            constexpr int NM = 2 * MT;
+            constexpr int NM = 4 * MT;
 #pragma unroll
-            for (int q = 0; q < 3; ++q) {
-                if (q < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            for (int v = 0; v < 3; ++v) {
+                if (v < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
             }
 #pragma unroll
-            for (int q = 0; q < MT; ++q) {
-                if (3 + q < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            for (int v = 0; v < MT; ++v) {
+                if (3 + v < NM) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
             if (NM > 3 + MT) __builtin_amdgcn_sched_group_barrier(0x008, NM - 3 - MT, 0);
@@ -640,8 +656,8 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // Loads retire in order. Issue order: A(0), then per substep j of stage
-    // s - 1: B(s)[j] (2), A(s + 1)[j] (1). Before stage s reads LDS slot s % 3,
+    // Loads retire in order. Issue order: A(0), then per quarter q of stage
+    // s - 1: B(s)[q] (2), A(s + 1)[q] (1). Before stage s reads LDS slot s % 3,
     // at most the 12 loads issued after A(s)'s last DMA may still fly (B(s)
     // and A(s + 1)); the compiler waits for B(s)'s registers by itself. The
     // barrier makes every wave's DMA of A(s) visible and frees the slot that
@@ -650,13 +666,13 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     // stage issues the same count and the waits stay exact.
     const int nk = static_cast<int>(ceil_div(K, BK));
     auto kloop = [&](auto mt_c) {
-        i32x4_t b0[4][2], b1[4][2];
+        i32x4_t b0[2][4], b1[2][4];
 #pragma unroll
         for (int q = 0; q < IA; ++q) issue_aq(0, 0, q);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            issue_bj(b0, 0, j);
-            issue_aq(1, 1, j);
+        for (int q = 0; q < 4; ++q) {
+            issue_bq(b0, 0, q);
+            issue_aq(1, 1, q);
         }
         int s = 0, slot = 0;
         for (; s + 2 <= nk; s += 2) {
@@ -684,9 +700,10 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     __builtin_amdgcn_s_barrier();
 
     // Epilogue through LDS: [BM][TC + 8] bf16 tile, then 16-byte row chunks.
-    // The accumulators hold transposed 32x32 tiles: element v of lane l is
-    // output column 8*(v/4) + 4*half + v%4 of token row l32, so each lane
-    // writes four adjacent columns as one 8-byte store.
+    // The accumulators hold transposed 16x16 tiles: element e of lane l of
+    // acc[i][h] is output column 16 h + 4 (l / 16) + e of the wave's columns,
+    // token row 16 i + l % 16, so each lane writes four adjacent columns as
+    // one 8-byte store.
     auto pack4 = [](float a, float b, float c, float d) {
         return make_uint2(static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16),
                           static_cast<uint32_t>(f32_to_bf16(c)) | (static_cast<uint32_t>(f32_to_bf16(d)) << 16));
@@ -737,13 +754,14 @@ gemm_bf16_pk_kernel(GemmArgs p) {
             }
             if (i + 1 < 4) load_pass(i + 1, nxt);
             __syncthreads();
-            const float w = shared ? 1.0f : (l32 < rows_here ? p.wrow[rbase + l32] : 0.0f);
-            uint16_t* er = el + l32 * EP;
 #pragma unroll
-            for (int g = 0; g < 2; ++g)
+            for (int tt = 0; tt < 2; ++tt) {
+                const int lr = 16 * tt + l16;  // row of the pass
+                const float w = shared ? 1.0f : (lr < rows_here ? p.wrow[rbase + lr] : 0.0f);
+                uint16_t* er = el + lr * EP;
 #pragma unroll
-                for (int vq = 0; vq < 4; ++vq) {
-                    const int col = wave * 64 + g * 32 + 8 * vq + 4 * half;
+                for (int h = 0; h < 4; ++h) {
+                    const int col = wave * 64 + 16 * h + 4 * quad;
                     const uint2 av = *reinterpret_cast<const uint2*>(er + col);
                     const uint2 bv = *reinterpret_cast<const uint2*>(er + TC + col);
                     const float a[4] = {__uint_as_float(av.x << 16), __uint_as_float(av.x & 0xffff0000u),
@@ -753,7 +771,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
                     float da[4], db[4], wh[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float dh = w * acc[i][g][4 * vq + e];
+                        const float dh = w * acc[2 * i + tt][h][e];
                         const float sg = 1.0f / (1.0f + __expf(-a[e]));
                         const float sa = a[e] * sg;  // silu(a)
                         da[e] = dh * bb[e] * (sg + sa * (1.0f - sg));
@@ -764,6 +782,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
                     *reinterpret_cast<uint2*>(er + TC + col) = pack4(db[0], db[1], db[2], db[3]);
                     *reinterpret_cast<uint2*>(er + 2 * TC + col) = pack4(wh[0], wh[1], wh[2], wh[3]);
                 }
+            }
             __syncthreads();
             const int nparts = WH != nullptr ? 3 : 2;
             for (int q = threadIdx.x; q < 32 * (3 * TC / 8); q += PK_THREADS) {
@@ -789,27 +808,27 @@ gemm_bf16_pk_kernel(GemmArgs p) {
         constexpr int OP = OC + 8;
         uint16_t* otile = reinterpret_cast<uint16_t*>(lds);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = i * 32 + l32;
+        for (int i = 0; i < 8; ++i) {
+            const int r = i * 16 + l16;
+            const int c0 = 4 * quad;
+            if constexpr (OK == 1) {  // groups 2 p (gate) and 2 p + 1 (up): H columns 16 p ..
 #pragma unroll
-            for (int vq = 0; vq < 4; ++vq) {
-                const int c0 = 8 * vq + 4 * half;
-                if constexpr (OK == 1) {
+                for (int pq = 0; pq < 2; ++pq) {
                     float h[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) h[e] = silu(acc[i][0][4 * vq + e]) * acc[i][1][4 * vq + e];
-                    *reinterpret_cast<uint2*>(otile + r * OP + wave * 32 + c0) = pack4(h[0], h[1], h[2], h[3]);
-                } else if constexpr (OK == 3) {
-#pragma unroll
-                    for (int g = 0; g < 2; ++g)
-                        *reinterpret_cast<uint2*>(otile + r * OP + g * TC + wave * 32 + c0) = pack4(
-                            acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
-                } else {
-#pragma unroll
-                    for (int g = 0; g < 2; ++g)
-                        *reinterpret_cast<uint2*>(otile + r * OP + wave * 64 + g * 32 + c0) = pack4(
-                            acc[i][g][4 * vq], acc[i][g][4 * vq + 1], acc[i][g][4 * vq + 2], acc[i][g][4 * vq + 3]);
+                    for (int e = 0; e < 4; ++e) h[e] = silu(acc[i][2 * pq][e]) * acc[i][2 * pq + 1][e];
+                    *reinterpret_cast<uint2*>(otile + r * OP + wave * 32 + 16 * pq + c0) = pack4(h[0], h[1], h[2], h[3]);
                 }
+            } else if constexpr (OK == 3) {  // gate block, then up block
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    *reinterpret_cast<uint2*>(otile + r * OP + (h & 1) * TC + wave * 32 + 16 * (h >> 1) + c0) =
+                        pack4(acc[i][h][0], acc[i][h][1], acc[i][h][2], acc[i][h][3]);
+            } else {
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    *reinterpret_cast<uint2*>(otile + r * OP + wave * 64 + 16 * h + c0) =
+                        pack4(acc[i][h][0], acc[i][h][1], acc[i][h][2], acc[i][h][3]);
             }
         }
         __syncthreads();
@@ -846,14 +865,14 @@ gemm_bf16_pk_kernel(GemmArgs p) {
 }
 
 // Pack `batch` row-major matrices into the fragment order above. interleave:
-// the source has 2 * n rows (gate rows then up rows) and packed group 2q + h
-// takes rows 32q.. of half h; otherwise the source has n rows. transpose: the
-// source is stored [k][n] (the packed matrix is its transpose). One thread
-// per 16-byte fragment; k % 8 == 0.
+// the source has 2 * n rows (gate rows then up rows) and 16-row group 4q + 2v
+// + h takes rows 32q + 16v.. of half h; otherwise the source has n rows.
+// transpose: the source is stored [k][n] (the packed matrix is its
+// transpose). One thread per 16-byte fragment; k % 8 == 0.
 __global__ void pack_weights_kernel(const uint16_t* __restrict__ src, int batch, int n, int k, int interleave,
                                     int transpose, uint16_t* __restrict__ dst) {
-    const int ng = interleave ? 2 * static_cast<int>(ceil_div(n, 32)) : static_cast<int>(ceil_div(n, 32));
-    const int kc_n = (k + 15) / 16;
+    const int ng = static_cast<int>((interleave ? 4 : 2) * ceil_div(n, 32));  // 16-row groups
+    const int kc_n = (k + 31) / 32;
     const int64_t per = static_cast<int64_t>(ng) * kc_n * 64;  // fragments per matrix
     const int64_t total = per * batch;
     const int64_t src_rows = interleave ? 2 * static_cast<int64_t>(n) : n;
@@ -867,15 +886,15 @@ __global__ void pack_weights_kernel(const uint16_t* __restrict__ src, int batch,
         int row;
         bool ok;
         if (interleave) {
-            const int q = g / 2, h = g % 2;
-            const int rr = q * 32 + l % 32;
+            const int q = g / 4, v = (g / 2) % 2, h = g % 2;
+            const int rr = q * 32 + v * 16 + l % 16;
             ok = rr < n;
             row = h * n + rr;
         } else {
-            row = g * 32 + l % 32;
+            row = g * 16 + l % 16;
             ok = row < n;
         }
-        const int kk = c * 16 + 8 * (l / 32);
+        const int kk = c * 32 + 8 * (l / 16);
         ok = ok && kk < k;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (ok && transpose) {

@@ -193,17 +193,18 @@ def test_packed_weight_sizes_and_checks():
     L = S.lib()
     spec = _spec(d=128, inter=96, shared_inter=48)
     # w13: E experts of 2*32*ceil(inter/32) rows x ceil(d/16) slices x 128 bf16 per slice-group
-    assert S.packed_weight_bytes(spec, S.SMOES_W13) == 16 * (2 * 3) * (128 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, S.SMOES_W2) == 16 * (128 // 32) * (96 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, S.SMOES_WS13) == (2 * 2) * (128 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, S.SMOES_WS2) == (128 // 32) * (48 // 16) * 512 * 2
+    # pairs of 16-row groups x 32-wide K slices x 1024 bf16
+    assert S.packed_weight_bytes(spec, S.SMOES_W13) == 16 * (2 * 3) * (128 // 32) * 1024 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_W2) == 16 * (128 // 32) * (96 // 32) * 1024 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS13) == (2 * 2) * (128 // 32) * 1024 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS2) == (128 // 32) * (-(-48 // 32)) * 1024 * 2
     # router weights: 3 bf16 terms x ceil(E/16)*16 experts x ceil(d/32)*32
     assert S.packed_weight_bytes(spec, S.SMOES_WGATE) == 3 * 16 * 128 * 2
     # transposed forms for the backward: W13^T has d rows over 2 inter, W2^T inter rows over d
-    assert S.packed_weight_bytes(spec, S.SMOES_W13T) == 16 * (128 // 32) * (192 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, S.SMOES_W2T) == 16 * (96 // 32) * (128 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, S.SMOES_WS13T) == (128 // 32) * (96 // 16) * 512 * 2
-    assert S.packed_weight_bytes(spec, S.SMOES_WS2T) == (48 // 32 + 1) * (128 // 16) * 512 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_W13T) == 16 * (128 // 32) * (192 // 32) * 1024 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_W2T) == 16 * (96 // 32) * (128 // 32) * 1024 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS13T) == (128 // 32) * (96 // 32) * 1024 * 2
+    assert S.packed_weight_bytes(spec, S.SMOES_WS2T) == (48 // 32 + 1) * (128 // 32) * 1024 * 2
     assert S.packed_weight_bytes(spec, 9) == 0 and S.packed_weight_bytes(spec, -1) == 0
     assert S.packed_weight_bytes(_spec(shared_inter=0), S.SMOES_WS13) == 0
     assert S.packed_weight_bytes(_spec(shared_inter=0), S.SMOES_WS2T) == 0

@@ -390,18 +390,24 @@ def test_layer_small_rowmajor_weights(layer):
 
 @pytest.mark.parametrize("layer", [i for i, L in enumerate(SMALL_LAYERS) if L["dtype"] == W.BF16])
 def test_packed_weights_match_rowmajor(layer):
-    """Both bf16 GEMM paths feed the matrix cores the same operands in the
-    same K order, so the outputs agree bit for bit."""
+    """The packed path (16x16x32 matrix instructions) and the row-major path
+    (32x32x16) multiply the same bf16 operands and differ only in the order of
+    their float32 accumulation, so the outputs agree to a few bf16 roundings."""
     cfg = W.small_config(seed=100 + layer, **dict(SMALL_LAYERS[layer]))
     inp = W.make_layer_inputs(cfg)
     _, _, a = run_gpu_layer(inp, packed=True)
     _, _, b = run_gpu_layer(inp, packed=False)
-    assert torch.equal(a["out"], b["out"])
+    a, b = a["out"].float().cpu(), b["out"].float().cpu()
+    assert torch.all(torch.isfinite(a))
+    assert float((a - b).norm() / b.norm()) <= 4e-3
+    assert torch.all((a - b).abs() <= 2.0 ** -6 * b.abs() + 1e-3)
 
 
 def _pack_reference(w, n, k, interleave):
-    """The packed layout written out with numpy: P[g][c][l][e] =
-    W[32g + l%32][16c + 8(l/32) + e], gate/up interleaved by 32-row groups."""
+    """The packed layout written out with numpy: P[h][c][l][e] =
+    W[16h + l%16][32c + 8(l/16) + e], rows padded to a multiple of 32; gate
+    and up interleaved by 16-row groups in blocks of 32 columns (gate rows
+    32q.., up rows 32q.., gate rows 32q+16.., up rows 32q+16..)."""
     batch = w.shape[0]
     rows = w.reshape(batch, -1, k)
     if interleave:
@@ -410,18 +416,18 @@ def _pack_reference(w, n, k, interleave):
         up = np.zeros((batch, ip, k), w.dtype)
         gate[:, :n] = rows[:, :n]
         up[:, :n] = rows[:, n:]
-        src = np.stack([gate.reshape(batch, ip // 32, 32, k), up.reshape(batch, ip // 32, 32, k)], axis=2)
+        src = np.stack([gate.reshape(batch, ip // 32, 2, 16, k), up.reshape(batch, ip // 32, 2, 16, k)], axis=3)
         src = src.reshape(batch, 2 * ip, k)
     else:
         np_ = -(-n // 32) * 32
         src = np.zeros((batch, np_, k), w.dtype)
         src[:, :n] = rows
-    kp = -(-k // 16) * 16
+    kp = -(-k // 32) * 32
     full = np.zeros((batch, src.shape[1], kp), w.dtype)
     full[:, :, :k] = src
-    g = full.shape[1] // 32
-    # [b][g][32 rows][kc][2 halves][8] -> [b][g][kc][half][32 rows][8]
-    v = full.reshape(batch, g, 32, kp // 16, 2, 8).transpose(0, 1, 3, 4, 2, 5)
+    g = full.shape[1] // 16
+    # [b][g][16 rows][kc][4 quads][8] -> [b][g][kc][quad][16 rows][8]
+    v = full.reshape(batch, g, 16, kp // 32, 4, 8).transpose(0, 1, 3, 4, 2, 5)
     return v.reshape(-1)
 
 
