@@ -39,10 +39,13 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def stage_work(cfg, T, merged=False):
+def stage_work(cfg, T, merged=False, fused=False):
     """Algorithmic flops and HBM bytes of every stage for T tokens. merged:
     the GEMM1 / GEMM2 stages cover the routed and the shared experts in one
-    launch (the schedule with side streams); the *_shared stages are empty."""
+    launch (the schedule with side streams); the *_shared stages are empty.
+    fused (with merged: bf16 packed layers with shared experts): GEMM2 covers
+    the routed experts only and GEMM2_SHARED is the shared down GEMM with the
+    combine in its epilogue (no shared output to HBM); the combine is empty."""
     s = 2 if cfg.dtype == "bf16" else 4
     d, E, k, I, SI = cfg.d, cfg.E, cfg.k, cfg.inter, cfg.shared_inter
     R = T * k
@@ -59,10 +62,14 @@ def stage_work(cfg, T, merged=False):
         "gemm2_shared": dict(flops=2 * T * SI * d, bytes=(d * SI + T * SI + T * d) * s),
     }
     if merged:
-        for g in ("gemm1", "gemm2"):
+        for g in (("gemm1",) if fused else ("gemm1", "gemm2")):
             sh = w.pop(g + "_shared")
             w[g] = dict(flops=w[g]["flops"] + sh["flops"], bytes=w[g]["bytes"] + sh["bytes"])
             w[g + "_shared"] = dict(flops=0, bytes=0)
+        if fused:
+            w["gemm2_shared"] = dict(flops=2 * T * SI * d + 2 * R * d,
+                                     bytes=(d * SI + T * SI + R * d + T * d) * s + R * 8)
+            w["combine"] = dict(flops=0, bytes=0)
     return w
 
 
@@ -380,13 +387,16 @@ def main():
     for ev in dom_events:
         ev.close()
     work = stage_work(cfg, cfg.T)  # one launch per GEMM part (the serial schedule)
-    work_m = stage_work(cfg, cfg.T, merged=True)  # the timed schedule: routed + shared per GEMM launch
+    # the timed schedule: routed + shared per GEMM launch, or the shared down
+    # GEMM with the combine in its epilogue (bf16 packed layers with shared experts)
+    fused = spec.act_dtype == S.SMOES_BF16 and bool(spec.weights_packed) and cfg.shared_inter > 0
+    work_m = stage_work(cfg, cfg.T, merged=True, fused=fused)
     stages = {}
     for name in S.STAGES:
-        if name.endswith("_shared"):
-            continue  # part of the merged GEMM launches
-        sec = stage_ms[name] * 1e-3
         wk = work_m[name]
+        if wk["flops"] == 0 and wk["bytes"] == 0:
+            continue  # part of the merged GEMM launches (or of the fused combine)
+        sec = stage_ms[name] * 1e-3
         stages[name] = {"ms": round(stage_ms[name], 5),
                         "tflops": round(wk["flops"] / sec / 1e12, 3) if wk["flops"] else 0.0,
                         "gbs": round(wk["bytes"] / sec / 1e9, 1)}

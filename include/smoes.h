@@ -345,7 +345,11 @@ typedef struct smoes_layer_io {
  * and GEMM2 each covering the routed and the shared experts (the two
  * *_SHARED stages are then empty event pairs), MODALITY and then MI (after
  * ROUTE) on side[0]; the caller's stream waits for side[0] before the
- * call's work is complete. */
+ * call's work is complete. Exception, with io->streams and a bf16 layer with
+ * packed weights and shared experts: GEMM2 covers the routed experts only,
+ * then GEMM2_SHARED runs the shared experts' down GEMM with the combine in
+ * its epilogue (COMBINE is an empty pair, and SMOES_BUF_Y_SHARED is not
+ * written); the output has the same bits as the separate combine's. */
 enum smoes_stage {
     SMOES_STAGE_ROUTE = 0,        /* router GEMM + softmax + top-k */
     SMOES_STAGE_MODALITY = 1,     /* statistics update (optional) + modality score */
@@ -384,7 +388,8 @@ enum smoes_buffer {
     SMOES_BUF_H_ROUTED = 0,   /* [T*k, inter] act_dtype: silu(gate) * up of every routed row */
     SMOES_BUF_H_SHARED = 1,   /* [T, shared_inter] act_dtype: the same for the shared experts */
     SMOES_BUF_Y_ROUTED = 2,   /* [T*k, d] act_dtype: expert output of every routed row */
-    SMOES_BUF_Y_SHARED = 3,   /* [T, d] act_dtype: shared experts' output */
+    SMOES_BUF_Y_SHARED = 3,   /* [T, d] act_dtype: shared experts' output (not written when the
+                                 combine runs in the shared GEMM2's epilogue, see smoes_stage) */
     SMOES_BUF_CHECK_FLAGS = 4 /* [1] int32: flag word of check_inputs (SMOES_CHECK_* bits) */
 };
 

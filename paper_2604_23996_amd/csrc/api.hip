@@ -423,8 +423,13 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     // GEMM covers the routed and the shared experts in one launch on s
     // (route -> permute -> GEMM1 -> GEMM2 -> combine): two concurrent GEMM
     // launches slow each other down more than they gain from overlapping.
+    // For bf16 layers with packed weights and shared experts the GEMM2 stage
+    // then runs the routed experts alone and the shared experts' GEMM2 follows
+    // with the combine in its epilogue (the shared output never goes to HBM;
+    // the combine stage is an empty pair).
     const smoes_streams* sides = io->streams;
     const bool merged = sides != nullptr;
+    const bool fuse = merged && L->act_dtype == SMOES_BF16 && L->weights_packed && L->shared_inter > 0;
     hipStream_t b = s;
     hipEvent_t e_fork = nullptr, e_routed = nullptr, e_join = nullptr;
     if (sides != nullptr) {
@@ -467,6 +472,7 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_PERMUTE + 1, s));
     if (merged) {  // the shared stages are part of the merged launches: empty pairs
         for (int st2 : {SMOES_STAGE_GEMM1_SHARED, SMOES_STAGE_GEMM2_SHARED}) {
+            if (fuse && st2 == SMOES_STAGE_GEMM2_SHARED) continue;
             SMOES_TRY(record(ev, 2 * st2, s));
             SMOES_TRY(record(ev, 2 * st2 + 1, s));
         }
@@ -475,11 +481,19 @@ int smoes_moe_forward(const smoes_layer* L, const smoes_layer_io* io, void* work
     SMOES_TRY(launch_experts_gemm1(a, w.experts, merged ? 0 : 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM1 + 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2, s));
-    SMOES_TRY(launch_experts_gemm2(a, w.experts, merged ? 0 : 1, s));
+    SMOES_TRY(launch_experts_gemm2(a, w.experts, merged && !fuse ? 0 : 1, s));
     SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2 + 1, s));
-    SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
-    SMOES_TRY(launch_experts_combine(a, w.experts, s));
-    SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));
+    if (fuse) {
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED, s));
+        SMOES_TRY(launch_experts_gemm2_combine(a, w.experts, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_GEMM2_SHARED + 1, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));
+    } else {
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE, s));
+        SMOES_TRY(launch_experts_combine(a, w.experts, s));
+        SMOES_TRY(record(ev, 2 * SMOES_STAGE_COMBINE + 1, s));
+    }
     if (sides != nullptr) SMOES_TRY(hipStreamWaitEvent(s, e_join, 0));
 #undef SMOES_TRY
     return SMOES_OK;

@@ -182,6 +182,10 @@ struct GemmArgs {
     void* dx_s;         // [T][d] shared experts' input gradient
     const float* wrow;  // [R] combine weight of each routed row
     void* wh_r;         // [R][inter] w H of each routed row (mode 4 output)
+    // shared down GEMM with the combine in its epilogue (mode 7)
+    const int32_t* inv;    // [T][k] routed row of each (token, slot)
+    const float* topk_w;   // [T][k] combine weights
+    void* out;             // [T][d] layer output
 };
 
 // ============================================================== bf16 MFMA path
@@ -466,7 +470,8 @@ constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instruction
 // raw gate and up outputs, 4 dH = dout W2 (rows gathered, scaled by the combine
 // weight) with the SwiGLU backward in the epilogue, 5 dX = [dA dB] W13, and 6
 // GEMM1 writing both H and the gate and up outputs (a forward that keeps them
-// for the backward). Modes 1, 3 and 6 pair gate and up groups (32 H columns
+// for the backward); 7 the shared experts' GEMM2 whose epilogue is the
+// combine (run after the routed GEMM2 has written every routed row). Modes 1, 3 and 6 pair gate and up groups (32 H columns
 // per wave); 2, 4 and 5 give each wave two consecutive 32-column groups.
 constexpr int pk_family(int mode) { return (mode == 1 || mode == 3 || mode == 6) ? 1 : 2; }
 constexpr int pk_tile_cols(int mode) { return pk_family(mode) == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
@@ -832,6 +837,85 @@ gemm_bf16_pk_kernel(GemmArgs p) {
             }
         }
         __syncthreads();
+        if constexpr (OK == 7) {
+            // out_j = sum_s w_js Y_r[inv(j, s)] + Ys_j for the tile's tokens and
+            // columns, in the combine kernel's order (float32, slots in order,
+            // then the bf16 shared row from the tile): two 8-column items per
+            // thread at a time, their row indices, then four row loads each
+            const int kk = p.k;
+            const int32_t* inv = p.inv;
+            const float* tw = p.topk_w;
+            const uint16_t* yr = static_cast<const uint16_t*>(p.y_r);
+            uint16_t* out = static_cast<uint16_t*>(p.out);
+            const int64_t dd = p.d;
+            constexpr int CH = OC / 8;
+            const int col0 = t.nt * TC;
+            for (int q0 = threadIdx.x; q0 < BM * CH; q0 += 2 * PK_THREADS) {
+                int64_t j[2];
+                int c[2], r[2];
+                bool ok[2];
+                float v[2][8];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int q = q0 + u * PK_THREADS;
+                    r[u] = q / CH;
+                    c[u] = col0 + (q % CH) * 8;
+                    j[u] = t.row0 + r[u];
+                    ok[u] = q < BM * CH && r[u] < t.rows && c[u] < n_out;  // d % 8 == 0
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[u][e] = 0.0f;
+                }
+                for (int s0 = 0; s0 < kk; s0 += 4) {
+                    int row[2][4];
+                    float wt[2][4];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+#pragma unroll
+                        for (int sv = 0; sv < 4; ++sv) {
+                            const bool in = ok[u] && s0 + sv < kk;
+                            row[u][sv] = in ? inv[j[u] * kk + s0 + sv] : -1;
+                            wt[u][sv] = in ? tw[j[u] * kk + s0 + sv] : 0.0f;
+                        }
+                    uint4 y[2][4];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+#pragma unroll
+                        for (int sv = 0; sv < 4; ++sv)
+                            y[u][sv] = row[u][sv] >= 0
+                                           ? *reinterpret_cast<const uint4*>(yr + static_cast<int64_t>(row[u][sv]) * dd + c[u])
+                                           : make_uint4(0, 0, 0, 0);
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+#pragma unroll
+                        for (int sv = 0; sv < 4; ++sv) {
+                            if (s0 + sv >= kk) continue;
+                            const uint32_t w4[4] = {y[u][sv].x, y[u][sv].y, y[u][sv].z, y[u][sv].w};
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                v[u][2 * e] = fmaf(wt[u][sv], __uint_as_float(w4[e] << 16), v[u][2 * e]);
+                                v[u][2 * e + 1] = fmaf(wt[u][sv], __uint_as_float(w4[e] & 0xffff0000u), v[u][2 * e + 1]);
+                            }
+                        }
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    if (!ok[u]) continue;
+                    const uint4 ys = *reinterpret_cast<const uint4*>(otile + r[u] * OP + (c[u] - col0));
+                    const uint32_t w4[4] = {ys.x, ys.y, ys.z, ys.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[u][2 * e] += __uint_as_float(w4[e] << 16);
+                        v[u][2 * e + 1] += __uint_as_float(w4[e] & 0xffff0000u);
+                    }
+                    *reinterpret_cast<uint4*>(out + j[u] * dd + c[u]) =
+                        make_uint4(static_cast<uint32_t>(f32_to_bf16(v[u][0])) | (static_cast<uint32_t>(f32_to_bf16(v[u][1])) << 16),
+                                   static_cast<uint32_t>(f32_to_bf16(v[u][2])) | (static_cast<uint32_t>(f32_to_bf16(v[u][3])) << 16),
+                                   static_cast<uint32_t>(f32_to_bf16(v[u][4])) | (static_cast<uint32_t>(f32_to_bf16(v[u][5])) << 16),
+                                   static_cast<uint32_t>(f32_to_bf16(v[u][6])) | (static_cast<uint32_t>(f32_to_bf16(v[u][7])) << 16));
+                }
+            }
+            return;
+        }
         uint16_t* O;
         if constexpr (OK == 1) O = shared ? static_cast<uint16_t*>(p.h_s) : static_cast<uint16_t*>(p.h_r);
         else if constexpr (OK == 3) O = shared ? static_cast<uint16_t*>(p.ab_s) : static_cast<uint16_t*>(p.ab_r);
@@ -1302,6 +1386,9 @@ GemmArgs make_args(const ExpertArgs& a, const ExpWs& w, const int32_t* work, int
     g.dab_r = g.dab_s = g.dx_r = g.dx_s = nullptr;
     g.wrow = nullptr;
     g.wh_r = nullptr;
+    g.inv = a.perm_inv;
+    g.topk_w = a.topk_w;
+    g.out = a.out;
     return g;
 }
 
@@ -1373,6 +1460,17 @@ hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, int part, hipStre
         hipLaunchKernelGGL((gemm_bf16_dma_kernel<1, DCfg>), grid, dim3(DCfg::THREADS), 0, stream, g);
     else
         hipLaunchKernelGGL(gemm_f32_kernel<1>, grid, dim3(kThreads), 0, stream, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_experts_gemm2_combine(const ExpertArgs& a, void* ws, hipStream_t stream) {
+    if (!(a.act_dtype == 1 && a.packed && a.shared_inter > 0)) return hipErrorInvalidValue;
+    ExpWs w = carve(ws, a.T, a.d, a.k, a.inter, a.shared_inter, a.act_dtype, a.E);
+    const Plan p = plan_of(a);
+    const GemmArgs g = make_args(a, w, w.work2, 2);
+    const dim3 grid(static_cast<unsigned>(work_bound(a.T, a.k, a.E, p.bm2, p.nt2, p.nt2, p.has_shared, 2)));
+    if (grid.x == 0) return hipSuccess;
+    hipLaunchKernelGGL(gemm_bf16_pk_kernel<7>, grid, dim3(PK_THREADS), 0, stream, g);
     return hipGetLastError();
 }
 

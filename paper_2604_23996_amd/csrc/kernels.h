@@ -75,6 +75,10 @@ WorkTables experts_work_tables(const ExpertArgs& a, void* ws);
 // the shared items' entries in the tables do not depend on the routing)
 hipError_t launch_experts_gemm1(const ExpertArgs& a, void* ws, int part, hipStream_t stream);
 hipError_t launch_experts_gemm2(const ExpertArgs& a, void* ws, int part, hipStream_t stream);
+// The shared experts' GEMM2 with the combine in its epilogue (bf16, packed
+// weights, shared experts present): writes `out`, not Y_s; every routed row
+// of Y_r must be written before it runs.
+hipError_t launch_experts_gemm2_combine(const ExpertArgs& a, void* ws, hipStream_t stream);
 hipError_t launch_experts_combine(const ExpertArgs& a, void* ws, hipStream_t stream);
 // packed bf16 expert weights: elements of `batch` packed n x k matrices
 // (interleave: gate and up halves of a 2n-row source)

@@ -489,11 +489,17 @@ def test_layer_tiny_fp32_full():
 @pytest.mark.parametrize("name", ["deepseekmoe-vlm", "finegrained-vlm", "deepseekmoe-vlm-train", "large-skewed-vlm"])
 def test_layer_full_size(name):
     """The full-size bf16 workloads in the launch configuration the benchmark
-    times; routing, scores and MI on every token, the output on a seeded
-    sample."""
+    times (caller-owned side streams: merged GEMM launches and, with shared
+    experts, the combine in the shared down GEMM's epilogue); routing, scores
+    and MI on every token, the output on a seeded sample."""
     cfg = W.workload(name)
     inp = W.make_layer_inputs(cfg)
-    spec, _, outs, ws = run_gpu_layer(inp, keep_workspace=True)
+    st = S.Streams()
+    try:
+        spec, _, outs, ws = run_gpu_layer(inp, keep_workspace=True, streams=st)
+        torch.cuda.synchronize()
+    finally:
+        st.close()
     rows = np.sort(np.random.default_rng(cfg.seed).choice(cfg.T, size=192, replace=False))
     ref = run_oracle_layer(inp, rows=rows)
     _check_layer(inp, spec, outs, ref, rows=rows, routed_outs=_routed_run(inp))
