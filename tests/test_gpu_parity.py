@@ -556,13 +556,25 @@ def test_stage_events():
     ev.close()
 
 
-def test_side_streams_match_single_stream():
+SIDE_STREAM_LAYERS = [
+    dict(seed=9, d=256, E=16, k=4, inter=96, n_shared=1, n_bins=4, samples=((300, 100), (50, 60))),
+    # ragged for the combine in the shared down GEMM's epilogue: k % 4 != 0,
+    # d % 256 != 0 (a partial column tile), T % 128 != 0, statistics fixed
+    dict(seed=19, d=136, E=12, k=6, inter=48, n_shared=2, n_bins=3, samples=((150, 47), (61, 33)),
+         update_stats=False),
+]
+
+
+@pytest.mark.parametrize("layer", range(len(SIDE_STREAM_LAYERS)))
+def test_side_streams_match_single_stream(layer):
     """With caller-owned side streams the modality score, the MI chain and the
-    shared GEMMs run beside the routed path; several calls in a row, with
-    outputs read right after each, give the oracle's results and are
-    bit-identical to the single-stream order (the joins make them complete)."""
-    cfg = W.small_config(seed=9, d=256, E=16, k=4, inter=96, n_shared=1, n_bins=4,
-                         samples=((300, 100), (50, 60)), dtype=W.BF16, update_stats=True)
+    shared GEMMs run beside the routed path (and the combine runs in the shared
+    down GEMM's epilogue); several calls in a row, with outputs read right
+    after each, give the oracle's results and are bit-identical to the
+    single-stream order (the joins make them complete)."""
+    kw = dict(SIDE_STREAM_LAYERS[layer])
+    kw.setdefault("update_stats", True)
+    cfg = W.small_config(dtype=W.BF16, **kw)
     inp = W.make_layer_inputs(cfg)
     wg = W.aligned_router(inp, 0.5)  # well-conditioned MI
     ref = run_oracle_layer(inp, w_gate=wg)
