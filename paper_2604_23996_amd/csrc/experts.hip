@@ -85,7 +85,7 @@ struct Tile {
 // tiling), so it can run before the routing has been permuted.
 __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, const int32_t* __restrict__ off,
                                             int E, int64_t T, int bm, int nt_routed, int nt_shared,
-                                            int part, Tile& t) {
+                                            int part, Tile& t, int group_m = kGroupM) {
     const int xcd = blockIdx.x & 7;
     const int slot = blockIdx.x >> 3;
     int g, local;
@@ -132,10 +132,10 @@ __device__ __forceinline__ bool decode_tile(const int32_t* __restrict__ work, co
         ntn = nt_shared;
     }
     const int m_tiles = static_cast<int>(ceil_div(rows_g, bm));
-    const int sb = local / (kGroupM * ntn);
-    const int r = local % (kGroupM * ntn);
-    const int gm = m_tiles - sb * kGroupM < kGroupM ? m_tiles - sb * kGroupM : kGroupM;
-    const int mt = sb * kGroupM + r % gm;
+    const int sb = local / (group_m * ntn);
+    const int r = local % (group_m * ntn);
+    const int gm = m_tiles - sb * group_m < group_m ? m_tiles - sb * group_m : group_m;
+    const int mt = sb * group_m + r % gm;
     t.g = g;
     t.nt = r / gm;
     t.row0 = base + static_cast<int64_t>(mt) * bm;
@@ -474,6 +474,15 @@ constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instruction
 // combine (run after the routed GEMM2 has written every routed row). Modes 1, 3 and 6 pair gate and up groups (32 H columns
 // per wave); 2, 4 and 5 give each wave two consecutive 32-column groups.
 constexpr int pk_family(int mode) { return (mode == 1 || mode == 3 || mode == 6) ? 1 : 2; }
+// Row tiles per super-row of the work order (row tiles that take one weight
+// slice back to back), chosen by same-box A/B at 16384 x 4096 with 160 + 2
+// experts: 16 for the gate/up products (modes 1, 3, 6; 8 -> 16 took the
+// merged launch from 2.83 to 2.79 ms), 4 for the down products of the
+// forward (modes 2, 7; 1.29 -> 1.27 ms), 8 for the backward's dH and dX
+// (modes 4, 5; 4 there made the backward 0.9 % slower).
+constexpr int pk_group_m(int mode) {
+    return pk_family(mode) == 1 ? 16 : ((mode == 2 || mode == 7) ? 4 : 8);
+}
 constexpr int pk_tile_cols(int mode) { return pk_family(mode) == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
 constexpr int pk_out_cols(int mode) {
     return (mode == 3 || mode == 6) ? 2 * pk_tile_cols(mode) : pk_tile_cols(mode);
@@ -503,7 +512,7 @@ gemm_bf16_pk_kernel(GemmArgs p) {
     const int nt_r = static_cast<int>(ceil_div((FAM == 1 || MODE == 4) ? p.inter : p.d, TC));
     const int nt_s = (FAM == 1 || MODE == 4) ? static_cast<int>(ceil_div(p.shared_inter, TC)) : nt_r;
     Tile t;
-    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, p.part, t)) return;
+    if (!decode_tile(p.work, p.off, p.E, p.T, BM, nt_r, nt_s, p.part, t, pk_group_m(MODE))) return;
     const bool shared = t.g == p.E;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
 
