@@ -15,9 +15,10 @@
 //     two: expert half x token half, so each fragment read from LDS feeds four
 //     (weights) or 3 x NE (tokens) MFMAs. Each range's partial logits go to the
 //     workspace.
-//   router_topk_kernel: one wave per token sums the KS partials in range
-//     order, adds the bias, and runs the softmax and the top-k (one lane per
-//     expert, DPP reductions).
+//   router_topk_row_kernel: 16 lanes per token (four tokens per wave) sum
+//     the KS partials in range order, add the bias, and run the softmax and
+//     the top-k (lane j holds experts j + 16 q; DPP reductions inside the
+//     16-lane row).
 // fp32 activations: one kernel, dot products accumulated in fp64, then the
 // same per-token softmax and top-k.
 #include "common.h"
@@ -316,30 +317,79 @@ __device__ __forceinline__ void softmax_topk_token(const float (&z)[Q], int64_t 
     }
 }
 
-// One wave per token: z = the KS partial logits summed in range order, plus
-// the bias; then softmax and top-k.
+// bf16 path, 16 lanes per token (four tokens per wave): lane j of a row holds
+// experts j + 16 q. z = the KS partial logits summed in range order plus the
+// bias; the softmax and the top-k rounds reduce inside the row with DPP
+// moves only (no cross-row reads), ties to the lower expert index.
 template <int Q>
 __global__ void __launch_bounds__(kTopkWaves * 64)
-router_topk_kernel(const float* __restrict__ part, int ks_n, int64_t T, int E, int E_pad,
-                   const float* __restrict__ bias, int k, int renorm, float* __restrict__ logits,
-                   float* __restrict__ probs, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
-    const int64_t tok = static_cast<int64_t>(blockIdx.x) * kTopkWaves + threadIdx.x / kWave;
-    if (tok >= T) return;  // wave-uniform
-    const int lane = lane_id();
+router_topk_row_kernel(const float* __restrict__ part, int ks_n, int64_t T, int E, int E_pad,
+                       const float* __restrict__ bias, int k, int renorm, float* __restrict__ logits,
+                       float* __restrict__ probs, int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+    const int lane = lane_id(), l16 = lane & 15;
+    const int64_t tok = (static_cast<int64_t>(blockIdx.x) * kTopkWaves + threadIdx.x / kWave) * 4 + (lane >> 4);
+    const bool live = tok < T;  // uniform in the row; every lane takes part in the row reductions
     float z[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-        const int e = lane + q * kWave;
-        if (e < E) {
-            float v = part[tok * E_pad + e];
-#pragma unroll 4
+        const int e = l16 + 16 * q;
+        float v = -INFINITY;
+        if (live && e < E) {
+            v = part[tok * E_pad + e];
             for (int ks = 1; ks < ks_n; ++ks) v += part[(static_cast<int64_t>(ks) * T + tok) * E_pad + e];
-            z[q] = v + (bias != nullptr ? bias[e] : 0.0f);
-        } else {
-            z[q] = -INFINITY;
+            v += bias != nullptr ? bias[e] : 0.0f;
+        }
+        z[q] = v;
+    }
+    float lm = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) lm = fmaxf(lm, z[q]);
+    const float m = row_allreduce(lm, [](float a, float b) { return fmaxf(a, b); });
+    float ls = 0.0f, g[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        g[q] = l16 + 16 * q < E ? expf(z[q] - m) : 0.0f;
+        ls += g[q];
+    }
+    const float inv = 1.0f / row_allreduce(ls, [](float a, float b) { return a + b; });
+    if (live) {
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int e = l16 + 16 * q;
+            if (e < E) {
+                probs[tok * E + e] = g[q] * inv;
+                if (logits != nullptr) logits[tok * E + e] = z[q];
+            }
         }
     }
-    softmax_topk_token<Q>(z, tok, E, k, renorm, logits, probs, topk_idx, topk_w);
+    uint32_t taken = 0;
+    int my_i = 0;
+    float my_w = 0.0f;
+    for (int rr = 0; rr < k; ++rr) {
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int e = l16 + 16 * q;
+            if (e < E && !((taken >> q) & 1u) && (bi == 0x7fffffff || z[q] > bv)) {
+                bv = z[q];
+                bi = e;
+            }
+        }
+        const float gm = row_allreduce(bi == 0x7fffffff ? -INFINITY : bv, [](float a, float b) { return fmaxf(a, b); });
+        const int gi = row_allreduce(bi != 0x7fffffff && bv == gm ? bi : 0x7fffffff,
+                                     [](int a, int b) { return a < b ? a : b; });
+        if ((gi & 15) == l16) taken |= 1u << (gi >> 4);
+        if (l16 == rr) {
+            my_i = gi;
+            my_w = expf(gm - m) * inv;  // the chosen expert's gate value, as in probs
+        }
+    }
+    if (renorm) my_w = my_w / row_allreduce(l16 < k ? my_w : 0.0f, [](float a, float b) { return a + b; });
+    if (live && l16 < k) {
+        topk_idx[tok * k + l16] = my_i;
+        topk_w[tok * k + l16] = my_w;
+    }
 }
 
 // fp32 activations: 16 tokens per workgroup, dot products in fp64 into an
@@ -406,25 +456,19 @@ hipError_t launch_router_bf16(const uint16_t* x, int64_t T, int d, const uint16_
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    const dim3 tgrid(static_cast<unsigned>(ceil_div(T, kTopkWaves)));
+    // four tokens per wave (16 lanes each), kTopkWaves waves per block
+    const dim3 tgrid(static_cast<unsigned>(ceil_div(T, 4 * kTopkWaves)));
     const dim3 tblock(kTopkWaves * 64);
-    switch ((E + kWave - 1) / kWave) {
-        case 1:
-            hipLaunchKernelGGL(router_topk_kernel<1>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
-                               renorm, logits, probs, topk_idx, topk_w);
-            break;
-        case 2:
-            hipLaunchKernelGGL(router_topk_kernel<2>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
-                               renorm, logits, probs, topk_idx, topk_w);
-            break;
-        case 3:
-            hipLaunchKernelGGL(router_topk_kernel<3>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
-                               renorm, logits, probs, topk_idx, topk_w);
-            break;
-        case 4:
-            hipLaunchKernelGGL(router_topk_kernel<4>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k,
-                               renorm, logits, probs, topk_idx, topk_w);
-            break;
+    switch ((E + 15) / 16) {
+#define SMOES_TOPK_Q(Q)                                                                                     \
+    case Q:                                                                                                 \
+        hipLaunchKernelGGL(router_topk_row_kernel<Q>, tgrid, tblock, 0, stream, part, p.ks, T, E, E_pad, bias, k, \
+                           renorm, logits, probs, topk_idx, topk_w);                                        \
+        break;
+        SMOES_TOPK_Q(1) SMOES_TOPK_Q(2) SMOES_TOPK_Q(3) SMOES_TOPK_Q(4) SMOES_TOPK_Q(5) SMOES_TOPK_Q(6)
+        SMOES_TOPK_Q(7) SMOES_TOPK_Q(8) SMOES_TOPK_Q(9) SMOES_TOPK_Q(10) SMOES_TOPK_Q(11) SMOES_TOPK_Q(12)
+        SMOES_TOPK_Q(13) SMOES_TOPK_Q(14) SMOES_TOPK_Q(15) SMOES_TOPK_Q(16)
+#undef SMOES_TOPK_Q
         default:
             return hipErrorInvalidValue;
     }
