@@ -476,13 +476,11 @@ constexpr int PK_IA = PK_BM * PK_BK * 2 / 1024 / PK_WAVES;  // A DMA instruction
 constexpr int pk_family(int mode) { return (mode == 1 || mode == 3 || mode == 6) ? 1 : 2; }
 // Row tiles per super-row of the work order (row tiles that take one weight
 // slice back to back), chosen by same-box A/B at 16384 x 4096 with 160 + 2
-// experts: 16 for the gate/up products (modes 1, 3, 6; 8 -> 16 took the
-// merged launch from 2.83 to 2.79 ms), 4 for the down products of the
-// forward (modes 2, 7; 1.29 -> 1.27 ms), 8 for the backward's dH and dX
-// (modes 4, 5; 4 there made the backward 0.9 % slower).
-constexpr int pk_group_m(int mode) {
-    return pk_family(mode) == 1 ? 16 : ((mode == 2 || mode == 7) ? 4 : 8);
-}
+// experts: 4 for the down products of the forward (modes 2, 7; 8 -> 4 took
+// the routed launch from 1.29 to 1.27 ms), 16 for the rest (gate/up: the
+// merged launch 2.83 -> 2.79 ms; the backward's dX 1.56 -> 1.53 ms, dH
+// unchanged; 4 there made the backward 0.9 % slower).
+constexpr int pk_group_m(int mode) { return (mode == 2 || mode == 7) ? 4 : 16; }
 constexpr int pk_tile_cols(int mode) { return pk_family(mode) == 1 ? PK_WAVES * 32 : PK_WAVES * 64; }
 constexpr int pk_out_cols(int mode) {
     return (mode == 3 || mode == 6) ? 2 * pk_tile_cols(mode) : pk_tile_cols(mode);
