@@ -9,15 +9,20 @@
 //
 // Block -> tile mapping: blocks are dealt round-robin to the 8 XCDs, so block b
 // runs on XCD b % 8. Each XCD takes one contiguous eighth of the work list,
-// ordered (group, super-row of 8 m-tiles, n-tile, m-tile): the tiles that
-// share a weight slice run back to back on one XCD and hit its L2.
+// ordered (group, super-row of m-tiles, n-tile, m-tile): the tiles that share
+// a weight slice run back to back on one XCD and hit its L2 (8 m-tiles per
+// super-row for the row-major path; the packed path picks the count per
+// product).
 //
-// bf16: 128 x 128 tiles, 4 waves of 64 x 64 (2 x 2 MFMA 32x32x16 bf16
-// tiles), fp32 accumulation. Operand tiles are copied HBM -> LDS by buffer
-// loads with an LDS destination (no register staging) through a three-stage
-// ring of K = 32 slices; the MFMA fragments are read back with 16-byte LDS
-// reads from XOR-swizzled rows. The results leave through LDS as 16-byte
-// row chunks.
+// bf16, packed weights (the fast path, gemm_bf16_pk_kernel): 16x16x32 MFMA
+// tiles with the weights loaded straight into registers; its layout and
+// schedule are described where it is defined.
+// bf16, row-major weights: 128 x 128 tiles, 4 waves of 64 x 64 (2 x 2 MFMA
+// 32x32x16 bf16 tiles), fp32 accumulation. Operand tiles are copied HBM ->
+// LDS by buffer loads with an LDS destination (no register staging) through
+// a three-stage ring of K = 32 slices; the MFMA fragments are read back with
+// 16-byte LDS reads from XOR-swizzled rows. The results leave through LDS as
+// 16-byte row chunks.
 //   GEMM1: B rows 0..63 are gate rows, 64..127 the matching up rows, so a
 //          wave holds gate and up outputs of the same (row, column) in the
 //          same lane: the SwiGLU epilogue is register-local. H is bf16.
@@ -79,7 +84,7 @@ struct Tile {
 // Block b runs on XCD b % 8. The routed items and the shared-expert items are
 // each cut into 8 contiguous ranges, one per XCD, so every XCD gets the same
 // share of both kinds (shared tiles can have a longer K than routed ones).
-// Inside a group items run (super-row of 8 m-tiles, n-tile, m-tile).
+// Inside a group items run (super-row of group_m m-tiles, n-tile, m-tile).
 // part: 0 every item, 1 routed items only, 2 shared items only. The shared
 // part never reads the work table (its item count follows from T and the
 // tiling), so it can run before the routing has been permuted.
