@@ -562,6 +562,10 @@ SIDE_STREAM_LAYERS = [
     # d % 256 != 0 (a partial column tile), T % 128 != 0, statistics fixed
     dict(seed=19, d=136, E=12, k=6, inter=48, n_shared=2, n_bins=3, samples=((150, 47), (61, 33)),
          update_stats=False),
+    # the maxima through the fused combine: 256 experts, top-16 (four slot groups per token), 64 bins
+    dict(seed=23, d=256, E=256, k=16, inter=64, n_shared=1, n_bins=64, samples=((300, 100),)),
+    # top-1: one routed slot per token beside the shared expert
+    dict(seed=29, d=128, E=8, k=1, inter=32, n_shared=1, n_bins=2, samples=((100, 28), (40, 9))),
 ]
 
 
